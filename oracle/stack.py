@@ -1,0 +1,113 @@
+"""Oracle composition of the worker share: the conv stack and the hybrid step.
+
+TEST INFRASTRUCTURE (see the package docstring): composes the pinned fp64
+layer functions of this package in the order the paper's worker runs them
+(sec. 3.1 and sec. 4: the convolutional layers run data-parallel on the
+local batch; the FC layers, split to 1/K of their outputs, run on the batch
+gathered by the modulo layer; backward runs the same path in reverse).
+
+The stack's layer list is an input: ``weights[l]`` (KCRS), ``biases[l]`` and
+``pool_after[l]`` (a ReLU + 2x2 max pool follows conv l; otherwise a ReLU
+follows it).  The stack must end with a pool.
+
+With ``bf16=True`` every tensor the bf16 GPU path stores in bfloat16 is
+rounded to bfloat16 at the same point: conv outputs (before the pool, or
+after the fused ReLU), the pooled outputs (already bf16 values), and the
+activation gradients produced by the data-gradient convolution.  Weight and
+bias gradients stay in full precision.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from . import (_f64, conv3x3_bwd_data, conv3x3_bwd_weight, conv3x3_fwd,
+               fc_bwd, fc_fwd, relu_maxpool_bwd, relu_maxpool_fwd, round_bf16)
+
+
+def _identity(a):
+    return a
+
+
+def vgg_forward(x, weights, biases, pool_after, bf16=False):
+    """Forward of the conv stack.  Returns a dict with
+    ``A``: list of layer inputs A[0] = x ... A[L] = stack output,
+    ``Z``: {l: pre-pool conv output} for pooled layers,
+    ``idx``: {l: pool window codes} for pooled layers."""
+    rnd = round_bf16 if bf16 else _identity
+    if not pool_after[-1]:
+        raise ValueError("the stack must end with a pooled layer")
+    A = [_f64(x)]
+    Z, idx = {}, {}
+    for l, w in enumerate(weights):
+        if pool_after[l]:
+            z = rnd(conv3x3_fwd(A[l], w, biases[l], relu=False))
+            y, code = relu_maxpool_fwd(z)
+            Z[l], idx[l] = z, code
+            A.append(y)
+        else:
+            A.append(rnd(conv3x3_fwd(A[l], w, biases[l], relu=True)))
+    return {"A": A, "Z": Z, "idx": idx}
+
+
+def vgg_backward(fwd, weights, pool_after, dy_top, bf16=False, want_dx=True):
+    """Backward of the conv stack from the gradient of its output.
+    Returns ``dZ`` (gradient at each conv output, after the ReLU/pool),
+    ``dA`` (gradient arriving at each pooled output), ``dW``, ``db`` and
+    ``dX`` (gradient of the stack input; None unless want_dx)."""
+    rnd = round_bf16 if bf16 else _identity
+    A, idx = fwd["A"], fwd["idx"]
+    L = len(weights)
+    dZ, dA, dW, db = {}, {}, {}, {}
+    g = dy_top                      # gradient at the output of layer L-1
+    dX = None
+    for l in reversed(range(L)):
+        if pool_after[l]:
+            dA[l] = g
+            g = relu_maxpool_bwd(g, idx[l])
+        dZ[l] = g
+        dW[l], db[l] = conv3x3_bwd_weight(A[l], g)
+        if l > 0:
+            mask = None if pool_after[l - 1] else A[l]
+            g = rnd(conv3x3_bwd_data(g, weights[l], mask_src=mask))
+        elif want_dx:
+            dX = rnd(conv3x3_bwd_data(g, weights[0]))
+    return {"dZ": dZ, "dA": dA, "dW": dW, "db": db, "dX": dX}
+
+
+def vgg_step(x, weights, biases, pool_after, dy_top, bf16=False, want_dx=True):
+    f = vgg_forward(x, weights, biases, pool_after, bf16=bf16)
+    b = vgg_backward(f, weights, pool_after, dy_top, bf16=bf16, want_dx=want_dx)
+    return f, b
+
+
+def hybrid_step(x, weights, biases, pool_after, fc0_w, fc0_b, fc1_w, fc1_b,
+                x0_remote, x1_remote, dy1):
+    """One worker's step of the hybrid scheme on one device.
+
+    The local conv stack output (flattened, one row per image) fills the
+    first rows of the gathered FC0 input; ``x0_remote`` supplies the rows of
+    the other replicas.  FC0's shard output (ReLU) fills the first feature
+    columns of FC1's input; ``x1_remote`` supplies the other shards' columns.
+    Backward: FC1's partial input gradient restricted to this shard's own
+    columns, masked by FC0's ReLU, is FC0's output gradient; FC0's partial
+    input gradient restricted to this replica's rows is the gradient of the
+    conv stack output.  (The cross-worker sums of the partial gradients are
+    collectives and are not part of one worker's compute.)
+    """
+    f = vgg_forward(x, weights, biases, pool_after)
+    top = f["A"][-1]
+    n = top.shape[0]
+    feat = int(np.prod(top.shape[1:]))
+    x0 = np.concatenate([top.reshape(n, feat), np.asarray(x0_remote, np.float64)], axis=0)
+    y0 = fc_fwd(x0, fc0_w, fc0_b, relu=True)
+    ns0 = y0.shape[1]
+    x1 = np.concatenate([y0, np.asarray(x1_remote, np.float64)], axis=1)
+    y1 = fc_fwd(x1, fc1_w, fc1_b, relu=False)
+    dx1p, dw1, db1 = fc_bwd(x1, fc1_w, dy1)
+    dy0 = np.ascontiguousarray(dx1p[:, :ns0])
+    dx0p, dw0, db0 = fc_bwd(x0, fc0_w, dy0, mask_src=y0)
+    dtop = np.ascontiguousarray(dx0p[:n]).reshape(top.shape)
+    b = vgg_backward(f, weights, pool_after, dtop)
+    return {"fwd": f, "bwd": b, "x0": x0, "y0": y0, "x1": x1, "y1": y1,
+            "dx1p": dx1p, "dw1": dw1, "db1": db1, "dy0": dy0,
+            "dx0p": dx0p, "dw0": dw0, "db0": db0}
