@@ -1,0 +1,188 @@
+/*
+ * sb.h -- C ABI of libsb, the MI355X (gfx950) compute library for one
+ * SplitBrain worker's share of a training step (arXiv 2112.15317).
+ *
+ * The paper splits a CNN into two halves (sec. 3.1, Model Parallelism): the
+ * convolutional layers, compute-heavy with few parameters, run data-parallel
+ * on each worker's local batch; the fully connected layers, which hold most
+ * parameters, are split to 1/K of their outputs and run on the batch that
+ * the modulo layer gathers from the K workers.  One worker's compute is
+ * therefore: 3x3 convolution forward / data gradient / weight gradient, the
+ * ReLU and 2x2 max pooling between them (sec. 2.2), and the forward and
+ * backward of its FC column shard.  Those are the calls below.  The
+ * collectives around them (modulo / shard layer exchanges, model averaging)
+ * are not part of this library.
+ *
+ * Conventions for every call
+ * --------------------------
+ *  * Tensor pointers are DEVICE pointers, owned by the caller, that stay
+ *    valid until the enqueued work has finished.  The library never
+ *    allocates, frees or synchronises inside these calls; scratch memory is
+ *    the caller's workspace (query its size first).
+ *  * `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *    All work is enqueued on it, asynchronously.
+ *  * Arguments are validated before anything is enqueued; on any error
+ *    nothing is launched and the status says why.  A launch failure
+ *    returns SB_ERR_HIP.  Faults during execution surface, as in HIP, at
+ *    the caller's next synchronisation.
+ *  * Outputs must not overlap inputs (checked by address range).
+ *  * Layouts: activations NCHW row-major; conv weights KCRS
+ *    ([out][in][3][3]); FC input X [M][Kin] and shard weights
+ *    W_shard [Kin][Ns] row-major.  Element strides are in elements.
+ *  * dtype SB_F32: every tensor fp32.  SB_BF16: activations, activation
+ *    gradients and conv weights are bfloat16 (round-to-nearest-even on
+ *    store); accumulation is fp32; bias, weight gradient and bias gradient
+ *    are fp32.
+ *  * Calls are thread-safe; the library keeps no state between calls.
+ */
+#ifndef SB_H
+#define SB_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    SB_OK = 0,
+    SB_ERR_INVALID_ARG = 1,   /* null pointer, bad size, overlap, bad flag */
+    SB_ERR_UNSUPPORTED = 2,   /* valid request this build does not provide */
+    SB_ERR_WORKSPACE = 3,     /* workspace missing or smaller than needed  */
+    SB_ERR_HIP = 4            /* a HIP runtime call or launch failed       */
+} sb_status;
+
+typedef enum { SB_F32 = 0, SB_BF16 = 1 } sb_dtype;
+
+/* flags */
+#define SB_FUSE_RELU 1u       /* apply ReLU to the output (conv fwd, FC fwd) */
+
+/* Returns a static string naming the status. */
+const char *sb_status_string(sb_status s);
+
+/* Library version as major*10000 + minor*100 + patch. */
+int sb_version(void);
+
+/* ------------------------------------------------------------------------
+ * 3x3 convolution, stride 1, zero padding 1 (sec. 2.2: each convolutional
+ * stage multiplies successive input patches with square filters; the
+ * operation is the cross-correlation used by deep-learning frameworks).
+ *
+ *   x  [n][c][h][w]    input activations
+ *   w  [k][c][3][3]    filters
+ *   y  [n][k][h][w]    output
+ * ---------------------------------------------------------------------- */
+typedef struct {
+    int n, c, h, w;       /* batch, input channels, height, width (all > 0) */
+    int k;                /* output channels (> 0)                          */
+    int dtype;            /* sb_dtype                                       */
+    unsigned flags;       /* SB_FUSE_RELU (forward only)                    */
+} sb_conv3x3_desc;
+
+enum { SB_PASS_FWD = 0, SB_PASS_BWD_DATA = 1, SB_PASS_BWD_WEIGHT = 2 };
+
+/* Workspace bytes that `pass` needs for `desc` (0 is a valid answer, and a
+ * NULL workspace is then accepted).  Returns (size_t)-1 for an invalid or
+ * unsupported descriptor. */
+size_t sb_conv3x3_workspace_bytes(const sb_conv3x3_desc *desc, int pass);
+
+/* Forward:  y[n,k,h,w] = bias[k] + sum_{c,r,s} x[n,c,h+r-1,w+s-1] * w[k,c,r,s]
+ * (x = 0 outside the image), then max(y, 0) when SB_FUSE_RELU is set.
+ * bias may be NULL (zero). */
+sb_status sb_conv3x3_fwd(const sb_conv3x3_desc *desc, const void *x,
+                         const void *w, const float *bias, void *y,
+                         void *workspace, size_t workspace_bytes, void *stream);
+
+/* Data gradient (sec. 2.2 backward propagation):
+ *   dx[n,c,i,j] = sum_{k,r,s} dy[n,k,i-r+1,j-s+1] * w[k,c,r,s]
+ * over in-image output positions.  When relu_mask_src is non-NULL (shape of
+ * dx: the activation of the layer below, whose ReLU this gradient crosses),
+ * dx is set to 0 wherever relu_mask_src <= 0.  desc->flags must be 0. */
+sb_status sb_conv3x3_bwd_data(const sb_conv3x3_desc *desc, const void *dy,
+                              const void *w, const void *relu_mask_src,
+                              void *dx, void *workspace,
+                              size_t workspace_bytes, void *stream);
+
+/* Weight gradient (sec. 2.2 backward propagation; sec. 3.1 Modulo Layer:
+ * the conv parameters are updated from the gradient of the whole local
+ * batch):
+ *   dw[k,c,r,s] = sum_{n,h,w} x[n,c,h+r-1,w+s-1] * dy[n,k,h,w]   (fp32)
+ *   db[k]       = sum_{n,h,w} dy[n,k,h,w]                        (fp32)
+ * dw and db are overwritten; db may be NULL.  The summation order is fixed
+ * (no atomics): repeated calls give bit-identical results. */
+sb_status sb_conv3x3_bwd_weight(const sb_conv3x3_desc *desc, const void *x,
+                                const void *dy, float *dw, float *db,
+                                void *workspace, size_t workspace_bytes,
+                                void *stream);
+
+/* ------------------------------------------------------------------------
+ * Fused ReLU + 2x2 max pooling, stride 2 (sec. 2.2: pooling layers
+ * subsample; sec. 3.1 Layer Partitioning: pooling is never partitioned).
+ *
+ *   x   [n][c][h][w]       h and w even and > 0
+ *   y   [n][c][h/2][w/2]   y = max(0, max of the window)
+ *   idx [n][c][h/2][w/2]   uint8 code per window: bits 0-1 = row-major
+ *                          position of the first maximum (0:(0,0) 1:(0,1)
+ *                          2:(1,0) 3:(1,1)); bit 7 set when that maximum
+ *                          is <= 0 (the ReLU blocks the gradient); bits
+ *                          2-6 zero.
+ * Backward: dx (un-pooled shape) is zero except dx[window position] = dy
+ * for windows whose bit 7 is clear.  dx is fully overwritten.
+ * ---------------------------------------------------------------------- */
+sb_status sb_relu_maxpool_fwd(int n, int c, int h, int w, int dtype,
+                              const void *x, void *y, uint8_t *idx,
+                              void *stream);
+sb_status sb_relu_maxpool_bwd(int n, int c, int h, int w, int dtype,
+                              const void *dy, const uint8_t *idx, void *dx,
+                              void *stream);
+
+/* ------------------------------------------------------------------------
+ * FC column shard (sec. 3.1 Layer Partitioning: a LINEAR layer is split to
+ * 1/K of its outputs; Modulo Layer: it runs on the batch gathered from the
+ * K workers; Shard Layer: its backward yields gradients over the full
+ * input, which are reduced across workers later).
+ *
+ *   x        [m][k_in]      gathered activations, row stride ldx
+ *   w_shard  [k_in][n_shard] this worker's columns of W, dense
+ *   y, dy    [m][n_shard]   row stride ldy
+ * ---------------------------------------------------------------------- */
+typedef struct {
+    int m, k_in, n_shard;  /* gathered rows, input features, shard columns */
+    int dtype;             /* sb_dtype (SB_F32 in this build)              */
+    int ldx;               /* row stride of x and dx_partial (>= k_in)     */
+    int ldy;               /* row stride of y, dy, relu_mask_src (>= n_shard) */
+    unsigned flags;        /* SB_FUSE_RELU (forward only)                  */
+} sb_fc_desc;
+
+enum { SB_FC_FWD = 0, SB_FC_BWD = 1 };
+
+/* Workspace bytes for `pass`; (size_t)-1 for an invalid descriptor. */
+size_t sb_fc_workspace_bytes(const sb_fc_desc *desc, int pass);
+
+/* y = x * w_shard + b_shard, then max(y, 0) with SB_FUSE_RELU.  b_shard
+ * [n_shard] may be NULL. */
+sb_status sb_fc_shard_fwd(const sb_fc_desc *desc, const void *x,
+                          const void *w_shard, const float *b_shard, void *y,
+                          void *workspace, size_t workspace_bytes, void *stream);
+
+/* With g = dy, or g = dy * [relu_mask_src > 0] when relu_mask_src (shape
+ * and stride of dy: this shard's ReLU output) is non-NULL:
+ *   dx_partial[i,k] = sum_j g[i,j] * w_shard[k,j]   (may be NULL: skipped)
+ *   dw_shard[k,j]   = (accumulate ? dw_shard[k,j] : 0) + sum_i x[i,k] g[i,j]
+ *   db_shard[j]     = (accumulate ? db_shard[j]   : 0) + sum_i g[i,j]
+ * dw_shard and db_shard are fp32; db_shard may be NULL.  accumulate = 1
+ * adds the gradient of the K successive modulo iterations in place.  The
+ * division by K that the paper applies to FC gradients is the optimiser's
+ * and is not done here. */
+sb_status sb_fc_shard_bwd(const sb_fc_desc *desc, const void *x,
+                          const void *w_shard, const void *dy,
+                          const void *relu_mask_src, void *dx_partial,
+                          float *dw_shard, float *db_shard, int accumulate,
+                          void *workspace, size_t workspace_bytes, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SB_H */

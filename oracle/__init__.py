@@ -69,6 +69,8 @@ def _load():
                 "or_fc_bwd_dw_at": [_i, _i, _i, _D, _D, _D, _i64, _I64, _D],
                 "or_round_bf16": [_D, _i64],
             }
+            lib.or_num_threads.argtypes = []
+            lib.or_num_threads.restype = _i
             for name, args in sig.items():
                 fn = getattr(lib, name)
                 fn.argtypes = args
@@ -249,6 +251,11 @@ def fc_bwd_dw_at(x, dy, flat, mask_src=None):
     out = np.empty(idx.size)
     _load().or_fc_bwd_dw_at(mm, kin, ns, _p(x), _p(dy), _p(m), idx.size, pidx, _p(out))
     return out
+
+
+def num_threads() -> int:
+    """OpenMP threads the oracle's loops use."""
+    return int(_load().or_num_threads())
 
 
 # ------------------------------------------------------------- rounding --

@@ -33,6 +33,7 @@
  * taken after the max, which gives the same value as before it.
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stddef.h>
 
@@ -405,3 +406,6 @@ EXPORT void or_round_bf16(double *a, int64_t count)
         a[i] = r;
     }
 }
+
+/* Number of OpenMP threads the loops above run on. */
+EXPORT int or_num_threads(void) { return omp_get_max_threads(); }

@@ -1,0 +1,129 @@
+// pool.hip -- fused ReLU + 2x2/2 max pooling with window codes, and its
+// backward (sec. 2.2: pooling subsamples the features between convolutional
+// stages).  Both directions are pure data movement, bound by HBM bandwidth:
+// each thread owns PER_THREAD horizontally adjacent windows, so it reads
+// 2*PER_THREAD contiguous elements from each of two input rows and writes
+// PER_THREAD outputs and codes; neighbouring threads touch neighbouring
+// addresses.  No window is shared between threads, so no atomics are needed.
+#include "sb_internal.hpp"
+
+namespace sb {
+
+// Window code: bits 0-1 = row-major position of the first maximum, bit 7 =
+// maximum <= 0 (ReLU blocks the gradient).
+template <typename T, int PER_THREAD>
+__global__ __launch_bounds__(256) void relu_maxpool_fwd_kernel(
+    const T* __restrict__ x, T* __restrict__ y, uint8_t* __restrict__ idx,
+    uint32_t Wo, uint32_t groups_per_row, uint32_t total_groups) {
+  uint32_t g = blockIdx.x * 256u + threadIdx.x;
+  if (g >= total_groups) return;
+  uint32_t row = g / groups_per_row;               // (n*C + c)*Ho + oh
+  uint32_t ow0 = (g - row * groups_per_row) * PER_THREAD;
+  const size_t W = 2 * (size_t)Wo;
+  const T* p0 = x + (size_t)row * 2 * W + 2 * ow0;  // input rows 2*oh, 2*oh+1
+  const T* p1 = p0 + W;
+  size_t o = (size_t)row * Wo + ow0;
+#pragma unroll
+  for (int j = 0; j < PER_THREAD; ++j) {
+    if (ow0 + j >= Wo) break;
+    float v0 = Elem<T>::load(p0, 2 * j), v1 = Elem<T>::load(p0, 2 * j + 1);
+    float v2 = Elem<T>::load(p1, 2 * j), v3 = Elem<T>::load(p1, 2 * j + 1);
+    float m = v0;
+    uint32_t a = 0;
+    if (v1 > m) { m = v1; a = 1; }
+    if (v2 > m) { m = v2; a = 2; }
+    if (v3 > m) { m = v3; a = 3; }
+    bool pos = m > 0.0f;
+    Elem<T>::store(y, o + j, pos ? m : 0.0f);
+    idx[o + j] = (uint8_t)(a | (pos ? 0u : 0x80u));
+  }
+}
+
+template <typename T, int PER_THREAD>
+__global__ __launch_bounds__(256) void relu_maxpool_bwd_kernel(
+    const T* __restrict__ dy, const uint8_t* __restrict__ idx, T* __restrict__ dx,
+    uint32_t Wo, uint32_t groups_per_row, uint32_t total_groups) {
+  uint32_t g = blockIdx.x * 256u + threadIdx.x;
+  if (g >= total_groups) return;
+  uint32_t row = g / groups_per_row;
+  uint32_t ow0 = (g - row * groups_per_row) * PER_THREAD;
+  const size_t W = 2 * (size_t)Wo;
+  T* p0 = dx + (size_t)row * 2 * W + 2 * ow0;
+  T* p1 = p0 + W;
+  size_t o = (size_t)row * Wo + ow0;
+#pragma unroll
+  for (int j = 0; j < PER_THREAD; ++j) {
+    if (ow0 + j >= Wo) break;
+    float gv = Elem<T>::load(dy, o + j);
+    uint32_t code = idx[o + j];
+    bool live = !(code & 0x80u);
+    uint32_t a = code & 3u;
+    Elem<T>::store(p0, 2 * j, (live && a == 0) ? gv : 0.0f);
+    Elem<T>::store(p0, 2 * j + 1, (live && a == 1) ? gv : 0.0f);
+    Elem<T>::store(p1, 2 * j, (live && a == 2) ? gv : 0.0f);
+    Elem<T>::store(p1, 2 * j + 1, (live && a == 3) ? gv : 0.0f);
+  }
+}
+
+template <typename T>
+static sb_status pool_launch(bool fwd, int n, int c, int h, int w, const void* in,
+                             const uint8_t* idx_in, void* out, uint8_t* idx_out,
+                             hipStream_t st) {
+  constexpr int PT = 2;
+  uint32_t Wo = (uint32_t)(w / 2);
+  uint32_t rows = (uint32_t)n * c * (h / 2);
+  uint32_t gpr = (Wo + PT - 1) / PT;
+  uint32_t total = rows * gpr;
+  dim3 grid((total + 255) / 256), block(256);
+  if (fwd)
+    relu_maxpool_fwd_kernel<T, PT><<<grid, block, 0, st>>>(
+        (const T*)in, (T*)out, idx_out, Wo, gpr, total);
+  else
+    relu_maxpool_bwd_kernel<T, PT><<<grid, block, 0, st>>>(
+        (const T*)in, idx_in, (T*)out, Wo, gpr, total);
+  return sbh::launch_status();
+}
+
+}  // namespace sb
+
+using namespace sb;
+
+static sb_status pool_check(int n, int c, int h, int w, int dtype) {
+  if (n <= 0 || c <= 0 || h <= 0 || w <= 0) return SB_ERR_INVALID_ARG;
+  if ((h & 1) || (w & 1)) return SB_ERR_INVALID_ARG;
+  if (dtype != SB_F32 && dtype != SB_BF16) return SB_ERR_INVALID_ARG;
+  // 32-bit window indexing inside the kernels.
+  if ((uint64_t)n * c * h * w >= (1ull << 32)) return SB_ERR_UNSUPPORTED;
+  return SB_OK;
+}
+
+extern "C" sb_status sb_relu_maxpool_fwd(int n, int c, int h, int w, int dtype,
+                                         const void* x, void* y, uint8_t* idx,
+                                         void* stream) {
+  sb_status s = pool_check(n, c, h, w, dtype);
+  if (s != SB_OK) return s;
+  if (!x || !y || !idx) return SB_ERR_INVALID_ARG;
+  size_t es = sbh::dsize(dtype);
+  size_t in_b = (size_t)n * c * h * w * es, out_n = (size_t)n * c * (h / 2) * (w / 2);
+  if (sbh::overlaps(x, in_b, y, out_n * es) || sbh::overlaps(x, in_b, idx, out_n) ||
+      sbh::overlaps(y, out_n * es, idx, out_n))
+    return SB_ERR_INVALID_ARG;
+  hipStream_t st = sbh::stream_of(stream);
+  return dtype == SB_F32 ? pool_launch<float>(true, n, c, h, w, x, nullptr, y, idx, st)
+                         : pool_launch<u16>(true, n, c, h, w, x, nullptr, y, idx, st);
+}
+
+extern "C" sb_status sb_relu_maxpool_bwd(int n, int c, int h, int w, int dtype,
+                                         const void* dy, const uint8_t* idx, void* dx,
+                                         void* stream) {
+  sb_status s = pool_check(n, c, h, w, dtype);
+  if (s != SB_OK) return s;
+  if (!dy || !idx || !dx) return SB_ERR_INVALID_ARG;
+  size_t es = sbh::dsize(dtype);
+  size_t out_b = (size_t)n * c * h * w * es, in_n = (size_t)n * c * (h / 2) * (w / 2);
+  if (sbh::overlaps(dx, out_b, dy, in_n * es) || sbh::overlaps(dx, out_b, idx, in_n))
+    return SB_ERR_INVALID_ARG;
+  hipStream_t st = sbh::stream_of(stream);
+  return dtype == SB_F32 ? pool_launch<float>(false, n, c, h, w, dy, idx, dx, nullptr, st)
+                         : pool_launch<u16>(false, n, c, h, w, dy, idx, dx, nullptr, st);
+}

@@ -1,0 +1,73 @@
+// sb_internal.hpp -- shared device helpers and host plumbing of libsb.
+// gfx950 (CDNA4) only: wave64, MFMA, 160 KB LDS per CU.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/sb.h"
+
+namespace sb {
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+typedef float f2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef uint16_t u16;
+
+constexpr int kWave = 64;
+
+// D(16x16) += A(16x4) * B(4x16), fp32 in / fp32 accumulate.
+// Lane l supplies A[l%16][l/16] and B[l/16][l%16]; it receives
+// D[4*(l/16)+i][l%16] in element i.
+__device__ __forceinline__ f4 mfma16x16x4(float a, float b, f4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+// bf16 <-> fp32.  bf16 is the upper half of an fp32 bit pattern; the
+// conversion to bf16 rounds to nearest, ties to even (NaN kept quiet).
+__device__ __forceinline__ float bf16_to_f32(u16 v) {
+  return __uint_as_float(((uint32_t)v) << 16);
+}
+__device__ __forceinline__ u16 f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu))
+    return (u16)((u >> 16) | 0x40);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (u16)(u >> 16);
+}
+
+template <typename T> struct Elem;
+template <> struct Elem<float> {
+  __device__ static __forceinline__ float load(const float* p, size_t i) { return p[i]; }
+  __device__ static __forceinline__ void store(float* p, size_t i, float v) { p[i] = v; }
+};
+template <> struct Elem<u16> {
+  __device__ static __forceinline__ float load(const u16* p, size_t i) { return bf16_to_f32(p[i]); }
+  __device__ static __forceinline__ void store(u16* p, size_t i, float v) { p[i] = f32_to_bf16(v); }
+};
+
+__host__ __device__ constexpr int cdiv(int a, int b) { return (a + b - 1) / b; }
+__host__ __device__ constexpr size_t round_up(size_t a, size_t b) { return (a + b - 1) / b * b; }
+
+}  // namespace sb
+
+// Host-side helpers shared by the entry points.
+namespace sbh {
+
+inline hipStream_t stream_of(void* s) { return reinterpret_cast<hipStream_t>(s); }
+
+inline bool overlaps(const void* a, size_t abytes, const void* b, size_t bbytes) {
+  if (!a || !b || !abytes || !bbytes) return false;
+  uintptr_t a0 = (uintptr_t)a, b0 = (uintptr_t)b;
+  return a0 < b0 + bbytes && b0 < a0 + abytes;
+}
+
+inline sb_status launch_status() {
+  hipError_t e = hipGetLastError();
+  return e == hipSuccess ? SB_OK : SB_ERR_HIP;
+}
+
+inline size_t dsize(int dtype) { return dtype == SB_BF16 ? 2 : 4; }
+
+}  // namespace sbh

@@ -1,0 +1,197 @@
+"""Thin Python binding of libsb (include/sb.h): argument marshalling only.
+
+Every function has the name of the C entry point it calls and takes torch
+tensors that live on the GPU (torch provides device memory and streams, and
+nothing else here): the tensor's dtype selects SB_F32 / SB_BF16, its data
+pointer is passed through, and the current torch stream is the HIP stream
+unless one is given.  Every step of the computation runs in libsb's HIP
+kernels.  A non-OK status raises ``SBError``.
+
+The library must have been built (``python -m paper_2112_15317_amd.build``);
+if ``libsb.so`` is missing, loading fails loudly: there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import threading
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libsb.so")
+
+SB_OK, SB_ERR_INVALID_ARG, SB_ERR_UNSUPPORTED, SB_ERR_WORKSPACE, SB_ERR_HIP = range(5)
+SB_F32, SB_BF16 = 0, 1
+SB_FUSE_RELU = 1
+SB_PASS_FWD, SB_PASS_BWD_DATA, SB_PASS_BWD_WEIGHT = 0, 1, 2
+SB_FC_FWD, SB_FC_BWD = 0, 1
+
+_vp = ctypes.c_void_p
+_i = ctypes.c_int
+_sz = ctypes.c_size_t
+
+
+class sb_conv3x3_desc(ctypes.Structure):
+    _fields_ = [("n", _i), ("c", _i), ("h", _i), ("w", _i), ("k", _i),
+                ("dtype", _i), ("flags", ctypes.c_uint)]
+
+
+class sb_fc_desc(ctypes.Structure):
+    _fields_ = [("m", _i), ("k_in", _i), ("n_shard", _i), ("dtype", _i),
+                ("ldx", _i), ("ldy", _i), ("flags", ctypes.c_uint)]
+
+
+# Every exported symbol of include/sb.h with its ctypes signature.
+SIGNATURES = {
+    "sb_status_string": (ctypes.c_char_p, [_i]),
+    "sb_version": (_i, []),
+    "sb_conv3x3_workspace_bytes": (_sz, [ctypes.POINTER(sb_conv3x3_desc), _i]),
+    "sb_conv3x3_fwd": (_i, [ctypes.POINTER(sb_conv3x3_desc), _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "sb_conv3x3_bwd_data": (_i, [ctypes.POINTER(sb_conv3x3_desc), _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "sb_conv3x3_bwd_weight": (_i, [ctypes.POINTER(sb_conv3x3_desc), _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "sb_relu_maxpool_fwd": (_i, [_i, _i, _i, _i, _i, _vp, _vp, _vp, _vp]),
+    "sb_relu_maxpool_bwd": (_i, [_i, _i, _i, _i, _i, _vp, _vp, _vp, _vp]),
+    "sb_fc_workspace_bytes": (_sz, [ctypes.POINTER(sb_fc_desc), _i]),
+    "sb_fc_shard_fwd": (_i, [ctypes.POINTER(sb_fc_desc), _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "sb_fc_shard_bwd": (_i, [ctypes.POINTER(sb_fc_desc), _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i,
+                             _vp, _sz, _vp]),
+}
+
+_lock = threading.Lock()
+_lib = None
+
+
+class SBError(RuntimeError):
+    def __init__(self, fn, status):
+        self.status = status
+        super().__init__("%s failed: %s" % (fn, status_name(status)))
+
+
+def load():
+    """Load libsb.so (raises if it has not been built)."""
+    global _lib
+    with _lock:
+        if _lib is None:
+            if not os.path.exists(LIB_PATH):
+                raise RuntimeError(
+                    "libsb.so not found at %s: build it with "
+                    "`python -m paper_2112_15317_amd.build` (no fallback exists)" % LIB_PATH)
+            lib = ctypes.CDLL(LIB_PATH)
+            for name, (res, args) in SIGNATURES.items():
+                fn = getattr(lib, name)
+                fn.restype = res
+                fn.argtypes = args
+            _lib = lib
+    return _lib
+
+
+def status_name(status: int) -> str:
+    return load().sb_status_string(int(status)).decode()
+
+
+def _check(fn, status):
+    if status != SB_OK:
+        raise SBError(fn, status)
+
+
+# ----------------------------------------------------------- marshalling --
+def _dtype_code(t):
+    import torch
+    if t.dtype == torch.float32:
+        return SB_F32
+    if t.dtype == torch.bfloat16:
+        return SB_BF16
+    raise TypeError("libsb takes float32 or bfloat16 tensors, got %s" % t.dtype)
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    if not t.is_cuda:
+        raise ValueError("libsb takes device tensors")
+    if not t.is_contiguous():
+        raise ValueError("libsb takes contiguous tensors (strides go in the descriptor)")
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _ws(ws):
+    if ws is None:
+        return None, 0
+    return ws.data_ptr(), ws.numel() * ws.element_size()
+
+
+def conv_desc(n, c, h, w, k, dtype=SB_F32, relu=False):
+    return sb_conv3x3_desc(n, c, h, w, k, dtype, SB_FUSE_RELU if relu else 0)
+
+
+def fc_desc(m, k_in, n_shard, dtype=SB_F32, ldx=None, ldy=None, relu=False):
+    return sb_fc_desc(m, k_in, n_shard, dtype, ldx or k_in, ldy or n_shard,
+                      SB_FUSE_RELU if relu else 0)
+
+
+# --------------------------------------------------------- entry points --
+def sb_version():
+    return load().sb_version()
+
+
+def sb_conv3x3_workspace_bytes(desc, pass_):
+    return load().sb_conv3x3_workspace_bytes(ctypes.byref(desc), pass_)
+
+
+def sb_conv3x3_fwd(desc, x, w, bias, y, ws=None, stream=None):
+    p, nb = _ws(ws)
+    _check("sb_conv3x3_fwd", load().sb_conv3x3_fwd(
+        ctypes.byref(desc), _ptr(x), _ptr(w), _ptr(bias), _ptr(y), p, nb, _stream(stream)))
+
+
+def sb_conv3x3_bwd_data(desc, dy, w, relu_mask_src, dx, ws=None, stream=None):
+    p, nb = _ws(ws)
+    _check("sb_conv3x3_bwd_data", load().sb_conv3x3_bwd_data(
+        ctypes.byref(desc), _ptr(dy), _ptr(w), _ptr(relu_mask_src), _ptr(dx), p, nb,
+        _stream(stream)))
+
+
+def sb_conv3x3_bwd_weight(desc, x, dy, dw, db, ws=None, stream=None):
+    p, nb = _ws(ws)
+    _check("sb_conv3x3_bwd_weight", load().sb_conv3x3_bwd_weight(
+        ctypes.byref(desc), _ptr(x), _ptr(dy), _ptr(dw), _ptr(db), p, nb, _stream(stream)))
+
+
+def sb_relu_maxpool_fwd(n, c, h, w, dtype, x, y, idx, stream=None):
+    _check("sb_relu_maxpool_fwd", load().sb_relu_maxpool_fwd(
+        n, c, h, w, dtype, _ptr(x), _ptr(y), _ptr(idx), _stream(stream)))
+
+
+def sb_relu_maxpool_bwd(n, c, h, w, dtype, dy, idx, dx, stream=None):
+    _check("sb_relu_maxpool_bwd", load().sb_relu_maxpool_bwd(
+        n, c, h, w, dtype, _ptr(dy), _ptr(idx), _ptr(dx), _stream(stream)))
+
+
+def sb_fc_workspace_bytes(desc, pass_):
+    return load().sb_fc_workspace_bytes(ctypes.byref(desc), pass_)
+
+
+def sb_fc_shard_fwd(desc, x, w_shard, b_shard, y, ws=None, stream=None):
+    p, nb = _ws(ws)
+    _check("sb_fc_shard_fwd", load().sb_fc_shard_fwd(
+        ctypes.byref(desc), _ptr(x), _ptr(w_shard), _ptr(b_shard), _ptr(y), p, nb,
+        _stream(stream)))
+
+
+def sb_fc_shard_bwd(desc, x, w_shard, dy, relu_mask_src, dx_partial, dw_shard, db_shard,
+                    accumulate=False, ws=None, stream=None):
+    p, nb = _ws(ws)
+    _check("sb_fc_shard_bwd", load().sb_fc_shard_bwd(
+        ctypes.byref(desc), _ptr(x), _ptr(w_shard), _ptr(dy), _ptr(relu_mask_src),
+        _ptr(dx_partial), _ptr(dw_shard), _ptr(db_shard), 1 if accumulate else 0, p, nb,
+        _stream(stream)))

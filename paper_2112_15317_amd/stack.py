@@ -1,0 +1,253 @@
+"""Host-side step drivers: buffer plan and call sequence of one worker step.
+
+A worker of the paper's hybrid scheme runs the convolutional layers on its
+local batch (data parallel) and its FC column shards on the batch gathered
+from all replicas (model parallel); backward retraces the same path (sec.
+3.1 and sec. 4).  These classes own the device buffers of that step and
+enqueue the libsb calls in order on one stream.  They do no arithmetic: every
+value is produced by a libsb kernel.  torch only allocates device memory.
+
+``ConvStack``   13-layer VGG conv stack fwd + bwd (ReLU, fused ReLU + pool)
+``FCShard``     one FC column shard fwd + bwd
+``HybridStep``  conv stack, then FC0 -> ReLU -> FC1 shards on the gathered
+                batch, then backward through both
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from . import sb
+from .configs import conv_layers
+
+
+def _dev_dtype(dtype: str):
+    return {"f32": torch.float32, "bf16": torch.bfloat16}[dtype]
+
+
+def _code(dtype: str):
+    return {"f32": sb.SB_F32, "bf16": sb.SB_BF16}[dtype]
+
+
+class EventTimer:
+    """Brackets calls with HIP events on the current stream; per-key lists of
+    (start, stop) pairs are read after a synchronisation."""
+
+    def __init__(self):
+        self.events = {}
+
+    def __call__(self, key, fn, *args):
+        s = torch.cuda.Event(enable_timing=True)
+        e = torch.cuda.Event(enable_timing=True)
+        s.record()
+        fn(*args)
+        e.record()
+        self.events.setdefault(key, []).append((s, e))
+
+    def mean_ms(self):
+        return {k: sum(s.elapsed_time(e) for s, e in v) / len(v) for k, v in self.events.items()}
+
+    def total_ms(self):
+        return {k: sum(s.elapsed_time(e) for s, e in v) for k, v in self.events.items()}
+
+
+def _plain(key, fn, *args):
+    fn(*args)
+
+
+class ConvStack:
+    """Buffers and calls of a 3x3 conv stack whose last layer is pooled.
+
+    Buffer names (per layer l, 0-based):
+      A[l]   input of layer l (A[0] = images, A[L] = stack output)
+      Z[l]   pre-pool conv output of a pooled layer
+      idx[l] pool window codes of a pooled layer
+      gA[l]  gradient arriving at A[l] (gA[L] = upstream gradient); when
+             layer l-1 has no pool, gA[l] already carries its ReLU mask,
+             i.e. it is the gradient of that layer's conv output
+      dZ[l]  gradient at the conv output of a pooled layer (pool backward)
+      dW[l], db[l]  fp32 parameter gradients
+    """
+
+    def __init__(self, schedule, n, in_ch, hw, dtype="f32", device="cuda",
+                 out_buffer=None, out_grad_buffer=None):
+        self.layers = conv_layers(schedule, in_ch, hw)
+        if not self.layers[-1].pool_after:
+            raise ValueError("the stack must end with a pooled layer")
+        self.n, self.dtype = n, dtype
+        self.code = _code(dtype)
+        tdt = _dev_dtype(dtype)
+        dev = torch.device(device)
+        self.device = dev
+        L = self.layers
+        self.A = [torch.empty((n, in_ch, hw, hw), dtype=tdt, device=dev)]
+        self.Z, self.idx, self.dZ = {}, {}, {}
+        for l in L:
+            if l.pool_after:
+                self.Z[l.index] = torch.empty((n, l.k, l.h, l.w), dtype=tdt, device=dev)
+                self.idx[l.index] = torch.empty((n, l.k, l.h // 2, l.w // 2), dtype=torch.uint8,
+                                                device=dev)
+                self.dZ[l.index] = torch.empty((n, l.k, l.h, l.w), dtype=tdt, device=dev)
+                shape = (n, l.k, l.h // 2, l.w // 2)
+            else:
+                shape = (n, l.k, l.h, l.w)
+            last = l.index == len(L) - 1
+            if last and out_buffer is not None:
+                self.A.append(out_buffer.view(shape))
+            else:
+                self.A.append(torch.empty(shape, dtype=tdt, device=dev))
+        self.gA = [torch.empty_like(a) for a in self.A[:-1]]
+        self.gA.append(out_grad_buffer.view(self.A[-1].shape) if out_grad_buffer is not None
+                       else torch.empty_like(self.A[-1]))
+        self.W = [torch.empty((l.k, l.c, 3, 3), dtype=tdt, device=dev) for l in L]
+        self.b = [torch.zeros((l.k,), dtype=torch.float32, device=dev) for l in L]
+        self.dW = [torch.empty((l.k, l.c, 3, 3), dtype=torch.float32, device=dev) for l in L]
+        self.db = [torch.empty((l.k,), dtype=torch.float32, device=dev) for l in L]
+        self.desc = [sb.conv_desc(n, l.c, l.h, l.w, l.k, self.code, relu=not l.pool_after)
+                     for l in L]
+        self.desc_b = [sb.conv_desc(n, l.c, l.h, l.w, l.k, self.code) for l in L]
+        need = 0
+        for l in L:
+            need = max(need,
+                       sb.sb_conv3x3_workspace_bytes(self.desc[l.index], sb.SB_PASS_FWD),
+                       sb.sb_conv3x3_workspace_bytes(self.desc_b[l.index], sb.SB_PASS_BWD_DATA),
+                       sb.sb_conv3x3_workspace_bytes(self.desc_b[l.index], sb.SB_PASS_BWD_WEIGHT))
+        self.ws = torch.empty((max(need, 256) + 255) // 256 * 256, dtype=torch.uint8, device=dev)
+        self.call = _plain      # replace with an EventTimer to time each call
+
+    # -- data placement (host -> device copies of seeded inputs) --------------
+    def load_inputs(self, x, weights, biases=None, dy_top=None):
+        def put(dst, src):
+            t = src if isinstance(src, torch.Tensor) else torch.from_numpy(np.ascontiguousarray(src))
+            dst.copy_(t.to(dst.dtype) if t.dtype != dst.dtype else t)
+        put(self.A[0], x)
+        for l, w in enumerate(weights):
+            put(self.W[l], w)
+        if biases is not None:
+            for l, b in enumerate(biases):
+                put(self.b[l], b)
+        if dy_top is not None:
+            put(self.gA[-1], dy_top)
+
+    # -- the step ---------------------------------------------------------------
+    def forward(self, stream=None):
+        c = self.call
+        for l in self.layers:
+            i = l.index
+            if l.pool_after:
+                c(("fwd", i), sb.sb_conv3x3_fwd, self.desc[i], self.A[i], self.W[i], self.b[i],
+                  self.Z[i], self.ws, stream)
+                c(("pool_fwd", i), sb.sb_relu_maxpool_fwd, self.n, l.k, l.h, l.w, self.code,
+                  self.Z[i], self.A[i + 1], self.idx[i], stream)
+            else:
+                c(("fwd", i), sb.sb_conv3x3_fwd, self.desc[i], self.A[i], self.W[i], self.b[i],
+                  self.A[i + 1], self.ws, stream)
+
+    def backward(self, stream=None, want_dx=True):
+        c = self.call
+        L = self.layers
+        for l in reversed(L):
+            i = l.index
+            if l.pool_after:
+                c(("pool_bwd", i), sb.sb_relu_maxpool_bwd, self.n, l.k, l.h, l.w, self.code,
+                  self.gA[i + 1], self.idx[i], self.dZ[i], stream)
+                g = self.dZ[i]
+            else:
+                g = self.gA[i + 1]
+            c(("wgrad", i), sb.sb_conv3x3_bwd_weight, self.desc_b[i], self.A[i], g, self.dW[i],
+              self.db[i], self.ws, stream)
+            if i > 0:
+                mask = None if L[i - 1].pool_after else self.A[i]
+                c(("dgrad", i), sb.sb_conv3x3_bwd_data, self.desc_b[i], g, self.W[i], mask,
+                  self.gA[i], self.ws, stream)
+            elif want_dx:
+                c(("dgrad", i), sb.sb_conv3x3_bwd_data, self.desc_b[i], g, self.W[i], None,
+                  self.gA[0], self.ws, stream)
+
+    def grad_at_conv_output(self, i):
+        """Gradient at conv output i (after its ReLU / pool backward)."""
+        return self.dZ[i] if self.layers[i].pool_after else self.gA[i + 1]
+
+    def step(self, stream=None):
+        self.forward(stream)
+        self.backward(stream)
+
+
+class FCShard:
+    """One FC column shard: X [m, k_in] (row stride ldx), W [k_in, ns]."""
+
+    def __init__(self, m, k_in, ns, relu=False, ldx=None, ldy=None, device="cuda"):
+        self.m, self.k_in, self.ns, self.relu = m, k_in, ns, relu
+        self.ldx, self.ldy = ldx or k_in, ldy or ns
+        dev = torch.device(device)
+        self.desc_f = sb.fc_desc(m, k_in, ns, sb.SB_F32, self.ldx, self.ldy, relu=relu)
+        self.desc_b = sb.fc_desc(m, k_in, ns, sb.SB_F32, self.ldx, self.ldy)
+        self.W = torch.empty((k_in, ns), dtype=torch.float32, device=dev)
+        self.b = torch.zeros((ns,), dtype=torch.float32, device=dev)
+        self.dW = torch.empty((k_in, ns), dtype=torch.float32, device=dev)
+        self.db = torch.empty((ns,), dtype=torch.float32, device=dev)
+        need = max(sb.sb_fc_workspace_bytes(self.desc_f, sb.SB_FC_FWD),
+                   sb.sb_fc_workspace_bytes(self.desc_b, sb.SB_FC_BWD))
+        self.ws = torch.empty((max(need, 256) + 255) // 256 * 256, dtype=torch.uint8, device=dev)
+
+    def forward(self, x_ptr, y_ptr, stream=None):
+        sb.sb_fc_shard_fwd(self.desc_f, x_ptr, self.W, self.b, y_ptr, self.ws, stream)
+
+    def backward(self, x_ptr, dy_ptr, mask_ptr, dx_ptr, accumulate=False, stream=None):
+        sb.sb_fc_shard_bwd(self.desc_b, x_ptr, self.W, dy_ptr, mask_ptr, dx_ptr, self.dW,
+                           self.db, accumulate, self.ws, stream)
+
+
+class HybridStep:
+    """Conv stack on the local batch, then the FC shards on the gathered batch.
+
+    X0 [R*n, F]: rows [0, n) are this replica's flattened conv output (the
+    stack writes them in place), rows [n, R*n) hold the other replicas'
+    rows.  X1 [R*n, S*ns0]: columns [0, ns0) are FC0's shard output (written
+    in place, ReLU), the rest hold the other shards' columns.  Backward: FC1's
+    partial input gradient restricted to this shard's columns is FC0's output
+    gradient (masked by FC0's ReLU inside the call); FC0's partial input
+    gradient restricted to this replica's rows is the conv stack's upstream
+    gradient.  The cross-worker sums are collectives, not part of this step.
+    """
+
+    def __init__(self, schedule, n, in_ch, hw, replicas, fc_shapes, shards, device="cuda"):
+        dev = torch.device(device)
+        self.n, self.R = n, replicas
+        m = n * replicas
+        (in0, out0), (in1, out1) = fc_shapes
+        ns0, ns1 = out0 // shards, out1 // shards
+        assert in1 == out0
+        self.m, self.in0, self.ns0, self.in1, self.ns1 = m, in0, ns0, in1, ns1
+        self.X0 = torch.empty((m, in0), dtype=torch.float32, device=dev)
+        self.dX0p = torch.empty((m, in0), dtype=torch.float32, device=dev)
+        self.X1 = torch.empty((m, in1), dtype=torch.float32, device=dev)
+        self.dX1p = torch.empty((m, in1), dtype=torch.float32, device=dev)
+        self.Y1 = torch.empty((m, ns1), dtype=torch.float32, device=dev)
+        self.dY1 = torch.empty((m, ns1), dtype=torch.float32, device=dev)
+        self.conv = ConvStack(schedule, n, in_ch, hw, "f32", device,
+                              out_buffer=self.X0[:n], out_grad_buffer=self.dX0p[:n])
+        top = self.conv.A[-1]
+        assert int(np.prod(top.shape[1:])) == in0
+        self.fc0 = FCShard(m, in0, ns0, relu=True, ldx=in0, ldy=in1, device=device)
+        self.fc1 = FCShard(m, in1, ns1, relu=False, ldx=in1, ldy=ns1, device=device)
+
+    def load_inputs(self, x, conv_w, conv_b, fc0_w, fc0_b, fc1_w, fc1_b, x0_remote, x1_remote,
+                    dy1):
+        t = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32))
+        self.conv.load_inputs(x, conv_w, conv_b)
+        self.fc0.W.copy_(t(fc0_w)); self.fc0.b.copy_(t(fc0_b))
+        self.fc1.W.copy_(t(fc1_w)); self.fc1.b.copy_(t(fc1_b))
+        self.X0[self.n:].copy_(t(x0_remote))
+        self.X1[:, self.ns0:].copy_(t(x1_remote))
+        self.dY1.copy_(t(dy1))
+
+    def step(self, stream=None):
+        self.conv.forward(stream)
+        X0, X1 = self.X0.data_ptr(), self.X1.data_ptr()
+        self.fc0.forward(X0, X1, stream)                       # Y0 -> X1[:, :ns0]
+        self.fc1.forward(X1, self.Y1.data_ptr(), stream)
+        self.fc1.backward(X1, self.dY1.data_ptr(), None, self.dX1p.data_ptr(), stream=stream)
+        # FC0's output gradient: dX1p[:, :ns0] (row stride in1), ReLU mask X1[:, :ns0].
+        self.fc0.backward(X0, self.dX1p.data_ptr(), X1, self.dX0p.data_ptr(), stream=stream)
+        self.conv.backward(stream)

@@ -1,0 +1,157 @@
+"""GPU parity at the workloads' real shapes, and end-to-end through the stacks.
+
+* Every distinct layer shape of the VGG-16 CIFAR stack (batch 128) runs each
+  conv pass in the same launch configuration the benchmark times; the oracle
+  evaluates a sample of outputs one by one.
+* The whole VGG-16 stack and the hybrid worker step run end-to-end from the
+  seeded inputs at a batch the oracle finishes in seconds; every forward
+  tensor, pool code and gradient is compared layer by layer.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from oracle import stack as OS
+from paper_2112_15317_amd import configs, sb, synth
+from paper_2112_15317_amd.stack import ConvStack, HybridStep
+from tests.helpers import TOL, print_case, rel_l2, sample_idx, to_dev, to_host
+
+pytestmark = pytest.mark.gpu
+
+VGG_CIFAR = configs.conv_layers(configs.VGG16, 3, 32)
+SAMPLES = 3000
+
+
+def _ws(nbytes):
+    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device="cuda")
+
+
+@pytest.mark.parametrize("L", VGG_CIFAR, ids=lambda L: "conv%d_%dx%d_%d" % (L.index + 1, L.c, L.k, L.h))
+def test_vgg_cifar_layer_full_size_sampled(L):
+    n = 128
+    print_case("layer_full", layer=L.index, c=L.c, k=L.k, h=L.h, n=n)
+    seed = 100 + L.index
+    x = np.maximum(synth.normal((n, L.c, L.h, L.w), seed, synth.TID.IMAGES), 0)
+    if L.index == 0:
+        x = synth.normal((n, L.c, L.h, L.w), seed, synth.TID.IMAGES)
+    wt = synth.he_normal_conv3x3(L.k, L.c, seed, synth.TID.CONV_W)
+    dy = synth.normal((n, L.k, L.h, L.w), seed, synth.TID.DY_TOP)
+    relu = not L.pool_after
+    mask = x if L.index > 0 else None
+    xd, wd, dyd = to_dev(x), to_dev(wt), to_dev(dy)
+    df = sb.conv_desc(n, L.c, L.h, L.w, L.k, sb.SB_F32, relu=relu)
+    db_ = sb.conv_desc(n, L.c, L.h, L.w, L.k, sb.SB_F32)
+    ws = _ws(max(sb.sb_conv3x3_workspace_bytes(df, 0), sb.sb_conv3x3_workspace_bytes(db_, 1),
+                 sb.sb_conv3x3_workspace_bytes(db_, 2)))
+    y = torch.empty((n, L.k, L.h, L.w), device="cuda")
+    dx = torch.empty((n, L.c, L.h, L.w), device="cuda")
+    dw = torch.empty((L.k, L.c, 3, 3), device="cuda")
+    dbias = torch.empty((L.k,), device="cuda")
+    sb.sb_conv3x3_fwd(df, xd, wd, None, y, ws)
+    sb.sb_conv3x3_bwd_data(db_, dyd, wd, xd if mask is not None else None, dx, ws)
+    sb.sb_conv3x3_bwd_weight(db_, xd, dyd, dw, dbias, ws)
+    torch.cuda.synchronize()
+    f = sample_idx(y.numel(), SAMPLES, seed)
+    assert rel_l2(to_host(y).ravel()[f], O.conv3x3_fwd_at(x, wt, f, relu=relu)) <= TOL["f32"]
+    f = sample_idx(dx.numel(), SAMPLES, seed + 1)
+    ref = O.conv3x3_bwd_data_at(dy, wt, f, mask_src=mask)
+    assert rel_l2(to_host(dx).ravel()[f], ref) <= TOL["f32"]
+    f = sample_idx(dw.numel(), min(SAMPLES, 600), seed + 2)
+    assert rel_l2(to_host(dw).ravel()[f], O.conv3x3_bwd_weight_at(x, dy, f)) <= TOL["f32"]
+    assert rel_l2(to_host(dbias), dy.astype(np.float64).sum(axis=(0, 2, 3))) <= TOL["f32"]
+
+
+def _vgg_inputs(n, hw, seed, layers):
+    x = synth.normal((n, 3, hw, hw), seed, synth.TID.IMAGES)
+    ws = [synth.he_normal_conv3x3(L.k, L.c, seed, synth.TID.CONV_W + L.index) for L in layers]
+    bs = [synth.normal((L.k,), seed, synth.TID.CONV_B + L.index, std=0.05) for L in layers]
+    return x, ws, bs
+
+
+def _near_ties(z, ref_idx, got_idx, eps):
+    """Windows whose codes differ must be near-ties in the oracle's values:
+    the two candidates (or the max and zero, for the ReLU flag) within eps."""
+    bad = np.nonzero(ref_idx.ravel() != got_idx.ravel())[0]
+    if bad.size == 0:
+        return 0
+    n, c, h, w = z.shape
+    zw = z.reshape(n, c, h // 2, 2, w // 2, 2).transpose(0, 1, 2, 4, 3, 5).reshape(-1, 4)
+    for f in bad:
+        a, b = ref_idx.ravel()[f], got_idx.ravel()[f]
+        va, vb = zw[f, a & 3], zw[f, b & 3]
+        gap = abs(va - vb) if (a & 3) != (b & 3) else 0.0
+        flag_gap = abs(va) if (a & 0x80) != (b & 0x80) else 0.0
+        assert max(gap, flag_gap) <= eps, "code mismatch at window %d is not a near-tie" % f
+    return bad.size
+
+
+def test_vgg16_cifar_stack_end_to_end():
+    n, hw = 2, 32
+    print_case("vgg16_stack", n=n, hw=hw)
+    layers = configs.conv_layers(configs.VGG16, 3, hw)
+    x, wts, bs = _vgg_inputs(n, hw, 5, layers)
+    dy_top = synth.normal((n, 512, 1, 1), 5, synth.TID.DY_TOP)
+    st = ConvStack(configs.VGG16, n, 3, hw, "f32")
+    st.load_inputs(x, wts, bs, dy_top)
+    st.step()
+    torch.cuda.synchronize()
+    pools = [L.pool_after for L in layers]
+    f, b = OS.vgg_step(x, wts, bs, pools, dy_top)
+    flips = 0
+    for L in layers:
+        i = L.index
+        if L.pool_after:
+            z = f["Z"][i]
+            assert rel_l2(to_host(st.Z[i]), z) <= TOL["f32"], "Z%d" % i
+            eps = 1e-5 * np.sqrt(np.mean(z * z))
+            flips += _near_ties(z, f["idx"][i], st.idx[i].cpu().numpy(), eps)
+        assert rel_l2(to_host(st.A[i + 1]), f["A"][i + 1]) <= TOL["f32"], "A%d" % (i + 1)
+    if flips == 0:
+        # Identical ReLU / pool decisions: every gradient meets the bound.
+        for L in layers:
+            i = L.index
+            assert rel_l2(to_host(st.grad_at_conv_output(i)), b["dZ"][i]) <= TOL["f32"], "dZ%d" % i
+            assert rel_l2(to_host(st.dW[i]), b["dW"][i]) <= TOL["f32"], "dW%d" % i
+            assert rel_l2(to_host(st.db[i]), b["db"][i]) <= TOL["f32"], "db%d" % i
+        assert rel_l2(to_host(st.gA[0]), b["dX"]) <= TOL["f32"]
+    else:
+        pytest.fail("%d certified near-tie pool decisions differ; choose another seed" % flips)
+
+
+def test_hybrid_worker_step_end_to_end():
+    n, hw, R, S = 2, 32, 4, 4
+    print_case("hybrid_step", n=n, replicas=R, shards=S)
+    layers = configs.conv_layers(configs.VGG16, 3, hw)
+    x, wts, bs = _vgg_inputs(n, hw, 6, layers)
+    (in0, out0), (in1, out1) = configs.CONFIGS[4]["fc"]
+    m, ns0, ns1 = n * R, out0 // S, out1 // S
+    w0 = np.ascontiguousarray(synth.xavier_uniform(in0, out0, 6, synth.TID.FC_W + 0)[:, :ns0])
+    w1 = np.ascontiguousarray(synth.xavier_uniform(in1, out1, 6, synth.TID.FC_W + 1)[:, :ns1])
+    b0 = synth.normal((ns0,), 6, synth.TID.FC_B + 0, std=0.05)
+    b1 = synth.normal((ns1,), 6, synth.TID.FC_B + 1, std=0.05)
+    x0r = synth.relu_normal((m - n, in0), 6, synth.TID.X0_REMOTE)
+    x1r = synth.relu_normal((m, in1 - ns0), 6, synth.TID.X1_REMOTE)
+    dy1 = synth.normal((m, ns1), 6, synth.TID.FC_DY)
+    hs = HybridStep(configs.VGG16, n, 3, hw, R, [(in0, out0), (in1, out1)], S)
+    hs.load_inputs(x, wts, bs, w0, b0, w1, b1, x0r, x1r, dy1)
+    hs.step()
+    torch.cuda.synchronize()
+    pools = [L.pool_after for L in layers]
+    r = OS.hybrid_step(x, wts, bs, pools, w0, b0, w1, b1, x0r, x1r, dy1)
+    tol = TOL["f32"]
+    assert rel_l2(to_host(hs.X0), r["x0"]) <= tol
+    assert rel_l2(to_host(hs.X1), r["x1"]) <= tol
+    assert rel_l2(to_host(hs.Y1), r["y1"]) <= tol
+    assert rel_l2(to_host(hs.dX1p), r["dx1p"]) <= tol
+    assert rel_l2(to_host(hs.fc1.dW), r["dw1"]) <= tol
+    assert rel_l2(to_host(hs.fc1.db), r["db1"]) <= tol
+    assert rel_l2(to_host(hs.dX0p), r["dx0p"]) <= tol
+    assert rel_l2(to_host(hs.fc0.dW), r["dw0"]) <= tol
+    assert rel_l2(to_host(hs.fc0.db), r["db0"]) <= tol
+    for L in layers:
+        i = L.index
+        if L.pool_after:
+            np.testing.assert_array_equal(hs.conv.idx[i].cpu().numpy(), r["fwd"]["idx"][i])
+        assert rel_l2(to_host(hs.conv.dW[i]), r["bwd"]["dW"][i]) <= tol, "dW%d" % i
+    assert rel_l2(to_host(hs.conv.gA[0]), r["bwd"]["dX"]) <= tol
