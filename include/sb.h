@@ -116,6 +116,14 @@ sb_status sb_conv3x3_bwd_weight(const sb_conv3x3_desc *desc, const void *x,
                                 void *workspace, size_t workspace_bytes,
                                 void *stream);
 
+/* Describes the launch plan `pass` would use for `desc`: the name of the
+ * main kernel as a profiler reports it, the grid and whether a split
+ * reduction follows.  Writes at most `len` bytes (NUL-terminated) into buf
+ * and returns the length of the full string plus one; returns 0 for an
+ * invalid or unsupported descriptor.  Enqueues nothing. */
+size_t sb_conv3x3_plan_string(const sb_conv3x3_desc *desc, int pass, char *buf,
+                              size_t len);
+
 /* ------------------------------------------------------------------------
  * Fused ReLU + 2x2 max pooling, stride 2 (sec. 2.2: pooling layers
  * subsample; sec. 3.1 Layer Partitioning: pooling is never partitioned).

@@ -9,6 +9,8 @@ sb_status conv_igemm_f32(bool dgrad, int N, int Cin, int H, int W, int Cout, con
                          const float* wt, const float* bias, const float* mask, float* out,
                          void* ws, size_t ws_bytes, int relu, hipStream_t st);
 size_t conv_wgrad_ws(int N, int C, int H, int W, int K);
+int conv_igemm_describe(bool dgrad, int N, int Cin, int H, int W, int Cout, char* buf, size_t len);
+int conv_wgrad_describe(int N, int C, int H, int W, int K, char* buf, size_t len);
 sb_status conv_wgrad_f32(int N, int C, int H, int W, int K, const float* x, const float* dy,
                          float* dw, float* db, void* ws, size_t ws_bytes, hipStream_t st);
 }  // namespace sbh
@@ -113,4 +115,17 @@ extern "C" sb_status sb_conv3x3_bwd_weight(const sb_conv3x3_desc* d, const void*
     return SB_ERR_INVALID_ARG;
   return sbh::conv_wgrad_f32(d->n, d->c, d->h, d->w, d->k, (const float*)x, (const float*)dy, dw,
                              db, ws, ws_bytes, sbh::stream_of(stream));
+}
+
+extern "C" size_t sb_conv3x3_plan_string(const sb_conv3x3_desc* d, int pass, char* buf,
+                                         size_t len) {
+  if (pass < SB_PASS_FWD || pass > SB_PASS_BWD_WEIGHT) return 0;
+  if (conv_check(d, pass) != SB_OK) return 0;
+  int r;
+  switch (pass) {
+    case SB_PASS_FWD: r = sbh::conv_igemm_describe(false, d->n, d->c, d->h, d->w, d->k, buf, len); break;
+    case SB_PASS_BWD_DATA: r = sbh::conv_igemm_describe(true, d->n, d->k, d->h, d->w, d->c, buf, len); break;
+    default: r = sbh::conv_wgrad_describe(d->n, d->c, d->h, d->w, d->k, buf, len); break;
+  }
+  return r < 0 ? 0 : (size_t)r + 1;
 }

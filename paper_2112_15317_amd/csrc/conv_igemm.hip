@@ -27,6 +27,7 @@
 #include "sb_internal.hpp"
 
 #include <algorithm>
+#include <cstdio>
 
 namespace sb {
 
@@ -40,7 +41,9 @@ struct ConvTile {
   // Channel stride of the halo in LDS: a multiple of 64 floats plus 16, so
   // the four k-rows an MFMA operand read touches land in different banks.
   static constexpr int PLANE_P = (PLANE + 63) / 64 * 64 + 16;
-  static constexpr int BN_P = BN + 16;
+  // Row stride of the filter slice in LDS: 16 for BN = 16 (four k-rows fill
+  // 64 consecutive banks), otherwise BN plus 16 (= 16 mod 64).
+  static constexpr int BN_P = BN == 16 ? 16 : BN + 16;
   static constexpr int HALO = CK * PLANE;
   static constexpr int WTS = 9 * CK * BN;
   static constexpr int HALO_PT = (HALO + 255) / 256;
@@ -48,7 +51,9 @@ struct ConvTile {
   static constexpr int LDS_X = CK * PLANE_P;
   static constexpr int LDS_W = 9 * CK * BN_P;
   static constexpr int LDS_BUF = LDS_X + LDS_W;
-  static constexpr int WN = BN / 2, WM = BM / 2;
+  // Waves split the tile 2 x 2 (BN >= 32) or 1 x 4 along pixels (BN = 16).
+  static constexpr int WAVES_N = BN >= 32 ? 2 : 1, WAVES_M = 4 / WAVES_N;
+  static constexpr int WN = BN / WAVES_N, WM = BM / WAVES_M;
   static constexpr int NB = WN / 16, MB = WM / 16;
   static constexpr size_t LDS_BYTES = 2 * LDS_BUF * sizeof(float);
   static_assert(LDS_BYTES <= 80 * 1024, "two blocks must fit in the 160 KB of LDS");
@@ -63,7 +68,7 @@ __global__ __launch_bounds__(256, 2) void conv3x3_igemm_f32(
   extern __shared__ float lds[];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wn = wave >> 1, wm = wave & 1;
+  const int wm = wave % T::WAVES_M, wn = wave / T::WAVES_M;
   const int kq = lane >> 4, lr = lane & 15;
 
   int bt = blockIdx.x;
@@ -233,15 +238,16 @@ __global__ __launch_bounds__(256, 2) void conv3x3_igemm_f32(
   }
 }
 
-// Sum of the split partials in split order, then the epilogue.
+// Sum of the split partials in a fixed order, then the epilogue.
 __global__ __launch_bounds__(256) void conv_splitk_reduce(
     const float* __restrict__ part, int splits, size_t total, int Cout, size_t HWs,
     const float* __restrict__ bias, int relu, const float* __restrict__ mask,
     float* __restrict__ out) {
-  size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= total) return;
-  float v = 0.f;
-  for (int s = 0; s < splits; ++s) v += part[(size_t)s * total + i];
+  __shared__ float lds[256];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const size_t i = (size_t)blockIdx.x * 64 + lane;
+  float v = SplitSum{part, splits, total}(i, wave, lds, lane);
+  if (wave != 0 || i >= total) return;
   if (bias) v += bias[(i / HWs) % Cout];
   if (relu && !(v > 0.f)) v = 0.f;
   if (mask && !(mask[i] > 0.f)) v = 0.f;
@@ -262,6 +268,7 @@ using TileW8 = ConvTile<8, 8, 2, 8, 64>;
 using TileW4 = ConvTile<4, 4, 8, 8, 64>;
 using TileW2 = ConvTile<2, 2, 32, 8, 64>;
 using TileW32c4 = ConvTile<4, 32, 1, 4, 64>;
+using TileW32n16 = ConvTile<4, 32, 1, 8, 16>;
 
 static void tile_dims(int t, int& th, int& tw, int& imgs, int& ck, int& bn) {
   switch (t) {
@@ -270,14 +277,16 @@ static void tile_dims(int t, int& th, int& tw, int& imgs, int& ck, int& bn) {
     case 2: th = 8; tw = 8; imgs = 2; ck = 8; break;
     case 3: th = 4; tw = 4; imgs = 8; ck = 8; break;
     case 4: th = 2; tw = 2; imgs = 32; ck = 8; break;
-    default: th = 4; tw = 32; imgs = 1; ck = 4; break;
+    case 5: th = 4; tw = 32; imgs = 1; ck = 4; break;
+    default: th = 4; tw = 32; imgs = 1; ck = 8; bn = 16; return;
   }
   bn = 64;
 }
 
 static IgemmPlan igemm_plan(int N, int Cin, int H, int W, int Cout) {
   IgemmPlan p{};
-  if (Cin <= 4 && W >= 32) p.tile = 5;
+  if (Cout <= 16 && Cin > 4 && W >= 32) p.tile = 6;
+  else if (Cin <= 4 && W >= 32) p.tile = 5;
   else if (W >= 32) p.tile = 0;
   else if (W >= 16) p.tile = 1;
   else if (W >= 8) p.tile = 2;
@@ -317,7 +326,7 @@ static void igemm_launch(const IgemmPlan& p, const float* in, const float* wt,
       Cout, p.tiles_w, p.tiles_h, p.cps, part ? 0 : relu, part ? 1 : 0);
   if (part) {
     size_t total = (size_t)N * Cout * H * W;
-    conv_splitk_reduce<<<(unsigned)((total + 255) / 256), 256, 0, st>>>(
+    conv_splitk_reduce<<<(unsigned)((total + 63) / 64), 256, 0, st>>>(
         ws, p.splits, total, Cout, (size_t)H * W, bias, relu, mask, out);
   }
 }
@@ -332,7 +341,8 @@ static void igemm_dispatch(const IgemmPlan& p, const float* in, const float* wt,
     case 2: igemm_launch<TileW8, DGRAD>(p, in, wt, bias, mask, out, ws, N, Cin, H, W, Cout, relu, st); break;
     case 3: igemm_launch<TileW4, DGRAD>(p, in, wt, bias, mask, out, ws, N, Cin, H, W, Cout, relu, st); break;
     case 4: igemm_launch<TileW2, DGRAD>(p, in, wt, bias, mask, out, ws, N, Cin, H, W, Cout, relu, st); break;
-    default: igemm_launch<TileW32c4, DGRAD>(p, in, wt, bias, mask, out, ws, N, Cin, H, W, Cout, relu, st); break;
+    case 5: igemm_launch<TileW32c4, DGRAD>(p, in, wt, bias, mask, out, ws, N, Cin, H, W, Cout, relu, st); break;
+    default: igemm_launch<TileW32n16, DGRAD>(p, in, wt, bias, mask, out, ws, N, Cin, H, W, Cout, relu, st); break;
   }
 }
 
@@ -343,6 +353,18 @@ namespace sbh {
 
 size_t conv_igemm_ws(int N, int Cin, int H, int W, int Cout) {
   return sb::igemm_plan(N, Cin, H, W, Cout).ws_bytes;
+}
+
+int conv_igemm_describe(bool dgrad, int N, int Cin, int H, int W, int Cout, char* buf,
+                        size_t len) {
+  sb::IgemmPlan p = sb::igemm_plan(N, Cin, H, W, Cout);
+  int th, tw, imgs, ck, bn;
+  sb::tile_dims(p.tile, th, tw, imgs, ck, bn);
+  return snprintf(buf, len,
+                  "sb::conv3x3_igemm_f32<sb::ConvTile<%d, %d, %d, %d, %d>, %s> grid=%dx%dx%d%s",
+                  th, tw, imgs, ck, bn, dgrad ? "true" : "false",
+                  p.tiles_w * p.tiles_h * p.tiles_n, p.co_tiles, p.splits,
+                  p.splits > 1 ? " +sb::conv_splitk_reduce" : "");
 }
 
 sb_status conv_igemm_f32(bool dgrad, int N, int Cin, int H, int W, int Cout, const float* in,

@@ -4,35 +4,45 @@
 //   db[k]       = sum_{n,h,w} dy[n,k,h,w]
 //
 // GEMM view: rows = output channels k, columns = (input channel c, tap),
-// reduction = every pixel of the batch.  A block owns 64 k x 16 c x 9 taps
-// and walks a contiguous range of 64-pixel tiles (IMGS images x TH rows x
-// TW cols).  Per pixel tile it stages in LDS
+// reduction = every pixel of the batch.  A block owns 64 k and walks a
+// contiguous range of 64-pixel tiles (IMGS images x TH rows x TW cols).  Per
+// pixel tile it stages in LDS
 //   * dy: 64 k x 64 pixels, stored [pixel][k] so an MFMA operand read of 16
 //     consecutive k is bank-conflict free, and
-//   * the x halo: 16 c x IMGS x (TH+2) x (TW+2), stored [halo pixel][c],
-//     read once and shifted for each of the 9 taps.
-// Each wave owns 16 k and multiplies one dy fragment against the 9 tap-
-// shifted x fragments per 4-pixel step (9 MFMAs per step).  Blocks of the
-// first c tile also multiply dy against a column of ones, which yields the
-// bias gradient in the same pass.
+//   * the x halo: BC channels x IMGS x (TH+2) x (TW+2), stored [halo pixel][c],
+//     read once and shifted per tap.
+// Two column layouts:
+//   * wide (C >= 16): a block owns 16 channels x 9 taps; per 4-pixel step a
+//     wave multiplies one dy fragment against 9 tap-shifted x fragments.
+//   * narrow (C <= 7, e.g. the RGB input layer): a block owns every (c, tap)
+//     pair, flattened into NCB blocks of 16 MFMA columns; each lane gathers
+//     its own (c, tap) from the halo, so only the padding of C*9 up to a
+//     multiple of 16 is wasted instead of 16 - C channels.
+// Blocks of the first column tile also multiply dy against a column of ones,
+// which yields the bias gradient in the same pass.
 //
 // The reduction dimension is long (up to N*H*W = 131072 here) while the
 // output is small, so pixel tiles are split over gridDim.z; each split writes
-// its partial sums to the workspace and wgrad_reduce adds the splits in a
+// its partial sums to the workspace and splits_reduce adds the splits in a
 // fixed order.  No atomics: results are bitwise reproducible.
 #include "sb_internal.hpp"
 
 #include <algorithm>
+#include <cstdio>
 
 namespace sb {
 
-template <int TH_, int TW_, int IMGS_>
+template <int TH_, int TW_, int IMGS_, int NCB_>
 struct WgTile {
   static constexpr int TH = TH_, TW = TW_, IMGS = IMGS_;
-  static constexpr int BP = IMGS * TH * TW;   // pixels per tile
+  static constexpr int NCB = NCB_;                  // 0: wide layout; else narrow column blocks
+  static constexpr bool NARROW = NCB_ > 0;
+  static constexpr int BP = IMGS * TH * TW;         // pixels per tile
   static_assert(BP == 64, "64-pixel tiles");
   static_assert(TW % 4 == 0 || (TW == 2 && TH == 2), "4-pixel steps must map uniformly");
-  static constexpr int BK = 64, BC = 16;
+  static constexpr int BK = 64;
+  static constexpr int BC = NARROW ? 8 : 16;        // channels staged per block
+  static constexpr int NACC = NARROW ? NCB : 9;     // accumulator blocks per wave
   static constexpr int HH = TH + 2, HW = TW + 2;
   static constexpr int PLANE = IMGS * HH * HW;      // halo pixels per channel
   static constexpr int DY_STRIDE = BK + 16;         // floats per pixel row of dy
@@ -71,9 +81,21 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_f32(
   // Lane offset of pixel (step base + jq) relative to the step base's halo offset.
   const int lane_hoff = wg_hoff<T>(jq);
 
-  f4 acc[9], accb = f4{0.f, 0.f, 0.f, 0.f};
+  // Narrow layout: this lane's (c, tap) column in each column block.
+  int col_off[T::NARROW ? T::NCB : 1];
+  bool col_ok[T::NARROW ? T::NCB : 1];
+  if (T::NARROW) {
 #pragma unroll
-  for (int t = 0; t < 9; ++t) acc[t] = f4{0.f, 0.f, 0.f, 0.f};
+    for (int cb = 0; cb < (T::NARROW ? T::NCB : 1); ++cb) {
+      int j = cb * 16 + lr, c = j / 9, t = j - c * 9;
+      col_ok[cb] = j < C * 9;
+      col_off[cb] = col_ok[cb] ? ((t / 3) * T::HW + (t % 3)) * T::BC + c : 0;
+    }
+  }
+
+  f4 acc[T::NACC], accb = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int t = 0; t < T::NACC; ++t) acc[t] = f4{0.f, 0.f, 0.f, 0.f};
 
   float rdy[T::DY_PT], rx[T::X_PT];
 
@@ -145,11 +167,21 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_f32(
       const int pbase = st * 4;
       const int hbase = wg_hoff<T>(pbase);          // compile-time after unrolling
       float a = Dl[(pbase + jq) * T::DY_STRIDE + wave * 16 + lr];
+      const float* Xp = Xl + (hbase + lane_hoff) * T::BC;
+      if (T::NARROW) {
 #pragma unroll
-      for (int t = 0; t < 9; ++t) {
-        const int toff = (t / 3) * T::HW + (t % 3);
-        float b = Xl[(hbase + lane_hoff + toff) * T::BC + lr];
-        acc[t] = mfma16x16x4(a, b, acc[t]);
+        for (int cb = 0; cb < T::NACC; ++cb) {
+          float b = Xp[col_off[cb % (T::NARROW ? T::NCB : 1)]];
+          b = col_ok[cb % (T::NARROW ? T::NCB : 1)] ? b : 0.f;
+          acc[cb] = mfma16x16x4(a, b, acc[cb]);
+        }
+      } else {
+#pragma unroll
+        for (int t = 0; t < 9; ++t) {
+          const int toff = (t / 3) * T::HW + (t % 3);
+          float b = Xp[toff * T::BC + lr];
+          acc[t] = mfma16x16x4(a, b, acc[t]);
+        }
       }
       if (do_db) accb = mfma16x16x4(a, 1.0f, accb);
     }
@@ -157,16 +189,25 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_f32(
     __syncthreads();
   }
 
-  // Output: acc[t] lane holds k = k0 + wave*16 + 4*jq + i, c = c0 + lr.
-  const int c = c0 + lr;
+  // acc[t] lane holds rows k = k0 + wave*16 + 4*jq + i and column lr of its block.
   const size_t wsz = (size_t)K * C * 9;
   float* dst = dw + (partial ? (size_t)blockIdx.z * wsz : 0);
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     int k = k0 + wave * 16 + 4 * jq + i;
-    if (k >= K || c >= C) continue;
+    if (k >= K) continue;
+    if (T::NARROW) {
 #pragma unroll
-    for (int t = 0; t < 9; ++t) dst[((size_t)k * C + c) * 9 + t] = acc[t][i];
+      for (int cb = 0; cb < T::NACC; ++cb) {
+        int j = cb * 16 + lr;                       // flattened (c, tap)
+        if (j < C * 9) dst[(size_t)k * C * 9 + j] = acc[cb][i];
+      }
+    } else {
+      int c = c0 + lr;
+      if (c >= C) continue;
+#pragma unroll
+      for (int t = 0; t < 9; ++t) dst[((size_t)k * C + c) * 9 + t] = acc[t][i];
+    }
   }
   if (do_db && lr == 0) {
     float* dbd = db + (partial ? (size_t)blockIdx.z * K : 0);
@@ -178,14 +219,14 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_f32(
   }
 }
 
-// dst[i] = sum over splits s (in order) of part[s*total + i].
+// dst[i] = sum over the splits of part[s*total + i], in a fixed order.
 __global__ __launch_bounds__(256) void splits_reduce(const float* __restrict__ part, int splits,
                                                      size_t total, float* __restrict__ dst) {
-  size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= total) return;
-  float v = 0.f;
-  for (int s = 0; s < splits; ++s) v += part[(size_t)s * total + i];
-  dst[i] = v;
+  __shared__ float lds[256];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const size_t i = (size_t)blockIdx.x * 64 + lane;
+  float v = SplitSum{part, splits, total}(i, wave, lds, lane);
+  if (wave == 0 && i < total) dst[i] = v;
 }
 
 struct WgPlan {
@@ -193,16 +234,27 @@ struct WgPlan {
   size_t ws_bytes;
 };
 
-using WgW32 = WgTile<2, 32, 1>;
-using WgW16 = WgTile<4, 16, 1>;
-using WgW8 = WgTile<8, 8, 1>;
-using WgW4 = WgTile<4, 4, 4>;
-using WgW2 = WgTile<2, 2, 16>;
+// Wide layouts (16 channels x 9 taps per block), by image width.
+using WgW32 = WgTile<2, 32, 1, 0>;
+using WgW16 = WgTile<4, 16, 1, 0>;
+using WgW8 = WgTile<8, 8, 1, 0>;
+using WgW4 = WgTile<4, 4, 4, 0>;
+using WgW2 = WgTile<2, 2, 16, 0>;
+// Narrow layouts (all C <= 7 channels x 9 taps in NCB column blocks).
+using WgN32_2 = WgTile<2, 32, 1, 2>;   // C <= 3
+using WgN32_4 = WgTile<2, 32, 1, 4>;   // C <= 7
+using WgN4_2 = WgTile<4, 4, 4, 2>;
+using WgN4_4 = WgTile<4, 4, 4, 4>;
 
 static WgPlan wg_plan(int N, int C, int H, int W, int K) {
   WgPlan p{};
   int th, tw, imgs;
-  if (W >= 32) { p.tile = 0; th = 2; tw = 32; imgs = 1; }
+  const bool narrow = C <= 7;
+  if (narrow) {
+    // 32-wide rows for wide images, 4x4 x 4-image tiles otherwise.
+    if (W >= 32) { th = 2; tw = 32; imgs = 1; p.tile = C <= 3 ? 5 : 6; }
+    else { th = 4; tw = 4; imgs = 4; p.tile = C <= 3 ? 7 : 8; }
+  } else if (W >= 32) { p.tile = 0; th = 2; tw = 32; imgs = 1; }
   else if (W >= 16) { p.tile = 1; th = 4; tw = 16; imgs = 1; }
   else if (W >= 8) { p.tile = 2; th = 8; tw = 8; imgs = 1; }
   else if (W >= 4) { p.tile = 3; th = 4; tw = 4; imgs = 4; }
@@ -211,11 +263,13 @@ static WgPlan wg_plan(int N, int C, int H, int W, int K) {
   p.tiles_h = cdiv(H, th);
   p.ptiles = p.tiles_w * p.tiles_h * cdiv(N, imgs);
   p.k_tiles = cdiv(K, 64);
-  p.c_tiles = cdiv(C, 16);
+  p.c_tiles = narrow ? 1 : cdiv(C, 16);
   long blocks = (long)p.k_tiles * p.c_tiles;
+  // About two blocks per CU, but at most 128 splits of the pixel range.
   const long target = 512;
   int splits = 1;
-  if (blocks < target) splits = (int)std::min<long>(p.ptiles, cdiv((int)target, (int)blocks));
+  if (blocks < target)
+    splits = (int)std::min<long>(std::min<long>(p.ptiles, 128), cdiv((int)target, (int)blocks));
   p.tps = cdiv(p.ptiles, splits);
   p.splits = cdiv(p.ptiles, p.tps);
   p.ws_bytes = p.splits > 1 ? (size_t)p.splits * ((size_t)K * C * 9 + K) * sizeof(float) : 0;
@@ -240,9 +294,9 @@ static void wg_launch(const WgPlan& p, const float* x, const float* dy, float* d
       x, dy, pdw, pdb, N, C, H, W, K, p.tiles_w, p.tiles_h, p.ptiles, p.tps, p.c_tiles,
       part ? 1 : 0);
   if (part) {
-    splits_reduce<<<(unsigned)((wsz + 255) / 256), 256, 0, st>>>(ws, p.splits, wsz, dw);
+    splits_reduce<<<(unsigned)((wsz + 63) / 64), 256, 0, st>>>(ws, p.splits, wsz, dw);
     if (db)
-      splits_reduce<<<(unsigned)((K + 255) / 256), 256, 0, st>>>(pdb, p.splits, (size_t)K, db);
+      splits_reduce<<<(unsigned)((K + 63) / 64), 256, 0, st>>>(pdb, p.splits, (size_t)K, db);
   }
 }
 
@@ -252,6 +306,16 @@ namespace sbh {
 
 size_t conv_wgrad_ws(int N, int C, int H, int W, int K) {
   return sb::wg_plan(N, C, H, W, K).ws_bytes;
+}
+
+int conv_wgrad_describe(int N, int C, int H, int W, int K, char* buf, size_t len) {
+  static const char* names[] = {"2, 32, 1, 0", "4, 16, 1, 0", "8, 8, 1, 0", "4, 4, 4, 0",
+                                "2, 2, 16, 0", "2, 32, 1, 2", "2, 32, 1, 4", "4, 4, 4, 2",
+                                "4, 4, 4, 4"};
+  sb::WgPlan p = sb::wg_plan(N, C, H, W, K);
+  return snprintf(buf, len, "sb::conv3x3_wgrad_f32<sb::WgTile<%s> > grid=%dx1x%d%s",
+                  names[p.tile], p.k_tiles * p.c_tiles, p.splits,
+                  p.splits > 1 ? " +sb::splits_reduce" : "");
 }
 
 sb_status conv_wgrad_f32(int N, int C, int H, int W, int K, const float* x, const float* dy,
@@ -264,7 +328,11 @@ sb_status conv_wgrad_f32(int N, int C, int H, int W, int K, const float* x, cons
     case 1: sb::wg_launch<sb::WgW16>(p, x, dy, dw, db, w, N, C, H, W, K, st); break;
     case 2: sb::wg_launch<sb::WgW8>(p, x, dy, dw, db, w, N, C, H, W, K, st); break;
     case 3: sb::wg_launch<sb::WgW4>(p, x, dy, dw, db, w, N, C, H, W, K, st); break;
-    default: sb::wg_launch<sb::WgW2>(p, x, dy, dw, db, w, N, C, H, W, K, st); break;
+    case 4: sb::wg_launch<sb::WgW2>(p, x, dy, dw, db, w, N, C, H, W, K, st); break;
+    case 5: sb::wg_launch<sb::WgN32_2>(p, x, dy, dw, db, w, N, C, H, W, K, st); break;
+    case 6: sb::wg_launch<sb::WgN32_4>(p, x, dy, dw, db, w, N, C, H, W, K, st); break;
+    case 7: sb::wg_launch<sb::WgN4_2>(p, x, dy, dw, db, w, N, C, H, W, K, st); break;
+    default: sb::wg_launch<sb::WgN4_4>(p, x, dy, dw, db, w, N, C, H, W, K, st); break;
   }
   return launch_status();
 }

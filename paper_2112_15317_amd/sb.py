@@ -45,6 +45,7 @@ SIGNATURES = {
     "sb_status_string": (ctypes.c_char_p, [_i]),
     "sb_version": (_i, []),
     "sb_conv3x3_workspace_bytes": (_sz, [ctypes.POINTER(sb_conv3x3_desc), _i]),
+    "sb_conv3x3_plan_string": (_sz, [ctypes.POINTER(sb_conv3x3_desc), _i, ctypes.c_char_p, _sz]),
     "sb_conv3x3_fwd": (_i, [ctypes.POINTER(sb_conv3x3_desc), _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "sb_conv3x3_bwd_data": (_i, [ctypes.POINTER(sb_conv3x3_desc), _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "sb_conv3x3_bwd_weight": (_i, [ctypes.POINTER(sb_conv3x3_desc), _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
@@ -146,6 +147,14 @@ def sb_version():
 
 def sb_conv3x3_workspace_bytes(desc, pass_):
     return load().sb_conv3x3_workspace_bytes(ctypes.byref(desc), pass_)
+
+
+def sb_conv3x3_plan_string(desc, pass_):
+    buf = ctypes.create_string_buffer(512)
+    n = load().sb_conv3x3_plan_string(ctypes.byref(desc), pass_, buf, 512)
+    if n == 0:
+        raise SBError("sb_conv3x3_plan_string", SB_ERR_INVALID_ARG)
+    return buf.value.decode()
 
 
 def sb_conv3x3_fwd(desc, x, w, bias, y, ws=None, stream=None):

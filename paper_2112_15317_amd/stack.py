@@ -33,12 +33,15 @@ class EventTimer:
     """Brackets calls with HIP events on the current stream; per-key lists of
     (start, stop) pairs are read after a synchronisation."""
 
-    def __init__(self):
+    def __init__(self, external=False):
+        # external=True: the events become record nodes of a captured graph
+        # and are stamped at every replay.
         self.events = {}
+        self.external = external
 
     def __call__(self, key, fn, *args):
-        s = torch.cuda.Event(enable_timing=True)
-        e = torch.cuda.Event(enable_timing=True)
+        s = torch.cuda.Event(enable_timing=True, external=self.external)
+        e = torch.cuda.Event(enable_timing=True, external=self.external)
         s.record()
         fn(*args)
         e.record()
@@ -53,6 +56,19 @@ class EventTimer:
 
 def _plain(key, fn, *args):
     fn(*args)
+
+
+def capture_graph(step_fn, steps=1):
+    """Record `steps` calls of step_fn into a HIP graph (through torch's
+    graph capture: libsb enqueues on the current stream, which is the
+    capturing one).  Launch-bound sequences of small kernels then replay with
+    no per-launch host cost.  step_fn must have run eagerly once before, so
+    that one-time kernel attribute setup happens outside the capture."""
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for _ in range(steps):
+            step_fn()
+    return g
 
 
 class ConvStack:
@@ -171,6 +187,17 @@ class ConvStack:
     def step(self, stream=None):
         self.forward(stream)
         self.backward(stream)
+
+    def step_calls(self):
+        """The ordered (key, libsb function, args) calls of one step."""
+        rec = []
+        saved = self.call
+        self.call = lambda key, fn, *args: rec.append((key, fn, args))
+        try:
+            self.step()
+        finally:
+            self.call = saved
+        return rec
 
 
 class FCShard:

@@ -155,3 +155,30 @@ def test_hybrid_worker_step_end_to_end():
             np.testing.assert_array_equal(hs.conv.idx[i].cpu().numpy(), r["fwd"]["idx"][i])
         assert rel_l2(to_host(hs.conv.dW[i]), r["bwd"]["dW"][i]) <= tol, "dW%d" % i
     assert rel_l2(to_host(hs.conv.gA[0]), r["bwd"]["dX"]) <= tol
+
+
+def test_graph_replay_matches_eager():
+    """The benchmark replays the step from a captured HIP graph: every replay,
+    with eager work and synchronisations in between, must reproduce the eager
+    step bit for bit (all kernels have a fixed summation order)."""
+    from paper_2112_15317_amd.stack import capture_graph
+    n, hw = 4, 32
+    print_case("graph_replay", n=n, hw=hw)
+    layers = configs.conv_layers(configs.VGG16, 3, hw)
+    x, wts, bs = _vgg_inputs(n, hw, 9, layers)
+    dy_top = synth.normal((n, 512, 1, 1), 9, synth.TID.DY_TOP)
+    st = ConvStack(configs.VGG16, n, 3, hw, "f32")
+    st.load_inputs(x, wts, bs, dy_top)
+    st.step()
+    torch.cuda.synchronize()
+    watch = [st.A[-1], st.gA[0]] + st.dW + st.db + list(st.idx.values())
+    ref = [t.clone() for t in watch]
+    g = capture_graph(st.step, 1)
+    for rep in range(3):
+        for t in watch:
+            t.zero_()                                  # eager work between replays
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for a, b in zip(watch, ref):
+            assert torch.equal(a, b), "replay %d differs from the eager step" % rep
