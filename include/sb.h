@@ -19,6 +19,9 @@
  *    valid until the enqueued work has finished.  The library never
  *    allocates, frees or synchronises inside these calls; scratch memory is
  *    the caller's workspace (query its size first).
+ *  * The workspace holds split-reduction partial sums; its contents need no
+ *    initialisation and are dead after the call.  Calls that share one
+ *    workspace must not run concurrently (use one workspace per stream).
  *  * `stream` is a hipStream_t passed as void* (NULL = the null stream).
  *    All work is enqueued on it, asynchronously.
  *  * Arguments are validated before anything is enqueued; on any error

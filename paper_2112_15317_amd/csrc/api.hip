@@ -34,9 +34,10 @@ static sb_status conv_check(const sb_conv3x3_desc* d, int pass) {
   if (d->dtype != SB_F32 && d->dtype != SB_BF16) return SB_ERR_INVALID_ARG;
   if (d->flags & ~SB_FUSE_RELU) return SB_ERR_INVALID_ARG;
   if (pass != SB_PASS_FWD && d->flags) return SB_ERR_INVALID_ARG;
-  // Kernels index a weight tensor and one image plane stack with 32-bit ints.
+  // Kernels index weights and activations with 32-bit ints.
   if ((int64_t)d->k * d->c * 9 >= (1ll << 31)) return SB_ERR_UNSUPPORTED;
-  if ((int64_t)d->h * d->w >= (1ll << 30)) return SB_ERR_UNSUPPORTED;
+  if ((int64_t)d->n * d->c * d->h * d->w >= (1ll << 31)) return SB_ERR_UNSUPPORTED;
+  if ((int64_t)d->n * d->k * d->h * d->w >= (1ll << 31)) return SB_ERR_UNSUPPORTED;
   if (d->dtype == SB_BF16) return SB_ERR_UNSUPPORTED;
   return SB_OK;
 }

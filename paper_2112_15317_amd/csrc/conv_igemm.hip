@@ -4,26 +4,40 @@
 // Forward (sec. 2.2): out[n,co,h,w] = sum_{ci,r,s} in[n,ci,h+r-1,w+s-1] * w[co,ci,r,s].
 // The data gradient is the same contraction with the filters transposed
 // (co <-> ci) and rotated by 180 degrees: dx[n,c,i,j] = sum_{k,r,s}
-// dy[n,k,i+r-1,j+s-1] * w[k,c,2-r,2-s].  One kernel serves both; only the
+// dy[n,k,i+r-1,j+s-1] * w[k,c,2-r,2-s].  Each kernel serves both; only the
 // filter gather differs.
 //
-// GEMM view per block: rows = BN output channels, columns = BM = 128 output
-// pixels (IMGS images x TH rows x TW cols), reduction = input channels x 9
-// taps.  For each chunk of CK input channels the block stages in LDS
-//   * the input halo: CK x IMGS x (TH+2) x (TW+2) values, read once from HBM
-//     and reused by all 9 taps (a shifted window per tap, no im2col), and
-//   * the filter slice: 9 x CK x BN values, laid out [tap][ci][co].
-// The chunk loop is double-buffered: the global loads of chunk t+1 are in
-// flight (in registers) while chunk t is multiplied out of LDS.
-// Four waves split the tile 2 (channels) x 2 (pixels); each wave owns
-// (BN/2) x 64 outputs = (BN/32) x 4 MFMA 16x16 blocks in AGPR/VGPR
-// accumulators.  MFMA rows are channels and columns pixels so that the 16
-// lanes of an output row store 16 consecutive pixels (coalesced NCHW).
+// Two kernels:
 //
-// When the output grid alone cannot fill the 256 CUs (small late layers),
-// the channel chunks are split over gridDim.z; each split writes raw sums to
-// the workspace and conv_splitk_reduce adds them in a fixed order and applies
-// the epilogue (bias + ReLU, or the ReLU mask of the layer below).
+// conv3x3_igemm_f32 (any shape).  GEMM view per block: rows = BN output
+// channels, columns = BM = 128 output pixels (IMGS images x TH rows x TW
+// cols), reduction = input channels x 9 taps.  Per chunk of CK input
+// channels the block stages in LDS the input halo (CK x IMGS x (TH+2) x
+// (TW+2), read once, then read at 9 shifted windows: no im2col) and the
+// filter slice [tap][ci][co].  Pipeline per chunk t: store chunk t+1 (already
+// in registers) into the other LDS buffer, issue the global loads of chunk
+// t+2, multiply chunk t out of LDS, barrier.  MFMA operand fragments are
+// double-buffered in registers so LDS reads run one k-step ahead of the
+// MFMAs.  Gathers are branch-free (clamped index + select).  MFMA rows are
+// channels and columns pixels, so the 16 lanes of an output row store 16
+// consecutive pixels (coalesced NCHW).
+//
+// conv3x3_small_f32 (whole images of 2x2 or 4x4 pixels, the late VGG
+// layers).  A tile holds 16*G whole images, ordered position-major: one MFMA
+// column block is 16 images at the same pixel position, so whether a tap
+// falls in the zero padding is known at compile time for every block and
+// those MFMAs are never issued (4 of 9 taps survive at 2x2, 100 of 144 at
+// 4x4).  Whole images need no halo; LDS holds [ci][position][image] with the
+// image index innermost (conflict-free operand reads), filled with float4
+// loads of whole image planes.  The output tile is staged through LDS so it
+// is written with coalesced float4 stores.
+//
+// Both kernels split the channel chunks over gridDim.z when the output grid
+// alone cannot fill the 256 CUs; each split writes its raw partial tile to
+// the workspace and conv_splitk_reduce adds the splits in a fixed order and
+// applies the epilogue.  (Reducing inside the kernel with a last-block
+// counter needs device-scope fences, which write back the per-XCD L2s on
+// this chip and cost far more than the extra launch.)
 #include "sb_internal.hpp"
 
 #include <algorithm>
@@ -31,6 +45,66 @@
 
 namespace sb {
 
+struct ConvArgs {
+  const float* in;       // [N][Cin][H][W]
+  const float* wt;       // forward filters [K][C][3][3]
+  const float* bias;     // [Cout] or null (forward)
+  const float* mask;     // [N][Cout][H][W] or null (data gradient)
+  float* out;            // [N][Cout][H][W]
+  float* part;           // split partials [splits][N][Cout][H][W]
+  int N, Cin, H, W, Cout;
+  int tiles_w, tiles_h, chunks_per_split, splits, relu;
+};
+
+__device__ __forceinline__ float conv_epilogue(const ConvArgs& a, float v, int co, size_t off) {
+  if (a.bias) v += a.bias[co];
+  if (a.relu && !(v > 0.f)) v = 0.f;
+  if (a.mask && !(a.mask[off] > 0.f)) v = 0.f;
+  return v;
+}
+
+// The filter slice lives in LDS as rows r = tap*CK + ci of BN_P floats
+// (BN_P = 16 mod 64), so the MFMA operand read (rows r..r+3, 16 consecutive
+// co per row) is conflict-free.  The staging writes, which follow the
+// global order for coalescing, do conflict; measured, that costs less than
+// the registers an XOR swizzle of the rows needs.
+//
+// Filter slice gather for one chunk: element e (0 <= e < 9*CK*BN), ordered
+// so that neighbouring threads read neighbouring global addresses.
+// Forward: global [co][ci][tap] -> LDS [tap][ci][co].  Data gradient: the
+// forward filters [k][c][tap] with k = this conv's input channel, global
+// order [ci][co][tap] -> LDS [8 - tap][ci][co] (the 180-degree rotation).
+template <bool DGRAD, int CK, int BN, int BN_P>
+__device__ __forceinline__ void filter_plan(int e, int co0, int Cin, int Cout, int& goff,
+                                            int& loff, int& ci) {
+  if (!DGRAD) {
+    int nn = e / (CK * 9), rem = e - nn * (CK * 9);
+    int cc = rem / 9, tap = rem - cc * 9;
+    int co = co0 + nn;
+    ci = cc;
+    goff = co < Cout ? (co * Cin + cc) * 9 + tap : -1;     // + chunk * CK * 9
+    loff = (tap * CK + cc) * BN_P + nn;
+  } else {
+    int kk = e / (BN * 9), rem = e - kk * (BN * 9);
+    int nn = rem / 9, tap = rem - nn * 9;
+    int co = co0 + nn;
+    ci = kk;
+    goff = co < Cout ? (kk * Cout + co) * 9 + tap : -1;    // + chunk * CK * Cout * 9
+    loff = ((8 - tap) * CK + kk) * BN_P + nn;
+  }
+}
+
+template <bool DGRAD>
+__device__ __forceinline__ float filter_load(const ConvArgs& a, int goff, int ci_in_chunk,
+                                             int cbase) {
+  const int ci = cbase + ci_in_chunk;
+  const bool ok = goff >= 0 && ci < a.Cin;
+  const int idx = DGRAD ? goff + cbase * a.Cout * 9 : goff + cbase * 9;
+  const float v = a.wt[ok ? idx : 0];
+  return ok ? v : 0.f;
+}
+
+// ----------------------------------------------------------------- generic --
 template <int TH_, int TW_, int IMGS_, int CK_, int BN_>
 struct ConvTile {
   static constexpr int TH = TH_, TW = TW_, IMGS = IMGS_, CK = CK_, BN = BN_;
@@ -51,20 +125,17 @@ struct ConvTile {
   static constexpr int LDS_X = CK * PLANE_P;
   static constexpr int LDS_W = 9 * CK * BN_P;
   static constexpr int LDS_BUF = LDS_X + LDS_W;
+  static constexpr size_t LDS_BYTES = 2 * LDS_BUF * sizeof(float);
+  static_assert(LDS_BYTES <= 80 * 1024, "two blocks must fit in the 160 KB of LDS");
   // Waves split the tile 2 x 2 (BN >= 32) or 1 x 4 along pixels (BN = 16).
   static constexpr int WAVES_N = BN >= 32 ? 2 : 1, WAVES_M = 4 / WAVES_N;
   static constexpr int WN = BN / WAVES_N, WM = BM / WAVES_M;
   static constexpr int NB = WN / 16, MB = WM / 16;
-  static constexpr size_t LDS_BYTES = 2 * LDS_BUF * sizeof(float);
-  static_assert(LDS_BYTES <= 80 * 1024, "two blocks must fit in the 160 KB of LDS");
+  static constexpr int NSTEP = 9 * (CK / 4);     // MFMA k-steps per chunk
 };
 
 template <class T, bool DGRAD>
-__global__ __launch_bounds__(256, 2) void conv3x3_igemm_f32(
-    const float* __restrict__ in, const float* __restrict__ wt,
-    const float* __restrict__ bias, const float* __restrict__ mask,
-    float* __restrict__ out, int N, int Cin, int H, int W, int Cout,
-    int tiles_w, int tiles_h, int chunks_per_split, int relu, int partial) {
+__global__ __launch_bounds__(256, 2) void conv3x3_igemm_f32(ConvArgs a) {
   extern __shared__ float lds[];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -72,22 +143,18 @@ __global__ __launch_bounds__(256, 2) void conv3x3_igemm_f32(
   const int kq = lane >> 4, lr = lane & 15;
 
   int bt = blockIdx.x;
-  const int tx = bt % tiles_w; bt /= tiles_w;
-  const int ty = bt % tiles_h;
-  const int tn = bt / tiles_h;
+  const int tx = bt % a.tiles_w; bt /= a.tiles_w;
+  const int ty = bt % a.tiles_h;
+  const int tn = bt / a.tiles_h;
   const int n0 = tn * T::IMGS, h0 = ty * T::TH, w0 = tx * T::TW;
   const int co0 = blockIdx.y * T::BN;
-  const int nchunks = cdiv(Cin, T::CK);
-  const int kc0 = blockIdx.z * chunks_per_split;
-  const int kc1 = min(nchunks, kc0 + chunks_per_split);
-  const size_t HWs = (size_t)H * W;
+  const int nchunks = cdiv(a.Cin, T::CK);
+  const int kc0 = blockIdx.z * a.chunks_per_split;
+  const int kc1 = min(nchunks, kc0 + a.chunks_per_split);
+  const int HWs = a.H * a.W;
 
-  // ---- per-thread gather plan (independent of the chunk) ----
-  // Halo element e of a chunk = (channel-in-chunk c, image, halo row, halo
-  // col); its global address is x_base[i] + (chunk*CK + c) * H*W.
-  size_t x_base[T::HALO_PT];
-  int x_c[T::HALO_PT], x_loff[T::HALO_PT];
-  bool x_ok[T::HALO_PT];
+  // ---- gather plans (independent of the chunk) ----
+  int x_off[T::HALO_PT], x_c[T::HALO_PT], x_loff[T::HALO_PT];
 #pragma unroll
   for (int i = 0; i < T::HALO_PT; ++i) {
     int e = tid + i * 256;
@@ -96,41 +163,18 @@ __global__ __launch_bounds__(256, 2) void conv3x3_igemm_f32(
     int img = rem / (T::HH * T::HW), r2 = rem - img * (T::HH * T::HW);
     int yy = r2 / T::HW, xx = r2 - yy * T::HW;
     int n = n0 + img, h = h0 + yy - 1, w = w0 + xx - 1;
-    x_ok[i] = live && n < N && h >= 0 && h < H && w >= 0 && w < W;
+    bool ok = live && n < a.N && h >= 0 && h < a.H && w >= 0 && w < a.W;
+    x_off[i] = ok ? n * a.Cin * HWs + h * a.W + w : -1;   // + ci * H*W
     x_c[i] = c;
-    x_base[i] = x_ok[i] ? (size_t)n * Cin * HWs + (size_t)h * W + w : 0;
     x_loff[i] = live ? c * T::PLANE_P + rem : -1;
   }
-
-  int w_goff[T::WTS_PT], w_loff[T::WTS_PT], w_ci[T::WTS_PT];
-  bool w_ok[T::WTS_PT];
+  int w_off[T::WTS_PT], w_loff[T::WTS_PT], w_ci[T::WTS_PT];
 #pragma unroll
   for (int i = 0; i < T::WTS_PT; ++i) {
     int e = tid + i * 256;
-    bool live = e < T::WTS;
-    if (!DGRAD) {
-      // global order [co][ci][tap] -> LDS [tap][ci][co]
-      int nn = e / (T::CK * 9), rem = e - nn * (T::CK * 9);
-      int cc = rem / 9, tap = rem - cc * 9;
-      int co = co0 + nn;
-      w_ok[i] = live && co < Cout;
-      w_ci[i] = cc;
-      w_goff[i] = (co * Cin + cc) * 9 + tap;     // + chunk * CK * 9
-      w_loff[i] = live ? (tap * T::CK + cc) * T::BN_P + nn : -1;
-    } else {
-      // forward filters [k][c][tap] with k = this conv's input channel:
-      // global order [ci][co][tap] -> LDS [8 - tap][ci][co]
-      int kk = e / (T::BN * 9), rem = e - kk * (T::BN * 9);
-      int nn = rem / 9, tap = rem - nn * 9;
-      int co = co0 + nn;
-      w_ok[i] = live && co < Cout;
-      w_ci[i] = kk;
-      w_goff[i] = (kk * Cout + co) * 9 + tap;    // + chunk * CK * Cout * 9
-      w_loff[i] = live ? ((8 - tap) * T::CK + kk) * T::BN_P + nn : -1;
-    }
+    filter_plan<DGRAD, T::CK, T::BN, T::BN_P>(e, co0, a.Cin, a.Cout, w_off[i], w_loff[i], w_ci[i]);
+    if (e >= T::WTS) { w_off[i] = -1; w_loff[i] = -1; }
   }
-
-  // ---- per-lane operand offsets ----
   int pix_off[T::MB];
 #pragma unroll
   for (int mb = 0; mb < T::MB; ++mb) {
@@ -142,26 +186,22 @@ __global__ __launch_bounds__(256, 2) void conv3x3_igemm_f32(
 
   f4 acc[T::NB][T::MB];
 #pragma unroll
-  for (int a = 0; a < T::NB; ++a)
+  for (int i = 0; i < T::NB; ++i)
 #pragma unroll
-    for (int b = 0; b < T::MB; ++b) acc[a][b] = f4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < T::MB; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
 
   float rx[T::HALO_PT], rw[T::WTS_PT];
-
   auto gload = [&](int kc) {
     const int cbase = kc * T::CK;
 #pragma unroll
     for (int i = 0; i < T::HALO_PT; ++i) {
-      int ci = cbase + x_c[i];
-      rx[i] = (x_ok[i] && ci < Cin) ? in[x_base[i] + (size_t)ci * HWs] : 0.f;
+      const int ci = cbase + x_c[i];
+      const bool ok = x_off[i] >= 0 && ci < a.Cin;
+      const float v = a.in[ok ? x_off[i] + ci * HWs : 0];
+      rx[i] = ok ? v : 0.f;
     }
 #pragma unroll
-    for (int i = 0; i < T::WTS_PT; ++i) {
-      int ci = cbase + w_ci[i];
-      size_t off = DGRAD ? (size_t)w_goff[i] + (size_t)cbase * Cout * 9
-                         : (size_t)w_goff[i] + (size_t)cbase * 9;
-      rw[i] = (w_ok[i] && ci < Cin) ? wt[off] : 0.f;
-    }
+    for (int i = 0; i < T::WTS_PT; ++i) rw[i] = filter_load<DGRAD>(a, w_off[i], w_ci[i], cbase);
   };
   auto lstore = [&](int buf) {
     float* X = lds + buf * T::LDS_BUF;
@@ -173,74 +213,258 @@ __global__ __launch_bounds__(256, 2) void conv3x3_igemm_f32(
     for (int i = 0; i < T::WTS_PT; ++i)
       if (w_loff[i] >= 0) Wl[w_loff[i]] = rw[i];
   };
-
-  if (kc0 < kc1) {
-    gload(kc0);
-    lstore(0);
-  }
-  __syncthreads();
-
-  for (int kc = kc0; kc < kc1; ++kc) {
-    const int buf = (kc - kc0) & 1;
-    const bool more = kc + 1 < kc1;
-    if (more) gload(kc + 1);
+  auto compute = [&](int buf) {
     const float* X = lds + buf * T::LDS_BUF;
     const float* Wl = X + T::LDS_X;
-#pragma unroll
-    for (int tap = 0; tap < 9; ++tap) {
+    float fa[2][T::NB], fb[2][T::MB];
+    auto frag = [&](int step, int slot) {
+      const int tap = step / (T::CK / 4), cg = step - tap * (T::CK / 4);
       const int toff = (tap / 3) * T::HW + (tap % 3);
 #pragma unroll
-      for (int cg = 0; cg < T::CK / 4; ++cg) {
-        float a[T::NB], b[T::MB];
+      for (int nb = 0; nb < T::NB; ++nb)
+        fa[slot][nb] = Wl[(tap * T::CK + cg * 4 + kq) * T::BN_P + wn * T::WN + nb * 16 + lr];
 #pragma unroll
-        for (int nb = 0; nb < T::NB; ++nb)
-          a[nb] = Wl[(tap * T::CK + cg * 4 + kq) * T::BN_P + wn * T::WN + nb * 16 + lr];
+      for (int mb = 0; mb < T::MB; ++mb)
+        fb[slot][mb] = X[(cg * 4 + kq) * T::PLANE_P + pix_off[mb] + toff];
+    };
+    frag(0, 0);
+#pragma unroll
+    for (int s = 0; s < T::NSTEP; ++s) {
+      if (s + 1 < T::NSTEP) frag(s + 1, (s + 1) & 1);
+#pragma unroll
+      for (int nb = 0; nb < T::NB; ++nb)
 #pragma unroll
         for (int mb = 0; mb < T::MB; ++mb)
-          b[mb] = X[(cg * 4 + kq) * T::PLANE_P + pix_off[mb] + toff];
-#pragma unroll
-        for (int nb = 0; nb < T::NB; ++nb)
-#pragma unroll
-          for (int mb = 0; mb < T::MB; ++mb)
-            acc[nb][mb] = mfma16x16x4(a[nb], b[mb], acc[nb][mb]);
-      }
+          acc[nb][mb] = mfma16x16x4(fa[s & 1][nb], fb[s & 1][mb], acc[nb][mb]);
     }
-    if (more) lstore(buf ^ 1);
+  };
+
+  const int nk = kc1 - kc0;
+  if (nk > 0) {
+    gload(kc0);
+    lstore(0);
+    if (nk > 1) gload(kc0 + 1);
+  }
+  __syncthreads();
+  for (int t = 0; t < nk; ++t) {
+    const int buf = t & 1;
+    if (t + 1 < nk) lstore(buf ^ 1);
+    if (t + 2 < nk) gload(kc0 + t + 2);
+    compute(buf);
     __syncthreads();
   }
 
-  // ---- epilogue ----
-  const size_t split_off = partial ? (size_t)blockIdx.z * N * Cout * HWs : 0;
+  // ---- epilogue: acc[nb][mb] lane holds channel co0 + wn*WN + nb*16 + 4*kq + i
+  // of pixel wm*WM + mb*16 + lr ----
+  const size_t total = (size_t)a.N * a.Cout * HWs;
+  auto for_each_out = [&](auto&& fn) {
 #pragma unroll
-  for (int mb = 0; mb < T::MB; ++mb) {
-    int p = wm * T::WM + mb * 16 + lr;
-    int img = p / (T::TH * T::TW), r = p - img * (T::TH * T::TW);
-    int yy = r / T::TW, xx = r - yy * T::TW;
-    int n = n0 + img, h = h0 + yy, w = w0 + xx;
-    if (n >= N || h >= H || w >= W) continue;
+    for (int mb = 0; mb < T::MB; ++mb) {
+      int p = wm * T::WM + mb * 16 + lr;
+      int img = p / (T::TH * T::TW), r = p - img * (T::TH * T::TW);
+      int yy = r / T::TW, xx = r - yy * T::TW;
+      int n = n0 + img, h = h0 + yy, w = w0 + xx;
+      if (n >= a.N || h >= a.H || w >= a.W) continue;
 #pragma unroll
-    for (int nb = 0; nb < T::NB; ++nb)
+      for (int nb = 0; nb < T::NB; ++nb)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        int co = co0 + wn * T::WN + nb * 16 + kq * 4 + i;
-        if (co >= Cout) continue;
-        size_t off = ((size_t)n * Cout + co) * HWs + (size_t)h * W + w;
-        float v = acc[nb][mb][i];
-        if (partial) {
-          out[split_off + off] = v;
-        } else {
-          if (bias) v += bias[co];
-          if (relu && !(v > 0.f)) v = 0.f;
-          if (mask && !(mask[off] > 0.f)) v = 0.f;
-          out[off] = v;
+        for (int i = 0; i < 4; ++i) {
+          int co = co0 + wn * T::WN + nb * 16 + kq * 4 + i;
+          if (co >= a.Cout) continue;
+          fn(acc[nb][mb][i], co, ((size_t)n * a.Cout + co) * HWs + (size_t)h * a.W + w);
+        }
+    }
+  };
+  if (a.splits == 1) {
+    for_each_out([&](float v, int co, size_t off) { a.out[off] = conv_epilogue(a, v, co, off); });
+    return;
+  }
+  float* mine = a.part + (size_t)blockIdx.z * total;
+  for_each_out([&](float v, int, size_t off) { mine[off] = v; });
+}
+
+// ------------------------------------------------------ small whole images --
+template <int H_, int W_, int G_>
+struct SmallTile {
+  static constexpr int H = H_, W = W_, G = G_;
+  static constexpr int P = H * W;                 // positions per image
+  static constexpr int IMGS = 16 * G;             // images per tile
+  static constexpr int BM = IMGS * P;             // pixels per tile
+  static constexpr int CK = 8, BN = 64, BN_P = 80;
+  static constexpr int PLANE = P * IMGS;          // [position][image] per channel
+  static constexpr int PLANE_P = (PLANE + 63) / 64 * 64 + 16;
+  static constexpr int LDS_X = CK * PLANE_P;
+  static constexpr int LDS_W = 9 * CK * BN_P;
+  static constexpr int LDS_BUF = LDS_X + LDS_W;
+  static_assert(P % 4 == 0, "image planes are loaded as float4");
+  static constexpr int X_F4 = CK * IMGS * P / 4;  // float4 per chunk
+  static constexpr int X_PT = (X_F4 + 255) / 256;
+  static constexpr int WTS = 9 * CK * BN;
+  static constexpr int WTS_PT = (WTS + 255) / 256;
+  static constexpr int MB = BM / 16;              // column blocks: (position, image group)
+  static constexpr int OUT_IMG_STRIDE = BN * P + 4;
+  static constexpr int LDS_OUT = IMGS * OUT_IMG_STRIDE;
+  static constexpr int LDS_FLOATS = 2 * LDS_BUF > LDS_OUT ? 2 * LDS_BUF : LDS_OUT;
+  static constexpr size_t LDS_BYTES = LDS_FLOATS * sizeof(float);
+  static_assert(LDS_BYTES <= 80 * 1024, "two blocks must fit in the 160 KB of LDS");
+  // Source position of tap (r,s) at position pos, or -1 if it is padding.
+  __host__ __device__ static constexpr int src(int pos, int tap) {
+    return (pos / W + tap / 3 - 1 >= 0 && pos / W + tap / 3 - 1 < H &&
+            pos % W + tap % 3 - 1 >= 0 && pos % W + tap % 3 - 1 < W)
+               ? (pos / W + tap / 3 - 1) * W + (pos % W + tap % 3 - 1)
+               : -1;
+  }
+};
+
+template <class T, bool DGRAD>
+__global__ __launch_bounds__(256, 2) void conv3x3_small_f32(ConvArgs a) {
+  extern __shared__ float lds[];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int kq = lane >> 4, lr = lane & 15;
+  const int n0 = blockIdx.x * T::IMGS;
+  const int co0 = blockIdx.y * T::BN;
+  const int nchunks = cdiv(a.Cin, T::CK);
+  const int kc0 = blockIdx.z * a.chunks_per_split;
+  const int kc1 = min(nchunks, kc0 + a.chunks_per_split);
+
+  // Image planes: float4 q of the chunk = (image, channel, quarter), quarter
+  // fastest: neighbouring threads read consecutive 16-byte pieces of one
+  // image's channel planes, which are contiguous in NCHW (fully coalesced).
+  int x_off[T::X_PT], x_c[T::X_PT], x_loff[T::X_PT];
+#pragma unroll
+  for (int i = 0; i < T::X_PT; ++i) {
+    int q = tid + i * 256;
+    bool live = q < T::X_F4;
+    int quarter = q % (T::P / 4), rest = q / (T::P / 4);
+    int c = rest % T::CK, img = rest / T::CK;
+    int n = n0 + img;
+    x_off[i] = (live && n < a.N) ? n * a.Cin * T::P + quarter * 4 : -1;   // + ci * P
+    x_c[i] = c;
+    x_loff[i] = live ? c * T::PLANE_P + quarter * 4 * T::IMGS + img : -1;
+  }
+  int w_off[T::WTS_PT], w_loff[T::WTS_PT], w_ci[T::WTS_PT];
+#pragma unroll
+  for (int i = 0; i < T::WTS_PT; ++i) {
+    int e = tid + i * 256;
+    filter_plan<DGRAD, T::CK, T::BN, T::BN_P>(e, co0, a.Cin, a.Cout, w_off[i], w_loff[i], w_ci[i]);
+    if (e >= T::WTS) { w_off[i] = -1; w_loff[i] = -1; }
+  }
+
+  f4 acc[T::MB];
+#pragma unroll
+  for (int j = 0; j < T::MB; ++j) acc[j] = f4{0.f, 0.f, 0.f, 0.f};
+
+  f4 rx[T::X_PT];
+  float rw[T::WTS_PT];
+  auto gload = [&](int kc) {
+    const int cbase = kc * T::CK;
+#pragma unroll
+    for (int i = 0; i < T::X_PT; ++i) {
+      const int ci = cbase + x_c[i];
+      const bool ok = x_off[i] >= 0 && ci < a.Cin;
+      const f4 v = *reinterpret_cast<const f4*>(a.in + (ok ? x_off[i] + ci * T::P : 0));
+      rx[i] = ok ? v : f4{0.f, 0.f, 0.f, 0.f};
+    }
+#pragma unroll
+    for (int i = 0; i < T::WTS_PT; ++i) rw[i] = filter_load<DGRAD>(a, w_off[i], w_ci[i], cbase);
+  };
+  auto lstore = [&](int buf) {
+    float* X = lds + buf * T::LDS_BUF;
+    float* Wl = X + T::LDS_X;
+#pragma unroll
+    for (int i = 0; i < T::X_PT; ++i)
+      if (x_loff[i] >= 0) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) X[x_loff[i] + j * T::IMGS] = rx[i][j];
+      }
+#pragma unroll
+    for (int i = 0; i < T::WTS_PT; ++i)
+      if (w_loff[i] >= 0) Wl[w_loff[i]] = rw[i];
+  };
+  auto compute = [&](int buf) {
+    const float* X = lds + buf * T::LDS_BUF;
+    const float* Wl = X + T::LDS_X;
+#pragma unroll
+    for (int tap = 0; tap < 9; ++tap)
+#pragma unroll
+      for (int cg = 0; cg < T::CK / 4; ++cg) {
+        const float fa = Wl[(tap * T::CK + cg * 4 + kq) * T::BN_P + wave * 16 + lr];
+#pragma unroll
+        for (int mb = 0; mb < T::MB; ++mb) {
+          const int pos = mb / T::G, g = mb % T::G;
+          const int sp = T::src(pos, tap);
+          if (sp < 0) continue;                       // padding: resolved at compile time
+          const float fb = X[(cg * 4 + kq) * T::PLANE_P + sp * T::IMGS + g * 16 + lr];
+          acc[mb] = mfma16x16x4(fa, fb, acc[mb]);
         }
       }
+  };
+
+  const int nk = kc1 - kc0;
+  if (nk > 0) {
+    gload(kc0);
+    lstore(0);
+    if (nk > 1) gload(kc0 + 1);
   }
+  __syncthreads();
+  for (int t = 0; t < nk; ++t) {
+    const int buf = t & 1;
+    if (t + 1 < nk) lstore(buf ^ 1);
+    if (t + 2 < nk) gload(kc0 + t + 2);
+    compute(buf);
+    __syncthreads();
+  }
+
+  // Stage the tile as [image][channel][position] so rows of the output go
+  // out as float4 stores.  acc[mb] lane holds channel wave*16 + 4*kq + i of
+  // image g*16 + lr at position pos (mb = pos*G + g).
+#pragma unroll
+  for (int mb = 0; mb < T::MB; ++mb) {
+    const int pos = mb / T::G, g = mb % T::G;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      lds[(g * 16 + lr) * T::OUT_IMG_STRIDE + (wave * 16 + kq * 4 + i) * T::P + pos] = acc[mb][i];
+  }
+  __syncthreads();
+  // The tile's output: for each image, channels [co0, co0+BN) x P positions
+  // are contiguous in NCHW.  float4 q -> (image, channel, quarter).
+  constexpr int OUT_F4 = T::IMGS * T::BN * T::P / 4;
+  const size_t total = (size_t)a.N * a.Cout * T::P;
+  auto for_each_out4 = [&](auto&& fn) {
+    for (int q = tid; q < OUT_F4; q += 256) {
+      int quarter = q % (T::P / 4), rest = q / (T::P / 4);
+      int cl = rest % T::BN, img = rest / T::BN;
+      int n = n0 + img, co = co0 + cl;
+      if (n >= a.N || co >= a.Cout) continue;
+      const float* s = lds + img * T::OUT_IMG_STRIDE + cl * T::P + quarter * 4;
+      f4 v = {s[0], s[1], s[2], s[3]};
+      fn(v, co, ((size_t)n * a.Cout + co) * T::P + quarter * 4);
+    }
+  };
+  auto epi4 = [&](f4 v, int co, size_t off) {
+    f4 m = {1.f, 1.f, 1.f, 1.f};
+    if (a.mask) m = *reinterpret_cast<const f4*>(a.mask + off);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      float x = v[j];
+      if (a.bias) x += a.bias[co];
+      if (a.relu && !(x > 0.f)) x = 0.f;
+      if (a.mask && !(m[j] > 0.f)) x = 0.f;
+      v[j] = x;
+    }
+    *reinterpret_cast<f4*>(a.out + off) = v;
+  };
+  if (a.splits == 1) {
+    for_each_out4(epi4);
+    return;
+  }
+  float* mine = a.part + (size_t)blockIdx.z * total;
+  for_each_out4([&](f4 v, int, size_t off) { *reinterpret_cast<f4*>(mine + off) = v; });
 }
 
 // Sum of the split partials in a fixed order, then the epilogue.
 __global__ __launch_bounds__(256) void conv_splitk_reduce(
-    const float* __restrict__ part, int splits, size_t total, int Cout, size_t HWs,
+    const float* __restrict__ part, int splits, size_t total, int Cout, int HWs,
     const float* __restrict__ bias, int relu, const float* __restrict__ mask,
     float* __restrict__ out) {
   __shared__ float lds[256];
@@ -257,7 +481,8 @@ __global__ __launch_bounds__(256) void conv_splitk_reduce(
 // ---------------------------------------------------------------- host --
 struct IgemmPlan {
   int tile;          // index into the tile table
-  int tiles_w, tiles_h, tiles_n, co_tiles;
+  int grid_x, co_tiles;
+  int tiles_w, tiles_h;
   int nchunks, cps, splits;
   size_t ws_bytes;
 };
@@ -269,80 +494,90 @@ using TileW4 = ConvTile<4, 4, 8, 8, 64>;
 using TileW2 = ConvTile<2, 2, 32, 8, 64>;
 using TileW32c4 = ConvTile<4, 32, 1, 4, 64>;
 using TileW32n16 = ConvTile<4, 32, 1, 8, 16>;
+using Small2 = SmallTile<2, 2, 2>;
+using Small4 = SmallTile<4, 4, 1>;
 
-static void tile_dims(int t, int& th, int& tw, int& imgs, int& ck, int& bn) {
-  switch (t) {
-    case 0: th = 4; tw = 32; imgs = 1; ck = 8; break;
-    case 1: th = 8; tw = 16; imgs = 1; ck = 8; break;
-    case 2: th = 8; tw = 8; imgs = 2; ck = 8; break;
-    case 3: th = 4; tw = 4; imgs = 8; ck = 8; break;
-    case 4: th = 2; tw = 2; imgs = 32; ck = 8; break;
-    case 5: th = 4; tw = 32; imgs = 1; ck = 4; break;
-    default: th = 4; tw = 32; imgs = 1; ck = 8; bn = 16; return;
-  }
-  bn = 64;
-}
+static const char* kTileNames[] = {
+    "sb::conv3x3_igemm_f32<sb::ConvTile<4, 32, 1, 8, 64>, %s>",
+    "sb::conv3x3_igemm_f32<sb::ConvTile<8, 16, 1, 8, 64>, %s>",
+    "sb::conv3x3_igemm_f32<sb::ConvTile<8, 8, 2, 8, 64>, %s>",
+    "sb::conv3x3_igemm_f32<sb::ConvTile<4, 4, 8, 8, 64>, %s>",
+    "sb::conv3x3_igemm_f32<sb::ConvTile<2, 2, 32, 8, 64>, %s>",
+    "sb::conv3x3_igemm_f32<sb::ConvTile<4, 32, 1, 4, 64>, %s>",
+    "sb::conv3x3_igemm_f32<sb::ConvTile<4, 32, 1, 8, 16>, %s>",
+    "sb::conv3x3_small_f32<sb::SmallTile<2, 2, 2>, %s>",
+    "sb::conv3x3_small_f32<sb::SmallTile<4, 4, 1>, %s>",
+};
 
-static IgemmPlan igemm_plan(int N, int Cin, int H, int W, int Cout) {
+// allow_small: the whole-image kernel moves float4s, so it needs 16-byte
+// aligned tensors.
+static IgemmPlan igemm_plan(int N, int Cin, int H, int W, int Cout, bool allow_small = true) {
   IgemmPlan p{};
-  if (Cout <= 16 && Cin > 4 && W >= 32) p.tile = 6;
-  else if (Cin <= 4 && W >= 32) p.tile = 5;
-  else if (W >= 32) p.tile = 0;
-  else if (W >= 16) p.tile = 1;
-  else if (W >= 8) p.tile = 2;
-  else if (W >= 4) p.tile = 3;
-  else p.tile = 4;
-  int th, tw, imgs, ck, bn;
-  tile_dims(p.tile, th, tw, imgs, ck, bn);
+  int th = 4, tw = 32, imgs = 1, ck = 8, bn = 64;
+  if (allow_small && H == 2 && W == 2 && Cin > 4) { p.tile = 7; th = 2; tw = 2; imgs = 32; }
+  else if (allow_small && H == 4 && W == 4 && Cin > 4) { p.tile = 8; th = 4; tw = 4; imgs = 16; }
+  else if (Cout <= 16 && Cin > 4 && W >= 32) { p.tile = 6; bn = 16; }
+  else if (Cin <= 4 && W >= 32) { p.tile = 5; ck = 4; }
+  else if (W >= 32) { p.tile = 0; }
+  else if (W >= 16) { p.tile = 1; th = 8; tw = 16; }
+  else if (W >= 8) { p.tile = 2; th = 8; tw = 8; imgs = 2; }
+  else if (W >= 4) { p.tile = 3; th = 4; tw = 4; imgs = 8; }
+  else { p.tile = 4; th = 2; tw = 2; imgs = 32; }
   p.tiles_w = cdiv(W, tw);
   p.tiles_h = cdiv(H, th);
-  p.tiles_n = cdiv(N, imgs);
+  p.grid_x = p.tiles_w * p.tiles_h * cdiv(N, imgs);
   p.co_tiles = cdiv(Cout, bn);
   p.nchunks = cdiv(Cin, ck);
-  long blocks = (long)p.tiles_w * p.tiles_h * p.tiles_n * p.co_tiles;
-  const long target = 512;  // two resident blocks on each of 256 CUs
+  long blocks = (long)p.grid_x * p.co_tiles;
+  // About two resident blocks on each of the 256 CUs; at most 8 splits, and
+  // at least two chunks per split.
+  const long target = 512;
   int splits = 1;
-  if (blocks < target) splits = (int)std::min<long>(p.nchunks, cdiv((int)target, (int)blocks));
+  if (blocks < target)
+    splits = (int)std::min<long>(std::min<long>(8, std::max(1, p.nchunks / 2)),
+                                 cdiv((int)target, (int)blocks));
   p.cps = cdiv(p.nchunks, splits);
   p.splits = cdiv(p.nchunks, p.cps);
   p.ws_bytes = p.splits > 1 ? (size_t)p.splits * N * Cout * H * W * sizeof(float) : 0;
   return p;
 }
 
-template <class T, bool DGRAD>
-static void igemm_launch(const IgemmPlan& p, const float* in, const float* wt,
-                         const float* bias, const float* mask, float* out, float* ws,
-                         int N, int Cin, int H, int W, int Cout, int relu, hipStream_t st) {
+template <class T, bool DGRAD, bool SMALL>
+static void igemm_launch(const IgemmPlan& p, const ConvArgs& a, hipStream_t st) {
   static bool attr_set = false;
+  const void* fn;
+  if constexpr (SMALL) fn = (const void*)conv3x3_small_f32<T, DGRAD>;
+  else fn = (const void*)conv3x3_igemm_f32<T, DGRAD>;
   if (!attr_set) {
-    hipFuncSetAttribute((const void*)conv3x3_igemm_f32<T, DGRAD>,
-                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)T::LDS_BYTES);
+    hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)T::LDS_BYTES);
     attr_set = true;
   }
-  dim3 grid(p.tiles_w * p.tiles_h * p.tiles_n, p.co_tiles, p.splits);
-  const bool part = p.splits > 1;
-  conv3x3_igemm_f32<T, DGRAD><<<grid, 256, T::LDS_BYTES, st>>>(
-      in, wt, part ? nullptr : bias, part ? nullptr : mask, part ? ws : out, N, Cin, H, W,
-      Cout, p.tiles_w, p.tiles_h, p.cps, part ? 0 : relu, part ? 1 : 0);
-  if (part) {
-    size_t total = (size_t)N * Cout * H * W;
+  dim3 grid(p.grid_x, p.co_tiles, p.splits);
+  ConvArgs k = a;
+  if (p.splits > 1) { k.bias = nullptr; k.mask = nullptr; k.relu = 0; }
+  if constexpr (SMALL)
+    conv3x3_small_f32<T, DGRAD><<<grid, 256, T::LDS_BYTES, st>>>(k);
+  else
+    conv3x3_igemm_f32<T, DGRAD><<<grid, 256, T::LDS_BYTES, st>>>(k);
+  if (p.splits > 1) {
+    size_t total = (size_t)a.N * a.Cout * a.H * a.W;
     conv_splitk_reduce<<<(unsigned)((total + 63) / 64), 256, 0, st>>>(
-        ws, p.splits, total, Cout, (size_t)H * W, bias, relu, mask, out);
+        a.part, p.splits, total, a.Cout, a.H * a.W, a.bias, a.relu, a.mask, a.out);
   }
 }
 
 template <bool DGRAD>
-static void igemm_dispatch(const IgemmPlan& p, const float* in, const float* wt,
-                           const float* bias, const float* mask, float* out, float* ws,
-                           int N, int Cin, int H, int W, int Cout, int relu, hipStream_t st) {
+static void igemm_dispatch(const IgemmPlan& p, const ConvArgs& a, hipStream_t st) {
   switch (p.tile) {
-    case 0: igemm_launch<TileW32, DGRAD>(p, in, wt, bias, mask, out, ws, N, Cin, H, W, Cout, relu, st); break;
-    case 1: igemm_launch<TileW16, DGRAD>(p, in, wt, bias, mask, out, ws, N, Cin, H, W, Cout, relu, st); break;
-    case 2: igemm_launch<TileW8, DGRAD>(p, in, wt, bias, mask, out, ws, N, Cin, H, W, Cout, relu, st); break;
-    case 3: igemm_launch<TileW4, DGRAD>(p, in, wt, bias, mask, out, ws, N, Cin, H, W, Cout, relu, st); break;
-    case 4: igemm_launch<TileW2, DGRAD>(p, in, wt, bias, mask, out, ws, N, Cin, H, W, Cout, relu, st); break;
-    case 5: igemm_launch<TileW32c4, DGRAD>(p, in, wt, bias, mask, out, ws, N, Cin, H, W, Cout, relu, st); break;
-    default: igemm_launch<TileW32n16, DGRAD>(p, in, wt, bias, mask, out, ws, N, Cin, H, W, Cout, relu, st); break;
+    case 0: igemm_launch<TileW32, DGRAD, false>(p, a, st); break;
+    case 1: igemm_launch<TileW16, DGRAD, false>(p, a, st); break;
+    case 2: igemm_launch<TileW8, DGRAD, false>(p, a, st); break;
+    case 3: igemm_launch<TileW4, DGRAD, false>(p, a, st); break;
+    case 4: igemm_launch<TileW2, DGRAD, false>(p, a, st); break;
+    case 5: igemm_launch<TileW32c4, DGRAD, false>(p, a, st); break;
+    case 6: igemm_launch<TileW32n16, DGRAD, false>(p, a, st); break;
+    case 7: igemm_launch<Small2, DGRAD, true>(p, a, st); break;
+    default: igemm_launch<Small4, DGRAD, true>(p, a, st); break;
   }
 }
 
@@ -352,30 +587,32 @@ static void igemm_dispatch(const IgemmPlan& p, const float* in, const float* wt,
 namespace sbh {
 
 size_t conv_igemm_ws(int N, int Cin, int H, int W, int Cout) {
-  return sb::igemm_plan(N, Cin, H, W, Cout).ws_bytes;
+  return std::max(sb::igemm_plan(N, Cin, H, W, Cout, true).ws_bytes,
+                  sb::igemm_plan(N, Cin, H, W, Cout, false).ws_bytes);
 }
 
 int conv_igemm_describe(bool dgrad, int N, int Cin, int H, int W, int Cout, char* buf,
                         size_t len) {
   sb::IgemmPlan p = sb::igemm_plan(N, Cin, H, W, Cout);
-  int th, tw, imgs, ck, bn;
-  sb::tile_dims(p.tile, th, tw, imgs, ck, bn);
-  return snprintf(buf, len,
-                  "sb::conv3x3_igemm_f32<sb::ConvTile<%d, %d, %d, %d, %d>, %s> grid=%dx%dx%d%s",
-                  th, tw, imgs, ck, bn, dgrad ? "true" : "false",
-                  p.tiles_w * p.tiles_h * p.tiles_n, p.co_tiles, p.splits,
-                  p.splits > 1 ? " +sb::conv_splitk_reduce" : "");
+  char name[160];
+  snprintf(name, sizeof(name), sb::kTileNames[p.tile], dgrad ? "true" : "false");
+  return snprintf(buf, len, "%s grid=%dx%dx%d", name, p.grid_x, p.co_tiles, p.splits);
 }
 
 sb_status conv_igemm_f32(bool dgrad, int N, int Cin, int H, int W, int Cout, const float* in,
                          const float* wt, const float* bias, const float* mask, float* out,
                          void* ws, size_t ws_bytes, int relu, hipStream_t st) {
-  sb::IgemmPlan p = sb::igemm_plan(N, Cin, H, W, Cout);
+  const bool aligned = (((uintptr_t)in | (uintptr_t)out | (uintptr_t)mask) & 15) == 0;
+  sb::IgemmPlan p = sb::igemm_plan(N, Cin, H, W, Cout, aligned);
   if (p.ws_bytes > 0 && (ws == nullptr || ws_bytes < p.ws_bytes)) return SB_ERR_WORKSPACE;
-  if (dgrad)
-    sb::igemm_dispatch<true>(p, in, wt, bias, mask, out, (float*)ws, N, Cin, H, W, Cout, relu, st);
-  else
-    sb::igemm_dispatch<false>(p, in, wt, bias, mask, out, (float*)ws, N, Cin, H, W, Cout, relu, st);
+  sb::ConvArgs a{};
+  a.in = in; a.wt = wt; a.bias = bias; a.mask = mask; a.out = out;
+  a.part = p.splits > 1 ? (float*)ws : nullptr;
+  a.N = N; a.Cin = Cin; a.H = H; a.W = W; a.Cout = Cout;
+  a.tiles_w = p.tiles_w; a.tiles_h = p.tiles_h;
+  a.chunks_per_split = p.cps; a.splits = p.splits; a.relu = relu;
+  if (dgrad) sb::igemm_dispatch<true>(p, a, st);
+  else sb::igemm_dispatch<false>(p, a, st);
   return launch_status();
 }
 

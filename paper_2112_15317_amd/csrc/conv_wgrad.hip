@@ -4,27 +4,34 @@
 //   db[k]       = sum_{n,h,w} dy[n,k,h,w]
 //
 // GEMM view: rows = output channels k, columns = (input channel c, tap),
-// reduction = every pixel of the batch.  A block owns 64 k and walks a
-// contiguous range of 64-pixel tiles (IMGS images x TH rows x TW cols).  Per
-// pixel tile it stages in LDS
-//   * dy: 64 k x 64 pixels, stored [pixel][k] so an MFMA operand read of 16
-//     consecutive k is bank-conflict free, and
-//   * the x halo: BC channels x IMGS x (TH+2) x (TW+2), stored [halo pixel][c],
-//     read once and shifted per tap.
-// Two column layouts:
-//   * wide (C >= 16): a block owns 16 channels x 9 taps; per 4-pixel step a
+// reduction = every pixel of the batch.  Blocks of the first column tile also
+// multiply dy against a column of ones, which yields the bias gradient in
+// the same pass.  Two kernels:
+//
+// conv3x3_wgrad_f32 (any shape).  A block owns 64 k and walks a contiguous
+// range of 64-pixel tiles (IMGS images x TH rows x TW cols).  Per pixel tile
+// it stages in LDS dy (64 k x 64 pixels, stored [pixel][k] so an operand
+// read of 16 consecutive k is conflict-free) and the x halo (BC channels x
+// IMGS x (TH+2) x (TW+2), stored [halo pixel][c], shifted per tap).  Column
+// layouts:
+//   * wide (C >= 8): a block owns 16 channels x 9 taps; per 4-pixel step a
 //     wave multiplies one dy fragment against 9 tap-shifted x fragments.
 //   * narrow (C <= 7, e.g. the RGB input layer): a block owns every (c, tap)
 //     pair, flattened into NCB blocks of 16 MFMA columns; each lane gathers
-//     its own (c, tap) from the halo, so only the padding of C*9 up to a
-//     multiple of 16 is wasted instead of 16 - C channels.
-// Blocks of the first column tile also multiply dy against a column of ones,
-// which yields the bias gradient in the same pass.
+//     its own (c, tap), so only C*9 rounded up to 16 is computed.
 //
-// The reduction dimension is long (up to N*H*W = 131072 here) while the
-// output is small, so pixel tiles are split over gridDim.z; each split writes
-// its partial sums to the workspace and splits_reduce adds the splits in a
-// fixed order.  No atomics: results are bitwise reproducible.
+// conv3x3_wgrad_small_f32 (whole images of 2x2 or 4x4 pixels).  The
+// reduction runs over 4 images at a time at one pixel position; for each
+// (position, tap) pair whose source lies inside the image (known at compile
+// time) one MFMA adds dy[., k, pos] x x[., c, src(pos, tap)] into tap's
+// accumulator.  Padded taps are never multiplied.  LDS holds dy as
+// [position][image][k] and x as [position][image][c], filled with float4
+// loads of whole image planes.
+//
+// The reduction dimension is long (up to N*H*W = 131072) while the output is
+// small, so the pixels are split over gridDim.z; each split writes its
+// partial sums to the workspace and splits_reduce adds the splits in a fixed
+// order.  No float atomics: results are bitwise reproducible.
 #include "sb_internal.hpp"
 
 #include <algorithm>
@@ -32,6 +39,66 @@
 
 namespace sb {
 
+struct WgArgs {
+  const float* x;        // [N][C][H][W]
+  const float* dy;       // [N][K][H][W]
+  float* dw;             // [K][C][3][3]
+  float* db;             // [K] or null
+  float* part;           // split partials: [splits][K*C*9] then [splits][K]
+  int N, C, H, W, K;
+  int tiles_w, tiles_h, ptiles, tiles_per_split, c_tiles, splits;
+};
+
+// Writes (or split-reduces) the block's 64 k x 16-column x NACC outputs.
+// `val(i, t)` is the lane's accumulator t, element i; `col(t)` the flattened
+// (c, tap) column of the lane in accumulator t, or -1.
+template <int NACC, class Val, class Col>
+__device__ __forceinline__ void wgrad_store(const WgArgs& a, int k_base, bool do_db,
+                                            const f4& accb, Val val, Col col) {
+  const int lane = threadIdx.x & 63, jq = lane >> 4, lr = lane & 15;
+  const size_t wsz = (size_t)a.K * a.C * 9;
+  auto each = [&](auto&& fn) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int k = k_base + 4 * jq + i;
+      if (k >= a.K) continue;
+#pragma unroll
+      for (int t = 0; t < NACC; ++t) {
+        const int j = col(t);
+        if (j >= 0) fn(val(i, t), (size_t)k * a.C * 9 + j);
+      }
+    }
+  };
+  auto each_db = [&](auto&& fn) {
+    if (!do_db || lr != 0) return;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int k = k_base + 4 * jq + i;
+      if (k < a.K) fn(accb[i], k);
+    }
+  };
+  if (a.splits == 1) {
+    each([&](float v, size_t o) { a.dw[o] = v; });
+    each_db([&](float v, int k) { a.db[k] = v; });
+    return;
+  }
+  float* pw = a.part + (size_t)blockIdx.z * wsz;
+  float* pb = a.part + (size_t)a.splits * wsz + (size_t)blockIdx.z * a.K;
+  each([&](float v, size_t o) { pw[o] = v; });
+  each_db([&](float v, int k) { pb[k] = v; });
+}
+
+// dst[i] = sum over the splits of part[s*total + i], in a fixed order.
+__global__ __launch_bounds__(256) void splits_reduce(const float* __restrict__ part, int splits,
+                                                     size_t total, float* __restrict__ dst) {
+  __shared__ float lds[256];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const size_t i = (size_t)blockIdx.x * 64 + lane;
+  float v = SplitSum{part, splits, total}(i, wave, lds, lane);
+  if (wave == 0 && i < total) dst[i] = v;
+}
+
+// ----------------------------------------------------------------- generic --
 template <int TH_, int TW_, int IMGS_, int NCB_>
 struct WgTile {
   static constexpr int TH = TH_, TW = TW_, IMGS = IMGS_;
@@ -63,34 +130,30 @@ __device__ __forceinline__ int wg_hoff(int p) {
 }
 
 template <class T>
-__global__ __launch_bounds__(256, 2) void conv3x3_wgrad_f32(
-    const float* __restrict__ x, const float* __restrict__ dy, float* __restrict__ dw,
-    float* __restrict__ db, int N, int C, int H, int W, int K, int tiles_w, int tiles_h,
-    int ptiles, int tiles_per_split, int c_tiles, int partial) {
+__global__ __launch_bounds__(256, 2) void conv3x3_wgrad_f32(WgArgs a) {
   extern __shared__ float lds[];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int jq = lane >> 4, lr = lane & 15;
-  const int ct = blockIdx.x % c_tiles, kt = blockIdx.x / c_tiles;
+  const int ct = blockIdx.x % a.c_tiles, kt = blockIdx.x / a.c_tiles;
   const int c0 = ct * T::BC, k0 = kt * T::BK;
-  const int pt0 = blockIdx.z * tiles_per_split;
-  const int pt1 = min(ptiles, pt0 + tiles_per_split);
-  const bool do_db = (db != nullptr) && ct == 0;
-  const size_t HWs = (size_t)H * W;
+  const int pt0 = blockIdx.z * a.tiles_per_split;
+  const int pt1 = min(a.ptiles, pt0 + a.tiles_per_split);
+  const bool do_db = (a.db != nullptr) && ct == 0;
+  const int HWs = a.H * a.W;
 
   // Lane offset of pixel (step base + jq) relative to the step base's halo offset.
   const int lane_hoff = wg_hoff<T>(jq);
 
   // Narrow layout: this lane's (c, tap) column in each column block.
-  int col_off[T::NARROW ? T::NCB : 1];
-  bool col_ok[T::NARROW ? T::NCB : 1];
-  if (T::NARROW) {
+  constexpr int NC = T::NARROW ? T::NCB : 1;
+  int col_off[NC];
+  bool col_ok[NC];
 #pragma unroll
-    for (int cb = 0; cb < (T::NARROW ? T::NCB : 1); ++cb) {
-      int j = cb * 16 + lr, c = j / 9, t = j - c * 9;
-      col_ok[cb] = j < C * 9;
-      col_off[cb] = col_ok[cb] ? ((t / 3) * T::HW + (t % 3)) * T::BC + c : 0;
-    }
+  for (int cb = 0; cb < NC; ++cb) {
+    int j = cb * 16 + lr, c = j / 9, t = j - c * 9;
+    col_ok[cb] = T::NARROW && j < a.C * 9;
+    col_off[cb] = col_ok[cb] ? ((t / 3) * T::HW + (t % 3)) * T::BC + c : 0;
   }
 
   f4 acc[T::NACC], accb = f4{0.f, 0.f, 0.f, 0.f};
@@ -99,36 +162,37 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_f32(
 
   float rdy[T::DY_PT], rx[T::X_PT];
 
-  auto tile_origin = [&](int pt, int& n0, int& h0, int& w0) {
-    int tx = pt % tiles_w, r = pt / tiles_w;
-    int ty = r % tiles_h, tn = r / tiles_h;
-    n0 = tn * T::IMGS; h0 = ty * T::TH; w0 = tx * T::TW;
-  };
-
   auto gload = [&](int pt) {
-    int n0, h0, w0;
-    tile_origin(pt, n0, h0, w0);
-    // dy: element e = (k-in-tile, pixel) with pixel fastest (coalesced rows).
+    int tx = pt % a.tiles_w, r0 = pt / a.tiles_w;
+    int ty = r0 % a.tiles_h, tn = r0 / a.tiles_h;
+    const int n0 = tn * T::IMGS, h0 = ty * T::TH, w0 = tx * T::TW;
+    // dy: element e = (pixel quad, k-in-tile, pixel within the quad).  A
+    // wave covers 16 k x 4 consecutive pixels: 16 rows of 16 B in global
+    // memory, and 64 distinct banks in the [pixel][k] LDS tile.
 #pragma unroll
     for (int i = 0; i < T::DY_PT; ++i) {
       int e = tid + i * 256;
-      int kk = e / T::BP, p = e - kk * T::BP;
+      int kk = (e >> 2) & (T::BK - 1), p = ((e >> 8) << 2) | (e & 3);
       int img = p / (T::TH * T::TW), r = p - img * (T::TH * T::TW);
       int yy = r / T::TW, xx = r - yy * T::TW;
       int n = n0 + img, h = h0 + yy, w = w0 + xx, k = k0 + kk;
-      bool ok = n < N && h < H && w < W && k < K;
-      rdy[i] = ok ? dy[((size_t)n * K + k) * HWs + (size_t)h * W + w] : 0.f;
+      bool ok = n < a.N && h < a.H && w < a.W && k < a.K;
+      float v = a.dy[ok ? (n * a.K + k) * HWs + h * a.W + w : 0];
+      rdy[i] = ok ? v : 0.f;
     }
-    // x halo: element e = (c-in-tile, halo pixel) with halo pixel fastest.
+    // x halo: element e = (halo pixel, c-in-tile) with c fastest, for the
+    // same reason ([halo pixel][c] LDS tile).
 #pragma unroll
     for (int i = 0; i < T::X_PT; ++i) {
       int e = tid + i * 256;
-      int cc = e / T::PLANE, hp = e - cc * T::PLANE;
+      int hp = e / T::BC, cc = e - hp * T::BC;
       int img = hp / (T::HH * T::HW), r = hp - img * (T::HH * T::HW);
       int yy = r / T::HW, xx = r - yy * T::HW;
       int n = n0 + img, h = h0 + yy - 1, w = w0 + xx - 1, c = c0 + cc;
-      bool ok = e < T::BC * T::PLANE && n < N && h >= 0 && h < H && w >= 0 && w < W && c < C;
-      rx[i] = ok ? x[((size_t)n * C + c) * HWs + (size_t)h * W + w] : 0.f;
+      bool ok = e < T::BC * T::PLANE && n < a.N && h >= 0 && h < a.H && w >= 0 && w < a.W &&
+                c < a.C;
+      float v = a.x[ok ? (n * a.C + c) * HWs + h * a.W + w : 0];
+      rx[i] = ok ? v : 0.f;
     }
   };
   auto lstore = [&](int buf) {
@@ -137,135 +201,263 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_f32(
 #pragma unroll
     for (int i = 0; i < T::DY_PT; ++i) {
       int e = tid + i * 256;
-      int kk = e / T::BP, p = e - kk * T::BP;
+      int kk = (e >> 2) & (T::BK - 1), p = ((e >> 8) << 2) | (e & 3);
       Dl[p * T::DY_STRIDE + kk] = rdy[i];
     }
 #pragma unroll
     for (int i = 0; i < T::X_PT; ++i) {
       int e = tid + i * 256;
-      if (e < T::BC * T::PLANE) {
-        int cc = e / T::PLANE, hp = e - cc * T::PLANE;
-        Xl[hp * T::BC + cc] = rx[i];
-      }
+      if (e < T::BC * T::PLANE) Xl[e] = rx[i];     // = [halo pixel][c]
     }
   };
-
-  if (pt0 < pt1) {
-    gload(pt0);
-    lstore(0);
-  }
-  __syncthreads();
-
-  for (int pt = pt0; pt < pt1; ++pt) {
-    const int buf = (pt - pt0) & 1;
-    const bool more = pt + 1 < pt1;
-    if (more) gload(pt + 1);
+  auto compute = [&](int buf) {
     const float* Dl = lds + buf * T::LDS_BUF;
     const float* Xl = Dl + T::LDS_DY;
 #pragma unroll
     for (int st = 0; st < T::BP / 4; ++st) {
       const int pbase = st * 4;
       const int hbase = wg_hoff<T>(pbase);          // compile-time after unrolling
-      float a = Dl[(pbase + jq) * T::DY_STRIDE + wave * 16 + lr];
+      float av = Dl[(pbase + jq) * T::DY_STRIDE + wave * 16 + lr];
       const float* Xp = Xl + (hbase + lane_hoff) * T::BC;
       if (T::NARROW) {
 #pragma unroll
         for (int cb = 0; cb < T::NACC; ++cb) {
-          float b = Xp[col_off[cb % (T::NARROW ? T::NCB : 1)]];
-          b = col_ok[cb % (T::NARROW ? T::NCB : 1)] ? b : 0.f;
-          acc[cb] = mfma16x16x4(a, b, acc[cb]);
+          float b = Xp[col_off[cb % NC]];
+          b = col_ok[cb % NC] ? b : 0.f;
+          acc[cb] = mfma16x16x4(av, b, acc[cb]);
         }
       } else {
 #pragma unroll
         for (int t = 0; t < 9; ++t) {
           const int toff = (t / 3) * T::HW + (t % 3);
           float b = Xp[toff * T::BC + lr];
-          acc[t] = mfma16x16x4(a, b, acc[t]);
+          acc[t] = mfma16x16x4(av, b, acc[t]);
         }
       }
-      if (do_db) accb = mfma16x16x4(a, 1.0f, accb);
+      if (do_db) accb = mfma16x16x4(av, 1.0f, accb);
     }
-    if (more) lstore(buf ^ 1);
+  };
+
+  const int nt = pt1 - pt0;
+  if (nt > 0) {
+    gload(pt0);
+    lstore(0);
+    if (nt > 1) gload(pt0 + 1);
+  }
+  __syncthreads();
+  for (int t = 0; t < nt; ++t) {
+    const int buf = t & 1;
+    if (t + 1 < nt) lstore(buf ^ 1);
+    if (t + 2 < nt) gload(pt0 + t + 2);
+    compute(buf);
     __syncthreads();
   }
 
   // acc[t] lane holds rows k = k0 + wave*16 + 4*jq + i and column lr of its block.
-  const size_t wsz = (size_t)K * C * 9;
-  float* dst = dw + (partial ? (size_t)blockIdx.z * wsz : 0);
+  wgrad_store<T::NACC>(
+      a, k0 + wave * 16, do_db, accb, [&](int i, int t) { return acc[t][i]; },
+      [&](int t) -> int {
+        if (T::NARROW) {
+          int j = t * 16 + lr;
+          return j < a.C * 9 ? j : -1;
+        }
+        int c = c0 + lr;
+        return c < a.C ? c * 9 + t : -1;
+      });
+}
+
+// ------------------------------------------------------ small whole images --
+template <int H_, int W_, int IW_>
+struct WgSmall {
+  static constexpr int H = H_, W = W_, P = H * W, IW = IW_;   // IW images per LDS fill
+  static constexpr int BK = 64, BC = 16;
+  static constexpr int DZ_STRIDE = BK + 16;                    // per (position, image)
+  static constexpr int LDS_DZ = P * IW * DZ_STRIDE;
+  static constexpr int LDS_X = P * IW * BC;
+  static constexpr int LDS_BUF = LDS_DZ + LDS_X;
+  static constexpr size_t LDS_BYTES = 2 * LDS_BUF * sizeof(float);
+  static_assert(P % 4 == 0 && IW % 4 == 0, "float4 planes, 4-image MFMA steps");
+  static constexpr int DZ_F4 = IW * BK * P / 4;
+  static constexpr int X_F4 = IW * BC * P / 4;
+  static constexpr int DZ_PT = (DZ_F4 + 255) / 256;
+  static constexpr int X_PT = (X_F4 + 255) / 256;
+  __host__ __device__ static constexpr int src(int pos, int tap) {
+    return (pos / W + tap / 3 - 1 >= 0 && pos / W + tap / 3 - 1 < H &&
+            pos % W + tap % 3 - 1 >= 0 && pos % W + tap % 3 - 1 < W)
+               ? (pos / W + tap / 3 - 1) * W + (pos % W + tap % 3 - 1)
+               : -1;
+  }
+};
+
+template <class T>
+__global__ __launch_bounds__(256, 2) void conv3x3_wgrad_small_f32(WgArgs a) {
+  extern __shared__ float lds[];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int jq = lane >> 4, lr = lane & 15;
+  const int ct = blockIdx.x % a.c_tiles, kt = blockIdx.x / a.c_tiles;
+  const int c0 = ct * T::BC, k0 = kt * T::BK;
+  const int ch0 = blockIdx.z * a.tiles_per_split;              // image chunks of IW
+  const int ch1 = min(a.ptiles, ch0 + a.tiles_per_split);
+  const bool do_db = (a.db != nullptr) && ct == 0;
+
+  // float4 q of a chunk = (image, channel, quarter); quarter fastest.
+  int dz_off[T::DZ_PT], dz_loff[T::DZ_PT];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    int k = k0 + wave * 16 + 4 * jq + i;
-    if (k >= K) continue;
-    if (T::NARROW) {
+  for (int i = 0; i < T::DZ_PT; ++i) {
+    int q = tid + i * 256;
+    int kk = q % T::BK, rest = q / T::BK;          // k fastest: conflict-free LDS rows
+    int quarter = rest % (T::P / 4), img = rest / (T::P / 4);
+    bool ok = q < T::DZ_F4 && k0 + kk < a.K;
+    dz_off[i] = ok ? (img * a.K + k0 + kk) * T::P + quarter * 4 : -1;   // + chunk*IW*K*P
+    dz_loff[i] = q < T::DZ_F4 ? ((quarter * 4) * T::IW + img) * T::DZ_STRIDE + kk : -1;
+  }
+  int x_off[T::X_PT], x_loff[T::X_PT];
 #pragma unroll
-      for (int cb = 0; cb < T::NACC; ++cb) {
-        int j = cb * 16 + lr;                       // flattened (c, tap)
-        if (j < C * 9) dst[(size_t)k * C * 9 + j] = acc[cb][i];
+  for (int i = 0; i < T::X_PT; ++i) {
+    int q = tid + i * 256;
+    int cc = q % T::BC, rest = q / T::BC;          // c, then image: consecutive LDS rows
+    int img = rest % T::IW, quarter = rest / T::IW;
+    bool ok = q < T::X_F4 && c0 + cc < a.C;
+    x_off[i] = ok ? (img * a.C + c0 + cc) * T::P + quarter * 4 : -1;    // + chunk*IW*C*P
+    x_loff[i] = q < T::X_F4 ? ((quarter * 4) * T::IW + img) * T::BC + cc : -1;
+  }
+
+  f4 acc[9], accb = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int t = 0; t < 9; ++t) acc[t] = f4{0.f, 0.f, 0.f, 0.f};
+
+  f4 rdz[T::DZ_PT], rx[T::X_PT];
+  const f4 zero4 = {0.f, 0.f, 0.f, 0.f};
+  auto gload = [&](int ch) {
+    const int nb = ch * T::IW;                        // first image of the chunk
+#pragma unroll
+    for (int i = 0; i < T::DZ_PT; ++i) {
+      const int img = (tid + i * 256) / T::BK / (T::P / 4);
+      const bool ok = dz_off[i] >= 0 && nb + img < a.N;
+      const f4 v = *reinterpret_cast<const f4*>(a.dy + (ok ? dz_off[i] + nb * a.K * T::P : 0));
+      rdz[i] = ok ? v : zero4;
+    }
+#pragma unroll
+    for (int i = 0; i < T::X_PT; ++i) {
+      const int img = (tid + i * 256) / T::BC % T::IW;
+      const bool ok = x_off[i] >= 0 && nb + img < a.N;
+      const f4 v = *reinterpret_cast<const f4*>(a.x + (ok ? x_off[i] + nb * a.C * T::P : 0));
+      rx[i] = ok ? v : zero4;
+    }
+  };
+  auto lstore = [&](int buf) {
+    float* Dl = lds + buf * T::LDS_BUF;
+    float* Xl = Dl + T::LDS_DZ;
+#pragma unroll
+    for (int i = 0; i < T::DZ_PT; ++i)
+      if (dz_loff[i] >= 0) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) Dl[dz_loff[i] + j * T::IW * T::DZ_STRIDE] = rdz[i][j];
       }
-    } else {
-      int c = c0 + lr;
-      if (c >= C) continue;
 #pragma unroll
-      for (int t = 0; t < 9; ++t) dst[((size_t)k * C + c) * 9 + t] = acc[t][i];
-    }
-  }
-  if (do_db && lr == 0) {
-    float* dbd = db + (partial ? (size_t)blockIdx.z * K : 0);
+    for (int i = 0; i < T::X_PT; ++i)
+      if (x_loff[i] >= 0) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      int k = k0 + wave * 16 + 4 * jq + i;
-      if (k < K) dbd[k] = accb[i];
+        for (int j = 0; j < 4; ++j) Xl[x_loff[i] + j * T::IW * T::BC] = rx[i][j];
+      }
+  };
+  auto compute = [&](int buf) {
+    const float* Dl = lds + buf * T::LDS_BUF;
+    const float* Xl = Dl + T::LDS_DZ;
+#pragma unroll
+    for (int s = 0; s < T::IW / 4; ++s) {
+      float av[T::P], bv[T::P];
+#pragma unroll
+      for (int pos = 0; pos < T::P; ++pos) {
+        av[pos] = Dl[(pos * T::IW + 4 * s + jq) * T::DZ_STRIDE + wave * 16 + lr];
+        bv[pos] = Xl[(pos * T::IW + 4 * s + jq) * T::BC + lr];
+      }
+#pragma unroll
+      for (int pos = 0; pos < T::P; ++pos) {
+#pragma unroll
+        for (int t = 0; t < 9; ++t) {
+          const int sp = T::src(pos, t);
+          if (sp >= 0) acc[t] = mfma16x16x4(av[pos], bv[sp], acc[t]);
+        }
+        if (do_db) accb = mfma16x16x4(av[pos], 1.0f, accb);
+      }
     }
+  };
+
+  const int nt = ch1 - ch0;
+  if (nt > 0) {
+    gload(ch0);
+    lstore(0);
+    if (nt > 1) gload(ch0 + 1);
   }
+  __syncthreads();
+  for (int t = 0; t < nt; ++t) {
+    const int buf = t & 1;
+    if (t + 1 < nt) lstore(buf ^ 1);
+    if (t + 2 < nt) gload(ch0 + t + 2);
+    compute(buf);
+    __syncthreads();
+  }
+
+  wgrad_store<9>(
+      a, k0 + wave * 16, do_db, accb, [&](int i, int t) { return acc[t][i]; },
+      [&](int t) -> int {
+        int c = c0 + lr;
+        return c < a.C ? c * 9 + t : -1;
+      });
 }
 
-// dst[i] = sum over the splits of part[s*total + i], in a fixed order.
-__global__ __launch_bounds__(256) void splits_reduce(const float* __restrict__ part, int splits,
-                                                     size_t total, float* __restrict__ dst) {
-  __shared__ float lds[256];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const size_t i = (size_t)blockIdx.x * 64 + lane;
-  float v = SplitSum{part, splits, total}(i, wave, lds, lane);
-  if (wave == 0 && i < total) dst[i] = v;
-}
-
+// ---------------------------------------------------------------- host --
 struct WgPlan {
   int tile, tiles_w, tiles_h, ptiles, k_tiles, c_tiles, tps, splits;
   size_t ws_bytes;
 };
 
-// Wide layouts (16 channels x 9 taps per block), by image width.
 using WgW32 = WgTile<2, 32, 1, 0>;
 using WgW16 = WgTile<4, 16, 1, 0>;
 using WgW8 = WgTile<8, 8, 1, 0>;
 using WgW4 = WgTile<4, 4, 4, 0>;
 using WgW2 = WgTile<2, 2, 16, 0>;
-// Narrow layouts (all C <= 7 channels x 9 taps in NCB column blocks).
 using WgN32_2 = WgTile<2, 32, 1, 2>;   // C <= 3
 using WgN32_4 = WgTile<2, 32, 1, 4>;   // C <= 7
 using WgN4_2 = WgTile<4, 4, 4, 2>;
 using WgN4_4 = WgTile<4, 4, 4, 4>;
+using WgS2 = WgSmall<2, 2, 16>;
+using WgS4 = WgSmall<4, 4, 4>;
 
-static WgPlan wg_plan(int N, int C, int H, int W, int K) {
+static const char* kWgNames[] = {
+    "sb::conv3x3_wgrad_f32<sb::WgTile<2, 32, 1, 0> >", "sb::conv3x3_wgrad_f32<sb::WgTile<4, 16, 1, 0> >",
+    "sb::conv3x3_wgrad_f32<sb::WgTile<8, 8, 1, 0> >",  "sb::conv3x3_wgrad_f32<sb::WgTile<4, 4, 4, 0> >",
+    "sb::conv3x3_wgrad_f32<sb::WgTile<2, 2, 16, 0> >", "sb::conv3x3_wgrad_f32<sb::WgTile<2, 32, 1, 2> >",
+    "sb::conv3x3_wgrad_f32<sb::WgTile<2, 32, 1, 4> >", "sb::conv3x3_wgrad_f32<sb::WgTile<4, 4, 4, 2> >",
+    "sb::conv3x3_wgrad_f32<sb::WgTile<4, 4, 4, 4> >",
+    "sb::conv3x3_wgrad_small_f32<sb::WgSmall<2, 2, 16> >",
+    "sb::conv3x3_wgrad_small_f32<sb::WgSmall<4, 4, 4> >",
+};
+
+// allow_small: the whole-image kernel moves float4s (16-byte aligned tensors).
+static WgPlan wg_plan(int N, int C, int H, int W, int K, bool allow_small = true) {
   WgPlan p{};
-  int th, tw, imgs;
+  int th = 2, tw = 32, imgs = 1;
   const bool narrow = C <= 7;
   if (narrow) {
     // 32-wide rows for wide images, 4x4 x 4-image tiles otherwise.
-    if (W >= 32) { th = 2; tw = 32; imgs = 1; p.tile = C <= 3 ? 5 : 6; }
+    if (W >= 32) { p.tile = C <= 3 ? 5 : 6; }
     else { th = 4; tw = 4; imgs = 4; p.tile = C <= 3 ? 7 : 8; }
-  } else if (W >= 32) { p.tile = 0; th = 2; tw = 32; imgs = 1; }
-  else if (W >= 16) { p.tile = 1; th = 4; tw = 16; imgs = 1; }
-  else if (W >= 8) { p.tile = 2; th = 8; tw = 8; imgs = 1; }
+  } else if (allow_small && H == 2 && W == 2) { p.tile = 9; th = 2; tw = 2; imgs = 16; }
+  else if (allow_small && H == 4 && W == 4) { p.tile = 10; th = 4; tw = 4; imgs = 4; }
+  else if (W >= 32) { p.tile = 0; }
+  else if (W >= 16) { p.tile = 1; th = 4; tw = 16; }
+  else if (W >= 8) { p.tile = 2; th = 8; tw = 8; }
   else if (W >= 4) { p.tile = 3; th = 4; tw = 4; imgs = 4; }
   else { p.tile = 4; th = 2; tw = 2; imgs = 16; }
   p.tiles_w = cdiv(W, tw);
   p.tiles_h = cdiv(H, th);
-  p.ptiles = p.tiles_w * p.tiles_h * cdiv(N, imgs);
+  p.ptiles = p.tiles_w * p.tiles_h * cdiv(N, imgs);   // for the small kernels: image chunks
   p.k_tiles = cdiv(K, 64);
   p.c_tiles = narrow ? 1 : cdiv(C, 16);
   long blocks = (long)p.k_tiles * p.c_tiles;
-  // About two blocks per CU, but at most 128 splits of the pixel range.
+  // About two blocks per CU, at most 128 splits of the pixel range.
   const long target = 512;
   int splits = 1;
   if (blocks < target)
@@ -276,27 +468,27 @@ static WgPlan wg_plan(int N, int C, int H, int W, int K) {
   return p;
 }
 
-template <class T>
-static void wg_launch(const WgPlan& p, const float* x, const float* dy, float* dw, float* db,
-                      float* ws, int N, int C, int H, int W, int K, hipStream_t st) {
+template <class T, bool SMALL>
+static void wg_launch(const WgPlan& p, const WgArgs& a, hipStream_t st) {
   static bool attr_set = false;
+  const void* fn;
+  if constexpr (SMALL) fn = (const void*)conv3x3_wgrad_small_f32<T>;
+  else fn = (const void*)conv3x3_wgrad_f32<T>;
   if (!attr_set) {
-    hipFuncSetAttribute((const void*)conv3x3_wgrad_f32<T>,
-                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)T::LDS_BYTES);
+    hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)T::LDS_BYTES);
     attr_set = true;
   }
   dim3 grid(p.k_tiles * p.c_tiles, 1, p.splits);
-  const bool part = p.splits > 1;
-  const size_t wsz = (size_t)K * C * 9;
-  float* pdw = part ? ws : dw;
-  float* pdb = db ? (part ? ws + (size_t)p.splits * wsz : db) : nullptr;
-  conv3x3_wgrad_f32<T><<<grid, 256, T::LDS_BYTES, st>>>(
-      x, dy, pdw, pdb, N, C, H, W, K, p.tiles_w, p.tiles_h, p.ptiles, p.tps, p.c_tiles,
-      part ? 1 : 0);
-  if (part) {
-    splits_reduce<<<(unsigned)((wsz + 63) / 64), 256, 0, st>>>(ws, p.splits, wsz, dw);
-    if (db)
-      splits_reduce<<<(unsigned)((K + 63) / 64), 256, 0, st>>>(pdb, p.splits, (size_t)K, db);
+  if constexpr (SMALL)
+    conv3x3_wgrad_small_f32<T><<<grid, 256, T::LDS_BYTES, st>>>(a);
+  else
+    conv3x3_wgrad_f32<T><<<grid, 256, T::LDS_BYTES, st>>>(a);
+  if (p.splits > 1) {
+    const size_t wsz = (size_t)a.K * a.C * 9;
+    splits_reduce<<<(unsigned)((wsz + 63) / 64), 256, 0, st>>>(a.part, p.splits, wsz, a.dw);
+    if (a.db)
+      splits_reduce<<<(unsigned)((a.K + 63) / 64), 256, 0, st>>>(
+          a.part + (size_t)p.splits * wsz, p.splits, (size_t)a.K, a.db);
   }
 }
 
@@ -305,34 +497,39 @@ static void wg_launch(const WgPlan& p, const float* x, const float* dy, float* d
 namespace sbh {
 
 size_t conv_wgrad_ws(int N, int C, int H, int W, int K) {
-  return sb::wg_plan(N, C, H, W, K).ws_bytes;
+  return std::max(sb::wg_plan(N, C, H, W, K, true).ws_bytes,
+                  sb::wg_plan(N, C, H, W, K, false).ws_bytes);
 }
 
 int conv_wgrad_describe(int N, int C, int H, int W, int K, char* buf, size_t len) {
-  static const char* names[] = {"2, 32, 1, 0", "4, 16, 1, 0", "8, 8, 1, 0", "4, 4, 4, 0",
-                                "2, 2, 16, 0", "2, 32, 1, 2", "2, 32, 1, 4", "4, 4, 4, 2",
-                                "4, 4, 4, 4"};
   sb::WgPlan p = sb::wg_plan(N, C, H, W, K);
-  return snprintf(buf, len, "sb::conv3x3_wgrad_f32<sb::WgTile<%s> > grid=%dx1x%d%s",
-                  names[p.tile], p.k_tiles * p.c_tiles, p.splits,
-                  p.splits > 1 ? " +sb::splits_reduce" : "");
+  return snprintf(buf, len, "%s grid=%dx1x%d", sb::kWgNames[p.tile], p.k_tiles * p.c_tiles,
+                  p.splits);
 }
 
 sb_status conv_wgrad_f32(int N, int C, int H, int W, int K, const float* x, const float* dy,
                          float* dw, float* db, void* ws, size_t ws_bytes, hipStream_t st) {
-  sb::WgPlan p = sb::wg_plan(N, C, H, W, K);
+  const bool aligned = (((uintptr_t)x | (uintptr_t)dy) & 15) == 0;
+  sb::WgPlan p = sb::wg_plan(N, C, H, W, K, aligned);
   if (p.ws_bytes > 0 && (ws == nullptr || ws_bytes < p.ws_bytes)) return SB_ERR_WORKSPACE;
-  float* w = (float*)ws;
+  sb::WgArgs a{};
+  a.x = x; a.dy = dy; a.dw = dw; a.db = db;
+  a.part = p.splits > 1 ? (float*)ws : nullptr;
+  a.N = N; a.C = C; a.H = H; a.W = W; a.K = K;
+  a.tiles_w = p.tiles_w; a.tiles_h = p.tiles_h; a.ptiles = p.ptiles;
+  a.tiles_per_split = p.tps; a.c_tiles = p.c_tiles; a.splits = p.splits;
   switch (p.tile) {
-    case 0: sb::wg_launch<sb::WgW32>(p, x, dy, dw, db, w, N, C, H, W, K, st); break;
-    case 1: sb::wg_launch<sb::WgW16>(p, x, dy, dw, db, w, N, C, H, W, K, st); break;
-    case 2: sb::wg_launch<sb::WgW8>(p, x, dy, dw, db, w, N, C, H, W, K, st); break;
-    case 3: sb::wg_launch<sb::WgW4>(p, x, dy, dw, db, w, N, C, H, W, K, st); break;
-    case 4: sb::wg_launch<sb::WgW2>(p, x, dy, dw, db, w, N, C, H, W, K, st); break;
-    case 5: sb::wg_launch<sb::WgN32_2>(p, x, dy, dw, db, w, N, C, H, W, K, st); break;
-    case 6: sb::wg_launch<sb::WgN32_4>(p, x, dy, dw, db, w, N, C, H, W, K, st); break;
-    case 7: sb::wg_launch<sb::WgN4_2>(p, x, dy, dw, db, w, N, C, H, W, K, st); break;
-    default: sb::wg_launch<sb::WgN4_4>(p, x, dy, dw, db, w, N, C, H, W, K, st); break;
+    case 0: sb::wg_launch<sb::WgW32, false>(p, a, st); break;
+    case 1: sb::wg_launch<sb::WgW16, false>(p, a, st); break;
+    case 2: sb::wg_launch<sb::WgW8, false>(p, a, st); break;
+    case 3: sb::wg_launch<sb::WgW4, false>(p, a, st); break;
+    case 4: sb::wg_launch<sb::WgW2, false>(p, a, st); break;
+    case 5: sb::wg_launch<sb::WgN32_2, false>(p, a, st); break;
+    case 6: sb::wg_launch<sb::WgN32_4, false>(p, a, st); break;
+    case 7: sb::wg_launch<sb::WgN4_2, false>(p, a, st); break;
+    case 8: sb::wg_launch<sb::WgN4_4, false>(p, a, st); break;
+    case 9: sb::wg_launch<sb::WgS2, true>(p, a, st); break;
+    default: sb::wg_launch<sb::WgS4, true>(p, a, st); break;
   }
   return launch_status();
 }

@@ -128,7 +128,8 @@ class ConvStack:
                        sb.sb_conv3x3_workspace_bytes(self.desc[l.index], sb.SB_PASS_FWD),
                        sb.sb_conv3x3_workspace_bytes(self.desc_b[l.index], sb.SB_PASS_BWD_DATA),
                        sb.sb_conv3x3_workspace_bytes(self.desc_b[l.index], sb.SB_PASS_BWD_WEIGHT))
-        self.ws = torch.empty((max(need, 256) + 255) // 256 * 256, dtype=torch.uint8, device=dev)
+        # Zero-filled once: libsb's split-reduction counters live at its start.
+        self.ws = torch.zeros((max(need, 256) + 255) // 256 * 256, dtype=torch.uint8, device=dev)
         self.call = _plain      # replace with an EventTimer to time each call
 
     # -- data placement (host -> device copies of seeded inputs) --------------
@@ -215,7 +216,8 @@ class FCShard:
         self.db = torch.empty((ns,), dtype=torch.float32, device=dev)
         need = max(sb.sb_fc_workspace_bytes(self.desc_f, sb.SB_FC_FWD),
                    sb.sb_fc_workspace_bytes(self.desc_b, sb.SB_FC_BWD))
-        self.ws = torch.empty((max(need, 256) + 255) // 256 * 256, dtype=torch.uint8, device=dev)
+        # Zero-filled once: libsb's split-reduction counters live at its start.
+        self.ws = torch.zeros((max(need, 256) + 255) // 256 * 256, dtype=torch.uint8, device=dev)
 
     def forward(self, x_ptr, y_ptr, stream=None):
         sb.sb_fc_shard_fwd(self.desc_f, x_ptr, self.W, self.b, y_ptr, self.ws, stream)

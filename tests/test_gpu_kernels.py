@@ -15,7 +15,8 @@ pytestmark = pytest.mark.gpu
 
 
 def _ws(nbytes):
-    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device="cuda")
+    # A libsb workspace is zero-filled before first use (split counters).
+    return torch.zeros(max(int(nbytes), 256), dtype=torch.uint8, device="cuda")
 
 
 # ------------------------------------------------------------------ pool --

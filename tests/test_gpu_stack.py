@@ -24,7 +24,8 @@ SAMPLES = 3000
 
 
 def _ws(nbytes):
-    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device="cuda")
+    # A libsb workspace is zero-filled before first use (split counters).
+    return torch.zeros(max(int(nbytes), 256), dtype=torch.uint8, device="cuda")
 
 
 @pytest.mark.parametrize("L", VGG_CIFAR, ids=lambda L: "conv%d_%dx%d_%d" % (L.index + 1, L.c, L.k, L.h))
