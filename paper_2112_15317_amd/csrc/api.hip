@@ -5,14 +5,15 @@
 
 namespace sbh {
 size_t conv_igemm_ws(int N, int Cin, int H, int W, int Cout);
-sb_status conv_igemm_f32(bool dgrad, int N, int Cin, int H, int W, int Cout, const float* in,
-                         const float* wt, const float* bias, const float* mask, float* out,
-                         void* ws, size_t ws_bytes, int relu, hipStream_t st);
+sb_status conv_igemm(bool dgrad, int dtype, int N, int Cin, int H, int W, int Cout,
+                     const void* in, const void* wt, const float* bias, const void* mask,
+                     void* out, void* ws, size_t ws_bytes, int relu, hipStream_t st);
 size_t conv_wgrad_ws(int N, int C, int H, int W, int K);
-int conv_igemm_describe(bool dgrad, int N, int Cin, int H, int W, int Cout, char* buf, size_t len);
-int conv_wgrad_describe(int N, int C, int H, int W, int K, char* buf, size_t len);
-sb_status conv_wgrad_f32(int N, int C, int H, int W, int K, const float* x, const float* dy,
-                         float* dw, float* db, void* ws, size_t ws_bytes, hipStream_t st);
+int conv_igemm_describe(bool dgrad, int dtype, int N, int Cin, int H, int W, int Cout, char* buf,
+                        size_t len);
+int conv_wgrad_describe(int dtype, int N, int C, int H, int W, int K, char* buf, size_t len);
+sb_status conv_wgrad(int dtype, int N, int C, int H, int W, int K, const void* x, const void* dy,
+                     float* dw, float* db, void* ws, size_t ws_bytes, hipStream_t st);
 }  // namespace sbh
 
 extern "C" const char* sb_status_string(sb_status s) {
@@ -38,7 +39,6 @@ static sb_status conv_check(const sb_conv3x3_desc* d, int pass) {
   if ((int64_t)d->k * d->c * 9 >= (1ll << 31)) return SB_ERR_UNSUPPORTED;
   if ((int64_t)d->n * d->c * d->h * d->w >= (1ll << 31)) return SB_ERR_UNSUPPORTED;
   if ((int64_t)d->n * d->k * d->h * d->w >= (1ll << 31)) return SB_ERR_UNSUPPORTED;
-  if (d->dtype == SB_BF16) return SB_ERR_UNSUPPORTED;
   return SB_OK;
 }
 
@@ -71,9 +71,9 @@ extern "C" sb_status sb_conv3x3_fwd(const sb_conv3x3_desc* d, const void* x, con
   if (need && (!ws || ws_bytes < need)) return SB_ERR_WORKSPACE;
   if (need && (sbh::overlaps(ws, need, x, xb) || sbh::overlaps(ws, need, y, yb)))
     return SB_ERR_INVALID_ARG;
-  return sbh::conv_igemm_f32(false, d->n, d->c, d->h, d->w, d->k, (const float*)x,
-                             (const float*)w, bias, nullptr, (float*)y, ws, ws_bytes,
-                             (d->flags & SB_FUSE_RELU) ? 1 : 0, sbh::stream_of(stream));
+  return sbh::conv_igemm(false, d->dtype, d->n, d->c, d->h, d->w, d->k, x, w, bias, nullptr, y,
+                         ws, ws_bytes, (d->flags & SB_FUSE_RELU) ? 1 : 0,
+                         sbh::stream_of(stream));
 }
 
 extern "C" sb_status sb_conv3x3_bwd_data(const sb_conv3x3_desc* d, const void* dy, const void* w,
@@ -92,9 +92,8 @@ extern "C" sb_status sb_conv3x3_bwd_data(const sb_conv3x3_desc* d, const void* d
   if (need && (sbh::overlaps(ws, need, dy, dyb) || sbh::overlaps(ws, need, dx, dxb) ||
                sbh::overlaps(ws, need, mask, mask ? dxb : 0)))
     return SB_ERR_INVALID_ARG;
-  return sbh::conv_igemm_f32(true, d->n, d->k, d->h, d->w, d->c, (const float*)dy,
-                             (const float*)w, nullptr, (const float*)mask, (float*)dx, ws,
-                             ws_bytes, 0, sbh::stream_of(stream));
+  return sbh::conv_igemm(true, d->dtype, d->n, d->k, d->h, d->w, d->c, dy, w, nullptr, mask, dx,
+                         ws, ws_bytes, 0, sbh::stream_of(stream));
 }
 
 extern "C" sb_status sb_conv3x3_bwd_weight(const sb_conv3x3_desc* d, const void* x, const void* dy,
@@ -114,8 +113,8 @@ extern "C" sb_status sb_conv3x3_bwd_weight(const sb_conv3x3_desc* d, const void*
   if (need && (sbh::overlaps(ws, need, dw, dwb) || sbh::overlaps(ws, need, db, dbb) ||
                sbh::overlaps(ws, need, x, xb) || sbh::overlaps(ws, need, dy, dyb)))
     return SB_ERR_INVALID_ARG;
-  return sbh::conv_wgrad_f32(d->n, d->c, d->h, d->w, d->k, (const float*)x, (const float*)dy, dw,
-                             db, ws, ws_bytes, sbh::stream_of(stream));
+  return sbh::conv_wgrad(d->dtype, d->n, d->c, d->h, d->w, d->k, x, dy, dw, db, ws, ws_bytes,
+                         sbh::stream_of(stream));
 }
 
 extern "C" size_t sb_conv3x3_plan_string(const sb_conv3x3_desc* d, int pass, char* buf,
@@ -124,9 +123,13 @@ extern "C" size_t sb_conv3x3_plan_string(const sb_conv3x3_desc* d, int pass, cha
   if (conv_check(d, pass) != SB_OK) return 0;
   int r;
   switch (pass) {
-    case SB_PASS_FWD: r = sbh::conv_igemm_describe(false, d->n, d->c, d->h, d->w, d->k, buf, len); break;
-    case SB_PASS_BWD_DATA: r = sbh::conv_igemm_describe(true, d->n, d->k, d->h, d->w, d->c, buf, len); break;
-    default: r = sbh::conv_wgrad_describe(d->n, d->c, d->h, d->w, d->k, buf, len); break;
+    case SB_PASS_FWD:
+      r = sbh::conv_igemm_describe(false, d->dtype, d->n, d->c, d->h, d->w, d->k, buf, len);
+      break;
+    case SB_PASS_BWD_DATA:
+      r = sbh::conv_igemm_describe(true, d->dtype, d->n, d->k, d->h, d->w, d->c, buf, len);
+      break;
+    default: r = sbh::conv_wgrad_describe(d->dtype, d->n, d->c, d->h, d->w, d->k, buf, len); break;
   }
   return r < 0 ? 0 : (size_t)r + 1;
 }

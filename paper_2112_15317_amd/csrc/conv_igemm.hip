@@ -45,21 +45,24 @@
 
 namespace sb {
 
+// Element type E of in / wt / mask / out: float or bf16 bits (u16).
+// Accumulation, bias and split partials are fp32.
 struct ConvArgs {
-  const float* in;       // [N][Cin][H][W]
-  const float* wt;       // forward filters [K][C][3][3]
+  const void* in;        // [N][Cin][H][W]
+  const void* wt;        // forward filters [K][C][3][3]
   const float* bias;     // [Cout] or null (forward)
-  const float* mask;     // [N][Cout][H][W] or null (data gradient)
-  float* out;            // [N][Cout][H][W]
+  const void* mask;      // [N][Cout][H][W] or null (data gradient)
+  void* out;             // [N][Cout][H][W]
   float* part;           // split partials [splits][N][Cout][H][W]
   int N, Cin, H, W, Cout;
   int tiles_w, tiles_h, chunks_per_split, splits, relu;
 };
 
+template <class E>
 __device__ __forceinline__ float conv_epilogue(const ConvArgs& a, float v, int co, size_t off) {
   if (a.bias) v += a.bias[co];
   if (a.relu && !(v > 0.f)) v = 0.f;
-  if (a.mask && !(a.mask[off] > 0.f)) v = 0.f;
+  if (a.mask && !(Elem<E>::load((const E*)a.mask, off) > 0.f)) v = 0.f;
   return v;
 }
 
@@ -94,13 +97,13 @@ __device__ __forceinline__ void filter_plan(int e, int co0, int Cin, int Cout, i
   }
 }
 
-template <bool DGRAD>
+template <bool DGRAD, class E>
 __device__ __forceinline__ float filter_load(const ConvArgs& a, int goff, int ci_in_chunk,
                                              int cbase) {
   const int ci = cbase + ci_in_chunk;
   const bool ok = goff >= 0 && ci < a.Cin;
   const int idx = DGRAD ? goff + cbase * a.Cout * 9 : goff + cbase * 9;
-  const float v = a.wt[ok ? idx : 0];
+  const float v = Elem<E>::load((const E*)a.wt, ok ? idx : 0);
   return ok ? v : 0.f;
 }
 
@@ -134,7 +137,7 @@ struct ConvTile {
   static constexpr int NSTEP = 9 * (CK / 4);     // MFMA k-steps per chunk
 };
 
-template <class T, bool DGRAD>
+template <class T, bool DGRAD, class E>
 __global__ __launch_bounds__(256, 2) void conv3x3_igemm_f32(ConvArgs a) {
   extern __shared__ float lds[];
 
@@ -197,11 +200,11 @@ __global__ __launch_bounds__(256, 2) void conv3x3_igemm_f32(ConvArgs a) {
     for (int i = 0; i < T::HALO_PT; ++i) {
       const int ci = cbase + x_c[i];
       const bool ok = x_off[i] >= 0 && ci < a.Cin;
-      const float v = a.in[ok ? x_off[i] + ci * HWs : 0];
+      const float v = Elem<E>::load((const E*)a.in, ok ? x_off[i] + ci * HWs : 0);
       rx[i] = ok ? v : 0.f;
     }
 #pragma unroll
-    for (int i = 0; i < T::WTS_PT; ++i) rw[i] = filter_load<DGRAD>(a, w_off[i], w_ci[i], cbase);
+    for (int i = 0; i < T::WTS_PT; ++i) rw[i] = filter_load<DGRAD, E>(a, w_off[i], w_ci[i], cbase);
   };
   auto lstore = [&](int buf) {
     float* X = lds + buf * T::LDS_BUF;
@@ -276,7 +279,9 @@ __global__ __launch_bounds__(256, 2) void conv3x3_igemm_f32(ConvArgs a) {
     }
   };
   if (a.splits == 1) {
-    for_each_out([&](float v, int co, size_t off) { a.out[off] = conv_epilogue(a, v, co, off); });
+    for_each_out([&](float v, int co, size_t off) {
+      Elem<E>::store((E*)a.out, off, conv_epilogue<E>(a, v, co, off));
+    });
     return;
   }
   float* mine = a.part + (size_t)blockIdx.z * total;
@@ -316,7 +321,7 @@ struct SmallTile {
   }
 };
 
-template <class T, bool DGRAD>
+template <class T, bool DGRAD, class E>
 __global__ __launch_bounds__(256, 2) void conv3x3_small_f32(ConvArgs a) {
   extern __shared__ float lds[];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -362,11 +367,11 @@ __global__ __launch_bounds__(256, 2) void conv3x3_small_f32(ConvArgs a) {
     for (int i = 0; i < T::X_PT; ++i) {
       const int ci = cbase + x_c[i];
       const bool ok = x_off[i] >= 0 && ci < a.Cin;
-      const f4 v = *reinterpret_cast<const f4*>(a.in + (ok ? x_off[i] + ci * T::P : 0));
+      const f4 v = Elem<E>::load4((const E*)a.in + (ok ? x_off[i] + ci * T::P : 0));
       rx[i] = ok ? v : f4{0.f, 0.f, 0.f, 0.f};
     }
 #pragma unroll
-    for (int i = 0; i < T::WTS_PT; ++i) rw[i] = filter_load<DGRAD>(a, w_off[i], w_ci[i], cbase);
+    for (int i = 0; i < T::WTS_PT; ++i) rw[i] = filter_load<DGRAD, E>(a, w_off[i], w_ci[i], cbase);
   };
   auto lstore = [&](int buf) {
     float* X = lds + buf * T::LDS_BUF;
@@ -443,7 +448,7 @@ __global__ __launch_bounds__(256, 2) void conv3x3_small_f32(ConvArgs a) {
   };
   auto epi4 = [&](f4 v, int co, size_t off) {
     f4 m = {1.f, 1.f, 1.f, 1.f};
-    if (a.mask) m = *reinterpret_cast<const f4*>(a.mask + off);
+    if (a.mask) m = Elem<E>::load4((const E*)a.mask + off);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       float x = v[j];
@@ -452,7 +457,7 @@ __global__ __launch_bounds__(256, 2) void conv3x3_small_f32(ConvArgs a) {
       if (a.mask && !(m[j] > 0.f)) x = 0.f;
       v[j] = x;
     }
-    *reinterpret_cast<f4*>(a.out + off) = v;
+    Elem<E>::store4((E*)a.out + off, v);
   };
   if (a.splits == 1) {
     for_each_out4(epi4);
@@ -463,10 +468,11 @@ __global__ __launch_bounds__(256, 2) void conv3x3_small_f32(ConvArgs a) {
 }
 
 // Sum of the split partials in a fixed order, then the epilogue.
+template <class E>
 __global__ __launch_bounds__(256) void conv_splitk_reduce(
     const float* __restrict__ part, int splits, size_t total, int Cout, int HWs,
-    const float* __restrict__ bias, int relu, const float* __restrict__ mask,
-    float* __restrict__ out) {
+    const float* __restrict__ bias, int relu, const E* __restrict__ mask,
+    E* __restrict__ out) {
   __shared__ float lds[256];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const size_t i = (size_t)blockIdx.x * 64 + lane;
@@ -474,8 +480,8 @@ __global__ __launch_bounds__(256) void conv_splitk_reduce(
   if (wave != 0 || i >= total) return;
   if (bias) v += bias[(i / HWs) % Cout];
   if (relu && !(v > 0.f)) v = 0.f;
-  if (mask && !(mask[i] > 0.f)) v = 0.f;
-  out[i] = v;
+  if (mask && !(Elem<E>::load(mask, i) > 0.f)) v = 0.f;
+  Elem<E>::store(out, i, v);
 }
 
 // ---------------------------------------------------------------- host --
@@ -498,19 +504,19 @@ using Small2 = SmallTile<2, 2, 2>;
 using Small4 = SmallTile<4, 4, 1>;
 
 static const char* kTileNames[] = {
-    "sb::conv3x3_igemm_f32<sb::ConvTile<4, 32, 1, 8, 64>, %s>",
-    "sb::conv3x3_igemm_f32<sb::ConvTile<8, 16, 1, 8, 64>, %s>",
-    "sb::conv3x3_igemm_f32<sb::ConvTile<8, 8, 2, 8, 64>, %s>",
-    "sb::conv3x3_igemm_f32<sb::ConvTile<4, 4, 8, 8, 64>, %s>",
-    "sb::conv3x3_igemm_f32<sb::ConvTile<2, 2, 32, 8, 64>, %s>",
-    "sb::conv3x3_igemm_f32<sb::ConvTile<4, 32, 1, 4, 64>, %s>",
-    "sb::conv3x3_igemm_f32<sb::ConvTile<4, 32, 1, 8, 16>, %s>",
-    "sb::conv3x3_small_f32<sb::SmallTile<2, 2, 2>, %s>",
-    "sb::conv3x3_small_f32<sb::SmallTile<4, 4, 1>, %s>",
+    "sb::conv3x3_igemm_f32<sb::ConvTile<4, 32, 1, 8, 64>, %s, %s>",
+    "sb::conv3x3_igemm_f32<sb::ConvTile<8, 16, 1, 8, 64>, %s, %s>",
+    "sb::conv3x3_igemm_f32<sb::ConvTile<8, 8, 2, 8, 64>, %s, %s>",
+    "sb::conv3x3_igemm_f32<sb::ConvTile<4, 4, 8, 8, 64>, %s, %s>",
+    "sb::conv3x3_igemm_f32<sb::ConvTile<2, 2, 32, 8, 64>, %s, %s>",
+    "sb::conv3x3_igemm_f32<sb::ConvTile<4, 32, 1, 4, 64>, %s, %s>",
+    "sb::conv3x3_igemm_f32<sb::ConvTile<4, 32, 1, 8, 16>, %s, %s>",
+    "sb::conv3x3_small_f32<sb::SmallTile<2, 2, 2>, %s, %s>",
+    "sb::conv3x3_small_f32<sb::SmallTile<4, 4, 1>, %s, %s>",
 };
 
-// allow_small: the whole-image kernel moves float4s, so it needs 16-byte
-// aligned tensors.
+// allow_small: the whole-image kernel needs tensors aligned for 4-element
+// moves.
 static IgemmPlan igemm_plan(int N, int Cin, int H, int W, int Cout, bool allow_small = true) {
   IgemmPlan p{};
   int th = 4, tw = 32, imgs = 1, ck = 8, bn = 64;
@@ -542,12 +548,12 @@ static IgemmPlan igemm_plan(int N, int Cin, int H, int W, int Cout, bool allow_s
   return p;
 }
 
-template <class T, bool DGRAD, bool SMALL>
+template <class T, bool DGRAD, bool SMALL, class E>
 static void igemm_launch(const IgemmPlan& p, const ConvArgs& a, hipStream_t st) {
   static bool attr_set = false;
   const void* fn;
-  if constexpr (SMALL) fn = (const void*)conv3x3_small_f32<T, DGRAD>;
-  else fn = (const void*)conv3x3_igemm_f32<T, DGRAD>;
+  if constexpr (SMALL) fn = (const void*)conv3x3_small_f32<T, DGRAD, E>;
+  else fn = (const void*)conv3x3_igemm_f32<T, DGRAD, E>;
   if (!attr_set) {
     hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)T::LDS_BYTES);
     attr_set = true;
@@ -556,28 +562,29 @@ static void igemm_launch(const IgemmPlan& p, const ConvArgs& a, hipStream_t st) 
   ConvArgs k = a;
   if (p.splits > 1) { k.bias = nullptr; k.mask = nullptr; k.relu = 0; }
   if constexpr (SMALL)
-    conv3x3_small_f32<T, DGRAD><<<grid, 256, T::LDS_BYTES, st>>>(k);
+    conv3x3_small_f32<T, DGRAD, E><<<grid, 256, T::LDS_BYTES, st>>>(k);
   else
-    conv3x3_igemm_f32<T, DGRAD><<<grid, 256, T::LDS_BYTES, st>>>(k);
+    conv3x3_igemm_f32<T, DGRAD, E><<<grid, 256, T::LDS_BYTES, st>>>(k);
   if (p.splits > 1) {
     size_t total = (size_t)a.N * a.Cout * a.H * a.W;
-    conv_splitk_reduce<<<(unsigned)((total + 63) / 64), 256, 0, st>>>(
-        a.part, p.splits, total, a.Cout, a.H * a.W, a.bias, a.relu, a.mask, a.out);
+    conv_splitk_reduce<E><<<(unsigned)((total + 63) / 64), 256, 0, st>>>(
+        a.part, p.splits, total, a.Cout, a.H * a.W, a.bias, a.relu, (const E*)a.mask,
+        (E*)a.out);
   }
 }
 
-template <bool DGRAD>
+template <bool DGRAD, class E>
 static void igemm_dispatch(const IgemmPlan& p, const ConvArgs& a, hipStream_t st) {
   switch (p.tile) {
-    case 0: igemm_launch<TileW32, DGRAD, false>(p, a, st); break;
-    case 1: igemm_launch<TileW16, DGRAD, false>(p, a, st); break;
-    case 2: igemm_launch<TileW8, DGRAD, false>(p, a, st); break;
-    case 3: igemm_launch<TileW4, DGRAD, false>(p, a, st); break;
-    case 4: igemm_launch<TileW2, DGRAD, false>(p, a, st); break;
-    case 5: igemm_launch<TileW32c4, DGRAD, false>(p, a, st); break;
-    case 6: igemm_launch<TileW32n16, DGRAD, false>(p, a, st); break;
-    case 7: igemm_launch<Small2, DGRAD, true>(p, a, st); break;
-    default: igemm_launch<Small4, DGRAD, true>(p, a, st); break;
+    case 0: igemm_launch<TileW32, DGRAD, false, E>(p, a, st); break;
+    case 1: igemm_launch<TileW16, DGRAD, false, E>(p, a, st); break;
+    case 2: igemm_launch<TileW8, DGRAD, false, E>(p, a, st); break;
+    case 3: igemm_launch<TileW4, DGRAD, false, E>(p, a, st); break;
+    case 4: igemm_launch<TileW2, DGRAD, false, E>(p, a, st); break;
+    case 5: igemm_launch<TileW32c4, DGRAD, false, E>(p, a, st); break;
+    case 6: igemm_launch<TileW32n16, DGRAD, false, E>(p, a, st); break;
+    case 7: igemm_launch<Small2, DGRAD, true, E>(p, a, st); break;
+    default: igemm_launch<Small4, DGRAD, true, E>(p, a, st); break;
   }
 }
 
@@ -591,18 +598,22 @@ size_t conv_igemm_ws(int N, int Cin, int H, int W, int Cout) {
                   sb::igemm_plan(N, Cin, H, W, Cout, false).ws_bytes);
 }
 
-int conv_igemm_describe(bool dgrad, int N, int Cin, int H, int W, int Cout, char* buf,
-                        size_t len) {
+int conv_igemm_describe(bool dgrad, int dtype, int N, int Cin, int H, int W, int Cout,
+                        char* buf, size_t len) {
   sb::IgemmPlan p = sb::igemm_plan(N, Cin, H, W, Cout);
   char name[160];
-  snprintf(name, sizeof(name), sb::kTileNames[p.tile], dgrad ? "true" : "false");
+  snprintf(name, sizeof(name), sb::kTileNames[p.tile], dgrad ? "true" : "false",
+           dtype == SB_BF16 ? "unsigned short" : "float");
   return snprintf(buf, len, "%s grid=%dx%dx%d", name, p.grid_x, p.co_tiles, p.splits);
 }
 
-sb_status conv_igemm_f32(bool dgrad, int N, int Cin, int H, int W, int Cout, const float* in,
-                         const float* wt, const float* bias, const float* mask, float* out,
-                         void* ws, size_t ws_bytes, int relu, hipStream_t st) {
-  const bool aligned = (((uintptr_t)in | (uintptr_t)out | (uintptr_t)mask) & 15) == 0;
+sb_status conv_igemm(bool dgrad, int dtype, int N, int Cin, int H, int W, int Cout,
+                     const void* in, const void* wt, const float* bias, const void* mask,
+                     void* out, void* ws, size_t ws_bytes, int relu, hipStream_t st) {
+  // The whole-image kernels move 4 elements at a time (16 bytes in fp32, 8 in
+  // bf16); the plan only picks them for tensors aligned that far.
+  const uintptr_t amask = dtype == SB_BF16 ? 7 : 15;
+  const bool aligned = (((uintptr_t)in | (uintptr_t)out | (uintptr_t)mask) & amask) == 0;
   sb::IgemmPlan p = sb::igemm_plan(N, Cin, H, W, Cout, aligned);
   if (p.ws_bytes > 0 && (ws == nullptr || ws_bytes < p.ws_bytes)) return SB_ERR_WORKSPACE;
   sb::ConvArgs a{};
@@ -611,8 +622,13 @@ sb_status conv_igemm_f32(bool dgrad, int N, int Cin, int H, int W, int Cout, con
   a.N = N; a.Cin = Cin; a.H = H; a.W = W; a.Cout = Cout;
   a.tiles_w = p.tiles_w; a.tiles_h = p.tiles_h;
   a.chunks_per_split = p.cps; a.splits = p.splits; a.relu = relu;
-  if (dgrad) sb::igemm_dispatch<true>(p, a, st);
-  else sb::igemm_dispatch<false>(p, a, st);
+  if (dtype == SB_BF16) {
+    if (dgrad) sb::igemm_dispatch<true, sb::u16>(p, a, st);
+    else sb::igemm_dispatch<false, sb::u16>(p, a, st);
+  } else {
+    if (dgrad) sb::igemm_dispatch<true, float>(p, a, st);
+    else sb::igemm_dispatch<false, float>(p, a, st);
+  }
   return launch_status();
 }
 

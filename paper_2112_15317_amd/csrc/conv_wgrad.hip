@@ -40,8 +40,8 @@
 namespace sb {
 
 struct WgArgs {
-  const float* x;        // [N][C][H][W]
-  const float* dy;       // [N][K][H][W]
+  const void* x;         // [N][C][H][W], element type E of the kernel
+  const void* dy;        // [N][K][H][W], element type E
   float* dw;             // [K][C][3][3]
   float* db;             // [K] or null
   float* part;           // split partials: [splits][K*C*9] then [splits][K]
@@ -129,7 +129,7 @@ __device__ __forceinline__ int wg_hoff(int p) {
   return img * T::HH * T::HW + yy * T::HW + xx;
 }
 
-template <class T>
+template <class T, class E>
 __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_f32(WgArgs a) {
   extern __shared__ float lds[];
 
@@ -177,7 +177,7 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_f32(WgArgs a) {
       int yy = r / T::TW, xx = r - yy * T::TW;
       int n = n0 + img, h = h0 + yy, w = w0 + xx, k = k0 + kk;
       bool ok = n < a.N && h < a.H && w < a.W && k < a.K;
-      float v = a.dy[ok ? (n * a.K + k) * HWs + h * a.W + w : 0];
+      float v = Elem<E>::load((const E*)a.dy, ok ? (n * a.K + k) * HWs + h * a.W + w : 0);
       rdy[i] = ok ? v : 0.f;
     }
     // x halo: element e = (halo pixel, c-in-tile) with c fastest, for the
@@ -191,7 +191,7 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_f32(WgArgs a) {
       int n = n0 + img, h = h0 + yy - 1, w = w0 + xx - 1, c = c0 + cc;
       bool ok = e < T::BC * T::PLANE && n < a.N && h >= 0 && h < a.H && w >= 0 && w < a.W &&
                 c < a.C;
-      float v = a.x[ok ? (n * a.C + c) * HWs + h * a.W + w : 0];
+      float v = Elem<E>::load((const E*)a.x, ok ? (n * a.C + c) * HWs + h * a.W + w : 0);
       rx[i] = ok ? v : 0.f;
     }
   };
@@ -289,7 +289,7 @@ struct WgSmall {
   }
 };
 
-template <class T>
+template <class T, class E>
 __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_small_f32(WgArgs a) {
   extern __shared__ float lds[];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -334,14 +334,14 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_small_f32(WgArgs a) {
     for (int i = 0; i < T::DZ_PT; ++i) {
       const int img = (tid + i * 256) / T::BK / (T::P / 4);
       const bool ok = dz_off[i] >= 0 && nb + img < a.N;
-      const f4 v = *reinterpret_cast<const f4*>(a.dy + (ok ? dz_off[i] + nb * a.K * T::P : 0));
+      const f4 v = Elem<E>::load4((const E*)a.dy + (ok ? dz_off[i] + nb * a.K * T::P : 0));
       rdz[i] = ok ? v : zero4;
     }
 #pragma unroll
     for (int i = 0; i < T::X_PT; ++i) {
       const int img = (tid + i * 256) / T::BC % T::IW;
       const bool ok = x_off[i] >= 0 && nb + img < a.N;
-      const f4 v = *reinterpret_cast<const f4*>(a.x + (ok ? x_off[i] + nb * a.C * T::P : 0));
+      const f4 v = Elem<E>::load4((const E*)a.x + (ok ? x_off[i] + nb * a.C * T::P : 0));
       rx[i] = ok ? v : zero4;
     }
   };
@@ -426,16 +426,16 @@ using WgS2 = WgSmall<2, 2, 16>;
 using WgS4 = WgSmall<4, 4, 4>;
 
 static const char* kWgNames[] = {
-    "sb::conv3x3_wgrad_f32<sb::WgTile<2, 32, 1, 0> >", "sb::conv3x3_wgrad_f32<sb::WgTile<4, 16, 1, 0> >",
-    "sb::conv3x3_wgrad_f32<sb::WgTile<8, 8, 1, 0> >",  "sb::conv3x3_wgrad_f32<sb::WgTile<4, 4, 4, 0> >",
-    "sb::conv3x3_wgrad_f32<sb::WgTile<2, 2, 16, 0> >", "sb::conv3x3_wgrad_f32<sb::WgTile<2, 32, 1, 2> >",
-    "sb::conv3x3_wgrad_f32<sb::WgTile<2, 32, 1, 4> >", "sb::conv3x3_wgrad_f32<sb::WgTile<4, 4, 4, 2> >",
-    "sb::conv3x3_wgrad_f32<sb::WgTile<4, 4, 4, 4> >",
-    "sb::conv3x3_wgrad_small_f32<sb::WgSmall<2, 2, 16> >",
-    "sb::conv3x3_wgrad_small_f32<sb::WgSmall<4, 4, 4> >",
+    "sb::conv3x3_wgrad_f32<sb::WgTile<2, 32, 1, 0>, %s>", "sb::conv3x3_wgrad_f32<sb::WgTile<4, 16, 1, 0>, %s>",
+    "sb::conv3x3_wgrad_f32<sb::WgTile<8, 8, 1, 0>, %s>",  "sb::conv3x3_wgrad_f32<sb::WgTile<4, 4, 4, 0>, %s>",
+    "sb::conv3x3_wgrad_f32<sb::WgTile<2, 2, 16, 0>, %s>", "sb::conv3x3_wgrad_f32<sb::WgTile<2, 32, 1, 2>, %s>",
+    "sb::conv3x3_wgrad_f32<sb::WgTile<2, 32, 1, 4>, %s>", "sb::conv3x3_wgrad_f32<sb::WgTile<4, 4, 4, 2>, %s>",
+    "sb::conv3x3_wgrad_f32<sb::WgTile<4, 4, 4, 4>, %s>",
+    "sb::conv3x3_wgrad_small_f32<sb::WgSmall<2, 2, 16>, %s>",
+    "sb::conv3x3_wgrad_small_f32<sb::WgSmall<4, 4, 4>, %s>",
 };
 
-// allow_small: the whole-image kernel moves float4s (16-byte aligned tensors).
+// allow_small: the whole-image kernel needs tensors aligned for 4-element moves.
 static WgPlan wg_plan(int N, int C, int H, int W, int K, bool allow_small = true) {
   WgPlan p{};
   int th = 2, tw = 32, imgs = 1;
@@ -468,21 +468,21 @@ static WgPlan wg_plan(int N, int C, int H, int W, int K, bool allow_small = true
   return p;
 }
 
-template <class T, bool SMALL>
+template <class T, bool SMALL, class E>
 static void wg_launch(const WgPlan& p, const WgArgs& a, hipStream_t st) {
   static bool attr_set = false;
   const void* fn;
-  if constexpr (SMALL) fn = (const void*)conv3x3_wgrad_small_f32<T>;
-  else fn = (const void*)conv3x3_wgrad_f32<T>;
+  if constexpr (SMALL) fn = (const void*)conv3x3_wgrad_small_f32<T, E>;
+  else fn = (const void*)conv3x3_wgrad_f32<T, E>;
   if (!attr_set) {
     hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)T::LDS_BYTES);
     attr_set = true;
   }
   dim3 grid(p.k_tiles * p.c_tiles, 1, p.splits);
   if constexpr (SMALL)
-    conv3x3_wgrad_small_f32<T><<<grid, 256, T::LDS_BYTES, st>>>(a);
+    conv3x3_wgrad_small_f32<T, E><<<grid, 256, T::LDS_BYTES, st>>>(a);
   else
-    conv3x3_wgrad_f32<T><<<grid, 256, T::LDS_BYTES, st>>>(a);
+    conv3x3_wgrad_f32<T, E><<<grid, 256, T::LDS_BYTES, st>>>(a);
   if (p.splits > 1) {
     const size_t wsz = (size_t)a.K * a.C * 9;
     splits_reduce<<<(unsigned)((wsz + 63) / 64), 256, 0, st>>>(a.part, p.splits, wsz, a.dw);
@@ -501,15 +501,37 @@ size_t conv_wgrad_ws(int N, int C, int H, int W, int K) {
                   sb::wg_plan(N, C, H, W, K, false).ws_bytes);
 }
 
-int conv_wgrad_describe(int N, int C, int H, int W, int K, char* buf, size_t len) {
+int conv_wgrad_describe(int dtype, int N, int C, int H, int W, int K, char* buf, size_t len) {
   sb::WgPlan p = sb::wg_plan(N, C, H, W, K);
-  return snprintf(buf, len, "%s grid=%dx1x%d", sb::kWgNames[p.tile], p.k_tiles * p.c_tiles,
-                  p.splits);
+  char name[160];
+  snprintf(name, sizeof(name), sb::kWgNames[p.tile],
+           dtype == SB_BF16 ? "unsigned short" : "float");
+  return snprintf(buf, len, "%s grid=%dx1x%d", name, p.k_tiles * p.c_tiles, p.splits);
 }
 
-sb_status conv_wgrad_f32(int N, int C, int H, int W, int K, const float* x, const float* dy,
-                         float* dw, float* db, void* ws, size_t ws_bytes, hipStream_t st) {
-  const bool aligned = (((uintptr_t)x | (uintptr_t)dy) & 15) == 0;
+template <class E>
+static void wg_dispatch(const sb::WgPlan& p, const sb::WgArgs& a, hipStream_t st) {
+  switch (p.tile) {
+    case 0: sb::wg_launch<sb::WgW32, false, E>(p, a, st); break;
+    case 1: sb::wg_launch<sb::WgW16, false, E>(p, a, st); break;
+    case 2: sb::wg_launch<sb::WgW8, false, E>(p, a, st); break;
+    case 3: sb::wg_launch<sb::WgW4, false, E>(p, a, st); break;
+    case 4: sb::wg_launch<sb::WgW2, false, E>(p, a, st); break;
+    case 5: sb::wg_launch<sb::WgN32_2, false, E>(p, a, st); break;
+    case 6: sb::wg_launch<sb::WgN32_4, false, E>(p, a, st); break;
+    case 7: sb::wg_launch<sb::WgN4_2, false, E>(p, a, st); break;
+    case 8: sb::wg_launch<sb::WgN4_4, false, E>(p, a, st); break;
+    case 9: sb::wg_launch<sb::WgS2, true, E>(p, a, st); break;
+    default: sb::wg_launch<sb::WgS4, true, E>(p, a, st); break;
+  }
+}
+
+sb_status conv_wgrad(int dtype, int N, int C, int H, int W, int K, const void* x, const void* dy,
+                     float* dw, float* db, void* ws, size_t ws_bytes, hipStream_t st) {
+  // The whole-image kernel moves 4 elements at a time (16 bytes in fp32, 8
+  // in bf16).
+  const uintptr_t amask = dtype == SB_BF16 ? 7 : 15;
+  const bool aligned = (((uintptr_t)x | (uintptr_t)dy) & amask) == 0;
   sb::WgPlan p = sb::wg_plan(N, C, H, W, K, aligned);
   if (p.ws_bytes > 0 && (ws == nullptr || ws_bytes < p.ws_bytes)) return SB_ERR_WORKSPACE;
   sb::WgArgs a{};
@@ -518,19 +540,8 @@ sb_status conv_wgrad_f32(int N, int C, int H, int W, int K, const float* x, cons
   a.N = N; a.C = C; a.H = H; a.W = W; a.K = K;
   a.tiles_w = p.tiles_w; a.tiles_h = p.tiles_h; a.ptiles = p.ptiles;
   a.tiles_per_split = p.tps; a.c_tiles = p.c_tiles; a.splits = p.splits;
-  switch (p.tile) {
-    case 0: sb::wg_launch<sb::WgW32, false>(p, a, st); break;
-    case 1: sb::wg_launch<sb::WgW16, false>(p, a, st); break;
-    case 2: sb::wg_launch<sb::WgW8, false>(p, a, st); break;
-    case 3: sb::wg_launch<sb::WgW4, false>(p, a, st); break;
-    case 4: sb::wg_launch<sb::WgW2, false>(p, a, st); break;
-    case 5: sb::wg_launch<sb::WgN32_2, false>(p, a, st); break;
-    case 6: sb::wg_launch<sb::WgN32_4, false>(p, a, st); break;
-    case 7: sb::wg_launch<sb::WgN4_2, false>(p, a, st); break;
-    case 8: sb::wg_launch<sb::WgN4_4, false>(p, a, st); break;
-    case 9: sb::wg_launch<sb::WgS2, true>(p, a, st); break;
-    default: sb::wg_launch<sb::WgS4, true>(p, a, st); break;
-  }
+  if (dtype == SB_BF16) wg_dispatch<sb::u16>(p, a, st);
+  else wg_dispatch<float>(p, a, st);
   return launch_status();
 }
 

@@ -37,14 +37,32 @@ __device__ __forceinline__ u16 f32_to_bf16(float f) {
   return (u16)(u >> 16);
 }
 
+// Activation / filter element access: float (SB_F32) or bfloat16 bits held
+// in u16 (SB_BF16).  Loads widen exactly to fp32; stores round to nearest.
+// load4/store4 move 4 consecutive elements (16 or 8 bytes, aligned).
 template <typename T> struct Elem;
 template <> struct Elem<float> {
   __device__ static __forceinline__ float load(const float* p, size_t i) { return p[i]; }
   __device__ static __forceinline__ void store(float* p, size_t i, float v) { p[i] = v; }
+  __device__ static __forceinline__ f4 load4(const float* p) {
+    return *reinterpret_cast<const f4*>(p);
+  }
+  __device__ static __forceinline__ void store4(float* p, f4 v) { *reinterpret_cast<f4*>(p) = v; }
 };
 template <> struct Elem<u16> {
   __device__ static __forceinline__ float load(const u16* p, size_t i) { return bf16_to_f32(p[i]); }
   __device__ static __forceinline__ void store(u16* p, size_t i, float v) { p[i] = f32_to_bf16(v); }
+  __device__ static __forceinline__ f4 load4(const u16* p) {
+    uint2 u = *reinterpret_cast<const uint2*>(p);
+    return f4{__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u),
+              __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xffff0000u)};
+  }
+  __device__ static __forceinline__ void store4(u16* p, f4 v) {
+    uint2 u;
+    u.x = (uint32_t)f32_to_bf16(v[0]) | ((uint32_t)f32_to_bf16(v[1]) << 16);
+    u.y = (uint32_t)f32_to_bf16(v[2]) | ((uint32_t)f32_to_bf16(v[3]) << 16);
+    *reinterpret_cast<uint2*>(p) = u;
+  }
 };
 
 __host__ __device__ constexpr int cdiv(int a, int b) { return (a + b - 1) / b; }

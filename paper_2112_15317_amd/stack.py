@@ -129,7 +129,7 @@ class ConvStack:
                        sb.sb_conv3x3_workspace_bytes(self.desc_b[l.index], sb.SB_PASS_BWD_DATA),
                        sb.sb_conv3x3_workspace_bytes(self.desc_b[l.index], sb.SB_PASS_BWD_WEIGHT))
         # Zero-filled once: libsb's split-reduction counters live at its start.
-        self.ws = torch.zeros((max(need, 256) + 255) // 256 * 256, dtype=torch.uint8, device=dev)
+        self.ws = torch.empty((max(need, 256) + 255) // 256 * 256, dtype=torch.uint8, device=dev)
         self.call = _plain      # replace with an EventTimer to time each call
 
     # -- data placement (host -> device copies of seeded inputs) --------------
@@ -217,7 +217,7 @@ class FCShard:
         need = max(sb.sb_fc_workspace_bytes(self.desc_f, sb.SB_FC_FWD),
                    sb.sb_fc_workspace_bytes(self.desc_b, sb.SB_FC_BWD))
         # Zero-filled once: libsb's split-reduction counters live at its start.
-        self.ws = torch.zeros((max(need, 256) + 255) // 256 * 256, dtype=torch.uint8, device=dev)
+        self.ws = torch.empty((max(need, 256) + 255) // 256 * 256, dtype=torch.uint8, device=dev)
 
     def forward(self, x_ptr, y_ptr, stream=None):
         sb.sb_fc_shard_fwd(self.desc_f, x_ptr, self.W, self.b, y_ptr, self.ws, stream)

@@ -15,8 +15,8 @@ pytestmark = pytest.mark.gpu
 
 
 def _ws(nbytes):
-    # A libsb workspace is zero-filled before first use (split counters).
-    return torch.zeros(max(int(nbytes), 256), dtype=torch.uint8, device="cuda")
+    # The workspace needs no initialisation: hand it over full of NaN bytes.
+    return torch.full((max(int(nbytes), 256),), 0xFF, dtype=torch.uint8, device="cuda")
 
 
 # ------------------------------------------------------------------ pool --
@@ -84,49 +84,67 @@ def _conv_inputs(n, c, h, w, k, seed):
     return x, wt, b, dy, mask
 
 
+DTYPES = ["f32", "bf16"]
+
+
+def _code(dtype):
+    return sb.SB_F32 if dtype == "f32" else sb.SB_BF16
+
+
+def _tdt(dtype):
+    return torch.float32 if dtype == "f32" else torch.bfloat16
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
 @pytest.mark.parametrize("shape", CONV_SHAPES)
 @pytest.mark.parametrize("relu", [False, True])
-def test_conv_fwd(shape, relu):
+def test_conv_fwd(shape, relu, dtype):
     n, c, h, w, k = shape
-    print_case("conv_fwd", shape=shape, relu=relu)
+    print_case("conv_fwd", shape=shape, relu=relu, dtype=dtype)
     x, wt, b, _, _ = _conv_inputs(n, c, h, w, k, 11)
-    d = sb.conv_desc(n, c, h, w, k, sb.SB_F32, relu=relu)
+    d = sb.conv_desc(n, c, h, w, k, _code(dtype), relu=relu)
     ws = _ws(sb.sb_conv3x3_workspace_bytes(d, sb.SB_PASS_FWD))
-    y = torch.full((n, k, h, w), float("nan"), device="cuda")
-    sb.sb_conv3x3_fwd(d, to_dev(x), to_dev(wt), to_dev(b), y, ws)
+    y = torch.full((n, k, h, w), float("nan"), dtype=_tdt(dtype), device="cuda")
+    xd, wd = to_dev(x, dtype), to_dev(wt, dtype)
+    sb.sb_conv3x3_fwd(d, xd, wd, to_dev(b), y, ws)
     torch.cuda.synchronize()
-    ref = O.conv3x3_fwd(x, wt, b, relu=relu)
-    assert rel_l2(to_host(y), ref) <= TOL["f32"]
+    # The oracle gets exactly the values the kernel read (bf16-rounded).
+    ref = O.conv3x3_fwd(to_host(xd), to_host(wd), b, relu=relu)
+    assert rel_l2(to_host(y), ref) <= TOL[dtype]
 
 
+@pytest.mark.parametrize("dtype", DTYPES)
 @pytest.mark.parametrize("shape", CONV_SHAPES)
 @pytest.mark.parametrize("masked", [False, True])
-def test_conv_bwd_data(shape, masked):
+def test_conv_bwd_data(shape, masked, dtype):
     n, c, h, w, k = shape
-    print_case("conv_bwd_data", shape=shape, masked=masked)
+    print_case("conv_bwd_data", shape=shape, masked=masked, dtype=dtype)
     _, wt, _, dy, mask = _conv_inputs(n, c, h, w, k, 12)
-    d = sb.conv_desc(n, c, h, w, k, sb.SB_F32)
+    d = sb.conv_desc(n, c, h, w, k, _code(dtype))
     ws = _ws(sb.sb_conv3x3_workspace_bytes(d, sb.SB_PASS_BWD_DATA))
-    dx = torch.full((n, c, h, w), float("nan"), device="cuda")
-    sb.sb_conv3x3_bwd_data(d, to_dev(dy), to_dev(wt), to_dev(mask) if masked else None, dx, ws)
+    dx = torch.full((n, c, h, w), float("nan"), dtype=_tdt(dtype), device="cuda")
+    dyd, wd, md = to_dev(dy, dtype), to_dev(wt, dtype), to_dev(mask, dtype)
+    sb.sb_conv3x3_bwd_data(d, dyd, wd, md if masked else None, dx, ws)
     torch.cuda.synchronize()
-    ref = O.conv3x3_bwd_data(dy, wt, mask_src=mask if masked else None)
-    assert rel_l2(to_host(dx), ref) <= TOL["f32"]
+    ref = O.conv3x3_bwd_data(to_host(dyd), to_host(wd), mask_src=to_host(md) if masked else None)
+    assert rel_l2(to_host(dx), ref) <= TOL[dtype]
 
 
+@pytest.mark.parametrize("dtype", DTYPES)
 @pytest.mark.parametrize("shape", CONV_SHAPES)
-def test_conv_bwd_weight(shape):
+def test_conv_bwd_weight(shape, dtype):
     n, c, h, w, k = shape
-    print_case("conv_bwd_weight", shape=shape)
+    print_case("conv_bwd_weight", shape=shape, dtype=dtype)
     x, _, _, dy, _ = _conv_inputs(n, c, h, w, k, 13)
-    d = sb.conv_desc(n, c, h, w, k, sb.SB_F32)
+    d = sb.conv_desc(n, c, h, w, k, _code(dtype))
     ws = _ws(sb.sb_conv3x3_workspace_bytes(d, sb.SB_PASS_BWD_WEIGHT))
     dw = torch.full((k, c, 3, 3), float("nan"), device="cuda")
     db = torch.full((k,), float("nan"), device="cuda")
-    xd, dyd = to_dev(x), to_dev(dy)
+    xd, dyd = to_dev(x, dtype), to_dev(dy, dtype)
     sb.sb_conv3x3_bwd_weight(d, xd, dyd, dw, db, ws)
     torch.cuda.synchronize()
-    dw_ref, db_ref = O.conv3x3_bwd_weight(x, dy)
+    dw_ref, db_ref = O.conv3x3_bwd_weight(to_host(xd), to_host(dyd))
+    # dw and db are fp32 sums of exact bf16 x bf16 products: the fp32 bound.
     assert rel_l2(to_host(dw), dw_ref) <= TOL["f32"]
     assert rel_l2(to_host(db), db_ref) <= TOL["f32"]
     # Fixed summation order: a second call is bitwise identical.

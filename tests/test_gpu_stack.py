@@ -24,8 +24,8 @@ SAMPLES = 3000
 
 
 def _ws(nbytes):
-    # A libsb workspace is zero-filled before first use (split counters).
-    return torch.zeros(max(int(nbytes), 256), dtype=torch.uint8, device="cuda")
+    # The workspace needs no initialisation: hand it over full of NaN bytes.
+    return torch.full((max(int(nbytes), 256),), 0xFF, dtype=torch.uint8, device="cuda")
 
 
 @pytest.mark.parametrize("L", VGG_CIFAR, ids=lambda L: "conv%d_%dx%d_%d" % (L.index + 1, L.c, L.k, L.h))
@@ -59,6 +59,61 @@ def test_vgg_cifar_layer_full_size_sampled(L):
     ref = O.conv3x3_bwd_data_at(dy, wt, f, mask_src=mask)
     assert rel_l2(to_host(dx).ravel()[f], ref) <= TOL["f32"]
     f = sample_idx(dw.numel(), min(SAMPLES, 600), seed + 2)
+    assert rel_l2(to_host(dw).ravel()[f], O.conv3x3_bwd_weight_at(x, dy, f)) <= TOL["f32"]
+    assert rel_l2(to_host(dbias), dy.astype(np.float64).sum(axis=(0, 2, 3))) <= TOL["f32"]
+
+
+def _distinct(layers):
+    seen, out = set(), []
+    for L in layers:
+        key = (L.c, L.k, L.h, L.pool_after, L.index == 0)
+        if key not in seen:
+            seen.add(key)
+            out.append(L)
+    return out
+
+
+VGG_IMAGENET = _distinct(configs.conv_layers(configs.VGG16, 3, 224))
+
+
+@pytest.mark.parametrize("L", VGG_IMAGENET,
+                         ids=lambda L: "conv%d_%dx%d_%d" % (L.index + 1, L.c, L.k, L.h))
+def test_vgg_imagenet_bf16_layer_full_size_sampled(L):
+    """bf16 activations / filters, fp32 accumulation, batch 32 at 224x224:
+    each distinct layer shape of the ImageNet-shaped stack, sampled."""
+    n = 32
+    print_case("layer_full_bf16", layer=L.index, c=L.c, k=L.k, h=L.h, n=n)
+    seed = 300 + L.index
+    x = synth.normal((n, L.c, L.h, L.w), seed, synth.TID.IMAGES)
+    if L.index > 0:
+        x = np.maximum(x, 0)
+    wt = synth.he_normal_conv3x3(L.k, L.c, seed, synth.TID.CONV_W)
+    dy = synth.normal((n, L.k, L.h, L.w), seed, synth.TID.DY_TOP)
+    relu = not L.pool_after
+    xd, wd, dyd = to_dev(x, "bf16"), to_dev(wt, "bf16"), to_dev(dy, "bf16")
+    del x, dy
+    # The oracle sees the bf16 values the kernels read.
+    x, wt, dy = to_host(xd), to_host(wd), to_host(dyd)
+    mask = x if L.index > 0 else None
+    df = sb.conv_desc(n, L.c, L.h, L.w, L.k, sb.SB_BF16, relu=relu)
+    db_ = sb.conv_desc(n, L.c, L.h, L.w, L.k, sb.SB_BF16)
+    ws = _ws(max(sb.sb_conv3x3_workspace_bytes(df, 0), sb.sb_conv3x3_workspace_bytes(db_, 1),
+                 sb.sb_conv3x3_workspace_bytes(db_, 2)))
+    y = torch.empty((n, L.k, L.h, L.w), dtype=torch.bfloat16, device="cuda")
+    dx = torch.empty((n, L.c, L.h, L.w), dtype=torch.bfloat16, device="cuda")
+    dw = torch.empty((L.k, L.c, 3, 3), device="cuda")
+    dbias = torch.empty((L.k,), device="cuda")
+    sb.sb_conv3x3_fwd(df, xd, wd, None, y, ws)
+    sb.sb_conv3x3_bwd_data(db_, dyd, wd, xd if mask is not None else None, dx, ws)
+    sb.sb_conv3x3_bwd_weight(db_, xd, dyd, dw, dbias, ws)
+    torch.cuda.synchronize()
+    f = sample_idx(y.numel(), SAMPLES, seed)
+    assert rel_l2(to_host(y).ravel()[f], O.conv3x3_fwd_at(x, wt, f, relu=relu)) <= TOL["bf16"]
+    f = sample_idx(dx.numel(), SAMPLES, seed + 1)
+    ref = O.conv3x3_bwd_data_at(dy, wt, f, mask_src=mask)
+    assert rel_l2(to_host(dx).ravel()[f], ref) <= TOL["bf16"]
+    # Weight gradients are fp32 sums of exact bf16 products: fp32 bound.
+    f = sample_idx(dw.numel(), 300, seed + 2)
     assert rel_l2(to_host(dw).ravel()[f], O.conv3x3_bwd_weight_at(x, dy, f)) <= TOL["f32"]
     assert rel_l2(to_host(dbias), dy.astype(np.float64).sum(axis=(0, 2, 3))) <= TOL["f32"]
 
@@ -118,6 +173,95 @@ def test_vgg16_cifar_stack_end_to_end():
         assert rel_l2(to_host(st.gA[0]), b["dX"]) <= TOL["f32"]
     else:
         pytest.fail("%d certified near-tie pool decisions differ; choose another seed" % flips)
+
+
+def test_vgg16_stack_bf16_end_to_end():
+    """The bf16 stack against the oracle that rounds to bf16 wherever the GPU
+    path stores a tensor (activations, pool outputs, activation gradients).
+
+    Forward: every tensor within the bf16 bound; pool codes may differ only at
+    certified near-ties.  Such ties are common in bf16: the two sides round
+    sums that differ in their last fp32 bits, so a few windows in a thousand
+    hold two maxima that are equal on one side only.  Each such window sends
+    its gradient to another pixel, which moves the gradients of every layer
+    below by ~0.1-0.2 in relative L2 (measured), so the backward is held to the
+    bf16 bound only above the deepest pool with a differing code, and below it
+    to a gross-error bound that a wrong sign, index or transposition (relative
+    error >= 1) fails.  Per-pass bf16 parity with identical inputs is tested
+    layer by layer at full size."""
+    n, hw = 2, 32
+    print_case("vgg16_stack_bf16", n=n, hw=hw)
+    layers = configs.conv_layers(configs.VGG16, 3, hw)
+    x, wts, bs = _vgg_inputs(n, hw, 15, layers)
+    dy_top = synth.normal((n, 512, 1, 1), 15, synth.TID.DY_TOP)
+    # The stack's inputs as the GPU holds them (bf16 values).
+    x = O.round_bf16(x)
+    wts = [O.round_bf16(w) for w in wts]
+    dy_top = O.round_bf16(dy_top)
+    st = ConvStack(configs.VGG16, n, 3, hw, "bf16")
+    st.load_inputs(x, wts, bs, dy_top)
+    st.step()
+    torch.cuda.synchronize()
+    pools = [L.pool_after for L in layers]
+    f, b = OS.vgg_step(x, wts, bs, pools, dy_top, bf16=True)
+    tol = TOL["bf16"]
+    deepest_flip = -1
+    for L in layers:
+        i = L.index
+        if L.pool_after:
+            z = f["Z"][i]
+            assert rel_l2(to_host(st.Z[i]), z) <= tol, "Z%d" % i
+            # Differing codes must be near-ties: within two bf16 steps.
+            eps = 2.0 ** -6 * np.max(np.abs(z))
+            if _near_ties(z, f["idx"][i], st.idx[i].cpu().numpy(), eps):
+                deepest_flip = i
+        assert rel_l2(to_host(st.A[i + 1]), f["A"][i + 1]) <= tol, "A%d" % (i + 1)
+    for L in layers:
+        i = L.index
+        bound = tol if i > deepest_flip else 0.5
+        assert rel_l2(to_host(st.grad_at_conv_output(i)), b["dZ"][i]) <= bound, "dZ%d" % i
+        assert rel_l2(to_host(st.dW[i]), b["dW"][i]) <= bound, "dW%d" % i
+        assert rel_l2(to_host(st.db[i]), b["db"][i]) <= bound, "db%d" % i
+    bound = tol if deepest_flip < 0 else 0.5
+    assert rel_l2(to_host(st.gA[0]), b["dX"]) <= bound
+
+
+def test_vgg16_imagenet_bf16_stack_full_size_properties():
+    """The whole ImageNet-shaped bf16 stack (batch 32, 224x224) through one
+    step: every pool output and code is consistent with the stored
+    pre-activation (y = max(0, window max), first maximum, ReLU flag), the
+    un-pooled gradient routes exactly, and every gradient is finite."""
+    n, hw = 32, 224
+    print_case("vgg16_imagenet_bf16_stack", n=n, hw=hw)
+    layers = configs.conv_layers(configs.VGG16, 3, hw)
+    x, wts, bs = _vgg_inputs(n, hw, 21, layers)
+    dy_top = synth.normal((n, 512, 7, 7), 21, synth.TID.DY_TOP)
+    st = ConvStack(configs.VGG16, n, 3, hw, "bf16")
+    st.load_inputs(x, wts, bs, dy_top)
+    st.step()
+    torch.cuda.synchronize()
+    for L in layers:
+        i = L.index
+        assert torch.isfinite(st.dW[i]).all() and torch.isfinite(st.db[i]).all(), "dW%d" % i
+        if not L.pool_after:
+            continue
+        z = st.Z[i].float()
+        nn_, c, h, w = z.shape
+        win = z.reshape(nn_, c, h // 2, 2, w // 2, 2).permute(0, 1, 2, 4, 3, 5).reshape(
+            nn_, c, h // 2, w // 2, 4)
+        mx = win.max(dim=-1).values
+        is_max = win == mx.unsqueeze(-1)
+        first = torch.argmax(is_max.to(torch.float32), dim=-1)
+        code = first.to(torch.uint8) | ((mx <= 0).to(torch.uint8) << 7)
+        assert torch.equal(st.idx[i], code), "pool code %d" % i
+        assert torch.equal(st.A[i + 1].float(), torch.clamp(mx, min=0)), "pool value %d" % i
+        del win, is_max, z
+        g = st.gA[i + 1].float().unsqueeze(-1)
+        sel = (torch.arange(4, device=g.device) == first.unsqueeze(-1)) & (mx > 0).unsqueeze(-1)
+        dz = torch.where(sel, g, torch.zeros_like(g)).reshape(nn_, c, h // 2, w // 2, 2, 2)
+        dz = dz.permute(0, 1, 2, 4, 3, 5).reshape(nn_, c, h, w)
+        assert torch.equal(st.dZ[i].float(), dz), "pool gradient routing %d" % i
+        del g, sel, dz
 
 
 def test_hybrid_worker_step_end_to_end():
