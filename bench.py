@@ -1,28 +1,52 @@
-"""Benchmark: one worker's VGG-16 CIFAR conv stack step on one MI355X.
+"""Benchmark: one SplitBrain worker's compute share on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+                    [--workload vgg16-cifar-f32 | vgg16-imagenet-bf16 |
+                                fc-shard-f32 | hybrid-f32]
+                    [--profile-pass]
 
-A step is the full forward and backward of the 13-layer VGG-16 conv stack on
-a batch of 128 synthetic 3x32x32 images in fp32 (conv fwd with fused ReLU,
-fused ReLU + 2x2 maxpool fwd/bwd, data and weight gradients of every layer,
-including the first layer's data gradient), with every input resident in
-HBM.  The step is ~60 short kernel launches, so it is captured once in a HIP
-graph (through torch.cuda.graph: libsb enqueues on the current stream) and
-the timed region is one replay of a graph of K steps, bracketed by HIP events.
+Default workload (the headline): one step of the 13-layer VGG-16 conv stack,
+forward and backward (conv fwd with fused ReLU, fused ReLU + 2x2 maxpool
+fwd/bwd, data and weight gradients of every layer, including the first
+layer's data gradient), on a batch of 128 synthetic 3x32x32 images in fp32,
+every input resident in HBM.  Other workloads:
 
-Prints one JSON line: `value` is images/s; the line also carries the
-achieved TFLOP/s (nominal 2*N*K*C*9*H*W per pass, and the valid-tap count
-that leaves out padded taps), a per-call duration table, the roofline of the
-dominant kernel and the fp64 CPU oracle's rate on a small sample of the same
-workload.  Per-call durations come from a second timed region: each call of
-the step captured K times back to back in its own graph, replayed between
-two HIP events on the stream the kernels run on.
+  vgg16-imagenet-bf16  the same stack on 32 images of 3x224x224, bf16
+                       activations and filters, fp32 accumulation;
+  fc-shard-f32         one FC column shard, forward and backward, on a
+                       gathered batch of 512 rows: X 512x4096, the shard's
+                       1024 of 4096 output columns;
+  hybrid-f32           the worker step: the VGG-16 CIFAR stack on 128 local
+                       images, FC0 (512 -> 1024 of 4096, ReLU) and FC1 (4096
+                       -> 1024 of 4096) shards on the gathered batch of 512,
+                       then backward through both.
+
+A step is one or several dozen kernel launches, so it is captured once in a
+HIP graph (through torch.cuda.graph: libsb enqueues on the current stream)
+and the timed region is one replay of a graph of K steps, bracketed by HIP
+events on that stream.
+
+Prints one JSON line: `value` is images/s (TFLOP/s for the FC shard alone);
+the line carries the achieved TFLOP/s (nominal 2*N*K*C*9*H*W per conv pass;
+the valid-tap count leaves out padded taps), a per-call duration table, the
+roofline of the dominant kernel and the fp64 CPU oracle's rate on a sample
+of the same workload.  Per-call durations come from a second timed region:
+each call of the step captured K times back to back in a graph of its own,
+replayed between two HIP events on the stream the kernels run on.
+
+--profile-pass runs W + K plain (eager, ungraphed) steps and then three
+copies of a 256 MiB buffer, and prints a one-line summary: the program that
+hardware-counter runs of the profiler measure (the copy is the reference of
+known size that scales the HBM byte counters).
 """
 from __future__ import annotations
 
 import argparse
+import glob
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -30,8 +54,14 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
-PEAK_FP32_MFMA_TFLOPS = 157.3      # MI355X dense fp32 matrix peak (256 CU x 2.4 GHz x 256 FLOP/clk)
+# MI355X published dense peaks (no sparsity) and HBM bandwidth.
+PEAK_MFMA_TFLOPS = {"f32": 157.3, "bf16": 2500.0}
 PEAK_HBM_GBS = 8000.0
+COPY_MIB = 256
+
+CIFAR_METRIC = "images/sec/GPU VGG-CIFAR conv fwd+bwd; achieved TFLOP/s vs MFMA peak"
+FC_SHAPE = (512, 4096, 1024, 4096)            # gathered rows, k_in, shard columns, full columns
+HYBRID_FC = [(512, 4096), (4096, 4096)]       # (in, out) of FC0, FC1; 4 replicas, 4 shards
 
 
 def layer_flops(L, n):
@@ -42,7 +72,7 @@ def layer_flops(L, n):
     return valid, nominal
 
 
-def pool_bytes(L, n, esize=4):
+def pool_bytes(L, n, esize):
     """Algorithmic HBM bytes of one fused ReLU + maxpool pass: per 2x2 window
     4 inputs + 1 output + 1 code byte (fwd), or 1 input + 1 code + 4 outputs
     (bwd) -- 5 elements + 1 byte either way."""
@@ -50,46 +80,286 @@ def pool_bytes(L, n, esize=4):
     return windows * (5 * esize + 1)
 
 
-def cpu_baseline(sample_n):
-    """Time the fp64 oracle on `sample_n` images of the same VGG-16 step."""
+def fc_flops(desc, kind, has_dx=True):
+    """FLOPs of an FC shard call: 2*m*k_in*n_shard per product."""
+    one = 2 * desc.m * desc.k_in * desc.n_shard
+    return one if kind == "fc_fwd" else one * (2 if has_dx else 1)
+
+
+def csrc_digest():
+    """sha256 over the HIP sources: a stored counter reading is only valid
+    for the kernels it was taken on."""
+    h = hashlib.sha256()
+    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2112_15317_amd", "csrc", "*"))):
+        h.update(os.path.basename(f).encode())
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def stored_traffic(kernel, workload):
+    """HBM bytes per launch of `kernel` from the committed counter summaries
+    (FETCH_SIZE + WRITE_SIZE, scaled by a plain copy of known size), or None
+    when there is no reading or the kernels changed since it was taken."""
+    digest = csrc_digest()
+    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*hbm_traffic*.md"))):
+        with open(path) as fh:
+            text = fh.read()
+        m = re.search(r"^csrc_sha256: *([0-9a-f]+)", text, re.M)
+        w = re.search(r"^workload: *(\S+)", text, re.M)
+        if not m or m.group(1) != digest or not w or w.group(1) != workload:
+            continue
+        col = None
+        for line in text.splitlines():
+            if not line.startswith("|"):
+                continue
+            cells = [c.strip().strip("`") for c in line.strip().strip("|").split("|")]
+            if "traffic_bytes_per_launch" in cells:
+                col = cells.index("traffic_bytes_per_launch")
+            elif col is not None and len(cells) > col and cells[0] == kernel:
+                return int(cells[col])
+    return None
+
+
+# ----------------------------------------------------------------- inputs --
+def vgg_inputs(n, hw, top):
     import numpy as np
-    import oracle
-    from oracle import stack as OS
     from paper_2112_15317_amd import configs, synth
-    layers = configs.conv_layers(configs.VGG16, 3, 32)
-    x = synth.normal((sample_n, 3, 32, 32), 0, synth.TID.IMAGES)
+    layers = configs.conv_layers(configs.VGG16, 3, hw)
+    x = synth.normal((n, 3, hw, hw), 0, synth.TID.IMAGES)
     ws = [synth.he_normal_conv3x3(L.k, L.c, 0, synth.TID.CONV_W + L.index) for L in layers]
     bs = [np.zeros(L.k, np.float32) for L in layers]
-    dy = synth.normal((sample_n, 512, 1, 1), 0, synth.TID.DY_TOP)
-    pools = [L.pool_after for L in layers]
-    t0 = time.perf_counter()
-    OS.vgg_step(x, ws, bs, pools, dy)
-    dt = time.perf_counter() - t0
-    return {"value": round(sample_n / dt, 3), "unit": "images/s", "cores": oracle.num_threads(),
-            "kind": "oracle",
-            "sample": "%d images of the same VGG-16 CIFAR fwd+bwd step (fp64 oracle), %.1f s"
-                      % (sample_n, dt)}
+    dy = synth.normal((n, 512, top, top), 0, synth.TID.DY_TOP)
+    return layers, x, ws, bs, dy
 
 
-def kernel_name(key, call_args):
-    """Name of the main kernel a step call launches (as a profiler shows it)."""
+def fc_inputs(rows=None):
+    import numpy as np
+    from paper_2112_15317_amd import synth
+    m, kin, ns, nfull = FC_SHAPE
+    m = rows or m
+    x = synth.relu_normal((m, kin), 0, synth.TID.FC_X)
+    w = np.ascontiguousarray(synth.xavier_uniform(kin, nfull, 0, synth.TID.FC_W)[:, :ns])
+    b = np.zeros(ns, np.float32)
+    dy = synth.normal((m, ns), 0, synth.TID.FC_DY)
+    return x, w, b, dy
+
+
+def hybrid_inputs(n):
+    import numpy as np
+    from paper_2112_15317_amd import synth
+    layers, x, ws, bs, _ = vgg_inputs(n, 32, 1)
+    (in0, out0), (in1, out1) = HYBRID_FC
+    R = S = 4
+    m, ns0, ns1 = n * R, out0 // S, out1 // S
+    w0 = np.ascontiguousarray(synth.xavier_uniform(in0, out0, 0, synth.TID.FC_W + 0)[:, :ns0])
+    w1 = np.ascontiguousarray(synth.xavier_uniform(in1, out1, 0, synth.TID.FC_W + 1)[:, :ns1])
+    b0, b1 = np.zeros(ns0, np.float32), np.zeros(ns1, np.float32)
+    x0r = synth.relu_normal((m - n, in0), 0, synth.TID.X0_REMOTE)
+    x1r = synth.relu_normal((m, in1 - ns0), 0, synth.TID.X1_REMOTE)
+    dy1 = synth.normal((m, ns1), 0, synth.TID.FC_DY)
+    return layers, x, ws, bs, w0, b0, w1, b1, x0r, x1r, dy1
+
+
+# --------------------------------------------------------------- workloads --
+class Workload:
+    """What a benchmark run needs: the step's calls, its work, its baseline."""
+    name = text = metric = dtype = None
+    images = 0            # images per step (0: not an image workload)
+    layers = ()
+
+    def build(self):      # -> list of (key, libsb fn, args)
+        raise NotImplementedError
+
+    def flops(self):      # -> {"nominal": F, "valid": F}
+        raise NotImplementedError
+
+    def cpu_baseline(self, sample):
+        raise NotImplementedError
+
+
+class VggWorkload(Workload):
+    def __init__(self, name, batch, hw, dtype, metric, text):
+        self.name, self.n, self.hw, self.dtype = name, batch, hw, dtype
+        self.metric, self.text, self.images = metric, text, batch
+        self.top = hw // 32
+
+    def build(self):
+        from paper_2112_15317_amd import configs
+        from paper_2112_15317_amd.stack import ConvStack
+        self.layers, x, ws, _, dy = vgg_inputs(self.n, self.hw, self.top)
+        self.st = ConvStack(configs.VGG16, self.n, 3, self.hw, self.dtype)
+        self.st.load_inputs(x, ws, None, dy)
+        return self.st.step_calls()
+
+    def flops(self):
+        from paper_2112_15317_amd import configs
+        return configs.stack_flops(self.layers, self.n)
+
+    def cpu_baseline(self, sample):
+        import oracle
+        from oracle import stack as OS
+        sample = sample or (self.n if self.hw <= 32 else 8)
+        layers, x, ws, bs, dy = vgg_inputs(sample, self.hw, self.top)
+        bf16 = self.dtype == "bf16"
+        if bf16:
+            x = oracle.round_bf16(x)
+            ws = [oracle.round_bf16(w) for w in ws]
+            dy = oracle.round_bf16(dy)
+        pools = [L.pool_after for L in layers]
+        reps = 3 if self.hw <= 32 else 1
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            OS.vgg_step(x, ws, bs, pools, dy, bf16=bf16)
+        dt = time.perf_counter() - t0
+        return {"value": round(reps * sample / dt, 3), "unit": "images/s",
+                "cores": oracle.num_threads(), "kind": "oracle",
+                "sample": "%d x the fwd+bwd step on %d images (fp64 oracle%s), %.1f s"
+                          % (reps, sample, ", bf16 rounding at storage points" if bf16 else "",
+                             dt)}
+
+
+class FcWorkload(Workload):
+    name = "fc-shard-f32"
+    dtype = "f32"
+    metric = "TFLOP/s FC column shard fwd+bwd on the gathered batch (fp32)"
+    text = ("FC column shard fwd+bwd: X 512x4096 gathered rows, W_shard 4096x1024 "
+            "(1024 of 4096 output columns), partial dX 512x4096, dW 4096x1024, fp32")
+
+    def build(self):
+        import torch
+        from paper_2112_15317_amd.stack import FCShard
+        m, kin, ns, _ = FC_SHAPE
+        x, w, b, dy = fc_inputs()
+        self.fc = FCShard(m, kin, ns)
+        t = lambda a: torch.from_numpy(a).cuda()
+        self.x, self.dy = t(x), t(dy)
+        self.fc.W.copy_(t(w))
+        self.fc.b.copy_(t(b))
+        self.y = torch.empty((m, ns), device="cuda")
+        self.dx = torch.empty((m, kin), device="cuda")
+        return [(("fc_fwd", 0),) + self.fc.fwd_call(self.x, self.y),
+                (("fc_bwd", 0),) + self.fc.bwd_call(self.x, self.dy, None, self.dx)]
+
+    def flops(self):
+        f = fc_flops(self.fc.desc_f, "fc_fwd") + fc_flops(self.fc.desc_b, "fc_bwd")
+        return {"nominal": f, "valid": f}
+
+    def cpu_baseline(self, sample):
+        import oracle
+        sample = sample or FC_SHAPE[0]
+        x, w, b, dy = fc_inputs(sample)
+        reps = 3
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            oracle.fc_fwd(x, w, b)
+            oracle.fc_bwd(x, w, dy)
+        dt = time.perf_counter() - t0
+        f = reps * 6 * sample * FC_SHAPE[1] * FC_SHAPE[2]
+        return {"value": round(f / dt / 1e12, 5), "unit": "TFLOP/s",
+                "cores": oracle.num_threads(), "kind": "oracle",
+                "sample": "%d x fwd+bwd of the shard on %d gathered rows (fp64 oracle), %.1f s"
+                          % (reps, sample, dt)}
+
+
+class HybridWorkload(Workload):
+    name = "hybrid-f32"
+    dtype = "f32"
+    images = 128
+    metric = "images/sec/GPU hybrid worker step (VGG-16 CIFAR conv DP + FC shards MP), fp32"
+    text = ("hybrid worker step: VGG-16 CIFAR conv stack on 128 local images, then FC0 512->1024 "
+            "(of 4096, ReLU) and FC1 4096->1024 (of 4096) shards on the gathered 512 rows, "
+            "fwd+bwd, fp32")
+
+    def build(self):
+        from paper_2112_15317_amd import configs
+        from paper_2112_15317_amd.stack import HybridStep
+        inp = hybrid_inputs(self.images)
+        self.layers = inp[0]
+        self.hs = HybridStep(configs.VGG16, self.images, 3, 32, 4, HYBRID_FC, 4)
+        self.hs.load_inputs(*inp[1:])
+        return self.hs.step_calls()
+
+    def flops(self):
+        from paper_2112_15317_amd import configs
+        f = configs.stack_flops(self.layers, self.images)
+        hs = self.hs
+        extra = sum(fc_flops(s.desc_f, "fc_fwd") + fc_flops(s.desc_b, "fc_bwd")
+                    for s in (hs.fc0, hs.fc1))
+        return {"nominal": f["nominal"] + extra, "valid": f["valid"] + extra}
+
+    def cpu_baseline(self, sample):
+        import oracle
+        from oracle import stack as OS
+        n = self.images
+        layers, x, ws, bs, w0, b0, w1, b1, x0r, x1r, dy1 = hybrid_inputs(n)
+        pools = [L.pool_after for L in layers]
+        reps = 1
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            OS.hybrid_step(x, ws, bs, pools, w0, b0, w1, b1, x0r, x1r, dy1)
+        dt = time.perf_counter() - t0
+        return {"value": round(reps * n / dt, 3), "unit": "images/s",
+                "cores": oracle.num_threads(), "kind": "oracle",
+                "sample": "%d x the whole hybrid step, %d local images (fp64 oracle), %.1f s"
+                          % (reps, n, dt)}
+
+
+def workloads():
+    return {
+        "vgg16-cifar-f32": VggWorkload(
+            "vgg16-cifar-f32", 128, 32, "f32", CIFAR_METRIC,
+            "VGG-16 CIFAR conv stack fwd+bwd (13 conv, 5 relu+maxpool), batch 128, 3x32x32, "
+            "fp32, NCHW"),
+        "vgg16-imagenet-bf16": VggWorkload(
+            "vgg16-imagenet-bf16", 32, 224, "bf16",
+            "images/sec/GPU VGG-16 ImageNet-shaped conv fwd+bwd (bf16); achieved TFLOP/s vs "
+            "MFMA peak",
+            "VGG-16 ImageNet-shaped conv stack fwd+bwd (13 conv, 5 relu+maxpool), batch 32, "
+            "3x224x224, bf16 activations and filters, fp32 accumulation, NCHW"),
+        "fc-shard-f32": FcWorkload(),
+        "hybrid-f32": HybridWorkload(),
+    }
+
+
+def kernel_name(key, call_args, dtype):
+    """Name of the main kernel a step call launches (as a profiler shows it);
+    FC calls launch several GEMMs and are grouped by call."""
     from paper_2112_15317_amd import sb
-    kind, _ = key
+    kind, j = key
     if kind in ("fwd", "dgrad", "wgrad"):
         p = {"fwd": sb.SB_PASS_FWD, "dgrad": sb.SB_PASS_BWD_DATA,
              "wgrad": sb.SB_PASS_BWD_WEIGHT}[kind]
         return sb.sb_conv3x3_plan_string(call_args[0], p)
-    return "sb::relu_maxpool_%s_kernel<float, 2>" % kind.split("_")[1]
+    if kind.startswith("fc_"):
+        d = call_args[0]
+        return "sb_fc_shard_%s m=%d k_in=%d n_shard=%d" % (kind[3:], d.m, d.k_in, d.n_shard)
+    return "sb::relu_maxpool_%s_kernel<%s, 2>" % (
+        kind.split("_")[1], "float" if dtype == "f32" else "unsigned short")
+
+
+def call_work(wl, key, args):
+    """Algorithmic work of one call: (amount, 'flop' | 'bytes')."""
+    kind, i = key
+    if kind in ("fwd", "dgrad", "wgrad"):
+        return layer_flops(wl.layers[i], args[0].n)[0], "flop"
+    if kind.startswith("fc_"):
+        return fc_flops(args[0], kind, kind == "fc_fwd" or args[5] is not None), "flop"
+    esize = 4 if wl.dtype == "f32" else 2
+    return pool_bytes(wl.layers[i], args[0], esize), "bytes"
 
 
 def main():
+    W = workloads()
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--batch", type=int, default=128)
+    ap.add_argument("--workload", choices=sorted(W), default="vgg16-cifar-f32")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample", type=int, default=16)
+    ap.add_argument("--cpu-sample", type=int, default=None,
+                    help="images (rows for the FC shard) the oracle times")
+    ap.add_argument("--profile-pass", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: this library has no multi-GPU path "
@@ -97,22 +367,32 @@ def main():
         sys.exit(2)
 
     import torch
-    from paper_2112_15317_amd import configs, synth
-    from paper_2112_15317_amd.stack import ConvStack, capture_graph
+    from paper_2112_15317_amd.stack import capture_graph
 
+    wl = W[args.workload]
+    dtype = wl.dtype
     torch.cuda.set_device(0)
-    n, K = args.batch, args.steps
-    layers = configs.conv_layers(configs.VGG16, 3, 32)
-    st = ConvStack(configs.VGG16, n, 3, 32, "f32")
-    x = synth.normal((n, 3, 32, 32), 0, synth.TID.IMAGES)
-    ws = [synth.he_normal_conv3x3(L.k, L.c, 0, synth.TID.CONV_W + L.index) for L in layers]
-    dy = synth.normal((n, 512, 1, 1), 0, synth.TID.DY_TOP)
-    st.load_inputs(x, ws, None, dy)
-    calls = st.step_calls()
+    K = args.steps
+    calls = wl.build()
 
     def run_step():
         for _, fn, a in calls:
             fn(*a)
+
+    if args.profile_pass:
+        for _ in range(args.warmup + K):
+            run_step()
+        torch.cuda.synchronize()
+        a = torch.empty(COPY_MIB << 18, dtype=torch.float32, device="cuda")
+        b = torch.empty_like(a)
+        a.fill_(1.0)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        print(json.dumps({"profile_pass": args.workload, "steps": args.warmup + K,
+                          "copy_bytes": COPY_MIB << 20, "csrc_sha256": csrc_digest()}),
+              flush=True)
+        return
 
     for _ in range(args.warmup):
         run_step()
@@ -130,6 +410,7 @@ def main():
     ev1.record()
     torch.cuda.synchronize()
     ms = ev0.elapsed_time(ev1) / K
+    del g
 
     # Timed region 2: every call of the step, K launches back to back in a
     # graph of its own, between two events -> average duration per launch.
@@ -145,52 +426,58 @@ def main():
         per_call[key] = ev0.elapsed_time(ev1) / K
         del gc
 
-    fl = configs.stack_flops(layers, n)
+    fl = wl.flops()
+    peak = PEAK_MFMA_TFLOPS[dtype]
     tf_nom = fl["nominal"] / (ms * 1e-3) / 1e12
     tf_valid = fl["valid"] / (ms * 1e-3) / 1e12
 
     # Group the calls by kernel; the dominant kernel has the largest time per step.
     groups = {}
     for key, fn, a in calls:
-        name = kernel_name(key, a)
+        name = kernel_name(key, a, dtype)
         base = name.split(" grid=")[0]
-        kind, i = key
-        L = layers[i]
-        work = layer_flops(L, n)[0] if kind in ("fwd", "dgrad", "wgrad") else pool_bytes(L, n)
-        gr = groups.setdefault(base, {"ms": 0.0, "work": 0, "calls": [], "split": False})
+        work, unit = call_work(wl, key, a)
+        gr = groups.setdefault(base, {"ms": 0.0, "work": 0, "unit": unit, "calls": [],
+                                      "split": False})
         gr["ms"] += per_call[key]
         gr["work"] += work
-        gr["calls"].append("%s%d" % (kind, i + 1))
-        gr["split"] |= "+" in name
+        gr["calls"].append("%s%d" % (key[0], key[1] + 1))
+        gr["split"] |= bool(re.search(r"grid=\d+x\d+x([2-9]|\d\d)", name))
     dom = max(groups, key=lambda k: groups[k]["ms"])
     G = groups[dom]
-    avg_us = G["ms"] * 1e3 / len(G["calls"])
-    if "relu_maxpool" in dom:
+    launches = len(G["calls"])
+    avg_us = G["ms"] * 1e3 / launches
+    if G["unit"] == "bytes":
         achieved = G["work"] / (G["ms"] * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
                 "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4)}
     else:
         achieved = G["work"] / (G["ms"] * 1e-3) / 1e12
-        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_FP32_MFMA_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(achieved / PEAK_FP32_MFMA_TFLOPS, 4)}
-    roof.update({"traffic": None, "kernel": dom, "calls": G["calls"],
-                 "avg_us": round(avg_us, 2), "work_per_step": G["work"],
+        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak,
+                "unit": "TFLOP/s", "frac": round(achieved / peak, 4)}
+    roof.update({"traffic": stored_traffic(dom, wl.name), "kernel": dom,
+                 "calls": G["calls"], "avg_us": round(avg_us, 2),
+                 "work_per_launch": G["work"] // launches,
+                 "work_unit": "bytes" if G["unit"] == "bytes" else "valid-tap FLOP",
                  "includes_split_reduce": G["split"]})
 
+    if wl.images:
+        value, unit = round(wl.images / (ms * 1e-3), 1), "images/s"
+    else:
+        value, unit = round(tf_nom, 2), "TFLOP/s"
     out = {
-        "metric": "images/sec/GPU VGG-CIFAR conv fwd+bwd; achieved TFLOP/s vs MFMA peak",
-        "value": round(n / (ms * 1e-3), 1),
-        "unit": "images/s",
+        "metric": wl.metric,
+        "value": value,
+        "unit": unit,
         "n_gpus": 1, "steps": K, "warmup": args.warmup,
         "ms_per_step": round(ms, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "f32", "data": "synthetic",
-        "config": {"workload": "VGG-16 CIFAR conv stack fwd+bwd (13 conv, 5 relu+maxpool), "
-                               "batch 128, 3x32x32, fp32, NCHW",
-                   "global_batch": n, "seq_len": None, "parallelism": "none (1 GPU)"},
+        "dtype": dtype, "data": "synthetic",
+        "config": {"workload": wl.text, "global_batch": wl.images or FC_SHAPE[0],
+                   "parallelism": "none (1 GPU)"},
         "launch": "HIP graph of %d steps" % K,
         "tflops_nominal": round(tf_nom, 2), "tflops_valid_tap": round(tf_valid, 2),
-        "frac_fp32_mfma_peak_nominal": round(tf_nom / PEAK_FP32_MFMA_TFLOPS, 4),
+        "frac_mfma_peak_nominal": round(tf_nom / peak, 4),
         "roofline": roof,
         "sum_of_calls_ms": round(sum(per_call.values()), 4),
         "per_call_us": {"%s%d" % (k[0], k[1] + 1): round(v * 1e3, 1) for k, v in per_call.items()},
@@ -198,7 +485,7 @@ def main():
                                    sorted(groups.items(), key=lambda kv: -kv[1]["ms"])},
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(args.cpu_sample)
+        out["cpu_baseline"] = wl.cpu_baseline(args.cpu_sample)
     print(json.dumps(out), flush=True)
 
 

@@ -29,31 +29,6 @@ def _code(dtype: str):
     return {"f32": sb.SB_F32, "bf16": sb.SB_BF16}[dtype]
 
 
-class EventTimer:
-    """Brackets calls with HIP events on the current stream; per-key lists of
-    (start, stop) pairs are read after a synchronisation."""
-
-    def __init__(self, external=False):
-        # external=True: the events become record nodes of a captured graph
-        # and are stamped at every replay.
-        self.events = {}
-        self.external = external
-
-    def __call__(self, key, fn, *args):
-        s = torch.cuda.Event(enable_timing=True, external=self.external)
-        e = torch.cuda.Event(enable_timing=True, external=self.external)
-        s.record()
-        fn(*args)
-        e.record()
-        self.events.setdefault(key, []).append((s, e))
-
-    def mean_ms(self):
-        return {k: sum(s.elapsed_time(e) for s, e in v) / len(v) for k, v in self.events.items()}
-
-    def total_ms(self):
-        return {k: sum(s.elapsed_time(e) for s, e in v) for k, v in self.events.items()}
-
-
 def _plain(key, fn, *args):
     fn(*args)
 
@@ -128,9 +103,9 @@ class ConvStack:
                        sb.sb_conv3x3_workspace_bytes(self.desc[l.index], sb.SB_PASS_FWD),
                        sb.sb_conv3x3_workspace_bytes(self.desc_b[l.index], sb.SB_PASS_BWD_DATA),
                        sb.sb_conv3x3_workspace_bytes(self.desc_b[l.index], sb.SB_PASS_BWD_WEIGHT))
-        # Zero-filled once: libsb's split-reduction counters live at its start.
+        # Split-reduction scratch; needs no initialisation.
         self.ws = torch.empty((max(need, 256) + 255) // 256 * 256, dtype=torch.uint8, device=dev)
-        self.call = _plain      # replace with an EventTimer to time each call
+        self.call = _plain      # hook: every libsb call of the step goes through it
 
     # -- data placement (host -> device copies of seeded inputs) --------------
     def load_inputs(self, x, weights, biases=None, dy_top=None):
@@ -216,15 +191,25 @@ class FCShard:
         self.db = torch.empty((ns,), dtype=torch.float32, device=dev)
         need = max(sb.sb_fc_workspace_bytes(self.desc_f, sb.SB_FC_FWD),
                    sb.sb_fc_workspace_bytes(self.desc_b, sb.SB_FC_BWD))
-        # Zero-filled once: libsb's split-reduction counters live at its start.
+        # Split-reduction scratch; needs no initialisation.
         self.ws = torch.empty((max(need, 256) + 255) // 256 * 256, dtype=torch.uint8, device=dev)
 
+    def fwd_call(self, x_ptr, y_ptr, stream=None):
+        """(libsb function, args) of the forward."""
+        return sb.sb_fc_shard_fwd, (self.desc_f, x_ptr, self.W, self.b, y_ptr, self.ws, stream)
+
+    def bwd_call(self, x_ptr, dy_ptr, mask_ptr, dx_ptr, accumulate=False, stream=None):
+        """(libsb function, args) of the backward."""
+        return sb.sb_fc_shard_bwd, (self.desc_b, x_ptr, self.W, dy_ptr, mask_ptr, dx_ptr,
+                                    self.dW, self.db, accumulate, self.ws, stream)
+
     def forward(self, x_ptr, y_ptr, stream=None):
-        sb.sb_fc_shard_fwd(self.desc_f, x_ptr, self.W, self.b, y_ptr, self.ws, stream)
+        fn, args = self.fwd_call(x_ptr, y_ptr, stream)
+        fn(*args)
 
     def backward(self, x_ptr, dy_ptr, mask_ptr, dx_ptr, accumulate=False, stream=None):
-        sb.sb_fc_shard_bwd(self.desc_b, x_ptr, self.W, dy_ptr, mask_ptr, dx_ptr, self.dW,
-                           self.db, accumulate, self.ws, stream)
+        fn, args = self.bwd_call(x_ptr, dy_ptr, mask_ptr, dx_ptr, accumulate, stream)
+        fn(*args)
 
 
 class HybridStep:
@@ -260,6 +245,7 @@ class HybridStep:
         assert int(np.prod(top.shape[1:])) == in0
         self.fc0 = FCShard(m, in0, ns0, relu=True, ldx=in0, ldy=in1, device=device)
         self.fc1 = FCShard(m, in1, ns1, relu=False, ldx=in1, ldy=ns1, device=device)
+        self.call = _plain      # hook: every libsb call of the step goes through it
 
     def load_inputs(self, x, conv_w, conv_b, fc0_w, fc0_b, fc1_w, fc1_b, x0_remote, x1_remote,
                     dy1):
@@ -272,11 +258,27 @@ class HybridStep:
         self.dY1.copy_(t(dy1))
 
     def step(self, stream=None):
+        def c(key, call):
+            fn, args = call
+            self.call(key, fn, *args)
         self.conv.forward(stream)
         X0, X1 = self.X0.data_ptr(), self.X1.data_ptr()
-        self.fc0.forward(X0, X1, stream)                       # Y0 -> X1[:, :ns0]
-        self.fc1.forward(X1, self.Y1.data_ptr(), stream)
-        self.fc1.backward(X1, self.dY1.data_ptr(), None, self.dX1p.data_ptr(), stream=stream)
+        c(("fc_fwd", 0), self.fc0.fwd_call(X0, X1, stream))          # Y0 -> X1[:, :ns0]
+        c(("fc_fwd", 1), self.fc1.fwd_call(X1, self.Y1.data_ptr(), stream))
+        c(("fc_bwd", 1), self.fc1.bwd_call(X1, self.dY1.data_ptr(), None,
+                                           self.dX1p.data_ptr(), stream=stream))
         # FC0's output gradient: dX1p[:, :ns0] (row stride in1), ReLU mask X1[:, :ns0].
-        self.fc0.backward(X0, self.dX1p.data_ptr(), X1, self.dX0p.data_ptr(), stream=stream)
+        c(("fc_bwd", 0), self.fc0.bwd_call(X0, self.dX1p.data_ptr(), X1,
+                                           self.dX0p.data_ptr(), stream=stream))
         self.conv.backward(stream)
+
+    def step_calls(self):
+        """The ordered (key, libsb function, args) calls of one step."""
+        rec = []
+        saved = self.call, self.conv.call
+        self.call = self.conv.call = lambda key, fn, *args: rec.append((key, fn, args))
+        try:
+            self.step()
+        finally:
+            self.call, self.conv.call = saved
+        return rec
