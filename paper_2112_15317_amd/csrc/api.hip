@@ -4,7 +4,7 @@
 #include "sb_internal.hpp"
 
 namespace sbh {
-size_t conv_igemm_ws(int N, int Cin, int H, int W, int Cout);
+size_t conv_igemm_ws(int dtype, int N, int Cin, int H, int W, int Cout);
 sb_status conv_igemm(bool dgrad, int dtype, int N, int Cin, int H, int W, int Cout,
                      const void* in, const void* wt, const float* bias, const void* mask,
                      void* out, void* ws, size_t ws_bytes, int relu, hipStream_t st);
@@ -46,8 +46,8 @@ extern "C" size_t sb_conv3x3_workspace_bytes(const sb_conv3x3_desc* d, int pass)
   if (pass < SB_PASS_FWD || pass > SB_PASS_BWD_WEIGHT) return (size_t)-1;
   if (conv_check(d, pass) != SB_OK) return (size_t)-1;
   switch (pass) {
-    case SB_PASS_FWD: return sbh::conv_igemm_ws(d->n, d->c, d->h, d->w, d->k);
-    case SB_PASS_BWD_DATA: return sbh::conv_igemm_ws(d->n, d->k, d->h, d->w, d->c);
+    case SB_PASS_FWD: return sbh::conv_igemm_ws(d->dtype, d->n, d->c, d->h, d->w, d->k);
+    case SB_PASS_BWD_DATA: return sbh::conv_igemm_ws(d->dtype, d->n, d->k, d->h, d->w, d->c);
     default: return sbh::conv_wgrad_ws(d->n, d->c, d->h, d->w, d->k);
   }
 }
@@ -67,9 +67,11 @@ extern "C" sb_status sb_conv3x3_fwd(const sb_conv3x3_desc* d, const void* x, con
   if (sbh::overlaps(y, yb, x, xb) || sbh::overlaps(y, yb, w, wb) ||
       sbh::overlaps(y, yb, bias, bias ? d->k * sizeof(float) : 0))
     return SB_ERR_INVALID_ARG;
-  size_t need = sbh::conv_igemm_ws(d->n, d->c, d->h, d->w, d->k);
+  size_t need = sbh::conv_igemm_ws(d->dtype, d->n, d->c, d->h, d->w, d->k);
   if (need && (!ws || ws_bytes < need)) return SB_ERR_WORKSPACE;
-  if (need && (sbh::overlaps(ws, need, x, xb) || sbh::overlaps(ws, need, y, yb)))
+  if (need && (sbh::overlaps(ws, need, x, xb) || sbh::overlaps(ws, need, y, yb) ||
+               sbh::overlaps(ws, need, w, wb) ||
+               sbh::overlaps(ws, need, bias, bias ? d->k * sizeof(float) : 0)))
     return SB_ERR_INVALID_ARG;
   return sbh::conv_igemm(false, d->dtype, d->n, d->c, d->h, d->w, d->k, x, w, bias, nullptr, y,
                          ws, ws_bytes, (d->flags & SB_FUSE_RELU) ? 1 : 0,
@@ -87,9 +89,10 @@ extern "C" sb_status sb_conv3x3_bwd_data(const sb_conv3x3_desc* d, const void* d
   if (sbh::overlaps(dx, dxb, dy, dyb) || sbh::overlaps(dx, dxb, w, wb) ||
       sbh::overlaps(dx, dxb, mask, mask ? dxb : 0))
     return SB_ERR_INVALID_ARG;
-  size_t need = sbh::conv_igemm_ws(d->n, d->k, d->h, d->w, d->c);
+  size_t need = sbh::conv_igemm_ws(d->dtype, d->n, d->k, d->h, d->w, d->c);
   if (need && (!ws || ws_bytes < need)) return SB_ERR_WORKSPACE;
   if (need && (sbh::overlaps(ws, need, dy, dyb) || sbh::overlaps(ws, need, dx, dxb) ||
+               sbh::overlaps(ws, need, w, wb) ||
                sbh::overlaps(ws, need, mask, mask ? dxb : 0)))
     return SB_ERR_INVALID_ARG;
   return sbh::conv_igemm(true, d->dtype, d->n, d->k, d->h, d->w, d->c, dy, w, nullptr, mask, dx,

@@ -50,12 +50,13 @@ namespace sb {
 struct ConvArgs {
   const void* in;        // [N][Cin][H][W]
   const void* wt;        // forward filters [K][C][3][3]
+  const void* wpk;       // the same, packed by filter_pack (workspace)
   const float* bias;     // [Cout] or null (forward)
   const void* mask;      // [N][Cout][H][W] or null (data gradient)
   void* out;             // [N][Cout][H][W]
   float* part;           // split partials [splits][N][Cout][H][W]
   int N, Cin, H, W, Cout;
-  int tiles_w, tiles_h, chunks_per_split, splits, relu;
+  int tiles_w, tiles_h, nchunks, chunks_per_split, splits, relu;
 };
 
 template <class E>
@@ -66,45 +67,48 @@ __device__ __forceinline__ float conv_epilogue(const ConvArgs& a, float v, int c
   return v;
 }
 
-// The filter slice lives in LDS as rows r = tap*CK + ci of BN_P floats
-// (BN_P = 16 mod 64), so the MFMA operand read (rows r..r+3, 16 consecutive
-// co per row) is conflict-free.  The staging writes, which follow the
-// global order for coalescing, do conflict; measured, that costs less than
-// the registers an XOR swizzle of the rows needs.
-//
-// Filter slice gather for one chunk: element e (0 <= e < 9*CK*BN), ordered
-// so that neighbouring threads read neighbouring global addresses.
-// Forward: global [co][ci][tap] -> LDS [tap][ci][co].  Data gradient: the
-// forward filters [k][c][tap] with k = this conv's input channel, global
-// order [ci][co][tap] -> LDS [8 - tap][ci][co] (the 180-degree rotation).
-template <bool DGRAD, int CK, int BN, int BN_P>
-__device__ __forceinline__ void filter_plan(int e, int co0, int Cin, int Cout, int& goff,
-                                            int& loff, int& ci) {
-  if (!DGRAD) {
-    int nn = e / (CK * 9), rem = e - nn * (CK * 9);
-    int cc = rem / 9, tap = rem - cc * 9;
-    int co = co0 + nn;
-    ci = cc;
-    goff = co < Cout ? (co * Cin + cc) * 9 + tap : -1;     // + chunk * CK * 9
-    loff = (tap * CK + cc) * BN_P + nn;
-  } else {
-    int kk = e / (BN * 9), rem = e - kk * (BN * 9);
-    int nn = rem / 9, tap = rem - nn * 9;
-    int co = co0 + nn;
-    ci = kk;
-    goff = co < Cout ? (kk * Cout + co) * 9 + tap : -1;    // + chunk * CK * Cout * 9
-    loff = ((8 - tap) * CK + kk) * BN_P + nn;
+// Filters are repacked before the convolution (filter_pack) into the order
+// the kernels stage them: for output-channel tile t (BN channels) and input-
+// channel chunk k (CK channels), 9*CK*BN contiguous elements ordered
+// [tap][ci][co], zero where a channel lies past the end.  For the data
+// gradient the same pass transposes (co <-> ci) and rotates the taps by 180
+// degrees.  A chunk's slice is then one coalesced read, and its LDS rows
+// r = tap*CK + ci (stride BN_P) are written by consecutive lanes along a row:
+// conflict-free, like the MFMA operand reads (rows r..r+3, 16 consecutive co
+// per row, BN_P = 16 mod 64).  The packed filters live in the workspace.
+template <bool DGRAD, int CK, int BN, class E>
+__global__ __launch_bounds__(256) void filter_pack(const E* __restrict__ w, E* __restrict__ out,
+                                                   int Cin, int Cout) {
+  // Cin, Cout: this convolution's input and output channels (for the data
+  // gradient: the forward layer's output and input channels).
+  const int nchunks = cdiv(Cin, CK);
+  const int slice = blockIdx.x;                       // co tile * nchunks + chunk
+  const int ct = slice / nchunks, kc = slice - ct * nchunks;
+  E* dst = out + (size_t)slice * (9 * CK * BN);
+  for (int e = threadIdx.x; e < 9 * CK * BN; e += 256) {
+    const int tap = e / (CK * BN), r = e - tap * (CK * BN);
+    const int cc = r / BN, nn = r - cc * BN;
+    const int co = ct * BN + nn, ci = kc * CK + cc;
+    E v{};
+    if (co < Cout && ci < Cin)
+      v = DGRAD ? w[((size_t)ci * Cout + co) * 9 + (8 - tap)] : w[((size_t)co * Cin + ci) * 9 + tap];
+    dst[e] = v;
   }
 }
 
-template <bool DGRAD, class E>
-__device__ __forceinline__ float filter_load(const ConvArgs& a, int goff, int ci_in_chunk,
-                                             int cbase) {
-  const int ci = cbase + ci_in_chunk;
-  const bool ok = goff >= 0 && ci < a.Cin;
-  const int idx = DGRAD ? goff + cbase * a.Cout * 9 : goff + cbase * 9;
-  const float v = Elem<E>::load((const E*)a.wt, ok ? idx : 0);
-  return ok ? v : 0.f;
+// Buffer resources of a block: its images of the input (from image n0 on)
+// and the whole filter tensor.
+template <class E>
+__device__ __forceinline__ rsrc_t input_rsrc(const ConvArgs& a, int n0, int imgs) {
+  const size_t img = (size_t)a.Cin * a.H * a.W;
+  const int cnt = min(imgs, a.N - n0);
+  return make_rsrc((const E*)a.in + n0 * img, (uint32_t)(cnt * img * sizeof(E)));
+}
+// The packed filter slices of output-channel tile `ct` (all chunks).
+template <class E, int WTS>
+__device__ __forceinline__ rsrc_t packed_rsrc(const ConvArgs& a, int ct) {
+  return make_rsrc((const E*)a.wpk + (size_t)ct * a.nchunks * WTS,
+                   (uint32_t)((size_t)a.nchunks * WTS * sizeof(E)));
 }
 
 // ----------------------------------------------------------------- generic --
@@ -127,7 +131,11 @@ struct ConvTile {
   static constexpr int WTS_PT = (WTS + 255) / 256;
   static constexpr int LDS_X = CK * PLANE_P;
   static constexpr int LDS_W = 9 * CK * BN_P;
-  static constexpr int LDS_BUF = LDS_X + LDS_W;
+  // Staging lanes past the end of the halo or filter slice store into a
+  // private slot after the two (256 floats), so every staging store is
+  // unconditional (no exec-mask juggling in the loop).
+  static constexpr int LDS_SPARE = 256;
+  static constexpr int LDS_BUF = LDS_X + LDS_W + LDS_SPARE;
   static constexpr size_t LDS_BYTES = 2 * LDS_BUF * sizeof(float);
   static_assert(LDS_BYTES <= 80 * 1024, "two blocks must fit in the 160 KB of LDS");
   // Waves split the tile 2 x 2 (BN >= 32) or 1 x 4 along pixels (BN = 16).
@@ -167,16 +175,16 @@ __global__ __launch_bounds__(256, 2) void conv3x3_igemm_f32(ConvArgs a) {
     int yy = r2 / T::HW, xx = r2 - yy * T::HW;
     int n = n0 + img, h = h0 + yy - 1, w = w0 + xx - 1;
     bool ok = live && n < a.N && h >= 0 && h < a.H && w >= 0 && w < a.W;
-    x_off[i] = ok ? n * a.Cin * HWs + h * a.W + w : -1;   // + ci * H*W
+    x_off[i] = ok ? img * a.Cin * HWs + h * a.W + w : -1;   // from image n0; + ci * H*W
     x_c[i] = c;
-    x_loff[i] = live ? c * T::PLANE_P + rem : -1;
+    x_loff[i] = live ? c * T::PLANE_P + rem : T::LDS_X + T::LDS_W + tid;
   }
-  int w_off[T::WTS_PT], w_loff[T::WTS_PT], w_ci[T::WTS_PT];
+  // Packed filter slice element e -> LDS row e / BN, column e % BN.
+  int w_loff[T::WTS_PT];
 #pragma unroll
   for (int i = 0; i < T::WTS_PT; ++i) {
     int e = tid + i * 256;
-    filter_plan<DGRAD, T::CK, T::BN, T::BN_P>(e, co0, a.Cin, a.Cout, w_off[i], w_loff[i], w_ci[i]);
-    if (e >= T::WTS) { w_off[i] = -1; w_loff[i] = -1; }
+    w_loff[i] = e < T::WTS ? (e / T::BN) * T::BN_P + e % T::BN : T::LDS_W + tid;
   }
   int pix_off[T::MB];
 #pragma unroll
@@ -193,6 +201,8 @@ __global__ __launch_bounds__(256, 2) void conv3x3_igemm_f32(ConvArgs a) {
 #pragma unroll
     for (int j = 0; j < T::MB; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
 
+  const rsrc_t xr = input_rsrc<E>(a, n0, T::IMGS);
+  const rsrc_t wr = packed_rsrc<E, T::WTS>(a, blockIdx.y);
   float rx[T::HALO_PT], rw[T::WTS_PT];
   auto gload = [&](int kc) {
     const int cbase = kc * T::CK;
@@ -200,21 +210,22 @@ __global__ __launch_bounds__(256, 2) void conv3x3_igemm_f32(ConvArgs a) {
     for (int i = 0; i < T::HALO_PT; ++i) {
       const int ci = cbase + x_c[i];
       const bool ok = x_off[i] >= 0 && ci < a.Cin;
-      const float v = Elem<E>::load((const E*)a.in, ok ? x_off[i] + ci * HWs : 0);
-      rx[i] = ok ? v : 0.f;
+      rx[i] = BufLoad<E>::one(xr, ok ? (uint32_t)(x_off[i] + ci * HWs) * (uint32_t)sizeof(E) : kOOB);
     }
 #pragma unroll
-    for (int i = 0; i < T::WTS_PT; ++i) rw[i] = filter_load<DGRAD, E>(a, w_off[i], w_ci[i], cbase);
+    for (int i = 0; i < T::WTS_PT; ++i) {
+      const int e = tid + i * 256;
+      rw[i] = BufLoad<E>::one(wr, e < T::WTS ? (uint32_t)(kc * T::WTS + e) * (uint32_t)sizeof(E)
+                                             : kOOB);
+    }
   };
   auto lstore = [&](int buf) {
     float* X = lds + buf * T::LDS_BUF;
     float* Wl = X + T::LDS_X;
 #pragma unroll
-    for (int i = 0; i < T::HALO_PT; ++i)
-      if (x_loff[i] >= 0) X[x_loff[i]] = rx[i];
+    for (int i = 0; i < T::HALO_PT; ++i) X[x_loff[i]] = rx[i];
 #pragma unroll
-    for (int i = 0; i < T::WTS_PT; ++i)
-      if (w_loff[i] >= 0) Wl[w_loff[i]] = rw[i];
+    for (int i = 0; i < T::WTS_PT; ++i) Wl[w_loff[i]] = rw[i];
   };
   auto compute = [&](int buf) {
     const float* X = lds + buf * T::LDS_BUF;
@@ -303,9 +314,11 @@ struct SmallTile {
   static constexpr int LDS_BUF = LDS_X + LDS_W;
   static_assert(P % 4 == 0, "image planes are loaded as float4");
   static constexpr int X_F4 = CK * IMGS * P / 4;  // float4 per chunk
-  static constexpr int X_PT = (X_F4 + 255) / 256;
+  static constexpr int X_PT = X_F4 / 256;
   static constexpr int WTS = 9 * CK * BN;
-  static constexpr int WTS_PT = (WTS + 255) / 256;
+  static constexpr int WTS_PT = WTS / 256;
+  // Every staging lane is live: the stores need no condition.
+  static_assert(X_F4 % 256 == 0 && WTS % 256 == 0, "staging covers whole 256-thread rounds");
   static constexpr int MB = BM / 16;              // column blocks: (position, image group)
   static constexpr int OUT_IMG_STRIDE = BN * P + 4;
   static constexpr int LDS_OUT = IMGS * OUT_IMG_STRIDE;
@@ -339,26 +352,27 @@ __global__ __launch_bounds__(256, 2) void conv3x3_small_f32(ConvArgs a) {
 #pragma unroll
   for (int i = 0; i < T::X_PT; ++i) {
     int q = tid + i * 256;
-    bool live = q < T::X_F4;
     int quarter = q % (T::P / 4), rest = q / (T::P / 4);
     int c = rest % T::CK, img = rest / T::CK;
     int n = n0 + img;
-    x_off[i] = (live && n < a.N) ? n * a.Cin * T::P + quarter * 4 : -1;   // + ci * P
+    x_off[i] = n < a.N ? img * a.Cin * T::P + quarter * 4 : -1;   // from image n0; + ci * P
     x_c[i] = c;
-    x_loff[i] = live ? c * T::PLANE_P + quarter * 4 * T::IMGS + img : -1;
+    x_loff[i] = c * T::PLANE_P + quarter * 4 * T::IMGS + img;
   }
-  int w_off[T::WTS_PT], w_loff[T::WTS_PT], w_ci[T::WTS_PT];
+  // Packed filter slice element e -> LDS row e / BN, column e % BN.
+  int w_loff[T::WTS_PT];
 #pragma unroll
   for (int i = 0; i < T::WTS_PT; ++i) {
     int e = tid + i * 256;
-    filter_plan<DGRAD, T::CK, T::BN, T::BN_P>(e, co0, a.Cin, a.Cout, w_off[i], w_loff[i], w_ci[i]);
-    if (e >= T::WTS) { w_off[i] = -1; w_loff[i] = -1; }
+    w_loff[i] = (e / T::BN) * T::BN_P + e % T::BN;
   }
 
   f4 acc[T::MB];
 #pragma unroll
   for (int j = 0; j < T::MB; ++j) acc[j] = f4{0.f, 0.f, 0.f, 0.f};
 
+  const rsrc_t xr = input_rsrc<E>(a, n0, T::IMGS);
+  const rsrc_t wr = packed_rsrc<E, T::WTS>(a, blockIdx.y);
   f4 rx[T::X_PT];
   float rw[T::WTS_PT];
   auto gload = [&](int kc) {
@@ -367,24 +381,21 @@ __global__ __launch_bounds__(256, 2) void conv3x3_small_f32(ConvArgs a) {
     for (int i = 0; i < T::X_PT; ++i) {
       const int ci = cbase + x_c[i];
       const bool ok = x_off[i] >= 0 && ci < a.Cin;
-      const f4 v = Elem<E>::load4((const E*)a.in + (ok ? x_off[i] + ci * T::P : 0));
-      rx[i] = ok ? v : f4{0.f, 0.f, 0.f, 0.f};
+      rx[i] = BufLoad<E>::four(xr, ok ? (uint32_t)(x_off[i] + ci * T::P) * (uint32_t)sizeof(E) : kOOB);
     }
 #pragma unroll
-    for (int i = 0; i < T::WTS_PT; ++i) rw[i] = filter_load<DGRAD, E>(a, w_off[i], w_ci[i], cbase);
+    for (int i = 0; i < T::WTS_PT; ++i)
+      rw[i] = BufLoad<E>::one(wr, (uint32_t)(kc * T::WTS + tid + i * 256) * (uint32_t)sizeof(E));
   };
   auto lstore = [&](int buf) {
     float* X = lds + buf * T::LDS_BUF;
     float* Wl = X + T::LDS_X;
 #pragma unroll
     for (int i = 0; i < T::X_PT; ++i)
-      if (x_loff[i] >= 0) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) X[x_loff[i] + j * T::IMGS] = rx[i][j];
-      }
+      for (int j = 0; j < 4; ++j) X[x_loff[i] + j * T::IMGS] = rx[i][j];
 #pragma unroll
-    for (int i = 0; i < T::WTS_PT; ++i)
-      if (w_loff[i] >= 0) Wl[w_loff[i]] = rw[i];
+    for (int i = 0; i < T::WTS_PT; ++i) Wl[w_loff[i]] = rw[i];
   };
   auto compute = [&](int buf) {
     const float* X = lds + buf * T::LDS_BUF;
@@ -487,9 +498,12 @@ __global__ __launch_bounds__(256) void conv_splitk_reduce(
 // ---------------------------------------------------------------- host --
 struct IgemmPlan {
   int tile;          // index into the tile table
+  int imgs;          // images per pixel tile
   int grid_x, co_tiles;
   int tiles_w, tiles_h;
   int nchunks, cps, splits;
+  size_t pack_bytes;  // packed filters, at the start of the workspace
+  size_t part_off;    // split partials, after them
   size_t ws_bytes;
 };
 
@@ -517,7 +531,8 @@ static const char* kTileNames[] = {
 
 // allow_small: the whole-image kernel needs tensors aligned for 4-element
 // moves.
-static IgemmPlan igemm_plan(int N, int Cin, int H, int W, int Cout, bool allow_small = true) {
+static IgemmPlan igemm_plan(int N, int Cin, int H, int W, int Cout, int esize,
+                            bool allow_small = true) {
   IgemmPlan p{};
   int th = 4, tw = 32, imgs = 1, ck = 8, bn = 64;
   if (allow_small && H == 2 && W == 2 && Cin > 4) { p.tile = 7; th = 2; tw = 2; imgs = 32; }
@@ -529,6 +544,7 @@ static IgemmPlan igemm_plan(int N, int Cin, int H, int W, int Cout, bool allow_s
   else if (W >= 8) { p.tile = 2; th = 8; tw = 8; imgs = 2; }
   else if (W >= 4) { p.tile = 3; th = 4; tw = 4; imgs = 8; }
   else { p.tile = 4; th = 2; tw = 2; imgs = 32; }
+  p.imgs = imgs;
   p.tiles_w = cdiv(W, tw);
   p.tiles_h = cdiv(H, th);
   p.grid_x = p.tiles_w * p.tiles_h * cdiv(N, imgs);
@@ -544,7 +560,10 @@ static IgemmPlan igemm_plan(int N, int Cin, int H, int W, int Cout, bool allow_s
                                  cdiv((int)target, (int)blocks));
   p.cps = cdiv(p.nchunks, splits);
   p.splits = cdiv(p.nchunks, p.cps);
-  p.ws_bytes = p.splits > 1 ? (size_t)p.splits * N * Cout * H * W * sizeof(float) : 0;
+  p.pack_bytes = (size_t)p.co_tiles * p.nchunks * 9 * ck * bn * esize;
+  p.part_off = round_up(p.pack_bytes, 256);
+  p.ws_bytes = p.part_off +
+               (p.splits > 1 ? (size_t)p.splits * N * Cout * H * W * sizeof(float) : 0);
   return p;
 }
 
@@ -555,9 +574,11 @@ static void igemm_launch(const IgemmPlan& p, const ConvArgs& a, hipStream_t st) 
   if constexpr (SMALL) fn = (const void*)conv3x3_small_f32<T, DGRAD, E>;
   else fn = (const void*)conv3x3_igemm_f32<T, DGRAD, E>;
   if (!attr_set) {
-    hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)T::LDS_BYTES);
+    (void)hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)T::LDS_BYTES);
     attr_set = true;
   }
+  filter_pack<DGRAD, T::CK, T::BN, E><<<p.co_tiles * p.nchunks, 256, 0, st>>>(
+      (const E*)a.wt, (E*)a.wpk, a.Cin, a.Cout);
   dim3 grid(p.grid_x, p.co_tiles, p.splits);
   ConvArgs k = a;
   if (p.splits > 1) { k.bias = nullptr; k.mask = nullptr; k.relu = 0; }
@@ -593,14 +614,15 @@ static void igemm_dispatch(const IgemmPlan& p, const ConvArgs& a, hipStream_t st
 // Entry points used by api.hip.
 namespace sbh {
 
-size_t conv_igemm_ws(int N, int Cin, int H, int W, int Cout) {
-  return std::max(sb::igemm_plan(N, Cin, H, W, Cout, true).ws_bytes,
-                  sb::igemm_plan(N, Cin, H, W, Cout, false).ws_bytes);
+size_t conv_igemm_ws(int dtype, int N, int Cin, int H, int W, int Cout) {
+  const int es = (int)dsize(dtype);
+  return std::max(sb::igemm_plan(N, Cin, H, W, Cout, es, true).ws_bytes,
+                  sb::igemm_plan(N, Cin, H, W, Cout, es, false).ws_bytes);
 }
 
 int conv_igemm_describe(bool dgrad, int dtype, int N, int Cin, int H, int W, int Cout,
                         char* buf, size_t len) {
-  sb::IgemmPlan p = sb::igemm_plan(N, Cin, H, W, Cout);
+  sb::IgemmPlan p = sb::igemm_plan(N, Cin, H, W, Cout, (int)dsize(dtype));
   char name[160];
   snprintf(name, sizeof(name), sb::kTileNames[p.tile], dgrad ? "true" : "false",
            dtype == SB_BF16 ? "unsigned short" : "float");
@@ -614,14 +636,21 @@ sb_status conv_igemm(bool dgrad, int dtype, int N, int Cin, int H, int W, int Co
   // bf16); the plan only picks them for tensors aligned that far.
   const uintptr_t amask = dtype == SB_BF16 ? 7 : 15;
   const bool aligned = (((uintptr_t)in | (uintptr_t)out | (uintptr_t)mask) & amask) == 0;
-  sb::IgemmPlan p = sb::igemm_plan(N, Cin, H, W, Cout, aligned);
-  if (p.ws_bytes > 0 && (ws == nullptr || ws_bytes < p.ws_bytes)) return SB_ERR_WORKSPACE;
+  const int64_t es = dsize(dtype);
+  sb::IgemmPlan p = sb::igemm_plan(N, Cin, H, W, Cout, (int)es, aligned);
+  // Buffer ranges: one block's images of the input, and one output-channel
+  // tile's packed filters.
+  if ((int64_t)std::min(p.imgs, N) * Cin * H * W * es >= (1ll << 31) ||
+      (int64_t)p.pack_bytes >= (1ll << 31))
+    return SB_ERR_UNSUPPORTED;
+  if (ws == nullptr || ws_bytes < p.ws_bytes) return SB_ERR_WORKSPACE;
   sb::ConvArgs a{};
   a.in = in; a.wt = wt; a.bias = bias; a.mask = mask; a.out = out;
-  a.part = p.splits > 1 ? (float*)ws : nullptr;
+  a.wpk = ws;
+  a.part = p.splits > 1 ? (float*)((char*)ws + p.part_off) : nullptr;
   a.N = N; a.Cin = Cin; a.H = H; a.W = W; a.Cout = Cout;
   a.tiles_w = p.tiles_w; a.tiles_h = p.tiles_h;
-  a.chunks_per_split = p.cps; a.splits = p.splits; a.relu = relu;
+  a.nchunks = p.nchunks; a.chunks_per_split = p.cps; a.splits = p.splits; a.relu = relu;
   if (dtype == SB_BF16) {
     if (dgrad) sb::igemm_dispatch<true, sb::u16>(p, a, st);
     else sb::igemm_dispatch<false, sb::u16>(p, a, st);

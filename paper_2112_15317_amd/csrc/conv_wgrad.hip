@@ -49,6 +49,15 @@ struct WgArgs {
   int tiles_w, tiles_h, ptiles, tiles_per_split, c_tiles, splits;
 };
 
+// Buffer resource over `imgs` images (clipped to the batch) of an NCHW tensor
+// from image n0 on; per_img = elements per image.
+template <class E>
+__device__ __forceinline__ rsrc_t image_rsrc(const void* t, int n0, int imgs, int N, int per_img) {
+  const int cnt = min(imgs, N - n0);
+  return make_rsrc((const E*)t + (size_t)n0 * per_img,
+                   (uint32_t)((size_t)cnt * per_img * sizeof(E)));
+}
+
 // Writes (or split-reduces) the block's 64 k x 16-column x NACC outputs.
 // `val(i, t)` is the lane's accumulator t, element i; `col(t)` the flattened
 // (c, tap) column of the lane in accumulator t, or -1.
@@ -115,10 +124,13 @@ struct WgTile {
   static constexpr int DY_STRIDE = BK + 16;         // floats per pixel row of dy
   static constexpr int LDS_DY = BP * DY_STRIDE;
   static constexpr int LDS_X = PLANE * BC;
-  static constexpr int LDS_BUF = LDS_DY + LDS_X;
+  // Halo staging lanes past the end store into a private slot (256 floats)
+  // after the halo, so the stores need no condition.
+  static constexpr int LDS_BUF = LDS_DY + LDS_X + 256;
   static constexpr int DY_PT = BK * BP / 256;       // 16
   static constexpr int X_PT = (BC * PLANE + 255) / 256;
   static constexpr size_t LDS_BYTES = 2 * LDS_BUF * sizeof(float);
+  static_assert(LDS_BYTES <= 80 * 1024, "two blocks must fit in the 160 KB of LDS");
 };
 
 // Halo offset of tile pixel p (0..BP-1).
@@ -166,6 +178,8 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_f32(WgArgs a) {
     int tx = pt % a.tiles_w, r0 = pt / a.tiles_w;
     int ty = r0 % a.tiles_h, tn = r0 / a.tiles_h;
     const int n0 = tn * T::IMGS, h0 = ty * T::TH, w0 = tx * T::TW;
+    const rsrc_t dr = image_rsrc<E>(a.dy, n0, T::IMGS, a.N, a.K * HWs);
+    const rsrc_t xr = image_rsrc<E>(a.x, n0, T::IMGS, a.N, a.C * HWs);
     // dy: element e = (pixel quad, k-in-tile, pixel within the quad).  A
     // wave covers 16 k x 4 consecutive pixels: 16 rows of 16 B in global
     // memory, and 64 distinct banks in the [pixel][k] LDS tile.
@@ -177,8 +191,8 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_f32(WgArgs a) {
       int yy = r / T::TW, xx = r - yy * T::TW;
       int n = n0 + img, h = h0 + yy, w = w0 + xx, k = k0 + kk;
       bool ok = n < a.N && h < a.H && w < a.W && k < a.K;
-      float v = Elem<E>::load((const E*)a.dy, ok ? (n * a.K + k) * HWs + h * a.W + w : 0);
-      rdy[i] = ok ? v : 0.f;
+      const int off = (img * a.K + k) * HWs + h * a.W + w;          // from image n0
+      rdy[i] = BufLoad<E>::one(dr, ok ? (uint32_t)off * (uint32_t)sizeof(E) : kOOB);
     }
     // x halo: element e = (halo pixel, c-in-tile) with c fastest, for the
     // same reason ([halo pixel][c] LDS tile).
@@ -191,8 +205,8 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_f32(WgArgs a) {
       int n = n0 + img, h = h0 + yy - 1, w = w0 + xx - 1, c = c0 + cc;
       bool ok = e < T::BC * T::PLANE && n < a.N && h >= 0 && h < a.H && w >= 0 && w < a.W &&
                 c < a.C;
-      float v = Elem<E>::load((const E*)a.x, ok ? (n * a.C + c) * HWs + h * a.W + w : 0);
-      rx[i] = ok ? v : 0.f;
+      const int off = (img * a.C + c) * HWs + h * a.W + w;          // from image n0
+      rx[i] = BufLoad<E>::one(xr, ok ? (uint32_t)off * (uint32_t)sizeof(E) : kOOB);
     }
   };
   auto lstore = [&](int buf) {
@@ -207,7 +221,7 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_f32(WgArgs a) {
 #pragma unroll
     for (int i = 0; i < T::X_PT; ++i) {
       int e = tid + i * 256;
-      if (e < T::BC * T::PLANE) Xl[e] = rx[i];     // = [halo pixel][c]
+      Xl[e < T::BC * T::PLANE ? e : T::LDS_X + tid] = rx[i];     // = [halo pixel][c]
     }
   };
   auto compute = [&](int buf) {
@@ -279,8 +293,10 @@ struct WgSmall {
   static_assert(P % 4 == 0 && IW % 4 == 0, "float4 planes, 4-image MFMA steps");
   static constexpr int DZ_F4 = IW * BK * P / 4;
   static constexpr int X_F4 = IW * BC * P / 4;
-  static constexpr int DZ_PT = (DZ_F4 + 255) / 256;
-  static constexpr int X_PT = (X_F4 + 255) / 256;
+  static constexpr int DZ_PT = DZ_F4 / 256;
+  static constexpr int X_PT = X_F4 / 256;
+  // Every staging lane is live: the stores need no condition.
+  static_assert(DZ_F4 % 256 == 0 && X_F4 % 256 == 0, "staging covers whole 256-thread rounds");
   __host__ __device__ static constexpr int src(int pos, int tap) {
     return (pos / W + tap / 3 - 1 >= 0 && pos / W + tap / 3 - 1 < H &&
             pos % W + tap % 3 - 1 >= 0 && pos % W + tap % 3 - 1 < W)
@@ -307,9 +323,9 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_small_f32(WgArgs a) {
     int q = tid + i * 256;
     int kk = q % T::BK, rest = q / T::BK;          // k fastest: conflict-free LDS rows
     int quarter = rest % (T::P / 4), img = rest / (T::P / 4);
-    bool ok = q < T::DZ_F4 && k0 + kk < a.K;
-    dz_off[i] = ok ? (img * a.K + k0 + kk) * T::P + quarter * 4 : -1;   // + chunk*IW*K*P
-    dz_loff[i] = q < T::DZ_F4 ? ((quarter * 4) * T::IW + img) * T::DZ_STRIDE + kk : -1;
+    bool ok = k0 + kk < a.K;
+    dz_off[i] = ok ? (img * a.K + k0 + kk) * T::P + quarter * 4 : -1;   // from the chunk's first image
+    dz_loff[i] = ((quarter * 4) * T::IW + img) * T::DZ_STRIDE + kk;
   }
   int x_off[T::X_PT], x_loff[T::X_PT];
 #pragma unroll
@@ -317,9 +333,9 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_small_f32(WgArgs a) {
     int q = tid + i * 256;
     int cc = q % T::BC, rest = q / T::BC;          // c, then image: consecutive LDS rows
     int img = rest % T::IW, quarter = rest / T::IW;
-    bool ok = q < T::X_F4 && c0 + cc < a.C;
-    x_off[i] = ok ? (img * a.C + c0 + cc) * T::P + quarter * 4 : -1;    // + chunk*IW*C*P
-    x_loff[i] = q < T::X_F4 ? ((quarter * 4) * T::IW + img) * T::BC + cc : -1;
+    bool ok = c0 + cc < a.C;
+    x_off[i] = ok ? (img * a.C + c0 + cc) * T::P + quarter * 4 : -1;    // from the chunk's first image
+    x_loff[i] = ((quarter * 4) * T::IW + img) * T::BC + cc;
   }
 
   f4 acc[9], accb = f4{0.f, 0.f, 0.f, 0.f};
@@ -327,22 +343,21 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_small_f32(WgArgs a) {
   for (int t = 0; t < 9; ++t) acc[t] = f4{0.f, 0.f, 0.f, 0.f};
 
   f4 rdz[T::DZ_PT], rx[T::X_PT];
-  const f4 zero4 = {0.f, 0.f, 0.f, 0.f};
   auto gload = [&](int ch) {
     const int nb = ch * T::IW;                        // first image of the chunk
+    const rsrc_t dr = image_rsrc<E>(a.dy, nb, T::IW, a.N, a.K * T::P);
+    const rsrc_t xr = image_rsrc<E>(a.x, nb, T::IW, a.N, a.C * T::P);
 #pragma unroll
     for (int i = 0; i < T::DZ_PT; ++i) {
       const int img = (tid + i * 256) / T::BK / (T::P / 4);
       const bool ok = dz_off[i] >= 0 && nb + img < a.N;
-      const f4 v = Elem<E>::load4((const E*)a.dy + (ok ? dz_off[i] + nb * a.K * T::P : 0));
-      rdz[i] = ok ? v : zero4;
+      rdz[i] = BufLoad<E>::four(dr, ok ? (uint32_t)dz_off[i] * (uint32_t)sizeof(E) : kOOB);
     }
 #pragma unroll
     for (int i = 0; i < T::X_PT; ++i) {
       const int img = (tid + i * 256) / T::BC % T::IW;
       const bool ok = x_off[i] >= 0 && nb + img < a.N;
-      const f4 v = Elem<E>::load4((const E*)a.x + (ok ? x_off[i] + nb * a.C * T::P : 0));
-      rx[i] = ok ? v : zero4;
+      rx[i] = BufLoad<E>::four(xr, ok ? (uint32_t)x_off[i] * (uint32_t)sizeof(E) : kOOB);
     }
   };
   auto lstore = [&](int buf) {
@@ -350,16 +365,12 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_small_f32(WgArgs a) {
     float* Xl = Dl + T::LDS_DZ;
 #pragma unroll
     for (int i = 0; i < T::DZ_PT; ++i)
-      if (dz_loff[i] >= 0) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) Dl[dz_loff[i] + j * T::IW * T::DZ_STRIDE] = rdz[i][j];
-      }
+      for (int j = 0; j < 4; ++j) Dl[dz_loff[i] + j * T::IW * T::DZ_STRIDE] = rdz[i][j];
 #pragma unroll
     for (int i = 0; i < T::X_PT; ++i)
-      if (x_loff[i] >= 0) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) Xl[x_loff[i] + j * T::IW * T::BC] = rx[i][j];
-      }
+      for (int j = 0; j < 4; ++j) Xl[x_loff[i] + j * T::IW * T::BC] = rx[i][j];
   };
   auto compute = [&](int buf) {
     const float* Dl = lds + buf * T::LDS_BUF;
@@ -409,6 +420,7 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_small_f32(WgArgs a) {
 
 // ---------------------------------------------------------------- host --
 struct WgPlan {
+  int imgs;          // images per pixel tile (per LDS fill for the small kernels)
   int tile, tiles_w, tiles_h, ptiles, k_tiles, c_tiles, tps, splits;
   size_t ws_bytes;
 };
@@ -451,6 +463,7 @@ static WgPlan wg_plan(int N, int C, int H, int W, int K, bool allow_small = true
   else if (W >= 8) { p.tile = 2; th = 8; tw = 8; }
   else if (W >= 4) { p.tile = 3; th = 4; tw = 4; imgs = 4; }
   else { p.tile = 4; th = 2; tw = 2; imgs = 16; }
+  p.imgs = imgs;
   p.tiles_w = cdiv(W, tw);
   p.tiles_h = cdiv(H, th);
   p.ptiles = p.tiles_w * p.tiles_h * cdiv(N, imgs);   // for the small kernels: image chunks
@@ -475,7 +488,7 @@ static void wg_launch(const WgPlan& p, const WgArgs& a, hipStream_t st) {
   if constexpr (SMALL) fn = (const void*)conv3x3_wgrad_small_f32<T, E>;
   else fn = (const void*)conv3x3_wgrad_f32<T, E>;
   if (!attr_set) {
-    hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)T::LDS_BYTES);
+    (void)hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)T::LDS_BYTES);
     attr_set = true;
   }
   dim3 grid(p.k_tiles * p.c_tiles, 1, p.splits);
@@ -533,6 +546,9 @@ sb_status conv_wgrad(int dtype, int N, int C, int H, int W, int K, const void* x
   const uintptr_t amask = dtype == SB_BF16 ? 7 : 15;
   const bool aligned = (((uintptr_t)x | (uintptr_t)dy) & amask) == 0;
   sb::WgPlan p = sb::wg_plan(N, C, H, W, K, aligned);
+  // Buffer ranges: one tile's images of x and of dy.
+  if ((int64_t)std::min(p.imgs, N) * std::max(C, K) * H * W * dsize(dtype) >= (1ll << 31))
+    return SB_ERR_UNSUPPORTED;
   if (p.ws_bytes > 0 && (ws == nullptr || ws_bytes < p.ws_bytes)) return SB_ERR_WORKSPACE;
   sb::WgArgs a{};
   a.x = x; a.dy = dy; a.dw = dw; a.db = db;

@@ -65,6 +65,42 @@ template <> struct Elem<u16> {
   }
 };
 
+// Raw buffer loads.  A 128-bit resource covers [base, base + bytes); a load at
+// a byte offset outside that range returns 0 (the hardware range check).
+// Staging loops select the offset (kOOB for a padded or ragged element)
+// instead of selecting the loaded value, so nothing waits on the load until
+// the value is stored to LDS, and the load latency hides behind the MFMAs.
+// The ranges a kernel builds stay below 2^31 bytes (checked on the host).
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+constexpr uint32_t kOOB = 0x80000000u;
+constexpr uint32_t kRsrcWord3 = 0x00020000u;   // raw, 32-bit data format (gfx9 family)
+
+__device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
+                                           (int)kRsrcWord3);
+}
+
+template <typename T> struct BufLoad;
+template <> struct BufLoad<float> {
+  __device__ static __forceinline__ float one(rsrc_t r, uint32_t off) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, 0));
+  }
+  __device__ static __forceinline__ f4 four(rsrc_t r, uint32_t off) {
+    return __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0));
+  }
+};
+template <> struct BufLoad<u16> {
+  __device__ static __forceinline__ float one(rsrc_t r, uint32_t off) {
+    return bf16_to_f32((u16)__builtin_amdgcn_raw_buffer_load_b16(r, (int)off, 0, 0));
+  }
+  __device__ static __forceinline__ f4 four(rsrc_t r, uint32_t off) {
+    typedef uint32_t u2 __attribute__((ext_vector_type(2)));
+    u2 u = __builtin_bit_cast(u2, __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, 0));
+    return f4{__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u),
+              __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xffff0000u)};
+  }
+};
+
 __host__ __device__ constexpr int cdiv(int a, int b) { return (a + b - 1) / b; }
 __host__ __device__ constexpr size_t round_up(size_t a, size_t b) { return (a + b - 1) / b * b; }
 
