@@ -112,11 +112,11 @@ __device__ __forceinline__ rsrc_t packed_rsrc(const ConvArgs& a, int ct) {
 }
 
 // ----------------------------------------------------------------- generic --
-template <int TH_, int TW_, int IMGS_, int CK_, int BN_>
+template <int TH_, int TW_, int IMGS_, int CK_, int BN_, int WAVES_N_>
 struct ConvTile {
   static constexpr int TH = TH_, TW = TW_, IMGS = IMGS_, CK = CK_, BN = BN_;
   static constexpr int BM = IMGS * TH * TW;
-  static_assert(BM == 128, "pixel tile must hold 128 pixels");
+  static_assert(BM == 128 || BM == 256, "pixel tile must hold 128 or 256 pixels");
   static constexpr int HH = TH + 2, HW = TW + 2;
   static constexpr int PLANE = IMGS * HH * HW;
   // Channel stride of the halo in LDS: a multiple of 64 floats plus 16, so
@@ -138,9 +138,13 @@ struct ConvTile {
   static constexpr int LDS_BUF = LDS_X + LDS_W + LDS_SPARE;
   static constexpr size_t LDS_BYTES = 2 * LDS_BUF * sizeof(float);
   static_assert(LDS_BYTES <= 80 * 1024, "two blocks must fit in the 160 KB of LDS");
-  // Waves split the tile 2 x 2 (BN >= 32) or 1 x 4 along pixels (BN = 16).
-  static constexpr int WAVES_N = BN >= 32 ? 2 : 1, WAVES_M = 4 / WAVES_N;
+  // Waves split the tile WAVES_N along channels x WAVES_M along pixels; a
+  // wave owns WN channels x WM pixels (NB x MB MFMA blocks).  The 256-pixel
+  // tiles give each wave 64 x 64, which halves the LDS operand reads per
+  // MFMA and the filter staging per MFMA against 32 x 64.
+  static constexpr int WAVES_N = WAVES_N_, WAVES_M = 4 / WAVES_N;
   static constexpr int WN = BN / WAVES_N, WM = BM / WAVES_M;
+  static_assert(WN % 16 == 0 && WM % 16 == 0, "whole 16 x 16 MFMA blocks per wave");
   static constexpr int NB = WN / 16, MB = WM / 16;
   static constexpr int NSTEP = 9 * (CK / 4);     // MFMA k-steps per chunk
 };
@@ -507,26 +511,32 @@ struct IgemmPlan {
   size_t ws_bytes;
 };
 
-using TileW32 = ConvTile<4, 32, 1, 8, 64>;
-using TileW16 = ConvTile<8, 16, 1, 8, 64>;
-using TileW8 = ConvTile<8, 8, 2, 8, 64>;
-using TileW4 = ConvTile<4, 4, 8, 8, 64>;
-using TileW2 = ConvTile<2, 2, 32, 8, 64>;
-using TileW32c4 = ConvTile<4, 32, 1, 4, 64>;
-using TileW32n16 = ConvTile<4, 32, 1, 8, 16>;
+using TileW32 = ConvTile<4, 32, 1, 8, 64, 2>;
+using TileW16 = ConvTile<8, 16, 1, 8, 64, 2>;
+using TileW8 = ConvTile<8, 8, 2, 8, 64, 2>;
+using TileW4 = ConvTile<4, 4, 8, 8, 64, 2>;
+using TileW2 = ConvTile<2, 2, 32, 8, 64, 2>;
+using TileW32c4 = ConvTile<4, 32, 1, 4, 64, 2>;
+using TileW32n16 = ConvTile<4, 32, 1, 8, 16, 1>;
+using TileW32L = ConvTile<8, 32, 1, 8, 64, 1>;
+using TileW16L = ConvTile<16, 16, 1, 8, 64, 1>;
+using TileW8L = ConvTile<8, 8, 4, 8, 64, 1>;
 using Small2 = SmallTile<2, 2, 2>;
 using Small4 = SmallTile<4, 4, 1>;
 
 static const char* kTileNames[] = {
-    "sb::conv3x3_igemm_f32<sb::ConvTile<4, 32, 1, 8, 64>, %s, %s>",
-    "sb::conv3x3_igemm_f32<sb::ConvTile<8, 16, 1, 8, 64>, %s, %s>",
-    "sb::conv3x3_igemm_f32<sb::ConvTile<8, 8, 2, 8, 64>, %s, %s>",
-    "sb::conv3x3_igemm_f32<sb::ConvTile<4, 4, 8, 8, 64>, %s, %s>",
-    "sb::conv3x3_igemm_f32<sb::ConvTile<2, 2, 32, 8, 64>, %s, %s>",
-    "sb::conv3x3_igemm_f32<sb::ConvTile<4, 32, 1, 4, 64>, %s, %s>",
-    "sb::conv3x3_igemm_f32<sb::ConvTile<4, 32, 1, 8, 16>, %s, %s>",
+    "sb::conv3x3_igemm_f32<sb::ConvTile<4, 32, 1, 8, 64, 2>, %s, %s>",
+    "sb::conv3x3_igemm_f32<sb::ConvTile<8, 16, 1, 8, 64, 2>, %s, %s>",
+    "sb::conv3x3_igemm_f32<sb::ConvTile<8, 8, 2, 8, 64, 2>, %s, %s>",
+    "sb::conv3x3_igemm_f32<sb::ConvTile<4, 4, 8, 8, 64, 2>, %s, %s>",
+    "sb::conv3x3_igemm_f32<sb::ConvTile<2, 2, 32, 8, 64, 2>, %s, %s>",
+    "sb::conv3x3_igemm_f32<sb::ConvTile<4, 32, 1, 4, 64, 2>, %s, %s>",
+    "sb::conv3x3_igemm_f32<sb::ConvTile<4, 32, 1, 8, 16, 1>, %s, %s>",
     "sb::conv3x3_small_f32<sb::SmallTile<2, 2, 2>, %s, %s>",
     "sb::conv3x3_small_f32<sb::SmallTile<4, 4, 1>, %s, %s>",
+    "sb::conv3x3_igemm_f32<sb::ConvTile<8, 32, 1, 8, 64, 1>, %s, %s>",
+    "sb::conv3x3_igemm_f32<sb::ConvTile<16, 16, 1, 8, 64, 1>, %s, %s>",
+    "sb::conv3x3_igemm_f32<sb::ConvTile<8, 8, 4, 8, 64, 1>, %s, %s>",
 };
 
 // allow_small: the whole-image kernel needs tensors aligned for 4-element
@@ -539,6 +549,7 @@ static IgemmPlan igemm_plan(int N, int Cin, int H, int W, int Cout, int esize,
   else if (allow_small && H == 4 && W == 4 && Cin > 4) { p.tile = 8; th = 4; tw = 4; imgs = 16; }
   else if (Cout <= 16 && Cin > 4 && W >= 32) { p.tile = 6; bn = 16; }
   else if (Cin <= 4 && W >= 32) { p.tile = 5; ck = 4; }
+  else if (W >= 32 && (long)N * cdiv(H, 8) * cdiv(W, 32) >= 512) { p.tile = 9; th = 8; }
   else if (W >= 32) { p.tile = 0; }
   else if (W >= 16) { p.tile = 1; th = 8; tw = 16; }
   else if (W >= 8) { p.tile = 2; th = 8; tw = 8; imgs = 2; }
@@ -605,7 +616,10 @@ static void igemm_dispatch(const IgemmPlan& p, const ConvArgs& a, hipStream_t st
     case 5: igemm_launch<TileW32c4, DGRAD, false, E>(p, a, st); break;
     case 6: igemm_launch<TileW32n16, DGRAD, false, E>(p, a, st); break;
     case 7: igemm_launch<Small2, DGRAD, true, E>(p, a, st); break;
-    default: igemm_launch<Small4, DGRAD, true, E>(p, a, st); break;
+    case 8: igemm_launch<Small4, DGRAD, true, E>(p, a, st); break;
+    case 9: igemm_launch<TileW32L, DGRAD, false, E>(p, a, st); break;
+    case 10: igemm_launch<TileW16L, DGRAD, false, E>(p, a, st); break;
+    default: igemm_launch<TileW8L, DGRAD, false, E>(p, a, st); break;
   }
 }
 
