@@ -112,9 +112,14 @@ __device__ __forceinline__ rsrc_t packed_rsrc(const ConvArgs& a, int ct) {
 }
 
 // ----------------------------------------------------------------- generic --
-template <int TH_, int TW_, int IMGS_, int CK_, int BN_, int WAVES_N_>
+template <int TH_, int TW_, int IMGS_, int CK_, int BN_, int WAVES_N_, int KSPLIT_ = 1>
 struct ConvTile {
   static constexpr int TH = TH_, TW = TW_, IMGS = IMGS_, CK = CK_, BN = BN_;
+  // KSPLIT groups of 256 threads share the block's output tile and take
+  // alternate channel chunks, each through its own LDS buffers; the groups'
+  // partial sums are added through LDS in a fixed order at the end.  This
+  // fills the chip on small grids without split partials in HBM.
+  static constexpr int KSPLIT = KSPLIT_, THREADS = 256 * KSPLIT;
   static constexpr int BM = IMGS * TH * TW;
   static_assert(BM == 128 || BM == 256, "pixel tile must hold 128 or 256 pixels");
   static constexpr int HH = TH + 2, HW = TW + 2;
@@ -136,8 +141,9 @@ struct ConvTile {
   // unconditional (no exec-mask juggling in the loop).
   static constexpr int LDS_SPARE = 256;
   static constexpr int LDS_BUF = LDS_X + LDS_W + LDS_SPARE;
-  static constexpr size_t LDS_BYTES = 2 * LDS_BUF * sizeof(float);
-  static_assert(LDS_BYTES <= 80 * 1024, "two blocks must fit in the 160 KB of LDS");
+  static constexpr size_t LDS_BYTES = KSPLIT * 2 * LDS_BUF * sizeof(float);
+  static_assert(LDS_BYTES * (KSPLIT == 1 ? 2 : 1) <= 160 * 1024,
+                "two blocks (one for KSPLIT = 2) must fit in the 160 KB of LDS");
   // Waves split the tile WAVES_N along channels x WAVES_M along pixels; a
   // wave owns WN channels x WM pixels (NB x MB MFMA blocks).  The 256-pixel
   // tiles give each wave 64 x 64, which halves the LDS operand reads per
@@ -147,13 +153,30 @@ struct ConvTile {
   static_assert(WN % 16 == 0 && WM % 16 == 0, "whole 16 x 16 MFMA blocks per wave");
   static constexpr int NB = WN / 16, MB = WM / 16;
   static constexpr int NSTEP = 9 * (CK / 4);     // MFMA k-steps per chunk
+  // Halo layout per channel: [halo row][halo column][image], image
+  // innermost, so that the 16 pixels of an MFMA column block (16 images, or
+  // a row segment of several images) are 16 consecutive LDS words for every
+  // tap: conflict-free operand reads however narrow the images.
+  __host__ __device__ static constexpr int hoff(int img, int hy, int hx) {
+    return (hy * HW + hx) * IMGS + img;
+  }
+  // Tile pixel p -> (image, row, column), in the same image-innermost order.
+  __device__ static void pix(int p, int& img, int& yy, int& xx) {
+    img = p % IMGS;
+    const int q = p / IMGS;
+    yy = q / TW;
+    xx = q - yy * TW;
+  }
 };
 
 template <class T, bool DGRAD, class E>
-__global__ __launch_bounds__(256, 2) void conv3x3_igemm_f32(ConvArgs a) {
-  extern __shared__ float lds[];
+__global__ __launch_bounds__(T::THREADS, 2 / T::KSPLIT) void conv3x3_igemm_f32(ConvArgs a) {
+  extern __shared__ float lds_all[];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // grp: which chunk stream this thread's 256-thread group takes.
+  const int grp = threadIdx.x >> 8;
+  float* lds = lds_all + grp * 2 * T::LDS_BUF;
+  const int tid = threadIdx.x & 255, lane = tid & 63, wave = tid >> 6;
   const int wm = wave % T::WAVES_M, wn = wave / T::WAVES_M;
   const int kq = lane >> 4, lr = lane & 15;
 
@@ -175,8 +198,8 @@ __global__ __launch_bounds__(256, 2) void conv3x3_igemm_f32(ConvArgs a) {
     int e = tid + i * 256;
     bool live = e < T::HALO;
     int c = e / T::PLANE, rem = e - c * T::PLANE;
-    int img = rem / (T::HH * T::HW), r2 = rem - img * (T::HH * T::HW);
-    int yy = r2 / T::HW, xx = r2 - yy * T::HW;
+    int img = rem % T::IMGS, q = rem / T::IMGS;          // rem = hoff(img, yy, xx)
+    int yy = q / T::HW, xx = q - yy * T::HW;
     int n = n0 + img, h = h0 + yy - 1, w = w0 + xx - 1;
     bool ok = live && n < a.N && h >= 0 && h < a.H && w >= 0 && w < a.W;
     x_off[i] = ok ? img * a.Cin * HWs + h * a.W + w : -1;   // from image n0; + ci * H*W
@@ -193,10 +216,9 @@ __global__ __launch_bounds__(256, 2) void conv3x3_igemm_f32(ConvArgs a) {
   int pix_off[T::MB];
 #pragma unroll
   for (int mb = 0; mb < T::MB; ++mb) {
-    int p = wm * T::WM + mb * 16 + lr;
-    int img = p / (T::TH * T::TW), r = p - img * (T::TH * T::TW);
-    int yy = r / T::TW, xx = r - yy * T::TW;
-    pix_off[mb] = img * T::HH * T::HW + yy * T::HW + xx;
+    int img, yy, xx;
+    T::pix(wm * T::WM + mb * 16 + lr, img, yy, xx);
+    pix_off[mb] = T::hoff(img, yy, xx);
   }
 
   f4 acc[T::NB][T::MB];
@@ -237,7 +259,7 @@ __global__ __launch_bounds__(256, 2) void conv3x3_igemm_f32(ConvArgs a) {
     float fa[2][T::NB], fb[2][T::MB];
     auto frag = [&](int step, int slot) {
       const int tap = step / (T::CK / 4), cg = step - tap * (T::CK / 4);
-      const int toff = (tap / 3) * T::HW + (tap % 3);
+      const int toff = T::hoff(0, tap / 3, tap % 3);
 #pragma unroll
       for (int nb = 0; nb < T::NB; ++nb)
         fa[slot][nb] = Wl[(tap * T::CK + cg * 4 + kq) * T::BN_P + wn * T::WN + nb * 16 + lr];
@@ -257,19 +279,47 @@ __global__ __launch_bounds__(256, 2) void conv3x3_igemm_f32(ConvArgs a) {
     }
   };
 
-  const int nk = kc1 - kc0;
+  // Group g takes chunks kc0 + g, kc0 + g + KSPLIT, ...; every group runs the
+  // same number of iterations (barriers are block-wide).
+  const int nk = (kc1 - kc0 - grp + T::KSPLIT - 1) / T::KSPLIT;
+  const int nit = (kc1 - kc0 + T::KSPLIT - 1) / T::KSPLIT;
+  auto chunk = [&](int t) { return kc0 + grp + t * T::KSPLIT; };
   if (nk > 0) {
-    gload(kc0);
+    gload(chunk(0));
     lstore(0);
-    if (nk > 1) gload(kc0 + 1);
+    if (nk > 1) gload(chunk(1));
   }
   __syncthreads();
-  for (int t = 0; t < nk; ++t) {
+  for (int t = 0; t < nit; ++t) {
     const int buf = t & 1;
     if (t + 1 < nk) lstore(buf ^ 1);
-    if (t + 2 < nk) gload(kc0 + t + 2);
-    compute(buf);
+    if (t + 2 < nk) gload(chunk(t + 2));
+    if (t < nk) compute(buf);
     __syncthreads();
+  }
+
+  if constexpr (T::KSPLIT == 2) {
+    // Group 1 hands its partial tile to group 0 through LDS (lane-major, so
+    // both the writes and the reads are conflict-free), group 0 adds it.
+    constexpr int NACC = T::NB * T::MB;
+    static_assert(4 * 64 * 4 * NACC <= 2 * T::LDS_BUF, "partial tile fits group 0's buffers");
+    float* xfer = lds_all + (size_t)(wave * NACC * 4) * 64 + lane;
+    if (grp == 1) {
+#pragma unroll
+      for (int nb = 0; nb < T::NB; ++nb)
+#pragma unroll
+        for (int mb = 0; mb < T::MB; ++mb)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) xfer[((nb * T::MB + mb) * 4 + i) * 64] = acc[nb][mb][i];
+    }
+    __syncthreads();
+    if (grp == 1) return;
+#pragma unroll
+    for (int nb = 0; nb < T::NB; ++nb)
+#pragma unroll
+      for (int mb = 0; mb < T::MB; ++mb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc[nb][mb][i] += xfer[((nb * T::MB + mb) * 4 + i) * 64];
   }
 
   // ---- epilogue: acc[nb][mb] lane holds channel co0 + wn*WN + nb*16 + 4*kq + i
@@ -278,9 +328,8 @@ __global__ __launch_bounds__(256, 2) void conv3x3_igemm_f32(ConvArgs a) {
   auto for_each_out = [&](auto&& fn) {
 #pragma unroll
     for (int mb = 0; mb < T::MB; ++mb) {
-      int p = wm * T::WM + mb * 16 + lr;
-      int img = p / (T::TH * T::TW), r = p - img * (T::TH * T::TW);
-      int yy = r / T::TW, xx = r - yy * T::TW;
+      int img, yy, xx;
+      T::pix(wm * T::WM + mb * 16 + lr, img, yy, xx);
       int n = n0 + img, h = h0 + yy, w = w0 + xx;
       if (n >= a.N || h >= a.H || w >= a.W) continue;
 #pragma unroll
@@ -521,22 +570,24 @@ using TileW32n16 = ConvTile<4, 32, 1, 8, 16, 1>;
 using TileW32L = ConvTile<8, 32, 1, 8, 64, 1>;
 using TileW16L = ConvTile<16, 16, 1, 8, 64, 1>;
 using TileW8L = ConvTile<8, 8, 4, 8, 64, 1>;
+using TileW8K2 = ConvTile<8, 8, 2, 8, 64, 2, 2>;
 using Small2 = SmallTile<2, 2, 2>;
 using Small4 = SmallTile<4, 4, 1>;
 
 static const char* kTileNames[] = {
-    "sb::conv3x3_igemm_f32<sb::ConvTile<4, 32, 1, 8, 64, 2>, %s, %s>",
-    "sb::conv3x3_igemm_f32<sb::ConvTile<8, 16, 1, 8, 64, 2>, %s, %s>",
-    "sb::conv3x3_igemm_f32<sb::ConvTile<8, 8, 2, 8, 64, 2>, %s, %s>",
-    "sb::conv3x3_igemm_f32<sb::ConvTile<4, 4, 8, 8, 64, 2>, %s, %s>",
-    "sb::conv3x3_igemm_f32<sb::ConvTile<2, 2, 32, 8, 64, 2>, %s, %s>",
-    "sb::conv3x3_igemm_f32<sb::ConvTile<4, 32, 1, 4, 64, 2>, %s, %s>",
-    "sb::conv3x3_igemm_f32<sb::ConvTile<4, 32, 1, 8, 16, 1>, %s, %s>",
+    "sb::conv3x3_igemm_f32<sb::ConvTile<4, 32, 1, 8, 64, 2, 1>, %s, %s>",
+    "sb::conv3x3_igemm_f32<sb::ConvTile<8, 16, 1, 8, 64, 2, 1>, %s, %s>",
+    "sb::conv3x3_igemm_f32<sb::ConvTile<8, 8, 2, 8, 64, 2, 1>, %s, %s>",
+    "sb::conv3x3_igemm_f32<sb::ConvTile<4, 4, 8, 8, 64, 2, 1>, %s, %s>",
+    "sb::conv3x3_igemm_f32<sb::ConvTile<2, 2, 32, 8, 64, 2, 1>, %s, %s>",
+    "sb::conv3x3_igemm_f32<sb::ConvTile<4, 32, 1, 4, 64, 2, 1>, %s, %s>",
+    "sb::conv3x3_igemm_f32<sb::ConvTile<4, 32, 1, 8, 16, 1, 1>, %s, %s>",
     "sb::conv3x3_small_f32<sb::SmallTile<2, 2, 2>, %s, %s>",
     "sb::conv3x3_small_f32<sb::SmallTile<4, 4, 1>, %s, %s>",
-    "sb::conv3x3_igemm_f32<sb::ConvTile<8, 32, 1, 8, 64, 1>, %s, %s>",
-    "sb::conv3x3_igemm_f32<sb::ConvTile<16, 16, 1, 8, 64, 1>, %s, %s>",
-    "sb::conv3x3_igemm_f32<sb::ConvTile<8, 8, 4, 8, 64, 1>, %s, %s>",
+    "sb::conv3x3_igemm_f32<sb::ConvTile<8, 32, 1, 8, 64, 1, 1>, %s, %s>",
+    "sb::conv3x3_igemm_f32<sb::ConvTile<16, 16, 1, 8, 64, 1, 1>, %s, %s>",
+    "sb::conv3x3_igemm_f32<sb::ConvTile<8, 8, 4, 8, 64, 1, 1>, %s, %s>",
+    "sb::conv3x3_igemm_f32<sb::ConvTile<8, 8, 2, 8, 64, 2, 2>, %s, %s>",
 };
 
 // allow_small: the whole-image kernel needs tensors aligned for 4-element
@@ -562,8 +613,11 @@ static IgemmPlan igemm_plan(int N, int Cin, int H, int W, int Cout, int esize,
   p.co_tiles = cdiv(Cout, bn);
   p.nchunks = cdiv(Cin, ck);
   long blocks = (long)p.grid_x * p.co_tiles;
-  // About two resident blocks on each of the 256 CUs; at most 8 splits, and
-  // at least two chunks per split.
+  // 8x8-image tiles that cannot fill the chip take the two-group block
+  // (intra-block split over channel chunks) before any split in HBM.
+  if (p.tile == 2 && blocks < 512 && p.nchunks >= 4) { p.tile = 12; blocks *= 2; }
+  // About two resident 256-thread groups on each of the 256 CUs; at most 8
+  // splits, and at least two chunks per split.
   const long target = 512;
   int splits = 1;
   if (blocks < target)
@@ -596,7 +650,7 @@ static void igemm_launch(const IgemmPlan& p, const ConvArgs& a, hipStream_t st) 
   if constexpr (SMALL)
     conv3x3_small_f32<T, DGRAD, E><<<grid, 256, T::LDS_BYTES, st>>>(k);
   else
-    conv3x3_igemm_f32<T, DGRAD, E><<<grid, 256, T::LDS_BYTES, st>>>(k);
+    conv3x3_igemm_f32<T, DGRAD, E><<<grid, T::THREADS, T::LDS_BYTES, st>>>(k);
   if (p.splits > 1) {
     size_t total = (size_t)a.N * a.Cout * a.H * a.W;
     conv_splitk_reduce<E><<<(unsigned)((total + 63) / 64), 256, 0, st>>>(
@@ -619,7 +673,8 @@ static void igemm_dispatch(const IgemmPlan& p, const ConvArgs& a, hipStream_t st
     case 8: igemm_launch<Small4, DGRAD, true, E>(p, a, st); break;
     case 9: igemm_launch<TileW32L, DGRAD, false, E>(p, a, st); break;
     case 10: igemm_launch<TileW16L, DGRAD, false, E>(p, a, st); break;
-    default: igemm_launch<TileW8L, DGRAD, false, E>(p, a, st); break;
+    case 11: igemm_launch<TileW8L, DGRAD, false, E>(p, a, st); break;
+    default: igemm_launch<TileW8K2, DGRAD, false, E>(p, a, st); break;
   }
 }
 

@@ -70,6 +70,8 @@ CONV_SHAPES = [
     (9, 40, 4, 4, 72),
     (33, 20, 2, 2, 130),     # more images than one tile holds, ragged
     (2, 12, 5, 37, 17),
+    (3, 40, 8, 8, 70),       # 8x8 two-group blocks, odd chunk count (groups uneven)
+    (2, 33, 9, 12, 20),      # the same with ragged rows and columns
     (1, 1, 1, 1, 1),         # degenerate: every tap but the centre is padding
     (1, 9, 3, 1, 5),
 ]
