@@ -8,45 +8,129 @@
 //             db  = (db +) column sums of G     [ns]
 // with G = dY, or dY * [mask > 0] (ReLU of this shard's output).
 //
-// One fp32 MFMA GEMM kernel serves the three products.  Operands are staged
-// in LDS as [k][m] and [k][n] (the MFMA-facing index contiguous) whatever
-// their layout in memory: a template flag says whether the global operand is
-// contiguous along the reduction index (then the copy into LDS transposes).
-// Block tile 128 x 128 x 16, four waves of 64 x 64 (4 x 4 MFMA 16x16 blocks),
-// double-buffered global -> register -> LDS pipeline.  When the output tile
-// count cannot fill the chip, the reduction is split over gridDim.z and
-// gemm_splitk_epilogue sums the splits in a fixed order.
+// One fp32 MFMA GEMM kernel serves the three products.  Block tile
+// 128 x 128 x 32, four waves of 64 x 64 (4 x 4 MFMA 16x16 blocks).  Each
+// operand keeps the layout it has in memory when it is staged in LDS:
+//   * contiguous along the reduction index ("K-contiguous"): [row][k], row
+//     stride 36 floats; a lane reads 4 consecutive k of its row (16 B), which
+//     feed four MFMA k-steps;
+//   * contiguous along its row index: [k][row], k stride 132 floats; a lane
+//     reads one float per k-step.
+// Inside each 16-wide slice of the reduction, MFMA k-step j takes element
+// k = 4*kq + j from lane group kq, for both operands, so the two layouts pair
+// up (any fixed order of the reduction gives the same sum up to rounding).
+// Both layouts are written and read without bank conflicts.  Global loads
+// are raw buffer loads whose out-of-range offsets read 0 (nothing waits on
+// them until the LDS store); the ReLU mask of dY is applied at that store.
+// When the output tiles cannot fill the chip the reduction is split over
+// gridDim.z, and gemm_splitk_epilogue sums the splits in a fixed order.
 #include "sb_internal.hpp"
 
 #include <algorithm>
 
 namespace sb {
 
-constexpr int GBM = 128, GBN = 128, GBK = 16;
-constexpr int GSTR = 128 + 16;         // LDS row stride (floats), = 16 mod 64
+constexpr int GBM = 128, GBN = 128, GBK = 32;
+constexpr int RK = GBK + 4;            // [row][k] row stride (floats)
+constexpr int RR = GBM + 4;            // [k][row] k stride (floats); 4 * RR = 16 mod 64
+constexpr int OPSZ = GBM * RK > GBK * RR ? GBM * RK : GBK * RR;   // floats per operand buffer
+constexpr size_t GEMM_LDS_BYTES = 2 * 2 * OPSZ * sizeof(float);    // 2 operands x 2 buffers
 
 struct GemmArgs {
-  const float* a; int lda;             // A element (m,k): K_CONTIG ? a[m*lda+k] : a[k*lda+m]
+  const float* a; int lda;             // A element (m,k): A_KC ? a[m*lda+k] : a[k*lda+m]
   const float* amask;                  // optional mask, same layout/stride as a
-  const float* b; int ldb;             // B element (k,n): K_CONTIG ? b[n*ldb+k] : b[k*ldb+n]
+  const float* b; int ldb;             // B element (k,n): B_KC ? b[n*ldb+k] : b[k*ldb+n]
   const float* bmask;
   float* c; int ldc;                   // C[m*ldc + n]
   int M, N, K;
   int k_per_split;
 };
 
-template <bool A_KCONTIG, bool B_KCONTIG>
-__global__ __launch_bounds__(256, 1) void gemm_f32(GemmArgs g, int partial,
+// One operand's staging: 1024 groups of 4 elements per 128 x 32 tile, 4 per
+// thread.  K-contiguous: group g = (k quad q = g / 128, row r = g % 128), the
+// 4 elements are 4 consecutive k of row r.  Row-contiguous: group g = (k =
+// g / 32, row quad = g % 32), the 4 elements are 4 consecutive rows.  VEC
+// loads each group with one 16-byte load (aligned, whole groups in range);
+// otherwise element by element.
+template <bool KC, bool VEC>
+struct OpStage {
+  f4 v[4];
+  __device__ __forceinline__ void load(rsrc_t r, rsrc_t rm, bool masked, int ld, int rows,
+                                       int r0, int k0, int ke, int tid) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int g = tid + i * 256;
+      const int row = KC ? r0 + (g & 127) : r0 + (g & 31) * 4;
+      const int k = KC ? k0 + (g >> 7) * 4 : k0 + (g >> 5);
+      f4 x, m = f4{1.f, 1.f, 1.f, 1.f};
+      if (VEC) {
+        const bool ok = row < rows && k < ke;       // whole group in range
+        const uint32_t off = ok ? (uint32_t)(KC ? row * ld + k : k * ld + row) * 4u : kOOB;
+        x = BufLoad<float>::four(r, off);
+        if (masked) m = BufLoad<float>::four(rm, off);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int rr = KC ? row : row + e, kk = KC ? k + e : k;
+          const bool ok = rr < rows && kk < ke;
+          const uint32_t off = ok ? (uint32_t)(KC ? rr * ld + kk : kk * ld + rr) * 4u : kOOB;
+          x[e] = BufLoad<float>::one(r, off);
+          if (masked) m[e] = BufLoad<float>::one(rm, off);
+        }
+      }
+      if (masked) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) x[e] = m[e] > 0.f ? x[e] : 0.f;
+      }
+      v[i] = x;
+    }
+  }
+  __device__ __forceinline__ void store(float* S, int tid) const {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int g = tid + i * 256;
+      float* p = KC ? S + (g & 127) * RK + (g >> 7) * 4 : S + (g >> 5) * RR + (g & 31) * 4;
+      *reinterpret_cast<f4*>(p) = v[i];
+    }
+  }
+};
+
+// Operand values of one 16-wide reduction slice for the four 16-row blocks of
+// a wave: f[blk][j] = element (row lr of block blk, k = 16*s + 4*kq + j).
+template <bool KC>
+__device__ __forceinline__ void frag16(const float* S, int row0, int s, int kq, int lr,
+                                       f4 (&f)[4]) {
+#pragma unroll
+  for (int blk = 0; blk < 4; ++blk) {
+    const int row = row0 + blk * 16 + lr;
+    if (KC) {
+      f[blk] = *reinterpret_cast<const f4*>(S + row * RK + s * 16 + kq * 4);
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) f[blk][j] = S[(s * 16 + kq * 4 + j) * RR + row];
+    }
+  }
+}
+
+template <bool A_KC, bool B_KC, bool VEC>
+__global__ __launch_bounds__(256, 2) void gemm_f32(GemmArgs g, int partial,
                                                    const float* __restrict__ bias, int relu,
                                                    int accumulate) {
-  __shared__ float As[2][GBK * GSTR];
-  __shared__ float Bs[2][GBK * GSTR];
+  extern __shared__ float lds[];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave & 1, wn = wave >> 1;
   const int kq = lane >> 4, lr = lane & 15;
   const int m0 = blockIdx.x * GBM, n0 = blockIdx.y * GBN;
   const int kb = blockIdx.z * g.k_per_split;
   const int ke = min(g.K, kb + g.k_per_split);
+  // Whole operand tensors (the host keeps them below 2^31 bytes).
+  const size_t a_elems = A_KC ? (size_t)(g.M - 1) * g.lda + g.K : (size_t)(g.K - 1) * g.lda + g.M;
+  const size_t b_elems = B_KC ? (size_t)(g.N - 1) * g.ldb + g.K : (size_t)(g.K - 1) * g.ldb + g.N;
+  const rsrc_t ra = make_rsrc(g.a, (uint32_t)(a_elems * 4));
+  const rsrc_t rb = make_rsrc(g.b, (uint32_t)(b_elems * 4));
+  const rsrc_t ram = make_rsrc(g.amask ? g.amask : g.a, (uint32_t)(a_elems * 4));
+  const rsrc_t rbm = make_rsrc(g.bmask ? g.bmask : g.b, (uint32_t)(b_elems * 4));
+  const bool amasked = g.amask != nullptr, bmasked = g.bmask != nullptr;
 
   f4 acc[4][4];
 #pragma unroll
@@ -54,73 +138,51 @@ __global__ __launch_bounds__(256, 1) void gemm_f32(GemmArgs g, int partial,
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
 
-  // 2048 elements per operand tile, 8 per thread.
-  float ra[8], rb[8];
-  auto load_op = [&](const float* p, const float* msk, int ld, bool kcontig, int rows, int r0,
-                     int k0, float* r) {
-    // Tile element (kk, rr): kk in [0,16), rr in [0,128).
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      int e = tid + i * 256;
-      int kk, rr;
-      if (kcontig) { rr = e / GBK; kk = e - rr * GBK; }   // consecutive threads walk k
-      else { kk = e / GBM; rr = e - kk * GBM; }            // consecutive threads walk rows
-      int row = r0 + rr, k = k0 + kk;
-      bool ok = row < rows && k < ke;
-      size_t off = kcontig ? (size_t)row * ld + k : (size_t)k * ld + row;
-      float v = ok ? p[off] : 0.f;
-      if (msk && ok && !(msk[off] > 0.f)) v = 0.f;
-      r[i] = v;
-    }
-  };
-  auto store_op = [&](float* S, bool kcontig, const float* r) {
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      int e = tid + i * 256;
-      int kk, rr;
-      if (kcontig) { rr = e / GBK; kk = e - rr * GBK; }
-      else { kk = e / GBM; rr = e - kk * GBM; }
-      S[kk * GSTR + rr] = r[i];
-    }
-  };
+  OpStage<A_KC, VEC> sa;
+  OpStage<B_KC, VEC> sb_;
+  auto Abuf = [&](int b) { return lds + b * 2 * OPSZ; };
+  auto Bbuf = [&](int b) { return lds + b * 2 * OPSZ + OPSZ; };
 
-  int nk = cdiv(ke - kb, GBK);
+  const int nk = cdiv(ke - kb, GBK);
   if (nk > 0) {
-    load_op(g.a, g.amask, g.lda, A_KCONTIG, g.M, m0, kb, ra);
-    load_op(g.b, g.bmask, g.ldb, B_KCONTIG, g.N, n0, kb, rb);
-    store_op(As[0], A_KCONTIG, ra);
-    store_op(Bs[0], B_KCONTIG, rb);
+    sa.load(ra, ram, amasked, g.lda, g.M, m0, kb, ke, tid);
+    sb_.load(rb, rbm, bmasked, g.ldb, g.N, n0, kb, ke, tid);
+    sa.store(Abuf(0), tid);
+    sb_.store(Bbuf(0), tid);
+    if (nk > 1) {
+      sa.load(ra, ram, amasked, g.lda, g.M, m0, kb + GBK, ke, tid);
+      sb_.load(rb, rbm, bmasked, g.ldb, g.N, n0, kb + GBK, ke, tid);
+    }
   }
   __syncthreads();
   for (int t = 0; t < nk; ++t) {
     const int buf = t & 1;
-    const bool more = t + 1 < nk;
-    if (more) {
-      load_op(g.a, g.amask, g.lda, A_KCONTIG, g.M, m0, kb + (t + 1) * GBK, ra);
-      load_op(g.b, g.bmask, g.ldb, B_KCONTIG, g.N, n0, kb + (t + 1) * GBK, rb);
+    if (t + 1 < nk) {
+      sa.store(Abuf(buf ^ 1), tid);
+      sb_.store(Bbuf(buf ^ 1), tid);
     }
-    const float* A = As[buf];
-    const float* B = Bs[buf];
-#pragma unroll
-    for (int ks = 0; ks < GBK / 4; ++ks) {
-      float av[4], bv[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) av[i] = A[(ks * 4 + kq) * GSTR + wm * 64 + i * 16 + lr];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) bv[j] = B[(ks * 4 + kq) * GSTR + wn * 64 + j * 16 + lr];
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = mfma16x16x4(av[i], bv[j], acc[i][j]);
+    if (t + 2 < nk) {
+      sa.load(ra, ram, amasked, g.lda, g.M, m0, kb + (t + 2) * GBK, ke, tid);
+      sb_.load(rb, rbm, bmasked, g.ldb, g.N, n0, kb + (t + 2) * GBK, ke, tid);
     }
-    if (more) {
-      store_op(As[buf ^ 1], A_KCONTIG, ra);
-      store_op(Bs[buf ^ 1], B_KCONTIG, rb);
+    const float* A = Abuf(buf);
+    const float* B = Bbuf(buf);
+#pragma unroll
+    for (int s = 0; s < GBK / 16; ++s) {
+      f4 fa[4], fb[4];
+      frag16<A_KC>(A, wm * 64, s, kq, lr, fa);
+      frag16<B_KC>(B, wn * 64, s, kq, lr, fb);
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int n = 0; n < 4; ++n) acc[i][n] = mfma16x16x4(fa[i][j], fb[n][j], acc[i][n]);
     }
     __syncthreads();
   }
 
-  // acc[i][j] lane holds C[m0 + wm*64 + i*16 + 4*kq + e][n0 + wn*64 + j*16 + lr].
+  // acc[i][n] lane holds C[m0 + wm*64 + i*16 + 4*kq + e][n0 + wn*64 + n*16 + lr].
   float* dst = g.c + (partial ? (size_t)blockIdx.z * g.M * g.ldc : 0);
 #pragma unroll
   for (int i = 0; i < 4; ++i)
@@ -129,13 +191,13 @@ __global__ __launch_bounds__(256, 1) void gemm_f32(GemmArgs g, int partial,
       int m = m0 + wm * 64 + i * 16 + 4 * kq + e;
       if (m >= g.M) continue;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        int n = n0 + wn * 64 + j * 16 + lr;
-        if (n >= g.N) continue;
-        float v = acc[i][j][e];
-        size_t o = (size_t)m * g.ldc + n;
+      for (int n = 0; n < 4; ++n) {
+        int col = n0 + wn * 64 + n * 16 + lr;
+        if (col >= g.N) continue;
+        float v = acc[i][n][e];
+        size_t o = (size_t)m * g.ldc + col;
         if (!partial) {
-          if (bias) v += bias[n];
+          if (bias) v += bias[col];
           if (relu && !(v > 0.f)) v = 0.f;
           if (accumulate) v += dst[o];
         }
@@ -160,19 +222,31 @@ __global__ __launch_bounds__(256) void gemm_splitk_epilogue(
   out[o] = v;
 }
 
-// db[j] = (db[j] +) sum_i G[i][j], rows summed in order.
-__global__ __launch_bounds__(256) void col_sum(const float* __restrict__ dy, const float* __restrict__ mask,
-                                               int M, int N, int ld, float* __restrict__ db,
-                                               int accumulate) {
-  int j = blockIdx.x * 256 + threadIdx.x;
-  if (j >= N) return;
-  float v = 0.f;
-  for (int i = 0; i < M; ++i) {
-    size_t o = (size_t)i * ld + j;
-    float g = dy[o];
-    if (mask && !(mask[o] > 0.f)) g = 0.f;
-    v += g;
+// db[j] = (db[j] +) sum_i G[i][j].  A block owns 64 columns; its 16 waves sum
+// every 16th row (four independent partial sums each, combined in a fixed
+// order), then the wave sums are added in order through LDS.
+__global__ __launch_bounds__(1024) void col_sum(const float* __restrict__ dy,
+                                                const float* __restrict__ mask, int M, int N,
+                                                int ld, float* __restrict__ db, int accumulate) {
+  __shared__ float part[16][64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int j = blockIdx.x * 64 + lane;
+  float s4[4] = {0.f, 0.f, 0.f, 0.f};
+  if (j < N) {
+    int u = 0;
+    for (int i = wave; i < M; i += 16, u = (u + 1) & 3) {
+      const size_t o = (size_t)i * ld + j;
+      float v = dy[o];
+      if (mask && !(mask[o] > 0.f)) v = 0.f;
+      s4[u] += v;
+    }
   }
+  part[wave][lane] = (s4[0] + s4[1]) + (s4[2] + s4[3]);
+  __syncthreads();
+  if (wave != 0 || j >= N) return;
+  float v = 0.f;
+#pragma unroll
+  for (int w = 0; w < 16; ++w) v += part[w][lane];
   db[j] = accumulate ? db[j] + v : v;
 }
 
@@ -183,15 +257,34 @@ static GemmPlan gemm_plan(int M, int N, int K) {
   p.mt = cdiv(M, GBM);
   p.nt = cdiv(N, GBN);
   long tiles = (long)p.mt * p.nt;
+  // About one block per CU, at least two k-tiles per split.
   const long target = 256;
-  int splits = 1;
-  if (tiles < target) splits = (int)std::min<long>(cdiv(K, GBK), cdiv((int)target, (int)tiles));
   int ktiles = cdiv(K, GBK);
+  int splits = 1;
+  if (tiles < target)
+    splits = (int)std::min<long>(std::max(1, ktiles / 2), cdiv((int)target, (int)tiles));
   int tps = cdiv(ktiles, splits);
   p.kps = tps * GBK;
   p.splits = cdiv(K, p.kps);
   p.ws_bytes = p.splits > 1 ? (size_t)p.splits * M * N * sizeof(float) : 0;
   return p;
+}
+
+static bool vec_ok(const void* p, int ld, int contiguous_extent) {
+  return ((uintptr_t)p & 15) == 0 && ld % 4 == 0 && contiguous_extent % 4 == 0;
+}
+
+template <bool AK, bool BK, bool VEC>
+static void gemm_launch(const GemmPlan& p, const GemmArgs& g, int partial, const float* bias,
+                        int relu, int accumulate, hipStream_t st) {
+  static bool attr_set = false;
+  if (!attr_set) {
+    (void)hipFuncSetAttribute((const void*)gemm_f32<AK, BK, VEC>,
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)GEMM_LDS_BYTES);
+    attr_set = true;
+  }
+  dim3 grid(p.mt, p.nt, p.splits);
+  gemm_f32<AK, BK, VEC><<<grid, 256, GEMM_LDS_BYTES, st>>>(g, partial, bias, relu, accumulate);
 }
 
 // C (ldc) = epi(A * B): the GEMM applies the epilogue itself when the
@@ -202,20 +295,27 @@ static sb_status gemm_run(GemmArgs g, const float* bias, int relu, int accumulat
                           size_t ws_bytes, hipStream_t st) {
   GemmPlan p = gemm_plan(g.M, g.N, g.K);
   if (p.ws_bytes > 0 && (!ws || ws_bytes < p.ws_bytes)) return SB_ERR_WORKSPACE;
+  // Buffer ranges cover whole operands.
+  const int64_t a_elems = AK ? (int64_t)(g.M - 1) * g.lda + g.K : (int64_t)(g.K - 1) * g.lda + g.M;
+  const int64_t b_elems = BK ? (int64_t)(g.N - 1) * g.ldb + g.K : (int64_t)(g.K - 1) * g.ldb + g.N;
+  if (a_elems * 4 >= (1ll << 31) || b_elems * 4 >= (1ll << 31)) return SB_ERR_UNSUPPORTED;
   g.k_per_split = p.kps;
-  dim3 grid(p.mt, p.nt, p.splits);
-  if (p.splits == 1) {
-    gemm_f32<AK, BK><<<grid, 256, 0, st>>>(g, 0, bias, relu, accumulate);
-    return SB_OK;
-  }
+  const bool vec = vec_ok(g.a, g.lda, AK ? g.K : g.M) && vec_ok(g.b, g.ldb, BK ? g.K : g.N) &&
+                   (!g.amask || vec_ok(g.amask, g.lda, AK ? g.K : g.M)) &&
+                   (!g.bmask || vec_ok(g.bmask, g.ldb, BK ? g.K : g.N)) && p.kps % 4 == 0;
   float* out = g.c;
   int ldo = g.ldc;
-  g.c = ws;
-  g.ldc = g.N;
-  gemm_f32<AK, BK><<<grid, 256, 0, st>>>(g, 1, nullptr, 0, 0);
-  size_t total = (size_t)g.M * g.N;
-  gemm_splitk_epilogue<<<(unsigned)((total + 255) / 256), 256, 0, st>>>(
-      ws, p.splits, g.M, g.N, g.N, out, ldo, bias, relu, accumulate);
+  const bool split = p.splits > 1;
+  if (split) { g.c = ws; g.ldc = g.N; }
+  if (vec) gemm_launch<AK, BK, true>(p, g, split, split ? nullptr : bias, split ? 0 : relu,
+                                     split ? 0 : accumulate, st);
+  else gemm_launch<AK, BK, false>(p, g, split, split ? nullptr : bias, split ? 0 : relu,
+                                  split ? 0 : accumulate, st);
+  if (split) {
+    size_t total = (size_t)g.M * g.N;
+    gemm_splitk_epilogue<<<(unsigned)((total + 255) / 256), 256, 0, st>>>(
+        ws, p.splits, g.M, g.N, g.N, out, ldo, bias, relu, accumulate);
+  }
   return SB_OK;
 }
 
@@ -313,7 +413,7 @@ extern "C" sb_status sb_fc_shard_bwd(const sb_fc_desc* d, const void* x, const v
     if (s != SB_OK) return s;
   }
   if (db)
-    col_sum<<<cdiv(d->n_shard, 256), 256, 0, st>>>((const float*)dy, (const float*)mask, d->m,
+    col_sum<<<cdiv(d->n_shard, 64), 1024, 0, st>>>((const float*)dy, (const float*)mask, d->m,
                                                    d->n_shard, d->ldy, db, accumulate);
   return sbh::launch_status();
 }
