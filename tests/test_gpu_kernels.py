@@ -271,3 +271,28 @@ def test_fc_strided_rows():
     assert rel_l2(to_host(dxp)[:, :kin], rdx) <= TOL["f32"]
     assert np.all(to_host(dxp)[:, kin:] == 5.0)
     assert rel_l2(to_host(dw), rdw) <= TOL["f32"]
+
+
+def test_fc_unaligned_operands():
+    """Operands that start off a 16-byte boundary take the element-wise
+    staging path; results are the same."""
+    m, kin, ns = 96, 128, 64
+    x, w, b, dy, mask = _fc_inputs(m, kin, ns, 25)
+    base = torch.zeros(m * kin + 1, device="cuda")
+    xd = base[1:].view(m, kin)
+    xd.copy_(to_dev(x))
+    df = sb.fc_desc(m, kin, ns, relu=True)
+    db_ = sb.fc_desc(m, kin, ns)
+    ws = _ws(max(sb.sb_fc_workspace_bytes(df, 0), sb.sb_fc_workspace_bytes(db_, 1)))
+    y = torch.empty((m, ns), device="cuda")
+    sb.sb_fc_shard_fwd(df, xd, to_dev(w), to_dev(b), y, ws)
+    dx = torch.empty((m, kin), device="cuda")
+    dw = torch.empty((kin, ns), device="cuda")
+    dbias = torch.empty((ns,), device="cuda")
+    sb.sb_fc_shard_bwd(db_, xd, to_dev(w), to_dev(dy), to_dev(mask), dx, dw, dbias, False, ws)
+    torch.cuda.synchronize()
+    assert rel_l2(to_host(y), O.fc_fwd(x, w, b, relu=True)) <= TOL["f32"]
+    rdx, rdw, rdb = O.fc_bwd(x, w, dy, mask_src=mask)
+    assert rel_l2(to_host(dx), rdx) <= TOL["f32"]
+    assert rel_l2(to_host(dw), rdw) <= TOL["f32"]
+    assert rel_l2(to_host(dbias), rdb) <= TOL["f32"]
