@@ -76,24 +76,54 @@ __device__ __forceinline__ float conv_epilogue(const ConvArgs& a, float v, int c
 // r = tap*CK + ci (stride BN_P) are written by consecutive lanes along a row:
 // conflict-free, like the MFMA operand reads (rows r..r+3, 16 consecutive co
 // per row, BN_P = 16 mod 64).  The packed filters live in the workspace.
+//
+// One block per slice: it reads the slice in the filters' own order (runs
+// of CK*9 contiguous elements per output channel, or BN*9 per input channel
+// for the data gradient), permutes it in LDS and writes it out contiguously.
 template <bool DGRAD, int CK, int BN, class E>
 __global__ __launch_bounds__(256) void filter_pack(const E* __restrict__ w, E* __restrict__ out,
                                                    int Cin, int Cout) {
   // Cin, Cout: this convolution's input and output channels (for the data
   // gradient: the forward layer's output and input channels).
+  constexpr int SL = 9 * CK * BN;
+  constexpr int RS = BN + 1;                          // padded LDS row: conflict-free writes
+  __shared__ E slice_lds[9 * CK * RS];
+  constexpr int PT = (SL + 255) / 256;
   const int nchunks = cdiv(Cin, CK);
   const int slice = blockIdx.x;                       // co tile * nchunks + chunk
   const int ct = slice / nchunks, kc = slice - ct * nchunks;
-  E* dst = out + (size_t)slice * (9 * CK * BN);
-  for (int e = threadIdx.x; e < 9 * CK * BN; e += 256) {
-    const int tap = e / (CK * BN), r = e - tap * (CK * BN);
-    const int cc = r / BN, nn = r - cc * BN;
-    const int co = ct * BN + nn, ci = kc * CK + cc;
-    E v{};
-    if (co < Cout && ci < Cin)
-      v = DGRAD ? w[((size_t)ci * Cout + co) * 9 + (8 - tap)] : w[((size_t)co * Cin + ci) * 9 + tap];
-    dst[e] = v;
+  // All loads first (PT per thread in flight), then the LDS permutation.
+  E v[PT];
+  int pos[PT];
+#pragma unroll
+  for (int i = 0; i < PT; ++i) {
+    const int g = threadIdx.x + i * 256;
+    int tap, cc, nn;
+    size_t src;
+    if (!DGRAD) {                                     // g = (nn, cc, tap), tap fastest
+      nn = g / (CK * 9);
+      const int r = g - nn * (CK * 9);
+      cc = r / 9;
+      tap = r - cc * 9;
+      src = ((size_t)(ct * BN + nn) * Cin + kc * CK + cc) * 9 + tap;
+    } else {                                          // g = (cc, nn, t), t fastest
+      cc = g / (BN * 9);
+      const int r = g - cc * (BN * 9);
+      nn = r / 9;
+      const int t = r - nn * 9;
+      tap = 8 - t;
+      src = ((size_t)(kc * CK + cc) * Cout + ct * BN + nn) * 9 + t;
+    }
+    const bool ok = g < SL && ct * BN + nn < Cout && kc * CK + cc < Cin;
+    v[i] = ok ? w[src] : E{};
+    pos[i] = g < SL ? (tap * CK + cc) * RS + nn : -1;
   }
+#pragma unroll
+  for (int i = 0; i < PT; ++i)
+    if (pos[i] >= 0) slice_lds[pos[i]] = v[i];
+  __syncthreads();
+  E* dst = out + (size_t)slice * SL;
+  for (int e = threadIdx.x; e < SL; e += 256) dst[e] = slice_lds[(e / BN) * RS + e % BN];
 }
 
 // Buffer resources of a block: its images of the input (from image n0 on)
@@ -540,7 +570,7 @@ __global__ __launch_bounds__(256) void conv_splitk_reduce(
   __shared__ float lds[256];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const size_t i = (size_t)blockIdx.x * 64 + lane;
-  float v = SplitSum{part, splits, total}(i, wave, lds, lane);
+  float v = SplitSum{part, splits, total, total}(i, wave, lds, lane);
   if (wave != 0 || i >= total) return;
   if (bias) v += bias[(i / HWs) % Cout];
   if (relu && !(v > 0.f)) v = 0.f;

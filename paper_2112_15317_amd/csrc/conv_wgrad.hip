@@ -44,7 +44,7 @@ struct WgArgs {
   const void* dy;        // [N][K][H][W], element type E
   float* dw;             // [K][C][3][3]
   float* db;             // [K] or null
-  float* part;           // split partials: [splits][K*C*9] then [splits][K]
+  float* part;           // split partials: [splits][K*C*9 + K] (dw, then db)
   int N, C, H, W, K;
   int tiles_w, tiles_h, ptiles, tiles_per_split, c_tiles, splits;
 };
@@ -91,20 +91,25 @@ __device__ __forceinline__ void wgrad_store(const WgArgs& a, int k_base, bool do
     each_db([&](float v, int k) { a.db[k] = v; });
     return;
   }
-  float* pw = a.part + (size_t)blockIdx.z * wsz;
-  float* pb = a.part + (size_t)a.splits * wsz + (size_t)blockIdx.z * a.K;
+  float* pw = a.part + (size_t)blockIdx.z * (wsz + a.K);
+  float* pb = pw + wsz;
   each([&](float v, size_t o) { pw[o] = v; });
   each_db([&](float v, int k) { pb[k] = v; });
 }
 
-// dst[i] = sum over the splits of part[s*total + i], in a fixed order.
+// Sum over the splits of part[s*stride + i], in a fixed order, for i < count:
+// dw[i] for i < wsz, then db[i - wsz].
 __global__ __launch_bounds__(256) void splits_reduce(const float* __restrict__ part, int splits,
-                                                     size_t total, float* __restrict__ dst) {
+                                                     size_t stride, size_t count, size_t wsz,
+                                                     float* __restrict__ dw,
+                                                     float* __restrict__ db) {
   __shared__ float lds[256];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const size_t i = (size_t)blockIdx.x * 64 + lane;
-  float v = SplitSum{part, splits, total}(i, wave, lds, lane);
-  if (wave == 0 && i < total) dst[i] = v;
+  float v = SplitSum{part, splits, stride, count}(i, wave, lds, lane);
+  if (wave != 0 || i >= count) return;
+  if (i < wsz) dw[i] = v;
+  else db[i - wsz] = v;
 }
 
 // ----------------------------------------------------------------- generic --
@@ -498,10 +503,9 @@ static void wg_launch(const WgPlan& p, const WgArgs& a, hipStream_t st) {
     conv3x3_wgrad_f32<T, E><<<grid, 256, T::LDS_BYTES, st>>>(a);
   if (p.splits > 1) {
     const size_t wsz = (size_t)a.K * a.C * 9;
-    splits_reduce<<<(unsigned)((wsz + 63) / 64), 256, 0, st>>>(a.part, p.splits, wsz, a.dw);
-    if (a.db)
-      splits_reduce<<<(unsigned)((a.K + 63) / 64), 256, 0, st>>>(
-          a.part + (size_t)p.splits * wsz, p.splits, (size_t)a.K, a.db);
+    const size_t count = wsz + (a.db ? a.K : 0);
+    splits_reduce<<<(unsigned)((count + 63) / 64), 256, 0, st>>>(a.part, p.splits, wsz + a.K,
+                                                                count, wsz, a.dw, a.db);
   }
 }
 

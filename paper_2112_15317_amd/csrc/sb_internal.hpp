@@ -104,24 +104,25 @@ template <> struct BufLoad<u16> {
 __host__ __device__ constexpr int cdiv(int a, int b) { return (a + b - 1) / b; }
 __host__ __device__ constexpr size_t round_up(size_t a, size_t b) { return (a + b - 1) / b * b; }
 
-// Deterministic sum of split-reduction partials: out[i] = sum_s part[s*total + i]
-// in a fixed order.  A block owns 64 consecutive outputs; its four waves each
-// sum every fourth split (s = wave, wave+4, ...) with several loads in
-// flight, then wave 0 adds the four wave sums in order.
+// Deterministic sum of split-reduction partials: out[i] = sum_s
+// part[s*stride + i] (i < count) in a fixed order.  A block owns 64
+// consecutive outputs; its four waves each sum every fourth split (s = wave,
+// wave+4, ...) with several loads in flight, then wave 0 adds the four wave
+// sums in order.
 struct SplitSum {
   const float* part;
   int splits;
-  size_t total;
+  size_t stride, count;
   __device__ __forceinline__ float operator()(size_t i, int wave, float* lds, int lane) const {
     float v = 0.f;
-    if (i < total) {
+    if (i < count) {
       int s = wave;
       for (; s + 12 < splits; s += 16) {
-        float a = part[(size_t)s * total + i], b = part[(size_t)(s + 4) * total + i];
-        float c = part[(size_t)(s + 8) * total + i], d = part[(size_t)(s + 12) * total + i];
+        float a = part[(size_t)s * stride + i], b = part[(size_t)(s + 4) * stride + i];
+        float c = part[(size_t)(s + 8) * stride + i], d = part[(size_t)(s + 12) * stride + i];
         v += a; v += b; v += c; v += d;
       }
-      for (; s < splits; s += 4) v += part[(size_t)s * total + i];
+      for (; s < splits; s += 4) v += part[(size_t)s * stride + i];
     }
     lds[wave * 64 + lane] = v;
     __syncthreads();
