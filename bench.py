@@ -2,7 +2,7 @@
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
                     [--workload vgg16-cifar-f32 | vgg16-imagenet-bf16 |
-                                fc-shard-f32 | hybrid-f32]
+                                fc-shard-f32 | hybrid-f32 | paper-variant-f32]
                     [--profile-pass]
 
 Default workload (the headline): one step of the 13-layer VGG-16 conv stack,
@@ -19,7 +19,10 @@ every input resident in HBM.  Other workloads:
   hybrid-f32           the worker step: the VGG-16 CIFAR stack on 128 local
                        images, FC0 (512 -> 1024 of 4096, ReLU) and FC1 (4096
                        -> 1024 of 4096) shards on the gathered batch of 512,
-                       then backward through both.
+                       then backward through both;
+  paper-variant-f32    the same worker step for the paper's own VGG variant
+                       (seven convs, FC 4096 -> 1024 -> 1024 -> 10) in an MP
+                       group of 2: 128 local images, 256 gathered rows.
 
 A step is one or several dozen kernel launches, so it is captured once in a
 HIP graph (through torch.cuda.graph: libsb enqueues on the current stream)
@@ -145,20 +148,26 @@ def fc_inputs(rows=None):
     return x, w, b, dy
 
 
-def hybrid_inputs(n):
+def hybrid_inputs(n, schedule, fc_shapes, group):
+    """Inputs of a worker step: conv stack on n local images, FC shards on the
+    rows gathered from `group` replicas, each FC split in `group` shards."""
     import numpy as np
-    from paper_2112_15317_amd import synth
-    layers, x, ws, bs, _ = vgg_inputs(n, 32, 1)
-    (in0, out0), (in1, out1) = HYBRID_FC
-    R = S = 4
-    m, ns0, ns1 = n * R, out0 // S, out1 // S
-    w0 = np.ascontiguousarray(synth.xavier_uniform(in0, out0, 0, synth.TID.FC_W + 0)[:, :ns0])
-    w1 = np.ascontiguousarray(synth.xavier_uniform(in1, out1, 0, synth.TID.FC_W + 1)[:, :ns1])
-    b0, b1 = np.zeros(ns0, np.float32), np.zeros(ns1, np.float32)
-    x0r = synth.relu_normal((m - n, in0), 0, synth.TID.X0_REMOTE)
-    x1r = synth.relu_normal((m, in1 - ns0), 0, synth.TID.X1_REMOTE)
-    dy1 = synth.normal((m, ns1), 0, synth.TID.FC_DY)
-    return layers, x, ws, bs, w0, b0, w1, b1, x0r, x1r, dy1
+    from paper_2112_15317_amd import configs, synth
+    layers = configs.conv_layers(schedule, 3, 32)
+    x = synth.normal((n, 3, 32, 32), 0, synth.TID.IMAGES)
+    ws = [synth.he_normal_conv3x3(L.k, L.c, 0, synth.TID.CONV_W + L.index) for L in layers]
+    bs = [np.zeros(L.k, np.float32) for L in layers]
+    m = n * group
+    ns = [fo // group for _, fo in fc_shapes]
+    fw = [np.ascontiguousarray(synth.xavier_uniform(fi, fo, 0, synth.TID.FC_W + j)[:, :ns[j]])
+          for j, (fi, fo) in enumerate(fc_shapes)]
+    fb = [np.zeros(k, np.float32) for k in ns]
+    rows = synth.relu_normal((m - n, fc_shapes[0][0]), 0, synth.TID.X0_REMOTE)
+    cols = [synth.relu_normal((m, fc_shapes[j][0] - ns[j - 1]), 0,
+                              synth.TID.X1_REMOTE if j == 1 else synth.TID.COLS_REMOTE + j)
+            for j in range(1, len(fc_shapes))]
+    dy = synth.normal((m, ns[-1]), 0, synth.TID.FC_DY)
+    return layers, x, ws, bs, fw, fb, rows, cols, dy
 
 
 # --------------------------------------------------------------- workloads --
@@ -263,49 +272,47 @@ class FcWorkload(Workload):
 
 
 class HybridWorkload(Workload):
-    name = "hybrid-f32"
     dtype = "f32"
     images = 128
-    metric = "images/sec/GPU hybrid worker step (VGG-16 CIFAR conv DP + FC shards MP), fp32"
-    text = ("hybrid worker step: VGG-16 CIFAR conv stack on 128 local images, then FC0 512->1024 "
-            "(of 4096, ReLU) and FC1 4096->1024 (of 4096) shards on the gathered 512 rows, "
-            "fwd+bwd, fp32")
+
+    def __init__(self, name, schedule, fc_shapes, group, metric, text):
+        self.name, self.schedule, self.fc_shapes, self.group = name, schedule, fc_shapes, group
+        self.metric, self.text = metric, text
 
     def build(self):
-        from paper_2112_15317_amd import configs
         from paper_2112_15317_amd.stack import HybridStep
-        inp = hybrid_inputs(self.images)
+        inp = hybrid_inputs(self.images, self.schedule, self.fc_shapes, self.group)
         self.layers = inp[0]
-        self.hs = HybridStep(configs.VGG16, self.images, 3, 32, 4, HYBRID_FC, 4)
+        self.hs = HybridStep(self.schedule, self.images, 3, 32, self.group, self.fc_shapes,
+                             self.group)
         self.hs.load_inputs(*inp[1:])
         return self.hs.step_calls()
 
     def flops(self):
         from paper_2112_15317_amd import configs
         f = configs.stack_flops(self.layers, self.images)
-        hs = self.hs
         extra = sum(fc_flops(s.desc_f, "fc_fwd") + fc_flops(s.desc_b, "fc_bwd")
-                    for s in (hs.fc0, hs.fc1))
+                    for s in self.hs.fc)
         return {"nominal": f["nominal"] + extra, "valid": f["valid"] + extra}
 
     def cpu_baseline(self, sample):
         import oracle
         from oracle import stack as OS
         n = self.images
-        layers, x, ws, bs, w0, b0, w1, b1, x0r, x1r, dy1 = hybrid_inputs(n)
+        layers, x, ws, bs, fw, fb, rows, cols, dy = hybrid_inputs(
+            n, self.schedule, self.fc_shapes, self.group)
         pools = [L.pool_after for L in layers]
-        reps = 1
         t0 = time.perf_counter()
-        for _ in range(reps):
-            OS.hybrid_step(x, ws, bs, pools, w0, b0, w1, b1, x0r, x1r, dy1)
+        OS.hybrid_step(x, ws, bs, pools, fw, fb, rows, cols, dy)
         dt = time.perf_counter() - t0
-        return {"value": round(reps * n / dt, 3), "unit": "images/s",
+        return {"value": round(n / dt, 3), "unit": "images/s",
                 "cores": oracle.num_threads(), "kind": "oracle",
-                "sample": "%d x the whole hybrid step, %d local images (fp64 oracle), %.1f s"
-                          % (reps, n, dt)}
+                "sample": "1 x the whole hybrid step, %d local images (fp64 oracle), %.1f s"
+                          % (n, dt)}
 
 
 def workloads():
+    from paper_2112_15317_amd import configs
     return {
         "vgg16-cifar-f32": VggWorkload(
             "vgg16-cifar-f32", 128, 32, "f32", CIFAR_METRIC,
@@ -318,7 +325,19 @@ def workloads():
             "VGG-16 ImageNet-shaped conv stack fwd+bwd (13 conv, 5 relu+maxpool), batch 32, "
             "3x224x224, bf16 activations and filters, fp32 accumulation, NCHW"),
         "fc-shard-f32": FcWorkload(),
-        "hybrid-f32": HybridWorkload(),
+        "hybrid-f32": HybridWorkload(
+            "hybrid-f32", configs.VGG16, HYBRID_FC, 4,
+            "images/sec/GPU hybrid worker step (VGG-16 CIFAR conv DP + FC shards MP), fp32",
+            "hybrid worker step: VGG-16 CIFAR conv stack on 128 local images, then FC0 "
+            "512->1024 (of 4096, ReLU) and FC1 4096->1024 (of 4096) shards on the gathered 512 "
+            "rows, fwd+bwd, fp32"),
+        "paper-variant-f32": HybridWorkload(
+            "paper-variant-f32", configs.PAPER_VARIANT_CONV, configs.PAPER_VARIANT_FC, 2,
+            "images/sec/GPU hybrid worker step of the paper's VGG variant (Table 1), fp32",
+            "the paper's VGG variant as one worker of an MP group of 2: seven 3x3 convs "
+            "(64,64,M,128,128,M,256,256,256,M) on 128 local 3x32x32 images, then FC "
+            "4096->1024->1024->10 split in 2 column shards on the gathered 256 rows, fwd+bwd, "
+            "fp32"),
     }
 
 

@@ -80,34 +80,41 @@ def vgg_step(x, weights, biases, pool_after, dy_top, bf16=False, want_dx=True):
     return f, b
 
 
-def hybrid_step(x, weights, biases, pool_after, fc0_w, fc0_b, fc1_w, fc1_b,
-                x0_remote, x1_remote, dy1):
-    """One worker's step of the hybrid scheme on one device.
+def hybrid_step(x, weights, biases, pool_after, fc_w, fc_b, rows_remote, cols_remote, dy):
+    """One worker's step of the hybrid scheme on one device, with L FC shards.
 
-    The local conv stack output (flattened, one row per image) fills the
-    first rows of the gathered FC0 input; ``x0_remote`` supplies the rows of
-    the other replicas.  FC0's shard output (ReLU) fills the first feature
-    columns of FC1's input; ``x1_remote`` supplies the other shards' columns.
-    Backward: FC1's partial input gradient restricted to this shard's own
-    columns, masked by FC0's ReLU, is FC0's output gradient; FC0's partial
-    input gradient restricted to this replica's rows is the gradient of the
-    conv stack output.  (The cross-worker sums of the partial gradients are
-    collectives and are not part of one worker's compute.)
+    The local conv stack output (flattened, one row per image, NCHW order)
+    fills the first rows of the gathered FC0 input; ``rows_remote`` supplies
+    the rows of the other replicas.  The shard output of FC j-1 (ReLU) fills
+    the first feature columns of FC j's input; ``cols_remote[j-1]`` supplies
+    the other shards' columns.  The last shard's output has no ReLU and
+    receives the gradient ``dy``.  Backward: FC j's partial input gradient
+    restricted to this shard's own columns of the layer below, masked by that
+    layer's ReLU, is its output gradient; FC0's partial input gradient
+    restricted to this replica's rows is the gradient of the conv stack
+    output.  (The cross-worker sums of the partial gradients are collectives
+    and are not part of one worker's compute.)
     """
+    L = len(fc_w)
     f = vgg_forward(x, weights, biases, pool_after)
     top = f["A"][-1]
     n = top.shape[0]
     feat = int(np.prod(top.shape[1:]))
-    x0 = np.concatenate([top.reshape(n, feat), np.asarray(x0_remote, np.float64)], axis=0)
-    y0 = fc_fwd(x0, fc0_w, fc0_b, relu=True)
-    ns0 = y0.shape[1]
-    x1 = np.concatenate([y0, np.asarray(x1_remote, np.float64)], axis=1)
-    y1 = fc_fwd(x1, fc1_w, fc1_b, relu=False)
-    dx1p, dw1, db1 = fc_bwd(x1, fc1_w, dy1)
-    dy0 = np.ascontiguousarray(dx1p[:, :ns0])
-    dx0p, dw0, db0 = fc_bwd(x0, fc0_w, dy0, mask_src=y0)
-    dtop = np.ascontiguousarray(dx0p[:n]).reshape(top.shape)
+    xs = [np.concatenate([top.reshape(n, feat), np.asarray(rows_remote, np.float64)], axis=0)]
+    ys = []
+    for j in range(L):
+        y = fc_fwd(xs[j], fc_w[j], fc_b[j], relu=j < L - 1)
+        ys.append(y)
+        if j < L - 1:
+            xs.append(np.concatenate([y, np.asarray(cols_remote[j], np.float64)], axis=1))
+    dxp, dw, db, dys = [None] * L, [None] * L, [None] * L, [None] * L
+    g = np.asarray(dy, np.float64)
+    for j in reversed(range(L)):
+        dys[j] = g
+        dxp[j], dw[j], db[j] = fc_bwd(xs[j], fc_w[j], g,
+                                      mask_src=ys[j] if j < L - 1 else None)
+        if j > 0:
+            g = np.ascontiguousarray(dxp[j][:, :ys[j - 1].shape[1]])
+    dtop = np.ascontiguousarray(dxp[0][:n]).reshape(top.shape)
     b = vgg_backward(f, weights, pool_after, dtop)
-    return {"fwd": f, "bwd": b, "x0": x0, "y0": y0, "x1": x1, "y1": y1,
-            "dx1p": dx1p, "dw1": dw1, "db1": db1, "dy0": dy0,
-            "dx0p": dx0p, "dw0": dw0, "db0": db0}
+    return {"fwd": f, "bwd": b, "xs": xs, "ys": ys, "dys": dys, "dxp": dxp, "dw": dw, "db": db}

@@ -213,63 +213,85 @@ class FCShard:
 
 
 class HybridStep:
-    """Conv stack on the local batch, then the FC shards on the gathered batch.
+    """Conv stack on the local batch, then L FC shards on the gathered batch.
 
-    X0 [R*n, F]: rows [0, n) are this replica's flattened conv output (the
-    stack writes them in place), rows [n, R*n) hold the other replicas'
-    rows.  X1 [R*n, S*ns0]: columns [0, ns0) are FC0's shard output (written
-    in place, ReLU), the rest hold the other shards' columns.  Backward: FC1's
-    partial input gradient restricted to this shard's columns is FC0's output
-    gradient (masked by FC0's ReLU inside the call); FC0's partial input
-    gradient restricted to this replica's rows is the conv stack's upstream
-    gradient.  The cross-worker sums are collectives, not part of this step.
+    X[0] [R*n, F]: rows [0, n) are this replica's flattened conv output (the
+    stack writes them in place, NCHW order per image), rows [n, R*n) hold the
+    other replicas' rows.  X[j] [R*n, in_j] for j >= 1: columns [0, ns_{j-1})
+    are FC j-1's shard output (written in place, ReLU), the rest hold the
+    other shards' columns.  The last shard's output Y has no ReLU.  Backward:
+    FC j's partial input gradient restricted to this shard's columns of the
+    layer below is that layer's output gradient (masked by its ReLU inside
+    the call); FC0's partial input gradient restricted to this replica's rows
+    is the conv stack's upstream gradient.  The cross-worker sums are
+    collectives, not part of this step.
     """
 
     def __init__(self, schedule, n, in_ch, hw, replicas, fc_shapes, shards, device="cuda"):
         dev = torch.device(device)
         self.n, self.R = n, replicas
         m = n * replicas
-        (in0, out0), (in1, out1) = fc_shapes
-        ns0, ns1 = out0 // shards, out1 // shards
-        assert in1 == out0
-        self.m, self.in0, self.ns0, self.in1, self.ns1 = m, in0, ns0, in1, ns1
-        self.X0 = torch.empty((m, in0), dtype=torch.float32, device=dev)
-        self.dX0p = torch.empty((m, in0), dtype=torch.float32, device=dev)
-        self.X1 = torch.empty((m, in1), dtype=torch.float32, device=dev)
-        self.dX1p = torch.empty((m, in1), dtype=torch.float32, device=dev)
-        self.Y1 = torch.empty((m, ns1), dtype=torch.float32, device=dev)
-        self.dY1 = torch.empty((m, ns1), dtype=torch.float32, device=dev)
+        self.m, self.L = m, len(fc_shapes)
+        self.ins = [fi for fi, _ in fc_shapes]
+        self.ns = [fo // shards for _, fo in fc_shapes]
+        for j in range(1, self.L):
+            assert self.ins[j] == fc_shapes[j - 1][1]
+        f32 = dict(dtype=torch.float32, device=dev)
+        self.X = [torch.empty((m, fi), **f32) for fi in self.ins]
+        self.dXp = [torch.empty((m, fi), **f32) for fi in self.ins]
+        self.Y = torch.empty((m, self.ns[-1]), **f32)
+        self.dY = torch.empty((m, self.ns[-1]), **f32)
         self.conv = ConvStack(schedule, n, in_ch, hw, "f32", device,
-                              out_buffer=self.X0[:n], out_grad_buffer=self.dX0p[:n])
+                              out_buffer=self.X[0][:n], out_grad_buffer=self.dXp[0][:n])
         top = self.conv.A[-1]
-        assert int(np.prod(top.shape[1:])) == in0
-        self.fc0 = FCShard(m, in0, ns0, relu=True, ldx=in0, ldy=in1, device=device)
-        self.fc1 = FCShard(m, in1, ns1, relu=False, ldx=in1, ldy=ns1, device=device)
+        assert int(np.prod(top.shape[1:])) == self.ins[0]
+        last = self.L - 1
+        self.fc = [FCShard(m, self.ins[j], self.ns[j], relu=j < last, ldx=self.ins[j],
+                           ldy=self.ins[j + 1] if j < last else self.ns[j], device=device)
+                   for j in range(self.L)]
         self.call = _plain      # hook: every libsb call of the step goes through it
 
-    def load_inputs(self, x, conv_w, conv_b, fc0_w, fc0_b, fc1_w, fc1_b, x0_remote, x1_remote,
-                    dy1):
+    # Two-layer names used by the tests of the four-replica worker step.
+    X0 = property(lambda self: self.X[0])
+    X1 = property(lambda self: self.X[1])
+    dX0p = property(lambda self: self.dXp[0])
+    dX1p = property(lambda self: self.dXp[1])
+    Y1 = property(lambda self: self.Y)
+    fc0 = property(lambda self: self.fc[0])
+    fc1 = property(lambda self: self.fc[1])
+
+    def load_inputs(self, x, conv_w, conv_b, fc_w, fc_b, rows_remote, cols_remote, dy):
+        """fc_w / fc_b: the shard weights and biases per layer; rows_remote:
+        the other replicas' rows of X[0]; cols_remote[j-1]: the other shards'
+        columns of X[j]; dy: the gradient of the last shard's output."""
         t = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32))
         self.conv.load_inputs(x, conv_w, conv_b)
-        self.fc0.W.copy_(t(fc0_w)); self.fc0.b.copy_(t(fc0_b))
-        self.fc1.W.copy_(t(fc1_w)); self.fc1.b.copy_(t(fc1_b))
-        self.X0[self.n:].copy_(t(x0_remote))
-        self.X1[:, self.ns0:].copy_(t(x1_remote))
-        self.dY1.copy_(t(dy1))
+        for f, w, b in zip(self.fc, fc_w, fc_b):
+            f.W.copy_(t(w))
+            f.b.copy_(t(b))
+        self.X[0][self.n:].copy_(t(rows_remote))
+        for j in range(1, self.L):
+            self.X[j][:, self.ns[j - 1]:].copy_(t(cols_remote[j - 1]))
+        self.dY.copy_(t(dy))
 
     def step(self, stream=None):
         def c(key, call):
             fn, args = call
             self.call(key, fn, *args)
         self.conv.forward(stream)
-        X0, X1 = self.X0.data_ptr(), self.X1.data_ptr()
-        c(("fc_fwd", 0), self.fc0.fwd_call(X0, X1, stream))          # Y0 -> X1[:, :ns0]
-        c(("fc_fwd", 1), self.fc1.fwd_call(X1, self.Y1.data_ptr(), stream))
-        c(("fc_bwd", 1), self.fc1.bwd_call(X1, self.dY1.data_ptr(), None,
-                                           self.dX1p.data_ptr(), stream=stream))
-        # FC0's output gradient: dX1p[:, :ns0] (row stride in1), ReLU mask X1[:, :ns0].
-        c(("fc_bwd", 0), self.fc0.bwd_call(X0, self.dX1p.data_ptr(), X1,
-                                           self.dX0p.data_ptr(), stream=stream))
+        L = self.L
+        X = [x.data_ptr() for x in self.X]
+        for j in range(L):
+            out = X[j + 1] if j + 1 < L else self.Y.data_ptr()
+            c(("fc_fwd", j), self.fc[j].fwd_call(X[j], out, stream))
+        for j in reversed(range(L)):
+            # Output gradient of layer j: the given dY, or layer j+1's partial
+            # input gradient on this shard's columns (row stride in_{j+1}),
+            # masked by layer j's ReLU output X[j+1][:, :ns_j].
+            dy = self.dY.data_ptr() if j == L - 1 else self.dXp[j + 1].data_ptr()
+            mask = None if j == L - 1 else X[j + 1]
+            c(("fc_bwd", j), self.fc[j].bwd_call(X[j], dy, mask, self.dXp[j].data_ptr(),
+                                                 stream=stream))
         self.conv.backward(stream)
 
     def step_calls(self):

@@ -38,6 +38,7 @@ class TID:
     X1_REMOTE = 501       # feature columns of the other shards (FC1 input)
     FC_DY = 502           # upstream gradient of the last FC shard
     FC_X = 600            # standalone FC-shard input
+    COLS_REMOTE = 700     # + FC layer index (>= 2): other shards' columns of its input
     MISC = 900            # + anything a test needs
 
 

@@ -264,42 +264,72 @@ def test_vgg16_imagenet_bf16_stack_full_size_properties():
         del g, sel, dz
 
 
-def test_hybrid_worker_step_end_to_end():
-    n, hw, R, S = 2, 32, 4, 4
-    print_case("hybrid_step", n=n, replicas=R, shards=S)
-    layers = configs.conv_layers(configs.VGG16, 3, hw)
-    x, wts, bs = _vgg_inputs(n, hw, 6, layers)
-    (in0, out0), (in1, out1) = configs.CONFIGS[4]["fc"]
-    m, ns0, ns1 = n * R, out0 // S, out1 // S
-    w0 = np.ascontiguousarray(synth.xavier_uniform(in0, out0, 6, synth.TID.FC_W + 0)[:, :ns0])
-    w1 = np.ascontiguousarray(synth.xavier_uniform(in1, out1, 6, synth.TID.FC_W + 1)[:, :ns1])
-    b0 = synth.normal((ns0,), 6, synth.TID.FC_B + 0, std=0.05)
-    b1 = synth.normal((ns1,), 6, synth.TID.FC_B + 1, std=0.05)
-    x0r = synth.relu_normal((m - n, in0), 6, synth.TID.X0_REMOTE)
-    x1r = synth.relu_normal((m, in1 - ns0), 6, synth.TID.X1_REMOTE)
-    dy1 = synth.normal((m, ns1), 6, synth.TID.FC_DY)
-    hs = HybridStep(configs.VGG16, n, 3, hw, R, [(in0, out0), (in1, out1)], S)
-    hs.load_inputs(x, wts, bs, w0, b0, w1, b1, x0r, x1r, dy1)
-    hs.step()
-    torch.cuda.synchronize()
-    pools = [L.pool_after for L in layers]
-    r = OS.hybrid_step(x, wts, bs, pools, w0, b0, w1, b1, x0r, x1r, dy1)
+def _hybrid_inputs(n, hw, R, S, schedule, fc_shapes, seed):
+    layers = configs.conv_layers(schedule, 3, hw)
+    x, wts, bs = _vgg_inputs(n, hw, seed, layers)
+    m = n * R
+    ns = [fo // S for _, fo in fc_shapes]
+    fw = [np.ascontiguousarray(synth.xavier_uniform(fi, fo, seed, synth.TID.FC_W + j)[:, :ns[j]])
+          for j, (fi, fo) in enumerate(fc_shapes)]
+    fb = [synth.normal((ns[j],), seed, synth.TID.FC_B + j, std=0.05) for j in range(len(ns))]
+    rows = synth.relu_normal((m - n, fc_shapes[0][0]), seed, synth.TID.X0_REMOTE)
+    cols = [synth.relu_normal((m, fc_shapes[j][0] - ns[j - 1]), seed,
+                              synth.TID.X1_REMOTE if j == 1 else synth.TID.COLS_REMOTE + j)
+            for j in range(1, len(fc_shapes))]
+    dy = synth.normal((m, ns[-1]), seed, synth.TID.FC_DY)
+    return layers, x, wts, bs, fw, fb, rows, cols, dy
+
+
+def _check_hybrid(hs, r, layers):
     tol = TOL["f32"]
-    assert rel_l2(to_host(hs.X0), r["x0"]) <= tol
-    assert rel_l2(to_host(hs.X1), r["x1"]) <= tol
-    assert rel_l2(to_host(hs.Y1), r["y1"]) <= tol
-    assert rel_l2(to_host(hs.dX1p), r["dx1p"]) <= tol
-    assert rel_l2(to_host(hs.fc1.dW), r["dw1"]) <= tol
-    assert rel_l2(to_host(hs.fc1.db), r["db1"]) <= tol
-    assert rel_l2(to_host(hs.dX0p), r["dx0p"]) <= tol
-    assert rel_l2(to_host(hs.fc0.dW), r["dw0"]) <= tol
-    assert rel_l2(to_host(hs.fc0.db), r["db0"]) <= tol
+    for j in range(hs.L):
+        assert rel_l2(to_host(hs.X[j]), r["xs"][j]) <= tol, "X%d" % j
+        assert rel_l2(to_host(hs.dXp[j]), r["dxp"][j]) <= tol, "dXp%d" % j
+        assert rel_l2(to_host(hs.fc[j].dW), r["dw"][j]) <= tol, "dW_fc%d" % j
+        assert rel_l2(to_host(hs.fc[j].db), r["db"][j]) <= tol, "db_fc%d" % j
+    assert rel_l2(to_host(hs.Y), r["ys"][-1]) <= tol
     for L in layers:
         i = L.index
         if L.pool_after:
             np.testing.assert_array_equal(hs.conv.idx[i].cpu().numpy(), r["fwd"]["idx"][i])
         assert rel_l2(to_host(hs.conv.dW[i]), r["bwd"]["dW"][i]) <= tol, "dW%d" % i
     assert rel_l2(to_host(hs.conv.gA[0]), r["bwd"]["dX"]) <= tol
+
+
+def test_hybrid_worker_step_end_to_end():
+    """VGG-16 conv stack, then FC0 512 -> 1024 (of 4096) and FC1 4096 -> 1024
+    (of 4096) shards on the rows gathered from 4 replicas."""
+    n, hw, R, S = 2, 32, 4, 4
+    print_case("hybrid_step", n=n, replicas=R, shards=S)
+    fc_shapes = configs.CONFIGS[4]["fc"]
+    layers, x, wts, bs, fw, fb, rows, cols, dy = _hybrid_inputs(
+        n, hw, R, S, configs.VGG16, fc_shapes, 6)
+    hs = HybridStep(configs.VGG16, n, 3, hw, R, fc_shapes, S)
+    hs.load_inputs(x, wts, bs, fw, fb, rows, cols, dy)
+    hs.step()
+    torch.cuda.synchronize()
+    pools = [L.pool_after for L in layers]
+    r = OS.hybrid_step(x, wts, bs, pools, fw, fb, rows, cols, dy)
+    _check_hybrid(hs, r, layers)
+
+
+def test_paper_variant_hybrid_step_end_to_end():
+    """The paper's own VGG variant (Table 1: seven convs, three pools, FC
+    4096 -> 1024 -> 1024 -> 10) as a worker of an MP group of 2: the flattened
+    256x4x4 conv output feeds FC0, every FC layer is split in two column
+    shards (512, 512 and 5 outputs here)."""
+    n, hw, R, S = 3, 32, 2, 2
+    print_case("paper_variant_hybrid", n=n, replicas=R, shards=S)
+    fc_shapes = configs.PAPER_VARIANT_FC
+    layers, x, wts, bs, fw, fb, rows, cols, dy = _hybrid_inputs(
+        n, hw, R, S, configs.PAPER_VARIANT_CONV, fc_shapes, 7)
+    hs = HybridStep(configs.PAPER_VARIANT_CONV, n, 3, hw, R, fc_shapes, S)
+    hs.load_inputs(x, wts, bs, fw, fb, rows, cols, dy)
+    hs.step()
+    torch.cuda.synchronize()
+    pools = [L.pool_after for L in layers]
+    r = OS.hybrid_step(x, wts, bs, pools, fw, fb, rows, cols, dy)
+    _check_hybrid(hs, r, layers)
 
 
 def test_graph_replay_matches_eager():

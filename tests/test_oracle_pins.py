@@ -314,33 +314,41 @@ def test_vgg_stack_matches_torch_autograd():
 
 
 def test_hybrid_step_matches_torch_autograd():
+    """Three FC shards (ReLU, ReLU, linear) after a two-conv stack, with
+    remote rows and remote shard columns as constants: the oracle's chain of
+    restricted partial gradients equals autograd of the same graph."""
     n, rep = 2, 3
     sched = [(3, 4, True), (4, 8, True)]          # 4x4 -> 2x2 -> 1x1, 8 features
     x = rng.standard_normal((n, 3, 4, 4))
     ws = [rng.standard_normal((k, c, 3, 3)) for c, k, _ in sched]
     bs = [np.zeros(k) for _, k, _ in sched]
     pools = [p for *_, p in sched]
-    w0 = rng.standard_normal((8, 5)); b0 = rng.standard_normal(5)
-    w1 = rng.standard_normal((5 + 7, 4)); b1 = rng.standard_normal(4)
-    x0r = np.maximum(rng.standard_normal((n * (rep - 1), 8)), 0)
-    x1r = np.maximum(rng.standard_normal((n * rep, 7)), 0)
-    dy1 = rng.standard_normal((n * rep, 4))
-    r = OS.hybrid_step(x, ws, bs, pools, w0, b0, w1, b1, x0r, x1r, dy1)
+    # FC j: local shard ns_j of the layer's outputs; the next layer's input is
+    # ns_j local columns + remote columns.
+    ns, remote = [5, 6, 4], [7, 3]
+    ins = [8, ns[0] + remote[0], ns[1] + remote[1]]
+    fw = [rng.standard_normal((ins[j], ns[j])) for j in range(3)]
+    fb = [rng.standard_normal(ns[j]) for j in range(3)]
+    rows = np.maximum(rng.standard_normal((n * (rep - 1), 8)), 0)
+    cols = [np.maximum(rng.standard_normal((n * rep, remote[j])), 0) for j in range(2)]
+    dy = rng.standard_normal((n * rep, ns[2]))
+    r = OS.hybrid_step(x, ws, bs, pools, fw, fb, rows, cols, dy)
     # torch: the same graph, remote stand-ins as constants; gradients flow to
     # the local rows / local columns only, exactly as the restriction does.
     xt = _t(x, True); wt = [_t(w, True) for w in ws]
     a = xt
     for l, w in enumerate(wt):
         a = torch.relu(F.max_pool2d(F.conv2d(a, w, padding=1), 2, 2))
-    x0 = torch.cat([a.reshape(n, 8), _t(x0r)], 0)
-    w0t, w1t = _t(w0, True), _t(w1, True)
-    y0 = torch.relu(x0 @ w0t + _t(b0))
-    x1 = torch.cat([y0, _t(x1r)], 1)
-    y1 = x1 @ w1t + _t(b1)
-    y1.backward(_t(dy1))
-    np.testing.assert_allclose(r["y1"], y1.detach().numpy(), rtol=1e-11, atol=1e-12)
-    np.testing.assert_allclose(r["dw1"], w1t.grad.numpy(), rtol=1e-11, atol=1e-12)
-    np.testing.assert_allclose(r["dw0"], w0t.grad.numpy(), rtol=1e-11, atol=1e-12)
+    h = torch.cat([a.reshape(n, 8), _t(rows)], 0)
+    fwt = [_t(w, True) for w in fw]
+    for j in range(3):
+        h = h @ fwt[j] + _t(fb[j])
+        if j < 2:
+            h = torch.cat([torch.relu(h), _t(cols[j])], 1)
+    h.backward(_t(dy))
+    np.testing.assert_allclose(r["ys"][2], h.detach().numpy(), rtol=1e-11, atol=1e-12)
+    for j in range(3):
+        np.testing.assert_allclose(r["dw"][j], fwt[j].grad.numpy(), rtol=1e-10, atol=1e-11)
     np.testing.assert_allclose(r["bwd"]["dX"], xt.grad.numpy(), rtol=1e-10, atol=1e-11)
     for l in range(2):
         np.testing.assert_allclose(r["bwd"]["dW"][l], wt[l].grad.numpy(), rtol=1e-10, atol=1e-11)
