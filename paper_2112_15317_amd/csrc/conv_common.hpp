@@ -1,0 +1,128 @@
+// conv_common.hpp -- pieces shared by the 3x3 convolution kernels (fp32
+// MFMA path and bf16 MFMA path): launch arguments, epilogue, buffer
+// resources and the split reduction.
+#pragma once
+
+#include "sb_internal.hpp"
+
+namespace sb {
+
+// Element type E of in / wt / mask / out: float or bf16 bits (u16).
+// Accumulation, bias and split partials are fp32.
+struct ConvArgs {
+  const void* in;        // [N][Cin][H][W]
+  const void* wt;        // forward filters [K][C][3][3]
+  const void* wpk;       // the same, packed by filter_pack (workspace)
+  const float* bias;     // [Cout] or null (forward)
+  const void* mask;      // [N][Cout][H][W] or null (data gradient)
+  void* out;             // [N][Cout][H][W]
+  float* part;           // split partials [splits][N][Cout][H][W]
+  int N, Cin, H, W, Cout;
+  int tiles_w, tiles_h, nchunks, chunks_per_split, splits, relu;
+};
+
+template <class E>
+__device__ __forceinline__ float conv_epilogue(const ConvArgs& a, float v, int co, size_t off) {
+  if (a.bias) v += a.bias[co];
+  if (a.relu && !(v > 0.f)) v = 0.f;
+  if (a.mask && !(Elem<E>::load((const E*)a.mask, off) > 0.f)) v = 0.f;
+  return v;
+}
+
+// Filters are repacked before the convolution (filter_pack) into the order
+// the kernels stage them: for output-channel tile t (BN channels) and input-
+// channel chunk k (CK channels), 9*CK*BN contiguous elements ordered
+// [tap][ci][co], zero where a channel lies past the end.  For the data
+// gradient the same pass transposes (co <-> ci) and rotates the taps by 180
+// degrees.  A chunk's slice is then one coalesced read, and its LDS rows
+// r = tap*CK + ci (stride BN_P) are written by consecutive lanes along a row:
+// conflict-free, like the MFMA operand reads (rows r..r+3, 16 consecutive co
+// per row, BN_P = 16 mod 64).  The packed filters live in the workspace.
+//
+// One block per slice: it reads the slice in the filters' own order (runs
+// of CK*9 contiguous elements per output channel, or BN*9 per input channel
+// for the data gradient), permutes it in LDS and writes it out contiguously.
+//
+// CI_INNER packs each slice [tap][co][ci] instead (input channels innermost),
+// the order of the bf16 kernels, whose lanes read 4 consecutive channels.
+template <bool DGRAD, int CK, int BN, class E, bool CI_INNER = false>
+__global__ __launch_bounds__(256) void filter_pack(const E* __restrict__ w, E* __restrict__ out,
+                                                   int Cin, int Cout) {
+  // Cin, Cout: this convolution's input and output channels (for the data
+  // gradient: the forward layer's output and input channels).
+  constexpr int SL = 9 * CK * BN;
+  // Padded LDS rows (one extra element) keep the permuting writes spread
+  // over the banks.
+  constexpr int ROW = CI_INNER ? CK : BN, RS = ROW + 1;
+  __shared__ E slice_lds[SL / ROW * RS];
+  constexpr int PT = (SL + 255) / 256;
+  const int nchunks = cdiv(Cin, CK);
+  const int slice = blockIdx.x;                       // co tile * nchunks + chunk
+  const int ct = slice / nchunks, kc = slice - ct * nchunks;
+  // All loads first (PT per thread in flight), then the LDS permutation.
+  E v[PT];
+  int pos[PT];
+#pragma unroll
+  for (int i = 0; i < PT; ++i) {
+    const int g = threadIdx.x + i * 256;
+    int tap, cc, nn;
+    size_t src;
+    if (!DGRAD) {                                     // g = (nn, cc, tap), tap fastest
+      nn = g / (CK * 9);
+      const int r = g - nn * (CK * 9);
+      cc = r / 9;
+      tap = r - cc * 9;
+      src = ((size_t)(ct * BN + nn) * Cin + kc * CK + cc) * 9 + tap;
+    } else {                                          // g = (cc, nn, t), t fastest
+      cc = g / (BN * 9);
+      const int r = g - cc * (BN * 9);
+      nn = r / 9;
+      const int t = r - nn * 9;
+      tap = 8 - t;
+      src = ((size_t)(kc * CK + cc) * Cout + ct * BN + nn) * 9 + t;
+    }
+    const bool ok = g < SL && ct * BN + nn < Cout && kc * CK + cc < Cin;
+    v[i] = ok ? w[src] : E{};
+    pos[i] = g < SL ? (CI_INNER ? (tap * BN + nn) * RS + cc : (tap * CK + cc) * RS + nn) : -1;
+  }
+#pragma unroll
+  for (int i = 0; i < PT; ++i)
+    if (pos[i] >= 0) slice_lds[pos[i]] = v[i];
+  __syncthreads();
+  E* dst = out + (size_t)slice * SL;
+  for (int e = threadIdx.x; e < SL; e += 256) dst[e] = slice_lds[(e / ROW) * RS + e % ROW];
+}
+
+// Buffer resources of a block: its images of the input (from image n0 on)
+// and the whole filter tensor.
+template <class E>
+__device__ __forceinline__ rsrc_t input_rsrc(const ConvArgs& a, int n0, int imgs) {
+  const size_t img = (size_t)a.Cin * a.H * a.W;
+  const int cnt = min(imgs, a.N - n0);
+  return make_rsrc((const E*)a.in + n0 * img, (uint32_t)(cnt * img * sizeof(E)));
+}
+// The packed filter slices of output-channel tile `ct` (all chunks).
+template <class E, int WTS>
+__device__ __forceinline__ rsrc_t packed_rsrc(const ConvArgs& a, int ct) {
+  return make_rsrc((const E*)a.wpk + (size_t)ct * a.nchunks * WTS,
+                   (uint32_t)((size_t)a.nchunks * WTS * sizeof(E)));
+}
+
+// Sum of the split partials in a fixed order, then the epilogue.
+template <class E>
+__global__ __launch_bounds__(256) void conv_splitk_reduce(
+    const float* __restrict__ part, int splits, size_t total, int Cout, int HWs,
+    const float* __restrict__ bias, int relu, const E* __restrict__ mask,
+    E* __restrict__ out) {
+  __shared__ float lds[256];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const size_t i = (size_t)blockIdx.x * 64 + lane;
+  float v = SplitSum{part, splits, total, total}(i, wave, lds, lane);
+  if (wave != 0 || i >= total) return;
+  if (bias) v += bias[(i / HWs) % Cout];
+  if (relu && !(v > 0.f)) v = 0.f;
+  if (mask && !(Elem<E>::load(mask, i) > 0.f)) v = 0.f;
+  Elem<E>::store(out, i, v);
+}
+
+}  // namespace sb

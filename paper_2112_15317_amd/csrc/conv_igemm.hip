@@ -38,108 +38,12 @@
 // applies the epilogue.  (Reducing inside the kernel with a last-block
 // counter needs device-scope fences, which write back the per-XCD L2s on
 // this chip and cost far more than the extra launch.)
-#include "sb_internal.hpp"
+#include "conv_common.hpp"
 
 #include <algorithm>
 #include <cstdio>
 
 namespace sb {
-
-// Element type E of in / wt / mask / out: float or bf16 bits (u16).
-// Accumulation, bias and split partials are fp32.
-struct ConvArgs {
-  const void* in;        // [N][Cin][H][W]
-  const void* wt;        // forward filters [K][C][3][3]
-  const void* wpk;       // the same, packed by filter_pack (workspace)
-  const float* bias;     // [Cout] or null (forward)
-  const void* mask;      // [N][Cout][H][W] or null (data gradient)
-  void* out;             // [N][Cout][H][W]
-  float* part;           // split partials [splits][N][Cout][H][W]
-  int N, Cin, H, W, Cout;
-  int tiles_w, tiles_h, nchunks, chunks_per_split, splits, relu;
-};
-
-template <class E>
-__device__ __forceinline__ float conv_epilogue(const ConvArgs& a, float v, int co, size_t off) {
-  if (a.bias) v += a.bias[co];
-  if (a.relu && !(v > 0.f)) v = 0.f;
-  if (a.mask && !(Elem<E>::load((const E*)a.mask, off) > 0.f)) v = 0.f;
-  return v;
-}
-
-// Filters are repacked before the convolution (filter_pack) into the order
-// the kernels stage them: for output-channel tile t (BN channels) and input-
-// channel chunk k (CK channels), 9*CK*BN contiguous elements ordered
-// [tap][ci][co], zero where a channel lies past the end.  For the data
-// gradient the same pass transposes (co <-> ci) and rotates the taps by 180
-// degrees.  A chunk's slice is then one coalesced read, and its LDS rows
-// r = tap*CK + ci (stride BN_P) are written by consecutive lanes along a row:
-// conflict-free, like the MFMA operand reads (rows r..r+3, 16 consecutive co
-// per row, BN_P = 16 mod 64).  The packed filters live in the workspace.
-//
-// One block per slice: it reads the slice in the filters' own order (runs
-// of CK*9 contiguous elements per output channel, or BN*9 per input channel
-// for the data gradient), permutes it in LDS and writes it out contiguously.
-template <bool DGRAD, int CK, int BN, class E>
-__global__ __launch_bounds__(256) void filter_pack(const E* __restrict__ w, E* __restrict__ out,
-                                                   int Cin, int Cout) {
-  // Cin, Cout: this convolution's input and output channels (for the data
-  // gradient: the forward layer's output and input channels).
-  constexpr int SL = 9 * CK * BN;
-  constexpr int RS = BN + 1;                          // padded LDS row: conflict-free writes
-  __shared__ E slice_lds[9 * CK * RS];
-  constexpr int PT = (SL + 255) / 256;
-  const int nchunks = cdiv(Cin, CK);
-  const int slice = blockIdx.x;                       // co tile * nchunks + chunk
-  const int ct = slice / nchunks, kc = slice - ct * nchunks;
-  // All loads first (PT per thread in flight), then the LDS permutation.
-  E v[PT];
-  int pos[PT];
-#pragma unroll
-  for (int i = 0; i < PT; ++i) {
-    const int g = threadIdx.x + i * 256;
-    int tap, cc, nn;
-    size_t src;
-    if (!DGRAD) {                                     // g = (nn, cc, tap), tap fastest
-      nn = g / (CK * 9);
-      const int r = g - nn * (CK * 9);
-      cc = r / 9;
-      tap = r - cc * 9;
-      src = ((size_t)(ct * BN + nn) * Cin + kc * CK + cc) * 9 + tap;
-    } else {                                          // g = (cc, nn, t), t fastest
-      cc = g / (BN * 9);
-      const int r = g - cc * (BN * 9);
-      nn = r / 9;
-      const int t = r - nn * 9;
-      tap = 8 - t;
-      src = ((size_t)(kc * CK + cc) * Cout + ct * BN + nn) * 9 + t;
-    }
-    const bool ok = g < SL && ct * BN + nn < Cout && kc * CK + cc < Cin;
-    v[i] = ok ? w[src] : E{};
-    pos[i] = g < SL ? (tap * CK + cc) * RS + nn : -1;
-  }
-#pragma unroll
-  for (int i = 0; i < PT; ++i)
-    if (pos[i] >= 0) slice_lds[pos[i]] = v[i];
-  __syncthreads();
-  E* dst = out + (size_t)slice * SL;
-  for (int e = threadIdx.x; e < SL; e += 256) dst[e] = slice_lds[(e / BN) * RS + e % BN];
-}
-
-// Buffer resources of a block: its images of the input (from image n0 on)
-// and the whole filter tensor.
-template <class E>
-__device__ __forceinline__ rsrc_t input_rsrc(const ConvArgs& a, int n0, int imgs) {
-  const size_t img = (size_t)a.Cin * a.H * a.W;
-  const int cnt = min(imgs, a.N - n0);
-  return make_rsrc((const E*)a.in + n0 * img, (uint32_t)(cnt * img * sizeof(E)));
-}
-// The packed filter slices of output-channel tile `ct` (all chunks).
-template <class E, int WTS>
-__device__ __forceinline__ rsrc_t packed_rsrc(const ConvArgs& a, int ct) {
-  return make_rsrc((const E*)a.wpk + (size_t)ct * a.nchunks * WTS,
-                   (uint32_t)((size_t)a.nchunks * WTS * sizeof(E)));
-}
 
 // ----------------------------------------------------------------- generic --
 template <int TH_, int TW_, int IMGS_, int CK_, int BN_, int WAVES_N_, int KSPLIT_ = 1>
@@ -561,23 +465,6 @@ __global__ __launch_bounds__(256, 2) void conv3x3_small_f32(ConvArgs a) {
   for_each_out4([&](f4 v, int, size_t off) { *reinterpret_cast<f4*>(mine + off) = v; });
 }
 
-// Sum of the split partials in a fixed order, then the epilogue.
-template <class E>
-__global__ __launch_bounds__(256) void conv_splitk_reduce(
-    const float* __restrict__ part, int splits, size_t total, int Cout, int HWs,
-    const float* __restrict__ bias, int relu, const E* __restrict__ mask,
-    E* __restrict__ out) {
-  __shared__ float lds[256];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const size_t i = (size_t)blockIdx.x * 64 + lane;
-  float v = SplitSum{part, splits, total, total}(i, wave, lds, lane);
-  if (wave != 0 || i >= total) return;
-  if (bias) v += bias[(i / HWs) % Cout];
-  if (relu && !(v > 0.f)) v = 0.f;
-  if (mask && !(Elem<E>::load(mask, i) > 0.f)) v = 0.f;
-  Elem<E>::store(out, i, v);
-}
-
 // ---------------------------------------------------------------- host --
 struct IgemmPlan {
   int tile;          // index into the tile table
@@ -713,7 +600,17 @@ static void igemm_dispatch(const IgemmPlan& p, const ConvArgs& a, hipStream_t st
 // Entry points used by api.hip.
 namespace sbh {
 
+// The bf16 MFMA path (conv_bf16.hip) for the bf16 shapes it takes.
+size_t conv_bf16_ws(int N, int Cin, int H, int W, int Cout);
+bool conv_bf16_takes(int N, int Cin, int H, int W, int Cout);
+int conv_bf16_describe(bool dgrad, int N, int Cin, int H, int W, int Cout, char* buf, size_t len);
+sb_status conv_bf16(bool dgrad, int N, int Cin, int H, int W, int Cout, const void* in,
+                    const void* wt, const float* bias, const void* mask, void* out, void* ws,
+                    size_t ws_bytes, int relu, hipStream_t st);
+
 size_t conv_igemm_ws(int dtype, int N, int Cin, int H, int W, int Cout) {
+  if (dtype == SB_BF16 && conv_bf16_takes(N, Cin, H, W, Cout))
+    return conv_bf16_ws(N, Cin, H, W, Cout);
   const int es = (int)dsize(dtype);
   return std::max(sb::igemm_plan(N, Cin, H, W, Cout, es, true).ws_bytes,
                   sb::igemm_plan(N, Cin, H, W, Cout, es, false).ws_bytes);
@@ -721,6 +618,8 @@ size_t conv_igemm_ws(int dtype, int N, int Cin, int H, int W, int Cout) {
 
 int conv_igemm_describe(bool dgrad, int dtype, int N, int Cin, int H, int W, int Cout,
                         char* buf, size_t len) {
+  if (dtype == SB_BF16 && conv_bf16_takes(N, Cin, H, W, Cout))
+    return conv_bf16_describe(dgrad, N, Cin, H, W, Cout, buf, len);
   sb::IgemmPlan p = sb::igemm_plan(N, Cin, H, W, Cout, (int)dsize(dtype));
   char name[160];
   snprintf(name, sizeof(name), sb::kTileNames[p.tile], dgrad ? "true" : "false",
@@ -731,6 +630,8 @@ int conv_igemm_describe(bool dgrad, int dtype, int N, int Cin, int H, int W, int
 sb_status conv_igemm(bool dgrad, int dtype, int N, int Cin, int H, int W, int Cout,
                      const void* in, const void* wt, const float* bias, const void* mask,
                      void* out, void* ws, size_t ws_bytes, int relu, hipStream_t st) {
+  if (dtype == SB_BF16 && conv_bf16_takes(N, Cin, H, W, Cout))
+    return conv_bf16(dgrad, N, Cin, H, W, Cout, in, wt, bias, mask, out, ws, ws_bytes, relu, st);
   // The whole-image kernels move 4 elements at a time (16 bytes in fp32, 8 in
   // bf16); the plan only picks them for tensors aligned that far.
   const uintptr_t amask = dtype == SB_BF16 ? 7 : 15;
