@@ -8,7 +8,7 @@ size_t conv_igemm_ws(int dtype, int N, int Cin, int H, int W, int Cout);
 sb_status conv_igemm(bool dgrad, int dtype, int N, int Cin, int H, int W, int Cout,
                      const void* in, const void* wt, const float* bias, const void* mask,
                      void* out, void* ws, size_t ws_bytes, int relu, hipStream_t st);
-size_t conv_wgrad_ws(int N, int C, int H, int W, int K);
+size_t conv_wgrad_ws(int dtype, int N, int C, int H, int W, int K);
 int conv_igemm_describe(bool dgrad, int dtype, int N, int Cin, int H, int W, int Cout, char* buf,
                         size_t len);
 int conv_wgrad_describe(int dtype, int N, int C, int H, int W, int K, char* buf, size_t len);
@@ -48,7 +48,7 @@ extern "C" size_t sb_conv3x3_workspace_bytes(const sb_conv3x3_desc* d, int pass)
   switch (pass) {
     case SB_PASS_FWD: return sbh::conv_igemm_ws(d->dtype, d->n, d->c, d->h, d->w, d->k);
     case SB_PASS_BWD_DATA: return sbh::conv_igemm_ws(d->dtype, d->n, d->k, d->h, d->w, d->c);
-    default: return sbh::conv_wgrad_ws(d->n, d->c, d->h, d->w, d->k);
+    default: return sbh::conv_wgrad_ws(d->dtype, d->n, d->c, d->h, d->w, d->k);
   }
 }
 
@@ -111,7 +111,7 @@ extern "C" sb_status sb_conv3x3_bwd_weight(const sb_conv3x3_desc* d, const void*
       sbh::overlaps(db, dbb, x, xb) || sbh::overlaps(db, dbb, dy, dyb) ||
       sbh::overlaps(dw, dwb, db, dbb))
     return SB_ERR_INVALID_ARG;
-  size_t need = sbh::conv_wgrad_ws(d->n, d->c, d->h, d->w, d->k);
+  size_t need = sbh::conv_wgrad_ws(d->dtype, d->n, d->c, d->h, d->w, d->k);
   if (need && (!ws || ws_bytes < need)) return SB_ERR_WORKSPACE;
   if (need && (sbh::overlaps(ws, need, dw, dwb) || sbh::overlaps(ws, need, db, dbb) ||
                sbh::overlaps(ws, need, x, xb) || sbh::overlaps(ws, need, dy, dyb)))

@@ -36,6 +36,7 @@
 
 #include <algorithm>
 #include <cstdio>
+#include <type_traits>
 
 namespace sb {
 
@@ -285,6 +286,299 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_f32(WgArgs a) {
       });
 }
 
+// --------------------------------------------------------- bf16 MFMA --
+// Weight gradient with bf16 operands on the bf16 MFMA
+// (v_mfma_f32_16x16x32_bf16, fp32 accumulate).  The same GEMM as the fp32
+// wide layout (rows = 64 output channels, columns = BC input channels x 9
+// taps, reduction over the 64 pixels of a tile per LDS stage), but a lane of
+// this MFMA supplies 8 consecutive pixels of its row / column, so a tile
+// row (TW = 32, 16 or 8 columns) is read in 16-byte pieces:
+//   * dy tile in LDS as [k][pixel] (rows of 64 pixels, pitch 72 bf16);
+//   * x halo in LDS as [c][halo row][column], stored three times: copy s
+//     holds halo columns s .. s+TW-1, i.e. the x values column tap s reads,
+//     so the 8 pixels a lane reads at tap (r, s) are 16 aligned bytes of
+//     copy s.  Channel planes sit 8 * odd words apart, so the 16 channels of
+//     a 16-lane group land in distinct bank groups.
+// With BC = 32 the four waves form a 2 x 2 grid, each wave 32 k x 16 c, so a
+// B operand read from LDS feeds two MFMAs.  The bias gradient is one more
+// MFMA per 16 k rows and step against a column of ones.
+//
+// Staging moves V consecutive columns per lane (V = 8, 4, 2 when the image
+// width is a multiple of V, else 1): one global load of V elements per tile
+// row piece, one LDS store per copy.  The copies shifted by one column take
+// the missing element from the neighbouring lane (a DPP row shift) or, at
+// the tile's left and right edges, from a separate 2-byte load.  A thread
+// owns a fixed column piece and a fixed set of rows, so every offset is a
+// per-tile base plus a compile-time constant.
+template <int TH_, int TW_, int BC_>
+struct WgBTile {
+  static constexpr int TH = TH_, TW = TW_, BC = BC_;
+  static constexpr int BP = TH * TW;                 // pixels per tile
+  static_assert(BP == 64 && TW % 8 == 0, "64-pixel tiles of 8-pixel row groups");
+  static constexpr int BK = 64;
+  static_assert(BC == 16 || BC == 32, "16 or 32 input channels per block");
+  static constexpr int WC = BC / 16;                 // waves along c
+  static constexpr int MA = WC;                      // 16-row blocks of k per wave
+  static constexpr int HH = TH + 2;
+  static constexpr int PLANE = HH * TW;              // one channel of one copy
+  static constexpr int plane_pitch(int p) { return (p / 2) % 8 == 4 ? p : plane_pitch(p + 8); }
+  static constexpr int PLANE_P = plane_pitch(PLANE);
+  static constexpr int DYP = BP + 8;                 // dy row pitch: 36 words
+  static constexpr int LDS_DY = BK * DYP;            // bf16 elements
+  static constexpr int LDS_XC = BC * PLANE_P;        // one shifted copy
+  static constexpr int LDS_BUF = LDS_DY + 3 * LDS_XC;
+  static_assert(PLANE % 8 == 0 && LDS_DY % 8 == 0 && LDS_XC % 8 == 0, "16-byte reads");
+  static constexpr size_t LDS_BYTES = 2 * LDS_BUF * sizeof(u16);
+  static_assert(LDS_BYTES <= 80 * 1024, "two blocks must fit in the 160 KB of LDS");
+};
+
+typedef short s8 __attribute__((ext_vector_type(8)));
+
+// V consecutive bf16 in V/2 dwords (V >= 2); element 2j in the low half of
+// dword j.
+template <int V> struct Vec { uint32_t d[V / 2]; };
+
+template <int V>
+__device__ __forceinline__ Vec<V> load_vec(rsrc_t r, uint32_t off) {
+  Vec<V> v;
+  if constexpr (V == 8) {
+    typedef uint32_t u4 __attribute__((ext_vector_type(4)));
+    u4 t = __builtin_bit_cast(u4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0));
+    v.d[0] = t[0]; v.d[1] = t[1]; v.d[2] = t[2]; v.d[3] = t[3];
+  } else if constexpr (V == 4) {
+    typedef uint32_t u2 __attribute__((ext_vector_type(2)));
+    u2 t = __builtin_bit_cast(u2, __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, 0));
+    v.d[0] = t[0]; v.d[1] = t[1];
+  } else {
+    v.d[0] = __builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, 0);
+  }
+  return v;
+}
+
+template <int V>
+__device__ __forceinline__ void store_vec(u16* p, const Vec<V>& v) {
+  if constexpr (V == 8) {
+    typedef uint32_t u4 __attribute__((ext_vector_type(4)));
+    *reinterpret_cast<u4*>(p) = u4{v.d[0], v.d[1], v.d[2], v.d[3]};
+  } else if constexpr (V == 4) {
+    typedef uint32_t u2 __attribute__((ext_vector_type(2)));
+    *reinterpret_cast<u2*>(p) = u2{v.d[0], v.d[1]};
+  } else {
+    *reinterpret_cast<uint32_t*>(p) = v.d[0];
+  }
+}
+
+template <class T, int V>
+__global__ __launch_bounds__(256, 2) void conv3x3_wgrad_bf16(WgArgs a) {
+  extern __shared__ u16 ldsw[];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int kq = lane >> 4, lr = lane & 15;
+  const int ct = blockIdx.x % a.c_tiles, kt = blockIdx.x / a.c_tiles;
+  const int c0 = ct * T::BC, k0 = kt * T::BK;
+  const int pt0 = blockIdx.z * a.tiles_per_split;
+  const int pt1 = min(a.ptiles, pt0 + a.tiles_per_split);
+  const int wc = wave % T::WC, wk = wave / T::WC;
+  const bool do_db = (a.db != nullptr) && ct == 0 && wc == 0;
+  const int HWs = a.H * a.W;
+
+  f4 acc[T::MA][9], accb[T::MA];
+#pragma unroll
+  for (int m = 0; m < T::MA; ++m) {
+    accb[m] = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int t = 0; t < 9; ++t) acc[m][t] = f4{0.f, 0.f, 0.f, 0.f};
+  }
+  s8 ones;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) ones[j] = 0x3f80;     // bf16 1.0
+
+  // Staging geometry: LPR lanes per tile row piece of TW columns, RPI rows
+  // per round of 256 threads.  dy rows are (k, tile row), k-major; x rows
+  // (halo row, c), c fastest.
+  constexpr int VV = V;
+  constexpr int LPR = T::TW / VV, RPI = 256 / LPR;
+  constexpr int DY_I = T::BK * T::TH / RPI;
+  constexpr int XROWS = T::HH * T::BC;
+  constexpr int X_I = (XROWS + RPI - 1) / RPI;
+  static_assert(RPI % T::TH == 0 && T::BK * T::TH % RPI == 0, "whole dy rounds");
+  static_assert(VV == 1 || 16 % LPR == 0, "a tile row piece within one DPP row");
+  const int vc = tid % LPR, col = vc * VV, r0 = tid / LPR;
+  const int dk = r0 / T::TH, dyy = r0 % T::TH;
+  const int kleft = a.K - k0 - dk;
+
+  // Next tile to load, advanced after every load.
+  int ntx = pt0 % a.tiles_w, nty = (pt0 / a.tiles_w) % a.tiles_h,
+      nn = pt0 / (a.tiles_w * a.tiles_h);
+
+  // Registers holding the tile in flight.
+  typedef typename std::conditional<(VV > 1), Vec<(VV > 1 ? VV : 2)>, u16>::type Piece;
+  Piece rdy[DY_I], rx[X_I];
+  u16 rel[X_I], rer[X_I];
+
+  auto gload = [&]() {
+    const int h0 = nty * T::TH, w0 = ntx * T::TW, n0 = nn;
+    if (++ntx == a.tiles_w) {
+      ntx = 0;
+      if (++nty == a.tiles_h) { nty = 0; ++nn; }
+    }
+    const rsrc_t dr = image_rsrc<u16>(a.dy, n0, 1, a.N, a.K * HWs);
+    const rsrc_t xr = image_rsrc<u16>(a.x, n0, 1, a.N, a.C * HWs);
+    const bool w_ok = w0 + col < a.W;
+    {
+      const bool ok = w_ok && h0 + dyy < a.H;
+      const int base = (k0 + dk) * HWs + (h0 + dyy) * a.W + w0 + col;
+#pragma unroll
+      for (int i = 0; i < DY_I; ++i) {
+        const int dki = (RPI / T::TH) * i;
+        const uint32_t off = ok && dki < kleft ? (uint32_t)(base + dki * HWs) * 2u : kOOB;
+        if constexpr (VV > 1) rdy[i] = load_vec<VV>(dr, off);
+        else rdy[i] = (u16)__builtin_amdgcn_raw_buffer_load_b16(dr, (int)off, 0, 0);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < X_I; ++i) {
+      const int r = r0 + RPI * i;
+      const int cc = r % T::BC, hy = r / T::BC;
+      const int h = h0 - 1 + hy, c = c0 + cc;
+      const bool row_ok = (XROWS % RPI == 0 || r < XROWS) && c < a.C &&
+                          (unsigned)h < (unsigned)a.H;
+      const int rbase = c * HWs + h * a.W + w0;
+      // Interior columns col .. col+V-1 of the tile (halo columns col+1 ..).
+      const uint32_t off = row_ok && w_ok ? (uint32_t)(rbase + col) * 2u : kOOB;
+      if constexpr (VV > 1) rx[i] = load_vec<VV>(xr, off);
+      else rx[i] = (u16)__builtin_amdgcn_raw_buffer_load_b16(xr, (int)off, 0, 0);
+      // Edge columns w0 - 1 (first piece of a row) and w0 + TW (last piece).
+      const bool l_ok = row_ok && vc == 0 && w0 > 0;
+      const bool r_ok = row_ok && vc == LPR - 1 && w0 + T::TW < a.W;
+      if constexpr (LPR == 1) {
+        rel[i] = (u16)__builtin_amdgcn_raw_buffer_load_b16(
+            xr, l_ok ? (int)((uint32_t)(rbase - 1) * 2u) : (int)kOOB, 0, 0);
+        rer[i] = (u16)__builtin_amdgcn_raw_buffer_load_b16(
+            xr, r_ok ? (int)((uint32_t)(rbase + T::TW) * 2u) : (int)kOOB, 0, 0);
+      } else {
+        const uint32_t eoff = l_ok ? (uint32_t)(rbase - 1) * 2u
+                              : r_ok ? (uint32_t)(rbase + T::TW) * 2u : kOOB;
+        rel[i] = (u16)__builtin_amdgcn_raw_buffer_load_b16(xr, (int)eoff, 0, 0);
+      }
+    }
+  };
+  auto lstore = [&](int buf) {
+    u16* Dl = ldsw + buf * T::LDS_BUF;
+    u16* Xl = Dl + T::LDS_DY;
+    {
+      u16* q = Dl + dk * T::DYP + dyy * T::TW + col;
+#pragma unroll
+      for (int i = 0; i < DY_I; ++i) {
+        if constexpr (VV > 1) store_vec<VV>(q + (RPI / T::TH) * i * T::DYP, rdy[i]);
+        else q[(RPI / T::TH) * i * T::DYP] = rdy[i];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < X_I; ++i) {
+      const int r = r0 + RPI * i;
+      if (XROWS % RPI != 0 && r >= XROWS) continue;
+      const int cc = r % T::BC, hy = r / T::BC;
+      u16* q = Xl + cc * T::PLANE_P + hy * T::TW + col;
+      // Copy s at column j holds halo column j + s, i.e. x column
+      // w0 + j + s - 1: copy 1 is the loaded piece itself, copy 0 the piece
+      // shifted right by one element, copy 2 shifted left by one.
+      if constexpr (VV > 1) {
+        constexpr int D = VV / 2;
+        const Vec<VV>& v = rx[i];
+        uint32_t left, right;     // x columns col - 1 and col + V (low 16 bits)
+        if constexpr (LPR == 1) {
+          left = rel[i];
+          right = rer[i];
+        } else {
+          // 0x111: row_shr:1 (lane - 1), 0x101: row_shl:1 (lane + 1).
+          const uint32_t pl = (uint32_t)__builtin_amdgcn_mov_dpp((int)v.d[D - 1], 0x111, 0xf, 0xf, true);
+          const uint32_t pr = (uint32_t)__builtin_amdgcn_mov_dpp((int)v.d[0], 0x101, 0xf, 0xf, true);
+          left = vc == 0 ? (uint32_t)rel[i] : pl >> 16;
+          right = vc == LPR - 1 ? (uint32_t)rel[i] : pr & 0xffffu;
+        }
+        Vec<VV> s0, s2;
+        s0.d[0] = (v.d[0] << 16) | (left & 0xffffu);
+#pragma unroll
+        for (int j = 1; j < D; ++j) s0.d[j] = (v.d[j] << 16) | (v.d[j - 1] >> 16);
+#pragma unroll
+        for (int j = 0; j + 1 < D; ++j) s2.d[j] = (v.d[j + 1] << 16) | (v.d[j] >> 16);
+        s2.d[D - 1] = (right << 16) | (v.d[D - 1] >> 16);
+        store_vec<VV>(q, s0);
+        store_vec<VV>(q + T::LDS_XC, v);
+        store_vec<VV>(q + 2 * T::LDS_XC, s2);
+      } else {
+        // One column per lane: copy 0 at col + 1, copy 1 at col, copy 2 at
+        // col - 1; the edge columns fill copy 0 at 0 and copy 2 at TW - 1.
+        if (col + 1 < T::TW) q[1] = rx[i];
+        q[T::LDS_XC] = rx[i];
+        if (col >= 1) q[2 * T::LDS_XC - 1] = rx[i];
+        if (col == 0) q[0] = rel[i];
+        if (col == T::TW - 1) q[2 * T::LDS_XC] = rel[i];
+      }
+    }
+  };
+  auto compute = [&](int buf) {
+    const u16* Dl = ldsw + buf * T::LDS_BUF;
+    const u16* Xl = Dl + T::LDS_DY;
+#pragma unroll
+    for (int st = 0; st < T::BP / 32; ++st) {
+      // Lane group kq takes pixels p .. p+7 of this 32-pixel step.
+      const int p = st * 32 + 8 * kq;
+      const int yy = p / T::TW, xx = p % T::TW;
+      s8 av[T::MA];
+#pragma unroll
+      for (int m = 0; m < T::MA; ++m)
+        av[m] = *reinterpret_cast<const s8*>(Dl + ((wk * T::MA + m) * 16 + lr) * T::DYP + p);
+#pragma unroll
+      for (int t = 0; t < 9; ++t) {
+        const int r = t / 3, sft = t % 3;
+        const s8 bv = *reinterpret_cast<const s8*>(Xl + sft * T::LDS_XC +
+                                                   (wc * 16 + lr) * T::PLANE_P +
+                                                   (yy + r) * T::TW + xx);
+#pragma unroll
+        for (int m = 0; m < T::MA; ++m)
+          acc[m][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+              __builtin_bit_cast(bf16x8, av[m]), __builtin_bit_cast(bf16x8, bv), acc[m][t], 0, 0,
+              0);
+      }
+      if (do_db) {
+#pragma unroll
+        for (int m = 0; m < T::MA; ++m)
+          accb[m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+              __builtin_bit_cast(bf16x8, av[m]), __builtin_bit_cast(bf16x8, ones), accb[m], 0, 0,
+              0);
+      }
+    }
+  };
+
+  const int nt = pt1 - pt0;
+  if (nt > 0) {
+    gload();
+    lstore(0);
+    if (nt > 1) gload();
+  }
+  __syncthreads();
+  for (int t = 0; t < nt; ++t) {
+    const int buf = t & 1;
+    if (t + 1 < nt) lstore(buf ^ 1);
+    if (t + 2 < nt) gload();
+    compute(buf);
+    __syncthreads();
+  }
+
+  // acc[m][t] lane holds rows k = k0 + (wk*MA + m)*16 + 4*kq + i and
+  // channel c0 + wc*16 + lr.
+#pragma unroll
+  for (int m = 0; m < T::MA; ++m)
+    wgrad_store<9>(
+        a, k0 + (wk * T::MA + m) * 16, do_db, accb[m],
+        [&](int i, int t) { return acc[m][t][i]; },
+        [&](int t) -> int {
+          int c = c0 + wc * 16 + lr;
+          return c < a.C ? c * 9 + t : -1;
+        });
+}
+
 // ------------------------------------------------------ small whole images --
 template <int H_, int W_, int IW_>
 struct WgSmall {
@@ -427,6 +721,7 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_small_f32(WgArgs a) {
 struct WgPlan {
   int imgs;          // images per pixel tile (per LDS fill for the small kernels)
   int tile, tiles_w, tiles_h, ptiles, k_tiles, c_tiles, tps, splits;
+  int bc;            // input channels per block of the bf16 MFMA kernel, 0 if not taken
   size_t ws_bytes;
 };
 
@@ -453,7 +748,8 @@ static const char* kWgNames[] = {
 };
 
 // allow_small: the whole-image kernel needs tensors aligned for 4-element moves.
-static WgPlan wg_plan(int N, int C, int H, int W, int K, bool allow_small = true) {
+// bf16: the wide tiles (0..2) run on the bf16 MFMA kernel.
+static WgPlan wg_plan(int N, int C, int H, int W, int K, bool allow_small, bool bf16) {
   WgPlan p{};
   int th = 2, tw = 32, imgs = 1;
   const bool narrow = C <= 7;
@@ -473,13 +769,14 @@ static WgPlan wg_plan(int N, int C, int H, int W, int K, bool allow_small = true
   p.tiles_h = cdiv(H, th);
   p.ptiles = p.tiles_w * p.tiles_h * cdiv(N, imgs);   // for the small kernels: image chunks
   p.k_tiles = cdiv(K, 64);
-  p.c_tiles = narrow ? 1 : cdiv(C, 16);
+  p.bc = bf16 && p.tile <= 2 ? (C >= 32 ? 32 : 16) : 0;
+  p.c_tiles = narrow ? 1 : cdiv(C, p.bc ? p.bc : 16);
   long blocks = (long)p.k_tiles * p.c_tiles;
-  // About two blocks per CU, at most 128 splits of the pixel range.
+  // About two blocks per CU, at most 256 splits of the pixel range.
   const long target = 512;
   int splits = 1;
   if (blocks < target)
-    splits = (int)std::min<long>(std::min<long>(p.ptiles, 128), cdiv((int)target, (int)blocks));
+    splits = (int)std::min<long>(std::min<long>(p.ptiles, 256), cdiv((int)target, (int)blocks));
   p.tps = cdiv(p.ptiles, splits);
   p.splits = cdiv(p.ptiles, p.tps);
   p.ws_bytes = p.splits > 1 ? (size_t)p.splits * ((size_t)K * C * 9 + K) * sizeof(float) : 0;
@@ -513,17 +810,64 @@ static void wg_launch(const WgPlan& p, const WgArgs& a, hipStream_t st) {
 
 namespace sbh {
 
-size_t conv_wgrad_ws(int N, int C, int H, int W, int K) {
-  return std::max(sb::wg_plan(N, C, H, W, K, true).ws_bytes,
-                  sb::wg_plan(N, C, H, W, K, false).ws_bytes);
+// Columns per staging load of the bf16 kernel: the largest of 8, 4, 2 that
+// divides the image width and the tile width and keeps both tensors' loads
+// aligned, else 1.
+static int wg_bf16_vec(int W, const void* x, const void* dy) {
+  const uintptr_t u = (uintptr_t)x | (uintptr_t)dy;
+  for (int v = 8; v >= 2; v /= 2)
+    if (W % v == 0 && (u % (2 * v)) == 0) return v;
+  return 1;
+}
+
+size_t conv_wgrad_ws(int dtype, int N, int C, int H, int W, int K) {
+  const bool bf16 = dtype == SB_BF16;
+  return std::max(sb::wg_plan(N, C, H, W, K, true, bf16).ws_bytes,
+                  sb::wg_plan(N, C, H, W, K, false, bf16).ws_bytes);
 }
 
 int conv_wgrad_describe(int dtype, int N, int C, int H, int W, int K, char* buf, size_t len) {
-  sb::WgPlan p = sb::wg_plan(N, C, H, W, K);
+  sb::WgPlan p = sb::wg_plan(N, C, H, W, K, true, dtype == SB_BF16);
   char name[160];
-  snprintf(name, sizeof(name), sb::kWgNames[p.tile],
-           dtype == SB_BF16 ? "unsigned short" : "float");
+  static const char* kBTiles[] = {"2, 32", "4, 16", "8, 8"};
+  // The bf16 kernel's staging width as for aligned tensors.
+  if (p.bc)
+    snprintf(name, sizeof(name), "sb::conv3x3_wgrad_bf16<sb::WgBTile<%s, %d>, %d>",
+             kBTiles[p.tile], p.bc, wg_bf16_vec(W, nullptr, nullptr));
+  else
+    snprintf(name, sizeof(name), sb::kWgNames[p.tile],
+             dtype == SB_BF16 ? "unsigned short" : "float");
   return snprintf(buf, len, "%s grid=%dx1x%d", name, p.k_tiles * p.c_tiles, p.splits);
+}
+
+// The bf16 weight gradient on the bf16 MFMA, for the wide 64-pixel tiles;
+// V columns per staging load.
+template <class T, int V>
+static void wg_launch_bf16(const sb::WgPlan& p, const sb::WgArgs& a, hipStream_t st) {
+  static bool attr_set = false;
+  if (!attr_set) {
+    (void)hipFuncSetAttribute((const void*)sb::conv3x3_wgrad_bf16<T, V>,
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)T::LDS_BYTES);
+    attr_set = true;
+  }
+  dim3 grid(p.k_tiles * p.c_tiles, 1, p.splits);
+  sb::conv3x3_wgrad_bf16<T, V><<<grid, 256, T::LDS_BYTES, st>>>(a);
+  if (p.splits > 1) {
+    const size_t wsz = (size_t)a.K * a.C * 9;
+    const size_t count = wsz + (a.db ? a.K : 0);
+    sb::splits_reduce<<<(unsigned)((count + 63) / 64), 256, 0, st>>>(
+        a.part, p.splits, wsz + a.K, count, wsz, a.dw, a.db);
+  }
+}
+
+template <class T>
+static void wg_launch_bf16v(int v, const sb::WgPlan& p, const sb::WgArgs& a, hipStream_t st) {
+  switch (v) {
+    case 8: wg_launch_bf16<T, 8>(p, a, st); break;
+    case 4: wg_launch_bf16<T, 4>(p, a, st); break;
+    case 2: wg_launch_bf16<T, 2>(p, a, st); break;
+    default: wg_launch_bf16<T, 1>(p, a, st); break;
+  }
 }
 
 template <class E>
@@ -549,7 +893,7 @@ sb_status conv_wgrad(int dtype, int N, int C, int H, int W, int K, const void* x
   // in bf16).
   const uintptr_t amask = dtype == SB_BF16 ? 7 : 15;
   const bool aligned = (((uintptr_t)x | (uintptr_t)dy) & amask) == 0;
-  sb::WgPlan p = sb::wg_plan(N, C, H, W, K, aligned);
+  sb::WgPlan p = sb::wg_plan(N, C, H, W, K, aligned, dtype == SB_BF16);
   // Buffer ranges: one tile's images of x and of dy.
   if ((int64_t)std::min(p.imgs, N) * std::max(C, K) * H * W * dsize(dtype) >= (1ll << 31))
     return SB_ERR_UNSUPPORTED;
@@ -560,8 +904,24 @@ sb_status conv_wgrad(int dtype, int N, int C, int H, int W, int K, const void* x
   a.N = N; a.C = C; a.H = H; a.W = W; a.K = K;
   a.tiles_w = p.tiles_w; a.tiles_h = p.tiles_h; a.ptiles = p.ptiles;
   a.tiles_per_split = p.tps; a.c_tiles = p.c_tiles; a.splits = p.splits;
-  if (dtype == SB_BF16) wg_dispatch<sb::u16>(p, a, st);
-  else wg_dispatch<float>(p, a, st);
+  const int v = p.bc ? wg_bf16_vec(W, x, dy) : 1;
+  if (p.bc == 32) {
+    switch (p.tile) {
+      case 0: wg_launch_bf16v<sb::WgBTile<2, 32, 32>>(v, p, a, st); break;
+      case 1: wg_launch_bf16v<sb::WgBTile<4, 16, 32>>(v, p, a, st); break;
+      default: wg_launch_bf16v<sb::WgBTile<8, 8, 32>>(v, p, a, st); break;
+    }
+  } else if (p.bc == 16) {
+    switch (p.tile) {
+      case 0: wg_launch_bf16v<sb::WgBTile<2, 32, 16>>(v, p, a, st); break;
+      case 1: wg_launch_bf16v<sb::WgBTile<4, 16, 16>>(v, p, a, st); break;
+      default: wg_launch_bf16v<sb::WgBTile<8, 8, 16>>(v, p, a, st); break;
+    }
+  } else if (dtype == SB_BF16) {
+    wg_dispatch<sb::u16>(p, a, st);
+  } else {
+    wg_dispatch<float>(p, a, st);
+  }
   return launch_status();
 }
 

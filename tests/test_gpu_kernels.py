@@ -72,6 +72,9 @@ CONV_SHAPES = [
     (2, 12, 5, 37, 17),
     (3, 40, 8, 8, 70),       # 8x8 two-group blocks, odd chunk count (groups uneven)
     (2, 33, 9, 12, 20),      # the same with ragged rows and columns
+    (2, 64, 6, 40, 80),      # 32-wide tiles, 32-channel blocks, ragged columns and k
+    (2, 36, 20, 20, 64),     # 16-wide tiles, ragged channel block
+    (2, 48, 14, 14, 64),     # 8x8 tiles over 14x14 (rows not a multiple of 4)
     (1, 1, 1, 1, 1),         # degenerate: every tap but the centre is padding
     (1, 9, 3, 1, 5),
 ]
@@ -155,6 +158,45 @@ def test_conv_bwd_weight(shape, dtype):
     sb.sb_conv3x3_bwd_weight(d, xd, dyd, dw2, db2, ws)
     torch.cuda.synchronize()
     assert torch.equal(dw, dw2) and torch.equal(db, db2)
+
+
+# bf16 weight-gradient shapes that reach each staging width of the bf16 MFMA
+# kernel (8, 4, 2 or 1 columns per load, from the image width) on each tile
+# shape (32, 16 and 8 columns wide), with ragged channel and k blocks.
+WGRAD_BF16_SHAPES = [
+    (2, 40, 5, 36, 64),      # 32-wide tiles, 4 columns per load
+    (1, 32, 4, 34, 70),      # 32-wide tiles, 2 columns per load
+    (2, 32, 6, 18, 64),      # 16-wide tiles, 2 columns per load
+    (2, 20, 7, 19, 33),      # 16-wide tiles, 1 column per load, 16-channel blocks
+    (2, 40, 9, 24, 70),      # 16-wide tiles, 8 columns per load, two column tiles
+    (2, 48, 9, 11, 64),      # 8-wide tiles, 1 column per load
+    (1, 64, 3, 64, 128),     # 32-wide tiles, two full column tiles
+]
+
+
+@pytest.mark.parametrize("shape", WGRAD_BF16_SHAPES)
+@pytest.mark.parametrize("offset", [0, 1])
+def test_conv_bwd_weight_bf16_staging(shape, offset):
+    """offset = 1 element shifts both tensors off their 16-byte alignment,
+    which takes the one-column staging whatever the width."""
+    n, c, h, w, k = shape
+    print_case("conv_bwd_weight_bf16", shape=shape, offset=offset)
+    x, _, _, dy, _ = _conv_inputs(n, c, h, w, k, 15)
+    d = sb.conv_desc(n, c, h, w, k, sb.SB_BF16)
+    ws = _ws(sb.sb_conv3x3_workspace_bytes(d, sb.SB_PASS_BWD_WEIGHT))
+    xb = torch.empty(x.size + offset, dtype=torch.bfloat16, device="cuda")
+    dyb = torch.empty(dy.size + offset, dtype=torch.bfloat16, device="cuda")
+    xd = xb[offset:].view(x.shape)
+    dyd = dyb[offset:].view(dy.shape)
+    xd.copy_(to_dev(x, "bf16"))
+    dyd.copy_(to_dev(dy, "bf16"))
+    dw = torch.full((k, c, 3, 3), float("nan"), device="cuda")
+    db = torch.full((k,), float("nan"), device="cuda")
+    sb.sb_conv3x3_bwd_weight(d, xd, dyd, dw, db, ws)
+    torch.cuda.synchronize()
+    dw_ref, db_ref = O.conv3x3_bwd_weight(to_host(xd), to_host(dyd))
+    assert rel_l2(to_host(dw), dw_ref) <= TOL["f32"]
+    assert rel_l2(to_host(db), db_ref) <= TOL["f32"]
 
 
 def test_conv_bwd_weight_without_bias_grad():
