@@ -1,21 +1,23 @@
 // conv_bf16.hip -- 3x3 / stride 1 / pad 1 convolution forward and data
-// gradient with bf16 operands on the bf16 MFMA (v_mfma_f32_16x16x16_bf16,
+// gradient with bf16 operands on the bf16 MFMA (v_mfma_f32_32x32x16_bf16,
 // fp32 accumulation), for SB_BF16 tensors.
 //
 // The same implicit GEMM as the fp32 kernels (rows = output channels,
-// columns = 128 output pixels, reduction = input channels x 9 taps, the
-// input halo of a chunk staged once in LDS and read at 9 shifted windows),
-// with both operands held channel-innermost in LDS, because a lane of this
-// MFMA supplies 4 consecutive reduction values (4 consecutive input
-// channels at one tap):
-//   * filters, packed per (output-channel tile, 16-channel chunk) as
-//     [tap][co][ci] (filter_pack with CI_INNER); LDS rows of 16 ci;
-//   * input halo, transposed on its way into LDS from NCHW to
-//     [halo pixel][ci].
-// LDS rows are 24 bf16 (48 bytes = 12 banks) apart, so the 16 lanes of a
-// lane group, reading 8 bytes from 16 consecutive rows, touch 16 distinct
-// 4-bank groups: the operand reads are conflict-free.  Each MFMA consumes
-// one 8-byte read per operand.
+// columns = output pixels, reduction = input channels x 9 taps, the input
+// halo of a 16-channel chunk staged once in LDS and read at 9 shifted
+// windows).  A block owns 64 output channels x 256 output pixels; each of
+// its four waves owns all 64 channels x 64 pixels (2 x 2 tiles of 32 x 32).
+// A lane of this MFMA supplies 8 consecutive reduction values (8
+// consecutive input channels at one tap), so both operands sit in LDS as
+// planes of 8 channels, each 16-byte row one (pixel or output channel):
+//   * filters, packed per (output-channel tile, chunk) as
+//     [tap][ci / 8][co][ci % 8] (filter_pack, PackCI8), staged as is;
+//   * input halo as [ci / 8][halo pixel][ci % 8], transposed from NCHW on
+//     its way in: a lane loads V consecutive columns of one channel (V = 8,
+//     4, 2 when the width allows, else 1) and stores them as V 2-byte
+//     writes 16 bytes apart.
+// The 32 lanes of an operand read fetch 32 consecutive 16-byte rows, so the
+// reads are free of bank conflicts without padding.
 //
 // The data gradient is the same contraction with the filters transposed and
 // rotated (done by the pack).  Splits over channel chunks, the epilogue and
@@ -27,56 +29,50 @@
 
 namespace sb {
 
-typedef short s4 __attribute__((ext_vector_type(4)));
+typedef short s8 __attribute__((ext_vector_type(8)));
+typedef float f16 __attribute__((ext_vector_type(16)));
 
-// D(16x16) += A(16x16) * B(16x16), bf16 in / fp32 accumulate.  Lane l
-// supplies A[l%16][4*(l/16) + j] and B[4*(l/16) + j][l%16] (j = 0..3) and
-// receives D[4*(l/16) + i][l%16] in element i.
-__device__ __forceinline__ f4 mfma16x16x16bf16(s4 a, s4 b, f4 c) {
-  return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, c, 0, 0, 0);
+// D(32x32) += A(32x16) * B(16x32), bf16 in / fp32 accumulate.  Lane l
+// supplies A[l%32][8*(l/32) + j] and B[8*(l/32) + j][l%32] (j = 0..7) and
+// receives D[8*(v/4) + 4*(l/32) + v%4][l%32] in element v.
+__device__ __forceinline__ f16 mfma32x32x16bf16(s8 a, s8 b, f16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
+                                                 __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
 
 template <int TH_, int TW_, int IMGS_>
 struct BTile {
   static constexpr int TH = TH_, TW = TW_, IMGS = IMGS_;
   static constexpr int BM = IMGS * TH * TW;
-  static_assert(BM == 128, "pixel tile must hold 128 pixels");
-  static constexpr int BN = 64, CK = 16, RP = 24;   // RP: LDS row pitch (bf16)
+  static_assert(BM == 256, "pixel tile must hold 256 pixels");
+  static constexpr int BN = 64, CK = 16;
   static constexpr int HH = TH + 2, HW = TW + 2;
-  static constexpr int PLANE = IMGS * HH * HW;      // halo pixels
-  static constexpr int HALO = CK * PLANE;           // halo elements per chunk
-  static constexpr int HALO_PT = (HALO + 255) / 256;
+  static constexpr int ROWS = IMGS * HH;            // halo rows
+  static constexpr int PLANE = ROWS * HW;           // halo pixels
   static constexpr int WTS = 9 * BN * CK;           // filter elements per chunk
-  static constexpr int WTS_PT = WTS / 4 / 256;      // 8-byte groups per thread
-  static_assert(WTS % 1024 == 0, "whole 256-thread rounds of 4-element groups");
-  static constexpr int LDS_X = PLANE * RP;          // bf16 elements
-  static constexpr int LDS_W = 9 * BN * RP;
-  static constexpr int LDS_SPARE = 256;             // idle halo lanes store here
-  static constexpr int LDS_BUF = LDS_X + LDS_W + LDS_SPARE;
-  static_assert(LDS_X % 8 == 0 && LDS_BUF % 8 == 0, "8-byte aligned regions");
+  static constexpr int WTS_V = WTS / 8;             // 16-byte rows of filters
+  static constexpr int WTS_I = (WTS_V + 255) / 256;
+  static constexpr int LDS_X = 2 * PLANE * 8;       // bf16 elements
+  static constexpr int LDS_BUF = LDS_X + WTS;
+  static_assert(LDS_X % 8 == 0 && LDS_BUF % 8 == 0, "16-byte aligned regions");
   static constexpr size_t LDS_BYTES = 2 * LDS_BUF * sizeof(u16);
   static_assert(LDS_BYTES <= 80 * 1024, "two blocks must fit in the 160 KB of LDS");
-  // Four waves 2 x 2; a wave owns 32 channels x 64 pixels (2 x 4 blocks).
-  static constexpr int WN = 32, WM = 64, NB = 2, MB = 4;
-  // Halo layout [halo row][halo column][image] (image innermost), as the
-  // fp32 tiles: the 16 pixels of an MFMA column block are consecutive rows.
-  __host__ __device__ static constexpr int hoff(int img, int hy, int hx) {
-    return (hy * HW + hx) * IMGS + img;
-  }
-  __device__ static void pix(int p, int& img, int& yy, int& xx) {
-    img = p % IMGS;
-    const int q = p / IMGS;
-    yy = q / TW;
-    xx = q - yy * TW;
+  // Pixel p of the tile: images outermost, then rows, then columns; a wave
+  // owns 64 consecutive pixels (two blocks of 32).
+  __host__ __device__ static constexpr int img_of(int p) { return p / (TH * TW); }
+  __host__ __device__ static constexpr int yy_of(int p) { return p % (TH * TW) / TW; }
+  __host__ __device__ static constexpr int xx_of(int p) { return p % TW; }
+  // Halo pixel of (image, halo row, halo column).
+  __host__ __device__ static constexpr int hp(int img, int hy, int hx) {
+    return (img * HH + hy) * HW + hx;
   }
 };
 
-template <class T, bool DGRAD>
+template <class T, bool DGRAD, int V>
 __global__ __launch_bounds__(256, 2) void conv3x3_igemm_bf16(ConvArgs a) {
   extern __shared__ u16 ldsb[];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave & 1, wn = wave >> 1;
-  const int kq = lane >> 4, lr = lane & 15;
+  const int lc = lane & 31, lh = lane >> 5;
 
   int bt = blockIdx.x;
   const int tx = bt % a.tiles_w; bt /= a.tiles_w;
@@ -88,89 +84,128 @@ __global__ __launch_bounds__(256, 2) void conv3x3_igemm_bf16(ConvArgs a) {
   const int kc1 = min(a.nchunks, kc0 + a.chunks_per_split);
   const int HWs = a.H * a.W;
 
-  // Halo element e = (channel cc, halo position rem), position fastest, so
-  // that neighbouring lanes read neighbouring pixels of one channel plane.
-  int x_off[T::HALO_PT], x_c[T::HALO_PT], x_loff[T::HALO_PT];
+  // Halo staging.  Thread -> channel ci = tid % 16 and a set of (row,
+  // column piece) combinations u = tid / 16 + 16 * round, rows fastest.
+  // Interior pieces cover tile columns vi*V .. vi*V+V-1 (halo columns + 1);
+  // the edge columns (halo columns 0 and TW+1) are single loads.
+  constexpr int VPR = T::TW / V;                    // pieces per row
+  constexpr int XI = (T::ROWS * VPR + 15) / 16;
+  constexpr int EI = (T::ROWS * 2 + 15) / 16;
+  const int ci = tid & 15;
+  int x_off[XI], x_lds[XI], e_off[EI], e_lds[EI];
 #pragma unroll
-  for (int i = 0; i < T::HALO_PT; ++i) {
-    int e = tid + i * 256;
-    bool live = e < T::HALO;
-    int cc = e / T::PLANE, rem = e - cc * T::PLANE;
-    int img = rem % T::IMGS, q = rem / T::IMGS;
-    int yy = q / T::HW, xx = q - yy * T::HW;
-    int n = n0 + img, h = h0 + yy - 1, w = w0 + xx - 1;
-    bool ok = live && n < a.N && h >= 0 && h < a.H && w >= 0 && w < a.W;
-    x_off[i] = ok ? img * a.Cin * HWs + h * a.W + w : -1;   // from image n0; + ci * H*W
-    x_c[i] = cc;
-    x_loff[i] = live ? rem * T::RP + cc : T::LDS_X + T::LDS_W + tid;
+  for (int i = 0; i < XI; ++i) {
+    const int u = (tid >> 4) + 16 * i;
+    const int row = u % T::ROWS, vi = u / T::ROWS;
+    const int img = row / T::HH, hy = row % T::HH;
+    const int h = h0 + hy - 1, w = w0 + vi * V;
+    const bool ok = u < T::ROWS * VPR && n0 + img < a.N && (unsigned)h < (unsigned)a.H &&
+                    w < a.W;
+    x_off[i] = ok ? (img * a.Cin + ci) * HWs + h * a.W + w : -1;   // from image n0
+    x_lds[i] = u < T::ROWS * VPR ? ((ci >> 3) * T::PLANE + T::hp(img, hy, 1 + vi * V)) * 8 + (ci & 7)
+                                 : -1;
   }
-  // Packed filter group g (4 consecutive ci of one (tap, co) row) -> LDS.
-  int w_loff[T::WTS_PT];
 #pragma unroll
-  for (int i = 0; i < T::WTS_PT; ++i) {
-    int g = tid + i * 256;
-    w_loff[i] = (g >> 2) * T::RP + (g & 3) * 4;
+  for (int i = 0; i < EI; ++i) {
+    const int u = (tid >> 4) + 16 * i;
+    const int row = u % T::ROWS, side = u / T::ROWS;
+    const int img = row / T::HH, hy = row % T::HH;
+    const int h = h0 + hy - 1, w = side ? w0 + T::TW : w0 - 1;
+    const bool ok = u < T::ROWS * 2 && n0 + img < a.N && (unsigned)h < (unsigned)a.H &&
+                    (unsigned)w < (unsigned)a.W;
+    e_off[i] = ok ? (img * a.Cin + ci) * HWs + h * a.W + w : -1;
+    e_lds[i] = u < T::ROWS * 2
+                   ? ((ci >> 3) * T::PLANE + T::hp(img, hy, side ? T::TW + 1 : 0)) * 8 + (ci & 7)
+                   : -1;
   }
-  int pix_off[T::MB];
+  // Operand rows of this lane: pixel lc of each of the wave's two pixel
+  // blocks (halo pixel at tap (0, 0)), channel-plane lh.
+  int b_off[2];
 #pragma unroll
-  for (int mb = 0; mb < T::MB; ++mb) {
-    int img, yy, xx;
-    T::pix(wm * T::WM + mb * 16 + lr, img, yy, xx);
-    pix_off[mb] = T::hoff(img, yy, xx) * T::RP + 4 * kq;
+  for (int mb = 0; mb < 2; ++mb) {
+    const int p = wave * 64 + mb * 32 + lc;
+    b_off[mb] = (lh * T::PLANE + T::hp(T::img_of(p), T::yy_of(p), T::xx_of(p))) * 8;
   }
 
-  f4 acc[T::NB][T::MB];
+  f16 acc[2][2];
 #pragma unroll
-  for (int i = 0; i < T::NB; ++i)
+  for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int j = 0; j < T::MB; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
   const rsrc_t xr = input_rsrc<u16>(a, n0, T::IMGS);
   const rsrc_t wr = packed_rsrc<u16, T::WTS>(a, blockIdx.y);
-  u16 rx[T::HALO_PT];
-  s4 rw[T::WTS_PT];
+  typedef typename std::conditional<(V > 1), Vec<(V > 1 ? V : 2)>, u16>::type Piece;
+  Piece rx[XI];
+  u16 re[EI];
+  s8 rw[T::WTS_I];
   auto gload = [&](int kc) {
-    const int cbase = kc * T::CK;
+    const int cb = kc * T::CK;
+    const int cleft = a.Cin - cb - ci;               // this lane's channel valid if > 0
 #pragma unroll
-    for (int i = 0; i < T::HALO_PT; ++i) {
-      const int ci = cbase + x_c[i];
-      const bool ok = x_off[i] >= 0 && ci < a.Cin;
-      rx[i] = (u16)__builtin_amdgcn_raw_buffer_load_b16(
-          xr, ok ? (int)((uint32_t)(x_off[i] + ci * HWs) * 2u) : (int)kOOB, 0, 0);
+    for (int i = 0; i < XI; ++i) {
+      const uint32_t off =
+          x_off[i] >= 0 && cleft > 0 ? (uint32_t)(x_off[i] + cb * HWs) * 2u : kOOB;
+      if constexpr (V > 1) rx[i] = load_vec<V>(xr, off);
+      else rx[i] = (u16)__builtin_amdgcn_raw_buffer_load_b16(xr, (int)off, 0, 0);
     }
 #pragma unroll
-    for (int i = 0; i < T::WTS_PT; ++i)
-      rw[i] = __builtin_bit_cast(
-          s4, __builtin_amdgcn_raw_buffer_load_b64(
-                  wr, (int)((uint32_t)(kc * T::WTS + (tid + i * 256) * 4) * 2u), 0, 0));
+    for (int i = 0; i < EI; ++i)
+      re[i] = (u16)__builtin_amdgcn_raw_buffer_load_b16(
+          xr, e_off[i] >= 0 && cleft > 0 ? (int)((uint32_t)(e_off[i] + cb * HWs) * 2u) : (int)kOOB,
+          0, 0);
+#pragma unroll
+    for (int i = 0; i < T::WTS_I; ++i) {
+      const int g = tid + 256 * i;
+      const uint32_t off = g < T::WTS_V ? (uint32_t)(kc * T::WTS + g * 8) * 2u : kOOB;
+      rw[i] = __builtin_bit_cast(s8, __builtin_amdgcn_raw_buffer_load_b128(wr, (int)off, 0, 0));
+    }
   };
   auto lstore = [&](int buf) {
     u16* X = ldsb + buf * T::LDS_BUF;
     u16* Wl = X + T::LDS_X;
 #pragma unroll
-    for (int i = 0; i < T::HALO_PT; ++i) X[x_loff[i]] = rx[i];
+    for (int i = 0; i < XI; ++i) {
+      if (x_lds[i] < 0) continue;
+      u16* q = X + x_lds[i];
+      if constexpr (V > 1) {
 #pragma unroll
-    for (int i = 0; i < T::WTS_PT; ++i) *reinterpret_cast<s4*>(Wl + w_loff[i]) = rw[i];
+        for (int j = 0; j < V / 2; ++j) {
+          q[(2 * j) * 8] = (u16)(rx[i].d[j] & 0xffffu);
+          q[(2 * j + 1) * 8] = (u16)(rx[i].d[j] >> 16);
+        }
+      } else {
+        q[0] = rx[i];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < EI; ++i)
+      if (e_lds[i] >= 0) X[e_lds[i]] = re[i];
+#pragma unroll
+    for (int i = 0; i < T::WTS_I; ++i) {
+      const int g = tid + 256 * i;
+      if (g < T::WTS_V) *reinterpret_cast<s8*>(Wl + g * 8) = rw[i];
+    }
   };
   auto compute = [&](int buf) {
     const u16* X = ldsb + buf * T::LDS_BUF;
     const u16* Wl = X + T::LDS_X;
 #pragma unroll
     for (int t = 0; t < 9; ++t) {
-      const int toff = T::hoff(0, t / 3, t % 3) * T::RP;
-      s4 fa[T::NB], fb[T::MB];
+      const int toff = T::hp(0, t / 3, t % 3) * 8;
+      s8 fa[2], fb[2];
 #pragma unroll
-      for (int nb = 0; nb < T::NB; ++nb)
-        fa[nb] = *reinterpret_cast<const s4*>(
-            Wl + (t * T::BN + wn * T::WN + nb * 16 + lr) * T::RP + 4 * kq);
+      for (int nb = 0; nb < 2; ++nb)
+        fa[nb] = *reinterpret_cast<const s8*>(Wl + ((t * 2 + lh) * T::BN + nb * 32 + lc) * 8);
 #pragma unroll
-      for (int mb = 0; mb < T::MB; ++mb)
-        fb[mb] = *reinterpret_cast<const s4*>(X + pix_off[mb] + toff);
+      for (int mb = 0; mb < 2; ++mb)
+        fb[mb] = *reinterpret_cast<const s8*>(X + b_off[mb] + toff);
 #pragma unroll
-      for (int nb = 0; nb < T::NB; ++nb)
+      for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
-        for (int mb = 0; mb < T::MB; ++mb)
-          acc[nb][mb] = mfma16x16x16bf16(fa[nb], fb[mb], acc[nb][mb]);
+        for (int mb = 0; mb < 2; ++mb) acc[nb][mb] = mfma32x32x16bf16(fa[nb], fb[mb], acc[nb][mb]);
     }
   };
 
@@ -189,86 +224,116 @@ __global__ __launch_bounds__(256, 2) void conv3x3_igemm_bf16(ConvArgs a) {
     __syncthreads();
   }
 
-  // acc[nb][mb] lane holds channel co0 + wn*WN + nb*16 + 4*kq + i of pixel
-  // wm*WM + mb*16 + lr.
-  const size_t total = (size_t)a.N * a.Cout * HWs;
+  // acc[nb][mb] element v: output channel co0 + nb*32 + 8*(v/4) + 4*lh +
+  // v%4 of pixel wave*64 + mb*32 + lc.
+  int pix[2];                                        // offset from image n0, -1 outside
+#pragma unroll
+  for (int mb = 0; mb < 2; ++mb) {
+    const int p = wave * 64 + mb * 32 + lc;
+    const int img = T::img_of(p), h = h0 + T::yy_of(p), w = w0 + T::xx_of(p);
+    pix[mb] = n0 + img < a.N && h < a.H && w < a.W ? img * a.Cout * HWs + h * a.W + w : -1;
+  }
+  auto co_of = [&](int nb, int v) { return co0 + nb * 32 + 8 * (v >> 2) + 4 * lh + (v & 3); };
   if (a.splits > 1) {
-    float* mine = a.part + (size_t)blockIdx.z * total;
+    float* mine = a.part + (size_t)blockIdx.z * a.N * a.Cout * HWs + (size_t)n0 * a.Cout * HWs;
 #pragma unroll
-    for (int mb = 0; mb < T::MB; ++mb) {
-      int img, yy, xx;
-      T::pix(wm * T::WM + mb * 16 + lr, img, yy, xx);
-      const int n = n0 + img, h = h0 + yy, w = w0 + xx;
-      if (n >= a.N || h >= a.H || w >= a.W) continue;
+    for (int mb = 0; mb < 2; ++mb) {
+      if (pix[mb] < 0) continue;
 #pragma unroll
-      for (int nb = 0; nb < T::NB; ++nb)
+      for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int co = co0 + wn * T::WN + nb * 16 + kq * 4 + i;
-          if (co < a.Cout) mine[((size_t)n * a.Cout + co) * HWs + (size_t)h * a.W + w] =
-              acc[nb][mb][i];
+        for (int v = 0; v < 16; ++v) {
+          const int co = co_of(nb, v);
+          if (co < a.Cout) mine[pix[mb] + co * HWs] = acc[nb][mb][v];
         }
     }
     return;
   }
-  // Element offsets from image n0 (the output and the ReLU mask share the
-  // layout); -1 outside the tensor.  The mask values are all requested
-  // before any is used.
-  int off[T::MB][T::NB][4];
+  // The block's 64 x 256 outputs go through LDS ([channel][pixel], bias and
+  // ReLU applied, rounded to bf16), then out to memory in pieces of V
+  // consecutive pixels of one channel, the ReLU mask read in the same
+  // pieces; every mask load is issued before the first store.
+  constexpr int EP = T::BM + 8;                      // LDS row pitch (bf16)
+  static_assert(64 * EP <= 2 * T::LDS_BUF, "output tile fits the staging LDS");
+  u16* E = ldsb;
 #pragma unroll
-  for (int mb = 0; mb < T::MB; ++mb) {
-    int img, yy, xx;
-    T::pix(wm * T::WM + mb * 16 + lr, img, yy, xx);
-    const bool pix_ok = n0 + img < a.N && h0 + yy < a.H && w0 + xx < a.W;
+  for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
-    for (int nb = 0; nb < T::NB; ++nb)
+    for (int v = 0; v < 16; ++v) {
+      const int co = co_of(nb, v);
+      const float bv = a.bias && co < a.Cout ? a.bias[co] : 0.f;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int co = co0 + wn * T::WN + nb * 16 + kq * 4 + i;
-        off[mb][nb][i] = pix_ok && co < a.Cout
-                             ? (img * a.Cout + co) * HWs + (h0 + yy) * a.W + w0 + xx : -1;
+      for (int mb = 0; mb < 2; ++mb) {
+        float r = acc[nb][mb][v] + bv;
+        if (a.relu && !(r > 0.f)) r = 0.f;
+        E[(co - co0) * EP + wave * 64 + mb * 32 + lc] = f32_to_bf16(r);
       }
+    }
+  __syncthreads();
+  constexpr int PPR = T::BM / V;                     // pieces per channel row
+  constexpr int EPI = 64 * PPR / 256;                // pieces per thread
+  static_assert(64 * PPR % 256 == 0, "whole rounds of pieces");
+  int goff[EPI];                                     // from image n0, -1 outside
+#pragma unroll
+  for (int i = 0; i < EPI; ++i) {
+    const int q = tid + 256 * i;
+    const int col = q / PPR, p = (q % PPR) * V;
+    const int img = T::img_of(p), h = h0 + T::yy_of(p), w = w0 + T::xx_of(p);
+    const int co = co0 + col;
+    goff[i] = co < a.Cout && n0 + img < a.N && h < a.H && w < a.W
+                  ? (img * a.Cout + co) * HWs + h * a.W + w : -1;
   }
-  float mv[T::MB][T::NB][4];
+  typedef typename std::conditional<(V > 1), Vec<(V > 1 ? V : 2)>, u16>::type Piece;
+  Piece mk[EPI];
   if (a.mask) {
     const int cnt = min(T::IMGS, a.N - n0);
     const rsrc_t mr = make_rsrc((const u16*)a.mask + (size_t)n0 * a.Cout * HWs,
                                 (uint32_t)((size_t)cnt * a.Cout * HWs * 2));
 #pragma unroll
-    for (int mb = 0; mb < T::MB; ++mb)
-#pragma unroll
-      for (int nb = 0; nb < T::NB; ++nb)
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          mv[mb][nb][i] = BufLoad<u16>::one(
-              mr, off[mb][nb][i] >= 0 ? (uint32_t)off[mb][nb][i] * 2u : kOOB);
+    for (int i = 0; i < EPI; ++i) {
+      const uint32_t off = goff[i] >= 0 ? (uint32_t)goff[i] * 2u : kOOB;
+      if constexpr (V > 1) mk[i] = load_vec<V>(mr, off);
+      else mk[i] = (u16)__builtin_amdgcn_raw_buffer_load_b16(mr, (int)off, 0, 0);
+    }
   }
+  // A bf16 mask value m keeps the output iff m > 0: bits 0x0001..0x7f80.
+  auto keep = [](uint32_t m16) { return ((m16 - 1u) & 0xffffu) < 0x7f80u; };
   u16* out = (u16*)a.out + (size_t)n0 * a.Cout * HWs;
 #pragma unroll
-  for (int mb = 0; mb < T::MB; ++mb)
+  for (int i = 0; i < EPI; ++i) {
+    if (goff[i] < 0) continue;
+    const int q = tid + 256 * i;
+    const u16* src = E + (q / PPR) * EP + (q % PPR) * V;
+    if constexpr (V > 1) {
+      Vec<V> o = lds_vec<V>(src);
 #pragma unroll
-    for (int nb = 0; nb < T::NB; ++nb)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        if (off[mb][nb][i] < 0) continue;
-        const int co = co0 + wn * T::WN + nb * 16 + kq * 4 + i;
-        float v = acc[nb][mb][i];
-        if (a.bias) v += a.bias[co];
-        if (a.relu && !(v > 0.f)) v = 0.f;
-        if (a.mask && !(mv[mb][nb][i] > 0.f)) v = 0.f;
-        out[off[mb][nb][i]] = f32_to_bf16(v);
+      for (int j = 0; j < V / 2; ++j) {
+        uint32_t d = o.d[j];
+        if (a.mask) {
+          const uint32_t m = mk[i].d[j];
+          if (!keep(m & 0xffffu)) d &= 0xffff0000u;
+          if (!keep(m >> 16)) d &= 0x0000ffffu;
+        }
+        o.d[j] = d;
       }
+      store_vec<V>(out + goff[i], o);
+    } else {
+      u16 d = src[0];
+      if (a.mask && !keep(mk[i])) d = 0;
+      out[goff[i]] = d;
+    }
+  }
 }
 
 // ---------------------------------------------------------------- host --
-using BTileW32 = BTile<4, 32, 1>;
-using BTileW16 = BTile<8, 16, 1>;
-using BTileW8 = BTile<8, 8, 2>;
+using BTileW32 = BTile<8, 32, 1>;
+using BTileW16 = BTile<16, 16, 1>;
+using BTileW8 = BTile<8, 8, 4>;
 
 static const char* kBTileNames[] = {
-    "sb::conv3x3_igemm_bf16<sb::BTile<4, 32, 1>, %s>",
-    "sb::conv3x3_igemm_bf16<sb::BTile<8, 16, 1>, %s>",
-    "sb::conv3x3_igemm_bf16<sb::BTile<8, 8, 2>, %s>",
+    "sb::conv3x3_igemm_bf16<sb::BTile<8, 32, 1>, %s, %d>",
+    "sb::conv3x3_igemm_bf16<sb::BTile<16, 16, 1>, %s, %d>",
+    "sb::conv3x3_igemm_bf16<sb::BTile<8, 8, 4>, %s, %d>",
 };
 
 struct BPlan {
@@ -283,9 +348,9 @@ static BPlan bf16_plan(int N, int Cin, int H, int W, int Cout) {
   BPlan p{};
   if (W < 8 || Cin < 16) return p;
   int th, tw, imgs = 1;
-  if (W >= 32) { p.tile = 0; th = 4; tw = 32; }
-  else if (W >= 16) { p.tile = 1; th = 8; tw = 16; }
-  else { p.tile = 2; th = 8; tw = 8; imgs = 2; }
+  if (W >= 32) { p.tile = 0; th = 8; tw = 32; }
+  else if (W >= 16) { p.tile = 1; th = 16; tw = 16; }
+  else { p.tile = 2; th = 8; tw = 8; imgs = 4; }
   p.ok = true;
   p.imgs = imgs;
   p.tiles_w = cdiv(W, tw);
@@ -310,20 +375,29 @@ static BPlan bf16_plan(int N, int Cin, int H, int W, int Cout) {
   return p;
 }
 
-template <class T, bool DGRAD>
+// Columns per halo load and per output / mask access: the largest of 8, 4,
+// 2 that divides the image width and keeps every such access aligned, else 1.
+static int bf16_vec(int W, const void* in, const void* out, const void* mask) {
+  const uintptr_t u = (uintptr_t)in | (uintptr_t)out | (uintptr_t)mask;
+  for (int v = 8; v >= 2; v /= 2)
+    if (W % v == 0 && (u % (2 * v)) == 0) return v;
+  return 1;
+}
+
+template <class T, bool DGRAD, int V>
 static void bf16_launch(const BPlan& p, const ConvArgs& a, hipStream_t st) {
   static bool attr_set = false;
   if (!attr_set) {
-    (void)hipFuncSetAttribute((const void*)conv3x3_igemm_bf16<T, DGRAD>,
+    (void)hipFuncSetAttribute((const void*)conv3x3_igemm_bf16<T, DGRAD, V>,
                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)T::LDS_BYTES);
     attr_set = true;
   }
-  filter_pack<DGRAD, T::CK, T::BN, u16, true><<<p.co_tiles * p.nchunks, 256, 0, st>>>(
+  filter_pack<DGRAD, T::CK, T::BN, u16, PackCI8><<<p.co_tiles * p.nchunks, 256, 0, st>>>(
       (const u16*)a.wt, (u16*)a.wpk, a.Cin, a.Cout);
   dim3 grid(p.grid_x, p.co_tiles, p.splits);
   ConvArgs k = a;
   if (p.splits > 1) { k.bias = nullptr; k.mask = nullptr; k.relu = 0; }
-  conv3x3_igemm_bf16<T, DGRAD><<<grid, 256, T::LDS_BYTES, st>>>(k);
+  conv3x3_igemm_bf16<T, DGRAD, V><<<grid, 256, T::LDS_BYTES, st>>>(k);
   if (p.splits > 1) {
     size_t total = (size_t)a.N * a.Cout * a.H * a.W;
     conv_splitk_reduce<u16><<<(unsigned)((total + 63) / 64), 256, 0, st>>>(
@@ -332,12 +406,22 @@ static void bf16_launch(const BPlan& p, const ConvArgs& a, hipStream_t st) {
   }
 }
 
+template <class T, bool DGRAD>
+static void bf16_launch_v(int v, const BPlan& p, const ConvArgs& a, hipStream_t st) {
+  switch (v) {
+    case 8: bf16_launch<T, DGRAD, 8>(p, a, st); break;
+    case 4: bf16_launch<T, DGRAD, 4>(p, a, st); break;
+    case 2: bf16_launch<T, DGRAD, 2>(p, a, st); break;
+    default: bf16_launch<T, DGRAD, 1>(p, a, st); break;
+  }
+}
+
 template <bool DGRAD>
-static void bf16_dispatch(const BPlan& p, const ConvArgs& a, hipStream_t st) {
+static void bf16_dispatch(int v, const BPlan& p, const ConvArgs& a, hipStream_t st) {
   switch (p.tile) {
-    case 0: bf16_launch<BTileW32, DGRAD>(p, a, st); break;
-    case 1: bf16_launch<BTileW16, DGRAD>(p, a, st); break;
-    default: bf16_launch<BTileW8, DGRAD>(p, a, st); break;
+    case 0: bf16_launch_v<BTileW32, DGRAD>(v, p, a, st); break;
+    case 1: bf16_launch_v<BTileW16, DGRAD>(v, p, a, st); break;
+    default: bf16_launch_v<BTileW8, DGRAD>(v, p, a, st); break;
   }
 }
 
@@ -355,10 +439,12 @@ bool conv_bf16_takes(int N, int Cin, int H, int W, int Cout) {
   return sb::bf16_plan(N, Cin, H, W, Cout).ok;
 }
 
+// Names the kernel as launched for aligned tensors.
 int conv_bf16_describe(bool dgrad, int N, int Cin, int H, int W, int Cout, char* buf, size_t len) {
   sb::BPlan p = sb::bf16_plan(N, Cin, H, W, Cout);
   char name[160];
-  snprintf(name, sizeof(name), sb::kBTileNames[p.tile], dgrad ? "true" : "false");
+  snprintf(name, sizeof(name), sb::kBTileNames[p.tile], dgrad ? "true" : "false",
+           sb::bf16_vec(W, nullptr, nullptr, nullptr));
   return snprintf(buf, len, "%s grid=%dx%dx%d", name, p.grid_x, p.co_tiles, p.splits);
 }
 
@@ -380,8 +466,9 @@ sb_status conv_bf16(bool dgrad, int N, int Cin, int H, int W, int Cout, const vo
   a.N = N; a.Cin = Cin; a.H = H; a.W = W; a.Cout = Cout;
   a.tiles_w = p.tiles_w; a.tiles_h = p.tiles_h;
   a.nchunks = p.nchunks; a.chunks_per_split = p.cps; a.splits = p.splits; a.relu = relu;
-  if (dgrad) sb::bf16_dispatch<true>(p, a, st);
-  else sb::bf16_dispatch<false>(p, a, st);
+  const int v = sb::bf16_vec(W, in, out, mask);
+  if (dgrad) sb::bf16_dispatch<true>(v, p, a, st);
+  else sb::bf16_dispatch<false>(v, p, a, st);
   return launch_status();
 }
 

@@ -43,17 +43,21 @@ __device__ __forceinline__ float conv_epilogue(const ConvArgs& a, float v, int c
 // of CK*9 contiguous elements per output channel, or BN*9 per input channel
 // for the data gradient), permutes it in LDS and writes it out contiguously.
 //
-// CI_INNER packs each slice [tap][co][ci] instead (input channels innermost),
-// the order of the bf16 kernels, whose lanes read 4 consecutive channels.
-template <bool DGRAD, int CK, int BN, class E, bool CI_INNER = false>
+// PackCI8 packs each slice [tap][ci / 8][co][ci % 8] instead: planes of 8
+// consecutive input channels per output channel, the operand order of the
+// bf16 kernels, whose lanes read 8 consecutive channels (16 bytes).
+constexpr int PackCO = 0, PackCI8 = 1;
+template <bool DGRAD, int CK, int BN, class E, int LAYOUT = PackCO>
 __global__ __launch_bounds__(256) void filter_pack(const E* __restrict__ w, E* __restrict__ out,
                                                    int Cin, int Cout) {
   // Cin, Cout: this convolution's input and output channels (for the data
   // gradient: the forward layer's output and input channels).
   constexpr int SL = 9 * CK * BN;
+  constexpr bool CI8 = LAYOUT == PackCI8;
+  static_assert(!CI8 || CK % 8 == 0, "whole 8-channel planes");
   // Padded LDS rows (one extra element) keep the permuting writes spread
   // over the banks.
-  constexpr int ROW = CI_INNER ? CK : BN, RS = ROW + 1;
+  constexpr int ROW = CI8 ? 8 : BN, RS = ROW + 1;
   __shared__ E slice_lds[SL / ROW * RS];
   constexpr int PT = (SL + 255) / 256;
   const int nchunks = cdiv(Cin, CK);
@@ -83,7 +87,9 @@ __global__ __launch_bounds__(256) void filter_pack(const E* __restrict__ w, E* _
     }
     const bool ok = g < SL && ct * BN + nn < Cout && kc * CK + cc < Cin;
     v[i] = ok ? w[src] : E{};
-    pos[i] = g < SL ? (CI_INNER ? (tap * BN + nn) * RS + cc : (tap * CK + cc) * RS + nn) : -1;
+    pos[i] = g < SL ? (CI8 ? ((tap * (CK / 8) + cc / 8) * BN + nn) * RS + cc % 8
+                           : (tap * CK + cc) * RS + nn)
+                    : -1;
   }
 #pragma unroll
   for (int i = 0; i < PT; ++i)

@@ -36,7 +36,6 @@
 
 #include <algorithm>
 #include <cstdio>
-#include <type_traits>
 
 namespace sb {
 
@@ -333,40 +332,6 @@ struct WgBTile {
 };
 
 typedef short s8 __attribute__((ext_vector_type(8)));
-
-// V consecutive bf16 in V/2 dwords (V >= 2); element 2j in the low half of
-// dword j.
-template <int V> struct Vec { uint32_t d[V / 2]; };
-
-template <int V>
-__device__ __forceinline__ Vec<V> load_vec(rsrc_t r, uint32_t off) {
-  Vec<V> v;
-  if constexpr (V == 8) {
-    typedef uint32_t u4 __attribute__((ext_vector_type(4)));
-    u4 t = __builtin_bit_cast(u4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0));
-    v.d[0] = t[0]; v.d[1] = t[1]; v.d[2] = t[2]; v.d[3] = t[3];
-  } else if constexpr (V == 4) {
-    typedef uint32_t u2 __attribute__((ext_vector_type(2)));
-    u2 t = __builtin_bit_cast(u2, __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, 0));
-    v.d[0] = t[0]; v.d[1] = t[1];
-  } else {
-    v.d[0] = __builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, 0);
-  }
-  return v;
-}
-
-template <int V>
-__device__ __forceinline__ void store_vec(u16* p, const Vec<V>& v) {
-  if constexpr (V == 8) {
-    typedef uint32_t u4 __attribute__((ext_vector_type(4)));
-    *reinterpret_cast<u4*>(p) = u4{v.d[0], v.d[1], v.d[2], v.d[3]};
-  } else if constexpr (V == 4) {
-    typedef uint32_t u2 __attribute__((ext_vector_type(2)));
-    *reinterpret_cast<u2*>(p) = u2{v.d[0], v.d[1]};
-  } else {
-    *reinterpret_cast<uint32_t*>(p) = v.d[0];
-  }
-}
 
 template <class T, int V>
 __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_bf16(WgArgs a) {

@@ -160,9 +160,9 @@ def test_conv_bwd_weight(shape, dtype):
     assert torch.equal(dw, dw2) and torch.equal(db, db2)
 
 
-# bf16 weight-gradient shapes that reach each staging width of the bf16 MFMA
-# kernel (8, 4, 2 or 1 columns per load, from the image width) on each tile
-# shape (32, 16 and 8 columns wide), with ragged channel and k blocks.
+# bf16 shapes that reach each staging width of the bf16 MFMA kernels (8, 4,
+# 2 or 1 columns per load, from the image width) on each tile shape (32, 16
+# and 8 columns wide), with ragged channel and k blocks.
 WGRAD_BF16_SHAPES = [
     (2, 40, 5, 36, 64),      # 32-wide tiles, 4 columns per load
     (1, 32, 4, 34, 70),      # 32-wide tiles, 2 columns per load
@@ -172,6 +172,39 @@ WGRAD_BF16_SHAPES = [
     (2, 48, 9, 11, 64),      # 8-wide tiles, 1 column per load
     (1, 64, 3, 64, 128),     # 32-wide tiles, two full column tiles
 ]
+
+
+def _dev_at(a, offset):
+    """a as a bf16 device tensor starting `offset` elements into a buffer."""
+    buf = torch.empty(a.size + offset, dtype=torch.bfloat16, device="cuda")
+    t = buf[offset:].view(a.shape)
+    t.copy_(to_dev(a, "bf16"))
+    return t
+
+
+@pytest.mark.parametrize("shape", WGRAD_BF16_SHAPES)
+@pytest.mark.parametrize("offset", [0, 1])
+def test_conv_fwd_bwd_data_bf16_staging(shape, offset):
+    """The bf16 forward and data-gradient kernels over the same staging
+    widths; offset = 1 element takes the one-column halo loads."""
+    n, c, h, w, k = shape
+    print_case("conv_fwd_bwd_data_bf16", shape=shape, offset=offset)
+    x, wt, b, dy, mask = _conv_inputs(n, c, h, w, k, 16)
+    df = sb.conv_desc(n, c, h, w, k, sb.SB_BF16, relu=True)
+    dd = sb.conv_desc(n, c, h, w, k, sb.SB_BF16)
+    ws = _ws(max(sb.sb_conv3x3_workspace_bytes(df, sb.SB_PASS_FWD),
+                 sb.sb_conv3x3_workspace_bytes(dd, sb.SB_PASS_BWD_DATA)))
+    xd, dyd, md = _dev_at(x, offset), _dev_at(dy, offset), _dev_at(mask, offset)
+    wd = to_dev(wt, "bf16")
+    y = torch.full((n, k, h, w), float("nan"), dtype=torch.bfloat16, device="cuda")
+    sb.sb_conv3x3_fwd(df, xd, wd, to_dev(b), y, ws)
+    dx = torch.full((n, c, h, w), float("nan"), dtype=torch.bfloat16, device="cuda")
+    sb.sb_conv3x3_bwd_data(dd, dyd, wd, md, dx, ws)
+    torch.cuda.synchronize()
+    ref = O.conv3x3_fwd(to_host(xd), to_host(wd), b, relu=True)
+    assert rel_l2(to_host(y), ref) <= TOL["bf16"]
+    ref = O.conv3x3_bwd_data(to_host(dyd), to_host(wd), mask_src=to_host(md))
+    assert rel_l2(to_host(dx), ref) <= TOL["bf16"]
 
 
 @pytest.mark.parametrize("shape", WGRAD_BF16_SHAPES)
@@ -184,12 +217,7 @@ def test_conv_bwd_weight_bf16_staging(shape, offset):
     x, _, _, dy, _ = _conv_inputs(n, c, h, w, k, 15)
     d = sb.conv_desc(n, c, h, w, k, sb.SB_BF16)
     ws = _ws(sb.sb_conv3x3_workspace_bytes(d, sb.SB_PASS_BWD_WEIGHT))
-    xb = torch.empty(x.size + offset, dtype=torch.bfloat16, device="cuda")
-    dyb = torch.empty(dy.size + offset, dtype=torch.bfloat16, device="cuda")
-    xd = xb[offset:].view(x.shape)
-    dyd = dyb[offset:].view(dy.shape)
-    xd.copy_(to_dev(x, "bf16"))
-    dyd.copy_(to_dev(dy, "bf16"))
+    xd, dyd = _dev_at(x, offset), _dev_at(dy, offset)
     dw = torch.full((k, c, 3, 3), float("nan"), device="cuda")
     db = torch.full((k,), float("nan"), device="cuda")
     sb.sb_conv3x3_bwd_weight(d, xd, dyd, dw, db, ws)
