@@ -342,11 +342,13 @@ struct BPlan {
   size_t pack_bytes, part_off, ws_bytes;
 };
 
-// The bf16 MFMA path takes images at least 8 wide with at least 16 input
-// channels; other shapes stay on the fp32-MFMA kernels.
+// The bf16 MFMA path takes images at least 8 wide; narrower ones stay on the
+// fp32-MFMA kernels.  Channel counts below the 16-channel chunk or the
+// 64-channel output tile are padded (the first layer's 3 input channels,
+// its data gradient's 3 output channels).
 static BPlan bf16_plan(int N, int Cin, int H, int W, int Cout) {
   BPlan p{};
-  if (W < 8 || Cin < 16) return p;
+  if (W < 8) return p;
   int th, tw, imgs = 1;
   if (W >= 32) { p.tile = 0; th = 8; tw = 32; }
   else if (W >= 16) { p.tile = 1; th = 16; tw = 16; }

@@ -717,7 +717,8 @@ static const char* kWgNames[] = {
 static WgPlan wg_plan(int N, int C, int H, int W, int K, bool allow_small, bool bf16) {
   WgPlan p{};
   int th = 2, tw = 32, imgs = 1;
-  const bool narrow = C <= 7;
+  // bf16 images at least 8 wide take the bf16 MFMA kernel whatever C.
+  const bool narrow = C <= 7 && !(bf16 && W >= 8);
   if (narrow) {
     // 32-wide rows for wide images, 4x4 x 4-image tiles otherwise.
     if (W >= 32) { p.tile = C <= 3 ? 5 : 6; }
