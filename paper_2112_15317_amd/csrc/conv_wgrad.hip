@@ -126,12 +126,12 @@ struct WgTile {
   static constexpr int NACC = NARROW ? NCB : 9;     // accumulator blocks per wave
   static constexpr int HH = TH + 2, HW = TW + 2;
   static constexpr int PLANE = IMGS * HH * HW;      // halo pixels per channel
-  static constexpr int DY_STRIDE = BK + 16;         // floats per pixel row of dy
-  static constexpr int LDS_DY = BP * DY_STRIDE;
+  // dy tile [k][pixel], rows 68 floats apart (4 mod 64 banks): the 16 rows
+  // x 4 pixels of an operand read and of a staging write hit 64 banks.
+  static constexpr int DYP = BP + 4;
+  static constexpr int LDS_DY = BK * DYP;
   static constexpr int LDS_X = PLANE * BC;
-  // Halo staging lanes past the end store into a private slot (256 floats)
-  // after the halo, so the stores need no condition.
-  static constexpr int LDS_BUF = LDS_DY + LDS_X + 256;
+  static constexpr int LDS_BUF = LDS_DY + LDS_X;
   static constexpr int DY_PT = BK * BP / 256;       // 16
   static constexpr int X_PT = (BC * PLANE + 255) / 256;
   static constexpr size_t LDS_BYTES = 2 * LDS_BUF * sizeof(float);
@@ -187,7 +187,7 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_f32(WgArgs a) {
     const rsrc_t xr = image_rsrc<E>(a.x, n0, T::IMGS, a.N, a.C * HWs);
     // dy: element e = (pixel quad, k-in-tile, pixel within the quad).  A
     // wave covers 16 k x 4 consecutive pixels: 16 rows of 16 B in global
-    // memory, and 64 distinct banks in the [pixel][k] LDS tile.
+    // memory, and 64 distinct banks in the [k][pixel] LDS tile.
 #pragma unroll
     for (int i = 0; i < T::DY_PT; ++i) {
       int e = tid + i * 256;
@@ -221,39 +221,51 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_f32(WgArgs a) {
     for (int i = 0; i < T::DY_PT; ++i) {
       int e = tid + i * 256;
       int kk = (e >> 2) & (T::BK - 1), p = ((e >> 8) << 2) | (e & 3);
-      Dl[p * T::DY_STRIDE + kk] = rdy[i];
+      Dl[kk * T::DYP + p] = rdy[i];
     }
 #pragma unroll
     for (int i = 0; i < T::X_PT; ++i) {
       int e = tid + i * 256;
-      Xl[e < T::BC * T::PLANE ? e : T::LDS_X + tid] = rx[i];     // = [halo pixel][c]
+      if (e < T::BC * T::PLANE) Xl[e] = rx[i];                 // = [halo pixel][c]
     }
+  };
+  // Operands of one 4-pixel step: the dy value and the NACC x values.  The
+  // next step's operands are read from LDS before this step's MFMAs issue,
+  // so their latency hides behind the MFMAs.
+  struct Ops { float a, b[T::NACC]; };
+  auto fetch = [&](const float* Dl, const float* Xl, int st) {
+    Ops o;
+    const int pbase = st * 4;
+    const int hbase = wg_hoff<T>(pbase);            // compile-time after unrolling
+    o.a = Dl[(wave * 16 + lr) * T::DYP + pbase + jq];
+    const float* Xp = Xl + (hbase + lane_hoff) * T::BC;
+    if (T::NARROW) {
+#pragma unroll
+      for (int cb = 0; cb < T::NACC; ++cb) {
+        float b = Xp[col_off[cb % NC]];
+        o.b[cb] = col_ok[cb % NC] ? b : 0.f;
+      }
+    } else {
+#pragma unroll
+      for (int t = 0; t < T::NACC; ++t) {
+        const int toff = (t / 3) * T::HW + (t % 3);
+        o.b[t] = Xp[toff * T::BC + lr];
+      }
+    }
+    return o;
   };
   auto compute = [&](int buf) {
     const float* Dl = lds + buf * T::LDS_BUF;
     const float* Xl = Dl + T::LDS_DY;
+    Ops cur = fetch(Dl, Xl, 0);
 #pragma unroll
     for (int st = 0; st < T::BP / 4; ++st) {
-      const int pbase = st * 4;
-      const int hbase = wg_hoff<T>(pbase);          // compile-time after unrolling
-      float av = Dl[(pbase + jq) * T::DY_STRIDE + wave * 16 + lr];
-      const float* Xp = Xl + (hbase + lane_hoff) * T::BC;
-      if (T::NARROW) {
+      Ops nxt;
+      if (st + 1 < T::BP / 4) nxt = fetch(Dl, Xl, st + 1);
 #pragma unroll
-        for (int cb = 0; cb < T::NACC; ++cb) {
-          float b = Xp[col_off[cb % NC]];
-          b = col_ok[cb % NC] ? b : 0.f;
-          acc[cb] = mfma16x16x4(av, b, acc[cb]);
-        }
-      } else {
-#pragma unroll
-        for (int t = 0; t < 9; ++t) {
-          const int toff = (t / 3) * T::HW + (t % 3);
-          float b = Xp[toff * T::BC + lr];
-          acc[t] = mfma16x16x4(av, b, acc[t]);
-        }
-      }
-      if (do_db) accb = mfma16x16x4(av, 1.0f, accb);
+      for (int t = 0; t < T::NACC; ++t) acc[t] = mfma16x16x4(cur.a, cur.b[t], acc[t]);
+      if (do_db) accb = mfma16x16x4(cur.a, 1.0f, accb);
+      if (st + 1 < T::BP / 4) cur = nxt;
     }
   };
 
