@@ -44,7 +44,9 @@ template <int TH_, int TW_, int IMGS_>
 struct BTile {
   static constexpr int TH = TH_, TW = TW_, IMGS = IMGS_;
   static constexpr int BM = IMGS * TH * TW;
-  static_assert(BM == 256, "pixel tile must hold 256 pixels");
+  static_assert(BM == 256 || BM == 512, "pixel tile must hold 256 or 512 pixels");
+  static constexpr int WP = BM / 4;                 // pixels per wave
+  static constexpr int MB = WP / 32;                // 32-pixel MFMA blocks per wave
   static constexpr int BN = 64, CK = 16;
   static constexpr int HH = TH + 2, HW = TW + 2;
   static constexpr int ROWS = IMGS * HH;            // halo rows
@@ -58,7 +60,7 @@ struct BTile {
   static constexpr size_t LDS_BYTES = 2 * LDS_BUF * sizeof(u16);
   static_assert(LDS_BYTES <= 80 * 1024, "two blocks must fit in the 160 KB of LDS");
   // Pixel p of the tile: images outermost, then rows, then columns; a wave
-  // owns 64 consecutive pixels (two blocks of 32).
+  // owns WP consecutive pixels (MB blocks of 32).
   __host__ __device__ static constexpr int img_of(int p) { return p / (TH * TW); }
   __host__ __device__ static constexpr int yy_of(int p) { return p % (TH * TW) / TW; }
   __host__ __device__ static constexpr int xx_of(int p) { return p % TW; }
@@ -120,18 +122,18 @@ __global__ __launch_bounds__(256, 2) void conv3x3_igemm_bf16(ConvArgs a) {
   }
   // Operand rows of this lane: pixel lc of each of the wave's two pixel
   // blocks (halo pixel at tap (0, 0)), channel-plane lh.
-  int b_off[2];
+  int b_off[T::MB];
 #pragma unroll
-  for (int mb = 0; mb < 2; ++mb) {
-    const int p = wave * 64 + mb * 32 + lc;
+  for (int mb = 0; mb < T::MB; ++mb) {
+    const int p = wave * T::WP + mb * 32 + lc;
     b_off[mb] = (lh * T::PLANE + T::hp(T::img_of(p), T::yy_of(p), T::xx_of(p))) * 8;
   }
 
-  f16 acc[2][2];
+  f16 acc[2][T::MB];
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < T::MB; ++j)
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
@@ -195,17 +197,18 @@ __global__ __launch_bounds__(256, 2) void conv3x3_igemm_bf16(ConvArgs a) {
 #pragma unroll
     for (int t = 0; t < 9; ++t) {
       const int toff = T::hp(0, t / 3, t % 3) * 8;
-      s8 fa[2], fb[2];
+      s8 fa[2], fb[T::MB];
 #pragma unroll
       for (int nb = 0; nb < 2; ++nb)
         fa[nb] = *reinterpret_cast<const s8*>(Wl + ((t * 2 + lh) * T::BN + nb * 32 + lc) * 8);
 #pragma unroll
-      for (int mb = 0; mb < 2; ++mb)
+      for (int mb = 0; mb < T::MB; ++mb)
         fb[mb] = *reinterpret_cast<const s8*>(X + b_off[mb] + toff);
 #pragma unroll
       for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
-        for (int mb = 0; mb < 2; ++mb) acc[nb][mb] = mfma32x32x16bf16(fa[nb], fb[mb], acc[nb][mb]);
+        for (int mb = 0; mb < T::MB; ++mb)
+          acc[nb][mb] = mfma32x32x16bf16(fa[nb], fb[mb], acc[nb][mb]);
     }
   };
 
@@ -226,10 +229,10 @@ __global__ __launch_bounds__(256, 2) void conv3x3_igemm_bf16(ConvArgs a) {
 
   // acc[nb][mb] element v: output channel co0 + nb*32 + 8*(v/4) + 4*lh +
   // v%4 of pixel wave*64 + mb*32 + lc.
-  int pix[2];                                        // offset from image n0, -1 outside
+  int pix[T::MB];                                    // offset from image n0, -1 outside
 #pragma unroll
-  for (int mb = 0; mb < 2; ++mb) {
-    const int p = wave * 64 + mb * 32 + lc;
+  for (int mb = 0; mb < T::MB; ++mb) {
+    const int p = wave * T::WP + mb * 32 + lc;
     const int img = T::img_of(p), h = h0 + T::yy_of(p), w = w0 + T::xx_of(p);
     pix[mb] = n0 + img < a.N && h < a.H && w < a.W ? img * a.Cout * HWs + h * a.W + w : -1;
   }
@@ -237,7 +240,7 @@ __global__ __launch_bounds__(256, 2) void conv3x3_igemm_bf16(ConvArgs a) {
   if (a.splits > 1) {
     float* mine = a.part + (size_t)blockIdx.z * a.N * a.Cout * HWs + (size_t)n0 * a.Cout * HWs;
 #pragma unroll
-    for (int mb = 0; mb < 2; ++mb) {
+    for (int mb = 0; mb < T::MB; ++mb) {
       if (pix[mb] < 0) continue;
 #pragma unroll
       for (int nb = 0; nb < 2; ++nb)
@@ -249,7 +252,7 @@ __global__ __launch_bounds__(256, 2) void conv3x3_igemm_bf16(ConvArgs a) {
     }
     return;
   }
-  // The block's 64 x 256 outputs go through LDS ([channel][pixel], bias and
+  // The block's 64 x BM outputs go through LDS ([channel][pixel], bias and
   // ReLU applied, rounded to bf16), then out to memory in pieces of V
   // consecutive pixels of one channel, the ReLU mask read in the same
   // pieces; every mask load is issued before the first store.
@@ -263,10 +266,10 @@ __global__ __launch_bounds__(256, 2) void conv3x3_igemm_bf16(ConvArgs a) {
       const int co = co_of(nb, v);
       const float bv = a.bias && co < a.Cout ? a.bias[co] : 0.f;
 #pragma unroll
-      for (int mb = 0; mb < 2; ++mb) {
+      for (int mb = 0; mb < T::MB; ++mb) {
         float r = acc[nb][mb][v] + bv;
         if (a.relu && !(r > 0.f)) r = 0.f;
-        E[(co - co0) * EP + wave * 64 + mb * 32 + lc] = f32_to_bf16(r);
+        E[(co - co0) * EP + wave * T::WP + mb * 32 + lc] = f32_to_bf16(r);
       }
     }
   __syncthreads();
@@ -329,11 +332,15 @@ __global__ __launch_bounds__(256, 2) void conv3x3_igemm_bf16(ConvArgs a) {
 using BTileW32 = BTile<8, 32, 1>;
 using BTileW16 = BTile<16, 16, 1>;
 using BTileW8 = BTile<8, 8, 4>;
+using BTileW32L = BTile<16, 32, 1>;     // 512 pixels: 64 x 128 per wave
+using BTileW64L = BTile<8, 64, 1>;
 
 static const char* kBTileNames[] = {
     "sb::conv3x3_igemm_bf16<sb::BTile<8, 32, 1>, %s, %d>",
     "sb::conv3x3_igemm_bf16<sb::BTile<16, 16, 1>, %s, %d>",
     "sb::conv3x3_igemm_bf16<sb::BTile<8, 8, 4>, %s, %d>",
+    "sb::conv3x3_igemm_bf16<sb::BTile<16, 32, 1>, %s, %d>",
+    "sb::conv3x3_igemm_bf16<sb::BTile<8, 64, 1>, %s, %d>",
 };
 
 struct BPlan {
@@ -345,14 +352,31 @@ struct BPlan {
 // The bf16 MFMA path takes images at least 8 wide; narrower ones stay on the
 // fp32-MFMA kernels.  Channel counts below the 16-channel chunk or the
 // 64-channel output tile are padded (the first layer's 3 input channels,
-// its data gradient's 3 output channels).
-static BPlan bf16_plan(int N, int Cin, int H, int W, int Cout) {
+// its data gradient's 3 output channels).  v8: the tensors allow 8-column
+// staging, which the 512-pixel tiles need (their registers leave no room for
+// the narrower staging).  The 512-pixel tiles pay off on long channel loops
+// (256 or more input channels); with fewer chunks per block the 256-pixel
+// tile's shorter prologue and epilogue win.
+static BPlan bf16_plan(int N, int Cin, int H, int W, int Cout, bool v8) {
   BPlan p{};
   if (W < 8) return p;
   int th, tw, imgs = 1;
-  if (W >= 32) { p.tile = 0; th = 8; tw = 32; }
-  else if (W >= 16) { p.tile = 1; th = 16; tw = 16; }
-  else { p.tile = 2; th = 8; tw = 8; imgs = 4; }
+  // 512-pixel tiles (each wave 64 channels x 128 pixels: a quarter fewer LDS
+  // operand bytes per MFMA than 64 x 64), 16 x 32 or 8 x 64, whichever pads
+  // the image less, when they still fill the chip without a split.
+  bool big = W >= 32 && v8 && Cin >= 256;
+  if (big) {
+    const long a16 = (long)round_up(H, 16) * round_up(W, 32);
+    const long a8 = (long)round_up(H, 8) * round_up(W, 64);
+    if (a16 <= a8) { p.tile = 3; th = 16; tw = 32; }
+    else { p.tile = 4; th = 8; tw = 64; }
+    big = (long)cdiv(W, tw) * cdiv(H, th) * N * cdiv(Cout, 64) >= 512;
+  }
+  if (!big) {
+    if (W >= 32) { p.tile = 0; th = 8; tw = 32; }
+    else if (W >= 16) { p.tile = 1; th = 16; tw = 16; }
+    else { p.tile = 2; th = 8; tw = 8; imgs = 4; }
+  }
   p.ok = true;
   p.imgs = imgs;
   p.tiles_w = cdiv(W, tw);
@@ -423,7 +447,9 @@ static void bf16_dispatch(int v, const BPlan& p, const ConvArgs& a, hipStream_t 
   switch (p.tile) {
     case 0: bf16_launch_v<BTileW32, DGRAD>(v, p, a, st); break;
     case 1: bf16_launch_v<BTileW16, DGRAD>(v, p, a, st); break;
-    default: bf16_launch_v<BTileW8, DGRAD>(v, p, a, st); break;
+    case 2: bf16_launch_v<BTileW8, DGRAD>(v, p, a, st); break;
+    case 3: bf16_launch<BTileW32L, DGRAD, 8>(p, a, st); break;
+    default: bf16_launch<BTileW64L, DGRAD, 8>(p, a, st); break;
   }
 }
 
@@ -431,19 +457,21 @@ static void bf16_dispatch(int v, const BPlan& p, const ConvArgs& a, hipStream_t 
 
 namespace sbh {
 
-// Workspace of the bf16 MFMA path, or 0 when it does not take the shape.
+// Workspace of the bf16 MFMA path (either staging width), or 0 when it does
+// not take the shape.
 size_t conv_bf16_ws(int N, int Cin, int H, int W, int Cout) {
-  sb::BPlan p = sb::bf16_plan(N, Cin, H, W, Cout);
-  return p.ok ? p.ws_bytes : 0;
+  sb::BPlan p = sb::bf16_plan(N, Cin, H, W, Cout, true);
+  sb::BPlan q = sb::bf16_plan(N, Cin, H, W, Cout, false);
+  return p.ok ? std::max(p.ws_bytes, q.ws_bytes) : 0;
 }
 
 bool conv_bf16_takes(int N, int Cin, int H, int W, int Cout) {
-  return sb::bf16_plan(N, Cin, H, W, Cout).ok;
+  return sb::bf16_plan(N, Cin, H, W, Cout, false).ok;
 }
 
 // Names the kernel as launched for aligned tensors.
 int conv_bf16_describe(bool dgrad, int N, int Cin, int H, int W, int Cout, char* buf, size_t len) {
-  sb::BPlan p = sb::bf16_plan(N, Cin, H, W, Cout);
+  sb::BPlan p = sb::bf16_plan(N, Cin, H, W, Cout, W % 8 == 0);
   char name[160];
   snprintf(name, sizeof(name), sb::kBTileNames[p.tile], dgrad ? "true" : "false",
            sb::bf16_vec(W, nullptr, nullptr, nullptr));
@@ -453,7 +481,8 @@ int conv_bf16_describe(bool dgrad, int N, int Cin, int H, int W, int Cout, char*
 sb_status conv_bf16(bool dgrad, int N, int Cin, int H, int W, int Cout, const void* in,
                     const void* wt, const float* bias, const void* mask, void* out, void* ws,
                     size_t ws_bytes, int relu, hipStream_t st) {
-  sb::BPlan p = sb::bf16_plan(N, Cin, H, W, Cout);
+  const int v = sb::bf16_vec(W, in, out, mask);
+  sb::BPlan p = sb::bf16_plan(N, Cin, H, W, Cout, v == 8);
   if (!p.ok) return SB_ERR_UNSUPPORTED;
   // Buffer ranges: one block's images of the input and of the output / mask,
   // one tile's packed filters.
@@ -468,7 +497,6 @@ sb_status conv_bf16(bool dgrad, int N, int Cin, int H, int W, int Cout, const vo
   a.N = N; a.Cin = Cin; a.H = H; a.W = W; a.Cout = Cout;
   a.tiles_w = p.tiles_w; a.tiles_h = p.tiles_h;
   a.nchunks = p.nchunks; a.chunks_per_split = p.cps; a.splits = p.splits; a.relu = relu;
-  const int v = sb::bf16_vec(W, in, out, mask);
   if (dgrad) sb::bf16_dispatch<true>(v, p, a, st);
   else sb::bf16_dispatch<false>(v, p, a, st);
   return launch_status();
