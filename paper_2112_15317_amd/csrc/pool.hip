@@ -65,13 +65,117 @@ __global__ __launch_bounds__(256) void relu_maxpool_bwd_kernel(
   }
 }
 
+// Vector form: 4 windows per thread, output width a multiple of 4 and every
+// tensor 16-byte aligned.  The two input rows of the 4 windows are 8
+// contiguous elements each (16 bytes in bf16, 32 in fp32), the 4 outputs and
+// the 4 codes contiguous too: every access is a whole vector.
+template <typename T> struct V8;                   // 8 elements
+template <> struct V8<float> {
+  typedef float t __attribute__((ext_vector_type(8)));
+  __device__ static float get(const t& v, int i) { return v[i]; }
+  __device__ static void put(t& v, int i, float x) { v[i] = x; }
+};
+template <> struct V8<u16> {
+  typedef u16 t __attribute__((ext_vector_type(8)));
+  __device__ static float get(const t& v, int i) { return bf16_to_f32(v[i]); }
+  __device__ static void put(t& v, int i, float x) { v[i] = f32_to_bf16(x); }
+};
+template <typename T> struct V4;                   // 4 elements
+template <> struct V4<float> {
+  typedef float t __attribute__((ext_vector_type(4)));
+  __device__ static float get(const t& v, int i) { return v[i]; }
+  __device__ static void put(t& v, int i, float x) { v[i] = x; }
+};
+template <> struct V4<u16> {
+  typedef u16 t __attribute__((ext_vector_type(4)));
+  __device__ static float get(const t& v, int i) { return bf16_to_f32(v[i]); }
+  __device__ static void put(t& v, int i, float x) { v[i] = f32_to_bf16(x); }
+};
+
+template <typename T>
+__global__ __launch_bounds__(256) void relu_maxpool_fwd_vec(
+    const T* __restrict__ x, T* __restrict__ y, uint8_t* __restrict__ idx,
+    uint32_t Wo, uint32_t groups_per_row, uint32_t total_groups) {
+  typedef typename V8<T>::t in_t;
+  typedef typename V4<T>::t out_t;
+  uint32_t g = blockIdx.x * 256u + threadIdx.x;
+  if (g >= total_groups) return;
+  uint32_t row = g / groups_per_row;               // (n*C + c)*Ho + oh
+  uint32_t ow0 = (g - row * groups_per_row) * 4;
+  const size_t W = 2 * (size_t)Wo;
+  const T* p0 = x + (size_t)row * 2 * W + 2 * ow0;
+  const in_t r0 = *reinterpret_cast<const in_t*>(p0);
+  const in_t r1 = *reinterpret_cast<const in_t*>(p0 + W);
+  out_t o;
+  uint32_t codes = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    float m = V8<T>::get(r0, 2 * j);
+    uint32_t a = 0;
+    const float v1 = V8<T>::get(r0, 2 * j + 1), v2 = V8<T>::get(r1, 2 * j),
+                v3 = V8<T>::get(r1, 2 * j + 1);
+    if (v1 > m) { m = v1; a = 1; }
+    if (v2 > m) { m = v2; a = 2; }
+    if (v3 > m) { m = v3; a = 3; }
+    const bool pos = m > 0.0f;
+    V4<T>::put(o, j, pos ? m : 0.0f);
+    codes |= (a | (pos ? 0u : 0x80u)) << (8 * j);
+  }
+  const size_t oo = (size_t)row * Wo + ow0;
+  *reinterpret_cast<out_t*>(y + oo) = o;
+  *reinterpret_cast<uint32_t*>(idx + oo) = codes;
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void relu_maxpool_bwd_vec(
+    const T* __restrict__ dy, const uint8_t* __restrict__ idx, T* __restrict__ dx,
+    uint32_t Wo, uint32_t groups_per_row, uint32_t total_groups) {
+  typedef typename V8<T>::t row_t;
+  typedef typename V4<T>::t in_t;
+  uint32_t g = blockIdx.x * 256u + threadIdx.x;
+  if (g >= total_groups) return;
+  uint32_t row = g / groups_per_row;
+  uint32_t ow0 = (g - row * groups_per_row) * 4;
+  const size_t W = 2 * (size_t)Wo;
+  const size_t oo = (size_t)row * Wo + ow0;
+  const in_t gv = *reinterpret_cast<const in_t*>(dy + oo);
+  const uint32_t codes = *reinterpret_cast<const uint32_t*>(idx + oo);
+  row_t r0, r1;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const uint32_t code = (codes >> (8 * j)) & 0xffu;
+    const bool live = !(code & 0x80u);
+    const uint32_t a = code & 3u;
+    const float v = V4<T>::get(gv, j);
+    V8<T>::put(r0, 2 * j, (live && a == 0) ? v : 0.0f);
+    V8<T>::put(r0, 2 * j + 1, (live && a == 1) ? v : 0.0f);
+    V8<T>::put(r1, 2 * j, (live && a == 2) ? v : 0.0f);
+    V8<T>::put(r1, 2 * j + 1, (live && a == 3) ? v : 0.0f);
+  }
+  T* p0 = dx + (size_t)row * 2 * W + 2 * ow0;
+  *reinterpret_cast<row_t*>(p0) = r0;
+  *reinterpret_cast<row_t*>(p0 + W) = r1;
+}
+
 template <typename T>
 static sb_status pool_launch(bool fwd, int n, int c, int h, int w, const void* in,
                              const uint8_t* idx_in, void* out, uint8_t* idx_out,
                              hipStream_t st) {
-  constexpr int PT = 2;
   uint32_t Wo = (uint32_t)(w / 2);
   uint32_t rows = (uint32_t)n * c * (h / 2);
+  const uintptr_t al = (uintptr_t)in | (uintptr_t)idx_in | (uintptr_t)out | (uintptr_t)idx_out;
+  if (Wo % 4 == 0 && al % 16 == 0) {
+    const uint32_t gpr = Wo / 4, total = rows * gpr;
+    dim3 grid((total + 255) / 256), block(256);
+    if (fwd)
+      relu_maxpool_fwd_vec<T><<<grid, block, 0, st>>>((const T*)in, (T*)out, idx_out, Wo, gpr,
+                                                      total);
+    else
+      relu_maxpool_bwd_vec<T><<<grid, block, 0, st>>>((const T*)in, idx_in, (T*)out, Wo, gpr,
+                                                      total);
+    return sbh::launch_status();
+  }
+  constexpr int PT = 2;
   uint32_t gpr = (Wo + PT - 1) / PT;
   uint32_t total = rows * gpr;
   dim3 grid((total + 255) / 256), block(256);

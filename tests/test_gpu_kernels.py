@@ -21,6 +21,7 @@ def _ws(nbytes):
 
 # ------------------------------------------------------------------ pool --
 POOL_SHAPES = [(2, 3, 4, 4), (3, 5, 6, 10), (1, 1, 2, 2), (4, 7, 8, 6), (2, 64, 32, 32),
+               (2, 5, 6, 16), (1, 3, 4, 24),    # 4-window vector form
                (1, 3, 2, 30), (128, 512, 2, 2)]
 
 
