@@ -58,11 +58,25 @@ __device__ __forceinline__ rsrc_t image_rsrc(const void* t, int n0, int imgs, in
                    (uint32_t)((size_t)cnt * per_img * sizeof(E)));
 }
 
+// The block's (column block, split) = (x, z), with the hardware block ids
+// remapped so that each of the 8 XCDs runs whole splits: the dispatcher
+// deals consecutive blocks round-robin to the XCDs, and all column blocks
+// of a split read the same pixel tiles of x and dy, which then come from
+// that XCD's L2 instead of every XCD fetching them.  Grids whose size is
+// not a multiple of 8 keep the plain order.
+struct WgBlock { int x, z; };
+__device__ __forceinline__ WgBlock wg_block() {
+  const int gx = gridDim.x, nb = gx * gridDim.z;
+  int h = blockIdx.x + gx * blockIdx.z;
+  if (nb % 8 == 0) h = (h % 8) * (nb / 8) + h / 8;
+  return WgBlock{h % gx, h / gx};
+}
+
 // Writes (or split-reduces) the block's 64 k x 16-column x NACC outputs.
 // `val(i, t)` is the lane's accumulator t, element i; `col(t)` the flattened
 // (c, tap) column of the lane in accumulator t, or -1.
 template <int NACC, class Val, class Col>
-__device__ __forceinline__ void wgrad_store(const WgArgs& a, int k_base, bool do_db,
+__device__ __forceinline__ void wgrad_store(const WgArgs& a, int z, int k_base, bool do_db,
                                             const f4& accb, Val val, Col col) {
   const int lane = threadIdx.x & 63, jq = lane >> 4, lr = lane & 15;
   const size_t wsz = (size_t)a.K * a.C * 9;
@@ -91,7 +105,7 @@ __device__ __forceinline__ void wgrad_store(const WgArgs& a, int k_base, bool do
     each_db([&](float v, int k) { a.db[k] = v; });
     return;
   }
-  float* pw = a.part + (size_t)blockIdx.z * (wsz + a.K);
+  float* pw = a.part + (size_t)z * (wsz + a.K);
   float* pb = pw + wsz;
   each([&](float v, size_t o) { pw[o] = v; });
   each_db([&](float v, int k) { pb[k] = v; });
@@ -152,9 +166,10 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_f32(WgArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int jq = lane >> 4, lr = lane & 15;
-  const int ct = blockIdx.x % a.c_tiles, kt = blockIdx.x / a.c_tiles;
+  const WgBlock blk = wg_block();
+  const int ct = blk.x % a.c_tiles, kt = blk.x / a.c_tiles;
   const int c0 = ct * T::BC, k0 = kt * T::BK;
-  const int pt0 = blockIdx.z * a.tiles_per_split;
+  const int pt0 = blk.z * a.tiles_per_split;
   const int pt1 = min(a.ptiles, pt0 + a.tiles_per_split);
   const bool do_db = (a.db != nullptr) && ct == 0;
   const int HWs = a.H * a.W;
@@ -286,7 +301,7 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_f32(WgArgs a) {
 
   // acc[t] lane holds rows k = k0 + wave*16 + 4*jq + i and column lr of its block.
   wgrad_store<T::NACC>(
-      a, k0 + wave * 16, do_db, accb, [&](int i, int t) { return acc[t][i]; },
+      a, blk.z, k0 + wave * 16, do_db, accb, [&](int i, int t) { return acc[t][i]; },
       [&](int t) -> int {
         if (T::NARROW) {
           int j = t * 16 + lr;
@@ -310,9 +325,13 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_f32(WgArgs a) {
 //     so the 8 pixels a lane reads at tap (r, s) are 16 aligned bytes of
 //     copy s.  Channel planes sit 8 * odd words apart, so the 16 channels of
 //     a 16-lane group land in distinct bank groups.
-// With BC = 32 the four waves form a 2 x 2 grid, each wave 32 k x 16 c, so a
-// B operand read from LDS feeds two MFMAs.  The bias gradient is one more
-// MFMA per 16 k rows and step against a column of ones.
+// The four waves split the block's 16-channel column groups (BC / 16 of
+// them), its k rows and the two 32-pixel steps of a stage: with BC = 32 a
+// wave owns all 64 k x 16 c for one of the two steps, so one B operand read
+// from LDS feeds four MFMAs (and an A read nine); with BC = 16, 32 k x 16 c
+// for one step.  The two step halves of a wave's columns are summed through
+// LDS at the end.  The bias gradient is one more MFMA per 16 k rows and step
+// against a column of ones.
 //
 // Staging moves V consecutive columns per lane (V = 8, 4, 2 when the image
 // width is a multiple of V, else 1): one global load of V elements per tile
@@ -329,7 +348,10 @@ struct WgBTile {
   static constexpr int BK = 64;
   static_assert(BC == 16 || BC == 32, "16 or 32 input channels per block");
   static constexpr int WC = BC / 16;                 // waves along c
-  static constexpr int MA = WC;                      // 16-row blocks of k per wave
+  static constexpr int WP = 2;                       // waves along the two pixel steps
+  static constexpr int WK = 4 / (WC * WP);           // waves along k
+  static constexpr int MA = 4 / WK;                  // 16-row blocks of k per wave
+  static_assert(WC * WP * WK == 4, "four waves");
   static constexpr int HH = TH + 2;
   static constexpr int PLANE = HH * TW;              // one channel of one copy
   static constexpr int plane_pitch(int p) { return (p / 2) % 8 == 4 ? p : plane_pitch(p + 8); }
@@ -350,11 +372,13 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_bf16(WgArgs a) {
   extern __shared__ u16 ldsw[];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int kq = lane >> 4, lr = lane & 15;
-  const int ct = blockIdx.x % a.c_tiles, kt = blockIdx.x / a.c_tiles;
+  const WgBlock blk = wg_block();
+  const int ct = blk.x % a.c_tiles, kt = blk.x / a.c_tiles;
   const int c0 = ct * T::BC, k0 = kt * T::BK;
-  const int pt0 = blockIdx.z * a.tiles_per_split;
+  const int pt0 = blk.z * a.tiles_per_split;
   const int pt1 = min(a.ptiles, pt0 + a.tiles_per_split);
-  const int wc = wave % T::WC, wk = wave / T::WC;
+  // wave = (wk, wp, wc), wc fastest.
+  const int wc = wave % T::WC, wp = (wave / T::WC) % T::WP, wk = wave / (T::WC * T::WP);
   const bool do_db = (a.db != nullptr) && ct == 0 && wc == 0;
   const int HWs = a.H * a.W;
 
@@ -494,13 +518,13 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_bf16(WgArgs a) {
       }
     }
   };
+  static_assert(T::BP / 32 == T::WP, "one 32-pixel step per wave and stage");
   auto compute = [&](int buf) {
     const u16* Dl = ldsw + buf * T::LDS_BUF;
     const u16* Xl = Dl + T::LDS_DY;
-#pragma unroll
-    for (int st = 0; st < T::BP / 32; ++st) {
-      // Lane group kq takes pixels p .. p+7 of this 32-pixel step.
-      const int p = st * 32 + 8 * kq;
+    {
+      // This wave's step wp; lane group kq takes pixels p .. p+7 of it.
+      const int p = wp * 32 + 8 * kq;
       const int yy = p / T::TW, xx = p % T::TW;
       s8 av[T::MA];
 #pragma unroll
@@ -543,12 +567,51 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_bf16(WgArgs a) {
     __syncthreads();
   }
 
+  // Sum the two step halves: waves wp = 1 hand their accumulators to the
+  // waves wp = 0 of the same (wk, wc) through LDS (lane fastest, so the
+  // stores and loads are conflict-free), in rounds of RA k blocks.
+  {
+    constexpr int RA =                                 // k blocks per round
+        T::MA >= 2 && T::WC * T::WK * 2 * 40 * 64 * 4 <= (int)T::LDS_BYTES ? 2 : 1;
+    constexpr int NF = RA * 10 * 4;                    // floats per lane per round
+    static_assert(T::WC * T::WK * NF * 64 * 4 <= T::LDS_BYTES, "reduction fits the LDS");
+    float* R = reinterpret_cast<float*>(ldsw) + (wk * T::WC + wc) * NF * 64;
+#pragma unroll
+    for (int r0 = 0; r0 < T::MA; r0 += RA) {
+      if (wp == 1) {
+#pragma unroll
+        for (int m = 0; m < RA; ++m) {
+#pragma unroll
+          for (int t = 0; t < 9; ++t)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) R[((m * 10 + t) * 4 + i) * 64 + lane] = acc[r0 + m][t][i];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) R[((m * 10 + 9) * 4 + i) * 64 + lane] = accb[r0 + m][i];
+        }
+      }
+      __syncthreads();
+      if (wp == 0) {
+#pragma unroll
+        for (int m = 0; m < RA; ++m) {
+#pragma unroll
+          for (int t = 0; t < 9; ++t)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) acc[r0 + m][t][i] += R[((m * 10 + t) * 4 + i) * 64 + lane];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) accb[r0 + m][i] += R[((m * 10 + 9) * 4 + i) * 64 + lane];
+        }
+      }
+      __syncthreads();
+    }
+  }
+  if (wp != 0) return;
+
   // acc[m][t] lane holds rows k = k0 + (wk*MA + m)*16 + 4*kq + i and
   // channel c0 + wc*16 + lr.
 #pragma unroll
   for (int m = 0; m < T::MA; ++m)
     wgrad_store<9>(
-        a, k0 + (wk * T::MA + m) * 16, do_db, accb[m],
+        a, blk.z, k0 + (wk * T::MA + m) * 16, do_db, accb[m],
         [&](int i, int t) { return acc[m][t][i]; },
         [&](int t) -> int {
           int c = c0 + wc * 16 + lr;
@@ -586,9 +649,10 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_small_f32(WgArgs a) {
   extern __shared__ float lds[];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int jq = lane >> 4, lr = lane & 15;
-  const int ct = blockIdx.x % a.c_tiles, kt = blockIdx.x / a.c_tiles;
+  const WgBlock blk = wg_block();
+  const int ct = blk.x % a.c_tiles, kt = blk.x / a.c_tiles;
   const int c0 = ct * T::BC, k0 = kt * T::BK;
-  const int ch0 = blockIdx.z * a.tiles_per_split;              // image chunks of IW
+  const int ch0 = blk.z * a.tiles_per_split;              // image chunks of IW
   const int ch1 = min(a.ptiles, ch0 + a.tiles_per_split);
   const bool do_db = (a.db != nullptr) && ct == 0;
 
@@ -687,7 +751,7 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_small_f32(WgArgs a) {
   }
 
   wgrad_store<9>(
-      a, k0 + wave * 16, do_db, accb, [&](int i, int t) { return acc[t][i]; },
+      a, blk.z, k0 + wave * 16, do_db, accb, [&](int i, int t) { return acc[t][i]; },
       [&](int t) -> int {
         int c = c0 + lr;
         return c < a.C ? c * 9 + t : -1;
