@@ -40,14 +40,15 @@ __device__ __forceinline__ f16 mfma32x32x16bf16(s8 a, s8 b, f16 c) {
                                                  __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
 
-template <int TH_, int TW_, int IMGS_>
+template <int TH_, int TW_, int IMGS_, int NB_ = 2>
 struct BTile {
   static constexpr int TH = TH_, TW = TW_, IMGS = IMGS_;
   static constexpr int BM = IMGS * TH * TW;
   static_assert(BM == 256 || BM == 512, "pixel tile must hold 256 or 512 pixels");
   static constexpr int WP = BM / 4;                 // pixels per wave
   static constexpr int MB = WP / 32;                // 32-pixel MFMA blocks per wave
-  static constexpr int BN = 64, CK = 16;
+  static constexpr int NB = NB_;                    // 32-channel MFMA blocks per wave
+  static constexpr int BN = 32 * NB, CK = 16;
   static constexpr int HH = TH + 2, HW = TW + 2;
   static constexpr int ROWS = IMGS * HH;            // halo rows
   static constexpr int PLANE = ROWS * HW;           // halo pixels
@@ -129,9 +130,9 @@ __global__ __launch_bounds__(256, 2) void conv3x3_igemm_bf16(ConvArgs a) {
     b_off[mb] = (lh * T::PLANE + T::hp(T::img_of(p), T::yy_of(p), T::xx_of(p))) * 8;
   }
 
-  f16 acc[2][T::MB];
+  f16 acc[T::NB][T::MB];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < T::NB; ++i)
 #pragma unroll
     for (int j = 0; j < T::MB; ++j)
 #pragma unroll
@@ -197,15 +198,15 @@ __global__ __launch_bounds__(256, 2) void conv3x3_igemm_bf16(ConvArgs a) {
 #pragma unroll
     for (int t = 0; t < 9; ++t) {
       const int toff = T::hp(0, t / 3, t % 3) * 8;
-      s8 fa[2], fb[T::MB];
+      s8 fa[T::NB], fb[T::MB];
 #pragma unroll
-      for (int nb = 0; nb < 2; ++nb)
+      for (int nb = 0; nb < T::NB; ++nb)
         fa[nb] = *reinterpret_cast<const s8*>(Wl + ((t * 2 + lh) * T::BN + nb * 32 + lc) * 8);
 #pragma unroll
       for (int mb = 0; mb < T::MB; ++mb)
         fb[mb] = *reinterpret_cast<const s8*>(X + b_off[mb] + toff);
 #pragma unroll
-      for (int nb = 0; nb < 2; ++nb)
+      for (int nb = 0; nb < T::NB; ++nb)
 #pragma unroll
         for (int mb = 0; mb < T::MB; ++mb)
           acc[nb][mb] = mfma32x32x16bf16(fa[nb], fb[mb], acc[nb][mb]);
@@ -243,7 +244,7 @@ __global__ __launch_bounds__(256, 2) void conv3x3_igemm_bf16(ConvArgs a) {
     for (int mb = 0; mb < T::MB; ++mb) {
       if (pix[mb] < 0) continue;
 #pragma unroll
-      for (int nb = 0; nb < 2; ++nb)
+      for (int nb = 0; nb < T::NB; ++nb)
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
           const int co = co_of(nb, v);
@@ -252,15 +253,15 @@ __global__ __launch_bounds__(256, 2) void conv3x3_igemm_bf16(ConvArgs a) {
     }
     return;
   }
-  // The block's 64 x BM outputs go through LDS ([channel][pixel], bias and
+  // The block's BN x BM outputs go through LDS ([channel][pixel], bias and
   // ReLU applied, rounded to bf16), then out to memory in pieces of V
   // consecutive pixels of one channel, the ReLU mask read in the same
   // pieces; every mask load is issued before the first store.
   constexpr int EP = T::BM + 8;                      // LDS row pitch (bf16)
-  static_assert(64 * EP <= 2 * T::LDS_BUF, "output tile fits the staging LDS");
+  static_assert(T::BN * EP <= 2 * T::LDS_BUF, "output tile fits the staging LDS");
   u16* E = ldsb;
 #pragma unroll
-  for (int nb = 0; nb < 2; ++nb)
+  for (int nb = 0; nb < T::NB; ++nb)
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
       const int co = co_of(nb, v);
@@ -274,8 +275,8 @@ __global__ __launch_bounds__(256, 2) void conv3x3_igemm_bf16(ConvArgs a) {
     }
   __syncthreads();
   constexpr int PPR = T::BM / V;                     // pieces per channel row
-  constexpr int EPI = 64 * PPR / 256;                // pieces per thread
-  static_assert(64 * PPR % 256 == 0, "whole rounds of pieces");
+  constexpr int EPI = T::BN * PPR / 256;             // pieces per thread
+  static_assert(T::BN * PPR % 256 == 0, "whole rounds of pieces");
   int goff[EPI];                                     // from image n0, -1 outside
 #pragma unroll
   for (int i = 0; i < EPI; ++i) {
@@ -334,6 +335,7 @@ using BTileW16 = BTile<16, 16, 1>;
 using BTileW8 = BTile<8, 8, 4>;
 using BTileW32L = BTile<16, 32, 1>;     // 512 pixels: 64 x 128 per wave
 using BTileW64L = BTile<8, 64, 1>;
+using BTileW32N = BTile<8, 32, 1, 1>;   // 32 output channels (few-channel outputs)
 
 static const char* kBTileNames[] = {
     "sb::conv3x3_igemm_bf16<sb::BTile<8, 32, 1>, %s, %d>",
@@ -341,6 +343,7 @@ static const char* kBTileNames[] = {
     "sb::conv3x3_igemm_bf16<sb::BTile<8, 8, 4>, %s, %d>",
     "sb::conv3x3_igemm_bf16<sb::BTile<16, 32, 1>, %s, %d>",
     "sb::conv3x3_igemm_bf16<sb::BTile<8, 64, 1>, %s, %d>",
+    "sb::conv3x3_igemm_bf16<sb::BTile<8, 32, 1, 1>, %s, %d>",
 };
 
 struct BPlan {
@@ -373,7 +376,8 @@ static BPlan bf16_plan(int N, int Cin, int H, int W, int Cout, bool v8) {
     big = (long)cdiv(W, tw) * cdiv(H, th) * N * cdiv(Cout, 64) >= 512;
   }
   if (!big) {
-    if (W >= 32) { p.tile = 0; th = 8; tw = 32; }
+    if (W >= 32 && Cout <= 32) { p.tile = 5; th = 8; tw = 32; }
+    else if (W >= 32) { p.tile = 0; th = 8; tw = 32; }
     else if (W >= 16) { p.tile = 1; th = 16; tw = 16; }
     else { p.tile = 2; th = 8; tw = 8; imgs = 4; }
   }
@@ -382,7 +386,8 @@ static BPlan bf16_plan(int N, int Cin, int H, int W, int Cout, bool v8) {
   p.tiles_w = cdiv(W, tw);
   p.tiles_h = cdiv(H, th);
   p.grid_x = p.tiles_w * p.tiles_h * cdiv(N, imgs);
-  p.co_tiles = cdiv(Cout, 64);
+  const int bn = p.tile == 5 ? 32 : 64;
+  p.co_tiles = cdiv(Cout, bn);
   p.nchunks = cdiv(Cin, 16);
   const long blocks = (long)p.grid_x * p.co_tiles;
   // About two resident blocks on each of the 256 CUs; at most 8 splits, and
@@ -394,7 +399,7 @@ static BPlan bf16_plan(int N, int Cin, int H, int W, int Cout, bool v8) {
                                  cdiv((int)target, (int)blocks));
   p.cps = cdiv(p.nchunks, splits);
   p.splits = cdiv(p.nchunks, p.cps);
-  p.pack_bytes = (size_t)p.co_tiles * p.nchunks * 9 * 16 * 64 * sizeof(u16);
+  p.pack_bytes = (size_t)p.co_tiles * p.nchunks * 9 * 16 * bn * sizeof(u16);
   p.part_off = round_up(p.pack_bytes, 256);
   p.ws_bytes = p.part_off +
                (p.splits > 1 ? (size_t)p.splits * N * Cout * H * W * sizeof(float) : 0);
@@ -449,7 +454,8 @@ static void bf16_dispatch(int v, const BPlan& p, const ConvArgs& a, hipStream_t 
     case 1: bf16_launch_v<BTileW16, DGRAD>(v, p, a, st); break;
     case 2: bf16_launch_v<BTileW8, DGRAD>(v, p, a, st); break;
     case 3: bf16_launch<BTileW32L, DGRAD, 8>(p, a, st); break;
-    default: bf16_launch<BTileW64L, DGRAD, 8>(p, a, st); break;
+    case 4: bf16_launch<BTileW64L, DGRAD, 8>(p, a, st); break;
+    default: bf16_launch_v<BTileW32N, DGRAD>(v, p, a, st); break;
   }
 }
 
