@@ -431,9 +431,8 @@ static void bf16_launch(const BPlan& p, const ConvArgs& a, hipStream_t st) {
   conv3x3_igemm_bf16<T, DGRAD, V><<<grid, 256, T::LDS_BYTES, st>>>(k);
   if (p.splits > 1) {
     size_t total = (size_t)a.N * a.Cout * a.H * a.W;
-    conv_splitk_reduce<u16><<<(unsigned)((total + 63) / 64), 256, 0, st>>>(
-        a.part, p.splits, total, a.Cout, a.H * a.W, a.bias, a.relu, (const u16*)a.mask,
-        (u16*)a.out);
+    launch_splitk_reduce<u16>(a.part, p.splits, total, a.Cout, a.H * a.W, a.bias, a.relu,
+                              (const u16*)a.mask, (u16*)a.out, st);
   }
 }
 

@@ -131,4 +131,40 @@ __global__ __launch_bounds__(256) void conv_splitk_reduce(
   Elem<E>::store(out, i, v);
 }
 
+// The same for 4 consecutive outputs per thread (total a multiple of 4 and
+// the partials 16-byte aligned): 16-byte partial loads, all splits of a
+// thread's outputs summed in one thread in split order.
+template <class E>
+__global__ __launch_bounds__(256) void conv_splitk_reduce4(
+    const float* __restrict__ part, int splits, size_t total, int Cout, int HWs,
+    const float* __restrict__ bias, int relu, const E* __restrict__ mask,
+    E* __restrict__ out) {
+  const size_t i4 = ((size_t)blockIdx.x * 256 + threadIdx.x) * 4;
+  if (i4 >= total) return;
+  f4 v = split_sum4(part, splits, total, i4);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const size_t i = i4 + j;
+    float r = v[j];
+    if (bias) r += bias[(i / HWs) % Cout];
+    if (relu && !(r > 0.f)) r = 0.f;
+    if (mask && !(Elem<E>::load(mask, i) > 0.f)) r = 0.f;
+    Elem<E>::store(out, i, r);
+  }
+}
+
+// Launches the split reduction of a convolution pass: the 4-wide form when
+// the sizes allow, else one output per lane.
+template <class E>
+inline void launch_splitk_reduce(const float* part, int splits, size_t total, int Cout, int HWs,
+                                 const float* bias, int relu, const E* mask, E* out,
+                                 hipStream_t st) {
+  if (total % 4 == 0 && ((uintptr_t)part & 15) == 0)
+    conv_splitk_reduce4<E><<<(unsigned)((total / 4 + 255) / 256), 256, 0, st>>>(
+        part, splits, total, Cout, HWs, bias, relu, mask, out);
+  else
+    conv_splitk_reduce<E><<<(unsigned)((total + 63) / 64), 256, 0, st>>>(
+        part, splits, total, Cout, HWs, bias, relu, mask, out);
+}
+
 }  // namespace sb

@@ -570,9 +570,8 @@ static void igemm_launch(const IgemmPlan& p, const ConvArgs& a, hipStream_t st) 
     conv3x3_igemm_f32<T, DGRAD, E><<<grid, T::THREADS, T::LDS_BYTES, st>>>(k);
   if (p.splits > 1) {
     size_t total = (size_t)a.N * a.Cout * a.H * a.W;
-    conv_splitk_reduce<E><<<(unsigned)((total + 63) / 64), 256, 0, st>>>(
-        a.part, p.splits, total, a.Cout, a.H * a.W, a.bias, a.relu, (const E*)a.mask,
-        (E*)a.out);
+    launch_splitk_reduce<E>(a.part, p.splits, total, a.Cout, a.H * a.W, a.bias, a.relu,
+                            (const E*)a.mask, (E*)a.out, st);
   }
 }
 

@@ -126,6 +126,37 @@ __global__ __launch_bounds__(256) void splits_reduce(const float* __restrict__ p
   else db[i - wsz] = v;
 }
 
+// The same for 4 consecutive outputs per thread (stride and count multiples
+// of 4): all splits of a thread's outputs summed in one thread, in order.
+__global__ __launch_bounds__(256) void splits_reduce4(const float* __restrict__ part, int splits,
+                                                      size_t stride, size_t count, size_t wsz,
+                                                      float* __restrict__ dw,
+                                                      float* __restrict__ db) {
+  const size_t i4 = ((size_t)blockIdx.x * 256 + threadIdx.x) * 4;
+  if (i4 >= count) return;
+  const f4 v = split_sum4(part, splits, stride, i4);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const size_t i = i4 + j;
+    if (i < wsz) dw[i] = v[j];
+    else db[i - wsz] = v[j];
+  }
+}
+
+// Launches the weight-gradient split reduction: dw (K*C*9) then, when db is
+// wanted, db (K), from partials [splits][K*C*9 + K].
+inline void launch_splits_reduce(const float* part, int splits, int K, int C, float* dw,
+                                 float* db, hipStream_t st) {
+  const size_t wsz = (size_t)K * C * 9, stride = wsz + K;
+  const size_t count = wsz + (db ? K : 0);
+  if (stride % 4 == 0 && count % 4 == 0 && ((uintptr_t)part & 15) == 0)
+    splits_reduce4<<<(unsigned)((count / 4 + 255) / 256), 256, 0, st>>>(part, splits, stride,
+                                                                       count, wsz, dw, db);
+  else
+    splits_reduce<<<(unsigned)((count + 63) / 64), 256, 0, st>>>(part, splits, stride, count,
+                                                                wsz, dw, db);
+}
+
 // ----------------------------------------------------------------- generic --
 template <int TH_, int TW_, int IMGS_, int NCB_>
 struct WgTile {
@@ -840,12 +871,7 @@ static void wg_launch(const WgPlan& p, const WgArgs& a, hipStream_t st) {
     conv3x3_wgrad_small_f32<T, E><<<grid, 256, T::LDS_BYTES, st>>>(a);
   else
     conv3x3_wgrad_f32<T, E><<<grid, 256, T::LDS_BYTES, st>>>(a);
-  if (p.splits > 1) {
-    const size_t wsz = (size_t)a.K * a.C * 9;
-    const size_t count = wsz + (a.db ? a.K : 0);
-    splits_reduce<<<(unsigned)((count + 63) / 64), 256, 0, st>>>(a.part, p.splits, wsz + a.K,
-                                                                count, wsz, a.dw, a.db);
-  }
+  if (p.splits > 1) launch_splits_reduce(a.part, p.splits, a.K, a.C, a.dw, a.db, st);
 }
 
 }  // namespace sb
@@ -894,12 +920,7 @@ static void wg_launch_bf16(const sb::WgPlan& p, const sb::WgArgs& a, hipStream_t
   }
   dim3 grid(p.k_tiles * p.c_tiles, 1, p.splits);
   sb::conv3x3_wgrad_bf16<T, V><<<grid, 256, T::LDS_BYTES, st>>>(a);
-  if (p.splits > 1) {
-    const size_t wsz = (size_t)a.K * a.C * 9;
-    const size_t count = wsz + (a.db ? a.K : 0);
-    sb::splits_reduce<<<(unsigned)((count + 63) / 64), 256, 0, st>>>(
-        a.part, p.splits, wsz + a.K, count, wsz, a.dw, a.db);
-  }
+  if (p.splits > 1) sb::launch_splits_reduce(a.part, p.splits, a.K, a.C, a.dw, a.db, st);
 }
 
 template <class T>

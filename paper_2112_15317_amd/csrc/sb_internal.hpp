@@ -184,6 +184,25 @@ struct SplitSum {
   }
 };
 
+// Sum over the splits of 4 consecutive partials (16-byte aligned, i4 a
+// multiple of 4): part[s*stride + i4 .. +3] for s = 0, 1, ... in that order
+// (the same order for every output, so the result is deterministic), with
+// four splits' loads in flight at a time.
+__device__ __forceinline__ f4 split_sum4(const float* __restrict__ part, int splits,
+                                         size_t stride, size_t i4) {
+  f4 v = f4{0.f, 0.f, 0.f, 0.f};
+  int s = 0;
+  for (; s + 4 <= splits; s += 4) {
+    const f4 a = *reinterpret_cast<const f4*>(part + (size_t)s * stride + i4);
+    const f4 b = *reinterpret_cast<const f4*>(part + (size_t)(s + 1) * stride + i4);
+    const f4 c = *reinterpret_cast<const f4*>(part + (size_t)(s + 2) * stride + i4);
+    const f4 d = *reinterpret_cast<const f4*>(part + (size_t)(s + 3) * stride + i4);
+    v += a; v += b; v += c; v += d;
+  }
+  for (; s < splits; ++s) v += *reinterpret_cast<const f4*>(part + (size_t)s * stride + i4);
+  return v;
+}
+
 }  // namespace sb
 
 // Host-side helpers shared by the entry points.
