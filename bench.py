@@ -353,6 +353,8 @@ def kernel_name(key, call_args, dtype):
     if kind.startswith("fc_"):
         d = call_args[0]
         return "sb_fc_shard_%s m=%d k_in=%d n_shard=%d" % (kind[3:], d.m, d.k_in, d.n_shard)
+    if kind == "pack":
+        return "sb::filter_pack_many"
     return "sb::relu_maxpool_%s_kernel<%s, 2>" % (
         kind.split("_")[1], "float" if dtype == "f32" else "unsigned short")
 
@@ -365,6 +367,8 @@ def call_work(wl, key, args):
     if kind.startswith("fc_"):
         return fc_flops(args[0], kind, kind == "fc_fwd" or args[5] is not None), "flop"
     esize = 4 if wl.dtype == "f32" else 2
+    if kind == "pack":             # every layer's filters read, twice packed written
+        return sum(3 * L.k * L.c * 9 * esize for L in wl.layers), "bytes"
     return pool_bytes(wl.layers[i], args[0], esize), "bytes"
 
 

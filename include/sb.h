@@ -60,6 +60,8 @@ typedef enum { SB_F32 = 0, SB_BF16 = 1 } sb_dtype;
 
 /* flags */
 #define SB_FUSE_RELU 1u       /* apply ReLU to the output (conv fwd, FC fwd) */
+#define SB_PACKED_FILTERS 2u  /* conv fwd / data gradient: `w` holds filters
+                                 packed by sb_conv3x3_pack_filters */
 
 /* Returns a static string naming the status. */
 const char *sb_status_string(sb_status s);
@@ -80,19 +82,58 @@ typedef struct {
     int n, c, h, w;       /* batch, input channels, height, width (all > 0) */
     int k;                /* output channels (> 0)                          */
     int dtype;            /* sb_dtype                                       */
-    unsigned flags;       /* SB_FUSE_RELU (forward only)                    */
+    unsigned flags;       /* SB_FUSE_RELU (forward only), SB_PACKED_FILTERS
+                             (forward and data gradient)                    */
 } sb_conv3x3_desc;
 
 enum { SB_PASS_FWD = 0, SB_PASS_BWD_DATA = 1, SB_PASS_BWD_WEIGHT = 2 };
 
 /* Workspace bytes that `pass` needs for `desc` (0 is a valid answer, and a
- * NULL workspace is then accepted).  Returns (size_t)-1 for an invalid or
- * unsupported descriptor. */
+ * NULL workspace is then accepted).  With SB_PACKED_FILTERS set the answer
+ * leaves out the room the call would otherwise use to pack the filters.
+ * Returns (size_t)-1 for an invalid or unsupported descriptor. */
 size_t sb_conv3x3_workspace_bytes(const sb_conv3x3_desc *desc, int pass);
+
+/* Packed filters.  The forward and data-gradient kernels read the filters
+ * rearranged into the order they stage them (slices per output-channel tile
+ * and input-channel chunk; for the data gradient the filters transposed and
+ * rotated by 180 degrees).  Every such call packs them first, into its
+ * workspace.  A caller that runs several calls with the same filters (a
+ * training step: forward, then data gradient), or wants the packing off the
+ * critical path (on another stream, ahead of the call), packs them once with
+ * sb_conv3x3_pack_filters and sets SB_PACKED_FILTERS on the calls, which
+ * then take the packed buffer as `w`.
+ *
+ * sb_conv3x3_packed_bytes: bytes of the packed filters of `pass`
+ * (SB_PASS_FWD or SB_PASS_BWD_DATA) for `desc`; 0 for an invalid descriptor
+ * or pass.  The flags of desc other than the dtype's are ignored.
+ *
+ * sb_conv3x3_pack_filters: packs w [k][c][3][3] (desc->dtype, device) into
+ * `packed` (device, packed_bytes >= sb_conv3x3_packed_bytes, not
+ * overlapping w), on `stream`.  The result serves every call of that pass
+ * on a descriptor with the same n, c, h, w, k and dtype, until w changes;
+ * the caller orders it before those calls (same stream, or an event).
+ * SB_ERR_INVALID_ARG for a bad descriptor, pass, pointer or size. */
+size_t sb_conv3x3_packed_bytes(const sb_conv3x3_desc *desc, int pass);
+sb_status sb_conv3x3_pack_filters(const sb_conv3x3_desc *desc, int pass,
+                                  const void *w, void *packed,
+                                  size_t packed_bytes, void *stream);
+
+/* The packing of `count` (1..64) filter tensors in one launch, each as
+ * sb_conv3x3_pack_filters(&descs[i], passes[i], w[i], packed[i],
+ * packed_bytes[i]) would do it; all descriptors of one dtype, the packed
+ * buffers disjoint.  A packing moves little data, so packing every layer of
+ * a network this way costs about one launch instead of one per layer and
+ * pass.  The host arrays are read before the call returns. */
+sb_status sb_conv3x3_pack_filters_many(int count, const sb_conv3x3_desc *descs,
+                                       const int *passes, const void *const *w,
+                                       void *const *packed,
+                                       const size_t *packed_bytes, void *stream);
 
 /* Forward:  y[n,k,h,w] = bias[k] + sum_{c,r,s} x[n,c,h+r-1,w+s-1] * w[k,c,r,s]
  * (x = 0 outside the image), then max(y, 0) when SB_FUSE_RELU is set.
- * bias may be NULL (zero). */
+ * bias may be NULL (zero).  With SB_PACKED_FILTERS, w is the forward
+ * packing of the filters (sb_conv3x3_pack_filters, SB_PASS_FWD). */
 sb_status sb_conv3x3_fwd(const sb_conv3x3_desc *desc, const void *x,
                          const void *w, const float *bias, void *y,
                          void *workspace, size_t workspace_bytes, void *stream);
@@ -101,7 +142,8 @@ sb_status sb_conv3x3_fwd(const sb_conv3x3_desc *desc, const void *x,
  *   dx[n,c,i,j] = sum_{k,r,s} dy[n,k,i-r+1,j-s+1] * w[k,c,r,s]
  * over in-image output positions.  When relu_mask_src is non-NULL (shape of
  * dx: the activation of the layer below, whose ReLU this gradient crosses),
- * dx is set to 0 wherever relu_mask_src <= 0.  desc->flags must be 0. */
+ * dx is set to 0 wherever relu_mask_src <= 0.  desc->flags must be 0 or
+ * SB_PACKED_FILTERS (w then the data-gradient packing, SB_PASS_BWD_DATA). */
 sb_status sb_conv3x3_bwd_data(const sb_conv3x3_desc *desc, const void *dy,
                               const void *w, const void *relu_mask_src,
                               void *dx, void *workspace,

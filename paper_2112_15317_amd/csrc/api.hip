@@ -1,13 +1,20 @@
 // api.hip -- the convolution entry points of libsb: argument validation,
 // workspace sizing and dispatch to the kernels.  Nothing is enqueued unless
 // every check passes.
-#include "sb_internal.hpp"
+#include "conv_common.hpp"
 
 namespace sbh {
-size_t conv_igemm_ws(int dtype, int N, int Cin, int H, int W, int Cout);
+int conv_igemm_pack_task(bool dgrad, int dtype, int N, int Cin, int H, int W, int Cout,
+                         const void* wt, void* packed, sb::PackTask* t);
+void conv_pack_many(int dtype, const sb::PackBatch& b, hipStream_t st);
+size_t conv_igemm_ws(int dtype, int N, int Cin, int H, int W, int Cout, bool prepacked);
+size_t conv_igemm_pack_bytes(int dtype, int N, int Cin, int H, int W, int Cout);
+void conv_igemm_pack(bool dgrad, int dtype, int N, int Cin, int H, int W, int Cout,
+                     const void* wt, void* packed, hipStream_t st);
 sb_status conv_igemm(bool dgrad, int dtype, int N, int Cin, int H, int W, int Cout,
                      const void* in, const void* wt, const float* bias, const void* mask,
-                     void* out, void* ws, size_t ws_bytes, int relu, hipStream_t st);
+                     void* out, void* ws, size_t ws_bytes, int relu, bool prepacked,
+                     hipStream_t st);
 size_t conv_wgrad_ws(int dtype, int N, int C, int H, int W, int K);
 int conv_igemm_describe(bool dgrad, int dtype, int N, int Cin, int H, int W, int Cout, char* buf,
                         size_t len);
@@ -33,8 +40,9 @@ static sb_status conv_check(const sb_conv3x3_desc* d, int pass) {
   if (!d) return SB_ERR_INVALID_ARG;
   if (d->n <= 0 || d->c <= 0 || d->h <= 0 || d->w <= 0 || d->k <= 0) return SB_ERR_INVALID_ARG;
   if (d->dtype != SB_F32 && d->dtype != SB_BF16) return SB_ERR_INVALID_ARG;
-  if (d->flags & ~SB_FUSE_RELU) return SB_ERR_INVALID_ARG;
-  if (pass != SB_PASS_FWD && d->flags) return SB_ERR_INVALID_ARG;
+  if (d->flags & ~(SB_FUSE_RELU | SB_PACKED_FILTERS)) return SB_ERR_INVALID_ARG;
+  if (pass != SB_PASS_FWD && (d->flags & SB_FUSE_RELU)) return SB_ERR_INVALID_ARG;
+  if (pass == SB_PASS_BWD_WEIGHT && d->flags) return SB_ERR_INVALID_ARG;
   // Kernels index weights and activations with 32-bit ints.
   if ((int64_t)d->k * d->c * 9 >= (1ll << 31)) return SB_ERR_UNSUPPORTED;
   if ((int64_t)d->n * d->c * d->h * d->w >= (1ll << 31)) return SB_ERR_UNSUPPORTED;
@@ -45,15 +53,91 @@ static sb_status conv_check(const sb_conv3x3_desc* d, int pass) {
 extern "C" size_t sb_conv3x3_workspace_bytes(const sb_conv3x3_desc* d, int pass) {
   if (pass < SB_PASS_FWD || pass > SB_PASS_BWD_WEIGHT) return (size_t)-1;
   if (conv_check(d, pass) != SB_OK) return (size_t)-1;
+  const bool pk = (d->flags & SB_PACKED_FILTERS) != 0;
   switch (pass) {
-    case SB_PASS_FWD: return sbh::conv_igemm_ws(d->dtype, d->n, d->c, d->h, d->w, d->k);
-    case SB_PASS_BWD_DATA: return sbh::conv_igemm_ws(d->dtype, d->n, d->k, d->h, d->w, d->c);
+    case SB_PASS_FWD: return sbh::conv_igemm_ws(d->dtype, d->n, d->c, d->h, d->w, d->k, pk);
+    case SB_PASS_BWD_DATA: return sbh::conv_igemm_ws(d->dtype, d->n, d->k, d->h, d->w, d->c, pk);
     default: return sbh::conv_wgrad_ws(d->dtype, d->n, d->c, d->h, d->w, d->k);
   }
 }
 
+// Packed-filter bytes of a forward or data-gradient pass (0: invalid).
+static size_t packed_bytes(const sb_conv3x3_desc* d, int pass) {
+  if (pass == SB_PASS_FWD) return sbh::conv_igemm_pack_bytes(d->dtype, d->n, d->c, d->h, d->w, d->k);
+  return sbh::conv_igemm_pack_bytes(d->dtype, d->n, d->k, d->h, d->w, d->c);
+}
+
+extern "C" size_t sb_conv3x3_packed_bytes(const sb_conv3x3_desc* d, int pass) {
+  if (pass != SB_PASS_FWD && pass != SB_PASS_BWD_DATA) return 0;
+  if (!d) return 0;
+  sb_conv3x3_desc q = *d;
+  q.flags = 0;
+  if (conv_check(&q, pass) != SB_OK) return 0;
+  return packed_bytes(&q, pass);
+}
+
+extern "C" sb_status sb_conv3x3_pack_filters(const sb_conv3x3_desc* d, int pass, const void* w,
+                                             void* packed, size_t packed_bytes_, void* stream) {
+  if (pass != SB_PASS_FWD && pass != SB_PASS_BWD_DATA) return SB_ERR_INVALID_ARG;
+  if (!d) return SB_ERR_INVALID_ARG;
+  sb_conv3x3_desc q = *d;
+  q.flags = 0;
+  sb_status s = conv_check(&q, pass);
+  if (s != SB_OK) return s;
+  if (!w || !packed) return SB_ERR_INVALID_ARG;
+  const size_t need = packed_bytes(&q, pass);
+  const size_t wb = (size_t)q.k * q.c * 9 * sbh::dsize(q.dtype);
+  if (packed_bytes_ < need || sbh::overlaps(w, wb, packed, need)) return SB_ERR_INVALID_ARG;
+  if (pass == SB_PASS_FWD)
+    sbh::conv_igemm_pack(false, q.dtype, q.n, q.c, q.h, q.w, q.k, w, packed,
+                         sbh::stream_of(stream));
+  else
+    sbh::conv_igemm_pack(true, q.dtype, q.n, q.k, q.h, q.w, q.c, w, packed,
+                         sbh::stream_of(stream));
+  return sbh::launch_status();
+}
+
 static size_t act_bytes(const sb_conv3x3_desc* d, int ch) {
   return (size_t)d->n * ch * d->h * d->w * sbh::dsize(d->dtype);
+}
+
+extern "C" sb_status sb_conv3x3_pack_filters_many(int count, const sb_conv3x3_desc* descs,
+                                                  const int* passes, const void* const* w,
+                                                  void* const* packed,
+                                                  const size_t* packed_bytes_, void* stream) {
+  if (count <= 0 || count > sb::kMaxPackTasks || !descs || !passes || !w || !packed ||
+      !packed_bytes_)
+    return SB_ERR_INVALID_ARG;
+  sb::PackBatch b{};
+  b.ntasks = count;
+  b.block0[0] = 0;
+  for (int i = 0; i < count; ++i) {
+    const int pass = passes[i];
+    if (pass != SB_PASS_FWD && pass != SB_PASS_BWD_DATA) return SB_ERR_INVALID_ARG;
+    sb_conv3x3_desc q = descs[i];
+    q.flags = 0;
+    sb_status s = conv_check(&q, pass);
+    if (s != SB_OK) return s;
+    if (q.dtype != descs[0].dtype) return SB_ERR_INVALID_ARG;
+    if (!w[i] || !packed[i]) return SB_ERR_INVALID_ARG;
+    const size_t need = packed_bytes(&q, pass);
+    const size_t wb = (size_t)q.k * q.c * 9 * sbh::dsize(q.dtype);
+    if (packed_bytes_[i] < need || sbh::overlaps(w[i], wb, packed[i], need))
+      return SB_ERR_INVALID_ARG;
+    // Packed outputs must not overlap one another.
+    for (int j = 0; j < i; ++j)
+      if (sbh::overlaps(packed[j], packed_bytes_[j], packed[i], need)) return SB_ERR_INVALID_ARG;
+    const int slices =
+        pass == SB_PASS_FWD
+            ? sbh::conv_igemm_pack_task(false, q.dtype, q.n, q.c, q.h, q.w, q.k, w[i], packed[i],
+                                        &b.t[i])
+            : sbh::conv_igemm_pack_task(true, q.dtype, q.n, q.k, q.h, q.w, q.c, w[i], packed[i],
+                                        &b.t[i]);
+    if ((int64_t)b.block0[i] + slices >= (1ll << 31)) return SB_ERR_UNSUPPORTED;
+    b.block0[i + 1] = b.block0[i] + slices;
+  }
+  sbh::conv_pack_many(descs[0].dtype, b, sbh::stream_of(stream));
+  return sbh::launch_status();
 }
 
 extern "C" sb_status sb_conv3x3_fwd(const sb_conv3x3_desc* d, const void* x, const void* w,
@@ -62,19 +146,20 @@ extern "C" sb_status sb_conv3x3_fwd(const sb_conv3x3_desc* d, const void* x, con
   sb_status s = conv_check(d, SB_PASS_FWD);
   if (s != SB_OK) return s;
   if (!x || !w || !y) return SB_ERR_INVALID_ARG;
+  const bool pk = (d->flags & SB_PACKED_FILTERS) != 0;
   size_t yb = act_bytes(d, d->k), xb = act_bytes(d, d->c);
-  size_t wb = (size_t)d->k * d->c * 9 * sbh::dsize(d->dtype);
+  size_t wb = pk ? packed_bytes(d, SB_PASS_FWD) : (size_t)d->k * d->c * 9 * sbh::dsize(d->dtype);
   if (sbh::overlaps(y, yb, x, xb) || sbh::overlaps(y, yb, w, wb) ||
       sbh::overlaps(y, yb, bias, bias ? d->k * sizeof(float) : 0))
     return SB_ERR_INVALID_ARG;
-  size_t need = sbh::conv_igemm_ws(d->dtype, d->n, d->c, d->h, d->w, d->k);
+  size_t need = sbh::conv_igemm_ws(d->dtype, d->n, d->c, d->h, d->w, d->k, pk);
   if (need && (!ws || ws_bytes < need)) return SB_ERR_WORKSPACE;
   if (need && (sbh::overlaps(ws, need, x, xb) || sbh::overlaps(ws, need, y, yb) ||
                sbh::overlaps(ws, need, w, wb) ||
                sbh::overlaps(ws, need, bias, bias ? d->k * sizeof(float) : 0)))
     return SB_ERR_INVALID_ARG;
   return sbh::conv_igemm(false, d->dtype, d->n, d->c, d->h, d->w, d->k, x, w, bias, nullptr, y,
-                         ws, ws_bytes, (d->flags & SB_FUSE_RELU) ? 1 : 0,
+                         ws, ws_bytes, (d->flags & SB_FUSE_RELU) ? 1 : 0, pk,
                          sbh::stream_of(stream));
 }
 
@@ -84,19 +169,21 @@ extern "C" sb_status sb_conv3x3_bwd_data(const sb_conv3x3_desc* d, const void* d
   sb_status s = conv_check(d, SB_PASS_BWD_DATA);
   if (s != SB_OK) return s;
   if (!dy || !w || !dx) return SB_ERR_INVALID_ARG;
+  const bool pk = (d->flags & SB_PACKED_FILTERS) != 0;
   size_t dxb = act_bytes(d, d->c), dyb = act_bytes(d, d->k);
-  size_t wb = (size_t)d->k * d->c * 9 * sbh::dsize(d->dtype);
+  size_t wb =
+      pk ? packed_bytes(d, SB_PASS_BWD_DATA) : (size_t)d->k * d->c * 9 * sbh::dsize(d->dtype);
   if (sbh::overlaps(dx, dxb, dy, dyb) || sbh::overlaps(dx, dxb, w, wb) ||
       sbh::overlaps(dx, dxb, mask, mask ? dxb : 0))
     return SB_ERR_INVALID_ARG;
-  size_t need = sbh::conv_igemm_ws(d->dtype, d->n, d->k, d->h, d->w, d->c);
+  size_t need = sbh::conv_igemm_ws(d->dtype, d->n, d->k, d->h, d->w, d->c, pk);
   if (need && (!ws || ws_bytes < need)) return SB_ERR_WORKSPACE;
   if (need && (sbh::overlaps(ws, need, dy, dyb) || sbh::overlaps(ws, need, dx, dxb) ||
                sbh::overlaps(ws, need, w, wb) ||
                sbh::overlaps(ws, need, mask, mask ? dxb : 0)))
     return SB_ERR_INVALID_ARG;
   return sbh::conv_igemm(true, d->dtype, d->n, d->k, d->h, d->w, d->c, dy, w, nullptr, mask, dx,
-                         ws, ws_bytes, 0, sbh::stream_of(stream));
+                         ws, ws_bytes, 0, pk, sbh::stream_of(stream));
 }
 
 extern "C" sb_status sb_conv3x3_bwd_weight(const sb_conv3x3_desc* d, const void* x, const void* dy,

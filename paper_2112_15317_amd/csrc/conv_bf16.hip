@@ -367,7 +367,9 @@ static BPlan bf16_plan(int N, int Cin, int H, int W, int Cout, bool v8) {
   // 512-pixel tiles (each wave 64 channels x 128 pixels: a quarter fewer LDS
   // operand bytes per MFMA than 64 x 64), 16 x 32 or 8 x 64, whichever pads
   // the image less, when they still fill the chip without a split.
-  bool big = W >= 32 && v8 && Cin >= 256;
+  // (Never for outputs of 32 channels or fewer: their 32-channel tile's
+  // filter layout must not depend on the tensors' alignment.)
+  bool big = W >= 32 && v8 && Cin >= 256 && Cout > 32;
   if (big) {
     const long a16 = (long)round_up(H, 16) * round_up(W, 32);
     const long a8 = (long)round_up(H, 8) * round_up(W, 64);
@@ -415,16 +417,30 @@ static int bf16_vec(int W, const void* in, const void* out, const void* mask) {
   return 1;
 }
 
+// Packs the filters of a layer for the bf16 kernels: [tap][ci/8][co][ci%8]
+// slices of 16 input x BN output channels (BN = 32 for the 32-channel tile).
+template <bool DGRAD>
+static void bf16_pack(const BPlan& p, const void* wt, void* packed, int Cin, int Cout,
+                      hipStream_t st) {
+  if (p.tile == 5)
+    filter_pack<DGRAD, 16, 32, u16, PackCI8><<<p.co_tiles * p.nchunks, 256, 0, st>>>(
+        (const u16*)wt, (u16*)packed, Cin, Cout);
+  else
+    filter_pack<DGRAD, 16, 64, u16, PackCI8><<<p.co_tiles * p.nchunks, 256, 0, st>>>(
+        (const u16*)wt, (u16*)packed, Cin, Cout);
+}
+
+// pack: the call packs the filters itself (into the workspace); otherwise
+// a.wpk already holds them.
 template <class T, bool DGRAD, int V>
-static void bf16_launch(const BPlan& p, const ConvArgs& a, hipStream_t st) {
+static void bf16_launch(const BPlan& p, const ConvArgs& a, bool pack, hipStream_t st) {
   static bool attr_set = false;
   if (!attr_set) {
     (void)hipFuncSetAttribute((const void*)conv3x3_igemm_bf16<T, DGRAD, V>,
                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)T::LDS_BYTES);
     attr_set = true;
   }
-  filter_pack<DGRAD, T::CK, T::BN, u16, PackCI8><<<p.co_tiles * p.nchunks, 256, 0, st>>>(
-      (const u16*)a.wt, (u16*)a.wpk, a.Cin, a.Cout);
+  if (pack) bf16_pack<DGRAD>(p, a.wt, (void*)a.wpk, a.Cin, a.Cout, st);
   dim3 grid(p.grid_x, p.co_tiles, p.splits);
   ConvArgs k = a;
   if (p.splits > 1) { k.bias = nullptr; k.mask = nullptr; k.relu = 0; }
@@ -437,24 +453,24 @@ static void bf16_launch(const BPlan& p, const ConvArgs& a, hipStream_t st) {
 }
 
 template <class T, bool DGRAD>
-static void bf16_launch_v(int v, const BPlan& p, const ConvArgs& a, hipStream_t st) {
+static void bf16_launch_v(int v, const BPlan& p, const ConvArgs& a, bool pack, hipStream_t st) {
   switch (v) {
-    case 8: bf16_launch<T, DGRAD, 8>(p, a, st); break;
-    case 4: bf16_launch<T, DGRAD, 4>(p, a, st); break;
-    case 2: bf16_launch<T, DGRAD, 2>(p, a, st); break;
-    default: bf16_launch<T, DGRAD, 1>(p, a, st); break;
+    case 8: bf16_launch<T, DGRAD, 8>(p, a, pack, st); break;
+    case 4: bf16_launch<T, DGRAD, 4>(p, a, pack, st); break;
+    case 2: bf16_launch<T, DGRAD, 2>(p, a, pack, st); break;
+    default: bf16_launch<T, DGRAD, 1>(p, a, pack, st); break;
   }
 }
 
 template <bool DGRAD>
-static void bf16_dispatch(int v, const BPlan& p, const ConvArgs& a, hipStream_t st) {
+static void bf16_dispatch(int v, const BPlan& p, const ConvArgs& a, bool pack, hipStream_t st) {
   switch (p.tile) {
-    case 0: bf16_launch_v<BTileW32, DGRAD>(v, p, a, st); break;
-    case 1: bf16_launch_v<BTileW16, DGRAD>(v, p, a, st); break;
-    case 2: bf16_launch_v<BTileW8, DGRAD>(v, p, a, st); break;
-    case 3: bf16_launch<BTileW32L, DGRAD, 8>(p, a, st); break;
-    case 4: bf16_launch<BTileW64L, DGRAD, 8>(p, a, st); break;
-    default: bf16_launch_v<BTileW32N, DGRAD>(v, p, a, st); break;
+    case 0: bf16_launch_v<BTileW32, DGRAD>(v, p, a, pack, st); break;
+    case 1: bf16_launch_v<BTileW16, DGRAD>(v, p, a, pack, st); break;
+    case 2: bf16_launch_v<BTileW8, DGRAD>(v, p, a, pack, st); break;
+    case 3: bf16_launch<BTileW32L, DGRAD, 8>(p, a, pack, st); break;
+    case 4: bf16_launch<BTileW64L, DGRAD, 8>(p, a, pack, st); break;
+    default: bf16_launch_v<BTileW32N, DGRAD>(v, p, a, pack, st); break;
   }
 }
 
@@ -463,11 +479,35 @@ static void bf16_dispatch(int v, const BPlan& p, const ConvArgs& a, hipStream_t 
 namespace sbh {
 
 // Workspace of the bf16 MFMA path (either staging width), or 0 when it does
-// not take the shape.
-size_t conv_bf16_ws(int N, int Cin, int H, int W, int Cout) {
+// not take the shape.  prepacked: the filters come packed, the workspace
+// holds only the split partials.
+size_t conv_bf16_ws(int N, int Cin, int H, int W, int Cout, bool prepacked) {
   sb::BPlan p = sb::bf16_plan(N, Cin, H, W, Cout, true);
   sb::BPlan q = sb::bf16_plan(N, Cin, H, W, Cout, false);
-  return p.ok ? std::max(p.ws_bytes, q.ws_bytes) : 0;
+  if (!p.ok) return 0;
+  if (prepacked) return std::max(p.ws_bytes - p.part_off, q.ws_bytes - q.part_off);
+  return std::max(p.ws_bytes, q.ws_bytes);
+}
+
+// Bytes of the packed filters (the same for either staging width).
+size_t conv_bf16_pack_bytes(int N, int Cin, int H, int W, int Cout) {
+  return sb::bf16_plan(N, Cin, H, W, Cout, false).pack_bytes;
+}
+
+// Slice geometry of the packed filters: CK input x BN output channels per
+// slice (PackCI8), `slices` slices.
+void conv_bf16_pack_geom(int N, int Cin, int H, int W, int Cout, int* ck, int* bn, int* slices) {
+  sb::BPlan p = sb::bf16_plan(N, Cin, H, W, Cout, false);
+  *ck = 16;
+  *bn = p.tile == 5 ? 32 : 64;
+  *slices = p.co_tiles * p.nchunks;
+}
+
+void conv_bf16_pack(bool dgrad, int N, int Cin, int H, int W, int Cout, const void* wt,
+                    void* packed, hipStream_t st) {
+  sb::BPlan p = sb::bf16_plan(N, Cin, H, W, Cout, false);
+  if (dgrad) sb::bf16_pack<true>(p, wt, packed, Cin, Cout, st);
+  else sb::bf16_pack<false>(p, wt, packed, Cin, Cout, st);
 }
 
 bool conv_bf16_takes(int N, int Cin, int H, int W, int Cout) {
@@ -485,7 +525,7 @@ int conv_bf16_describe(bool dgrad, int N, int Cin, int H, int W, int Cout, char*
 
 sb_status conv_bf16(bool dgrad, int N, int Cin, int H, int W, int Cout, const void* in,
                     const void* wt, const float* bias, const void* mask, void* out, void* ws,
-                    size_t ws_bytes, int relu, hipStream_t st) {
+                    size_t ws_bytes, int relu, bool prepacked, hipStream_t st) {
   const int v = sb::bf16_vec(W, in, out, mask);
   sb::BPlan p = sb::bf16_plan(N, Cin, H, W, Cout, v == 8);
   if (!p.ok) return SB_ERR_UNSUPPORTED;
@@ -494,16 +534,18 @@ sb_status conv_bf16(bool dgrad, int N, int Cin, int H, int W, int Cout, const vo
   if ((int64_t)std::min(p.imgs, N) * std::max(Cin, Cout) * H * W * 2 >= (1ll << 31) ||
       (int64_t)p.pack_bytes >= (1ll << 31))
     return SB_ERR_UNSUPPORTED;
-  if (ws == nullptr || ws_bytes < p.ws_bytes) return SB_ERR_WORKSPACE;
+  const size_t part_off = prepacked ? 0 : p.part_off;
+  const size_t need = prepacked ? p.ws_bytes - p.part_off : p.ws_bytes;
+  if (need && (ws == nullptr || ws_bytes < need)) return SB_ERR_WORKSPACE;
   sb::ConvArgs a{};
   a.in = in; a.wt = wt; a.bias = bias; a.mask = mask; a.out = out;
-  a.wpk = ws;
-  a.part = p.splits > 1 ? (float*)((char*)ws + p.part_off) : nullptr;
+  a.wpk = prepacked ? wt : ws;
+  a.part = p.splits > 1 ? (float*)((char*)ws + part_off) : nullptr;
   a.N = N; a.Cin = Cin; a.H = H; a.W = W; a.Cout = Cout;
   a.tiles_w = p.tiles_w; a.tiles_h = p.tiles_h;
   a.nchunks = p.nchunks; a.chunks_per_split = p.cps; a.splits = p.splits; a.relu = relu;
-  if (dgrad) sb::bf16_dispatch<true>(v, p, a, st);
-  else sb::bf16_dispatch<false>(v, p, a, st);
+  if (dgrad) sb::bf16_dispatch<true>(v, p, a, !prepacked, st);
+  else sb::bf16_dispatch<false>(v, p, a, !prepacked, st);
   return launch_status();
 }
 

@@ -47,9 +47,16 @@ __device__ __forceinline__ float conv_epilogue(const ConvArgs& a, float v, int c
 // consecutive input channels per output channel, the operand order of the
 // bf16 kernels, whose lanes read 8 consecutive channels (16 bytes).
 constexpr int PackCO = 0, PackCI8 = 1;
-template <bool DGRAD, int CK, int BN, class E, int LAYOUT = PackCO>
-__global__ __launch_bounds__(256) void filter_pack(const E* __restrict__ w, E* __restrict__ out,
-                                                   int Cin, int Cout) {
+
+// Packs slice `slice` of one layer's filters, permuting through `slice_lds`
+// (at least slice_lds_bytes<CK, BN, E, LAYOUT>() bytes).
+template <int CK, int BN, class E, int LAYOUT>
+__host__ __device__ constexpr int slice_lds_elems() {
+  return 9 * CK * BN / (LAYOUT == PackCI8 ? 8 : BN) * ((LAYOUT == PackCI8 ? 8 : BN) + 1);
+}
+template <bool DGRAD, int CK, int BN, class E, int LAYOUT>
+__device__ __forceinline__ void pack_slice(const E* __restrict__ w, E* __restrict__ out, int Cin,
+                                           int Cout, int slice, E* slice_lds) {
   // Cin, Cout: this convolution's input and output channels (for the data
   // gradient: the forward layer's output and input channels).
   constexpr int SL = 9 * CK * BN;
@@ -58,11 +65,9 @@ __global__ __launch_bounds__(256) void filter_pack(const E* __restrict__ w, E* _
   // Padded LDS rows (one extra element) keep the permuting writes spread
   // over the banks.
   constexpr int ROW = CI8 ? 8 : BN, RS = ROW + 1;
-  __shared__ E slice_lds[SL / ROW * RS];
   constexpr int PT = (SL + 255) / 256;
   const int nchunks = cdiv(Cin, CK);
-  const int slice = blockIdx.x;                       // co tile * nchunks + chunk
-  const int ct = slice / nchunks, kc = slice - ct * nchunks;
+  const int ct = slice / nchunks, kc = slice - ct * nchunks;   // co tile, chunk
   // All loads first (PT per thread in flight), then the LDS permutation.
   E v[PT];
   int pos[PT];
@@ -97,6 +102,71 @@ __global__ __launch_bounds__(256) void filter_pack(const E* __restrict__ w, E* _
   __syncthreads();
   E* dst = out + (size_t)slice * SL;
   for (int e = threadIdx.x; e < SL; e += 256) dst[e] = slice_lds[(e / ROW) * RS + e % ROW];
+}
+
+// One block per slice of one layer.
+template <bool DGRAD, int CK, int BN, class E, int LAYOUT = PackCO>
+__global__ __launch_bounds__(256) void filter_pack(const E* __restrict__ w, E* __restrict__ out,
+                                                   int Cin, int Cout) {
+  __shared__ E slice_lds[slice_lds_elems<CK, BN, E, LAYOUT>()];
+  pack_slice<DGRAD, CK, BN, E, LAYOUT>(w, out, Cin, Cout, blockIdx.x, slice_lds);
+}
+
+// Several layers' (and passes') filters in one launch: a pack task per
+// (filters, pass); the blocks of task t are block0[t] .. block0[t+1]-1, one
+// per slice.  `kind` names the slice geometry (pack_kind()).  One launch
+// instead of one per task: a pack moves little data, so each separate
+// launch would cost mostly its own ramp-up and drain.
+constexpr int kMaxPackTasks = 64;
+struct PackTask {
+  const void* w;
+  void* out;
+  int Cin, Cout;   // of the convolution (for the data gradient, the transposed one)
+  int kind;
+};
+struct PackBatch {
+  PackTask t[kMaxPackTasks];
+  int block0[kMaxPackTasks + 1];
+  int ntasks;
+};
+// kind = DGRAD | CI8 << 1 | ck_code << 2 | bn_code << 4, with ck_code 0, 1, 2
+// for CK = 4, 8, 16 and bn_code 0, 1, 2 for BN = 16, 32, 64.
+__host__ __device__ constexpr int pack_kind(bool dgrad, int layout, int ck, int bn) {
+  return (dgrad ? 1 : 0) | (layout == PackCI8 ? 2 : 0) | ((ck == 4 ? 0 : ck == 8 ? 1 : 2) << 2) |
+         ((bn == 16 ? 0 : bn == 32 ? 1 : 2) << 4);
+}
+
+template <class E>
+__global__ __launch_bounds__(256) void filter_pack_many(PackBatch b) {
+  constexpr int LDS = slice_lds_elems<16, 64, E, PackCI8>() > slice_lds_elems<8, 64, E, PackCO>()
+                          ? slice_lds_elems<16, 64, E, PackCI8>()
+                          : slice_lds_elems<8, 64, E, PackCO>();
+  __shared__ E slice_lds[LDS];
+  const int blk = blockIdx.x;
+  int t = 0;
+  while (t + 1 < b.ntasks && b.block0[t + 1] <= blk) ++t;
+  const PackTask& k = b.t[t];
+  const int slice = blk - b.block0[t];
+  const E* w = (const E*)k.w;
+  E* out = (E*)k.out;
+#define SB_PACK_CASE(DG, LAY, CK, BN)                                                      \
+  case pack_kind(DG, LAY, CK, BN):                                                         \
+    pack_slice<DG, CK, BN, E, LAY>(w, out, k.Cin, k.Cout, slice, slice_lds);                \
+    break;
+  switch (k.kind) {
+    SB_PACK_CASE(false, PackCO, 8, 64)
+    SB_PACK_CASE(true, PackCO, 8, 64)
+    SB_PACK_CASE(false, PackCO, 4, 64)
+    SB_PACK_CASE(true, PackCO, 4, 64)
+    SB_PACK_CASE(false, PackCO, 8, 16)
+    SB_PACK_CASE(true, PackCO, 8, 16)
+    SB_PACK_CASE(false, PackCI8, 16, 64)
+    SB_PACK_CASE(true, PackCI8, 16, 64)
+    SB_PACK_CASE(false, PackCI8, 16, 32)
+    SB_PACK_CASE(true, PackCI8, 16, 32)
+    default: break;
+  }
+#undef SB_PACK_CASE
 }
 
 // Buffer resources of a block: its images of the input (from image n0 on)

@@ -549,8 +549,10 @@ static IgemmPlan igemm_plan(int N, int Cin, int H, int W, int Cout, int esize,
   return p;
 }
 
+// pack: the call packs the filters itself (into the workspace); otherwise
+// a.wpk already holds them.
 template <class T, bool DGRAD, bool SMALL, class E>
-static void igemm_launch(const IgemmPlan& p, const ConvArgs& a, hipStream_t st) {
+static void igemm_launch(const IgemmPlan& p, const ConvArgs& a, bool pack, hipStream_t st) {
   static bool attr_set = false;
   const void* fn;
   if constexpr (SMALL) fn = (const void*)conv3x3_small_f32<T, DGRAD, E>;
@@ -559,8 +561,9 @@ static void igemm_launch(const IgemmPlan& p, const ConvArgs& a, hipStream_t st) 
     (void)hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)T::LDS_BYTES);
     attr_set = true;
   }
-  filter_pack<DGRAD, T::CK, T::BN, E><<<p.co_tiles * p.nchunks, 256, 0, st>>>(
-      (const E*)a.wt, (E*)a.wpk, a.Cin, a.Cout);
+  if (pack)
+    filter_pack<DGRAD, T::CK, T::BN, E><<<p.co_tiles * p.nchunks, 256, 0, st>>>(
+        (const E*)a.wt, (E*)a.wpk, a.Cin, a.Cout);
   dim3 grid(p.grid_x, p.co_tiles, p.splits);
   ConvArgs k = a;
   if (p.splits > 1) { k.bias = nullptr; k.mask = nullptr; k.relu = 0; }
@@ -576,22 +579,37 @@ static void igemm_launch(const IgemmPlan& p, const ConvArgs& a, hipStream_t st) 
 }
 
 template <bool DGRAD, class E>
-static void igemm_dispatch(const IgemmPlan& p, const ConvArgs& a, hipStream_t st) {
+static void igemm_dispatch(const IgemmPlan& p, const ConvArgs& a, bool pack, hipStream_t st) {
   switch (p.tile) {
-    case 0: igemm_launch<TileW32, DGRAD, false, E>(p, a, st); break;
-    case 1: igemm_launch<TileW16, DGRAD, false, E>(p, a, st); break;
-    case 2: igemm_launch<TileW8, DGRAD, false, E>(p, a, st); break;
-    case 3: igemm_launch<TileW4, DGRAD, false, E>(p, a, st); break;
-    case 4: igemm_launch<TileW2, DGRAD, false, E>(p, a, st); break;
-    case 5: igemm_launch<TileW32c4, DGRAD, false, E>(p, a, st); break;
-    case 6: igemm_launch<TileW32n16, DGRAD, false, E>(p, a, st); break;
-    case 7: igemm_launch<Small2, DGRAD, true, E>(p, a, st); break;
-    case 8: igemm_launch<Small4, DGRAD, true, E>(p, a, st); break;
-    case 9: igemm_launch<TileW32L, DGRAD, false, E>(p, a, st); break;
-    case 10: igemm_launch<TileW16L, DGRAD, false, E>(p, a, st); break;
-    case 11: igemm_launch<TileW8L, DGRAD, false, E>(p, a, st); break;
-    default: igemm_launch<TileW8K2, DGRAD, false, E>(p, a, st); break;
+    case 0: igemm_launch<TileW32, DGRAD, false, E>(p, a, pack, st); break;
+    case 1: igemm_launch<TileW16, DGRAD, false, E>(p, a, pack, st); break;
+    case 2: igemm_launch<TileW8, DGRAD, false, E>(p, a, pack, st); break;
+    case 3: igemm_launch<TileW4, DGRAD, false, E>(p, a, pack, st); break;
+    case 4: igemm_launch<TileW2, DGRAD, false, E>(p, a, pack, st); break;
+    case 5: igemm_launch<TileW32c4, DGRAD, false, E>(p, a, pack, st); break;
+    case 6: igemm_launch<TileW32n16, DGRAD, false, E>(p, a, pack, st); break;
+    case 7: igemm_launch<Small2, DGRAD, true, E>(p, a, pack, st); break;
+    case 8: igemm_launch<Small4, DGRAD, true, E>(p, a, pack, st); break;
+    case 9: igemm_launch<TileW32L, DGRAD, false, E>(p, a, pack, st); break;
+    case 10: igemm_launch<TileW16L, DGRAD, false, E>(p, a, pack, st); break;
+    case 11: igemm_launch<TileW8L, DGRAD, false, E>(p, a, pack, st); break;
+    default: igemm_launch<TileW8K2, DGRAD, false, E>(p, a, pack, st); break;
   }
+}
+
+// Packs the filters of a layer for the fp32-MFMA kernels: [tap][ci][co]
+// slices of CK input x BN output channels, as the plan's tile stages them
+// (CK = 8, BN = 64 but for the 4-channel-chunk and 16-channel-output tiles).
+template <bool DGRAD, class E>
+static void igemm_pack(const IgemmPlan& p, const void* wt, void* packed, int Cin, int Cout,
+                       hipStream_t st) {
+  const unsigned g = p.co_tiles * p.nchunks;
+  if (p.tile == 5)
+    filter_pack<DGRAD, 4, 64, E><<<g, 256, 0, st>>>((const E*)wt, (E*)packed, Cin, Cout);
+  else if (p.tile == 6)
+    filter_pack<DGRAD, 8, 16, E><<<g, 256, 0, st>>>((const E*)wt, (E*)packed, Cin, Cout);
+  else
+    filter_pack<DGRAD, 8, 64, E><<<g, 256, 0, st>>>((const E*)wt, (E*)packed, Cin, Cout);
 }
 
 }  // namespace sb
@@ -600,19 +618,82 @@ static void igemm_dispatch(const IgemmPlan& p, const ConvArgs& a, hipStream_t st
 namespace sbh {
 
 // The bf16 MFMA path (conv_bf16.hip) for the bf16 shapes it takes.
-size_t conv_bf16_ws(int N, int Cin, int H, int W, int Cout);
+size_t conv_bf16_ws(int N, int Cin, int H, int W, int Cout, bool prepacked);
 bool conv_bf16_takes(int N, int Cin, int H, int W, int Cout);
 int conv_bf16_describe(bool dgrad, int N, int Cin, int H, int W, int Cout, char* buf, size_t len);
+size_t conv_bf16_pack_bytes(int N, int Cin, int H, int W, int Cout);
+void conv_bf16_pack(bool dgrad, int N, int Cin, int H, int W, int Cout, const void* wt,
+                    void* packed, hipStream_t st);
 sb_status conv_bf16(bool dgrad, int N, int Cin, int H, int W, int Cout, const void* in,
                     const void* wt, const float* bias, const void* mask, void* out, void* ws,
-                    size_t ws_bytes, int relu, hipStream_t st);
+                    size_t ws_bytes, int relu, bool prepacked, hipStream_t st);
 
-size_t conv_igemm_ws(int dtype, int N, int Cin, int H, int W, int Cout) {
+// Workspace of a forward / data-gradient call; prepacked: the filters come
+// packed, the workspace holds only the split partials.
+size_t conv_igemm_ws(int dtype, int N, int Cin, int H, int W, int Cout, bool prepacked) {
   if (dtype == SB_BF16 && conv_bf16_takes(N, Cin, H, W, Cout))
-    return conv_bf16_ws(N, Cin, H, W, Cout);
+    return conv_bf16_ws(N, Cin, H, W, Cout, prepacked);
   const int es = (int)dsize(dtype);
-  return std::max(sb::igemm_plan(N, Cin, H, W, Cout, es, true).ws_bytes,
-                  sb::igemm_plan(N, Cin, H, W, Cout, es, false).ws_bytes);
+  const sb::IgemmPlan p = sb::igemm_plan(N, Cin, H, W, Cout, es, true);
+  const sb::IgemmPlan q = sb::igemm_plan(N, Cin, H, W, Cout, es, false);
+  if (prepacked) return std::max(p.ws_bytes - p.part_off, q.ws_bytes - q.part_off);
+  return std::max(p.ws_bytes, q.ws_bytes);
+}
+
+// Bytes of the packed filters.  The packed layout depends on the shape only
+// (the whole-image tiles that aligned tensors may take stage the same slices
+// as the tiles they replace).
+size_t conv_igemm_pack_bytes(int dtype, int N, int Cin, int H, int W, int Cout) {
+  if (dtype == SB_BF16 && conv_bf16_takes(N, Cin, H, W, Cout))
+    return conv_bf16_pack_bytes(N, Cin, H, W, Cout);
+  return sb::igemm_plan(N, Cin, H, W, Cout, (int)dsize(dtype), false).pack_bytes;
+}
+
+void conv_bf16_pack_geom(int N, int Cin, int H, int W, int Cout, int* ck, int* bn, int* slices);
+
+// One packing task: the kernel kind (slice geometry and layout) and the
+// number of slices of a forward or data-gradient packing.
+int conv_igemm_pack_task(bool dgrad, int dtype, int N, int Cin, int H, int W, int Cout,
+                         const void* wt, void* packed, sb::PackTask* t) {
+  int ck, bn, slices, layout;
+  if (dtype == SB_BF16 && conv_bf16_takes(N, Cin, H, W, Cout)) {
+    conv_bf16_pack_geom(N, Cin, H, W, Cout, &ck, &bn, &slices);
+    layout = sb::PackCI8;
+  } else {
+    const sb::IgemmPlan p = sb::igemm_plan(N, Cin, H, W, Cout, (int)dsize(dtype), false);
+    ck = p.tile == 5 ? 4 : 8;
+    bn = p.tile == 6 ? 16 : 64;
+    slices = p.co_tiles * p.nchunks;
+    layout = sb::PackCO;
+  }
+  t->w = wt;
+  t->out = packed;
+  t->Cin = Cin;
+  t->Cout = Cout;
+  t->kind = sb::pack_kind(dgrad, layout, ck, bn);
+  return slices;
+}
+
+void conv_pack_many(int dtype, const sb::PackBatch& b, hipStream_t st) {
+  const unsigned blocks = (unsigned)b.block0[b.ntasks];
+  if (dtype == SB_BF16) sb::filter_pack_many<sb::u16><<<blocks, 256, 0, st>>>(b);
+  else sb::filter_pack_many<float><<<blocks, 256, 0, st>>>(b);
+}
+
+void conv_igemm_pack(bool dgrad, int dtype, int N, int Cin, int H, int W, int Cout,
+                     const void* wt, void* packed, hipStream_t st) {
+  if (dtype == SB_BF16 && conv_bf16_takes(N, Cin, H, W, Cout)) {
+    conv_bf16_pack(dgrad, N, Cin, H, W, Cout, wt, packed, st);
+    return;
+  }
+  const sb::IgemmPlan p = sb::igemm_plan(N, Cin, H, W, Cout, (int)dsize(dtype), false);
+  if (dtype == SB_BF16) {
+    if (dgrad) sb::igemm_pack<true, sb::u16>(p, wt, packed, Cin, Cout, st);
+    else sb::igemm_pack<false, sb::u16>(p, wt, packed, Cin, Cout, st);
+  } else {
+    if (dgrad) sb::igemm_pack<true, float>(p, wt, packed, Cin, Cout, st);
+    else sb::igemm_pack<false, float>(p, wt, packed, Cin, Cout, st);
+  }
 }
 
 int conv_igemm_describe(bool dgrad, int dtype, int N, int Cin, int H, int W, int Cout,
@@ -628,9 +709,11 @@ int conv_igemm_describe(bool dgrad, int dtype, int N, int Cin, int H, int W, int
 
 sb_status conv_igemm(bool dgrad, int dtype, int N, int Cin, int H, int W, int Cout,
                      const void* in, const void* wt, const float* bias, const void* mask,
-                     void* out, void* ws, size_t ws_bytes, int relu, hipStream_t st) {
+                     void* out, void* ws, size_t ws_bytes, int relu, bool prepacked,
+                     hipStream_t st) {
   if (dtype == SB_BF16 && conv_bf16_takes(N, Cin, H, W, Cout))
-    return conv_bf16(dgrad, N, Cin, H, W, Cout, in, wt, bias, mask, out, ws, ws_bytes, relu, st);
+    return conv_bf16(dgrad, N, Cin, H, W, Cout, in, wt, bias, mask, out, ws, ws_bytes, relu,
+                     prepacked, st);
   // The whole-image kernels move 4 elements at a time (16 bytes in fp32, 8 in
   // bf16); the plan only picks them for tensors aligned that far.
   const uintptr_t amask = dtype == SB_BF16 ? 7 : 15;
@@ -642,20 +725,22 @@ sb_status conv_igemm(bool dgrad, int dtype, int N, int Cin, int H, int W, int Co
   if ((int64_t)std::min(p.imgs, N) * Cin * H * W * es >= (1ll << 31) ||
       (int64_t)p.pack_bytes >= (1ll << 31))
     return SB_ERR_UNSUPPORTED;
-  if (ws == nullptr || ws_bytes < p.ws_bytes) return SB_ERR_WORKSPACE;
+  const size_t part_off = prepacked ? 0 : p.part_off;
+  const size_t need = prepacked ? p.ws_bytes - p.part_off : p.ws_bytes;
+  if (need && (ws == nullptr || ws_bytes < need)) return SB_ERR_WORKSPACE;
   sb::ConvArgs a{};
   a.in = in; a.wt = wt; a.bias = bias; a.mask = mask; a.out = out;
-  a.wpk = ws;
-  a.part = p.splits > 1 ? (float*)((char*)ws + p.part_off) : nullptr;
+  a.wpk = prepacked ? wt : ws;
+  a.part = p.splits > 1 ? (float*)((char*)ws + part_off) : nullptr;
   a.N = N; a.Cin = Cin; a.H = H; a.W = W; a.Cout = Cout;
   a.tiles_w = p.tiles_w; a.tiles_h = p.tiles_h;
   a.nchunks = p.nchunks; a.chunks_per_split = p.cps; a.splits = p.splits; a.relu = relu;
   if (dtype == SB_BF16) {
-    if (dgrad) sb::igemm_dispatch<true, sb::u16>(p, a, st);
-    else sb::igemm_dispatch<false, sb::u16>(p, a, st);
+    if (dgrad) sb::igemm_dispatch<true, sb::u16>(p, a, !prepacked, st);
+    else sb::igemm_dispatch<false, sb::u16>(p, a, !prepacked, st);
   } else {
-    if (dgrad) sb::igemm_dispatch<true, float>(p, a, st);
-    else sb::igemm_dispatch<false, float>(p, a, st);
+    if (dgrad) sb::igemm_dispatch<true, float>(p, a, !prepacked, st);
+    else sb::igemm_dispatch<false, float>(p, a, !prepacked, st);
   }
   return launch_status();
 }

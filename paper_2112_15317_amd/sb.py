@@ -22,6 +22,7 @@ LIB_PATH = os.path.join(HERE, "libsb.so")
 SB_OK, SB_ERR_INVALID_ARG, SB_ERR_UNSUPPORTED, SB_ERR_WORKSPACE, SB_ERR_HIP = range(5)
 SB_F32, SB_BF16 = 0, 1
 SB_FUSE_RELU = 1
+SB_PACKED_FILTERS = 2
 SB_PASS_FWD, SB_PASS_BWD_DATA, SB_PASS_BWD_WEIGHT = 0, 1, 2
 SB_FC_FWD, SB_FC_BWD = 0, 1
 
@@ -45,6 +46,11 @@ SIGNATURES = {
     "sb_status_string": (ctypes.c_char_p, [_i]),
     "sb_version": (_i, []),
     "sb_conv3x3_workspace_bytes": (_sz, [ctypes.POINTER(sb_conv3x3_desc), _i]),
+    "sb_conv3x3_packed_bytes": (_sz, [ctypes.POINTER(sb_conv3x3_desc), _i]),
+    "sb_conv3x3_pack_filters": (_i, [ctypes.POINTER(sb_conv3x3_desc), _i, _vp, _vp, _sz, _vp]),
+    "sb_conv3x3_pack_filters_many": (_i, [_i, ctypes.POINTER(sb_conv3x3_desc),
+                                          ctypes.POINTER(_i), ctypes.POINTER(_vp),
+                                          ctypes.POINTER(_vp), ctypes.POINTER(_sz), _vp]),
     "sb_conv3x3_plan_string": (_sz, [ctypes.POINTER(sb_conv3x3_desc), _i, ctypes.c_char_p, _sz]),
     "sb_conv3x3_fwd": (_i, [ctypes.POINTER(sb_conv3x3_desc), _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "sb_conv3x3_bwd_data": (_i, [ctypes.POINTER(sb_conv3x3_desc), _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
@@ -131,8 +137,9 @@ def _ws(ws):
     return ws.data_ptr(), ws.numel() * ws.element_size()
 
 
-def conv_desc(n, c, h, w, k, dtype=SB_F32, relu=False):
-    return sb_conv3x3_desc(n, c, h, w, k, dtype, SB_FUSE_RELU if relu else 0)
+def conv_desc(n, c, h, w, k, dtype=SB_F32, relu=False, packed=False):
+    return sb_conv3x3_desc(n, c, h, w, k, dtype,
+                           (SB_FUSE_RELU if relu else 0) | (SB_PACKED_FILTERS if packed else 0))
 
 
 def fc_desc(m, k_in, n_shard, dtype=SB_F32, ldx=None, ldy=None, relu=False):
@@ -155,6 +162,37 @@ def sb_conv3x3_plan_string(desc, pass_):
     if n == 0:
         raise SBError("sb_conv3x3_plan_string", SB_ERR_INVALID_ARG)
     return buf.value.decode()
+
+
+def sb_conv3x3_packed_bytes(desc, pass_):
+    return load().sb_conv3x3_packed_bytes(ctypes.byref(desc), pass_)
+
+
+def sb_conv3x3_pack_filters(desc, pass_, w, packed, stream=None):
+    _check("sb_conv3x3_pack_filters", load().sb_conv3x3_pack_filters(
+        ctypes.byref(desc), pass_, _ptr(w), _ptr(packed),
+        packed.numel() * packed.element_size(), _stream(stream)))
+
+
+class PackList:
+    """Marshalled arguments of sb_conv3x3_pack_filters_many for a fixed list
+    of (desc, pass, filters, packed buffer): built once, passed to every
+    call (the buffers must stay alive)."""
+
+    def __init__(self, items):
+        n = len(items)
+        self.count = n
+        self.descs = (sb_conv3x3_desc * n)(*[d for d, _, _, _ in items])
+        self.passes = (_i * n)(*[p for _, p, _, _ in items])
+        self.w = (_vp * n)(*[_ptr(w) for _, _, w, _ in items])
+        self.packed = (_vp * n)(*[_ptr(o) for _, _, _, o in items])
+        self.nbytes = (_sz * n)(*[o.numel() * o.element_size() for _, _, _, o in items])
+
+
+def sb_conv3x3_pack_filters_many(plist, stream=None):
+    _check("sb_conv3x3_pack_filters_many", load().sb_conv3x3_pack_filters_many(
+        plist.count, plist.descs, plist.passes, plist.w, plist.packed, plist.nbytes,
+        _stream(stream)))
 
 
 def sb_conv3x3_fwd(desc, x, w, bias, y, ws=None, stream=None):

@@ -61,7 +61,7 @@ class ConvStack:
     """
 
     def __init__(self, schedule, n, in_ch, hw, dtype="f32", device="cuda",
-                 out_buffer=None, out_grad_buffer=None):
+                 out_buffer=None, out_grad_buffer=None, packed=True):
         self.layers = conv_layers(schedule, in_ch, hw)
         if not self.layers[-1].pool_after:
             raise ValueError("the stack must end with a pooled layer")
@@ -97,11 +97,34 @@ class ConvStack:
         self.desc = [sb.conv_desc(n, l.c, l.h, l.w, l.k, self.code, relu=not l.pool_after)
                      for l in L]
         self.desc_b = [sb.conv_desc(n, l.c, l.h, l.w, l.k, self.code) for l in L]
+        # packed: every layer's filters are packed for the forward and the
+        # data-gradient pass in one launch at the start of the step
+        # (sb_conv3x3_pack_filters_many), and the passes take them with
+        # SB_PACKED_FILTERS, instead of each pass packing its own ahead of it
+        # (26 small launches on VGG-16, each mostly ramp-up and drain).
+        self.packed = packed
+        self.pdesc = self.desc
+        self.pdesc_b = self.desc_b
+        if packed:
+            self.pdesc = [sb.conv_desc(n, l.c, l.h, l.w, l.k, self.code, relu=not l.pool_after,
+                                       packed=True) for l in L]
+            self.pdesc_b = [sb.conv_desc(n, l.c, l.h, l.w, l.k, self.code, packed=True)
+                            for l in L]
+
+            def buf(i, pass_):
+                nb = sb.sb_conv3x3_packed_bytes(self.desc_b[i], pass_)
+                return torch.empty((max(nb, 256),), dtype=torch.uint8, device=dev)
+            self.Wf = [buf(l.index, sb.SB_PASS_FWD) for l in L]
+            self.Wb = [buf(l.index, sb.SB_PASS_BWD_DATA) for l in L]
+            self.packs = sb.PackList(
+                [(self.desc_b[i], sb.SB_PASS_FWD, self.W[i], self.Wf[i]) for i in range(len(L))] +
+                [(self.desc_b[i], sb.SB_PASS_BWD_DATA, self.W[i], self.Wb[i])
+                 for i in range(len(L))])
         need = 0
         for l in L:
             need = max(need,
-                       sb.sb_conv3x3_workspace_bytes(self.desc[l.index], sb.SB_PASS_FWD),
-                       sb.sb_conv3x3_workspace_bytes(self.desc_b[l.index], sb.SB_PASS_BWD_DATA),
+                       sb.sb_conv3x3_workspace_bytes(self.pdesc[l.index], sb.SB_PASS_FWD),
+                       sb.sb_conv3x3_workspace_bytes(self.pdesc_b[l.index], sb.SB_PASS_BWD_DATA),
                        sb.sb_conv3x3_workspace_bytes(self.desc_b[l.index], sb.SB_PASS_BWD_WEIGHT))
         # Split-reduction scratch; needs no initialisation.
         self.ws = torch.empty((max(need, 256) + 255) // 256 * 256, dtype=torch.uint8, device=dev)
@@ -124,15 +147,18 @@ class ConvStack:
     # -- the step ---------------------------------------------------------------
     def forward(self, stream=None):
         c = self.call
+        if self.packed:
+            c(("pack", 0), sb.sb_conv3x3_pack_filters_many, self.packs, stream)
         for l in self.layers:
             i = l.index
+            w = self.Wf[i] if self.packed else self.W[i]
             if l.pool_after:
-                c(("fwd", i), sb.sb_conv3x3_fwd, self.desc[i], self.A[i], self.W[i], self.b[i],
+                c(("fwd", i), sb.sb_conv3x3_fwd, self.pdesc[i], self.A[i], w, self.b[i],
                   self.Z[i], self.ws, stream)
                 c(("pool_fwd", i), sb.sb_relu_maxpool_fwd, self.n, l.k, l.h, l.w, self.code,
                   self.Z[i], self.A[i + 1], self.idx[i], stream)
             else:
-                c(("fwd", i), sb.sb_conv3x3_fwd, self.desc[i], self.A[i], self.W[i], self.b[i],
+                c(("fwd", i), sb.sb_conv3x3_fwd, self.pdesc[i], self.A[i], w, self.b[i],
                   self.A[i + 1], self.ws, stream)
 
     def backward(self, stream=None, want_dx=True):
@@ -148,12 +174,13 @@ class ConvStack:
                 g = self.gA[i + 1]
             c(("wgrad", i), sb.sb_conv3x3_bwd_weight, self.desc_b[i], self.A[i], g, self.dW[i],
               self.db[i], self.ws, stream)
+            w = self.Wb[i] if self.packed else self.W[i]
             if i > 0:
                 mask = None if L[i - 1].pool_after else self.A[i]
-                c(("dgrad", i), sb.sb_conv3x3_bwd_data, self.desc_b[i], g, self.W[i], mask,
+                c(("dgrad", i), sb.sb_conv3x3_bwd_data, self.pdesc_b[i], g, w, mask,
                   self.gA[i], self.ws, stream)
             elif want_dx:
-                c(("dgrad", i), sb.sb_conv3x3_bwd_data, self.desc_b[i], g, self.W[i], None,
+                c(("dgrad", i), sb.sb_conv3x3_bwd_data, self.pdesc_b[i], g, w, None,
                   self.gA[0], self.ws, stream)
 
     def grad_at_conv_output(self, i):

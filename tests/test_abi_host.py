@@ -106,3 +106,56 @@ def test_binding_refuses_host_tensors():
     with pytest.raises(ValueError):
         sb.sb_conv3x3_fwd(d, torch.zeros(1, 1, 2, 2), torch.zeros(1, 1, 3, 3), None,
                           torch.zeros(1, 1, 2, 2), None, stream=0)
+
+
+def test_packed_filter_sizes_and_validation():
+    d = sb.conv_desc(128, 512, 2, 2, 512)
+    for pass_ in (sb.SB_PASS_FWD, sb.SB_PASS_BWD_DATA):
+        pb = sb.sb_conv3x3_packed_bytes(d, pass_)
+        assert pb >= 512 * 512 * 9 * 4        # every filter element, padded to whole slices
+        # The workspace of a call with packed filters leaves out the packing room.
+        dp = sb.conv_desc(128, 512, 2, 2, 512, packed=True)
+        full = sb.sb_conv3x3_workspace_bytes(d, pass_)
+        part = sb.sb_conv3x3_workspace_bytes(dp, pass_)
+        assert part < full and full - part >= pb
+    assert sb.sb_conv3x3_packed_bytes(d, sb.SB_PASS_BWD_WEIGHT) == 0
+    assert sb.sb_conv3x3_packed_bytes(sb.conv_desc(0, 3, 8, 8, 4), 0) == 0
+    # The flag is for the forward and data-gradient passes only, and ReLU
+    # stays forward-only with it.
+    dp = sb.conv_desc(2, 3, 8, 8, 4, packed=True)
+    assert sb.sb_conv3x3_workspace_bytes(dp, sb.SB_PASS_BWD_WEIGHT) == 2 ** 64 - 1
+    dpr = sb.conv_desc(2, 3, 8, 8, 4, relu=True, packed=True)
+    assert sb.sb_conv3x3_workspace_bytes(dpr, sb.SB_PASS_FWD) != 2 ** 64 - 1
+    assert sb.sb_conv3x3_workspace_bytes(dpr, sb.SB_PASS_BWD_DATA) == 2 ** 64 - 1
+    small = sb.conv_desc(2, 3, 8, 8, 4)
+    need = sb.sb_conv3x3_packed_bytes(small, sb.SB_PASS_FWD)
+    pk = _raw
+    # Bad pass, null pointers, a short buffer, a buffer overlapping the filters.
+    assert pk("sb_conv3x3_pack_filters", ctypes.byref(small), 2, P, P + (1 << 20), need, None) == sb.SB_ERR_INVALID_ARG
+    assert pk("sb_conv3x3_pack_filters", ctypes.byref(small), 0, None, P + (1 << 20), need, None) == sb.SB_ERR_INVALID_ARG
+    assert pk("sb_conv3x3_pack_filters", ctypes.byref(small), 0, P, None, need, None) == sb.SB_ERR_INVALID_ARG
+    assert pk("sb_conv3x3_pack_filters", ctypes.byref(small), 0, P, P + (1 << 20), need - 1, None) == sb.SB_ERR_INVALID_ARG
+    assert pk("sb_conv3x3_pack_filters", ctypes.byref(small), 0, P, P + 8, need, None) == sb.SB_ERR_INVALID_ARG
+
+
+def test_packed_filters_many_validation():
+    d = sb.conv_desc(2, 3, 8, 8, 4)
+    need = sb.sb_conv3x3_packed_bytes(d, sb.SB_PASS_FWD)
+
+    def call(descs, passes, ws, outs, sizes):
+        n = len(descs)
+        return _raw("sb_conv3x3_pack_filters_many", n, (sb.sb_conv3x3_desc * n)(*descs),
+                    (ctypes.c_int * n)(*passes), (ctypes.c_void_p * n)(*ws),
+                    (ctypes.c_void_p * n)(*outs), (ctypes.c_size_t * n)(*sizes), None)
+    w0, o0, o1 = P, P + (1 << 20), P + (2 << 20)
+    assert _raw("sb_conv3x3_pack_filters_many", 0, None, None, None, None, None, None) == sb.SB_ERR_INVALID_ARG
+    # More tasks than one launch takes.
+    many = 65
+    assert call([d] * many, [0] * many, [w0] * many, [o0 + (i << 16) for i in range(many)],
+                [need] * many) == sb.SB_ERR_INVALID_ARG
+    # Mixed dtypes, a bad pass, a short buffer, overlapping outputs.
+    db = sb.conv_desc(2, 3, 8, 8, 4, sb.SB_BF16)
+    assert call([d, db], [0, 0], [w0, w0], [o0, o1], [need, need]) == sb.SB_ERR_INVALID_ARG
+    assert call([d], [2], [w0], [o0], [need]) == sb.SB_ERR_INVALID_ARG
+    assert call([d], [0], [w0], [o0], [need - 1]) == sb.SB_ERR_INVALID_ARG
+    assert call([d, d], [0, 1], [w0, w0], [o0, o0 + 4], [need, need]) == sb.SB_ERR_INVALID_ARG

@@ -228,6 +228,78 @@ def test_conv_bwd_weight_bf16_staging(shape, offset):
     assert rel_l2(to_host(db), db_ref) <= TOL["f32"]
 
 
+PACKED_SHAPES = [(8, 3, 32, 32, 64), (2, 5, 7, 9, 70), (9, 40, 4, 4, 72), (33, 20, 2, 2, 130),
+                 (2, 64, 6, 40, 80), (2, 36, 20, 20, 64), (2, 48, 14, 14, 64), (2, 12, 5, 37, 17)]
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("shape", PACKED_SHAPES)
+def test_conv_packed_filters_match(shape, dtype):
+    """Filters packed once (sb_conv3x3_pack_filters) and passed with
+    SB_PACKED_FILTERS give bit-identical results to calls that pack them
+    themselves, forward and data gradient."""
+    n, c, h, w, k = shape
+    print_case("conv_packed_filters", shape=shape, dtype=dtype)
+    x, wt, b, dy, mask = _conv_inputs(n, c, h, w, k, 17)
+    code = _code(dtype)
+    xd, wd, dyd, md = to_dev(x, dtype), to_dev(wt, dtype), to_dev(dy, dtype), to_dev(mask, dtype)
+    bd = to_dev(b)
+    for pass_ in (sb.SB_PASS_FWD, sb.SB_PASS_BWD_DATA):
+        d = sb.conv_desc(n, c, h, w, k, code, relu=pass_ == sb.SB_PASS_FWD)
+        dp = sb.conv_desc(n, c, h, w, k, code, relu=pass_ == sb.SB_PASS_FWD, packed=True)
+        ws = _ws(sb.sb_conv3x3_workspace_bytes(d, pass_))
+        wsp = _ws(sb.sb_conv3x3_workspace_bytes(dp, pass_))
+        packed = torch.full((max(sb.sb_conv3x3_packed_bytes(d, pass_), 256),), 0xFF,
+                            dtype=torch.uint8, device="cuda")
+        sb.sb_conv3x3_pack_filters(d, pass_, wd, packed)
+        if pass_ == sb.SB_PASS_FWD:
+            shape_out = (n, k, h, w)
+            ref = torch.full(shape_out, float("nan"), dtype=_tdt(dtype), device="cuda")
+            got = torch.full_like(ref, float("nan"))
+            sb.sb_conv3x3_fwd(d, xd, wd, bd, ref, ws)
+            sb.sb_conv3x3_fwd(dp, xd, packed, bd, got, wsp)
+        else:
+            shape_out = (n, c, h, w)
+            ref = torch.full(shape_out, float("nan"), dtype=_tdt(dtype), device="cuda")
+            got = torch.full_like(ref, float("nan"))
+            sb.sb_conv3x3_bwd_data(d, dyd, wd, md, ref, ws)
+            sb.sb_conv3x3_bwd_data(dp, dyd, packed, md, got, wsp)
+        torch.cuda.synchronize()
+        assert torch.equal(ref, got)
+    # And against the oracle once (forward).
+    y = torch.empty((n, k, h, w), dtype=_tdt(dtype), device="cuda")
+    dp = sb.conv_desc(n, c, h, w, k, code, relu=True, packed=True)
+    d = sb.conv_desc(n, c, h, w, k, code, relu=True)
+    packed = torch.empty((max(sb.sb_conv3x3_packed_bytes(d, 0), 256),), dtype=torch.uint8,
+                         device="cuda")
+    sb.sb_conv3x3_pack_filters(d, 0, wd, packed)
+    sb.sb_conv3x3_fwd(dp, xd, packed, bd, y, _ws(sb.sb_conv3x3_workspace_bytes(dp, 0)))
+    torch.cuda.synchronize()
+    assert rel_l2(to_host(y), O.conv3x3_fwd(to_host(xd), to_host(wd), b, relu=True)) <= TOL[dtype]
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_conv_pack_filters_many_matches_single(dtype):
+    """One batched packing of several layers and passes writes exactly what
+    the per-layer packings write."""
+    code = _code(dtype)
+    items = []
+    for j, (n, c, h, w, k) in enumerate(PACKED_SHAPES):
+        wt = to_dev(synth.he_normal_conv3x3(k, c, 18 + j, synth.TID.CONV_W), dtype)
+        d = sb.conv_desc(n, c, h, w, k, code)
+        for pass_ in (sb.SB_PASS_FWD, sb.SB_PASS_BWD_DATA):
+            nb = max(sb.sb_conv3x3_packed_bytes(d, pass_), 256)
+            one = torch.full((nb,), 0xAB, dtype=torch.uint8, device="cuda")
+            many = torch.full((nb,), 0xAB, dtype=torch.uint8, device="cuda")
+            sb.sb_conv3x3_pack_filters(d, pass_, wt, one)
+            items.append((d, pass_, wt, many, one))
+    print_case("pack_filters_many", dtype=dtype, tasks=len(items))
+    sb.sb_conv3x3_pack_filters_many(sb.PackList([(d, p_, w_, m) for d, p_, w_, m, _ in items]))
+    torch.cuda.synchronize()
+    for d, p_, _, many, one in items:
+        assert torch.equal(many, one), (d.n, d.c, d.h, d.w, d.k, p_)
+
+
 def test_conv_bwd_weight_without_bias_grad():
     n, c, h, w, k = 2, 8, 6, 6, 20
     x, _, _, dy, _ = _conv_inputs(n, c, h, w, k, 14)

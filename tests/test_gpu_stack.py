@@ -357,3 +357,24 @@ def test_graph_replay_matches_eager():
         torch.cuda.synchronize()
         for a, b in zip(watch, ref):
             assert torch.equal(a, b), "replay %d differs from the eager step" % rep
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_packed_filter_step_matches_unpacked(dtype):
+    """The stack packs every layer's filters once per step on a side stream
+    (SB_PACKED_FILTERS); the step must equal, bit for bit, a stack whose
+    calls pack their filters themselves."""
+    n, hw = 4, 32
+    print_case("packed_step", n=n, hw=hw, dtype=dtype)
+    layers = configs.conv_layers(configs.VGG16, 3, hw)
+    x, wts, bs = _vgg_inputs(n, hw, 10, layers)
+    dy_top = synth.normal((n, 512, 1, 1), 10, synth.TID.DY_TOP)
+    outs = []
+    for packed in (True, False):
+        st = ConvStack(configs.VGG16, n, 3, hw, dtype, packed=packed)
+        st.load_inputs(x, wts, bs, dy_top)
+        st.step()
+        torch.cuda.synchronize()
+        outs.append([st.A[-1], st.gA[0]] + st.dW + st.db + list(st.idx.values()))
+    for a, b in zip(*outs):
+        assert torch.equal(a, b)
