@@ -191,11 +191,12 @@ __device__ __forceinline__ int wg_hoff(int p) {
   return img * T::HH * T::HW + yy * T::HW + xx;
 }
 
-// WHOLE: every tile is one whole image (IMGS = 1, H = TH, W = TW), so a
-// staged element's offset within its image and whether it lies in the image
-// are the same for every tile: both are worked out once per thread, and a
-// tile's loads then take only the image's buffer range.
-template <class T, class E, bool WHOLE = false>
+// ROWS: every tile spans the image's full width (IMGS = 1, W = TW), so a
+// staged element's offset within its image is a per-thread constant plus the
+// tile's first row, and only its row can leave the image: the constants are
+// worked out once per thread, and per tile an element costs an add and a row
+// test.
+template <class T, class E, bool ROWS = false>
 __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_f32(WgArgs a) {
   extern __shared__ float lds[];
 
@@ -229,36 +230,50 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_f32(WgArgs a) {
 
   float rdy[T::DY_PT], rx[T::X_PT];
 
-  // Whole-image tiles: byte offsets within the image, kOOB outside.
-  static_assert(!WHOLE || T::IMGS == 1, "one image per whole-image tile");
-  uint32_t dy_boff[WHOLE ? T::DY_PT : 1], x_boff[WHOLE ? T::X_PT : 1];
-  if constexpr (WHOLE) {
+  // Full-width tiles: each element's offset in its image for a tile at row
+  // 0, and its row in the tile (dy) or halo (x); a row of kNone marks an
+  // element that no tile has (k, channel or column outside, or past the
+  // staged range).
+  static_assert(!ROWS || T::IMGS == 1, "one image per full-width tile");
+  constexpr int kNone = 1 << 20;
+  int dy_rel[ROWS ? T::DY_PT : 1], dy_row[ROWS ? T::DY_PT : 1];
+  int x_rel[ROWS ? T::X_PT : 1], x_row[ROWS ? T::X_PT : 1];
+  if constexpr (ROWS) {
 #pragma unroll
     for (int i = 0; i < T::DY_PT; ++i) {
       const int e = tid + i * 256;
       const int kk = (e >> 2) & (T::BK - 1), p = ((e >> 8) << 2) | (e & 3);
       const int yy = p / T::TW, xx = p % T::TW;
-      dy_boff[i] = k0 + kk < a.K ? (uint32_t)((k0 + kk) * HWs + yy * a.W + xx) * sizeof(E) : kOOB;
+      dy_rel[i] = (k0 + kk) * HWs + yy * a.W + xx;
+      dy_row[i] = k0 + kk < a.K ? yy : kNone;
     }
 #pragma unroll
     for (int i = 0; i < T::X_PT; ++i) {
       const int e = tid + i * 256;
       const int hp = e / T::BC, cc = e - hp * T::BC;
-      const int h = hp / T::HW - 1, w = hp % T::HW - 1, c = c0 + cc;
-      const bool ok = e < T::BC * T::PLANE && c < a.C && (unsigned)h < (unsigned)a.H &&
-                      (unsigned)w < (unsigned)a.W;
-      x_boff[i] = ok ? (uint32_t)(c * HWs + h * a.W + w) * sizeof(E) : kOOB;
+      const int hy = hp / T::HW, w = hp % T::HW - 1, c = c0 + cc;
+      const bool ok = e < T::BC * T::PLANE && c < a.C && (unsigned)w < (unsigned)a.W;
+      x_rel[i] = c * HWs + (hy - 1) * a.W + w;
+      x_row[i] = ok ? hy - 1 : kNone;
     }
   }
 
   auto gload = [&](int pt) {
-    if constexpr (WHOLE) {
-      const rsrc_t dr = image_rsrc<E>(a.dy, pt, 1, a.N, a.K * HWs);
-      const rsrc_t xr = image_rsrc<E>(a.x, pt, 1, a.N, a.C * HWs);
+    if constexpr (ROWS) {
+      const int ty = pt % a.tiles_h, n0 = pt / a.tiles_h;
+      const int h0 = ty * T::TH, hoff = h0 * a.W;
+      const rsrc_t dr = image_rsrc<E>(a.dy, n0, 1, a.N, a.K * HWs);
+      const rsrc_t xr = image_rsrc<E>(a.x, n0, 1, a.N, a.C * HWs);
 #pragma unroll
-      for (int i = 0; i < T::DY_PT; ++i) rdy[i] = BufLoad<E>::one(dr, dy_boff[i]);
+      for (int i = 0; i < T::DY_PT; ++i)
+        rdy[i] = BufLoad<E>::one(dr, h0 + dy_row[i] < a.H
+                                         ? (uint32_t)(dy_rel[i] + hoff) * (uint32_t)sizeof(E)
+                                         : kOOB);
 #pragma unroll
-      for (int i = 0; i < T::X_PT; ++i) rx[i] = BufLoad<E>::one(xr, x_boff[i]);
+      for (int i = 0; i < T::X_PT; ++i)
+        rx[i] = BufLoad<E>::one(xr, (unsigned)(h0 + x_row[i]) < (unsigned)a.H
+                                        ? (uint32_t)(x_rel[i] + hoff) * (uint32_t)sizeof(E)
+                                        : kOOB);
       return;
     }
     int tx = pt % a.tiles_w, r0 = pt / a.tiles_w;
@@ -891,12 +906,12 @@ static WgPlan wg_plan(int N, int C, int H, int W, int K, bool allow_small, bool 
   return p;
 }
 
-template <class T, bool SMALL, class E, bool WHOLE = false>
+template <class T, bool SMALL, class E, bool ROWS = false>
 static void wg_launch(const WgPlan& p, const WgArgs& a, hipStream_t st) {
   static bool attr_set = false;
   const void* fn;
   if constexpr (SMALL) fn = (const void*)conv3x3_wgrad_small_f32<T, E>;
-  else fn = (const void*)conv3x3_wgrad_f32<T, E, WHOLE>;
+  else fn = (const void*)conv3x3_wgrad_f32<T, E, ROWS>;
   if (!attr_set) {
     (void)hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)T::LDS_BYTES);
     attr_set = true;
@@ -905,7 +920,7 @@ static void wg_launch(const WgPlan& p, const WgArgs& a, hipStream_t st) {
   if constexpr (SMALL)
     conv3x3_wgrad_small_f32<T, E><<<grid, 256, T::LDS_BYTES, st>>>(a);
   else
-    conv3x3_wgrad_f32<T, E, WHOLE><<<grid, 256, T::LDS_BYTES, st>>>(a);
+    conv3x3_wgrad_f32<T, E, ROWS><<<grid, 256, T::LDS_BYTES, st>>>(a);
   if (p.splits > 1) launch_splits_reduce(a.part, p.splits, a.K, a.C, a.dw, a.db, st);
 }
 
@@ -971,11 +986,17 @@ static void wg_launch_bf16v(int v, const sb::WgPlan& p, const sb::WgArgs& a, hip
 template <class E>
 static void wg_dispatch(const sb::WgPlan& p, const sb::WgArgs& a, hipStream_t st) {
   switch (p.tile) {
-    case 0: sb::wg_launch<sb::WgW32, false, E>(p, a, st); break;
-    case 1: sb::wg_launch<sb::WgW16, false, E>(p, a, st); break;
+    // Images exactly as wide as the tile take the full-width staging.
+    case 0:
+      if (a.W == 32) sb::wg_launch<sb::WgW32, false, E, true>(p, a, st);
+      else sb::wg_launch<sb::WgW32, false, E>(p, a, st);
+      break;
+    case 1:
+      if (a.W == 16) sb::wg_launch<sb::WgW16, false, E, true>(p, a, st);
+      else sb::wg_launch<sb::WgW16, false, E>(p, a, st);
+      break;
     case 2:
-      // 8x8 images: each 8x8 tile is a whole image.
-      if (a.H == 8 && a.W == 8) sb::wg_launch<sb::WgW8, false, E, true>(p, a, st);
+      if (a.W == 8) sb::wg_launch<sb::WgW8, false, E, true>(p, a, st);
       else sb::wg_launch<sb::WgW8, false, E>(p, a, st);
       break;
     case 3: sb::wg_launch<sb::WgW4, false, E>(p, a, st); break;
