@@ -71,7 +71,16 @@ struct BTile {
   }
 };
 
-template <class T, bool DGRAD, int V>
+// ONE: a single LDS buffer (for short channel loops: a block then needs
+// about half the LDS, so more blocks share a CU and one block's prologue and
+// epilogue overlap another's MFMAs); the next chunk still loads into
+// registers while the current one is computed.
+template <class T>
+__host__ __device__ constexpr size_t one_buf_lds_bytes() {
+  return (T::LDS_BUF > T::BN * (T::BM + 8) ? T::LDS_BUF : T::BN * (T::BM + 8)) * sizeof(u16);
+}
+
+template <class T, bool DGRAD, int V, bool ONE = false>
 __global__ __launch_bounds__(256, 2) void conv3x3_igemm_bf16(ConvArgs a) {
   extern __shared__ u16 ldsb[];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -214,18 +223,35 @@ __global__ __launch_bounds__(256, 2) void conv3x3_igemm_bf16(ConvArgs a) {
   };
 
   const int nk = kc1 - kc0;
-  if (nk > 0) {
-    gload(kc0);
-    lstore(0);
-    if (nk > 1) gload(kc0 + 1);
-  }
-  __syncthreads();
-  for (int t = 0; t < nk; ++t) {
-    const int buf = t & 1;
-    if (t + 1 < nk) lstore(buf ^ 1);
-    if (t + 2 < nk) gload(kc0 + t + 2);
-    compute(buf);
+  if constexpr (ONE) {
+    if (nk > 0) {
+      gload(kc0);
+      lstore(0);
+    }
     __syncthreads();
+    for (int t = 0; t < nk; ++t) {
+      if (t + 1 < nk) gload(kc0 + t + 1);
+      compute(0);
+      __syncthreads();
+      if (t + 1 < nk) {
+        lstore(0);
+        __syncthreads();
+      }
+    }
+  } else {
+    if (nk > 0) {
+      gload(kc0);
+      lstore(0);
+      if (nk > 1) gload(kc0 + 1);
+    }
+    __syncthreads();
+    for (int t = 0; t < nk; ++t) {
+      const int buf = t & 1;
+      if (t + 1 < nk) lstore(buf ^ 1);
+      if (t + 2 < nk) gload(kc0 + t + 2);
+      compute(buf);
+      __syncthreads();
+    }
   }
 
   // acc[nb][mb] element v: output channel co0 + nb*32 + 8*(v/4) + 4*lh +
@@ -258,7 +284,8 @@ __global__ __launch_bounds__(256, 2) void conv3x3_igemm_bf16(ConvArgs a) {
   // consecutive pixels of one channel, the ReLU mask read in the same
   // pieces; every mask load is issued before the first store.
   constexpr int EP = T::BM + 8;                      // LDS row pitch (bf16)
-  static_assert(T::BN * EP <= 2 * T::LDS_BUF, "output tile fits the staging LDS");
+  static_assert(T::BN * EP * sizeof(u16) <= (ONE ? one_buf_lds_bytes<T>() : T::LDS_BYTES),
+                "output tile fits the staging LDS");
   u16* E = ldsb;
 #pragma unroll
   for (int nb = 0; nb < T::NB; ++nb)
@@ -434,17 +461,32 @@ static void bf16_pack(const BPlan& p, const void* wt, void* packed, int Cin, int
 // a.wpk already holds them.
 template <class T, bool DGRAD, int V>
 static void bf16_launch(const BPlan& p, const ConvArgs& a, bool pack, hipStream_t st) {
+  // Short channel loops (at most 8 chunks) on the 256-pixel tiles take the
+  // single-buffer form.
+  constexpr bool can_one = T::BM == 256;
+  const bool one = can_one && p.cps <= 8;
   static bool attr_set = false;
   if (!attr_set) {
     (void)hipFuncSetAttribute((const void*)conv3x3_igemm_bf16<T, DGRAD, V>,
                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)T::LDS_BYTES);
+    if constexpr (can_one)
+      (void)hipFuncSetAttribute((const void*)conv3x3_igemm_bf16<T, DGRAD, V, true>,
+                                hipFuncAttributeMaxDynamicSharedMemorySize,
+                                (int)one_buf_lds_bytes<T>());
     attr_set = true;
   }
   if (pack) bf16_pack<DGRAD>(p, a.wt, (void*)a.wpk, a.Cin, a.Cout, st);
   dim3 grid(p.grid_x, p.co_tiles, p.splits);
   ConvArgs k = a;
   if (p.splits > 1) { k.bias = nullptr; k.mask = nullptr; k.relu = 0; }
-  conv3x3_igemm_bf16<T, DGRAD, V><<<grid, 256, T::LDS_BYTES, st>>>(k);
+  if constexpr (can_one) {
+    if (one)
+      conv3x3_igemm_bf16<T, DGRAD, V, true><<<grid, 256, one_buf_lds_bytes<T>(), st>>>(k);
+    else
+      conv3x3_igemm_bf16<T, DGRAD, V><<<grid, 256, T::LDS_BYTES, st>>>(k);
+  } else {
+    conv3x3_igemm_bf16<T, DGRAD, V><<<grid, 256, T::LDS_BYTES, st>>>(k);
+  }
   if (p.splits > 1) {
     size_t total = (size_t)a.N * a.Cout * a.H * a.W;
     launch_splitk_reduce<u16>(a.part, p.splits, total, a.Cout, a.H * a.W, a.bias, a.relu,
