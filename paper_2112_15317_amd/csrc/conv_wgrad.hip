@@ -143,16 +143,61 @@ __global__ __launch_bounds__(256) void splits_reduce4(const float* __restrict__ 
   }
 }
 
+// The same with the splits shared out over the G waves of a block: wave w
+// sums its contiguous range of splits in order, then the G range sums are
+// added in wave order (fixed for a given shape, so still deterministic).
+template <int G>
+__global__ __launch_bounds__(64 * G) void splits_reduce4w(const float* __restrict__ part,
+                                                          int splits, size_t stride,
+                                                          size_t count, size_t wsz,
+                                                          float* __restrict__ dw,
+                                                          float* __restrict__ db) {
+  __shared__ f4 red[G][64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const size_t i4 = ((size_t)blockIdx.x * 64 + lane) * 4;
+  const int per = (splits + G - 1) / G;
+  const int s0 = min(splits, wave * per), s1 = min(splits, s0 + per);
+  red[wave][lane] = i4 < count ? split_sum4(part, s0, s1, stride, i4) : f4{0.f, 0.f, 0.f, 0.f};
+  __syncthreads();
+  if (wave != 0 || i4 >= count) return;
+  f4 v = red[0][lane];
+#pragma unroll
+  for (int w = 1; w < G; ++w) v += red[w][lane];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const size_t i = i4 + j;
+    if (i < wsz) dw[i] = v[j];
+    else db[i - wsz] = v[j];
+  }
+}
+
 // Launches the weight-gradient split reduction: dw (K*C*9) then, when db is
 // wanted, db (K), from partials [splits][K*C*9 + K].
 inline void launch_splits_reduce(const float* part, int splits, int K, int C, float* dw,
                                  float* db, hipStream_t st) {
   const size_t wsz = (size_t)K * C * 9, stride = wsz + K;
   const size_t count = wsz + (db ? K : 0);
-  if (stride % 4 == 0 && count % 4 == 0 && ((uintptr_t)part & 15) == 0)
-    splits_reduce4<<<(unsigned)((count / 4 + 255) / 256), 256, 0, st>>>(part, splits, stride,
-                                                                       count, wsz, dw, db);
-  else
+  if (stride % 4 == 0 && count % 4 == 0 && ((uintptr_t)part & 15) == 0) {
+    const unsigned blocks64 = (unsigned)((count / 4 + 63) / 64);
+    switch (split_waves(count, splits)) {
+      case 1:
+        splits_reduce4<<<(unsigned)((count / 4 + 255) / 256), 256, 0, st>>>(
+            part, splits, stride, count, wsz, dw, db);
+        break;
+      case 2:
+        splits_reduce4w<2><<<blocks64, 128, 0, st>>>(part, splits, stride, count, wsz, dw, db);
+        break;
+      case 4:
+        splits_reduce4w<4><<<blocks64, 256, 0, st>>>(part, splits, stride, count, wsz, dw, db);
+        break;
+      case 8:
+        splits_reduce4w<8><<<blocks64, 512, 0, st>>>(part, splits, stride, count, wsz, dw, db);
+        break;
+      default:
+        splits_reduce4w<16><<<blocks64, 1024, 0, st>>>(part, splits, stride, count, wsz, dw, db);
+        break;
+    }
+  } else
     splits_reduce<<<(unsigned)((count + 63) / 64), 256, 0, st>>>(part, splits, stride, count,
                                                                 wsz, dw, db);
 }

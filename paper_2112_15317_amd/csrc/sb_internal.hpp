@@ -184,23 +184,40 @@ struct SplitSum {
   }
 };
 
-// Sum over the splits of 4 consecutive partials (16-byte aligned, i4 a
-// multiple of 4): part[s*stride + i4 .. +3] for s = 0, 1, ... in that order
-// (the same order for every output, so the result is deterministic), with
-// four splits' loads in flight at a time.
-__device__ __forceinline__ f4 split_sum4(const float* __restrict__ part, int splits,
+// Sum over splits s0 <= s < s1 of 4 consecutive partials (16-byte aligned,
+// i4 a multiple of 4): part[s*stride + i4 .. +3] in increasing s (the same
+// order for every output, so the result is deterministic), with four
+// splits' loads in flight at a time.
+__device__ __forceinline__ f4 split_sum4(const float* __restrict__ part, int s0, int s1,
                                          size_t stride, size_t i4) {
   f4 v = f4{0.f, 0.f, 0.f, 0.f};
-  int s = 0;
-  for (; s + 4 <= splits; s += 4) {
+  int s = s0;
+  for (; s + 4 <= s1; s += 4) {
     const f4 a = *reinterpret_cast<const f4*>(part + (size_t)s * stride + i4);
     const f4 b = *reinterpret_cast<const f4*>(part + (size_t)(s + 1) * stride + i4);
     const f4 c = *reinterpret_cast<const f4*>(part + (size_t)(s + 2) * stride + i4);
     const f4 d = *reinterpret_cast<const f4*>(part + (size_t)(s + 3) * stride + i4);
     v += a; v += b; v += c; v += d;
   }
-  for (; s < splits; ++s) v += *reinterpret_cast<const f4*>(part + (size_t)s * stride + i4);
+  for (; s < s1; ++s) v += *reinterpret_cast<const f4*>(part + (size_t)s * stride + i4);
   return v;
+}
+
+__device__ __forceinline__ f4 split_sum4(const float* __restrict__ part, int splits,
+                                         size_t stride, size_t i4) {
+  return split_sum4(part, 0, splits, stride, i4);
+}
+
+// Waves per block for a 4-wide split reduction of `count` outputs: 1 while
+// one lane per 4 outputs already makes about 64K lanes; otherwise up to 16
+// waves share out the splits (at least 4 splits a wave), so a small output
+// with many splits does not leave a few hundred lanes each walking a long
+// chain of dependent loads.
+inline int split_waves(size_t count, int splits) {
+  const size_t lanes = (count + 3) / 4;
+  int g = 1;
+  while (g < 16 && lanes * g < 65536 && splits >= 8 * g) g *= 2;
+  return g;
 }
 
 }  // namespace sb
