@@ -6,7 +6,7 @@
 // GEMM view: rows = output channels k, columns = (input channel c, tap),
 // reduction = every pixel of the batch.  Blocks of the first column tile also
 // multiply dy against a column of ones, which yields the bias gradient in
-// the same pass.  Two kernels:
+// the same pass.  Three kernels:
 //
 // conv3x3_wgrad_f32 (any shape).  A block owns 64 k and walks a contiguous
 // range of 64-pixel tiles (IMGS images x TH rows x TW cols).  Per pixel tile
@@ -20,7 +20,12 @@
 //     pair, flattened into NCB blocks of 16 MFMA columns; each lane gathers
 //     its own (c, tap), so only C*9 rounded up to 16 is computed.
 //
-// conv3x3_wgrad_small_f32 (whole images of 2x2 or 4x4 pixels).  The
+// conv3x3_wgrad_2x2 (2x2 images): every (output, input) position pair of
+// an image is a tap inside it, so the gradient is one dense GEMM over the
+// images with rows (k, position) and columns (c, position), folded into the
+// 9 taps in the epilogue.
+//
+// conv3x3_wgrad_small_f32 (whole images of 4x4 pixels).  The
 // reduction runs over 4 images at a time at one pixel position; for each
 // (position, tap) pair whose source lies inside the image (known at compile
 // time) one MFMA adds dy[., k, pos] x x[., c, src(pos, tap)] into tap's
@@ -884,6 +889,174 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_small_f32(WgArgs a) {
       });
 }
 
+// ------------------------------------------------- 2x2 images: one GEMM --
+// At 2x2 every input position lies in the 3x3 window of every output
+// position, so all 16 (output position p, input position q) pairs of an
+// image are taps inside the image, and the weight gradient is a dense
+// product over the images,
+//   G[(k,p)][(c,q)] = sum_n dy[n][k][p] * x[n][c][q],
+// whose rows (k,p) and columns (c,q) follow dy's and x's NCHW order, folded
+// afterwards: dW[k][c][r][s] sums G over the pairs with q = p + (r-1, s-1).
+// No MFMA is spent on padding.  Block tile 128 rows (32 k) x 128 columns
+// (32 c), four waves of 64 x 64 (4 x 4 blocks of the 16x16x4 MFMA), 32
+// images per LDS stage, double-buffered; both operands are staged as
+// [image][row] with 16-byte loads of 4 consecutive rows.  The fold runs in
+// the epilogue through LDS (G is never written out); the bias gradient is
+// one more MFMA per row block against a column of ones, in the first
+// column tile's blocks.  Splits over the images write partials as the other
+// weight-gradient kernels do.
+struct Wg2 {
+  static constexpr int BM = 128, BN = 128, BI = 32;
+  static constexpr int RS = BM + 4;                 // [image][row] stride: 4*RS = 16 mod 64 banks
+  static constexpr int OP = BI * RS;                // floats per operand stage
+  static constexpr int KS = 260;                    // fold tile: [k 16][c 16][p 4][q 4], k stride
+  static constexpr int FOLD = 16 * KS;              // floats per wave
+  static constexpr int LDS_FLOATS = 4 * OP > 4 * FOLD ? 4 * OP : 4 * FOLD;
+  static constexpr size_t LDS_BYTES = LDS_FLOATS * sizeof(float);
+};
+
+template <class E>
+__global__ __launch_bounds__(256, 2) void conv3x3_wgrad_2x2(WgArgs a) {
+  using T = Wg2;
+  extern __shared__ float lds[];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave & 1, wn = wave >> 1;
+  const int kq = lane >> 4, lr = lane & 15;
+  const WgBlock blk = wg_block();
+  const int ct = blk.x % a.c_tiles, kt = blk.x / a.c_tiles;
+  const int M = a.K * 4, NC = a.C * 4;              // rows and columns of G
+  const int m0 = kt * T::BM, n0 = ct * T::BN;
+  const int s0 = blk.z * a.tiles_per_split;         // image stages of BI
+  const int s1 = min(a.ptiles, s0 + a.tiles_per_split);
+  const bool do_db = a.db != nullptr && ct == 0 && wn == 0;   // wave-uniform
+
+  f4 acc[4][4], accb[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    accb[i] = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int n = 0; n < 4; ++n) acc[i][n] = f4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  // Staging group g = tid + 256 i: image g / 32, rows 4 (g % 32) .. +3.
+  f4 ra[4], rb[4];
+  auto gload = [&](int s) {
+    const int nb = s * T::BI;
+    const rsrc_t dr = image_rsrc<E>(a.dy, nb, T::BI, a.N, M);
+    const rsrc_t xr = image_rsrc<E>(a.x, nb, T::BI, a.N, NC);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int g = tid + i * 256, img = g >> 5, r4 = (g & 31) * 4;
+      const bool iok = nb + img < a.N;
+      ra[i] = BufLoad<E>::four(
+          dr, iok && m0 + r4 < M ? (uint32_t)(img * M + m0 + r4) * (uint32_t)sizeof(E) : kOOB);
+      rb[i] = BufLoad<E>::four(
+          xr, iok && n0 + r4 < NC ? (uint32_t)(img * NC + n0 + r4) * (uint32_t)sizeof(E) : kOOB);
+    }
+  };
+  auto lstore = [&](int buf) {
+    float* A = lds + buf * 2 * T::OP;
+    float* B = A + T::OP;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int g = tid + i * 256, off = (g >> 5) * T::RS + (g & 31) * 4;
+      *reinterpret_cast<f4*>(A + off) = ra[i];
+      *reinterpret_cast<f4*>(B + off) = rb[i];
+    }
+  };
+  // MFMA k-step j of a 16-image slice takes image 16 s + 4 kq + j from lane
+  // group kq, for both operands.
+  auto compute = [&](int buf) {
+    const float* A = lds + buf * 2 * T::OP;
+    const float* B = A + T::OP;
+#pragma unroll
+    for (int s = 0; s < T::BI / 16; ++s) {
+      float fa[4][4], fb[4][4];
+#pragma unroll
+      for (int b = 0; b < 4; ++b)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int r = (s * 16 + kq * 4 + j) * T::RS + b * 16 + lr;
+          fa[b][j] = A[r + wm * 64];
+          fb[b][j] = B[r + wn * 64];
+        }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int n = 0; n < 4; ++n) acc[i][n] = mfma16x16x4(fa[i][j], fb[n][j], acc[i][n]);
+        if (do_db) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) accb[i] = mfma16x16x4(fa[i][j], 1.0f, accb[i]);
+        }
+      }
+    }
+  };
+
+  const int nt = s1 - s0;
+  if (nt > 0) {
+    gload(s0);
+    lstore(0);
+    if (nt > 1) gload(s0 + 1);
+  }
+  __syncthreads();
+  for (int t = 0; t < nt; ++t) {
+    const int buf = t & 1;
+    if (t + 1 < nt) lstore(buf ^ 1);
+    if (t + 2 < nt) gload(s0 + t + 2);
+    compute(buf);
+    __syncthreads();
+  }
+
+  // acc[i][n] element e is G at row wm*64 + i*16 + 4*kq + e of the block
+  // (k = 4i + kq of the wave's 16, p = e) and column wn*64 + n*16 + lr
+  // (c = 4n + lr/4 of the wave's 16, q = lr % 4): the wave's fold tile.
+  float* F = lds + wave * T::FOLD;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int n = 0; n < 4; ++n)
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        F[(i * 4 + kq) * T::KS + (n * 4 + (lr >> 2)) * 16 + e * 4 + (lr & 3)] = acc[i][n][e];
+  __syncthreads();
+  const size_t wsz = (size_t)a.K * a.C * 9;
+  float* out = a.splits == 1 ? a.dw : a.part + (size_t)blk.z * (wsz + a.K);
+  const int kb = (m0 >> 2) + wm * 16, cb = (n0 >> 2) + wn * 16;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int pr = lane + 64 * r, kl = pr >> 4, cl = pr & 15;
+    const float* g = F + kl * T::KS + cl * 16;
+    float t9[9];
+#pragma unroll
+    for (int t = 0; t < 9; ++t) t9[t] = 0.f;
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      const f4 gp = *reinterpret_cast<const f4*>(g + p * 4);
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        t9[((q >> 1) - (p >> 1) + 1) * 3 + ((q & 1) - (p & 1) + 1)] += gp[q];
+    }
+    const int k = kb + kl, c = cb + cl;
+    if (k < a.K && c < a.C) {
+#pragma unroll
+      for (int t = 0; t < 9; ++t) out[((size_t)k * a.C + c) * 9 + t] = t9[t];
+    }
+  }
+  if (do_db && lr == 0) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int k = kb + i * 4 + kq;
+      if (k < a.K) {
+        const float v = (accb[i][0] + accb[i][1]) + (accb[i][2] + accb[i][3]);
+        if (a.splits == 1) a.db[k] = v;
+        else out[wsz + k] = v;
+      }
+    }
+  }
+}
+
 // ---------------------------------------------------------------- host --
 struct WgPlan {
   int imgs;          // images per pixel tile (per LDS fill for the small kernels)
@@ -901,7 +1074,6 @@ using WgN32_2 = WgTile<2, 32, 1, 2>;   // C <= 3
 using WgN32_4 = WgTile<2, 32, 1, 4>;   // C <= 7
 using WgN4_2 = WgTile<4, 4, 4, 2>;
 using WgN4_4 = WgTile<4, 4, 4, 4>;
-using WgS2 = WgSmall<2, 2, 16>;
 using WgS4 = WgSmall<4, 4, 4>;
 
 static const char* kWgNames[] = {
@@ -910,7 +1082,7 @@ static const char* kWgNames[] = {
     "sb::conv3x3_wgrad_f32<sb::WgTile<2, 2, 16, 0>, %s>", "sb::conv3x3_wgrad_f32<sb::WgTile<2, 32, 1, 2>, %s>",
     "sb::conv3x3_wgrad_f32<sb::WgTile<2, 32, 1, 4>, %s>", "sb::conv3x3_wgrad_f32<sb::WgTile<4, 4, 4, 2>, %s>",
     "sb::conv3x3_wgrad_f32<sb::WgTile<4, 4, 4, 4>, %s>",
-    "sb::conv3x3_wgrad_small_f32<sb::WgSmall<2, 2, 16>, %s>",
+    "sb::conv3x3_wgrad_2x2<%s>",
     "sb::conv3x3_wgrad_small_f32<sb::WgSmall<4, 4, 4>, %s>",
 };
 
@@ -925,7 +1097,7 @@ static WgPlan wg_plan(int N, int C, int H, int W, int K, bool allow_small, bool 
     // 32-wide rows for wide images, 4x4 x 4-image tiles otherwise.
     if (W >= 32) { p.tile = C <= 3 ? 5 : 6; }
     else { th = 4; tw = 4; imgs = 4; p.tile = C <= 3 ? 7 : 8; }
-  } else if (allow_small && H == 2 && W == 2) { p.tile = 9; th = 2; tw = 2; imgs = 16; }
+  } else if (allow_small && H == 2 && W == 2) { p.tile = 9; th = 2; tw = 2; imgs = Wg2::BI; }
   else if (allow_small && H == 4 && W == 4) { p.tile = 10; th = 4; tw = 4; imgs = 4; }
   else if (W >= 32) { p.tile = 0; }
   else if (W >= 16) { p.tile = 1; th = 4; tw = 16; }
@@ -939,9 +1111,14 @@ static WgPlan wg_plan(int N, int C, int H, int W, int K, bool allow_small, bool 
   p.k_tiles = cdiv(K, 64);
   p.bc = bf16 && p.tile <= 2 ? (C >= 32 ? 32 : 16) : 0;
   p.c_tiles = narrow ? 1 : cdiv(C, p.bc ? p.bc : 16);
+  if (p.tile == 9) {                      // 32 k x 32 c per block
+    p.k_tiles = cdiv(K, 32);
+    p.c_tiles = cdiv(C, 32);
+  }
   long blocks = (long)p.k_tiles * p.c_tiles;
-  // About two blocks per CU, at most 256 splits of the pixel range.
-  const long target = 512;
+  // About two blocks per CU (one for the 2x2 GEMM, whose splits would each
+  // write a whole dW), at most 256 splits of the pixel range.
+  const long target = p.tile == 9 ? 256 : 512;
   int splits = 1;
   if (blocks < target)
     splits = (int)std::min<long>(std::min<long>(p.ptiles, 256), cdiv((int)target, (int)blocks));
@@ -949,6 +1126,19 @@ static WgPlan wg_plan(int N, int C, int H, int W, int K, bool allow_small, bool 
   p.splits = cdiv(p.ptiles, p.tps);
   p.ws_bytes = p.splits > 1 ? (size_t)p.splits * ((size_t)K * C * 9 + K) * sizeof(float) : 0;
   return p;
+}
+
+template <class E>
+static void wg_launch_2x2(const WgPlan& p, const WgArgs& a, hipStream_t st) {
+  static bool attr_set = false;
+  if (!attr_set) {
+    (void)hipFuncSetAttribute((const void*)conv3x3_wgrad_2x2<E>,
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)Wg2::LDS_BYTES);
+    attr_set = true;
+  }
+  dim3 grid(p.k_tiles * p.c_tiles, 1, p.splits);
+  conv3x3_wgrad_2x2<E><<<grid, 256, Wg2::LDS_BYTES, st>>>(a);
+  if (p.splits > 1) launch_splits_reduce(a.part, p.splits, a.K, a.C, a.dw, a.db, st);
 }
 
 template <class T, bool SMALL, class E, bool ROWS = false>
@@ -1050,7 +1240,7 @@ static void wg_dispatch(const sb::WgPlan& p, const sb::WgArgs& a, hipStream_t st
     case 6: sb::wg_launch<sb::WgN32_4, false, E>(p, a, st); break;
     case 7: sb::wg_launch<sb::WgN4_2, false, E>(p, a, st); break;
     case 8: sb::wg_launch<sb::WgN4_4, false, E>(p, a, st); break;
-    case 9: sb::wg_launch<sb::WgS2, true, E>(p, a, st); break;
+    case 9: sb::wg_launch_2x2<E>(p, a, st); break;
     default: sb::wg_launch<sb::WgS4, true, E>(p, a, st); break;
   }
 }

@@ -70,6 +70,7 @@ CONV_SHAPES = [
     (5, 24, 8, 8, 96),
     (9, 40, 4, 4, 72),
     (33, 20, 2, 2, 130),     # more images than one tile holds, ragged
+    (5, 40, 2, 2, 36),       # 2x2 in one image stage: unsplit, two ragged row and column tiles
     (2, 12, 5, 37, 17),
     (3, 40, 8, 8, 70),       # 8x8 two-group blocks, odd chunk count (groups uneven)
     (2, 33, 9, 12, 20),      # the same with ragged rows and columns
