@@ -2,7 +2,8 @@
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
                     [--workload vgg16-cifar-f32 | vgg16-imagenet-bf16 |
-                                fc-shard-f32 | hybrid-f32 | paper-variant-f32]
+                                fc-shard-f32 | hybrid-f32 | paper-variant-f32 |
+                                exchange-f32]
                     [--profile-pass]
 
 Default workload (the headline): one step of the 13-layer VGG-16 conv stack,
@@ -22,14 +23,20 @@ every input resident in HBM.  Other workloads:
                        then backward through both;
   paper-variant-f32    the same worker step for the paper's own VGG variant
                        (seven convs, FC 4096 -> 1024 -> 1024 -> 10) in an MP
-                       group of 2: 128 local images, 256 gathered rows.
+                       group of 2: 128 local images, 256 gathered rows;
+  exchange-f32         the modulo- and shard-layer data movement of one MP
+                       group of 4 workers held on this device, at the hybrid
+                       step's shapes, over the 4 modulo iterations: gather
+                       128 x 512 rows, assemble 128 x 4096 from 1024-column
+                       shards, sum and split the partial gradients back.
 
 A step is one or several dozen kernel launches, so it is captured once in a
 HIP graph (through torch.cuda.graph: libsb enqueues on the current stream)
 and the timed region is one replay of a graph of K steps, bracketed by HIP
 events on that stream.
 
-Prints one JSON line: `value` is images/s (TFLOP/s for the FC shard alone);
+Prints one JSON line: `value` is images/s (TFLOP/s for the FC shard alone,
+GB/s for the exchange data movement);
 the line carries the achieved TFLOP/s (nominal 2*N*K*C*9*H*W per conv pass;
 the valid-tap count leaves out padded taps), a per-call duration table, the
 roofline of the dominant kernel and the fp64 CPU oracle's rate on a sample
@@ -311,6 +318,79 @@ class HybridWorkload(Workload):
                           % (n, dt)}
 
 
+class ExchangeWorkload(Workload):
+    """Modulo / shard layers of one MP group (sec. 3.1, 3.2) on one device."""
+    name = "exchange-f32"
+    dtype = "f32"
+    metric = "GB/s modulo + shard layer data movement of one MP group on one GPU (fp32)"
+    text = ("modulo and shard layers of an MP group of 4 workers held on one GPU, all 4 "
+            "modulo iterations: gather 128x512 (of 4 local batches of 128x512), assemble "
+            "128x4096 from 4 shards of 128x1024, sum 4 partial 128x4096 gradients into the "
+            "shards' slices and 4 partial 128x512 into the local rows, fp32")
+    K, B, F, NS = 4, 128, 512, 1024
+
+    def inputs(self):
+        from paper_2112_15317_amd import synth
+        K, B, F, NS = self.K, self.B, self.F, self.NS
+        T = synth.TID.MISC
+        return (synth.normal((K, B, F), 0, T + 11), synth.normal((K, B, K * NS), 0, T + 12),
+                synth.normal((K, B, NS), 0, T + 13), synth.normal((K, B, F), 0, T + 14))
+
+    def build(self):
+        import numpy as np
+        import torch
+        from paper_2112_15317_amd import sb
+        K, B, F, NS = self.K, self.B, self.F, self.NS
+        local, dfull, parts, dg = (torch.from_numpy(a.astype(np.float32)).cuda()
+                                   for a in self.inputs())
+        self.t = dict(local=local, dfull=dfull, parts=parts, dg=dg,
+                      gathered=torch.empty((B, F), device="cuda"),
+                      full=torch.empty((B, K * NS), device="cuda"),
+                      dparts=torch.empty((K, B, NS), device="cuda"),
+                      dlocal=torch.empty((K, B, F), device="cuda"))
+        md, sd = sb.modulo_desc(K, K, B, F), sb.shard_desc(K, K, B, NS)
+        t = self.t
+        calls = []
+        for k in range(K):
+            calls += [(("mfwd", k), sb.sb_modulo_fwd, (md, 0, k, t["local"], t["gathered"])),
+                      (("sfwd", k), sb.sb_shard_fwd, (sd, 0, t["parts"], t["full"])),
+                      (("sbwd", k), sb.sb_shard_bwd, (sd, 0, t["dfull"], t["dparts"])),
+                      (("mbwd", k), sb.sb_modulo_bwd, (md, 0, k, t["dg"], t["dlocal"]))]
+        return calls
+
+    def call_bytes(self, kind):
+        K, B, F, NS = self.K, self.B, self.F, self.NS
+        return 4 * {"mfwd": 2 * B * F, "sfwd": 2 * K * B * NS,
+                    "sbwd": K * B * K * NS + K * B * NS, "mbwd": K * B * F + B * F}[kind]
+
+    def bytes_per_step(self):
+        return self.K * sum(self.call_bytes(k) for k in ("mfwd", "sfwd", "sbwd", "mbwd"))
+
+    def flops(self):
+        return {"nominal": 0, "valid": 0}
+
+    def cpu_baseline(self, sample):
+        from oracle import modulo as OM
+        import numpy as np
+        local, dfull, parts, dg = self.inputs()
+        K = self.K
+        reps = 0
+        t0 = time.perf_counter()
+        while reps == 0 or time.perf_counter() - t0 < 10.0:   # about 10 s of CPU work
+            dl = np.zeros_like(dg)
+            for k in range(K):
+                OM.modulo_fwd(local, 0, k, K)
+                OM.shard_fwd(parts, 0, K)
+                OM.shard_bwd(dfull, 0, K, np.zeros_like(parts))
+                dl = OM.modulo_bwd(dg, 0, k, K, dl)
+            reps += 1
+        dt = time.perf_counter() - t0
+        return {"value": round(reps * self.bytes_per_step() / dt / 1e9, 3), "unit": "GB/s",
+                "cores": 1, "kind": "oracle",
+                "sample": "%d x the whole step (4 modulo iterations; fp64 numpy oracle, one "
+                          "thread), %.1f s" % (reps, dt)}
+
+
 def workloads():
     from paper_2112_15317_amd import configs
     return {
@@ -338,6 +418,7 @@ def workloads():
             "(64,64,M,128,128,M,256,256,256,M) on 128 local 3x32x32 images, then FC "
             "4096->1024->1024->10 split in 2 column shards on the gathered 256 rows, fwd+bwd, "
             "fp32"),
+        "exchange-f32": ExchangeWorkload(),
     }
 
 
@@ -355,6 +436,9 @@ def kernel_name(key, call_args, dtype):
         return "sb_fc_shard_%s m=%d k_in=%d n_shard=%d" % (kind[3:], d.m, d.k_in, d.n_shard)
     if kind == "pack":
         return "sb::filter_pack_many"
+    if kind in ("mfwd", "mbwd", "sfwd", "sbwd"):
+        return "sb::%s_%s_kernel<4>" % ("modulo" if kind[0] == "m" else "shard",
+                                        "fwd" if kind[1:] == "fwd" else "bwd")
     return "sb::relu_maxpool_%s_kernel<%s, 2>" % (
         kind.split("_")[1], "float" if dtype == "f32" else "unsigned short")
 
@@ -366,6 +450,8 @@ def call_work(wl, key, args):
         return layer_flops(wl.layers[i], args[0].n)[0], "flop"
     if kind.startswith("fc_"):
         return fc_flops(args[0], kind, kind == "fc_fwd" or args[5] is not None), "flop"
+    if kind in ("mfwd", "mbwd", "sfwd", "sbwd"):
+        return wl.call_bytes(kind), "bytes"
     esize = 4 if wl.dtype == "f32" else 2
     if kind == "pack":             # every layer's filters read, twice packed written
         return sum(3 * L.k * L.c * 9 * esize for L in wl.layers), "bytes"
@@ -453,6 +539,7 @@ def main():
     peak = PEAK_MFMA_TFLOPS[dtype]
     tf_nom = fl["nominal"] / (ms * 1e-3) / 1e12
     tf_valid = fl["valid"] / (ms * 1e-3) / 1e12
+    moved = getattr(wl, "bytes_per_step", None)
 
     # Group the calls by kernel; the dominant kernel has the largest time per step.
     groups = {}
@@ -486,6 +573,8 @@ def main():
 
     if wl.images:
         value, unit = round(wl.images / (ms * 1e-3), 1), "images/s"
+    elif moved:
+        value, unit = round(moved() / (ms * 1e-3) / 1e9, 1), "GB/s"
     else:
         value, unit = round(tf_nom, 2), "TFLOP/s"
     out = {
@@ -499,8 +588,9 @@ def main():
         "config": {"workload": wl.text, "global_batch": wl.images or FC_SHAPE[0],
                    "parallelism": "none (1 GPU)"},
         "launch": "HIP graph of %d steps" % K,
-        "tflops_nominal": round(tf_nom, 2), "tflops_valid_tap": round(tf_valid, 2),
-        "frac_mfma_peak_nominal": round(tf_nom / peak, 4),
+        "tflops_nominal": None if moved else round(tf_nom, 2),
+        "tflops_valid_tap": None if moved else round(tf_valid, 2),
+        "frac_mfma_peak_nominal": None if moved else round(tf_nom / peak, 4),
         "roofline": roof,
         "sum_of_calls_ms": round(sum(per_call.values()), 4),
         "per_call_us": {"%s%d" % (k[0], k[1] + 1): round(v * 1e3, 1) for k, v in per_call.items()},

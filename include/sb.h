@@ -9,9 +9,11 @@
  * the modulo layer gathers from the K workers.  One worker's compute is
  * therefore: 3x3 convolution forward / data gradient / weight gradient, the
  * ReLU and 2x2 max pooling between them (sec. 2.2), and the forward and
- * backward of its FC column shard.  Those are the calls below.  The
- * collectives around them (modulo / shard layer exchanges, model averaging)
- * are not part of this library.
+ * backward of its FC column shard.  Those are the calls below, together
+ * with the data movement of the modulo and shard layers around the FC
+ * shards for the case where every worker's buffers sit on one device.
+ * Exchanges between devices and model averaging are not part of this
+ * library.
  *
  * Conventions for every call
  * --------------------------
@@ -233,6 +235,77 @@ sb_status sb_fc_shard_bwd(const sb_fc_desc *desc, const void *x,
                           const void *relu_mask_src, void *dx_partial,
                           float *dw_shard, float *db_shard, int accumulate,
                           void *workspace, size_t workspace_bytes, void *stream);
+
+/* ------------------------------------------------------------------------
+ * Modulo and shard layers on one device (sec. 3.1, Modulo Layer and Shard
+ * Layer; sec. 3.2, Group MP Extension).
+ *
+ * The buffers of `workers` emulated workers sit on this device, worker w's
+ * slot at w * stride elements from the base pointer (the layout an
+ * exchange between devices would fill, one slot per peer).  Workers form MP
+ * groups of `mp` consecutive ids (group of worker i: first id
+ * g = (i / mp) * mp); inside a group the paper's K is mp, so mp = 1 is plain
+ * data parallelism and mp = workers a single group.  A call serves the
+ * group of worker `iproc`: all workers of a group gather the same data, and
+ * a backward call writes the results of every worker of the group.  All
+ * tensors are fp32, row-major; sums run over the group's workers in
+ * increasing id (the result does not depend on the launch).  Strides are
+ * in elements and at least one slot's size; input and output slots of the
+ * group must not overlap.  Invalid arguments return SB_ERR_INVALID_ARG with
+ * nothing enqueued.
+ * ---------------------------------------------------------------------- */
+typedef struct {
+    int workers;   /* N, a multiple of mp                                  */
+    int mp;        /* MP group size (the paper's K), >= 1                  */
+    int batch;     /* B: examples per local batch, a multiple of mp        */
+    int features;  /* F: elements per example                              */
+} sb_modulo_desc;
+
+/* Modulo layer forward, iteration k (the counter modulo mp, 0 <= k < mp).
+ * Gathered example b comes from worker g + b / s (the paper's b / size
+ * within the group, s = B / mp), block k of its local batch:
+ *   gathered[b][f] = local[(g + b/s) * local_stride + (k*s + b%s) * F + f]
+ * local: `workers` slots of [B][F]; gathered: [B][F]. */
+sb_status sb_modulo_fwd(const sb_modulo_desc *desc, int iproc, int k,
+                        const float *local, size_t local_stride,
+                        float *gathered, void *stream);
+
+/* Modulo layer backward, iteration k.  dgathered: `workers` slots of [B][F],
+ * each worker's gradient with respect to its gathered batch (a partial sum:
+ * its FC shard covers 1/mp of the layer's outputs).  For each worker g + r
+ * of the group, rows k*s .. k*s + s - 1 of its dlocal slot receive the
+ * group's sum at the gathered examples it supplied:
+ *   dlocal[(g + r) * dl_stride + (k*s + j) * F + f]
+ *       = sum_{w = 0 .. mp-1} dgathered[(g + w) * dg_stride + (r*s + j) * F + f]
+ * Other rows of dlocal are left as they are (the mp iterations fill them in
+ * turn). */
+sb_status sb_modulo_bwd(const sb_modulo_desc *desc, int iproc, int k,
+                        const float *dgathered, size_t dg_stride,
+                        float *dlocal, size_t dl_stride, void *stream);
+
+typedef struct {
+    int workers;   /* N, a multiple of mp                                  */
+    int mp;        /* MP group size, >= 1                                  */
+    int rows;      /* M: rows of the batch                                 */
+    int shard;     /* Ns: output columns of one worker's partition         */
+} sb_shard_desc;
+
+/* Shard layer forward: the next layer's full input [M][mp*Ns] from the
+ * group's partitioned outputs (`workers` slots of [M][Ns]):
+ *   full[m][r*Ns + c] = parts[(g + r) * parts_stride + m*Ns + c] */
+sb_status sb_shard_fwd(const sb_shard_desc *desc, int iproc,
+                       const float *parts, size_t parts_stride, float *full,
+                       void *stream);
+
+/* Shard layer backward: dfull holds `workers` slots of [M][mp*Ns], each
+ * worker's gradient with respect to the full input (partial sums from its
+ * shard of the layer above).  Worker g + r receives its column slice,
+ * summed over the group:
+ *   dparts[(g + r) * dp_stride + m*Ns + c]
+ *       = sum_{w = 0 .. mp-1} dfull[(g + w) * df_stride + m*mp*Ns + r*Ns + c] */
+sb_status sb_shard_bwd(const sb_shard_desc *desc, int iproc,
+                       const float *dfull, size_t df_stride, float *dparts,
+                       size_t dp_stride, void *stream);
 
 #ifdef __cplusplus
 }

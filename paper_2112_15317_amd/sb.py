@@ -41,6 +41,14 @@ class sb_fc_desc(ctypes.Structure):
                 ("ldx", _i), ("ldy", _i), ("flags", ctypes.c_uint)]
 
 
+class sb_modulo_desc(ctypes.Structure):
+    _fields_ = [("workers", _i), ("mp", _i), ("batch", _i), ("features", _i)]
+
+
+class sb_shard_desc(ctypes.Structure):
+    _fields_ = [("workers", _i), ("mp", _i), ("rows", _i), ("shard", _i)]
+
+
 # Every exported symbol of include/sb.h with its ctypes signature.
 SIGNATURES = {
     "sb_status_string": (ctypes.c_char_p, [_i]),
@@ -61,6 +69,10 @@ SIGNATURES = {
     "sb_fc_shard_fwd": (_i, [ctypes.POINTER(sb_fc_desc), _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "sb_fc_shard_bwd": (_i, [ctypes.POINTER(sb_fc_desc), _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i,
                              _vp, _sz, _vp]),
+    "sb_modulo_fwd": (_i, [ctypes.POINTER(sb_modulo_desc), _i, _i, _vp, _sz, _vp, _vp]),
+    "sb_modulo_bwd": (_i, [ctypes.POINTER(sb_modulo_desc), _i, _i, _vp, _sz, _vp, _sz, _vp]),
+    "sb_shard_fwd": (_i, [ctypes.POINTER(sb_shard_desc), _i, _vp, _sz, _vp, _vp]),
+    "sb_shard_bwd": (_i, [ctypes.POINTER(sb_shard_desc), _i, _vp, _sz, _vp, _sz, _vp]),
 }
 
 _lock = threading.Lock()
@@ -242,3 +254,50 @@ def sb_fc_shard_bwd(desc, x, w_shard, dy, relu_mask_src, dx_partial, dw_shard, d
         ctypes.byref(desc), _ptr(x), _ptr(w_shard), _ptr(dy), _ptr(relu_mask_src),
         _ptr(dx_partial), _ptr(dw_shard), _ptr(db_shard), 1 if accumulate else 0, p, nb,
         _stream(stream)))
+
+
+# ------------------------------------------------ modulo and shard layers --
+# Slotted buffers: worker w's slot starts at w * stride elements; by default
+# the stride is the tensor's element count divided by the number of workers
+# (a contiguous [workers][...] tensor).
+def modulo_desc(workers, mp, batch, features):
+    return sb_modulo_desc(workers, mp, batch, features)
+
+
+def shard_desc(workers, mp, rows, shard):
+    return sb_shard_desc(workers, mp, rows, shard)
+
+
+def _slot_stride(t, workers, stride):
+    if stride is not None:
+        return int(stride)
+    if t is None or isinstance(t, int):
+        raise ValueError("give the slot stride for a raw pointer")
+    return t.numel() // workers
+
+
+def sb_modulo_fwd(desc, iproc, k, local, gathered, local_stride=None, stream=None):
+    _check("sb_modulo_fwd", load().sb_modulo_fwd(
+        ctypes.byref(desc), int(iproc), int(k), _ptr(local),
+        _slot_stride(local, desc.workers, local_stride), _ptr(gathered), _stream(stream)))
+
+
+def sb_modulo_bwd(desc, iproc, k, dgathered, dlocal, dg_stride=None, dl_stride=None,
+                  stream=None):
+    _check("sb_modulo_bwd", load().sb_modulo_bwd(
+        ctypes.byref(desc), int(iproc), int(k), _ptr(dgathered),
+        _slot_stride(dgathered, desc.workers, dg_stride), _ptr(dlocal),
+        _slot_stride(dlocal, desc.workers, dl_stride), _stream(stream)))
+
+
+def sb_shard_fwd(desc, iproc, parts, full, parts_stride=None, stream=None):
+    _check("sb_shard_fwd", load().sb_shard_fwd(
+        ctypes.byref(desc), int(iproc), _ptr(parts),
+        _slot_stride(parts, desc.workers, parts_stride), _ptr(full), _stream(stream)))
+
+
+def sb_shard_bwd(desc, iproc, dfull, dparts, df_stride=None, dp_stride=None, stream=None):
+    _check("sb_shard_bwd", load().sb_shard_bwd(
+        ctypes.byref(desc), int(iproc), _ptr(dfull),
+        _slot_stride(dfull, desc.workers, df_stride), _ptr(dparts),
+        _slot_stride(dparts, desc.workers, dp_stride), _stream(stream)))

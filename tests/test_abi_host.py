@@ -159,3 +159,39 @@ def test_packed_filters_many_validation():
     assert call([d], [2], [w0], [o0], [need]) == sb.SB_ERR_INVALID_ARG
     assert call([d], [0], [w0], [o0], [need - 1]) == sb.SB_ERR_INVALID_ARG
     assert call([d, d], [0, 1], [w0, w0], [o0, o0 + 4], [need, need]) == sb.SB_ERR_INVALID_ARG
+
+
+def test_modulo_and_shard_argument_validation():
+    E = sb.SB_ERR_INVALID_ARG
+    good = sb.modulo_desc(4, 2, 8, 16)         # slots of 8 x 16 = 128 elements
+    slot = 128
+    bad_descs = [sb.modulo_desc(4, 0, 8, 16), sb.modulo_desc(3, 2, 8, 16),   # mp 0; N % mp
+                 sb.modulo_desc(4, 2, 7, 16), sb.modulo_desc(4, 2, 8, 0),    # B % mp; F = 0
+                 sb.modulo_desc(2, 4, 8, 16)]                                # mp > N
+    for d in bad_descs:
+        assert _raw("sb_modulo_fwd", ctypes.byref(d), 0, 0, P, slot, P + 1 << 24, None) == E
+        assert _raw("sb_modulo_bwd", ctypes.byref(d), 0, 0, P, slot, P + 1 << 24, slot, None) == E
+    g = ctypes.byref(good)
+    # iproc and k out of range, null pointers, short strides.
+    assert _raw("sb_modulo_fwd", g, 4, 0, P, slot, P + (1 << 24), None) == E
+    assert _raw("sb_modulo_fwd", g, -1, 0, P, slot, P + (1 << 24), None) == E
+    assert _raw("sb_modulo_fwd", g, 0, 2, P, slot, P + (1 << 24), None) == E
+    assert _raw("sb_modulo_fwd", g, 0, 0, None, slot, P + (1 << 24), None) == E
+    assert _raw("sb_modulo_fwd", g, 0, 0, P, slot - 1, P + (1 << 24), None) == E
+    assert _raw("sb_modulo_bwd", g, 0, 0, P, slot, P + (1 << 24), slot - 1, None) == E
+    assert _raw("sb_modulo_bwd", g, 0, 0, P, slot, None, slot, None) == E
+    # Output overlapping the group's input slots (group of worker 3: slots 2, 3).
+    assert _raw("sb_modulo_fwd", g, 3, 0, P, slot, P + 2 * slot * 4 + 64, None) == E
+    assert _raw("sb_modulo_bwd", g, 1, 0, P, slot, P + 4 * slot, slot, None) == E
+
+    sgood = sb.shard_desc(4, 2, 5, 8)          # slots of 5 x 8; full input 5 x 16
+    s = ctypes.byref(sgood)
+    for d in [sb.shard_desc(4, 3, 5, 8), sb.shard_desc(4, 2, 0, 8), sb.shard_desc(4, 2, 5, 0)]:
+        assert _raw("sb_shard_fwd", ctypes.byref(d), 0, P, 40, P + (1 << 24), None) == E
+        assert _raw("sb_shard_bwd", ctypes.byref(d), 0, P, 80, P + (1 << 24), 40, None) == E
+    assert _raw("sb_shard_fwd", s, 4, P, 40, P + (1 << 24), None) == E
+    assert _raw("sb_shard_fwd", s, 0, P, 39, P + (1 << 24), None) == E
+    assert _raw("sb_shard_bwd", s, 0, P, 79, P + (1 << 24), 40, None) == E    # dfull slot is 80
+    assert _raw("sb_shard_bwd", s, 0, P, 80, P + (1 << 24), 39, None) == E
+    assert _raw("sb_shard_fwd", s, 0, P, 40, P + 100, None) == E               # overlap
+    assert _raw("sb_shard_bwd", s, 2, P, 80, P + 2 * 80 * 4 + 8, 40, None) == E
