@@ -42,6 +42,7 @@
 
 #include <algorithm>
 #include <cstdio>
+#include <type_traits>
 
 namespace sb {
 
@@ -103,8 +104,25 @@ struct ConvTile {
   }
 };
 
-template <class T, bool DGRAD, class E>
+// Whether MFMA column block mb of a wave at pixel-row position wm only
+// multiplies zero padding at tap `tap`, when a tile spans the whole image
+// height (H = TH): a 16-pixel column block lies in one tile row, and a tap
+// in the top (bottom) filter row reads the padding row above (below) the
+// image for the image's first (last) row.  Known at compile time after
+// unrolling, so those MFMAs are never issued.
+template <class T, bool WHOLE_H>
+__device__ constexpr bool igemm_pad_block(int wm, int mb, int tap) {
+  if (!WHOLE_H) return false;
+  const int yy = (wm * T::WM + mb * 16) / T::IMGS / T::TW;
+  return (tap / 3 == 0 && yy == 0) || (tap / 3 == 2 && yy == T::TH - 1);
+}
+
+// WHOLE_H: every tile spans the whole image height (H = TH); the MFMAs of
+// column blocks whose taps read only padding rows are skipped.
+template <class T, bool DGRAD, class E, bool WHOLE_H = false>
 __global__ __launch_bounds__(T::THREADS, 2 / T::KSPLIT) void conv3x3_igemm_f32(ConvArgs a) {
+  static_assert(!WHOLE_H || (T::TW * T::IMGS) % 16 == 0,
+                "column blocks must not straddle tile rows");
   extern __shared__ float lds_all[];
 
   // grp: which chunk stream this thread's 256-thread group takes.
@@ -187,7 +205,10 @@ __global__ __launch_bounds__(T::THREADS, 2 / T::KSPLIT) void conv3x3_igemm_f32(C
 #pragma unroll
     for (int i = 0; i < T::WTS_PT; ++i) Wl[w_loff[i]] = rw[i];
   };
-  auto compute = [&](int buf) {
+  // WMC: the wave's pixel-row position wm as a compile-time constant (only
+  // used with WHOLE_H, to skip padding blocks).
+  auto compute_wm = [&](int buf, auto WMC) {
+    constexpr int WMc = decltype(WMC)::value;
     const float* X = lds + buf * T::LDS_BUF;
     const float* Wl = X + T::LDS_X;
     float fa[2][T::NB], fb[2][T::MB];
@@ -199,17 +220,31 @@ __global__ __launch_bounds__(T::THREADS, 2 / T::KSPLIT) void conv3x3_igemm_f32(C
         fa[slot][nb] = Wl[(tap * T::CK + cg * 4 + kq) * T::BN_P + wn * T::WN + nb * 16 + lr];
 #pragma unroll
       for (int mb = 0; mb < T::MB; ++mb)
-        fb[slot][mb] = X[(cg * 4 + kq) * T::PLANE_P + pix_off[mb] + toff];
+        fb[slot][mb] = igemm_pad_block<T, WHOLE_H>(WMc, mb, tap)
+                           ? 0.f : X[(cg * 4 + kq) * T::PLANE_P + pix_off[mb] + toff];
     };
     frag(0, 0);
 #pragma unroll
     for (int s = 0; s < T::NSTEP; ++s) {
       if (s + 1 < T::NSTEP) frag(s + 1, (s + 1) & 1);
+      const int tap = s / (T::CK / 4);
 #pragma unroll
       for (int nb = 0; nb < T::NB; ++nb)
 #pragma unroll
         for (int mb = 0; mb < T::MB; ++mb)
-          acc[nb][mb] = mfma16x16x4(fa[s & 1][nb], fb[s & 1][mb], acc[nb][mb]);
+          if (!igemm_pad_block<T, WHOLE_H>(WMc, mb, tap))
+            acc[nb][mb] = mfma16x16x4(fa[s & 1][nb], fb[s & 1][mb], acc[nb][mb]);
+    }
+  };
+  auto compute = [&](int buf) {
+    if constexpr (WHOLE_H) {
+      static_assert(T::WAVES_M <= 4, "at most four pixel-row positions");
+      if (wm == 0) compute_wm(buf, std::integral_constant<int, 0>{});
+      else if (T::WAVES_M > 1 && wm == 1) compute_wm(buf, std::integral_constant<int, 1>{});
+      else if (T::WAVES_M > 2 && wm == 2) compute_wm(buf, std::integral_constant<int, 2>{});
+      else if (T::WAVES_M > 3) compute_wm(buf, std::integral_constant<int, 3>{});
+    } else {
+      compute_wm(buf, std::integral_constant<int, 0>{});
     }
   };
 
@@ -551,14 +586,31 @@ static IgemmPlan igemm_plan(int N, int Cin, int H, int W, int Cout, int esize,
 
 // pack: the call packs the filters itself (into the workspace); otherwise
 // a.wpk already holds them.
+// Tiles of 8x8 pixels (whole images of 8-row layers) have a variant that
+// skips the MFMAs of padding rows.
+template <class T, bool SMALL>
+constexpr bool has_whole_h() {
+  if constexpr (SMALL) return false;
+  else return T::TH == 8 && T::TW == 8;
+}
+
 template <class T, bool DGRAD, bool SMALL, class E>
 static void igemm_launch(const IgemmPlan& p, const ConvArgs& a, bool pack, hipStream_t st) {
   static bool attr_set = false;
-  const void* fn;
-  if constexpr (SMALL) fn = (const void*)conv3x3_small_f32<T, DGRAD, E>;
-  else fn = (const void*)conv3x3_igemm_f32<T, DGRAD, E>;
+  constexpr bool can_whole = has_whole_h<T, SMALL>();
+  const bool whole = can_whole && a.H == 8;
   if (!attr_set) {
-    (void)hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)T::LDS_BYTES);
+    if constexpr (SMALL) {
+      (void)hipFuncSetAttribute((const void*)conv3x3_small_f32<T, DGRAD, E>,
+                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)T::LDS_BYTES);
+    } else {
+      (void)hipFuncSetAttribute((const void*)conv3x3_igemm_f32<T, DGRAD, E>,
+                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)T::LDS_BYTES);
+      if constexpr (can_whole)
+        (void)hipFuncSetAttribute((const void*)conv3x3_igemm_f32<T, DGRAD, E, true>,
+                                  hipFuncAttributeMaxDynamicSharedMemorySize,
+                                  (int)T::LDS_BYTES);
+    }
     attr_set = true;
   }
   if (pack)
@@ -567,10 +619,16 @@ static void igemm_launch(const IgemmPlan& p, const ConvArgs& a, bool pack, hipSt
   dim3 grid(p.grid_x, p.co_tiles, p.splits);
   ConvArgs k = a;
   if (p.splits > 1) { k.bias = nullptr; k.mask = nullptr; k.relu = 0; }
-  if constexpr (SMALL)
+  if constexpr (SMALL) {
     conv3x3_small_f32<T, DGRAD, E><<<grid, 256, T::LDS_BYTES, st>>>(k);
-  else
-    conv3x3_igemm_f32<T, DGRAD, E><<<grid, T::THREADS, T::LDS_BYTES, st>>>(k);
+  } else {
+    if constexpr (can_whole) {
+      if (whole) conv3x3_igemm_f32<T, DGRAD, E, true><<<grid, T::THREADS, T::LDS_BYTES, st>>>(k);
+      else conv3x3_igemm_f32<T, DGRAD, E><<<grid, T::THREADS, T::LDS_BYTES, st>>>(k);
+    } else {
+      conv3x3_igemm_f32<T, DGRAD, E><<<grid, T::THREADS, T::LDS_BYTES, st>>>(k);
+    }
+  }
   if (p.splits > 1) {
     size_t total = (size_t)a.N * a.Cout * a.H * a.W;
     launch_splitk_reduce<E>(a.part, p.splits, total, a.Cout, a.H * a.W, a.bias, a.relu,

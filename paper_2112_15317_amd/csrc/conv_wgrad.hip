@@ -241,13 +241,27 @@ __device__ __forceinline__ int wg_hoff(int p) {
   return img * T::HH * T::HW + yy * T::HW + xx;
 }
 
+// Whether the MFMA of 4-pixel step st at tap t only multiplies zero padding
+// when a tile is one whole image (H = TH, W = TW): the step's pixels share a
+// row, and a tap in the top (bottom) filter row reads the padding row above
+// (below) the image for the image's first (last) row.  Known at compile time
+// after unrolling, so those MFMAs are never issued.
+template <class T, bool WHOLE>
+__device__ constexpr bool wg_pad_step(int st, int t) {
+  if (!WHOLE) return false;
+  const int yy = (st * 4) % (T::TH * T::TW) / T::TW;
+  return (t / 3 == 0 && yy == 0) || (t / 3 == 2 && yy == T::TH - 1);
+}
+
 // ROWS: every tile spans the image's full width (IMGS = 1, W = TW), so a
 // staged element's offset within its image is a per-thread constant plus the
 // tile's first row, and only its row can leave the image: the constants are
 // worked out once per thread, and per tile an element costs an add and a row
-// test.
-template <class T, class E, bool ROWS = false>
+// test.  WHOLE (with ROWS): every tile is a whole image (H = TH as well), and
+// the steps whose taps read only padding are skipped (wg_pad_step).
+template <class T, class E, bool ROWS = false, bool WHOLE = false>
 __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_f32(WgArgs a) {
+  static_assert(!WHOLE || (ROWS && T::IMGS == 1 && !T::NARROW), "whole-image tiles are full-width");
   extern __shared__ float lds[];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -395,7 +409,7 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_f32(WgArgs a) {
 #pragma unroll
       for (int t = 0; t < T::NACC; ++t) {
         const int toff = (t / 3) * T::HW + (t % 3);
-        o.b[t] = Xp[toff * T::BC + lr];
+        o.b[t] = wg_pad_step<T, WHOLE>(st, t) ? 0.f : Xp[toff * T::BC + lr];
       }
     }
     return o;
@@ -409,7 +423,8 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_f32(WgArgs a) {
       Ops nxt;
       if (st + 1 < T::BP / 4) nxt = fetch(Dl, Xl, st + 1);
 #pragma unroll
-      for (int t = 0; t < T::NACC; ++t) acc[t] = mfma16x16x4(cur.a, cur.b[t], acc[t]);
+      for (int t = 0; t < T::NACC; ++t)
+        if (!wg_pad_step<T, WHOLE>(st, t)) acc[t] = mfma16x16x4(cur.a, cur.b[t], acc[t]);
       if (do_db) accb = mfma16x16x4(cur.a, 1.0f, accb);
       if (st + 1 < T::BP / 4) cur = nxt;
     }
@@ -1141,12 +1156,12 @@ static void wg_launch_2x2(const WgPlan& p, const WgArgs& a, hipStream_t st) {
   if (p.splits > 1) launch_splits_reduce(a.part, p.splits, a.K, a.C, a.dw, a.db, st);
 }
 
-template <class T, bool SMALL, class E, bool ROWS = false>
+template <class T, bool SMALL, class E, bool ROWS = false, bool WHOLE = false>
 static void wg_launch(const WgPlan& p, const WgArgs& a, hipStream_t st) {
   static bool attr_set = false;
   const void* fn;
   if constexpr (SMALL) fn = (const void*)conv3x3_wgrad_small_f32<T, E>;
-  else fn = (const void*)conv3x3_wgrad_f32<T, E, ROWS>;
+  else fn = (const void*)conv3x3_wgrad_f32<T, E, ROWS, WHOLE>;
   if (!attr_set) {
     (void)hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)T::LDS_BYTES);
     attr_set = true;
@@ -1155,7 +1170,7 @@ static void wg_launch(const WgPlan& p, const WgArgs& a, hipStream_t st) {
   if constexpr (SMALL)
     conv3x3_wgrad_small_f32<T, E><<<grid, 256, T::LDS_BYTES, st>>>(a);
   else
-    conv3x3_wgrad_f32<T, E, ROWS><<<grid, 256, T::LDS_BYTES, st>>>(a);
+    conv3x3_wgrad_f32<T, E, ROWS, WHOLE><<<grid, 256, T::LDS_BYTES, st>>>(a);
   if (p.splits > 1) launch_splits_reduce(a.part, p.splits, a.K, a.C, a.dw, a.db, st);
 }
 
@@ -1231,7 +1246,8 @@ static void wg_dispatch(const sb::WgPlan& p, const sb::WgArgs& a, hipStream_t st
       else sb::wg_launch<sb::WgW16, false, E>(p, a, st);
       break;
     case 2:
-      if (a.W == 8) sb::wg_launch<sb::WgW8, false, E, true>(p, a, st);
+      if (a.W == 8 && a.H == 8) sb::wg_launch<sb::WgW8, false, E, true, true>(p, a, st);
+      else if (a.W == 8) sb::wg_launch<sb::WgW8, false, E, true>(p, a, st);
       else sb::wg_launch<sb::WgW8, false, E>(p, a, st);
       break;
     case 3: sb::wg_launch<sb::WgW4, false, E>(p, a, st); break;
