@@ -27,16 +27,19 @@ __device__ __forceinline__ f4 mfma16x16x4(float a, float b, f4 c) {
 }
 
 // bf16 <-> fp32.  bf16 is the upper half of an fp32 bit pattern; the
-// conversion to bf16 rounds to nearest, ties to even (NaN kept quiet).
+// conversion to bf16 rounds to nearest, ties to even (NaN kept quiet), in
+// one hardware conversion (v_cvt_pk_bf16_f32, two values per instruction).
 __device__ __forceinline__ float bf16_to_f32(u16 v) {
   return __uint_as_float(((uint32_t)v) << 16);
 }
 __device__ __forceinline__ u16 f32_to_bf16(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu))
-    return (u16)((u >> 16) | 0x40);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (u16)(u >> 16);
+  return __builtin_bit_cast(u16, (__bf16)f);
+}
+// lo in bits 0..15, hi in bits 16..31.
+__device__ __forceinline__ uint32_t f32x2_to_bf16x2(float lo, float hi) {
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+  typedef float f32x2_t __attribute__((ext_vector_type(2)));
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){lo, hi}, bf16x2_t));
 }
 
 // Activation / filter element access: float (SB_F32) or bfloat16 bits held
@@ -61,8 +64,8 @@ template <> struct Elem<u16> {
   }
   __device__ static __forceinline__ void store4(u16* p, f4 v) {
     uint2 u;
-    u.x = (uint32_t)f32_to_bf16(v[0]) | ((uint32_t)f32_to_bf16(v[1]) << 16);
-    u.y = (uint32_t)f32_to_bf16(v[2]) | ((uint32_t)f32_to_bf16(v[3]) << 16);
+    u.x = f32x2_to_bf16x2(v[0], v[1]);
+    u.y = f32x2_to_bf16x2(v[2], v[3]);
     *reinterpret_cast<uint2*>(p) = u;
   }
 };

@@ -137,6 +137,51 @@ def test_conv_bwd_data(shape, masked, dtype):
     assert rel_l2(to_host(dx), ref) <= TOL[dtype]
 
 
+# bf16 outputs are rounded from the fp32 accumulator to nearest, ties to
+# even.  One live product per output (centre tap 1.5 on channel 0, every
+# other filter value zero) makes the accumulator exactly 1.5 * input, which
+# often lies halfway between two bf16 values; the expected bits come from
+# torch's CPU rounding.  The shapes reach the bf16 MFMA epilogue (unsplit and
+# through the split reduction) and the fp32-MFMA kernels' bf16 stores.
+ROUNDING_SHAPES = [(2, 16, 32, 32, 64), (2, 64, 16, 16, 64), (2, 64, 4, 4, 64), (3, 5, 5, 7, 8),
+                   (4, 64, 2, 2, 96)]
+
+
+@pytest.mark.parametrize("shape", ROUNDING_SHAPES)
+@pytest.mark.parametrize("pass_", ["fwd", "bwd_data"])
+def test_bf16_store_rounds_ties_to_even(shape, pass_):
+    n, c, h, w, k = shape
+    print_case("bf16_rounding", shape=shape, pass_=pass_)
+    # Forward: inputs x [n, c], filters [k, c]; data gradient: the same
+    # layer transposed (dy [n, k] in, dx [n, c] out), the live filter value
+    # on k = 0.
+    cin, cout = (c, k) if pass_ == "fwd" else (k, c)
+    src = synth.normal((n, cin, h, w), 3, synth.TID.IMAGES).astype(np.float32)
+    src_d = torch.from_numpy(src).to(torch.bfloat16).cuda()
+    wt = np.zeros((k, c, 3, 3), np.float32)
+    if pass_ == "fwd":
+        wt[:, 0, 1, 1] = 1.5
+    else:
+        wt[0, :, 1, 1] = 1.5
+    wd = torch.from_numpy(wt).to(torch.bfloat16).cuda()
+    d = sb.conv_desc(n, c, h, w, k, sb.SB_BF16)
+    out = torch.full((n, cout, h, w), float("nan"), dtype=torch.bfloat16, device="cuda")
+    if pass_ == "fwd":
+        ws = _ws(sb.sb_conv3x3_workspace_bytes(d, sb.SB_PASS_FWD))
+        sb.sb_conv3x3_fwd(d, src_d, wd, None, out, ws)
+    else:
+        ws = _ws(sb.sb_conv3x3_workspace_bytes(d, sb.SB_PASS_BWD_DATA))
+        sb.sb_conv3x3_bwd_data(d, src_d, wd, None, out, ws)
+    torch.cuda.synchronize()
+    exact = src_d.float().cpu()[:, :1] * 1.5                  # fp32-exact products
+    expect = exact.to(torch.bfloat16).expand(n, cout, h, w)
+    got = out.cpu()
+    assert torch.equal(got.view(torch.int16), expect.contiguous().view(torch.int16))
+    # The case really has ties (rounding up and down both occur).
+    halfway = (exact.view(torch.int32) & 0xFFFF) == 0x8000
+    assert int(halfway.sum()) > 0
+
+
 @pytest.mark.parametrize("dtype", DTYPES)
 @pytest.mark.parametrize("shape", CONV_SHAPES)
 def test_conv_bwd_weight(shape, dtype):
