@@ -307,6 +307,43 @@ sb_status sb_shard_bwd(const sb_shard_desc *desc, int iproc,
                        const float *dfull, size_t df_stride, float *dparts,
                        size_t dp_stride, void *stream);
 
+/* ------------------------------------------------------------------------
+ * Loss and parameter update (NEXT after the worker's forward and backward).
+ *
+ * Log-softmax and negative log-likelihood on the complete model output
+ * (sec. 3.1 Layer Partitioning: when the last FC layer is partitioned, a
+ * shard layer before the LOG_SOFTMAX layer hands every worker the full
+ * output, so the output error is evaluated as for a complete local model).
+ * Per row i of the logits z [m][classes] (row stride ldz, fp32):
+ *   logp[i][c] = z[i][c] - log(sum_j exp(z[i][j]))
+ *   loss[i]    = -logp[i][labels[i]]
+ *   dz[i][c]   = scale * (exp(logp[i][c]) - [c == labels[i]])
+ * i.e. dz is the gradient of scale * sum_i loss[i] (scale = 1/m for the
+ * batch mean).  labels [m] are int32 device values; the kernel never
+ * indexes memory with them: a label outside [0, classes) gives loss[i] =
+ * NaN and a NaN row of dz.  logp, loss and dz may each be NULL (not
+ * written); logp and dz use row stride ldz.  Outputs must not overlap z or
+ * labels.  Sums run in a fixed order (bitwise reproducible).
+ * ---------------------------------------------------------------------- */
+sb_status sb_log_softmax_nll(int m, int classes, int ldz, const float *z,
+                             const int32_t *labels, float scale, float *logp,
+                             float *loss, float *dz, void *stream);
+
+/* Plain SGD step on `count` fp32 tensors (sec. 4: SGD on mini-batches;
+ * sec. 3.1 Modulo Layer: the FC layers, updated K times per local batch,
+ * divide their gradients by K):
+ *   w[t][i] = w[t][i] - (lr * scale[t]) * g[t][i],  i < n[t]
+ * with the product lr * scale[t] formed once (fp32) and one fused
+ * multiply-add per element.  w, g, n and scale are HOST arrays of `count`
+ * entries (1 <= count <= SB_SGD_MAX_TENSORS); w[t] and g[t] are device
+ * pointers, n[t] may be 0 (nothing to do; pointers may then be NULL).  A
+ * gradient must not overlap any parameter tensor of the call, and the
+ * parameter tensors must not overlap each other. */
+enum { SB_SGD_MAX_TENSORS = 64 };
+sb_status sb_sgd_update(int count, float *const *w, const float *const *g,
+                        const size_t *n, const float *scale, float lr,
+                        void *stream);
+
 #ifdef __cplusplus
 }
 #endif

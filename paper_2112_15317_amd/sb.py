@@ -25,6 +25,7 @@ SB_FUSE_RELU = 1
 SB_PACKED_FILTERS = 2
 SB_PASS_FWD, SB_PASS_BWD_DATA, SB_PASS_BWD_WEIGHT = 0, 1, 2
 SB_FC_FWD, SB_FC_BWD = 0, 1
+SB_SGD_MAX_TENSORS = 64
 
 _vp = ctypes.c_void_p
 _i = ctypes.c_int
@@ -73,6 +74,9 @@ SIGNATURES = {
     "sb_modulo_bwd": (_i, [ctypes.POINTER(sb_modulo_desc), _i, _i, _vp, _sz, _vp, _sz, _vp]),
     "sb_shard_fwd": (_i, [ctypes.POINTER(sb_shard_desc), _i, _vp, _sz, _vp, _vp]),
     "sb_shard_bwd": (_i, [ctypes.POINTER(sb_shard_desc), _i, _vp, _sz, _vp, _sz, _vp]),
+    "sb_log_softmax_nll": (_i, [_i, _i, _i, _vp, _vp, ctypes.c_float, _vp, _vp, _vp, _vp]),
+    "sb_sgd_update": (_i, [_i, ctypes.POINTER(_vp), ctypes.POINTER(_vp), ctypes.POINTER(_sz),
+                           ctypes.POINTER(ctypes.c_float), ctypes.c_float, _vp]),
 }
 
 _lock = threading.Lock()
@@ -301,3 +305,37 @@ def sb_shard_bwd(desc, iproc, dfull, dparts, df_stride=None, dp_stride=None, str
         ctypes.byref(desc), int(iproc), _ptr(dfull),
         _slot_stride(dfull, desc.workers, df_stride), _ptr(dparts),
         _slot_stride(dparts, desc.workers, dp_stride), _stream(stream)))
+
+
+# --------------------------------------------------- loss and SGD update --
+def sb_log_softmax_nll(m, classes, z, labels, scale, logp=None, loss=None, dz=None, ldz=None,
+                       stream=None):
+    """z, logp, dz: fp32 [m][ldz] (ldz defaults to classes); labels: int32 [m]."""
+    _check("sb_log_softmax_nll", load().sb_log_softmax_nll(
+        int(m), int(classes), int(ldz or classes), _ptr(z), _ptr(labels), float(scale),
+        _ptr(logp), _ptr(loss), _ptr(dz), _stream(stream)))
+
+
+class SgdList:
+    """Marshalled arguments of sb_sgd_update for a fixed list of
+    (parameter, gradient, scale) fp32 tensors: built once, passed to every
+    call (the tensors must stay alive)."""
+
+    def __init__(self, items):
+        import torch
+        n = len(items)
+        if not 1 <= n <= SB_SGD_MAX_TENSORS:
+            raise ValueError("1 to %d tensors per update" % SB_SGD_MAX_TENSORS)
+        for w, g, _ in items:
+            if w.dtype != torch.float32 or g.dtype != torch.float32 or w.numel() != g.numel():
+                raise ValueError("fp32 parameter and gradient of equal size")
+        self.count = n
+        self.w = (_vp * n)(*[_ptr(w) for w, _, _ in items])
+        self.g = (_vp * n)(*[_ptr(g) for _, g, _ in items])
+        self.n = (_sz * n)(*[w.numel() for w, _, _ in items])
+        self.scale = (ctypes.c_float * n)(*[float(sc) for _, _, sc in items])
+
+
+def sb_sgd_update(slist, lr, stream=None):
+    _check("sb_sgd_update", load().sb_sgd_update(
+        slist.count, slist.w, slist.g, slist.n, slist.scale, float(lr), _stream(stream)))

@@ -195,3 +195,39 @@ def test_modulo_and_shard_argument_validation():
     assert _raw("sb_shard_bwd", s, 0, P, 80, P + (1 << 24), 39, None) == E
     assert _raw("sb_shard_fwd", s, 0, P, 40, P + 100, None) == E               # overlap
     assert _raw("sb_shard_bwd", s, 2, P, 80, P + 2 * 80 * 4 + 8, 40, None) == E
+
+
+def test_loss_and_sgd_argument_validation():
+    f = ctypes.c_float
+    # Bad sizes, null logits or labels, non-finite scale, too small row stride.
+    assert _raw("sb_log_softmax_nll", -1, 10, 10, P, P + 4096, f(1.0), None, None, None, None) == sb.SB_ERR_INVALID_ARG
+    assert _raw("sb_log_softmax_nll", 4, 0, 10, P, P + 4096, f(1.0), None, None, None, None) == sb.SB_ERR_INVALID_ARG
+    assert _raw("sb_log_softmax_nll", 4, 10, 9, P, P + 4096, f(1.0), None, None, None, None) == sb.SB_ERR_INVALID_ARG
+    assert _raw("sb_log_softmax_nll", 4, 10, 10, None, P + 4096, f(1.0), None, None, None, None) == sb.SB_ERR_INVALID_ARG
+    assert _raw("sb_log_softmax_nll", 4, 10, 10, P, None, f(1.0), None, None, None, None) == sb.SB_ERR_INVALID_ARG
+    assert _raw("sb_log_softmax_nll", 4, 10, 10, P, P + 4096, f(float("nan")), None, None, None, None) == sb.SB_ERR_INVALID_ARG
+    # Outputs overlapping the logits, the labels or each other.
+    assert _raw("sb_log_softmax_nll", 4, 10, 10, P, P + 4096, f(1.0), P + 8, None, None, None) == sb.SB_ERR_INVALID_ARG
+    assert _raw("sb_log_softmax_nll", 4, 10, 10, P, P + 4096, f(1.0), None, P + 4100, None, None) == sb.SB_ERR_INVALID_ARG
+    assert _raw("sb_log_softmax_nll", 4, 10, 10, P, P + 4096, f(1.0), P + 8192, None, P + 8200, None) == sb.SB_ERR_INVALID_ARG
+    # No rows: nothing to do.
+    assert _raw("sb_log_softmax_nll", 0, 10, 10, P, None, f(1.0), None, None, None, None) == sb.SB_OK
+
+    def sgd(ws, gs, ns, scales, lr=0.1, count=None):
+        n = len(ws)
+        return _raw("sb_sgd_update", n if count is None else count,
+                    (ctypes.c_void_p * max(n, 1))(*ws), (ctypes.c_void_p * max(n, 1))(*gs),
+                    (ctypes.c_size_t * max(n, 1))(*ns), (ctypes.c_float * max(n, 1))(*scales),
+                    f(lr), None)
+    assert sgd([P], [P + 4096], [16], [1.0], count=0) == sb.SB_ERR_INVALID_ARG
+    assert sgd([P], [P + 4096], [16], [1.0], count=sb.SB_SGD_MAX_TENSORS + 1) == sb.SB_ERR_INVALID_ARG
+    assert sgd([None], [P + 4096], [16], [1.0]) == sb.SB_ERR_INVALID_ARG
+    assert sgd([P], [None], [16], [1.0]) == sb.SB_ERR_INVALID_ARG
+    assert sgd([P], [P + 4096], [16], [float("inf")]) == sb.SB_ERR_INVALID_ARG
+    assert sgd([P], [P + 4096], [16], [1.0], lr=float("nan")) == sb.SB_ERR_INVALID_ARG
+    # A gradient overlapping a parameter (its own or another's); parameters overlapping.
+    assert sgd([P], [P + 32], [16], [1.0]) == sb.SB_ERR_INVALID_ARG
+    assert sgd([P, P + 4096], [P + 8192, P + 4100], [16, 16], [1.0, 1.0]) == sb.SB_ERR_INVALID_ARG
+    assert sgd([P, P + 32], [P + 8192, P + 12288], [16, 16], [1.0, 1.0]) == sb.SB_ERR_INVALID_ARG
+    # Only empty tensors: nothing to do.
+    assert sgd([None], [None], [0], [1.0]) == sb.SB_OK
