@@ -68,6 +68,7 @@ if ROOT not in sys.path:
 PEAK_MFMA_TFLOPS = {"f32": 157.3, "bf16": 2500.0}
 PEAK_HBM_GBS = 8000.0
 COPY_MIB = 256
+TRAIN_LR = 0.01                                # SGD rate of the training-step workload
 
 CIFAR_METRIC = "images/sec/GPU VGG-CIFAR conv fwd+bwd; achieved TFLOP/s vs MFMA peak"
 FC_SHAPE = (512, 4096, 1024, 4096)            # gathered rows, k_in, shard columns, full columns
@@ -177,6 +178,14 @@ def hybrid_inputs(n, schedule, fc_shapes, group):
     return layers, x, ws, bs, fw, fb, rows, cols, dy
 
 
+def train_targets(n, fc_shapes, group):
+    """Labels of the gathered rows and the other shards' logit columns."""
+    from paper_2112_15317_amd import synth
+    m, classes = n * group, fc_shapes[-1][1]
+    return (synth.labels(m, classes, 0, synth.TID.LABELS),
+            synth.normal((m, classes - classes // group), 0, synth.TID.LOGITS_REMOTE))
+
+
 # --------------------------------------------------------------- workloads --
 class Workload:
     """What a benchmark run needs: the step's calls, its work, its baseline."""
@@ -282,18 +291,29 @@ class HybridWorkload(Workload):
     dtype = "f32"
     images = 128
 
-    def __init__(self, name, schedule, fc_shapes, group, metric, text):
+    def __init__(self, name, schedule, fc_shapes, group, metric, text, train=False):
         self.name, self.schedule, self.fc_shapes, self.group = name, schedule, fc_shapes, group
-        self.metric, self.text = metric, text
+        self.metric, self.text, self.train = metric, text, train
 
     def build(self):
         from paper_2112_15317_amd.stack import HybridStep
         inp = hybrid_inputs(self.images, self.schedule, self.fc_shapes, self.group)
         self.layers = inp[0]
         self.hs = HybridStep(self.schedule, self.images, 3, 32, self.group, self.fc_shapes,
-                             self.group)
+                             self.group, train=self.train, lr=TRAIN_LR)
         self.hs.load_inputs(*inp[1:])
+        if self.train:
+            self.hs.load_targets(*train_targets(self.images, self.fc_shapes, self.group))
         return self.hs.step_calls()
+
+    def call_bytes(self, kind):
+        hs = self.hs
+        if kind == "loss":           # logits read, gradient written, labels and losses
+            return 2 * hs.m * hs.classes * 4 + 2 * hs.m * 4
+        # sgd: each parameter read and written, its gradient read
+        n = sum(w.numel() for w in hs.conv.W + hs.conv.b) + sum(
+            f.W.numel() + f.b.numel() for f in hs.fc)
+        return 12 * n
 
     def flops(self):
         from paper_2112_15317_amd import configs
@@ -309,13 +329,18 @@ class HybridWorkload(Workload):
         layers, x, ws, bs, fw, fb, rows, cols, dy = hybrid_inputs(
             n, self.schedule, self.fc_shapes, self.group)
         pools = [L.pool_after for L in layers]
+        train = None
+        if self.train:
+            labels, logits_remote = train_targets(n, self.fc_shapes, self.group)
+            train = {"labels": labels, "logits_remote": logits_remote, "lr": TRAIN_LR,
+                     "shards": self.group}
         t0 = time.perf_counter()
-        OS.hybrid_step(x, ws, bs, pools, fw, fb, rows, cols, dy)
+        OS.hybrid_step(x, ws, bs, pools, fw, fb, rows, cols, dy, train=train)
         dt = time.perf_counter() - t0
         return {"value": round(n / dt, 3), "unit": "images/s",
                 "cores": oracle.num_threads(), "kind": "oracle",
-                "sample": "1 x the whole hybrid step, %d local images (fp64 oracle), %.1f s"
-                          % (n, dt)}
+                "sample": "1 x the whole %s step, %d local images (fp64 oracle), %.1f s"
+                          % ("training" if self.train else "hybrid", n, dt)}
 
 
 class ExchangeWorkload(Workload):
@@ -413,11 +438,13 @@ def workloads():
             "rows, fwd+bwd, fp32"),
         "paper-variant-f32": HybridWorkload(
             "paper-variant-f32", configs.PAPER_VARIANT_CONV, configs.PAPER_VARIANT_FC, 2,
-            "images/sec/GPU hybrid worker step of the paper's VGG variant (Table 1), fp32",
+            "images/sec/GPU training step of the paper's VGG variant (Table 1), one worker, "
+            "fp32",
             "the paper's VGG variant as one worker of an MP group of 2: seven 3x3 convs "
             "(64,64,M,128,128,M,256,256,256,M) on 128 local 3x32x32 images, then FC "
-            "4096->1024->1024->10 split in 2 column shards on the gathered 256 rows, fwd+bwd, "
-            "fp32"),
+            "4096->1024->1024->10 split in 2 column shards on the gathered 256 rows; fwd, "
+            "log-softmax + NLL of the 10-class logits, bwd, SGD (conv at lr, FC shards at "
+            "lr/2), fp32", train=True),
         "exchange-f32": ExchangeWorkload(),
     }
 
@@ -439,6 +466,10 @@ def kernel_name(key, call_args, dtype):
     if kind in ("mfwd", "mbwd", "sfwd", "sbwd"):
         return "sb::%s_%s_kernel<4>" % ("modulo" if kind[0] == "m" else "shard",
                                         "fwd" if kind[1:] == "fwd" else "bwd")
+    if kind == "loss":
+        return "sb::log_softmax_nll_kernel"
+    if kind == "sgd":
+        return "sb::sgd_update_kernel"
     return "sb::relu_maxpool_%s_kernel<%s, 2>" % (
         kind.split("_")[1], "float" if dtype == "f32" else "unsigned short")
 
@@ -450,7 +481,7 @@ def call_work(wl, key, args):
         return layer_flops(wl.layers[i], args[0].n)[0], "flop"
     if kind.startswith("fc_"):
         return fc_flops(args[0], kind, kind == "fc_fwd" or args[5] is not None), "flop"
-    if kind in ("mfwd", "mbwd", "sfwd", "sbwd"):
+    if kind in ("mfwd", "mbwd", "sfwd", "sbwd", "loss", "sgd"):
         return wl.call_bytes(kind), "bytes"
     esize = 4 if wl.dtype == "f32" else 2
     if kind == "pack":             # every layer's filters read, twice packed written

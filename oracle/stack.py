@@ -22,6 +22,7 @@ import numpy as np
 
 from . import (_f64, conv3x3_bwd_data, conv3x3_bwd_weight, conv3x3_fwd,
                fc_bwd, fc_fwd, relu_maxpool_bwd, relu_maxpool_fwd, round_bf16)
+from .train import log_softmax_nll, sgd_update
 
 
 def _identity(a):
@@ -80,8 +81,18 @@ def vgg_step(x, weights, biases, pool_after, dy_top, bf16=False, want_dx=True):
     return f, b
 
 
-def hybrid_step(x, weights, biases, pool_after, fc_w, fc_b, rows_remote, cols_remote, dy):
+def hybrid_step(x, weights, biases, pool_after, fc_w, fc_b, rows_remote, cols_remote, dy,
+                train=None):
     """One worker's step of the hybrid scheme on one device, with L FC shards.
+
+    ``train`` (a dict with ``labels``, ``logits_remote``, ``lr``, ``shards``)
+    makes it a whole training step: the last shard's output and the other
+    shards' columns ``logits_remote`` form the full logits (the shard layer
+    before the LOG_SOFTMAX layer, sec. 3.1), whose log-softmax + NLL over the
+    gathered rows (batch mean) gives the last shard's output gradient in
+    place of ``dy``; after the backward, SGD at rate ``lr`` updates the conv
+    parameters and, with the gradient divided by ``shards`` (the paper's K,
+    sec. 3.1 Modulo Layer), the FC shards.
 
     The local conv stack output (flattened, one row per image, NCHW order)
     fills the first rows of the gathered FC0 input; ``rows_remote`` supplies
@@ -108,7 +119,13 @@ def hybrid_step(x, weights, biases, pool_after, fc_w, fc_b, rows_remote, cols_re
         if j < L - 1:
             xs.append(np.concatenate([y, np.asarray(cols_remote[j], np.float64)], axis=1))
     dxp, dw, db, dys = [None] * L, [None] * L, [None] * L, [None] * L
-    g = np.asarray(dy, np.float64)
+    loss = dz = None
+    if train is not None:
+        z = np.concatenate([ys[-1], np.asarray(train["logits_remote"], np.float64)], axis=1)
+        _, loss, dz = log_softmax_nll(z, train["labels"], 1.0 / z.shape[0])
+        g = np.ascontiguousarray(dz[:, :ys[-1].shape[1]])
+    else:
+        g = np.asarray(dy, np.float64)
     for j in reversed(range(L)):
         dys[j] = g
         dxp[j], dw[j], db[j] = fc_bwd(xs[j], fc_w[j], g,
@@ -117,4 +134,12 @@ def hybrid_step(x, weights, biases, pool_after, fc_w, fc_b, rows_remote, cols_re
             g = np.ascontiguousarray(dxp[j][:, :ys[j - 1].shape[1]])
     dtop = np.ascontiguousarray(dxp[0][:n]).reshape(top.shape)
     b = vgg_backward(f, weights, pool_after, dtop)
-    return {"fwd": f, "bwd": b, "xs": xs, "ys": ys, "dys": dys, "dxp": dxp, "dw": dw, "db": db}
+    out = {"fwd": f, "bwd": b, "xs": xs, "ys": ys, "dys": dys, "dxp": dxp, "dw": dw, "db": db}
+    if train is not None:
+        lr, k = train["lr"], 1.0 / train["shards"]
+        out.update(loss=loss, dz=dz,
+                   conv_w_new=[sgd_update(w, b["dW"][i], lr, 1.0) for i, w in enumerate(weights)],
+                   conv_b_new=[sgd_update(bb, b["db"][i], lr, 1.0) for i, bb in enumerate(biases)],
+                   fc_w_new=[sgd_update(w, dw[j], lr, k) for j, w in enumerate(fc_w)],
+                   fc_b_new=[sgd_update(bb, db[j], lr, k) for j, bb in enumerate(fc_b)])
+    return out

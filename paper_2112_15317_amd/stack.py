@@ -254,7 +254,17 @@ class HybridStep:
     collectives, not part of this step.
     """
 
-    def __init__(self, schedule, n, in_ch, hw, replicas, fc_shapes, shards, device="cuda"):
+    def __init__(self, schedule, n, in_ch, hw, replicas, fc_shapes, shards, device="cuda",
+                 train=False, lr=0.01):
+        """train: a whole training step.  The last shard writes its columns of
+        the full logits Zl [m, classes] (the shard layer before the
+        LOG_SOFTMAX layer; the other shards' columns are stand-ins), the
+        log-softmax + NLL of the gathered rows (batch mean) gives the
+        gradient of the last shard's output, and after the backward one SGD
+        step at rate lr updates the conv parameters and, with the gradient
+        divided by the number of shards K, the FC shards (sec. 3.1, Modulo
+        Layer).  Otherwise the last shard's output Y takes a given gradient
+        dY and nothing is updated."""
         dev = torch.device(device)
         self.n, self.R = n, replicas
         m = n * replicas
@@ -266,16 +276,34 @@ class HybridStep:
         f32 = dict(dtype=torch.float32, device=dev)
         self.X = [torch.empty((m, fi), **f32) for fi in self.ins]
         self.dXp = [torch.empty((m, fi), **f32) for fi in self.ins]
-        self.Y = torch.empty((m, self.ns[-1]), **f32)
-        self.dY = torch.empty((m, self.ns[-1]), **f32)
+        self.train, self.lr, self.shards = train, lr, shards
+        self.classes = fc_shapes[-1][1]
+        if train:
+            self.Zl = torch.empty((m, self.classes), **f32)
+            self.dZl = torch.empty((m, self.classes), **f32)
+            self.labels = torch.zeros((m,), dtype=torch.int32, device=dev)
+            self.loss = torch.empty((m,), **f32)
+            out_last, ld_last = self.Zl, self.classes
+        else:
+            self.Y = torch.empty((m, self.ns[-1]), **f32)
+            self.dY = torch.empty((m, self.ns[-1]), **f32)
+            out_last, ld_last = self.Y, self.ns[-1]
+        self.out_last, self.dout_last = out_last, (self.dZl if train else self.dY)
         self.conv = ConvStack(schedule, n, in_ch, hw, "f32", device,
                               out_buffer=self.X[0][:n], out_grad_buffer=self.dXp[0][:n])
         top = self.conv.A[-1]
         assert int(np.prod(top.shape[1:])) == self.ins[0]
         last = self.L - 1
         self.fc = [FCShard(m, self.ins[j], self.ns[j], relu=j < last, ldx=self.ins[j],
-                           ldy=self.ins[j + 1] if j < last else self.ns[j], device=device)
+                           ldy=self.ins[j + 1] if j < last else ld_last, device=device)
                    for j in range(self.L)]
+        if train:
+            c = self.conv
+            self.sgd = sb.SgdList(
+                [(c.W[i], c.dW[i], 1.0) for i in range(len(c.layers))] +
+                [(c.b[i], c.db[i], 1.0) for i in range(len(c.layers))] +
+                [(f.W, f.dW, 1.0 / shards) for f in self.fc] +
+                [(f.b, f.db, 1.0 / shards) for f in self.fc])
         self.call = _plain      # hook: every libsb call of the step goes through it
 
     # Two-layer names used by the tests of the four-replica worker step.
@@ -299,7 +327,15 @@ class HybridStep:
         self.X[0][self.n:].copy_(t(rows_remote))
         for j in range(1, self.L):
             self.X[j][:, self.ns[j - 1]:].copy_(t(cols_remote[j - 1]))
-        self.dY.copy_(t(dy))
+        if not self.train:
+            self.dY.copy_(t(dy))
+
+    def load_targets(self, labels, logits_remote):
+        """Training step: the labels of the gathered rows and the other
+        shards' columns of the last FC output."""
+        self.labels.copy_(torch.from_numpy(np.ascontiguousarray(labels, dtype=np.int32)))
+        self.Zl[:, self.ns[-1]:].copy_(
+            torch.from_numpy(np.ascontiguousarray(logits_remote, dtype=np.float32)))
 
     def step(self, stream=None):
         def c(key, call):
@@ -309,17 +345,23 @@ class HybridStep:
         L = self.L
         X = [x.data_ptr() for x in self.X]
         for j in range(L):
-            out = X[j + 1] if j + 1 < L else self.Y.data_ptr()
+            out = X[j + 1] if j + 1 < L else self.out_last.data_ptr()
             c(("fc_fwd", j), self.fc[j].fwd_call(X[j], out, stream))
+        if self.train:
+            self.call(("loss", 0), sb.sb_log_softmax_nll, self.m, self.classes, self.Zl,
+                      self.labels, 1.0 / self.m, None, self.loss, self.dZl, self.classes, stream)
         for j in reversed(range(L)):
-            # Output gradient of layer j: the given dY, or layer j+1's partial
-            # input gradient on this shard's columns (row stride in_{j+1}),
-            # masked by layer j's ReLU output X[j+1][:, :ns_j].
-            dy = self.dY.data_ptr() if j == L - 1 else self.dXp[j + 1].data_ptr()
+            # Output gradient of layer j: the last layer's (given, or from the
+            # loss), or layer j+1's partial input gradient on this shard's
+            # columns (row stride in_{j+1}), masked by layer j's ReLU output
+            # X[j+1][:, :ns_j].
+            dy = self.dout_last.data_ptr() if j == L - 1 else self.dXp[j + 1].data_ptr()
             mask = None if j == L - 1 else X[j + 1]
             c(("fc_bwd", j), self.fc[j].bwd_call(X[j], dy, mask, self.dXp[j].data_ptr(),
                                                  stream=stream))
         self.conv.backward(stream)
+        if self.train:
+            self.call(("sgd", 0), sb.sb_sgd_update, self.sgd, self.lr, stream)
 
     def step_calls(self):
         """The ordered (key, libsb function, args) calls of one step."""

@@ -37,6 +37,8 @@ class TID:
     X0_REMOTE = 500       # gathered rows of the other replicas (FC0 input)
     X1_REMOTE = 501       # feature columns of the other shards (FC1 input)
     FC_DY = 502           # upstream gradient of the last FC shard
+    LABELS = 503          # class labels of the gathered rows
+    LOGITS_REMOTE = 504   # the other shards' columns of the last FC output
     FC_X = 600            # standalone FC-shard input
     COLS_REMOTE = 700     # + FC layer index (>= 2): other shards' columns of its input
     MISC = 900            # + anything a test needs
@@ -68,6 +70,11 @@ def xavier_uniform(fan_in: int, fan_out: int, seed: int, tensor_id: int) -> np.n
     a = math.sqrt(6.0 / (fan_in + fan_out))
     g = generator(seed, tensor_id)
     return g.uniform(-a, a, size=(fan_in, fan_out)).astype(np.float32)
+
+
+def labels(m: int, classes: int, seed: int, tensor_id: int) -> np.ndarray:
+    """int32 array of m class labels ~ U{0, ..., classes - 1}."""
+    return generator(seed, tensor_id).integers(0, classes, size=m).astype(np.int32)
 
 
 def zeros(shape) -> np.ndarray:

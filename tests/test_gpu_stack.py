@@ -332,6 +332,44 @@ def test_paper_variant_hybrid_step_end_to_end():
     _check_hybrid(hs, r, layers)
 
 
+def test_paper_variant_training_step_end_to_end():
+    """The paper's VGG variant as a whole training step of one worker of an
+    MP group of 2: the log-softmax + NLL of the full 10-class logits (this
+    shard's 5 columns and a stand-in for the other shard's) gives the
+    gradient of the last shard, and one SGD step updates the conv layers at
+    rate lr and the FC shards at lr / K."""
+    n, hw, R, S, lr = 3, 32, 2, 2, 0.05
+    print_case("paper_variant_training_step", n=n, replicas=R, shards=S)
+    fc_shapes = configs.PAPER_VARIANT_FC
+    layers, x, wts, bs, fw, fb, rows, cols, _ = _hybrid_inputs(
+        n, hw, R, S, configs.PAPER_VARIANT_CONV, fc_shapes, 9)
+    m, classes, ns = n * R, fc_shapes[-1][1], fc_shapes[-1][1] // S
+    labels = synth.labels(m, classes, 9, synth.TID.LABELS)
+    logits_remote = synth.normal((m, classes - ns), 9, synth.TID.LOGITS_REMOTE)
+    hs = HybridStep(configs.PAPER_VARIANT_CONV, n, 3, hw, R, fc_shapes, S, train=True, lr=lr)
+    hs.load_inputs(x, wts, bs, fw, fb, rows, cols, None)
+    hs.load_targets(labels, logits_remote)
+    hs.step()
+    torch.cuda.synchronize()
+    pools = [L.pool_after for L in layers]
+    r = OS.hybrid_step(x, wts, bs, pools, fw, fb, rows, cols, None,
+                       train={"labels": labels, "logits_remote": logits_remote, "lr": lr,
+                              "shards": S})
+    tol = TOL["f32"]
+    assert rel_l2(to_host(hs.loss), r["loss"]) <= tol
+    assert rel_l2(to_host(hs.dZl)[:, :ns], r["dz"][:, :ns]) <= tol
+    for j in range(hs.L):
+        assert rel_l2(to_host(hs.fc[j].dW), r["dw"][j]) <= tol, "dW_fc%d" % j
+        # The update itself (new minus old parameters): lr / K times the gradient.
+        assert rel_l2(to_host(hs.fc[j].W) - fw[j], r["fc_w_new"][j] - fw[j]) <= tol, "W_fc%d" % j
+        assert rel_l2(to_host(hs.fc[j].b) - fb[j], r["fc_b_new"][j] - fb[j]) <= tol, "b_fc%d" % j
+    for L in layers:
+        i = L.index
+        assert rel_l2(to_host(hs.conv.dW[i]), r["bwd"]["dW"][i]) <= tol, "dW%d" % i
+        assert rel_l2(to_host(hs.conv.W[i]) - wts[i], r["conv_w_new"][i] - wts[i]) <= tol, "W%d" % i
+        assert rel_l2(to_host(hs.conv.b[i]) - bs[i], r["conv_b_new"][i] - bs[i]) <= tol, "b%d" % i
+
+
 def test_graph_replay_matches_eager():
     """The benchmark replays the step from a captured HIP graph: every replay,
     with eager work and synchronisations in between, must reproduce the eager
