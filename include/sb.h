@@ -204,7 +204,11 @@ sb_status sb_relu_maxpool_bwd(int n, int c, int h, int w, int dtype,
  * ---------------------------------------------------------------------- */
 typedef struct {
     int m, k_in, n_shard;  /* gathered rows, input features, shard columns */
-    int dtype;             /* sb_dtype (SB_F32 in this build)              */
+    int dtype;             /* sb_dtype: SB_F32, or SB_BF16 (x, w_shard, y,
+                              dy, relu_mask_src, dx_partial bfloat16; b_shard,
+                              dw_shard, db_shard fp32; products on fp32 MFMA
+                              from the exactly widened values, y and
+                              dx_partial rounded to nearest-even)          */
     int ldx;               /* row stride of x and dx_partial (>= k_in)     */
     int ldy;               /* row stride of y, dy, relu_mask_src (>= n_shard) */
     unsigned flags;        /* SB_FUSE_RELU (forward only)                  */

@@ -8,6 +8,11 @@
 //             db  = (db +) column sums of G     [ns]
 // with G = dY, or dY * [mask > 0] (ReLU of this shard's output).
 //
+// SB_BF16: x, w_shard, y, dy, the ReLU mask and dx_partial are bfloat16;
+// the kernel widens them exactly to fp32 as it stages them (so the products
+// and sums are the fp32 path's, on the same fp32 MFMA) and rounds y and
+// dx_partial to nearest-even on store; dW and db stay fp32.
+//
 // One fp32 MFMA GEMM kernel serves the three products.  Block tile
 // 128 x 128 x 32, four waves of 64 x 64 (4 x 4 MFMA 16x16 blocks).  Each
 // operand keeps the layout it has in memory when it is staged in LDS:
@@ -36,12 +41,14 @@ constexpr int RR = GBM + 4;            // [k][row] k stride (floats); 4 * RR = 1
 constexpr int OPSZ = GBM * RK > GBK * RR ? GBM * RK : GBK * RR;   // floats per operand buffer
 constexpr size_t GEMM_LDS_BYTES = 2 * 2 * OPSZ * sizeof(float);    // 2 operands x 2 buffers
 
+// Operands and masks hold elements of the GEMM's operand type E (float or
+// bf16 bits), C elements of its output type (or fp32 split partials).
 struct GemmArgs {
-  const float* a; int lda;             // A element (m,k): A_KC ? a[m*lda+k] : a[k*lda+m]
-  const float* amask;                  // optional mask, same layout/stride as a
-  const float* b; int ldb;             // B element (k,n): B_KC ? b[n*ldb+k] : b[k*ldb+n]
-  const float* bmask;
-  float* c; int ldc;                   // C[m*ldc + n]
+  const void* a; int lda;              // A element (m,k): A_KC ? a[m*lda+k] : a[k*lda+m]
+  const void* amask;                   // optional mask, same layout/stride as a
+  const void* b; int ldb;              // B element (k,n): B_KC ? b[n*ldb+k] : b[k*ldb+n]
+  const void* bmask;
+  void* c; int ldc;                    // C[m*ldc + n]
   int M, N, K;
   int k_per_split;
 };
@@ -50,9 +57,9 @@ struct GemmArgs {
 // thread.  K-contiguous: group g = (k quad q = g / 128, row r = g % 128), the
 // 4 elements are 4 consecutive k of row r.  Row-contiguous: group g = (k =
 // g / 32, row quad = g % 32), the 4 elements are 4 consecutive rows.  VEC
-// loads each group with one 16-byte load (aligned, whole groups in range);
-// otherwise element by element.
-template <bool KC, bool VEC>
+// loads each group with one vector load (aligned, whole groups in range);
+// otherwise element by element.  Elements of type E, widened to fp32.
+template <bool KC, bool VEC, class E>
 struct OpStage {
   f4 v[4];
   __device__ __forceinline__ void load(rsrc_t r, rsrc_t rm, bool masked, int ld, int rows,
@@ -65,17 +72,19 @@ struct OpStage {
       f4 x, m = f4{1.f, 1.f, 1.f, 1.f};
       if (VEC) {
         const bool ok = row < rows && k < ke;       // whole group in range
-        const uint32_t off = ok ? (uint32_t)(KC ? row * ld + k : k * ld + row) * 4u : kOOB;
-        x = BufLoad<float>::four(r, off);
-        if (masked) m = BufLoad<float>::four(rm, off);
+        const uint32_t off =
+            ok ? (uint32_t)(KC ? row * ld + k : k * ld + row) * (uint32_t)sizeof(E) : kOOB;
+        x = BufLoad<E>::four(r, off);
+        if (masked) m = BufLoad<E>::four(rm, off);
       } else {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int rr = KC ? row : row + e, kk = KC ? k + e : k;
           const bool ok = rr < rows && kk < ke;
-          const uint32_t off = ok ? (uint32_t)(KC ? rr * ld + kk : kk * ld + rr) * 4u : kOOB;
-          x[e] = BufLoad<float>::one(r, off);
-          if (masked) m[e] = BufLoad<float>::one(rm, off);
+          const uint32_t off =
+              ok ? (uint32_t)(KC ? rr * ld + kk : kk * ld + rr) * (uint32_t)sizeof(E) : kOOB;
+          x[e] = BufLoad<E>::one(r, off);
+          if (masked) m[e] = BufLoad<E>::one(rm, off);
         }
       }
       if (masked) {
@@ -112,7 +121,7 @@ __device__ __forceinline__ void frag16(const float* S, int row0, int s, int kq, 
   }
 }
 
-template <bool A_KC, bool B_KC, bool VEC>
+template <bool A_KC, bool B_KC, bool VEC, class E, class CE>
 __global__ __launch_bounds__(256, 2) void gemm_f32(GemmArgs g, int partial,
                                                    const float* __restrict__ bias, int relu,
                                                    int accumulate) {
@@ -126,10 +135,10 @@ __global__ __launch_bounds__(256, 2) void gemm_f32(GemmArgs g, int partial,
   // Whole operand tensors (the host keeps them below 2^31 bytes).
   const size_t a_elems = A_KC ? (size_t)(g.M - 1) * g.lda + g.K : (size_t)(g.K - 1) * g.lda + g.M;
   const size_t b_elems = B_KC ? (size_t)(g.N - 1) * g.ldb + g.K : (size_t)(g.K - 1) * g.ldb + g.N;
-  const rsrc_t ra = make_rsrc(g.a, (uint32_t)(a_elems * 4));
-  const rsrc_t rb = make_rsrc(g.b, (uint32_t)(b_elems * 4));
-  const rsrc_t ram = make_rsrc(g.amask ? g.amask : g.a, (uint32_t)(a_elems * 4));
-  const rsrc_t rbm = make_rsrc(g.bmask ? g.bmask : g.b, (uint32_t)(b_elems * 4));
+  const rsrc_t ra = make_rsrc(g.a, (uint32_t)(a_elems * sizeof(E)));
+  const rsrc_t rb = make_rsrc(g.b, (uint32_t)(b_elems * sizeof(E)));
+  const rsrc_t ram = make_rsrc(g.amask ? g.amask : g.a, (uint32_t)(a_elems * sizeof(E)));
+  const rsrc_t rbm = make_rsrc(g.bmask ? g.bmask : g.b, (uint32_t)(b_elems * sizeof(E)));
   const bool amasked = g.amask != nullptr, bmasked = g.bmask != nullptr;
 
   f4 acc[4][4];
@@ -138,8 +147,8 @@ __global__ __launch_bounds__(256, 2) void gemm_f32(GemmArgs g, int partial,
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
 
-  OpStage<A_KC, VEC> sa;
-  OpStage<B_KC, VEC> sb_;
+  OpStage<A_KC, VEC, E> sa;
+  OpStage<B_KC, VEC, E> sb_;
   auto Abuf = [&](int b) { return lds + b * 2 * OPSZ; };
   auto Bbuf = [&](int b) { return lds + b * 2 * OPSZ + OPSZ; };
 
@@ -183,7 +192,9 @@ __global__ __launch_bounds__(256, 2) void gemm_f32(GemmArgs g, int partial,
   }
 
   // acc[i][n] lane holds C[m0 + wm*64 + i*16 + 4*kq + e][n0 + wn*64 + n*16 + lr].
-  float* dst = g.c + (partial ? (size_t)blockIdx.z * g.M * g.ldc : 0);
+  // Split partials are fp32 (one slab per split); otherwise C has type CE.
+  float* part = partial ? (float*)g.c + (size_t)blockIdx.z * g.M * g.ldc : nullptr;
+  CE* dst = (CE*)g.c;
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -196,19 +207,23 @@ __global__ __launch_bounds__(256, 2) void gemm_f32(GemmArgs g, int partial,
         if (col >= g.N) continue;
         float v = acc[i][n][e];
         size_t o = (size_t)m * g.ldc + col;
-        if (!partial) {
-          if (bias) v += bias[col];
-          if (relu && !(v > 0.f)) v = 0.f;
-          if (accumulate) v += dst[o];
+        if (partial) {
+          part[o] = v;
+          continue;
         }
-        dst[o] = v;
+        if (bias) v += bias[col];
+        if (relu && !(v > 0.f)) v = 0.f;
+        if (accumulate) v += Elem<CE>::load(dst, o);
+        Elem<CE>::store(dst, o, v);
       }
     }
 }
 
-// out[m, n] = epi(sum_s part[s][m][n]): + bias[n], ReLU, + out (accumulate).
+// out[m, n] = epi(sum_s part[s][m][n]): + bias[n], ReLU, + out (accumulate),
+// rounded to the output type CE.
+template <class CE>
 __global__ __launch_bounds__(256) void gemm_splitk_epilogue(
-    const float* __restrict__ part, int splits, int M, int N, int ldp, float* __restrict__ out,
+    const float* __restrict__ part, int splits, int M, int N, int ldp, CE* __restrict__ out,
     int ldo, const float* __restrict__ bias, int relu, int accumulate) {
   size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
   if (i >= (size_t)M * N) return;
@@ -218,15 +233,16 @@ __global__ __launch_bounds__(256) void gemm_splitk_epilogue(
   if (bias) v += bias[n];
   if (relu && !(v > 0.f)) v = 0.f;
   size_t o = (size_t)m * ldo + n;
-  if (accumulate) v += out[o];
-  out[o] = v;
+  if (accumulate) v += Elem<CE>::load(out, o);
+  Elem<CE>::store(out, o, v);
 }
 
 // db[j] = (db[j] +) sum_i G[i][j].  A block owns 64 columns; its 16 waves sum
 // every 16th row (four independent partial sums each, combined in a fixed
 // order), then the wave sums are added in order through LDS.
-__global__ __launch_bounds__(1024) void col_sum(const float* __restrict__ dy,
-                                                const float* __restrict__ mask, int M, int N,
+template <class E>
+__global__ __launch_bounds__(1024) void col_sum(const E* __restrict__ dy,
+                                                const E* __restrict__ mask, int M, int N,
                                                 int ld, float* __restrict__ db, int accumulate) {
   __shared__ float part[16][64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -236,8 +252,8 @@ __global__ __launch_bounds__(1024) void col_sum(const float* __restrict__ dy,
     int u = 0;
     for (int i = wave; i < M; i += 16, u = (u + 1) & 3) {
       const size_t o = (size_t)i * ld + j;
-      float v = dy[o];
-      if (mask && !(mask[o] > 0.f)) v = 0.f;
+      float v = Elem<E>::load(dy, o);
+      if (mask && !(Elem<E>::load(mask, o) > 0.f)) v = 0.f;
       s4[u] += v;
     }
   }
@@ -270,27 +286,30 @@ static GemmPlan gemm_plan(int M, int N, int K) {
   return p;
 }
 
+// 4-element groups load as one vector (16 bytes fp32, 8 bytes bf16).
+template <class E>
 static bool vec_ok(const void* p, int ld, int contiguous_extent) {
-  return ((uintptr_t)p & 15) == 0 && ld % 4 == 0 && contiguous_extent % 4 == 0;
+  return ((uintptr_t)p & (4 * sizeof(E) - 1)) == 0 && ld % 4 == 0 && contiguous_extent % 4 == 0;
 }
 
-template <bool AK, bool BK, bool VEC>
+template <bool AK, bool BK, bool VEC, class E, class CE>
 static void gemm_launch(const GemmPlan& p, const GemmArgs& g, int partial, const float* bias,
                         int relu, int accumulate, hipStream_t st) {
   static bool attr_set = false;
   if (!attr_set) {
-    (void)hipFuncSetAttribute((const void*)gemm_f32<AK, BK, VEC>,
+    (void)hipFuncSetAttribute((const void*)gemm_f32<AK, BK, VEC, E, CE>,
                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)GEMM_LDS_BYTES);
     attr_set = true;
   }
   dim3 grid(p.mt, p.nt, p.splits);
-  gemm_f32<AK, BK, VEC><<<grid, 256, GEMM_LDS_BYTES, st>>>(g, partial, bias, relu, accumulate);
+  gemm_f32<AK, BK, VEC, E, CE><<<grid, 256, GEMM_LDS_BYTES, st>>>(g, partial, bias, relu,
+                                                                   accumulate);
 }
 
 // C (ldc) = epi(A * B): the GEMM applies the epilogue itself when the
 // reduction is not split; otherwise it writes per-split partial sums to the
 // workspace and gemm_splitk_epilogue adds them in order and applies it.
-template <bool AK, bool BK>
+template <bool AK, bool BK, class E, class CE>
 static sb_status gemm_run(GemmArgs g, const float* bias, int relu, int accumulate, float* ws,
                           size_t ws_bytes, hipStream_t st) {
   GemmPlan p = gemm_plan(g.M, g.N, g.K);
@@ -298,22 +317,24 @@ static sb_status gemm_run(GemmArgs g, const float* bias, int relu, int accumulat
   // Buffer ranges cover whole operands.
   const int64_t a_elems = AK ? (int64_t)(g.M - 1) * g.lda + g.K : (int64_t)(g.K - 1) * g.lda + g.M;
   const int64_t b_elems = BK ? (int64_t)(g.N - 1) * g.ldb + g.K : (int64_t)(g.K - 1) * g.ldb + g.N;
-  if (a_elems * 4 >= (1ll << 31) || b_elems * 4 >= (1ll << 31)) return SB_ERR_UNSUPPORTED;
+  const int64_t es = (int64_t)sizeof(E);
+  if (a_elems * es >= (1ll << 31) || b_elems * es >= (1ll << 31)) return SB_ERR_UNSUPPORTED;
   g.k_per_split = p.kps;
-  const bool vec = vec_ok(g.a, g.lda, AK ? g.K : g.M) && vec_ok(g.b, g.ldb, BK ? g.K : g.N) &&
-                   (!g.amask || vec_ok(g.amask, g.lda, AK ? g.K : g.M)) &&
-                   (!g.bmask || vec_ok(g.bmask, g.ldb, BK ? g.K : g.N)) && p.kps % 4 == 0;
-  float* out = g.c;
+  const bool vec = vec_ok<E>(g.a, g.lda, AK ? g.K : g.M) &&
+                   vec_ok<E>(g.b, g.ldb, BK ? g.K : g.N) &&
+                   (!g.amask || vec_ok<E>(g.amask, g.lda, AK ? g.K : g.M)) &&
+                   (!g.bmask || vec_ok<E>(g.bmask, g.ldb, BK ? g.K : g.N)) && p.kps % 4 == 0;
+  CE* out = (CE*)g.c;
   int ldo = g.ldc;
   const bool split = p.splits > 1;
   if (split) { g.c = ws; g.ldc = g.N; }
-  if (vec) gemm_launch<AK, BK, true>(p, g, split, split ? nullptr : bias, split ? 0 : relu,
-                                     split ? 0 : accumulate, st);
-  else gemm_launch<AK, BK, false>(p, g, split, split ? nullptr : bias, split ? 0 : relu,
-                                  split ? 0 : accumulate, st);
+  if (vec) gemm_launch<AK, BK, true, E, CE>(p, g, split, split ? nullptr : bias,
+                                            split ? 0 : relu, split ? 0 : accumulate, st);
+  else gemm_launch<AK, BK, false, E, CE>(p, g, split, split ? nullptr : bias, split ? 0 : relu,
+                                         split ? 0 : accumulate, st);
   if (split) {
     size_t total = (size_t)g.M * g.N;
-    gemm_splitk_epilogue<<<(unsigned)((total + 255) / 256), 256, 0, st>>>(
+    gemm_splitk_epilogue<CE><<<(unsigned)((total + 255) / 256), 256, 0, st>>>(
         ws, p.splits, g.M, g.N, g.N, out, ldo, bias, relu, accumulate);
   }
   return SB_OK;
@@ -330,8 +351,7 @@ static sb_status fc_check(const sb_fc_desc* d) {
   if (d->m <= 0 || d->k_in <= 0 || d->n_shard <= 0) return SB_ERR_INVALID_ARG;
   if (d->ldx < d->k_in || d->ldy < d->n_shard) return SB_ERR_INVALID_ARG;
   if (d->flags & ~SB_FUSE_RELU) return SB_ERR_INVALID_ARG;
-  if (d->dtype == SB_BF16) return SB_ERR_UNSUPPORTED;
-  if (d->dtype != SB_F32) return SB_ERR_INVALID_ARG;
+  if (d->dtype != SB_F32 && d->dtype != SB_BF16) return SB_ERR_INVALID_ARG;
   return SB_OK;
 }
 
@@ -343,28 +363,67 @@ extern "C" size_t sb_fc_workspace_bytes(const sb_fc_desc* d, int pass) {
   return (size_t)-1;
 }
 
+// Forward on operands of type E (fp32, or bf16 bits with a bf16 output).
+template <class E>
+static sb_status fc_fwd_run(const sb_fc_desc* d, const void* x, const void* w, const float* b,
+                            void* y, void* ws, size_t ws_bytes, hipStream_t st) {
+  GemmArgs g{};
+  g.a = x; g.lda = d->ldx; g.amask = nullptr;
+  g.b = w; g.ldb = d->n_shard; g.bmask = nullptr;
+  g.c = y; g.ldc = d->ldy;
+  g.M = d->m; g.N = d->n_shard; g.K = d->k_in;
+  return gemm_run<true, false, E, E>(g, b, (d->flags & SB_FUSE_RELU) ? 1 : 0, 0, (float*)ws,
+                                     ws_bytes, st);
+}
+
 extern "C" sb_status sb_fc_shard_fwd(const sb_fc_desc* d, const void* x, const void* w,
                                      const float* b, void* y, void* ws, size_t ws_bytes,
                                      void* stream) {
   sb_status s = fc_check(d);
   if (s != SB_OK) return s;
   if (!x || !w || !y) return SB_ERR_INVALID_ARG;
-  const size_t es = 4;
+  const size_t es = d->dtype == SB_BF16 ? 2 : 4;
   size_t xb = ((size_t)(d->m - 1) * d->ldx + d->k_in) * es;
   size_t yb = ((size_t)(d->m - 1) * d->ldy + d->n_shard) * es;
   size_t wb = (size_t)d->k_in * d->n_shard * es;
   if (sbh::overlaps(y, yb, x, xb) || sbh::overlaps(y, yb, w, wb) ||
-      sbh::overlaps(y, yb, b, b ? d->n_shard * es : 0))
+      sbh::overlaps(y, yb, b, b ? d->n_shard * sizeof(float) : 0))
     return SB_ERR_INVALID_ARG;
-  GemmArgs g{};
-  g.a = (const float*)x; g.lda = d->ldx; g.amask = nullptr;
-  g.b = (const float*)w; g.ldb = d->n_shard; g.bmask = nullptr;
-  g.c = (float*)y; g.ldc = d->ldy;
-  g.M = d->m; g.N = d->n_shard; g.K = d->k_in;
   hipStream_t st = sbh::stream_of(stream);
-  s = gemm_run<true, false>(g, b, (d->flags & SB_FUSE_RELU) ? 1 : 0, 0, (float*)ws, ws_bytes, st);
+  s = d->dtype == SB_BF16 ? fc_fwd_run<u16>(d, x, w, b, y, ws, ws_bytes, st)
+                          : fc_fwd_run<float>(d, x, w, b, y, ws, ws_bytes, st);
   if (s != SB_OK) return s;
   return sbh::launch_status();
+}
+
+// Backward on operands of type E: dx_partial has type E, dW and db fp32.
+template <class E>
+static sb_status fc_bwd_run(const sb_fc_desc* d, const void* x, const void* w, const void* dy,
+                            const void* mask, void* dxp, float* dw, float* db, int accumulate,
+                            void* ws, size_t ws_bytes, hipStream_t st) {
+  sb_status s;
+  if (dxp) {
+    GemmArgs g{};
+    g.a = dy; g.lda = d->ldy; g.amask = mask;
+    g.b = w; g.ldb = d->n_shard; g.bmask = nullptr;
+    g.c = dxp; g.ldc = d->ldx;
+    g.M = d->m; g.N = d->k_in; g.K = d->n_shard;
+    s = gemm_run<true, true, E, E>(g, nullptr, 0, 0, (float*)ws, ws_bytes, st);
+    if (s != SB_OK) return s;
+  }
+  {
+    GemmArgs g{};
+    g.a = x; g.lda = d->ldx; g.amask = nullptr;
+    g.b = dy; g.ldb = d->ldy; g.bmask = mask;
+    g.c = dw; g.ldc = d->n_shard;
+    g.M = d->k_in; g.N = d->n_shard; g.K = d->m;
+    s = gemm_run<false, false, E, float>(g, nullptr, 0, accumulate, (float*)ws, ws_bytes, st);
+    if (s != SB_OK) return s;
+  }
+  if (db)
+    col_sum<E><<<cdiv(d->n_shard, 64), 1024, 0, st>>>((const E*)dy, (const E*)mask, d->m,
+                                                      d->n_shard, d->ldy, db, accumulate);
+  return SB_OK;
 }
 
 extern "C" sb_status sb_fc_shard_bwd(const sb_fc_desc* d, const void* x, const void* w,
@@ -376,15 +435,16 @@ extern "C" sb_status sb_fc_shard_bwd(const sb_fc_desc* d, const void* x, const v
   if (d->flags != 0) return SB_ERR_INVALID_ARG;
   if (!x || !w || !dy || !dw) return SB_ERR_INVALID_ARG;
   if (accumulate != 0 && accumulate != 1) return SB_ERR_INVALID_ARG;
-  const size_t es = 4;
+  const size_t es = d->dtype == SB_BF16 ? 2 : 4;
   size_t xb = ((size_t)(d->m - 1) * d->ldx + d->k_in) * es;
   size_t yb = ((size_t)(d->m - 1) * d->ldy + d->n_shard) * es;
   size_t wb = (size_t)d->k_in * d->n_shard * es;
-  size_t dbb = (size_t)d->n_shard * es;
+  size_t dwb = (size_t)d->k_in * d->n_shard * sizeof(float);
+  size_t dbb = (size_t)d->n_shard * sizeof(float);
   const void* ins[4] = {x, w, dy, mask};
   size_t insb[4] = {xb, wb, yb, mask ? yb : 0};
   void* outs[3] = {dxp, dw, db};
-  size_t outsb[3] = {dxp ? xb : 0, wb, db ? dbb : 0};
+  size_t outsb[3] = {dxp ? xb : 0, dwb, db ? dbb : 0};
   for (int o = 0; o < 3; ++o) {
     for (int i = 0; i < 4; ++i)
       if (sbh::overlaps(outs[o], outsb[o], ins[i], insb[i])) return SB_ERR_INVALID_ARG;
@@ -394,26 +454,9 @@ extern "C" sb_status sb_fc_shard_bwd(const sb_fc_desc* d, const void* x, const v
   size_t need = sb_fc_workspace_bytes(d, SB_FC_BWD);
   if (need > 0 && (!ws || ws_bytes < need)) return SB_ERR_WORKSPACE;
   hipStream_t st = sbh::stream_of(stream);
-  if (dxp) {
-    GemmArgs g{};
-    g.a = (const float*)dy; g.lda = d->ldy; g.amask = (const float*)mask;
-    g.b = (const float*)w; g.ldb = d->n_shard; g.bmask = nullptr;
-    g.c = (float*)dxp; g.ldc = d->ldx;
-    g.M = d->m; g.N = d->k_in; g.K = d->n_shard;
-    s = gemm_run<true, true>(g, nullptr, 0, 0, (float*)ws, ws_bytes, st);
-    if (s != SB_OK) return s;
-  }
-  {
-    GemmArgs g{};
-    g.a = (const float*)x; g.lda = d->ldx; g.amask = nullptr;
-    g.b = (const float*)dy; g.ldb = d->ldy; g.bmask = (const float*)mask;
-    g.c = dw; g.ldc = d->n_shard;
-    g.M = d->k_in; g.N = d->n_shard; g.K = d->m;
-    s = gemm_run<false, false>(g, nullptr, 0, accumulate, (float*)ws, ws_bytes, st);
-    if (s != SB_OK) return s;
-  }
-  if (db)
-    col_sum<<<cdiv(d->n_shard, 64), 1024, 0, st>>>((const float*)dy, (const float*)mask, d->m,
-                                                   d->n_shard, d->ldy, db, accumulate);
+  s = d->dtype == SB_BF16
+          ? fc_bwd_run<u16>(d, x, w, dy, mask, dxp, dw, db, accumulate, ws, ws_bytes, st)
+          : fc_bwd_run<float>(d, x, w, dy, mask, dxp, dw, db, accumulate, ws, ws_bytes, st);
+  if (s != SB_OK) return s;
   return sbh::launch_status();
 }

@@ -89,11 +89,13 @@ def test_fc_argument_validation():
     ok = sb.fc_desc(16, 32, 8)
     assert sb.sb_fc_workspace_bytes(ok, sb.SB_FC_FWD) != 2 ** 64 - 1
     for bad in [sb.fc_desc(0, 32, 8), sb.fc_desc(16, 32, 8, ldx=16), sb.fc_desc(16, 32, 8, ldy=4),
-                sb.sb_fc_desc(16, 32, 8, 0, 32, 8, 4)]:
+                sb.sb_fc_desc(16, 32, 8, 0, 32, 8, 4), sb.sb_fc_desc(16, 32, 8, 7, 32, 8, 0)]:
         assert sb.sb_fc_workspace_bytes(bad, 0) == 2 ** 64 - 1
         assert _raw("sb_fc_shard_fwd", ctypes.byref(bad), P, P + 8192, None, P + 65536, None, 0, None) == sb.SB_ERR_INVALID_ARG
+    # bf16 is validated like fp32 (element size 2): an output overlapping x.
     bf = sb.fc_desc(16, 32, 8, dtype=sb.SB_BF16)
-    assert _raw("sb_fc_shard_fwd", ctypes.byref(bf), P, P + 8192, None, P + 65536, None, 0, None) == sb.SB_ERR_UNSUPPORTED
+    assert sb.sb_fc_workspace_bytes(bf, sb.SB_FC_FWD) != 2 ** 64 - 1
+    assert _raw("sb_fc_shard_fwd", ctypes.byref(bf), P, P + 8192, None, P + 1000, None, 0, None) == sb.SB_ERR_INVALID_ARG
     # Missing dW, bad accumulate flag, overlapping outputs.
     assert _raw("sb_fc_shard_bwd", ctypes.byref(ok), P, P + 8192, P + 16384, None, None, None, None, 0, None, 0, None) == sb.SB_ERR_INVALID_ARG
     assert _raw("sb_fc_shard_bwd", ctypes.byref(ok), P, P + 8192, P + 16384, None, None, P + 65536, None, 2, None, 0, None) == sb.SB_ERR_INVALID_ARG

@@ -383,36 +383,47 @@ def _fc_inputs(m, kin, ns, seed):
     return x, w, b, dy, mask
 
 
+@pytest.mark.parametrize("dtype", DTYPES)
 @pytest.mark.parametrize("shape", FC_SHAPES)
 @pytest.mark.parametrize("relu", [False, True])
-def test_fc_fwd(shape, relu):
+def test_fc_fwd(shape, relu, dtype):
     m, kin, ns = shape
-    print_case("fc_fwd", shape=shape, relu=relu)
+    print_case("fc_fwd", shape=shape, relu=relu, dtype=dtype)
     x, w, b, _, _ = _fc_inputs(m, kin, ns, 21)
-    d = sb.fc_desc(m, kin, ns, relu=relu)
+    d = sb.fc_desc(m, kin, ns, _code(dtype), relu=relu)
     ws = _ws(sb.sb_fc_workspace_bytes(d, sb.SB_FC_FWD))
-    y = torch.full((m, ns), float("nan"), device="cuda")
-    sb.sb_fc_shard_fwd(d, to_dev(x), to_dev(w), to_dev(b), y, ws)
+    y = torch.full((m, ns), float("nan"), dtype=_tdt(dtype), device="cuda")
+    xd, wd = to_dev(x, dtype), to_dev(w, dtype)
+    sb.sb_fc_shard_fwd(d, xd, wd, to_dev(b), y, ws)
     torch.cuda.synchronize()
-    assert rel_l2(to_host(y), O.fc_fwd(x, w, b, relu=relu)) <= TOL["f32"]
+    # The oracle gets the values the kernel read; bf16 outputs are rounded.
+    ref = O.fc_fwd(to_host(xd), to_host(wd), b, relu=relu)
+    if dtype == "bf16":
+        ref = O.round_bf16(ref)
+    assert rel_l2(to_host(y), ref) <= TOL[dtype]
 
 
+@pytest.mark.parametrize("dtype", DTYPES)
 @pytest.mark.parametrize("shape", FC_SHAPES)
 @pytest.mark.parametrize("masked", [False, True])
-def test_fc_bwd(shape, masked):
+def test_fc_bwd(shape, masked, dtype):
     m, kin, ns = shape
-    print_case("fc_bwd", shape=shape, masked=masked)
+    print_case("fc_bwd", shape=shape, masked=masked, dtype=dtype)
     x, w, _, dy, mask = _fc_inputs(m, kin, ns, 22)
-    d = sb.fc_desc(m, kin, ns)
+    d = sb.fc_desc(m, kin, ns, _code(dtype))
     ws = _ws(sb.sb_fc_workspace_bytes(d, sb.SB_FC_BWD))
-    dxp = torch.full((m, kin), float("nan"), device="cuda")
+    dxp = torch.full((m, kin), float("nan"), dtype=_tdt(dtype), device="cuda")
     dw = torch.full((kin, ns), float("nan"), device="cuda")
     db = torch.full((ns,), float("nan"), device="cuda")
-    sb.sb_fc_shard_bwd(d, to_dev(x), to_dev(w), to_dev(dy), to_dev(mask) if masked else None,
-                       dxp, dw, db, False, ws)
+    xd, wd, dyd, md = (to_dev(a, dtype) for a in (x, w, dy, mask))
+    sb.sb_fc_shard_bwd(d, xd, wd, dyd, md if masked else None, dxp, dw, db, False, ws)
     torch.cuda.synchronize()
-    rdx, rdw, rdb = O.fc_bwd(x, w, dy, mask_src=mask if masked else None)
-    assert rel_l2(to_host(dxp), rdx) <= TOL["f32"]
+    rdx, rdw, rdb = O.fc_bwd(to_host(xd), to_host(wd), to_host(dyd),
+                             mask_src=to_host(md) if masked else None)
+    if dtype == "bf16":
+        rdx = O.round_bf16(rdx)
+    assert rel_l2(to_host(dxp), rdx) <= TOL[dtype]
+    # dW and db are fp32 sums of exact products of the bf16 values.
     assert rel_l2(to_host(dw), rdw) <= TOL["f32"]
     assert rel_l2(to_host(db), rdb) <= TOL["f32"]
 
