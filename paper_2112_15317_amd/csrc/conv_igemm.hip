@@ -16,7 +16,8 @@
 // (TW+2), read once, then read at 9 shifted windows: no im2col) and the
 // filter slice [tap][ci][co].  Pipeline per chunk t: store chunk t+1 (already
 // in registers) into the other LDS buffer, issue the global loads of chunk
-// t+2, multiply chunk t out of LDS, barrier.  MFMA operand fragments are
+// t+2, multiply chunk t out of LDS, barrier (the two-group 8x8 tiles do the
+// store and the loads halfway through the multiply).  MFMA operand fragments are
 // double-buffered in registers so LDS reads run one k-step ahead of the
 // MFMAs.  Gathers are branch-free (clamped index + select).  MFMA rows are
 // channels and columns pixels, so the 16 lanes of an output row store 16
@@ -207,7 +208,12 @@ __global__ __launch_bounds__(T::THREADS, 2 / T::KSPLIT) void conv3x3_igemm_f32(C
   };
   // WMC: the wave's pixel-row position wm as a compile-time constant (only
   // used with WHOLE_H, to skip padding blocks).
-  auto compute_wm = [&](int buf, auto WMC) {
+  // mid(): staged at step MID of the chunk's MFMA sequence (the next
+  // chunk's LDS store and the one after's global loads).  The two-group
+  // 8x8 tiles stage halfway through, so the wait for the loads and the LDS
+  // stores hide behind MFMAs; the other tiles stage before the first step.
+  constexpr int MID = T::KSPLIT == 2 ? T::NSTEP / 2 : 0;
+  auto compute_wm = [&](int buf, auto WMC, auto&& mid) {
     constexpr int WMc = decltype(WMC)::value;
     const float* X = lds + buf * T::LDS_BUF;
     const float* Wl = X + T::LDS_X;
@@ -226,6 +232,7 @@ __global__ __launch_bounds__(T::THREADS, 2 / T::KSPLIT) void conv3x3_igemm_f32(C
     frag(0, 0);
 #pragma unroll
     for (int s = 0; s < T::NSTEP; ++s) {
+      if (s == MID) mid();
       if (s + 1 < T::NSTEP) frag(s + 1, (s + 1) & 1);
       const int tap = s / (T::CK / 4);
 #pragma unroll
@@ -236,15 +243,15 @@ __global__ __launch_bounds__(T::THREADS, 2 / T::KSPLIT) void conv3x3_igemm_f32(C
             acc[nb][mb] = mfma16x16x4(fa[s & 1][nb], fb[s & 1][mb], acc[nb][mb]);
     }
   };
-  auto compute = [&](int buf) {
+  auto compute = [&](int buf, auto&& mid) {
     if constexpr (WHOLE_H) {
       static_assert(T::WAVES_M <= 4, "at most four pixel-row positions");
-      if (wm == 0) compute_wm(buf, std::integral_constant<int, 0>{});
-      else if (T::WAVES_M > 1 && wm == 1) compute_wm(buf, std::integral_constant<int, 1>{});
-      else if (T::WAVES_M > 2 && wm == 2) compute_wm(buf, std::integral_constant<int, 2>{});
-      else if (T::WAVES_M > 3) compute_wm(buf, std::integral_constant<int, 3>{});
+      if (wm == 0) compute_wm(buf, std::integral_constant<int, 0>{}, mid);
+      else if (T::WAVES_M > 1 && wm == 1) compute_wm(buf, std::integral_constant<int, 1>{}, mid);
+      else if (T::WAVES_M > 2 && wm == 2) compute_wm(buf, std::integral_constant<int, 2>{}, mid);
+      else if (T::WAVES_M > 3) compute_wm(buf, std::integral_constant<int, 3>{}, mid);
     } else {
-      compute_wm(buf, std::integral_constant<int, 0>{});
+      compute_wm(buf, std::integral_constant<int, 0>{}, mid);
     }
   };
 
@@ -261,9 +268,14 @@ __global__ __launch_bounds__(T::THREADS, 2 / T::KSPLIT) void conv3x3_igemm_f32(C
   __syncthreads();
   for (int t = 0; t < nit; ++t) {
     const int buf = t & 1;
-    if (t + 1 < nk) lstore(buf ^ 1);
-    if (t + 2 < nk) gload(chunk(t + 2));
-    if (t < nk) compute(buf);
+    // Buffer buf ^ 1 was last read before the previous barrier, so its next
+    // contents may be stored at any point of this iteration.
+    auto mid = [&]() {
+      if (t + 1 < nk) lstore(buf ^ 1);
+      if (t + 2 < nk) gload(chunk(t + 2));
+    };
+    if (t < nk) compute(buf, mid);
+    else mid();
     __syncthreads();
   }
 
