@@ -218,6 +218,11 @@ WGRAD_BF16_SHAPES = [
     (2, 40, 9, 24, 70),      # 16-wide tiles, 8 columns per load, two column tiles
     (2, 48, 9, 11, 64),      # 8-wide tiles, 1 column per load
     (1, 64, 3, 64, 128),     # 32-wide tiles, two full column tiles
+    # 64 or more input channels, ragged in c and k
+    (2, 70, 5, 40, 140),     # 32-wide tiles, 8 columns per load, three c and three k tiles
+    (2, 64, 6, 20, 96),      # 16-wide tiles, 4 columns per load
+    (2, 100, 9, 10, 130),    # 8-wide tiles, 2 columns per load
+    (1, 72, 3, 37, 200),     # 32-wide tiles, 1 column per load
 ]
 
 
