@@ -48,9 +48,16 @@
 namespace sb {
 
 // ----------------------------------------------------------------- generic --
-template <int TH_, int TW_, int IMGS_, int CK_, int BN_, int WAVES_N_, int KSPLIT_ = 1>
+template <int TH_, int TW_, int IMGS_, int CK_, int BN_, int WAVES_N_, int KSPLIT_ = 1,
+          int STAGED_ = 0>
 struct ConvTile {
   static constexpr int TH = TH_, TW = TW_, IMGS = IMGS_, CK = CK_, BN = BN_;
+  // STAGED: the unsplit output tile goes out through LDS ([channel][pixel])
+  // in 16-byte pieces of 4 pixels of one row (full-row coalesced stores,
+  // the mask read in the same pieces), instead of one 4-byte store per
+  // accumulator element (16 lanes = 64 contiguous bytes).  For memory-bound
+  // layers whose short channel loop leaves the epilogue a large share.
+  static constexpr bool STAGED = STAGED_ != 0;
   // KSPLIT groups of 256 threads share the block's output tile and take
   // alternate channel chunks, each through its own LDS buffers; the groups'
   // partial sums are added through LDS in a fixed order at the end.  This
@@ -294,13 +301,18 @@ __global__ __launch_bounds__(T::THREADS, 2 / T::KSPLIT) void conv3x3_igemm_f32(C
           for (int i = 0; i < 4; ++i) xfer[((nb * T::MB + mb) * 4 + i) * 64] = acc[nb][mb][i];
     }
     __syncthreads();
-    if (grp == 1) return;
+    if (grp == 1) {
+      // Without the staged output group 1 is done; with it, it still takes
+      // part in the barriers and the stores below.
+      if constexpr (!T::STAGED) return;
+    } else {
 #pragma unroll
-    for (int nb = 0; nb < T::NB; ++nb)
+      for (int nb = 0; nb < T::NB; ++nb)
 #pragma unroll
-      for (int mb = 0; mb < T::MB; ++mb)
+        for (int mb = 0; mb < T::MB; ++mb)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) acc[nb][mb][i] += xfer[((nb * T::MB + mb) * 4 + i) * 64];
+          for (int i = 0; i < 4; ++i) acc[nb][mb][i] += xfer[((nb * T::MB + mb) * 4 + i) * 64];
+    }
   }
 
   // ---- epilogue: acc[nb][mb] lane holds channel co0 + wn*WN + nb*16 + 4*kq + i
@@ -323,6 +335,68 @@ __global__ __launch_bounds__(T::THREADS, 2 / T::KSPLIT) void conv3x3_igemm_f32(C
         }
     }
   };
+  if constexpr (T::STAGED) {
+    // Output tile in LDS as [channel][image][row][column] (image-major, so
+    // 4 consecutive tile columns are 4 consecutive image columns).
+    static_assert(T::TW % 4 == 0, "4-pixel pieces within a tile row");
+    constexpr int EP = T::BM + 4;                    // LDS row pitch: 4 mod 64 banks
+    static_assert(T::BN * EP <= 2 * T::LDS_BUF, "output tile fits the LDS buffers");
+    if (a.splits == 1) {
+      // With one group every wave has passed the loop's last barrier; with
+      // two, group 0 has just read the transfer area.
+      if constexpr (T::KSPLIT == 2) __syncthreads();
+      if (grp == 0) {
+#pragma unroll
+        for (int mb = 0; mb < T::MB; ++mb) {
+          int img, yy, xx;
+          T::pix(wm * T::WM + mb * 16 + lr, img, yy, xx);
+          const int lp = (img * T::TH + yy) * T::TW + xx;
+#pragma unroll
+          for (int nb = 0; nb < T::NB; ++nb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              lds_all[(wn * T::WN + nb * 16 + kq * 4 + i) * EP + lp] = acc[nb][mb][i];
+        }
+      }
+      __syncthreads();
+      constexpr int QPR = T::BM / 4;                 // 4-pixel pieces per channel row
+      static_assert(T::BN * QPR % T::THREADS == 0, "whole rounds of pieces");
+      const bool vec = std::is_same<E, float>::value && a.W % 4 == 0 &&
+                       (((uintptr_t)a.out | (uintptr_t)a.mask) & 15) == 0;
+#pragma unroll
+      for (int j = 0; j < T::BN * QPR / T::THREADS; ++j) {
+        const int q = (int)threadIdx.x + T::THREADS * j;
+        const int col = q / QPR, px = (q % QPR) * 4;
+        const int img = px / (T::TH * T::TW), rem = px % (T::TH * T::TW);
+        const int co = co0 + col, h = h0 + rem / T::TW, w = w0 + rem % T::TW;
+        if (co >= a.Cout || n0 + img >= a.N || h >= a.H || w >= a.W) continue;
+        const f4 v = *reinterpret_cast<const f4*>(lds_all + col * EP + px);
+        const size_t off = ((size_t)(n0 + img) * a.Cout + co) * HWs + (size_t)h * a.W + w;
+        if (vec) {
+          const float bv = a.bias ? a.bias[co] : 0.f;
+          f4 mk = f4{1.f, 1.f, 1.f, 1.f};
+          if (a.mask) mk = *reinterpret_cast<const f4*>((const float*)a.mask + off);
+          f4 o;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            float r = v[e] + bv;
+            if (a.relu && !(r > 0.f)) r = 0.f;
+            o[e] = mk[e] > 0.f ? r : 0.f;
+          }
+          *reinterpret_cast<f4*>((float*)a.out + off) = o;
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (w + e < a.W)
+              Elem<E>::store((E*)a.out, off + e, conv_epilogue<E>(a, v[e], co, off + e));
+        }
+      }
+      return;
+    }
+  }
+  if constexpr (T::KSPLIT == 2 && T::STAGED) {
+    if (grp == 1) return;                            // split partials: group 0 writes them
+  }
   if (a.splits == 1) {
     for_each_out([&](float v, int co, size_t off) {
       Elem<E>::store((E*)a.out, off, conv_epilogue<E>(a, v, co, off));
@@ -524,34 +598,34 @@ struct IgemmPlan {
   size_t ws_bytes;
 };
 
-using TileW32 = ConvTile<4, 32, 1, 8, 64, 2>;
-using TileW16 = ConvTile<8, 16, 1, 8, 64, 2>;
-using TileW8 = ConvTile<8, 8, 2, 8, 64, 2>;
+using TileW32 = ConvTile<4, 32, 1, 8, 64, 2, 1, 1>;
+using TileW16 = ConvTile<8, 16, 1, 8, 64, 2, 1, 1>;
+using TileW8 = ConvTile<8, 8, 2, 8, 64, 2, 1, 1>;
 using TileW4 = ConvTile<4, 4, 8, 8, 64, 2>;
 using TileW2 = ConvTile<2, 2, 32, 8, 64, 2>;
-using TileW32c4 = ConvTile<4, 32, 1, 4, 64, 2>;
+using TileW32c4 = ConvTile<4, 32, 1, 4, 64, 2, 1, 1>;   // output staged through LDS
 using TileW32n16 = ConvTile<4, 32, 1, 8, 16, 1>;
-using TileW32L = ConvTile<8, 32, 1, 8, 64, 1>;
-using TileW16L = ConvTile<16, 16, 1, 8, 64, 1>;
-using TileW8L = ConvTile<8, 8, 4, 8, 64, 1>;
-using TileW8K2 = ConvTile<8, 8, 2, 8, 64, 2, 2>;
+using TileW32L = ConvTile<8, 32, 1, 8, 64, 1, 1, 1>;
+using TileW16L = ConvTile<16, 16, 1, 8, 64, 1, 1, 1>;
+using TileW8L = ConvTile<8, 8, 4, 8, 64, 1, 1, 1>;
+using TileW8K2 = ConvTile<8, 8, 2, 8, 64, 2, 2, 1>;
 using Small2 = SmallTile<2, 2, 2>;
 using Small4 = SmallTile<4, 4, 1>;
 
 static const char* kTileNames[] = {
-    "sb::conv3x3_igemm_f32<sb::ConvTile<4, 32, 1, 8, 64, 2, 1>, %s, %s>",
-    "sb::conv3x3_igemm_f32<sb::ConvTile<8, 16, 1, 8, 64, 2, 1>, %s, %s>",
-    "sb::conv3x3_igemm_f32<sb::ConvTile<8, 8, 2, 8, 64, 2, 1>, %s, %s>",
-    "sb::conv3x3_igemm_f32<sb::ConvTile<4, 4, 8, 8, 64, 2, 1>, %s, %s>",
-    "sb::conv3x3_igemm_f32<sb::ConvTile<2, 2, 32, 8, 64, 2, 1>, %s, %s>",
-    "sb::conv3x3_igemm_f32<sb::ConvTile<4, 32, 1, 4, 64, 2, 1>, %s, %s>",
-    "sb::conv3x3_igemm_f32<sb::ConvTile<4, 32, 1, 8, 16, 1, 1>, %s, %s>",
+    "sb::conv3x3_igemm_f32<sb::ConvTile<4, 32, 1, 8, 64, 2, 1, 1>, %s, %s>",
+    "sb::conv3x3_igemm_f32<sb::ConvTile<8, 16, 1, 8, 64, 2, 1, 1>, %s, %s>",
+    "sb::conv3x3_igemm_f32<sb::ConvTile<8, 8, 2, 8, 64, 2, 1, 1>, %s, %s>",
+    "sb::conv3x3_igemm_f32<sb::ConvTile<4, 4, 8, 8, 64, 2, 1, 0>, %s, %s>",
+    "sb::conv3x3_igemm_f32<sb::ConvTile<2, 2, 32, 8, 64, 2, 1, 0>, %s, %s>",
+    "sb::conv3x3_igemm_f32<sb::ConvTile<4, 32, 1, 4, 64, 2, 1, 1>, %s, %s>",
+    "sb::conv3x3_igemm_f32<sb::ConvTile<4, 32, 1, 8, 16, 1, 1, 0>, %s, %s>",
     "sb::conv3x3_small_f32<sb::SmallTile<2, 2, 2>, %s, %s>",
     "sb::conv3x3_small_f32<sb::SmallTile<4, 4, 1>, %s, %s>",
-    "sb::conv3x3_igemm_f32<sb::ConvTile<8, 32, 1, 8, 64, 1, 1>, %s, %s>",
-    "sb::conv3x3_igemm_f32<sb::ConvTile<16, 16, 1, 8, 64, 1, 1>, %s, %s>",
-    "sb::conv3x3_igemm_f32<sb::ConvTile<8, 8, 4, 8, 64, 1, 1>, %s, %s>",
-    "sb::conv3x3_igemm_f32<sb::ConvTile<8, 8, 2, 8, 64, 2, 2>, %s, %s>",
+    "sb::conv3x3_igemm_f32<sb::ConvTile<8, 32, 1, 8, 64, 1, 1, 1>, %s, %s>",
+    "sb::conv3x3_igemm_f32<sb::ConvTile<16, 16, 1, 8, 64, 1, 1, 1>, %s, %s>",
+    "sb::conv3x3_igemm_f32<sb::ConvTile<8, 8, 4, 8, 64, 1, 1, 1>, %s, %s>",
+    "sb::conv3x3_igemm_f32<sb::ConvTile<8, 8, 2, 8, 64, 2, 2, 1>, %s, %s>",
 };
 
 // allow_small: the whole-image kernel needs tensors aligned for 4-element

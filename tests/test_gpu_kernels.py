@@ -77,6 +77,10 @@ CONV_SHAPES = [
     (2, 64, 6, 40, 80),      # 32-wide tiles, 32-channel blocks, ragged columns and k
     (2, 36, 20, 20, 64),     # 16-wide tiles, ragged channel block
     (2, 48, 14, 14, 64),     # 8x8 tiles over 14x14 (rows not a multiple of 4)
+    (2, 3, 6, 36, 40),       # RGB-like input (output staged through LDS, 4-pixel pieces,
+                             # ragged column tile); 3-channel data gradient in two groups
+                             # over an odd number of chunks
+    (3, 2, 5, 38, 12),       # the same with an odd width (element-wise stores)
     (1, 1, 1, 1, 1),         # degenerate: every tap but the centre is padding
     (1, 9, 3, 1, 5),
 ]
