@@ -445,6 +445,49 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_f32(WgArgs a) {
     __syncthreads();
   }
 
+  // Wide layout: the block's 64 k x (16 c x 9 taps) weight gradient goes out
+  // through LDS as 64 rows of 144 consecutive floats (k, then c * 9 + tap,
+  // the dw order), written in 16-byte pieces; otherwise each lane would
+  // write single floats 9 apart.  The loop's last barrier has freed the LDS.
+  if constexpr (!T::NARROW) {
+    constexpr int RW = 16 * 9, RP = RW + 4;          // row width and LDS pitch (floats)
+    static_assert(T::BK * RP * sizeof(float) <= T::LDS_BYTES, "tile fits the LDS");
+    const int cw = min(16, a.C - c0) * 9;            // live columns of the tile
+    const size_t wsz = (size_t)a.K * a.C * 9;
+    float* dst = a.splits == 1 ? a.dw : a.part + (size_t)blk.z * (wsz + a.K);
+    const bool vec = (a.C * 9) % 4 == 0 && cw % 4 == 0 &&
+                     (((uintptr_t)dst + (size_t)c0 * 9 * sizeof(float)) & 15) == 0;
+#pragma unroll
+    for (int t = 0; t < 9; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) lds[(wave * 16 + 4 * jq + i) * RP + lr * 9 + t] = acc[t][i];
+    __syncthreads();
+    if (vec) {
+      constexpr int QPR = RW / 4;                    // 36 pieces per row
+#pragma unroll
+      for (int j = 0; j < T::BK * QPR / 256; ++j) {
+        const int q = tid + 256 * j, row = q / QPR, col = (q % QPR) * 4;
+        const int k = k0 + row;
+        if (k >= a.K || col >= cw) continue;
+        *reinterpret_cast<f4*>(dst + (size_t)k * a.C * 9 + (size_t)c0 * 9 + col) =
+            *reinterpret_cast<const f4*>(lds + row * RP + col);
+      }
+    } else {
+      for (int e = tid; e < T::BK * RW; e += 256) {
+        const int row = e / RW, col = e % RW, k = k0 + row;
+        if (k < a.K && col < cw) dst[(size_t)k * a.C * 9 + (size_t)c0 * 9 + col] = lds[row * RP + col];
+      }
+    }
+    if (do_db && lr == 0) {
+      float* pb = a.splits == 1 ? a.db : dst + wsz;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int k = k0 + wave * 16 + 4 * jq + i;
+        if (k < a.K) pb[k] = accb[i];
+      }
+    }
+    return;
+  }
   // acc[t] lane holds rows k = k0 + wave*16 + 4*jq + i and column lr of its block.
   wgrad_store<T::NACC>(
       a, blk.z, k0 + wave * 16, do_db, accb, [&](int i, int t) { return acc[t][i]; },
