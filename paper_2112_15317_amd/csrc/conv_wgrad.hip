@@ -793,19 +793,61 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_bf16(WgArgs a) {
       __syncthreads();
     }
   }
-  if (wp != 0) return;
-
-  // acc[m][t] lane holds rows k = k0 + (wk*MA + m)*16 + 4*kq + i and
-  // channel c0 + wc*16 + lr.
+  // acc[m][t] of the waves wp = 0 holds rows k = k0 + (wk*MA + m)*16 +
+  // 4*kq + i and channel c0 + wc*16 + lr.  The block's 64 k x (BC c x 9
+  // taps) tile goes out through LDS in rounds of 32 rows of BC * 9
+  // consecutive floats (the dw order), written in 16-byte pieces; every
+  // wave takes part in the barriers and the stores.
+  {
+    constexpr int RW = T::BC * 9, RP = RW + 4, ROWS = 32, QPR = RW / 4;
+    static_assert(ROWS * RP * sizeof(float) <= T::LDS_BYTES && RW % 4 == 0, "rows fit the LDS");
+    float* L = reinterpret_cast<float*>(ldsw);
+    const int cw = min(T::BC, a.C - c0) * 9;         // live columns of the tile
+    const size_t wsz = (size_t)a.K * a.C * 9;
+    float* dst = a.splits == 1 ? a.dw : a.part + (size_t)blk.z * (wsz + a.K);
+    const bool vec = (a.C * 9) % 4 == 0 && cw % 4 == 0 &&
+                     (((uintptr_t)dst + (size_t)c0 * 9 * sizeof(float)) & 15) == 0;
 #pragma unroll
-  for (int m = 0; m < T::MA; ++m)
-    wgrad_store<9>(
-        a, blk.z, k0 + (wk * T::MA + m) * 16, do_db, accb[m],
-        [&](int i, int t) { return acc[m][t][i]; },
-        [&](int t) -> int {
-          int c = c0 + wc * 16 + lr;
-          return c < a.C ? c * 9 + t : -1;
-        });
+    for (int r0 = 0; r0 < T::BK; r0 += ROWS) {
+      __syncthreads();                                // the LDS is free
+      if (wp == 0) {
+#pragma unroll
+        for (int m = 0; m < T::MA; ++m) {
+          const int row = (wk * T::MA + m) * 16 - r0;
+          if (row < 0 || row >= ROWS) continue;
+#pragma unroll
+          for (int t = 0; t < 9; ++t)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              L[(row + 4 * kq + i) * RP + (wc * 16 + lr) * 9 + t] = acc[m][t][i];
+        }
+      }
+      __syncthreads();
+      for (int q = tid; q < ROWS * QPR; q += 256) {
+        const int row = q / QPR, col = (q % QPR) * 4, k = k0 + r0 + row;
+        if (k >= a.K || col >= cw) continue;
+        float* o = dst + (size_t)k * a.C * 9 + (size_t)c0 * 9 + col;
+        const float* l = L + row * RP + col;
+        if (vec) {
+          *reinterpret_cast<f4*>(o) = *reinterpret_cast<const f4*>(l);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (col + e < cw) o[e] = l[e];
+        }
+      }
+    }
+    if (wp == 0 && do_db && lr == 0) {
+      float* pb = a.splits == 1 ? a.db : dst + wsz;
+#pragma unroll
+      for (int m = 0; m < T::MA; ++m)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int k = k0 + (wk * T::MA + m) * 16 + 4 * kq + i;
+          if (k < a.K) pb[k] = accb[m][i];
+        }
+    }
+  }
 }
 
 // ------------------------------------------------------ small whole images --
