@@ -207,6 +207,51 @@ inline void launch_splits_reduce(const float* part, int splits, int K, int C, fl
                                                                 wsz, dw, db);
 }
 
+// Writes a block's weight gradient of 64 k x (16 c x 9 taps): acc[t] of wave
+// w, lane (jq, lr) holds rows k0 + 16 w + 4 jq + i, channel c0 + lr, tap t.
+// The tile goes out through LDS (64 x 148 floats, free when this is called)
+// as 64 rows of 144 consecutive floats (k, then c * 9 + tap: the dw order),
+// written in 16-byte pieces, to dw or to this split's partials; otherwise
+// each lane would write single floats 9 apart.
+__device__ __forceinline__ void wgrad_store_rows(const WgArgs& a, int z, int k0, int c0,
+                                                 bool do_db, const f4& accb, const f4 (&acc)[9],
+                                                 float* lds) {
+  constexpr int BK = 64, RW = 16 * 9, RP = RW + 4, QPR = RW / 4;
+  const int tid = threadIdx.x, wave = tid >> 6, jq = (tid & 63) >> 4, lr = tid & 15;
+  const int cw = min(16, a.C - c0) * 9;              // live columns of the tile
+  const size_t wsz = (size_t)a.K * a.C * 9;
+  float* dst = a.splits == 1 ? a.dw : a.part + (size_t)z * (wsz + a.K);
+  const bool vec = (a.C * 9) % 4 == 0 && cw % 4 == 0 &&
+                   (((uintptr_t)dst + (size_t)c0 * 9 * sizeof(float)) & 15) == 0;
+#pragma unroll
+  for (int t = 0; t < 9; ++t)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) lds[(wave * 16 + 4 * jq + i) * RP + lr * 9 + t] = acc[t][i];
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < BK * QPR / 256; ++j) {
+    const int q = tid + 256 * j, row = q / QPR, col = (q % QPR) * 4, k = k0 + row;
+    if (k >= a.K || col >= cw) continue;
+    float* o = dst + (size_t)k * a.C * 9 + (size_t)c0 * 9 + col;
+    const float* l = lds + row * RP + col;
+    if (vec) {
+      *reinterpret_cast<f4*>(o) = *reinterpret_cast<const f4*>(l);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (col + e < cw) o[e] = l[e];
+    }
+  }
+  if (do_db && lr == 0) {
+    float* pb = a.splits == 1 ? a.db : dst + wsz;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int k = k0 + wave * 16 + 4 * jq + i;
+      if (k < a.K) pb[k] = accb[i];
+    }
+  }
+}
+
 // ----------------------------------------------------------------- generic --
 template <int TH_, int TW_, int IMGS_, int NCB_>
 struct WgTile {
@@ -445,47 +490,9 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_f32(WgArgs a) {
     __syncthreads();
   }
 
-  // Wide layout: the block's 64 k x (16 c x 9 taps) weight gradient goes out
-  // through LDS as 64 rows of 144 consecutive floats (k, then c * 9 + tap,
-  // the dw order), written in 16-byte pieces; otherwise each lane would
-  // write single floats 9 apart.  The loop's last barrier has freed the LDS.
   if constexpr (!T::NARROW) {
-    constexpr int RW = 16 * 9, RP = RW + 4;          // row width and LDS pitch (floats)
-    static_assert(T::BK * RP * sizeof(float) <= T::LDS_BYTES, "tile fits the LDS");
-    const int cw = min(16, a.C - c0) * 9;            // live columns of the tile
-    const size_t wsz = (size_t)a.K * a.C * 9;
-    float* dst = a.splits == 1 ? a.dw : a.part + (size_t)blk.z * (wsz + a.K);
-    const bool vec = (a.C * 9) % 4 == 0 && cw % 4 == 0 &&
-                     (((uintptr_t)dst + (size_t)c0 * 9 * sizeof(float)) & 15) == 0;
-#pragma unroll
-    for (int t = 0; t < 9; ++t)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) lds[(wave * 16 + 4 * jq + i) * RP + lr * 9 + t] = acc[t][i];
-    __syncthreads();
-    if (vec) {
-      constexpr int QPR = RW / 4;                    // 36 pieces per row
-#pragma unroll
-      for (int j = 0; j < T::BK * QPR / 256; ++j) {
-        const int q = tid + 256 * j, row = q / QPR, col = (q % QPR) * 4;
-        const int k = k0 + row;
-        if (k >= a.K || col >= cw) continue;
-        *reinterpret_cast<f4*>(dst + (size_t)k * a.C * 9 + (size_t)c0 * 9 + col) =
-            *reinterpret_cast<const f4*>(lds + row * RP + col);
-      }
-    } else {
-      for (int e = tid; e < T::BK * RW; e += 256) {
-        const int row = e / RW, col = e % RW, k = k0 + row;
-        if (k < a.K && col < cw) dst[(size_t)k * a.C * 9 + (size_t)c0 * 9 + col] = lds[row * RP + col];
-      }
-    }
-    if (do_db && lr == 0) {
-      float* pb = a.splits == 1 ? a.db : dst + wsz;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int k = k0 + wave * 16 + 4 * jq + i;
-        if (k < a.K) pb[k] = accb[i];
-      }
-    }
+    static_assert(64 * (16 * 9 + 4) * sizeof(float) <= T::LDS_BYTES, "tile fits the LDS");
+    wgrad_store_rows(a, blk.z, k0, c0, do_db, accb, acc, lds);
     return;
   }
   // acc[t] lane holds rows k = k0 + wave*16 + 4*jq + i and column lr of its block.
@@ -981,12 +988,8 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_small_f32(WgArgs a) {
     __syncthreads();
   }
 
-  wgrad_store<9>(
-      a, blk.z, k0 + wave * 16, do_db, accb, [&](int i, int t) { return acc[t][i]; },
-      [&](int t) -> int {
-        int c = c0 + lr;
-        return c < a.C ? c * 9 + t : -1;
-      });
+  static_assert(64 * (16 * 9 + 4) * sizeof(float) <= T::LDS_BYTES, "tile fits the LDS");
+  wgrad_store_rows(a, blk.z, k0, c0, do_db, accb, acc, lds);
 }
 
 // ------------------------------------------------- 2x2 images: one GEMM --
