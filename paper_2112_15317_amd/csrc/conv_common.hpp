@@ -5,6 +5,8 @@
 
 #include "sb_internal.hpp"
 
+#include <type_traits>
+
 namespace sb {
 
 // Element type E of in / wt / mask / out: float or bf16 bits (u16).
@@ -68,6 +70,75 @@ __device__ __forceinline__ void pack_slice(const E* __restrict__ w, E* __restric
   constexpr int PT = (SL + 255) / 256;
   const int nchunks = cdiv(Cin, CK);
   const int ct = slice / nchunks, kc = slice - ct * nchunks;   // co tile, chunk
+  // fp32 filters whose channel counts are multiples of 4 (and 16-byte
+  // aligned): every run of consecutive source elements (CK * 9 per output
+  // channel, or BN * 9 per input channel for the data gradient) starts
+  // 16-byte aligned and is a multiple of 4 long, so the slice is read in
+  // groups of 4 consecutive slice elements with one 16-byte load each (a
+  // quarter of the load instructions).  A group lies in one run; it is read
+  // whole when all 4 elements are in range, element by element otherwise.
+  if constexpr (std::is_same<E, float>::value) {
+    static_assert(SL % 4 == 0 && (CK * 9) % 4 == 0 && (BN * 9) % 4 == 0, "whole groups per run");
+    if (Cin % 4 == 0 && Cout % 4 == 0 && ((uintptr_t)w & 15) == 0) {
+      constexpr int PT4 = (SL / 4 + 255) / 256;
+      // Slice element g -> (channel within the run's tile, its source offset).
+      auto locate = [&](int g, int& tap, int& cc, int& nn, size_t& src) {
+        if (!DGRAD) {                                 // g = (nn, cc, tap), tap fastest
+          nn = g / (CK * 9);
+          const int r = g - nn * (CK * 9);
+          cc = r / 9;
+          tap = r - cc * 9;
+          src = ((size_t)(ct * BN + nn) * Cin + kc * CK + cc) * 9 + tap;
+        } else {                                      // g = (cc, nn, t), t fastest
+          cc = g / (BN * 9);
+          const int r = g - cc * (BN * 9);
+          nn = r / 9;
+          const int t = r - nn * 9;
+          tap = 8 - t;
+          src = ((size_t)(kc * CK + cc) * Cout + ct * BN + nn) * 9 + t;
+        }
+      };
+      auto live = [&](int cc, int nn) { return ct * BN + nn < Cout && kc * CK + cc < Cin; };
+      f4 v4[PT4];
+#pragma unroll
+      for (int i = 0; i < PT4; ++i) {
+        const int g = (threadIdx.x + i * 256) * 4;
+        if (g >= SL) continue;
+        int tap, cc, nn, tap3, cc3, nn3;
+        size_t src, src3;
+        locate(g, tap, cc, nn, src);
+        locate(g + 3, tap3, cc3, nn3, src3);
+        if (live(cc, nn) && live(cc3, nn3)) {         // the group's first and last in range
+          v4[i] = *reinterpret_cast<const f4*>(w + src);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            int te, ce, ne;
+            size_t se;
+            locate(g + e, te, ce, ne, se);
+            v4[i][e] = live(ce, ne) ? w[se] : 0.f;
+          }
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < PT4; ++i) {
+        const int g0 = (threadIdx.x + i * 256) * 4;
+        if (g0 >= SL) continue;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          int tap, cc, nn;
+          size_t src;
+          locate(g0 + e, tap, cc, nn, src);
+          slice_lds[CI8 ? ((tap * (CK / 8) + cc / 8) * BN + nn) * RS + cc % 8
+                        : (tap * CK + cc) * RS + nn] = v4[i][e];
+        }
+      }
+      __syncthreads();
+      E* dst = out + (size_t)slice * SL;
+      for (int e = threadIdx.x; e < SL; e += 256) dst[e] = slice_lds[(e / ROW) * RS + e % ROW];
+      return;
+    }
+  }
   // All loads first (PT per thread in flight), then the LDS permutation.
   E v[PT];
   int pos[PT];
