@@ -408,9 +408,14 @@ __global__ __launch_bounds__(T::THREADS, 2 / T::KSPLIT) void conv3x3_igemm_f32(C
 }
 
 // ------------------------------------------------------ small whole images --
-template <int H_, int W_, int G_>
+template <int H_, int W_, int G_, int KSPLIT_ = 1>
 struct SmallTile {
   static constexpr int H = H_, W = W_, G = G_;
+  // KSPLIT = 2: two groups of 256 threads take alternate channel chunks
+  // through LDS buffers of their own and add their tiles in LDS at the end
+  // (as the two-group 8x8 tiles): half the split partials in HBM for the
+  // same number of resident waves.
+  static constexpr int KSPLIT = KSPLIT_, THREADS = 256 * KSPLIT;
   static constexpr int P = H * W;                 // positions per image
   static constexpr int IMGS = 16 * G;             // images per tile
   static constexpr int BM = IMGS * P;             // pixels per tile
@@ -430,9 +435,11 @@ struct SmallTile {
   static constexpr int MB = BM / 16;              // column blocks: (position, image group)
   static constexpr int OUT_IMG_STRIDE = BN * P + 4;
   static constexpr int LDS_OUT = IMGS * OUT_IMG_STRIDE;
-  static constexpr int LDS_FLOATS = 2 * LDS_BUF > LDS_OUT ? 2 * LDS_BUF : LDS_OUT;
+  static constexpr int LDS_FLOATS =
+      KSPLIT * 2 * LDS_BUF > LDS_OUT ? KSPLIT * 2 * LDS_BUF : LDS_OUT;
   static constexpr size_t LDS_BYTES = LDS_FLOATS * sizeof(float);
-  static_assert(LDS_BYTES <= 80 * 1024, "two blocks must fit in the 160 KB of LDS");
+  static_assert(LDS_BYTES * (KSPLIT == 1 ? 2 : 1) <= 160 * 1024,
+                "two blocks (one for KSPLIT = 2) must fit in the 160 KB of LDS");
   // Source position of tap (r,s) at position pos, or -1 if it is padding.
   __host__ __device__ static constexpr int src(int pos, int tap) {
     return (pos / W + tap / 3 - 1 >= 0 && pos / W + tap / 3 - 1 < H &&
@@ -443,9 +450,12 @@ struct SmallTile {
 };
 
 template <class T, bool DGRAD, class E>
-__global__ __launch_bounds__(256, 2) void conv3x3_small_f32(ConvArgs a) {
-  extern __shared__ float lds[];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+__global__ __launch_bounds__(T::THREADS, 2 / T::KSPLIT) void conv3x3_small_f32(ConvArgs a) {
+  extern __shared__ float lds_all[];
+  // grp: which chunk stream this thread's 256-thread group takes.
+  const int grp = threadIdx.x >> 8;
+  float* lds = lds_all + grp * 2 * T::LDS_BUF;
+  const int tid = threadIdx.x & 255, lane = tid & 63, wave = tid >> 6;
   const int kq = lane >> 4, lr = lane & 15;
   const int n0 = blockIdx.x * T::IMGS;
   const int co0 = blockIdx.y * T::BN;
@@ -524,32 +534,61 @@ __global__ __launch_bounds__(256, 2) void conv3x3_small_f32(ConvArgs a) {
       }
   };
 
-  const int nk = kc1 - kc0;
+  // Group g takes chunks kc0 + g, kc0 + g + KSPLIT, ...; every group runs
+  // the same number of iterations (barriers are block-wide).
+  const int nk = (kc1 - kc0 - grp + T::KSPLIT - 1) / T::KSPLIT;
+  const int nit = (kc1 - kc0 + T::KSPLIT - 1) / T::KSPLIT;
+  auto chunk = [&](int t) { return kc0 + grp + t * T::KSPLIT; };
   if (nk > 0) {
-    gload(kc0);
+    gload(chunk(0));
     lstore(0);
-    if (nk > 1) gload(kc0 + 1);
+    if (nk > 1) gload(chunk(1));
   }
   __syncthreads();
-  for (int t = 0; t < nk; ++t) {
+  for (int t = 0; t < nit; ++t) {
     const int buf = t & 1;
     if (t + 1 < nk) lstore(buf ^ 1);
-    if (t + 2 < nk) gload(kc0 + t + 2);
-    compute(buf);
+    if (t + 2 < nk) gload(chunk(t + 2));
+    if (t < nk) compute(buf);
+    __syncthreads();
+  }
+  if constexpr (T::KSPLIT == 2) {
+    // Group 1 hands its tile to group 0 through LDS (lane-major:
+    // conflict-free), group 0 adds it; both then take part in the staging
+    // barrier below, and group 1 leaves before the stores.
+    static_assert(4 * 64 * 4 * T::MB <= T::LDS_FLOATS, "partial tile fits the LDS");
+    float* xfer = lds_all + (size_t)(wave * T::MB * 4) * 64 + lane;
+    if (grp == 1) {
+#pragma unroll
+      for (int mb = 0; mb < T::MB; ++mb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) xfer[(mb * 4 + i) * 64] = acc[mb][i];
+    }
+    __syncthreads();
+    if (grp == 0) {
+#pragma unroll
+      for (int mb = 0; mb < T::MB; ++mb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc[mb][i] += xfer[(mb * 4 + i) * 64];
+    }
     __syncthreads();
   }
 
   // Stage the tile as [image][channel][position] so rows of the output go
   // out as float4 stores.  acc[mb] lane holds channel wave*16 + 4*kq + i of
   // image g*16 + lr at position pos (mb = pos*G + g).
+  if (grp == 0) {
 #pragma unroll
-  for (int mb = 0; mb < T::MB; ++mb) {
-    const int pos = mb / T::G, g = mb % T::G;
+    for (int mb = 0; mb < T::MB; ++mb) {
+      const int pos = mb / T::G, g = mb % T::G;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      lds[(g * 16 + lr) * T::OUT_IMG_STRIDE + (wave * 16 + kq * 4 + i) * T::P + pos] = acc[mb][i];
+      for (int i = 0; i < 4; ++i)
+        lds_all[(g * 16 + lr) * T::OUT_IMG_STRIDE + (wave * 16 + kq * 4 + i) * T::P + pos] =
+            acc[mb][i];
+    }
   }
   __syncthreads();
+  if (grp != 0) return;
   // The tile's output: for each image, channels [co0, co0+BN) x P positions
   // are contiguous in NCHW.  float4 q -> (image, channel, quarter).
   constexpr int OUT_F4 = T::IMGS * T::BN * T::P / 4;
@@ -611,6 +650,8 @@ using TileW8L = ConvTile<8, 8, 4, 8, 64, 1, 1, 1>;
 using TileW8K2 = ConvTile<8, 8, 2, 8, 64, 2, 2, 1>;
 using Small2 = SmallTile<2, 2, 2>;
 using Small4 = SmallTile<4, 4, 1>;
+using Small2K2 = SmallTile<2, 2, 2, 2>;
+using Small4K2 = SmallTile<4, 4, 1, 2>;
 
 static const char* kTileNames[] = {
     "sb::conv3x3_igemm_f32<sb::ConvTile<4, 32, 1, 8, 64, 2, 1, 1>, %s, %s>",
@@ -620,12 +661,14 @@ static const char* kTileNames[] = {
     "sb::conv3x3_igemm_f32<sb::ConvTile<2, 2, 32, 8, 64, 2, 1, 0>, %s, %s>",
     "sb::conv3x3_igemm_f32<sb::ConvTile<4, 32, 1, 4, 64, 2, 1, 1>, %s, %s>",
     "sb::conv3x3_igemm_f32<sb::ConvTile<4, 32, 1, 8, 16, 1, 1, 0>, %s, %s>",
-    "sb::conv3x3_small_f32<sb::SmallTile<2, 2, 2>, %s, %s>",
-    "sb::conv3x3_small_f32<sb::SmallTile<4, 4, 1>, %s, %s>",
+    "sb::conv3x3_small_f32<sb::SmallTile<2, 2, 2, 1>, %s, %s>",
+    "sb::conv3x3_small_f32<sb::SmallTile<4, 4, 1, 1>, %s, %s>",
     "sb::conv3x3_igemm_f32<sb::ConvTile<8, 32, 1, 8, 64, 1, 1, 1>, %s, %s>",
     "sb::conv3x3_igemm_f32<sb::ConvTile<16, 16, 1, 8, 64, 1, 1, 1>, %s, %s>",
     "sb::conv3x3_igemm_f32<sb::ConvTile<8, 8, 4, 8, 64, 1, 1, 1>, %s, %s>",
     "sb::conv3x3_igemm_f32<sb::ConvTile<8, 8, 2, 8, 64, 2, 2, 1>, %s, %s>",
+    "sb::conv3x3_small_f32<sb::SmallTile<2, 2, 2, 2>, %s, %s>",
+    "sb::conv3x3_small_f32<sb::SmallTile<4, 4, 1, 2>, %s, %s>",
 };
 
 // allow_small: the whole-image kernel needs tensors aligned for 4-element
@@ -654,6 +697,12 @@ static IgemmPlan igemm_plan(int N, int Cin, int H, int W, int Cout, int esize,
   // 8x8-image tiles that cannot fill the chip take the two-group block
   // (intra-block split over channel chunks) before any split in HBM.
   if (p.tile == 2 && blocks < 512 && p.nchunks >= 4) { p.tile = 12; blocks *= 2; }
+  // Whole-image tiles likewise: two groups per block halve the split
+  // partials written to and read back from HBM.
+  if ((p.tile == 7 || p.tile == 8) && blocks < 512 && p.nchunks >= 4) {
+    p.tile = p.tile == 7 ? 13 : 14;
+    blocks *= 2;
+  }
   // About two resident 256-thread groups on each of the 256 CUs; at most 8
   // splits, and at least two chunks per split.
   const long target = 512;
@@ -706,7 +755,7 @@ static void igemm_launch(const IgemmPlan& p, const ConvArgs& a, bool pack, hipSt
   ConvArgs k = a;
   if (p.splits > 1) { k.bias = nullptr; k.mask = nullptr; k.relu = 0; }
   if constexpr (SMALL) {
-    conv3x3_small_f32<T, DGRAD, E><<<grid, 256, T::LDS_BYTES, st>>>(k);
+    conv3x3_small_f32<T, DGRAD, E><<<grid, T::THREADS, T::LDS_BYTES, st>>>(k);
   } else {
     if constexpr (can_whole) {
       if (whole) conv3x3_igemm_f32<T, DGRAD, E, true><<<grid, T::THREADS, T::LDS_BYTES, st>>>(k);
@@ -737,7 +786,9 @@ static void igemm_dispatch(const IgemmPlan& p, const ConvArgs& a, bool pack, hip
     case 9: igemm_launch<TileW32L, DGRAD, false, E>(p, a, pack, st); break;
     case 10: igemm_launch<TileW16L, DGRAD, false, E>(p, a, pack, st); break;
     case 11: igemm_launch<TileW8L, DGRAD, false, E>(p, a, pack, st); break;
-    default: igemm_launch<TileW8K2, DGRAD, false, E>(p, a, pack, st); break;
+    case 12: igemm_launch<TileW8K2, DGRAD, false, E>(p, a, pack, st); break;
+    case 13: igemm_launch<Small2K2, DGRAD, true, E>(p, a, pack, st); break;
+    default: igemm_launch<Small4K2, DGRAD, true, E>(p, a, pack, st); break;
   }
 }
 
