@@ -416,6 +416,52 @@ class ExchangeWorkload(Workload):
                           "thread), %.1f s" % (reps, dt)}
 
 
+
+class AverageWorkload(Workload):
+    """Model averaging of DP replicas (sec. 2, sec. 4) on one device."""
+    name = "average-f32"
+    dtype = "f32"
+    metric = "GB/s model averaging of data-parallel replicas on one GPU (fp32)"
+    text = ("model averaging of 4 data-parallel replicas held on one GPU: every replica's "
+            "VGG-16 conv parameters (14,714,688 fp32 weights and biases) replaced by the "
+            "mean of the 4, in place")
+    W = 4
+
+    def n(self):
+        from paper_2112_15317_amd import configs
+        return sum(L.k * L.c * 9 + L.k for L in configs.conv_layers(configs.VGG16, 3, 32))
+
+    def build(self):
+        import torch
+        from paper_2112_15317_amd import sb, synth
+        self.p = torch.from_numpy(synth.normal((self.W, self.n()), 0, synth.TID.MISC + 15)).cuda()
+        return [(("avg", 0), sb.sb_model_average, (self.W, 1, self.p))]
+
+    def call_bytes(self, kind):
+        return 2 * self.W * self.n() * 4          # every slot read once and written once
+
+    def bytes_per_step(self):
+        return self.call_bytes("avg")
+
+    def flops(self):
+        return {"nominal": 0, "valid": 0}
+
+    def cpu_baseline(self, sample):
+        from oracle import average as OA
+        from paper_2112_15317_amd import synth
+        rows = sample or 1 << 20                   # parameters per replica in the sample
+        p = synth.normal((self.W, rows), 0, synth.TID.MISC + 15)
+        reps = 0
+        t0 = time.perf_counter()
+        while reps == 0 or time.perf_counter() - t0 < 10.0:   # about 10 s of CPU work
+            OA.model_average(p, 1)
+            reps += 1
+        dt = time.perf_counter() - t0
+        return {"value": round(reps * 2 * self.W * rows * 4 / dt / 1e9, 3), "unit": "GB/s",
+                "cores": 1, "kind": "oracle",
+                "sample": "%d x averaging 4 replicas of %d parameters (fp64 numpy oracle, one "
+                          "thread), %.1f s" % (reps, rows, dt)}
+
 def workloads():
     from paper_2112_15317_amd import configs
     return {
@@ -446,6 +492,7 @@ def workloads():
             "log-softmax + NLL of the 10-class logits, bwd, SGD (conv at lr, FC shards at "
             "lr/2), fp32", train=True),
         "exchange-f32": ExchangeWorkload(),
+        "average-f32": AverageWorkload(),
     }
 
 
@@ -470,6 +517,8 @@ def kernel_name(key, call_args, dtype):
         return "sb::log_softmax_nll_kernel"
     if kind == "sgd":
         return "sb::sgd_update_kernel"
+    if kind == "avg":
+        return "sb::model_average_kernel<4>"
     return "sb::relu_maxpool_%s_kernel<%s, 2>" % (
         kind.split("_")[1], "float" if dtype == "f32" else "unsigned short")
 
@@ -481,7 +530,7 @@ def call_work(wl, key, args):
         return layer_flops(wl.layers[i], args[0].n)[0], "flop"
     if kind.startswith("fc_"):
         return fc_flops(args[0], kind, kind == "fc_fwd" or args[5] is not None), "flop"
-    if kind in ("mfwd", "mbwd", "sfwd", "sbwd", "loss", "sgd"):
+    if kind in ("mfwd", "mbwd", "sfwd", "sbwd", "loss", "sgd", "avg"):
         return wl.call_bytes(kind), "bytes"
     esize = 4 if wl.dtype == "f32" else 2
     if kind == "pack":             # every layer's filters read, twice packed written

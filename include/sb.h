@@ -311,6 +311,21 @@ sb_status sb_shard_bwd(const sb_shard_desc *desc, int iproc,
                        const float *dfull, size_t df_stride, float *dparts,
                        size_t dp_stride, void *stream);
 
+/* Model averaging (sec. 2: data-parallel replicas reach a global model by
+ * averaging; sec. 4: every worker exchanges its parameters up to the modulo
+ * layer every few batches, and the FC model shards are averaged across the
+ * MP groups).  params holds `workers` slots of n fp32 elements (worker w at
+ * w * stride elements, stride >= n).  Worker g * mp + r holds shard r of
+ * group g (sec. 3.2), so each slot is replaced, in place, by the mean over
+ * the workers holding the same parameters:
+ *   mp = 1: all workers (the conv layers' replicas);
+ *   mp > 1: the workers r, mp + r, 2 mp + r, ... (FC shard r across groups).
+ * Each mean is the sum in increasing worker id, divided once by the count.
+ * workers must be a multiple of mp; slots must not overlap (stride >= n).
+ * n = 0 does nothing. */
+sb_status sb_model_average(int workers, int mp, size_t n, float *params,
+                           size_t stride, void *stream);
+
 /* ------------------------------------------------------------------------
  * Loss and parameter update (NEXT after the worker's forward and backward).
  *

@@ -95,6 +95,30 @@ __global__ __launch_bounds__(256) void shard_bwd_kernel(const float* __restrict_
   st<V>(dparts + (size_t)(g + r) * dps + rem, acc);
 }
 
+// Model averaging: one thread per V consecutive elements of one averaging
+// set (shard r): the set's slots r, mp + r, ... are read in increasing
+// worker id and all of them receive the sum divided by their count.
+template <int V>
+__global__ __launch_bounds__(256) void model_average_kernel(float* __restrict__ p, size_t stride,
+                                                            int mp, int groups, size_t per_slot,
+                                                            size_t total) {
+  const size_t q = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (q >= total) return;
+  const int r = (int)(q / per_slot);
+  float* base = p + (size_t)r * stride + (q - (size_t)r * per_slot) * V;
+  const size_t step = (size_t)mp * stride;
+  typename VecOf<V>::T acc = ld<V>(base);
+  for (int g = 1; g < groups; ++g) acc += ld<V>(base + g * step);
+  const float cnt = (float)groups;
+  if constexpr (V == 1) {
+    acc = acc / cnt;
+  } else {
+#pragma unroll
+    for (int j = 0; j < V; ++j) acc[j] = acc[j] / cnt;
+  }
+  for (int g = 0; g < groups; ++g) st<V>(base + g * step, acc);
+}
+
 }  // namespace sb
 
 using namespace sb;
@@ -213,5 +237,27 @@ extern "C" sb_status sb_shard_bwd(const sb_shard_desc* d, int iproc, const float
   else
     shard_bwd_kernel<1><<<blocks_for(total), 256, 0, st>>>(
         dfull, df_stride, dparts, dp_stride, g, mp, d->rows, d->shard, total);
+  return sbh::launch_status();
+}
+
+extern "C" sb_status sb_model_average(int workers, int mp, size_t n, float* params, size_t stride,
+                                      void* stream) {
+  if (workers < 1 || mp < 1 || workers % mp != 0) return SB_ERR_INVALID_ARG;
+  if (n == 0) return SB_OK;
+  if (!params || stride < n) return SB_ERR_INVALID_ARG;
+  if ((uint64_t)(workers - 1) * stride + n >= (1ull << 40)) return SB_ERR_UNSUPPORTED;
+  const int groups = workers / mp;
+  if (groups == 1) return SB_OK;                  // one worker per set: nothing to average
+  hipStream_t st = sbh::stream_of(stream);
+  const bool v4 = n % 4 == 0 && stride % 4 == 0 && aligned16(params);
+  if (v4) {
+    const size_t per = n / 4, total = per * mp;
+    model_average_kernel<4><<<blocks_for(total), 256, 0, st>>>(params, stride, mp, groups, per,
+                                                               total);
+  } else {
+    const size_t total = n * mp;
+    model_average_kernel<1><<<blocks_for(total), 256, 0, st>>>(params, stride, mp, groups, n,
+                                                               total);
+  }
   return sbh::launch_status();
 }

@@ -74,6 +74,7 @@ SIGNATURES = {
     "sb_modulo_bwd": (_i, [ctypes.POINTER(sb_modulo_desc), _i, _i, _vp, _sz, _vp, _sz, _vp]),
     "sb_shard_fwd": (_i, [ctypes.POINTER(sb_shard_desc), _i, _vp, _sz, _vp, _vp]),
     "sb_shard_bwd": (_i, [ctypes.POINTER(sb_shard_desc), _i, _vp, _sz, _vp, _sz, _vp]),
+    "sb_model_average": (_i, [_i, _i, _sz, _vp, _sz, _vp]),
     "sb_log_softmax_nll": (_i, [_i, _i, _i, _vp, _vp, ctypes.c_float, _vp, _vp, _vp, _vp]),
     "sb_sgd_update": (_i, [_i, ctypes.POINTER(_vp), ctypes.POINTER(_vp), ctypes.POINTER(_sz),
                            ctypes.POINTER(ctypes.c_float), ctypes.c_float, _vp]),
@@ -305,6 +306,14 @@ def sb_shard_bwd(desc, iproc, dfull, dparts, df_stride=None, dp_stride=None, str
         ctypes.byref(desc), int(iproc), _ptr(dfull),
         _slot_stride(dfull, desc.workers, df_stride), _ptr(dparts),
         _slot_stride(dparts, desc.workers, dp_stride), _stream(stream)))
+
+
+def sb_model_average(workers, mp, params, n=None, stride=None, stream=None):
+    """params: `workers` slots of fp32 parameters (a contiguous
+    [workers][...] tensor by default: n = stride = numel / workers)."""
+    st = _slot_stride(params, workers, stride)
+    _check("sb_model_average", load().sb_model_average(
+        int(workers), int(mp), int(st if n is None else n), _ptr(params), st, _stream(stream)))
 
 
 # --------------------------------------------------- loss and SGD update --

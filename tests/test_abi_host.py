@@ -233,3 +233,14 @@ def test_loss_and_sgd_argument_validation():
     assert sgd([P, P + 32], [P + 8192, P + 12288], [16, 16], [1.0, 1.0]) == sb.SB_ERR_INVALID_ARG
     # Only empty tensors: nothing to do.
     assert sgd([None], [None], [0], [1.0]) == sb.SB_OK
+
+
+def test_model_average_argument_validation():
+    avg = lambda *a: _raw("sb_model_average", *a)
+    assert avg(0, 1, 16, P, 16, None) == sb.SB_ERR_INVALID_ARG
+    assert avg(4, 0, 16, P, 16, None) == sb.SB_ERR_INVALID_ARG
+    assert avg(6, 4, 16, P, 16, None) == sb.SB_ERR_INVALID_ARG      # not whole groups
+    assert avg(4, 1, 16, None, 16, None) == sb.SB_ERR_INVALID_ARG
+    assert avg(4, 1, 16, P, 8, None) == sb.SB_ERR_INVALID_ARG       # slots would overlap
+    assert avg(4, 1, 0, None, 0, None) == sb.SB_OK                  # nothing to average
+    assert avg(4, 4, 16, P, 16, None) == sb.SB_OK                   # one worker per set
