@@ -135,7 +135,17 @@ __device__ __forceinline__ void pack_slice(const E* __restrict__ w, E* __restric
       }
       __syncthreads();
       E* dst = out + (size_t)slice * SL;
-      for (int e = threadIdx.x; e < SL; e += 256) dst[e] = slice_lds[(e / ROW) * RS + e % ROW];
+      if (((uintptr_t)out & 15) == 0) {
+        // Rows of ROW (a multiple of 4) elements: a group of 4 never crosses
+        // a row, and each slice starts 16-byte aligned (SL % 4 == 0).
+        static_assert(ROW % 4 == 0, "whole groups per LDS row");
+        for (int e = threadIdx.x * 4; e < SL; e += 1024) {
+          const float* l = slice_lds + (e / ROW) * RS + e % ROW;
+          *reinterpret_cast<f4*>(dst + e) = f4{l[0], l[1], l[2], l[3]};
+        }
+      } else {
+        for (int e = threadIdx.x; e < SL; e += 256) dst[e] = slice_lds[(e / ROW) * RS + e % ROW];
+      }
       return;
     }
   }

@@ -4,9 +4,12 @@
 //   db[k]       = sum_{n,h,w} dy[n,k,h,w]
 //
 // GEMM view: rows = output channels k, columns = (input channel c, tap),
-// reduction = every pixel of the batch.  Blocks of the first column tile also
-// multiply dy against a column of ones, which yields the bias gradient in
-// the same pass.  Three kernels:
+// reduction = every pixel of the batch.  The bias gradient comes in the same
+// pass: each lane adds up the dy operands it feeds the MFMAs on the vector
+// ALU (which runs beside the matrix pipe), and a butterfly over the lanes
+// completes the row sums; only blocks of the first column tile write them.
+// An MFMA against a column of ones in those blocks alone would make them
+// the slowest of the grid.  Three kernels:
 //
 // conv3x3_wgrad_f32 (any shape).  A block owns 64 k and walks a contiguous
 // range of 64-pixel tiles (IMGS images x TH rows x TW cols).  Per pixel tile
@@ -207,6 +210,19 @@ inline void launch_splits_reduce(const float* part, int splits, int K, int C, fl
                                                                 wsz, dw, db);
 }
 
+// Bias gradient of a wave's 16 rows, summed on the vector ALU beside the
+// MFMAs: lane (jq, lr) has added the dy values it supplied as MFMA operand
+// (row lr, the pixels of lane group jq).  Returns the row sums in the MFMA
+// result layout the stores expect: element i of lane (jq, lr) is row
+// 4 jq + i.  A fixed butterfly: bitwise reproducible.
+__device__ __forceinline__ f4 wave_row_sums(float s) {
+  s += __shfl_xor(s, 16, 64);
+  s += __shfl_xor(s, 32, 64);
+  const int jq = (threadIdx.x & 63) >> 4;
+  return f4{__shfl(s, 4 * jq + 0, 64), __shfl(s, 4 * jq + 1, 64), __shfl(s, 4 * jq + 2, 64),
+            __shfl(s, 4 * jq + 3, 64)};
+}
+
 // Writes a block's weight gradient of 64 k x (16 c x 9 taps): acc[t] of wave
 // w, lane (jq, lr) holds rows k0 + 16 w + 4 jq + i, channel c0 + lr, tap t.
 // The tile goes out through LDS (64 x 148 floats, free when this is called)
@@ -333,7 +349,8 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_f32(WgArgs a) {
     col_off[cb] = col_ok[cb] ? ((t / 3) * T::HW + (t % 3)) * T::BC + c : 0;
   }
 
-  f4 acc[T::NACC], accb = f4{0.f, 0.f, 0.f, 0.f};
+  f4 acc[T::NACC];
+  float sbias = 0.f;     // this lane's share of its row's bias gradient
 #pragma unroll
   for (int t = 0; t < T::NACC; ++t) acc[t] = f4{0.f, 0.f, 0.f, 0.f};
 
@@ -470,7 +487,7 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_f32(WgArgs a) {
 #pragma unroll
       for (int t = 0; t < T::NACC; ++t)
         if (!wg_pad_step<T, WHOLE>(st, t)) acc[t] = mfma16x16x4(cur.a, cur.b[t], acc[t]);
-      if (do_db) accb = mfma16x16x4(cur.a, 1.0f, accb);
+      sbias += cur.a;
       if (st + 1 < T::BP / 4) cur = nxt;
     }
   };
@@ -490,6 +507,7 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_f32(WgArgs a) {
     __syncthreads();
   }
 
+  const f4 accb = wave_row_sums(sbias);
   if constexpr (!T::NARROW) {
     static_assert(64 * (16 * 9 + 4) * sizeof(float) <= T::LDS_BYTES, "tile fits the LDS");
     wgrad_store_rows(a, blk.z, k0, c0, do_db, accb, acc, lds);
@@ -526,8 +544,8 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_f32(WgArgs a) {
 // wave owns all 64 k x 16 c for one of the two steps, so one B operand read
 // from LDS feeds four MFMAs (and an A read nine); with BC = 16, 32 k x 16 c
 // for one step.  The two step halves of a wave's columns are summed through
-// LDS at the end.  The bias gradient is one more MFMA per 16 k rows and step
-// against a column of ones.
+// LDS at the end.  The bias gradient adds the dy operands on the vector ALU
+// (bf16 pair dot products against ones, fp32 sums).
 //
 // Staging moves V consecutive columns per lane (V = 8, 4, 2 when the image
 // width is a multiple of V, else 1): one global load of V elements per tile
@@ -579,15 +597,13 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_bf16(WgArgs a) {
   const int HWs = a.H * a.W;
 
   f4 acc[T::MA][9], accb[T::MA];
+  float sbias[T::MA];    // this lane's share of the bias gradient of row block m
 #pragma unroll
   for (int m = 0; m < T::MA; ++m) {
-    accb[m] = f4{0.f, 0.f, 0.f, 0.f};
+    sbias[m] = 0.f;
 #pragma unroll
     for (int t = 0; t < 9; ++t) acc[m][t] = f4{0.f, 0.f, 0.f, 0.f};
   }
-  s8 ones;
-#pragma unroll
-  for (int j = 0; j < 8; ++j) ones[j] = 0x3f80;     // bf16 1.0
 
   // Staging geometry: LPR lanes per tile row piece of TW columns, RPI rows
   // per round of 256 threads.  dy rows are (k, tile row), k-major; x rows
@@ -738,12 +754,21 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_bf16(WgArgs a) {
               __builtin_bit_cast(bf16x8, av[m]), __builtin_bit_cast(bf16x8, bv), acc[m][t], 0, 0,
               0);
       }
-      if (do_db) {
+      // Bias gradient: the 8 dy values of each A operand added into fp32 by
+      // four bf16 pair dot products against (1, 1) on the vector ALU.
+      typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+      const bf16x2 one2 = {(__bf16)1.0f, (__bf16)1.0f};
 #pragma unroll
-        for (int m = 0; m < T::MA; ++m)
-          accb[m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-              __builtin_bit_cast(bf16x8, av[m]), __builtin_bit_cast(bf16x8, ones), accb[m], 0, 0,
-              0);
+      for (int m = 0; m < T::MA; ++m) {
+        const bf16x8 v = __builtin_bit_cast(bf16x8, av[m]);
+        sbias[m] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(v, v, 0, 1), one2,
+                                                   sbias[m], false);
+        sbias[m] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(v, v, 2, 3), one2,
+                                                   sbias[m], false);
+        sbias[m] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(v, v, 4, 5), one2,
+                                                   sbias[m], false);
+        sbias[m] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(v, v, 6, 7), one2,
+                                                   sbias[m], false);
       }
     }
   };
@@ -762,6 +787,8 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_bf16(WgArgs a) {
     compute(buf);
     __syncthreads();
   }
+#pragma unroll
+  for (int m = 0; m < T::MA; ++m) accb[m] = wave_row_sums(sbias[m]);
 
   // Sum the two step halves: waves wp = 1 hand their accumulators to the
   // waves wp = 0 of the same (wk, wc) through LDS (lane fastest, so the
@@ -916,7 +943,8 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_small_f32(WgArgs a) {
     x_loff[i] = ((quarter * 4) * T::IW + img) * T::BC + cc;
   }
 
-  f4 acc[9], accb = f4{0.f, 0.f, 0.f, 0.f};
+  f4 acc[9];
+  float sbias = 0.f;     // this lane's share of its row's bias gradient
 #pragma unroll
   for (int t = 0; t < 9; ++t) acc[t] = f4{0.f, 0.f, 0.f, 0.f};
 
@@ -968,7 +996,7 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_small_f32(WgArgs a) {
           const int sp = T::src(pos, t);
           if (sp >= 0) acc[t] = mfma16x16x4(av[pos], bv[sp], acc[t]);
         }
-        if (do_db) accb = mfma16x16x4(av[pos], 1.0f, accb);
+        sbias += av[pos];
       }
     }
   };
@@ -989,7 +1017,7 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_small_f32(WgArgs a) {
   }
 
   static_assert(64 * (16 * 9 + 4) * sizeof(float) <= T::LDS_BYTES, "tile fits the LDS");
-  wgrad_store_rows(a, blk.z, k0, c0, do_db, accb, acc, lds);
+  wgrad_store_rows(a, blk.z, k0, c0, do_db, wave_row_sums(sbias), acc, lds);
 }
 
 // ------------------------------------------------- 2x2 images: one GEMM --
@@ -1005,7 +1033,7 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_small_f32(WgArgs a) {
 // images per LDS stage, double-buffered; both operands are staged as
 // [image][row] with 16-byte loads of 4 consecutive rows.  The fold runs in
 // the epilogue through LDS (G is never written out); the bias gradient is
-// one more MFMA per row block against a column of ones, in the first
+// summed from the dy operands on the vector ALU and written by the first
 // column tile's blocks.  Splits over the images write partials as the other
 // weight-gradient kernels do.
 struct Wg2 {
@@ -1033,10 +1061,11 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_2x2(WgArgs a) {
   const int s1 = min(a.ptiles, s0 + a.tiles_per_split);
   const bool do_db = a.db != nullptr && ct == 0 && wn == 0;   // wave-uniform
 
-  f4 acc[4][4], accb[4];
+  f4 acc[4][4];
+  float sbias[4];        // this lane's share of the bias gradient of rows i*16 + lr
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    accb[i] = f4{0.f, 0.f, 0.f, 0.f};
+    sbias[i] = 0.f;
 #pragma unroll
     for (int n = 0; n < 4; ++n) acc[i][n] = f4{0.f, 0.f, 0.f, 0.f};
   }
@@ -1089,10 +1118,8 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_2x2(WgArgs a) {
         for (int i = 0; i < 4; ++i)
 #pragma unroll
           for (int n = 0; n < 4; ++n) acc[i][n] = mfma16x16x4(fa[i][j], fb[n][j], acc[i][n]);
-        if (do_db) {
 #pragma unroll
-          for (int i = 0; i < 4; ++i) accb[i] = mfma16x16x4(fa[i][j], 1.0f, accb[i]);
-        }
+        for (int i = 0; i < 4; ++i) sbias[i] += fa[i][j];
       }
     }
   };
@@ -1147,15 +1174,19 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_2x2(WgArgs a) {
       for (int t = 0; t < 9; ++t) out[((size_t)k * a.C + c) * 9 + t] = t9[t];
     }
   }
-  if (do_db && lr == 0) {
+  // Bias gradient: row i*16 + lr of the wave is (k = 4i + lr/4, p = lr%4);
+  // sum over the lane groups (images), then over p (a fixed butterfly).
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int k = kb + i * 4 + kq;
-      if (k < a.K) {
-        const float v = (accb[i][0] + accb[i][1]) + (accb[i][2] + accb[i][3]);
-        if (a.splits == 1) a.db[k] = v;
-        else out[wsz + k] = v;
-      }
+  for (int i = 0; i < 4; ++i) {
+    float v = sbias[i];
+    v += __shfl_xor(v, 16, 64);
+    v += __shfl_xor(v, 32, 64);
+    v += __shfl_xor(v, 1, 64);
+    v += __shfl_xor(v, 2, 64);
+    const int k = kb + i * 4 + (lr >> 2);
+    if (do_db && kq == 0 && (lr & 3) == 0 && k < a.K) {
+      if (a.splits == 1) a.db[k] = v;
+      else out[wsz + k] = v;
     }
   }
 }
