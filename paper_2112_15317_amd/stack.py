@@ -4,8 +4,9 @@ A worker of the paper's hybrid scheme runs the convolutional layers on its
 local batch (data parallel) and its FC column shards on the batch gathered
 from all replicas (model parallel); backward retraces the same path (sec.
 3.1 and sec. 4).  These classes own the device buffers of that step and
-enqueue the libsb calls in order on one stream.  They do no arithmetic: every
-value is produced by a libsb kernel.  torch only allocates device memory.
+enqueue the libsb calls in order (the conv weight gradients on a second
+stream, see ``ConvStack``).  They do no arithmetic: every value is produced
+by a libsb kernel.  torch only allocates device memory and orders streams.
 
 ``ConvStack``   13-layer VGG conv stack fwd + bwd (ReLU, fused ReLU + pool)
 ``FCShard``     one FC column shard fwd + bwd
@@ -58,10 +59,16 @@ class ConvStack:
              i.e. it is the gradient of that layer's conv output
       dZ[l]  gradient at the conv output of a pooled layer (pool backward)
       dW[l], db[l]  fp32 parameter gradients
+
+    overlap: in backward the weight gradient of each layer runs on a second
+    stream, forked after its output gradient is ready and joined at the end,
+    so it overlaps the data-gradient chain (the two only share inputs, and
+    each has its own split-reduction workspace).  Kernel tails, small grids
+    and split reductions of one chain then fill CUs the other leaves idle.
     """
 
     def __init__(self, schedule, n, in_ch, hw, dtype="f32", device="cuda",
-                 out_buffer=None, out_grad_buffer=None, packed=True):
+                 out_buffer=None, out_grad_buffer=None, packed=True, overlap=True):
         self.layers = conv_layers(schedule, in_ch, hw)
         if not self.layers[-1].pool_after:
             raise ValueError("the stack must end with a pooled layer")
@@ -128,6 +135,14 @@ class ConvStack:
                        sb.sb_conv3x3_workspace_bytes(self.desc_b[l.index], sb.SB_PASS_BWD_WEIGHT))
         # Split-reduction scratch; needs no initialisation.
         self.ws = torch.empty((max(need, 256) + 255) // 256 * 256, dtype=torch.uint8, device=dev)
+        self.overlap = overlap and dev.type == "cuda"
+        self.ws_w = self.ws
+        if self.overlap:
+            need_w = max(sb.sb_conv3x3_workspace_bytes(self.desc_b[l.index], sb.SB_PASS_BWD_WEIGHT)
+                         for l in L)
+            self.ws_w = torch.empty((max(need_w, 256) + 255) // 256 * 256, dtype=torch.uint8,
+                                    device=dev)
+            self.side = torch.cuda.Stream(device=dev)     # default priority
         self.call = _plain      # hook: every libsb call of the step goes through it
 
     # -- data placement (host -> device copies of seeded inputs) --------------
@@ -164,6 +179,11 @@ class ConvStack:
     def backward(self, stream=None, want_dx=True):
         c = self.call
         L = self.layers
+        # Two streams only for the real calls: a recorded call list
+        # (step_calls) stays stream-agnostic.
+        fork = self.overlap and c is _plain
+        if fork:
+            main = stream if stream is not None else torch.cuda.current_stream(self.device)
         for l in reversed(L):
             i = l.index
             if l.pool_after:
@@ -172,8 +192,14 @@ class ConvStack:
                 g = self.dZ[i]
             else:
                 g = self.gA[i + 1]
+            ws_stream = stream
+            if fork:
+                ready = torch.cuda.Event()
+                ready.record(main)
+                self.side.wait_event(ready)
+                ws_stream = self.side
             c(("wgrad", i), sb.sb_conv3x3_bwd_weight, self.desc_b[i], self.A[i], g, self.dW[i],
-              self.db[i], self.ws, stream)
+              self.db[i], self.ws_w, ws_stream)
             w = self.Wb[i] if self.packed else self.W[i]
             if i > 0:
                 mask = None if L[i - 1].pool_after else self.A[i]
@@ -182,6 +208,10 @@ class ConvStack:
             elif want_dx:
                 c(("dgrad", i), sb.sb_conv3x3_bwd_data, self.pdesc_b[i], g, w, None,
                   self.gA[0], self.ws, stream)
+        if fork:
+            done = torch.cuda.Event()
+            done.record(self.side)
+            main.wait_event(done)
 
     def grad_at_conv_output(self, i):
         """Gradient at conv output i (after its ReLU / pool backward)."""
