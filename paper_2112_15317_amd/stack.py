@@ -179,9 +179,11 @@ class ConvStack:
     def backward(self, stream=None, want_dx=True):
         c = self.call
         L = self.layers
-        # Two streams only for the real calls: a recorded call list
-        # (step_calls) stays stream-agnostic.
-        fork = self.overlap and c is _plain
+        # Two streams only for the real calls (a recorded call list, from
+        # step_calls, stays stream-agnostic) and for a torch stream or the
+        # current one (a raw stream handle cannot record events here).
+        fork = (self.overlap and c is _plain and
+                (stream is None or isinstance(stream, torch.cuda.Stream)))
         if fork:
             main = stream if stream is not None else torch.cuda.current_stream(self.device)
         for l in reversed(L):
