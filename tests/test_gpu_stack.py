@@ -398,6 +398,45 @@ def test_graph_replay_matches_eager():
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_overlapped_backward_matches_single_stream(dtype):
+    """The weight gradients run on a second stream beside the data-gradient
+    chain; eagerly on a non-default torch stream and replayed from a graph,
+    the step must equal, bit for bit, the same step on one stream."""
+    from paper_2112_15317_amd.stack import capture_graph
+    n, hw = 4, 32
+    print_case("overlapped_backward", n=n, hw=hw, dtype=dtype)
+    layers = configs.conv_layers(configs.VGG16, 3, hw)
+    x, wts, bs = _vgg_inputs(n, hw, 10, layers)
+    dy_top = synth.normal((n, 512, 1, 1), 10, synth.TID.DY_TOP)
+    one = ConvStack(configs.VGG16, n, 3, hw, dtype, overlap=False)
+    two = ConvStack(configs.VGG16, n, 3, hw, dtype, overlap=True)
+    for st in (one, two):
+        st.load_inputs(x, wts, bs, dy_top)
+    one.step()
+    torch.cuda.synchronize()
+
+    def watch(st):
+        return [st.A[-1], st.gA[0]] + st.dW + st.db
+    ref = [t.clone() for t in watch(one)]
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        two.step(side)
+    torch.cuda.synchronize()
+    for a, b in zip(watch(two), ref):
+        assert torch.equal(a, b), "eager overlapped step differs"
+    g = capture_graph(two.step, 1)
+    for rep in range(2):
+        for t in watch(two):
+            t.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for a, b in zip(watch(two), ref):
+            assert torch.equal(a, b), "replay %d of the overlapped step differs" % rep
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_packed_filter_step_matches_unpacked(dtype):
     """The stack packs every layer's filters once per step on a side stream
     (SB_PACKED_FILTERS); the step must equal, bit for bit, a stack whose
