@@ -420,8 +420,15 @@ struct SmallTile {
   static constexpr int IMGS = 16 * G;             // images per tile
   static constexpr int BM = IMGS * P;             // pixels per tile
   static constexpr int CK = 8, BN = 64, BN_P = 80;
-  static constexpr int PLANE = P * IMGS;          // [position][image] per channel
-  static constexpr int PLANE_P = (PLANE + 63) / 64 * 64 + 16;
+  // Channel plane in LDS: [position][image], position rows PS = IMGS + 1
+  // apart.  The staging stores of a wave (4 positions x 8 channels x 2
+  // images for the 4x4 tile) then spread over 32 banks instead of 8; the
+  // operand reads (16 consecutive images of one row) stay conflict-free.
+  static constexpr int PS = IMGS + 1;
+  static constexpr int PLANE = P * PS;
+  // Channel stride: the smallest >= PLANE that is 16 mod 64, so the four
+  // k-rows of an operand read land in different banks.
+  static constexpr int PLANE_P = (PLANE - 16 + 63) / 64 * 64 + 16;
   static constexpr int LDS_X = CK * PLANE_P;
   static constexpr int LDS_W = 9 * CK * BN_P;
   static constexpr int LDS_BUF = LDS_X + LDS_W;
@@ -475,7 +482,7 @@ __global__ __launch_bounds__(T::THREADS, 2 / T::KSPLIT) void conv3x3_small_f32(C
     int n = n0 + img;
     x_off[i] = n < a.N ? img * a.Cin * T::P + quarter * 4 : -1;   // from image n0; + ci * P
     x_c[i] = c;
-    x_loff[i] = c * T::PLANE_P + quarter * 4 * T::IMGS + img;
+    x_loff[i] = c * T::PLANE_P + quarter * 4 * T::PS + img;
   }
   // Packed filter slice element e -> LDS row e / BN, column e % BN.
   int w_loff[T::WTS_PT];
@@ -511,7 +518,7 @@ __global__ __launch_bounds__(T::THREADS, 2 / T::KSPLIT) void conv3x3_small_f32(C
 #pragma unroll
     for (int i = 0; i < T::X_PT; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) X[x_loff[i] + j * T::IMGS] = rx[i][j];
+      for (int j = 0; j < 4; ++j) X[x_loff[i] + j * T::PS] = rx[i][j];
 #pragma unroll
     for (int i = 0; i < T::WTS_PT; ++i) Wl[w_loff[i]] = rw[i];
   };
@@ -528,7 +535,7 @@ __global__ __launch_bounds__(T::THREADS, 2 / T::KSPLIT) void conv3x3_small_f32(C
           const int pos = mb / T::G, g = mb % T::G;
           const int sp = T::src(pos, tap);
           if (sp < 0) continue;                       // padding: resolved at compile time
-          const float fb = X[(cg * 4 + kq) * T::PLANE_P + sp * T::IMGS + g * 16 + lr];
+          const float fb = X[(cg * 4 + kq) * T::PLANE_P + sp * T::PS + g * 16 + lr];
           acc[mb] = mfma16x16x4(fa, fb, acc[mb]);
         }
       }
