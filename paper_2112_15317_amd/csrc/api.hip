@@ -124,9 +124,15 @@ extern "C" sb_status sb_conv3x3_pack_filters_many(int count, const sb_conv3x3_de
     const size_t wb = (size_t)q.k * q.c * 9 * sbh::dsize(q.dtype);
     if (packed_bytes_[i] < need || sbh::overlaps(w[i], wb, packed[i], need))
       return SB_ERR_INVALID_ARG;
-    // Packed outputs must not overlap one another.
+    // Packed outputs must not overlap one another, nor any task's source
+    // filters (all tasks run in one launch).
     for (int j = 0; j < i; ++j)
       if (sbh::overlaps(packed[j], packed_bytes_[j], packed[i], need)) return SB_ERR_INVALID_ARG;
+    for (int j = 0; j < count; ++j) {
+      if (!w[j]) return SB_ERR_INVALID_ARG;
+      const size_t wbj = (size_t)descs[j].k * descs[j].c * 9 * sbh::dsize(descs[j].dtype);
+      if (sbh::overlaps(w[j], wbj, packed[i], need)) return SB_ERR_INVALID_ARG;
+    }
     const int slices =
         pass == SB_PASS_FWD
             ? sbh::conv_igemm_pack_task(false, q.dtype, q.n, q.c, q.h, q.w, q.k, w[i], packed[i],

@@ -389,6 +389,12 @@ extern "C" sb_status sb_fc_shard_fwd(const sb_fc_desc* d, const void* x, const v
   if (sbh::overlaps(y, yb, x, xb) || sbh::overlaps(y, yb, w, wb) ||
       sbh::overlaps(y, yb, b, b ? d->n_shard * sizeof(float) : 0))
     return SB_ERR_INVALID_ARG;
+  // The workspace (split partials) must not overlap any operand.
+  const size_t need = sb_fc_workspace_bytes(d, SB_FC_FWD);
+  if (need > 0 && (sbh::overlaps(ws, need, x, xb) || sbh::overlaps(ws, need, w, wb) ||
+                   sbh::overlaps(ws, need, y, yb) ||
+                   sbh::overlaps(ws, need, b, b ? d->n_shard * sizeof(float) : 0)))
+    return SB_ERR_INVALID_ARG;
   hipStream_t st = sbh::stream_of(stream);
   s = d->dtype == SB_BF16 ? fc_fwd_run<u16>(d, x, w, b, y, ws, ws_bytes, st)
                           : fc_fwd_run<float>(d, x, w, b, y, ws, ws_bytes, st);
@@ -453,6 +459,13 @@ extern "C" sb_status sb_fc_shard_bwd(const sb_fc_desc* d, const void* x, const v
   }
   size_t need = sb_fc_workspace_bytes(d, SB_FC_BWD);
   if (need > 0 && (!ws || ws_bytes < need)) return SB_ERR_WORKSPACE;
+  // The workspace (split partials) must not overlap any operand.
+  if (need > 0) {
+    for (int i = 0; i < 4; ++i)
+      if (sbh::overlaps(ws, need, ins[i], insb[i])) return SB_ERR_INVALID_ARG;
+    for (int o = 0; o < 3; ++o)
+      if (sbh::overlaps(ws, need, outs[o], outsb[o])) return SB_ERR_INVALID_ARG;
+  }
   hipStream_t st = sbh::stream_of(stream);
   s = d->dtype == SB_BF16
           ? fc_bwd_run<u16>(d, x, w, dy, mask, dxp, dw, db, accumulate, ws, ws_bytes, st)

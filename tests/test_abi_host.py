@@ -244,3 +244,37 @@ def test_model_average_argument_validation():
     assert avg(4, 1, 16, P, 8, None) == sb.SB_ERR_INVALID_ARG       # slots would overlap
     assert avg(4, 1, 0, None, 0, None) == sb.SB_OK                  # nothing to average
     assert avg(4, 4, 16, P, 16, None) == sb.SB_OK                   # one worker per set
+
+
+def test_pack_many_rejects_packing_over_another_tasks_filters():
+    d = sb.conv_desc(2, 3, 8, 8, 4)
+    need = sb.sb_conv3x3_packed_bytes(d, sb.SB_PASS_FWD)
+    n = 2
+    w0, w1, o0 = P, P + (1 << 20), P + (2 << 20)
+    args = lambda outs: (n, (sb.sb_conv3x3_desc * n)(d, d), (ctypes.c_int * n)(0, 1),
+                         (ctypes.c_void_p * n)(w0, w1), (ctypes.c_void_p * n)(*outs),
+                         (ctypes.c_size_t * n)(need, need), None)
+    # Task 0 packs into task 1's source filters (and the reverse): one launch
+    # would read and write the same bytes.
+    assert _raw("sb_conv3x3_pack_filters_many", *args([w1, o0])) == sb.SB_ERR_INVALID_ARG
+    assert _raw("sb_conv3x3_pack_filters_many", *args([o0, w0 + 16])) == sb.SB_ERR_INVALID_ARG
+
+
+def test_fc_workspace_must_not_overlap_operands():
+    d = sb.fc_desc(512, 4096, 1024)            # 32 output tiles: the reduction is split
+    need_f = sb.sb_fc_workspace_bytes(d, sb.SB_FC_FWD)
+    need_b = sb.sb_fc_workspace_bytes(d, sb.SB_FC_BWD)
+    assert need_f > 0 and need_b > 0
+    x, w, y = P, P + (16 << 20), P + (96 << 20)
+    ws = P + (128 << 20)
+    fwd = lambda ws_: _raw("sb_fc_shard_fwd", ctypes.byref(d), x, w, None, y, ws_, need_f, None)
+    assert fwd(x + 64) == sb.SB_ERR_INVALID_ARG          # over x
+    assert fwd(w + 4096) == sb.SB_ERR_INVALID_ARG        # over w
+    assert fwd(y - 1024) == sb.SB_ERR_INVALID_ARG        # over y
+    dy, dx, dw = P + (200 << 20), P + (240 << 20), P + (300 << 20)
+    ws = P + (400 << 20)
+    bwd = lambda ws_: _raw("sb_fc_shard_bwd", ctypes.byref(d), x, w, dy, None, dx, dw, None, 0,
+                           ws_, need_b, None)
+    for bad in (x, w, dy, dx, dw):
+        assert bwd(bad + 256) == sb.SB_ERR_INVALID_ARG
+
