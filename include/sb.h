@@ -163,6 +163,29 @@ sb_status sb_conv3x3_bwd_weight(const sb_conv3x3_desc *desc, const void *x,
                                 void *workspace, size_t workspace_bytes,
                                 void *stream);
 
+/* Weight gradient for callers that cannot allocate device memory: code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation.
+ * Computes exactly what sb_conv3x3_bwd_weight computes, with the same kernels
+ * and the same summation order (bit-identical results), but takes no
+ * workspace: the split partial sums go to a scratch array of
+ * SB_NOALLOC_SCRATCH_BYTES that the library keeps in device memory, one per
+ * device, reserved when the library's device code is first loaded on that
+ * device and held until the process ends.  The call itself allocates and
+ * frees nothing.
+ *  * The stream must belong to the current device (the scratch array used is
+ *    the current device's).
+ *  * Every call on a device shares that device's array, and its contents
+ *    after a call are dead.  Calls on one device that may overlap in time
+ *    (different streams without ordering between them) race on it: the
+ *    caller serialises them.
+ *  * SB_ERR_WORKSPACE when sb_conv3x3_workspace_bytes(desc,
+ *    SB_PASS_BWD_WEIGHT) exceeds SB_NOALLOC_SCRATCH_BYTES (nothing enqueued);
+ *    other errors as for sb_conv3x3_bwd_weight. */
+#define SB_NOALLOC_SCRATCH_BYTES (40u << 20)
+sb_status sb_conv3x3_bwd_weight_noalloc(const sb_conv3x3_desc *desc,
+                                        const void *x, const void *dy,
+                                        float *dw, float *db, void *stream);
+
 /* Describes the launch plan `pass` would use for `desc`: the name of the
  * main kernel as a profiler reports it, the grid and whether a split
  * reduction follows.  Writes at most `len` bytes (NUL-terminated) into buf

@@ -3,6 +3,8 @@
 // every check passes.
 #include "conv_common.hpp"
 
+#include <mutex>
+
 namespace sbh {
 int conv_igemm_pack_task(bool dgrad, int dtype, int N, int Cin, int H, int W, int Cout,
                          const void* wt, void* packed, sb::PackTask* t);
@@ -211,6 +213,61 @@ extern "C" sb_status sb_conv3x3_bwd_weight(const sb_conv3x3_desc* d, const void*
     return SB_ERR_INVALID_ARG;
   return sbh::conv_wgrad(d->dtype, d->n, d->c, d->h, d->w, d->k, x, dy, dw, db, ws, ws_bytes,
                          sbh::stream_of(stream));
+}
+
+// ---------------------------------------------------------------------------
+// Weight gradient without allocation: the split partial sums go to a scratch
+// array that the library holds in device memory.  `scratch` is a host-side
+// stand-in in host code: its device address is looked up once per device
+// (hipGetSymbolAddress, with that device current) and only that address is
+// ever handed to a kernel.
+namespace {
+constexpr size_t kScratchBytes = (size_t)SB_NOALLOC_SCRATCH_BYTES;
+__device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of the current device's scratch array.
+sb_status scratch_address(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return SB_ERR_HIP;
+  if (dev < 0 || dev >= kMaxDevices) return SB_ERR_UNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr)
+      return SB_ERR_HIP;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return SB_OK;
+}
+}  // namespace
+
+extern "C" sb_status sb_conv3x3_bwd_weight_noalloc(const sb_conv3x3_desc* d, const void* x,
+                                                   const void* dy, float* dw, float* db,
+                                                   void* stream) {
+  sb_status s = conv_check(d, SB_PASS_BWD_WEIGHT);
+  if (s != SB_OK) return s;
+  if (!x || !dy || !dw) return SB_ERR_INVALID_ARG;
+  size_t xb = act_bytes(d, d->c), dyb = act_bytes(d, d->k);
+  size_t dwb = (size_t)d->k * d->c * 9 * sizeof(float), dbb = db ? d->k * sizeof(float) : 0;
+  if (sbh::overlaps(dw, dwb, x, xb) || sbh::overlaps(dw, dwb, dy, dyb) ||
+      sbh::overlaps(db, dbb, x, xb) || sbh::overlaps(db, dbb, dy, dyb) ||
+      sbh::overlaps(dw, dwb, db, dbb))
+    return SB_ERR_INVALID_ARG;
+  const size_t need = sbh::conv_wgrad_ws(d->dtype, d->n, d->c, d->h, d->w, d->k);
+  if (need > kScratchBytes) return SB_ERR_WORKSPACE;
+  void* ws = nullptr;
+  s = scratch_address(&ws);
+  if (s != SB_OK) return s;
+  if (need && (sbh::overlaps(ws, need, dw, dwb) || sbh::overlaps(ws, need, db, dbb) ||
+               sbh::overlaps(ws, need, x, xb) || sbh::overlaps(ws, need, dy, dyb)))
+    return SB_ERR_INVALID_ARG;
+  return sbh::conv_wgrad(d->dtype, d->n, d->c, d->h, d->w, d->k, x, dy, dw, db, ws,
+                         kScratchBytes, sbh::stream_of(stream));
 }
 
 extern "C" size_t sb_conv3x3_plan_string(const sb_conv3x3_desc* d, int pass, char* buf,

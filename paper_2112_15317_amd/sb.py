@@ -26,6 +26,7 @@ SB_PACKED_FILTERS = 2
 SB_PASS_FWD, SB_PASS_BWD_DATA, SB_PASS_BWD_WEIGHT = 0, 1, 2
 SB_FC_FWD, SB_FC_BWD = 0, 1
 SB_SGD_MAX_TENSORS = 64
+SB_NOALLOC_SCRATCH_BYTES = 40 << 20
 
 _vp = ctypes.c_void_p
 _i = ctypes.c_int
@@ -64,6 +65,8 @@ SIGNATURES = {
     "sb_conv3x3_fwd": (_i, [ctypes.POINTER(sb_conv3x3_desc), _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "sb_conv3x3_bwd_data": (_i, [ctypes.POINTER(sb_conv3x3_desc), _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "sb_conv3x3_bwd_weight": (_i, [ctypes.POINTER(sb_conv3x3_desc), _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "sb_conv3x3_bwd_weight_noalloc": (_i, [ctypes.POINTER(sb_conv3x3_desc), _vp, _vp, _vp, _vp,
+                                           _vp]),
     "sb_relu_maxpool_fwd": (_i, [_i, _i, _i, _i, _i, _vp, _vp, _vp, _vp]),
     "sb_relu_maxpool_bwd": (_i, [_i, _i, _i, _i, _i, _vp, _vp, _vp, _vp]),
     "sb_fc_workspace_bytes": (_sz, [ctypes.POINTER(sb_fc_desc), _i]),
@@ -229,6 +232,11 @@ def sb_conv3x3_bwd_weight(desc, x, dy, dw, db, ws=None, stream=None):
     p, nb = _ws(ws)
     _check("sb_conv3x3_bwd_weight", load().sb_conv3x3_bwd_weight(
         ctypes.byref(desc), _ptr(x), _ptr(dy), _ptr(dw), _ptr(db), p, nb, _stream(stream)))
+
+
+def sb_conv3x3_bwd_weight_noalloc(desc, x, dy, dw, db, stream=None):
+    _check("sb_conv3x3_bwd_weight_noalloc", load().sb_conv3x3_bwd_weight_noalloc(
+        ctypes.byref(desc), _ptr(x), _ptr(dy), _ptr(dw), _ptr(db), _stream(stream)))
 
 
 def sb_relu_maxpool_fwd(n, c, h, w, dtype, x, y, idx, stream=None):

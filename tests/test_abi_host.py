@@ -278,3 +278,30 @@ def test_fc_workspace_must_not_overlap_operands():
     for bad in (x, w, dy, dx, dw):
         assert bwd(bad + 256) == sb.SB_ERR_INVALID_ARG
 
+
+def _noalloc(d, x, dy, dw, db):
+    return _raw("sb_conv3x3_bwd_weight_noalloc", ctypes.byref(d), x, dy, dw, db, None)
+
+
+def test_noalloc_weight_gradient_validation():
+    """The no-allocation weight gradient validates like sb_conv3x3_bwd_weight
+    and refuses, before touching any device, a call whose split partials
+    would not fit its fixed scratch array."""
+    d = sb.conv_desc(2, 3, 8, 8, 4)
+    assert _noalloc(d, None, P, P + (1 << 20), None) == sb.SB_ERR_INVALID_ARG
+    assert _noalloc(d, P, P + 8192, None, None) == sb.SB_ERR_INVALID_ARG
+    assert _noalloc(sb.conv_desc(2, 3, 8, 8, 4, relu=True), P, P + 8192, P + (1 << 20),
+                    None) == sb.SB_ERR_INVALID_ARG
+    assert _noalloc(d, P, P + 8192, P + 64, None) == sb.SB_ERR_INVALID_ARG    # dw over x
+    # A shape whose split partials exceed the scratch array: 511 blocks of
+    # 64 k x 32 c in bf16 give two splits of 448 x 2336 x 9 fp32 each.
+    big = sb.conv_desc(8, 2336, 32, 32, 448, sb.SB_BF16)
+    need = sb.sb_conv3x3_workspace_bytes(big, sb.SB_PASS_BWD_WEIGHT)
+    assert need > sb.SB_NOALLOC_SCRATCH_BYTES
+    assert _noalloc(big, P, P + (1 << 30), P + (2 << 30), None) == sb.SB_ERR_WORKSPACE
+    # Every VGG-16 layer of both workloads fits.
+    from paper_2112_15317_amd import configs
+    for hw, n, dt in ((32, 128, sb.SB_F32), (224, 32, sb.SB_BF16)):
+        for L in configs.conv_layers(configs.VGG16, 3, hw):
+            q = sb.conv_desc(n, L.c, L.h, L.w, L.k, dt)
+            assert sb.sb_conv3x3_workspace_bytes(q, 2) <= sb.SB_NOALLOC_SCRATCH_BYTES
