@@ -178,14 +178,6 @@ def hybrid_inputs(n, schedule, fc_shapes, group):
     return layers, x, ws, bs, fw, fb, rows, cols, dy
 
 
-def train_targets(n, fc_shapes, group):
-    """Labels of the gathered rows and the other shards' logit columns."""
-    from paper_2112_15317_amd import synth
-    m, classes = n * group, fc_shapes[-1][1]
-    return (synth.labels(m, classes, 0, synth.TID.LABELS),
-            synth.normal((m, classes - classes // group), 0, synth.TID.LOGITS_REMOTE))
-
-
 # --------------------------------------------------------------- workloads --
 class Workload:
     """What a benchmark run needs: the step's calls, its work, its baseline."""
@@ -291,29 +283,18 @@ class HybridWorkload(Workload):
     dtype = "f32"
     images = 128
 
-    def __init__(self, name, schedule, fc_shapes, group, metric, text, train=False):
+    def __init__(self, name, schedule, fc_shapes, group, metric, text):
         self.name, self.schedule, self.fc_shapes, self.group = name, schedule, fc_shapes, group
-        self.metric, self.text, self.train = metric, text, train
+        self.metric, self.text = metric, text
 
     def build(self):
         from paper_2112_15317_amd.stack import HybridStep
         inp = hybrid_inputs(self.images, self.schedule, self.fc_shapes, self.group)
         self.layers = inp[0]
         self.hs = HybridStep(self.schedule, self.images, 3, 32, self.group, self.fc_shapes,
-                             self.group, train=self.train, lr=TRAIN_LR)
+                             self.group)
         self.hs.load_inputs(*inp[1:])
-        if self.train:
-            self.hs.load_targets(*train_targets(self.images, self.fc_shapes, self.group))
         return self.hs.step_calls()
-
-    def call_bytes(self, kind):
-        hs = self.hs
-        if kind == "loss":           # logits read, gradient written, labels and losses
-            return 2 * hs.m * hs.classes * 4 + 2 * hs.m * 4
-        # sgd: each parameter read and written, its gradient read
-        n = sum(w.numel() for w in hs.conv.W + hs.conv.b) + sum(
-            f.W.numel() + f.b.numel() for f in hs.fc)
-        return 12 * n
 
     def flops(self):
         from paper_2112_15317_amd import configs
@@ -329,18 +310,93 @@ class HybridWorkload(Workload):
         layers, x, ws, bs, fw, fb, rows, cols, dy = hybrid_inputs(
             n, self.schedule, self.fc_shapes, self.group)
         pools = [L.pool_after for L in layers]
-        train = None
-        if self.train:
-            labels, logits_remote = train_targets(n, self.fc_shapes, self.group)
-            train = {"labels": labels, "logits_remote": logits_remote, "lr": TRAIN_LR,
-                     "shards": self.group}
         t0 = time.perf_counter()
-        OS.hybrid_step(x, ws, bs, pools, fw, fb, rows, cols, dy, train=train)
+        OS.hybrid_step(x, ws, bs, pools, fw, fb, rows, cols, dy)
         dt = time.perf_counter() - t0
         return {"value": round(n / dt, 3), "unit": "images/s",
                 "cores": oracle.num_threads(), "kind": "oracle",
-                "sample": "1 x the whole %s step, %d local images (fp64 oracle), %.1f s"
-                          % ("training" if self.train else "hybrid", n, dt)}
+                "sample": "1 x the whole hybrid step, %d local images (fp64 oracle), %.1f s"
+                          % (n, dt)}
+
+
+def group_inputs(n, schedule, fc_shapes, K):
+    """Inputs of an MP group's training step: worker 0's conv stack on n
+    local images, the other workers' conv outputs, the full dense layers
+    (worker r's shard = its 1/K of the columns) and the labels of every
+    iteration's gathered rows."""
+    import numpy as np
+    from paper_2112_15317_amd import configs, synth
+    layers = configs.conv_layers(schedule, 3, 32)
+    x = synth.normal((n, 3, 32, 32), 0, synth.TID.IMAGES)
+    ws = [synth.he_normal_conv3x3(L.k, L.c, 0, synth.TID.CONV_W + L.index) for L in layers]
+    bs = [np.zeros(L.k, np.float32) for L in layers]
+    fw = [synth.xavier_uniform(fi, fo, 0, synth.TID.FC_W + j)
+          for j, (fi, fo) in enumerate(fc_shapes)]
+    fb = [np.zeros(fo, np.float32) for _, fo in fc_shapes]
+    remote = synth.relu_normal((K - 1, n, fc_shapes[0][0]), 0, synth.TID.X0_REMOTE)
+    labels = synth.labels(K * n, fc_shapes[-1][1], 0, synth.TID.LABELS).reshape(K, n)
+    return layers, x, ws, bs, fw, fb, remote, labels
+
+
+class GroupWorkload(Workload):
+    """Training step of an MP group of K (sec. 3.1): worker 0's conv stack,
+    K modulo iterations of every worker's FC shards with an SGD step after
+    each, the conv backward and update."""
+    dtype = "f32"
+    images = 128
+
+    def __init__(self, name, schedule, fc_shapes, K, metric, text):
+        self.name, self.schedule, self.fc_shapes, self.K = name, schedule, fc_shapes, K
+        self.metric, self.text = metric, text
+
+    def build(self):
+        from paper_2112_15317_amd import partition as P
+        from paper_2112_15317_amd.stack import GroupTrainStep
+        inp = group_inputs(self.images, self.schedule, self.fc_shapes, self.K)
+        self.layers = inp[0]
+        plan = P.fc_plan(P.partition(P.vgg_net(self.schedule, 3, 32, self.fc_shapes), self.K))
+        self.gs = GroupTrainStep(self.schedule, self.images, 3, 32, plan, lr=TRAIN_LR)
+        self.gs.load_inputs(*inp[1:])
+        return self.gs.step_calls()
+
+    def call_bytes(self, key, args):
+        gs, (kind, j) = self.gs, key
+        K, B = gs.K, gs.B
+        if kind == "loss":           # logits read, gradient written, labels and losses
+            return 2 * B * gs.classes * 4 + 2 * B * 4
+        if kind in ("mfwd", "mbwd"):
+            return 4 * (2 * B * gs.F if kind == "mfwd" else (K + 1) * B * gs.F)
+        if kind in ("sfwd", "sbwd"):
+            ns = gs.ns[j] if kind == "sfwd" else gs.ns[j - 1]
+            return 4 * (2 * K * B * ns if kind == "sfwd" else (K + 1) * K * B * ns)
+        # sgd: each parameter read and written, its gradient read
+        if kind == "sgd_fc":
+            n = sum(w.numel() + b.numel() for w, b in zip(gs.W, gs.b))
+        else:
+            n = sum(w.numel() + b.numel() for w, b in zip(gs.conv.W, gs.conv.b))
+        return 12 * n
+
+    def flops(self):
+        from paper_2112_15317_amd import configs
+        f = configs.stack_flops(self.layers, self.images)
+        gs = self.gs
+        # K iterations x K workers' shards, forward and backward (both products).
+        extra = sum(gs.K * gs.K * 6 * gs.B * gs.ins[j] * gs.ns[j] for j in range(gs.L))
+        return {"nominal": f["nominal"] + extra, "valid": f["valid"] + extra}
+
+    def cpu_baseline(self, sample):
+        import oracle
+        from oracle import stack as OS
+        layers, x, ws, bs, fw, fb, remote, labels = group_inputs(
+            self.images, self.schedule, self.fc_shapes, self.K)
+        pools = [L.pool_after for L in layers]
+        t0 = time.perf_counter()
+        OS.group_train_step(x, ws, bs, pools, fw, fb, remote, labels, TRAIN_LR)
+        dt = time.perf_counter() - t0
+        return {"value": round(self.images / dt, 3), "unit": "images/s",
+                "cores": oracle.num_threads(), "kind": "oracle",
+                "sample": "1 x the whole training step of the group, %d local images on "
+                          "worker 0 (fp64 oracle), %.1f s" % (self.images, dt)}
 
 
 class ExchangeWorkload(Workload):
@@ -383,13 +439,14 @@ class ExchangeWorkload(Workload):
                       (("mbwd", k), sb.sb_modulo_bwd, (md, 0, k, t["dg"], t["dlocal"]))]
         return calls
 
-    def call_bytes(self, kind):
+    def call_bytes(self, key, args=None):
         K, B, F, NS = self.K, self.B, self.F, self.NS
+        kind = key[0]
         return 4 * {"mfwd": 2 * B * F, "sfwd": 2 * K * B * NS,
                     "sbwd": K * B * K * NS + K * B * NS, "mbwd": K * B * F + B * F}[kind]
 
     def bytes_per_step(self):
-        return self.K * sum(self.call_bytes(k) for k in ("mfwd", "sfwd", "sbwd", "mbwd"))
+        return self.K * sum(self.call_bytes((k, 0)) for k in ("mfwd", "sfwd", "sbwd", "mbwd"))
 
     def flops(self):
         return {"nominal": 0, "valid": 0}
@@ -437,11 +494,11 @@ class AverageWorkload(Workload):
         self.p = torch.from_numpy(synth.normal((self.W, self.n()), 0, synth.TID.MISC + 15)).cuda()
         return [(("avg", 0), sb.sb_model_average, (self.W, 1, self.p))]
 
-    def call_bytes(self, kind):
+    def call_bytes(self, key=None, args=None):
         return 2 * self.W * self.n() * 4          # every slot read once and written once
 
     def bytes_per_step(self):
-        return self.call_bytes("avg")
+        return self.call_bytes()
 
     def flops(self):
         return {"nominal": 0, "valid": 0}
@@ -482,15 +539,16 @@ def workloads():
             "hybrid worker step: VGG-16 CIFAR conv stack on 128 local images, then FC0 "
             "512->1024 (of 4096, ReLU) and FC1 4096->1024 (of 4096) shards on the gathered 512 "
             "rows, fwd+bwd, fp32"),
-        "paper-variant-f32": HybridWorkload(
+        "paper-variant-f32": GroupWorkload(
             "paper-variant-f32", configs.PAPER_VARIANT_CONV, configs.PAPER_VARIANT_FC, 2,
-            "images/sec/GPU training step of the paper's VGG variant (Table 1), one worker, "
-            "fp32",
-            "the paper's VGG variant as one worker of an MP group of 2: seven 3x3 convs "
-            "(64,64,M,128,128,M,256,256,256,M) on 128 local 3x32x32 images, then FC "
-            "4096->1024->1024->10 split in 2 column shards on the gathered 256 rows; fwd, "
-            "log-softmax + NLL of the 10-class logits, bwd, SGD (conv at lr, FC shards at "
-            "lr/2), fp32", train=True),
+            "images/sec/GPU training step of the paper's VGG variant (Table 1) in an MP group "
+            "of 2, fp32",
+            "training step of the paper's VGG variant in an MP group of 2 on one GPU: seven "
+            "3x3 convs (64,64,M,128,128,M,256,256,256,M) on worker 0's 128 local 3x32x32 "
+            "images; 2 modulo iterations, each gathering 128 rows (64 per worker) and running "
+            "both workers' column shards of FC 4096->1024->1024->10 with shard layers "
+            "between them, log-softmax + NLL of the full 10-class logits, the backward and an "
+            "FC SGD step at lr/2; then the conv backward and SGD at lr; fp32"),
         "exchange-f32": ExchangeWorkload(),
         "average-f32": AverageWorkload(),
     }
@@ -515,7 +573,7 @@ def kernel_name(key, call_args, dtype):
                                         "fwd" if kind[1:] == "fwd" else "bwd")
     if kind == "loss":
         return "sb::log_softmax_nll_kernel"
-    if kind == "sgd":
+    if kind in ("sgd_fc", "sgd_conv"):
         return "sb::sgd_update_kernel"
     if kind == "avg":
         return "sb::model_average_kernel<4>"
@@ -530,8 +588,8 @@ def call_work(wl, key, args):
         return layer_flops(wl.layers[i], args[0].n)[0], "flop"
     if kind.startswith("fc_"):
         return fc_flops(args[0], kind, kind == "fc_fwd" or args[5] is not None), "flop"
-    if kind in ("mfwd", "mbwd", "sfwd", "sbwd", "loss", "sgd", "avg"):
-        return wl.call_bytes(kind), "bytes"
+    if kind in ("mfwd", "mbwd", "sfwd", "sbwd", "loss", "sgd_fc", "sgd_conv", "avg"):
+        return wl.call_bytes(key, args), "bytes"
     esize = 4 if wl.dtype == "f32" else 2
     if kind == "pack":             # every layer's filters read, twice packed written
         return sum(3 * L.k * L.c * 9 * esize for L in wl.layers), "bytes"
@@ -603,7 +661,7 @@ def main():
 
     # Timed region 2: every call of the step, K launches back to back in a
     # graph of its own, between two events -> average duration per launch.
-    per_call = {}
+    per_call = []                 # ms per launch, in the order of `calls`
     for key, fn, a in calls:
         gc = capture_graph(lambda: fn(*a), K)
         gc.replay()
@@ -612,8 +670,15 @@ def main():
         gc.replay()
         ev1.record()
         torch.cuda.synchronize()
-        per_call[key] = ev0.elapsed_time(ev1) / K
+        per_call.append(ev0.elapsed_time(ev1) / K)
         del gc
+    # Call names: kind + 1-based index, "#n" for a repeated key (a group
+    # step runs the same layer's call once per worker and iteration).
+    names, seen = [], {}
+    for key, _, _ in calls:
+        base = "%s%d" % (key[0], key[1] + 1)
+        seen[base] = seen.get(base, 0) + 1
+        names.append(base if seen[base] == 1 else "%s#%d" % (base, seen[base]))
 
     fl = wl.flops()
     peak = PEAK_MFMA_TFLOPS[dtype]
@@ -623,15 +688,15 @@ def main():
 
     # Group the calls by kernel; the dominant kernel has the largest time per step.
     groups = {}
-    for key, fn, a in calls:
+    for (key, fn, a), t, cname in zip(calls, per_call, names):
         name = kernel_name(key, a, dtype)
         base = name.split(" grid=")[0]
         work, unit = call_work(wl, key, a)
         gr = groups.setdefault(base, {"ms": 0.0, "work": 0, "unit": unit, "calls": [],
                                       "split": False})
-        gr["ms"] += per_call[key]
+        gr["ms"] += t
         gr["work"] += work
-        gr["calls"].append("%s%d" % (key[0], key[1] + 1))
+        gr["calls"].append(cname)
         gr["split"] |= bool(re.search(r"grid=\d+x\d+x([2-9]|\d\d)", name))
     dom = max(groups, key=lambda k: groups[k]["ms"])
     G = groups[dom]
@@ -672,8 +737,8 @@ def main():
         "tflops_valid_tap": None if moved else round(tf_valid, 2),
         "frac_mfma_peak_nominal": None if moved else round(tf_nom / peak, 4),
         "roofline": roof,
-        "sum_of_calls_ms": round(sum(per_call.values()), 4),
-        "per_call_us": {"%s%d" % (k[0], k[1] + 1): round(v * 1e3, 1) for k, v in per_call.items()},
+        "sum_of_calls_ms": round(sum(per_call), 4),
+        "per_call_us": {n: round(v * 1e3, 1) for n, v in zip(names, per_call)},
         "per_kernel_us_per_step": {k: round(v["ms"] * 1e3, 1) for k, v in
                                    sorted(groups.items(), key=lambda kv: -kv[1]["ms"])},
     }

@@ -22,6 +22,7 @@ import numpy as np
 
 from . import (_f64, conv3x3_bwd_data, conv3x3_bwd_weight, conv3x3_fwd,
                fc_bwd, fc_fwd, relu_maxpool_bwd, relu_maxpool_fwd, round_bf16)
+from .modulo import modulo_bwd, modulo_fwd, shard_bwd, shard_fwd
 from .train import log_softmax_nll, sgd_update
 
 
@@ -81,18 +82,12 @@ def vgg_step(x, weights, biases, pool_after, dy_top, bf16=False, want_dx=True):
     return f, b
 
 
-def hybrid_step(x, weights, biases, pool_after, fc_w, fc_b, rows_remote, cols_remote, dy,
-                train=None):
-    """One worker's step of the hybrid scheme on one device, with L FC shards.
-
-    ``train`` (a dict with ``labels``, ``logits_remote``, ``lr``, ``shards``)
-    makes it a whole training step: the last shard's output and the other
-    shards' columns ``logits_remote`` form the full logits (the shard layer
-    before the LOG_SOFTMAX layer, sec. 3.1), whose log-softmax + NLL over the
-    gathered rows (batch mean) gives the last shard's output gradient in
-    place of ``dy``; after the backward, SGD at rate ``lr`` updates the conv
-    parameters and, with the gradient divided by ``shards`` (the paper's K,
-    sec. 3.1 Modulo Layer), the FC shards.
+def hybrid_step(x, weights, biases, pool_after, fc_w, fc_b, rows_remote, cols_remote, dy):
+    """One worker's forward and backward of the hybrid scheme on one device,
+    with L FC shards and no update (so the gathered rows of all K modulo
+    iterations can go through the FC shards in one batch: with no update in
+    between, the iterations' results are the same rows in another order and
+    their weight gradients add up to the same sums).
 
     The local conv stack output (flattened, one row per image, NCHW order)
     fills the first rows of the gathered FC0 input; ``rows_remote`` supplies
@@ -119,13 +114,7 @@ def hybrid_step(x, weights, biases, pool_after, fc_w, fc_b, rows_remote, cols_re
         if j < L - 1:
             xs.append(np.concatenate([y, np.asarray(cols_remote[j], np.float64)], axis=1))
     dxp, dw, db, dys = [None] * L, [None] * L, [None] * L, [None] * L
-    loss = dz = None
-    if train is not None:
-        z = np.concatenate([ys[-1], np.asarray(train["logits_remote"], np.float64)], axis=1)
-        _, loss, dz = log_softmax_nll(z, train["labels"], 1.0 / z.shape[0])
-        g = np.ascontiguousarray(dz[:, :ys[-1].shape[1]])
-    else:
-        g = np.asarray(dy, np.float64)
+    g = np.asarray(dy, np.float64)
     for j in reversed(range(L)):
         dys[j] = g
         dxp[j], dw[j], db[j] = fc_bwd(xs[j], fc_w[j], g,
@@ -134,12 +123,99 @@ def hybrid_step(x, weights, biases, pool_after, fc_w, fc_b, rows_remote, cols_re
             g = np.ascontiguousarray(dxp[j][:, :ys[j - 1].shape[1]])
     dtop = np.ascontiguousarray(dxp[0][:n]).reshape(top.shape)
     b = vgg_backward(f, weights, pool_after, dtop)
-    out = {"fwd": f, "bwd": b, "xs": xs, "ys": ys, "dys": dys, "dxp": dxp, "dw": dw, "db": db}
-    if train is not None:
-        lr, k = train["lr"], 1.0 / train["shards"]
-        out.update(loss=loss, dz=dz,
-                   conv_w_new=[sgd_update(w, b["dW"][i], lr, 1.0) for i, w in enumerate(weights)],
-                   conv_b_new=[sgd_update(bb, b["db"][i], lr, 1.0) for i, bb in enumerate(biases)],
-                   fc_w_new=[sgd_update(w, dw[j], lr, k) for j, w in enumerate(fc_w)],
-                   fc_b_new=[sgd_update(bb, db[j], lr, k) for j, bb in enumerate(fc_b)])
-    return out
+    return {"fwd": f, "bwd": b, "xs": xs, "ys": ys, "dys": dys, "dxp": dxp, "dw": dw, "db": db}
+
+
+def group_train_step(x, weights, biases, pool_after, fc_w, fc_b, local_remote, labels, lr):
+    """One training step of an MP group of K workers, as sec. 3.1 (Modulo
+    Layer, Shard Layer) runs it, with the FC side of every worker of the
+    group and the conv stack of worker 0.
+
+    * Worker 0 runs its conv stack forward once on its local batch of B
+      images (``x``); ``local_remote`` [K-1][B][F] holds the flattened conv
+      outputs of workers 1 .. K-1 (their own data-parallel stacks, not
+      computed here).  K = ``len(local_remote) + 1`` and B must divide by K.
+    * Then K modulo iterations k = 0 .. K-1.  Each gathers a batch of B rows,
+      B/K from every worker of the group (block k of its local batch), with
+      the modulo layer's index map; runs every FC layer as K column shards
+      (worker r holds columns r*Ns .. (r+1)*Ns - 1 of ``fc_w[j]`` and
+      ``fc_b[j]``, the full layers), a shard layer assembling the full input
+      of the next layer from the K partitions (and the full logits before
+      LOG_SOFTMAX); evaluates log-softmax + NLL of the full logits against
+      ``labels[k]`` [B] (the labels of iteration k's gathered rows), averaged
+      over the B rows; backpropagates: the last shards take their columns of
+      the full logits' gradient (every worker evaluates the same loss), each
+      later shard layer sums the group's partial input gradients over each
+      worker's slice, and the modulo layer sums them back into the local
+      rows of the workers that supplied them.  After the backward of
+      iteration k every FC shard takes an SGD step with its gradient divided
+      by K, so iteration k + 1 runs on the updated FC weights.
+    * After the K iterations, worker 0's local rows hold the gradient of its
+      conv output for the whole local batch; the conv stack runs backward
+      and its parameters take one SGD step at rate ``lr``.
+
+    Everything is float64.  Returns a dict with the conv forward and
+    backward (``fwd``, ``bwd``), the per-iteration records ``iters``, the
+    updated parameters (``fc_w_new``, ``fc_b_new`` as full layers,
+    ``conv_w_new``, ``conv_b_new``) and ``dlocal`` [K][B][F], every worker's
+    conv-output gradient as the modulo layer delivers it.
+    """
+    K = len(local_remote) + 1
+    L = len(fc_w)
+    f = vgg_forward(x, weights, biases, pool_after)
+    top = f["A"][-1]
+    B = top.shape[0]
+    feat = int(np.prod(top.shape[1:]))
+    if B % K:
+        raise ValueError("the local batch must divide into K blocks")
+    local = np.concatenate([top.reshape(1, B, feat), np.asarray(local_remote, np.float64)])
+    W = [np.array(w, np.float64) for w in fc_w]
+    bvec = [np.array(b, np.float64) for b in fc_b]
+    ns = []
+    for w in W:
+        if w.shape[1] % K:
+            raise ValueError("FC outputs must split in K shards")
+        ns.append(w.shape[1] // K)
+    cols = [[slice(r * n, (r + 1) * n) for r in range(K)] for n in ns]
+    dlocal = np.zeros_like(local)
+    iters = []
+    for k in range(K):
+        gathered = modulo_fwd(local, 0, k, K)
+        xs, parts = [gathered], []
+        for j in range(L):
+            pj = [fc_fwd(xs[j], W[j][:, cols[j][r]], bvec[j][cols[j][r]], relu=j < L - 1)
+                  for r in range(K)]
+            parts.append(pj)
+            xs.append(shard_fwd(np.stack(pj), 0, K))
+        logits = xs[-1]
+        _, loss, dz = log_softmax_nll(logits, labels[k], 1.0 / B)
+        dws, dbs = [None] * L, [None] * L
+        dfull = [None] * L
+        dpart = None
+        for j in reversed(range(L)):
+            gw, gb, gx = [], [], []
+            for r in range(K):
+                dy = dz[:, cols[j][r]] if j == L - 1 else dpart[r]
+                dx, dw, db = fc_bwd(xs[j], W[j][:, cols[j][r]], np.ascontiguousarray(dy),
+                                    mask_src=parts[j][r] if j < L - 1 else None)
+                gx.append(dx)
+                gw.append(dw)
+                gb.append(db)
+            dws[j], dbs[j], dfull[j] = gw, gb, np.stack(gx)
+            if j > 0:
+                dpart = shard_bwd(dfull[j], 0, K, np.zeros((K, B, ns[j - 1])))
+            else:
+                dlocal = modulo_bwd(dfull[0], 0, k, K, dlocal)
+        iters.append({"gathered": gathered, "xs": xs, "parts": parts, "logits": logits,
+                      "loss": loss, "dz": dz, "dfull": dfull, "dw": dws, "db": dbs,
+                      "w_before": [w.copy() for w in W], "b_before": [b.copy() for b in bvec]})
+        for j in range(L):
+            for r in range(K):
+                W[j][:, cols[j][r]] = sgd_update(W[j][:, cols[j][r]], dws[j][r], lr, 1.0 / K)
+                bvec[j][cols[j][r]] = sgd_update(bvec[j][cols[j][r]], dbs[j][r], lr, 1.0 / K)
+    dtop = np.ascontiguousarray(dlocal[0]).reshape(top.shape)
+    b = vgg_backward(f, weights, pool_after, dtop)
+    return {"fwd": f, "bwd": b, "iters": iters, "dlocal": dlocal,
+            "fc_w_new": W, "fc_b_new": bvec,
+            "conv_w_new": [sgd_update(w, b["dW"][i], lr, 1.0) for i, w in enumerate(weights)],
+            "conv_b_new": [sgd_update(bb, b["db"][i], lr, 1.0) for i, bb in enumerate(biases)]}

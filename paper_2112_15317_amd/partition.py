@@ -23,8 +23,10 @@ activations, ``4 * (i + o)``; the default threshold, 1 FLOP/byte, splits
 every FC layer of the paper's VGG variant (whose three FC layers it splits
 for their memory, sec. 5).
 
-Host code: this module computes nothing on the GPU and feeds the driver
-(``stack.HybridStep``) its shard shapes.
+Host code: this module computes nothing on the GPU.  ``fc_plan`` turns the
+partitioned list into the call sequence of the training step
+(``stack.GroupTrainStep``): its modulo, shard, split dense and loss layers,
+in order.
 """
 from __future__ import annotations
 
@@ -79,68 +81,108 @@ def ccr(layer: Layer) -> float:
     return 6.0 * i * o / (4.0 * (i + o))
 
 
+# How each layer kind treats the width of its input (sec. 3.1, Layer
+# Partitioning): layers that reshape, pad, convolve or pool see whole
+# examples only; element-wise layers keep whatever width they are given; a
+# dense layer may be split over its outputs; the loss needs the whole output.
+_ROLE = {RESHAPE: "whole", PAD: "whole", CONV: "whole", POOLING: "whole",
+         DROPOUT: "pointwise", RELU: "pointwise", LINEAR: "dense", LOG_SOFTMAX: "loss"}
+
+
+def flatten(net: Layer) -> List[Layer]:
+    """The leaves of nested SEQ containers, in order."""
+    if net.kind != SEQ:
+        return [net]
+    return [leaf for child in net.children for leaf in flatten(child)]
+
+
 def partition(net: Layer, workers: int, threshold: float = 1.0) -> List[Layer]:
     """The hybrid layer list of ``net`` for MP groups of ``workers`` (the
-    paper's K; 1 = no model parallelism)."""
+    paper's K; 1 = no model parallelism).
+
+    A fold over the flattened layers that carries two widths per example:
+    the activation as this worker holds it (``local``) and as the unsplit
+    model has it (``whole``); they differ exactly while the activation is
+    partitioned.  Before a dense layer with a partitioned input a SHARD
+    layer restores the whole width; a dense layer with a whole input that is
+    split becomes the first split layer, so a MODULO layer goes in front of
+    it (the input is still per-worker data, gathered by rows); before the
+    loss a partitioned output is made whole by a SHARD layer."""
     if workers < 1:
         raise ValueError("workers must be >= 1")
-    use_mp = workers > 1
+    leaves = flatten(net)
+    if not leaves:
+        return []
     out: List[Layer] = []
-    first = net.children[0] if net.kind == SEQ and net.children else net
-    start = _first_dim(first)
-    state = {"dim": start, "dim_full": start}
+    local = whole = leaves[0].in_dim
 
-    def split(layer: Layer) -> Layer:
-        o = layer.full_out or layer.out_dim
-        if o % workers:
-            raise ValueError("%d outputs do not split in %d shards" % (o, workers))
-        return Layer(LINEAR, layer.in_dim, o // workers, shards=workers, full_out=o)
-
-    def walk(layer: Layer) -> None:
-        dim, full = state["dim"], state["dim_full"]
-        k = layer.kind
-        if k == SEQ:
-            for child in layer.children:
-                walk(child)
-            return
-        if k in _UNSPLIT:
-            if dim != full:
-                raise ValueError("partitioned input unsupported by %s" % k)
-            state["dim"] = state["dim_full"] = layer.resize(dim)
-        elif k in _ELEMENTWISE:
-            state["dim"] = layer.resize(dim)        # follows the partitioned width
-        elif k == LINEAR:
-            if layer.in_dim != full:
-                raise ValueError("LINEAR expects %d inputs, the model gives %d"
-                                 % (layer.in_dim, full))
-            if dim == full:
-                # Whole input: the first FC layer to split gets the modulo layer.
-                if use_mp and ccr(layer) > threshold:
-                    out.append(Layer(MODULO, full, full))
-                    layer = split(layer)
-            else:
-                # Partitioned input: assemble the full input first.
-                out.append(Layer(SHARD, dim, full))
-                if use_mp and ccr(layer) > threshold:
-                    layer = split(layer)
-            state["dim"] = layer.out_dim
-            state["dim_full"] = layer.full_out or layer.out_dim
-        elif k == LOG_SOFTMAX:
-            if dim != full:
-                out.append(Layer(SHARD, dim, full))
-                state["dim"] = full
-        else:
-            raise ValueError("unknown layer kind %s" % k)
-        out.append(layer)
-
-    walk(net)
+    for layer in leaves:
+        role = _ROLE.get(layer.kind)
+        if role is None:
+            raise ValueError("no partitioning rule for layer kind %r" % layer.kind)
+        if role == "whole":
+            if local != whole:
+                raise ValueError("%s cannot take a column-split input (%d of %d features)"
+                                 % (layer.kind, local, whole))
+            local = whole = layer.resize(whole)
+            out.append(layer)
+        elif role == "pointwise":
+            local = layer.resize(local)
+            out.append(layer)
+        elif role == "dense":
+            if layer.in_dim != whole:
+                raise ValueError("dense layer of %d inputs after %d features"
+                                 % (layer.in_dim, whole))
+            split = workers > 1 and ccr(layer) > threshold
+            if local != whole:
+                out.append(Layer(SHARD, local, whole))
+            elif split:
+                out.append(Layer(MODULO, whole, whole))
+            full_out = layer.full_out or layer.out_dim
+            if split:
+                if full_out % workers:
+                    raise ValueError("%d outputs cannot be split evenly over %d workers"
+                                     % (full_out, workers))
+                layer = Layer(LINEAR, layer.in_dim, full_out // workers, shards=workers,
+                              full_out=full_out)
+            out.append(layer)
+            local, whole = layer.out_dim, full_out
+        else:                                   # the loss
+            if local != whole:
+                out.append(Layer(SHARD, local, whole))
+                local = whole
+            out.append(layer)
     return out
 
 
-def _first_dim(layer: Layer) -> int:
-    while layer.kind == SEQ:
-        layer = layer.children[0]
-    return layer.in_dim
+def fc_plan(layers: List[Layer]):
+    """The model-parallel tail of a partitioned layer list as the training
+    step runs it: from the MODULO layer on, a list of
+    ``("modulo", features)``, ``("linear", in, shard_out, full_out, relu)``
+    (relu: a ReLU follows the layer), ``("shard", part, full)`` and
+    ``("loss", classes)`` entries.  Dropout is not part of any workload and
+    is refused, as is a tail that does not start with a MODULO layer."""
+    kinds = [l.kind for l in layers]
+    if MODULO not in kinds:
+        raise ValueError("no model-parallel part: the list has no MODULO layer")
+    tail = layers[kinds.index(MODULO):]
+    plan = []
+    for i, l in enumerate(tail):
+        if l.kind == MODULO:
+            plan.append(("modulo", l.in_dim))
+        elif l.kind == LINEAR:
+            relu = i + 1 < len(tail) and tail[i + 1].kind == RELU
+            plan.append(("linear", l.in_dim, l.out_dim, l.full_out or l.out_dim, relu))
+        elif l.kind == SHARD:
+            plan.append(("shard", l.in_dim, l.out_dim))
+        elif l.kind == LOG_SOFTMAX:
+            width = plan[-1][2] if plan[-1][0] == "shard" else plan[-1][3]
+            plan.append(("loss", width))
+        elif l.kind == RELU:
+            continue                              # fused into the layer before
+        else:
+            raise ValueError("%s in the model-parallel part is not supported" % l.kind)
+    return plan
 
 
 def fc_shards(layers: List[Layer]):
@@ -154,3 +196,25 @@ def parameters(layers: List[Layer], conv_params: int = 0) -> int:
     weight (and bias) columns."""
     return conv_params + sum(l.in_dim * l.out_dim + l.out_dim for l in layers
                              if l.kind == LINEAR)
+
+
+def vgg_net(schedule, in_ch: int, hw: int, fc) -> Layer:
+    """A sequential VGG-style CNN as a layer list: 3x3 convs (each followed
+    by a ReLU) and 2x2 pools per the channel schedule, a flatten, the dense
+    layers ``fc`` [(in, out)] with a ReLU between them, then LOG_SOFTMAX."""
+    from .configs import POOL
+    layers, c = [], in_ch
+    for v in schedule:
+        if v == POOL:
+            layers.append(Layer(POOLING, c * hw * hw, c * (hw // 2) ** 2))
+            hw //= 2
+        else:
+            layers += [Layer(CONV, c * hw * hw, v * hw * hw), Layer(RELU)]
+            c = v
+    layers.append(Layer(RESHAPE, c * hw * hw, c * hw * hw))
+    for j, (i, o) in enumerate(fc):
+        layers.append(linear(i, o))
+        if j < len(fc) - 1:
+            layers.append(Layer(RELU))
+    layers.append(Layer(LOG_SOFTMAX))
+    return seq(*layers)

@@ -12,6 +12,9 @@ by a libsb kernel.  torch only allocates device memory and orders streams.
 ``FCShard``     one FC column shard fwd + bwd
 ``HybridStep``  conv stack, then FC0 -> ReLU -> FC1 shards on the gathered
                 batch, then backward through both
+``GroupTrainStep``  a training step of an MP group: conv stack, K modulo
+                iterations of the FC shards with an update after each, conv
+                backward and update
 """
 from __future__ import annotations
 
@@ -286,17 +289,10 @@ class HybridStep:
     collectives, not part of this step.
     """
 
-    def __init__(self, schedule, n, in_ch, hw, replicas, fc_shapes, shards, device="cuda",
-                 train=False, lr=0.01):
-        """train: a whole training step.  The last shard writes its columns of
-        the full logits Zl [m, classes] (the shard layer before the
-        LOG_SOFTMAX layer; the other shards' columns are stand-ins), the
-        log-softmax + NLL of the gathered rows (batch mean) gives the
-        gradient of the last shard's output, and after the backward one SGD
-        step at rate lr updates the conv parameters and, with the gradient
-        divided by the number of shards K, the FC shards (sec. 3.1, Modulo
-        Layer).  Otherwise the last shard's output Y takes a given gradient
-        dY and nothing is updated."""
+    def __init__(self, schedule, n, in_ch, hw, replicas, fc_shapes, shards, device="cuda"):
+        """The last shard's output Y takes a given gradient dY; nothing is
+        updated (the training step with its K modulo iterations is
+        ``GroupTrainStep``)."""
         dev = torch.device(device)
         self.n, self.R = n, replicas
         m = n * replicas
@@ -308,34 +304,16 @@ class HybridStep:
         f32 = dict(dtype=torch.float32, device=dev)
         self.X = [torch.empty((m, fi), **f32) for fi in self.ins]
         self.dXp = [torch.empty((m, fi), **f32) for fi in self.ins]
-        self.train, self.lr, self.shards = train, lr, shards
-        self.classes = fc_shapes[-1][1]
-        if train:
-            self.Zl = torch.empty((m, self.classes), **f32)
-            self.dZl = torch.empty((m, self.classes), **f32)
-            self.labels = torch.zeros((m,), dtype=torch.int32, device=dev)
-            self.loss = torch.empty((m,), **f32)
-            out_last, ld_last = self.Zl, self.classes
-        else:
-            self.Y = torch.empty((m, self.ns[-1]), **f32)
-            self.dY = torch.empty((m, self.ns[-1]), **f32)
-            out_last, ld_last = self.Y, self.ns[-1]
-        self.out_last, self.dout_last = out_last, (self.dZl if train else self.dY)
+        self.Y = torch.empty((m, self.ns[-1]), **f32)
+        self.dY = torch.empty((m, self.ns[-1]), **f32)
         self.conv = ConvStack(schedule, n, in_ch, hw, "f32", device,
                               out_buffer=self.X[0][:n], out_grad_buffer=self.dXp[0][:n])
         top = self.conv.A[-1]
         assert int(np.prod(top.shape[1:])) == self.ins[0]
         last = self.L - 1
         self.fc = [FCShard(m, self.ins[j], self.ns[j], relu=j < last, ldx=self.ins[j],
-                           ldy=self.ins[j + 1] if j < last else ld_last, device=device)
+                           ldy=self.ins[j + 1] if j < last else self.ns[-1], device=device)
                    for j in range(self.L)]
-        if train:
-            c = self.conv
-            self.sgd = sb.SgdList(
-                [(c.W[i], c.dW[i], 1.0) for i in range(len(c.layers))] +
-                [(c.b[i], c.db[i], 1.0) for i in range(len(c.layers))] +
-                [(f.W, f.dW, 1.0 / shards) for f in self.fc] +
-                [(f.b, f.db, 1.0 / shards) for f in self.fc])
         self.call = _plain      # hook: every libsb call of the step goes through it
 
     # Two-layer names used by the tests of the four-replica worker step.
@@ -343,7 +321,6 @@ class HybridStep:
     X1 = property(lambda self: self.X[1])
     dX0p = property(lambda self: self.dXp[0])
     dX1p = property(lambda self: self.dXp[1])
-    Y1 = property(lambda self: self.Y)
     fc0 = property(lambda self: self.fc[0])
     fc1 = property(lambda self: self.fc[1])
 
@@ -359,15 +336,7 @@ class HybridStep:
         self.X[0][self.n:].copy_(t(rows_remote))
         for j in range(1, self.L):
             self.X[j][:, self.ns[j - 1]:].copy_(t(cols_remote[j - 1]))
-        if not self.train:
-            self.dY.copy_(t(dy))
-
-    def load_targets(self, labels, logits_remote):
-        """Training step: the labels of the gathered rows and the other
-        shards' columns of the last FC output."""
-        self.labels.copy_(torch.from_numpy(np.ascontiguousarray(labels, dtype=np.int32)))
-        self.Zl[:, self.ns[-1]:].copy_(
-            torch.from_numpy(np.ascontiguousarray(logits_remote, dtype=np.float32)))
+        self.dY.copy_(t(dy))
 
     def step(self, stream=None):
         def c(key, call):
@@ -377,23 +346,204 @@ class HybridStep:
         L = self.L
         X = [x.data_ptr() for x in self.X]
         for j in range(L):
-            out = X[j + 1] if j + 1 < L else self.out_last.data_ptr()
+            out = X[j + 1] if j + 1 < L else self.Y.data_ptr()
             c(("fc_fwd", j), self.fc[j].fwd_call(X[j], out, stream))
-        if self.train:
-            self.call(("loss", 0), sb.sb_log_softmax_nll, self.m, self.classes, self.Zl,
-                      self.labels, 1.0 / self.m, None, self.loss, self.dZl, self.classes, stream)
         for j in reversed(range(L)):
-            # Output gradient of layer j: the last layer's (given, or from the
-            # loss), or layer j+1's partial input gradient on this shard's
-            # columns (row stride in_{j+1}), masked by layer j's ReLU output
-            # X[j+1][:, :ns_j].
-            dy = self.dout_last.data_ptr() if j == L - 1 else self.dXp[j + 1].data_ptr()
+            # Output gradient of layer j: the last layer's (given), or layer
+            # j+1's partial input gradient on this shard's columns (row
+            # stride in_{j+1}), masked by layer j's ReLU output X[j+1][:, :ns_j].
+            dy = self.dY.data_ptr() if j == L - 1 else self.dXp[j + 1].data_ptr()
             mask = None if j == L - 1 else X[j + 1]
             c(("fc_bwd", j), self.fc[j].bwd_call(X[j], dy, mask, self.dXp[j].data_ptr(),
                                                  stream=stream))
         self.conv.backward(stream)
-        if self.train:
-            self.call(("sgd", 0), sb.sb_sgd_update, self.sgd, self.lr, stream)
+
+    def step_calls(self):
+        """The ordered (key, libsb function, args) calls of one step."""
+        rec = []
+        saved = self.call, self.conv.call
+        self.call = self.conv.call = lambda key, fn, *args: rec.append((key, fn, args))
+        try:
+            self.step()
+        finally:
+            self.call, self.conv.call = saved
+        return rec
+
+
+class GroupTrainStep:
+    """One training step of an MP group of K workers on one device (sec. 3.1,
+    Modulo Layer and Shard Layer), with the FC side of every worker of the
+    group and the conv stack of worker 0.
+
+    The model-parallel part runs the call sequence of ``plan``
+    (``partition.fc_plan`` of the partitioned layer list): the modulo layer,
+    then split dense layers each followed by a shard layer, then the loss.
+    Worker 0 runs its conv stack forward once and writes the flattened
+    output into slot 0 of ``local`` [K][B][F]; slots 1 .. K-1 hold the conv
+    outputs of the group's other workers (their own data-parallel stacks,
+    given as inputs).  Then K modulo iterations k = 0 .. K-1 each
+
+      * gather B rows, B/K from every worker (``sb_modulo_fwd``, block k);
+      * run, for every worker r, its column shard of each dense layer
+        (``sb_fc_shard_fwd``, ReLU fused), and after each layer the shard
+        layer that assembles the full input of the next one from the K
+        partitions (``sb_shard_fwd``; before the loss: the full logits);
+      * evaluate log-softmax + NLL of the full logits against the labels of
+        the gathered rows, averaged over the B rows (``sb_log_softmax_nll``);
+      * backpropagate: the last shards take their columns of the logits'
+        gradient (every worker evaluates the same loss), each shard layer
+        sums the group's partial input gradients over every worker's slice
+        (``sb_shard_bwd``), and the modulo layer sums the first layer's
+        partial input gradients back into the local rows of block k
+        (``sb_modulo_bwd``);
+      * take an SGD step on every FC shard with its gradient divided by K
+        (``sb_sgd_update``), so iteration k + 1 runs on the updated weights.
+
+    After the K iterations slot 0 of ``dlocal`` holds the gradient of worker
+    0's conv output over its whole local batch: the conv stack runs backward
+    and takes one SGD step at rate lr.
+
+    Buffers (j: dense layer, r: worker): ``W[j]``/``b[j]`` [K][in_j][ns_j] /
+    [K][ns_j] (worker r's shard, fp32), ``dW[j]``/``db[j]`` their gradients,
+    ``X[j]`` [B][in_j] the full input of layer j (``X[0]`` the gathered
+    batch, ``X[L]`` the full logits), ``P[j]`` [K][B][ns_j] the shard
+    outputs, ``dF[j]`` [K][B][in_j] every worker's partial input gradient,
+    ``dP[j]`` [K][B][ns_j] the shard layers' sums, ``labels`` [K][B] (int32,
+    the labels of iteration k's gathered rows), ``loss`` [K][B].
+    """
+
+    def __init__(self, schedule, n, in_ch, hw, plan, lr=0.01, device="cuda"):
+        dev = torch.device(device)
+        if not plan or plan[0][0] != "modulo" or plan[-1][0] != "loss":
+            raise ValueError("the plan must run from a modulo layer to the loss")
+        lin = [e for e in plan[1:-1] if e[0] == "linear"]
+        shards = [e for e in plan[1:-1] if e[0] == "shard"]
+        body = [e[0] for e in plan[1:-1]]
+        if body != ["linear", "shard"] * len(lin):
+            raise ValueError("every dense layer must be split and followed by a shard layer")
+        K = lin[0][3] // lin[0][2]
+        for (_, i, ns, full, _), (_, part, whole) in zip(lin, shards):
+            if ns * K != full or (part, whole) != (ns, full):
+                raise ValueError("inconsistent shard widths in the plan")
+        if n % K:
+            raise ValueError("the local batch must divide into K blocks")
+        self.K, self.B, self.L, self.lr = K, n, len(lin), lr
+        self.ins = [e[1] for e in lin]
+        self.ns = [e[2] for e in lin]
+        self.full = [e[3] for e in lin]
+        self.relu = [e[4] for e in lin]
+        self.F = plan[0][1]
+        self.classes = plan[-1][1]
+        if self.ins[0] != self.F or self.full[-1] != self.classes:
+            raise ValueError("the plan's widths do not chain")
+        for j in range(1, self.L):
+            if self.ins[j] != self.full[j - 1]:
+                raise ValueError("the plan's widths do not chain")
+        f32 = dict(dtype=torch.float32, device=dev)
+        K, B, F = self.K, self.B, self.F
+        self.local = torch.empty((K, B, F), **f32)
+        self.dlocal = torch.empty((K, B, F), **f32)
+        self.conv = ConvStack(schedule, n, in_ch, hw, "f32", device,
+                              out_buffer=self.local[0], out_grad_buffer=self.dlocal[0])
+        if int(np.prod(self.conv.A[-1].shape[1:])) != F:
+            raise ValueError("the conv stack's output does not have the plan's width")
+        L = self.L
+        self.W = [torch.empty((K, self.ins[j], self.ns[j]), **f32) for j in range(L)]
+        self.b = [torch.empty((K, self.ns[j]), **f32) for j in range(L)]
+        self.dW = [torch.empty_like(w) for w in self.W]
+        self.db = [torch.empty_like(b) for b in self.b]
+        self.X = [torch.empty((B, self.ins[j]), **f32) for j in range(L)]
+        self.X.append(torch.empty((B, self.classes), **f32))
+        self.P = [torch.empty((K, B, self.ns[j]), **f32) for j in range(L)]
+        self.dF = [torch.empty((K, B, self.ins[j]), **f32) for j in range(L)]
+        self.dP = [torch.empty((K, B, self.ns[j]), **f32) for j in range(L)]
+        self.dZl = torch.empty((B, self.classes), **f32)
+        self.labels = torch.zeros((K, B), dtype=torch.int32, device=dev)
+        self.loss = torch.empty((K, B), **f32)
+        self.mdesc = sb.modulo_desc(K, K, B, F)
+        self.sdesc = [sb.shard_desc(K, K, B, self.ns[j]) for j in range(L)]
+        # Forward writes each shard's output densely ([B][ns_j]); the last
+        # layer's backward reads its columns of the full logits' gradient.
+        self.fdesc = [sb.fc_desc(B, self.ins[j], self.ns[j], relu=self.relu[j]) for j in range(L)]
+        self.bdesc = [sb.fc_desc(B, self.ins[j], self.ns[j],
+                                 ldy=self.classes if j == L - 1 else self.ns[j])
+                      for j in range(L)]
+        need = 0
+        for j in range(L):
+            need = max(need, sb.sb_fc_workspace_bytes(self.fdesc[j], sb.SB_FC_FWD),
+                       sb.sb_fc_workspace_bytes(self.bdesc[j], sb.SB_FC_BWD))
+        self.ws = torch.empty((max(need, 256) + 255) // 256 * 256, dtype=torch.uint8, device=dev)
+        self.sgd_fc = sb.SgdList([(self.W[j], self.dW[j], 1.0 / K) for j in range(L)] +
+                                 [(self.b[j], self.db[j], 1.0 / K) for j in range(L)])
+        c = self.conv
+        self.sgd_conv = sb.SgdList([(c.W[i], c.dW[i], 1.0) for i in range(len(c.layers))] +
+                                   [(c.b[i], c.db[i], 1.0) for i in range(len(c.layers))])
+        self.call = _plain      # hook: every libsb call of the step goes through it
+
+    def load_inputs(self, x, conv_w, conv_b, fc_w, fc_b, local_remote, labels):
+        """fc_w / fc_b: the full dense layers ([in][out], [out]); worker r's
+        shard is columns r*ns .. (r+1)*ns - 1.  local_remote [K-1][B][F]:
+        the other workers' conv outputs; labels [K][B]."""
+        t = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32))
+        self.conv.load_inputs(x, conv_w, conv_b)
+        K = self.K
+        for j in range(self.L):
+            w = np.asarray(fc_w[j], np.float32).reshape(self.ins[j], K, self.ns[j])
+            self.W[j].copy_(t(w.transpose(1, 0, 2)))
+            self.b[j].copy_(t(np.asarray(fc_b[j], np.float32).reshape(K, self.ns[j])))
+        if K > 1:
+            self.local[1:].copy_(t(local_remote))
+        self.labels.copy_(torch.from_numpy(np.ascontiguousarray(labels, dtype=np.int32)))
+
+    def full_weights(self, j):
+        """Layer j's full weight [in][out] on the host (the shards side by side)."""
+        w = self.W[j].detach().cpu().numpy()
+        return np.ascontiguousarray(w.transpose(1, 0, 2).reshape(self.ins[j], -1))
+
+    def full_bias(self, j):
+        return self.b[j].detach().cpu().numpy().reshape(-1)
+
+    # -- the step ---------------------------------------------------------------
+    def iteration(self, k, stream=None):
+        """Modulo iteration k: forward, loss, backward and FC update."""
+        c = self.call
+        K, L = self.K, self.L
+        c(("mfwd", k), sb.sb_modulo_fwd, self.mdesc, 0, k, self.local, self.X[0], None, stream)
+        for j in range(L):
+            for r in range(K):
+                c(("fc_fwd", j), sb.sb_fc_shard_fwd, self.fdesc[j], self.X[j], self.W[j][r],
+                  self.b[j][r], self.P[j][r], self.ws, stream)
+            c(("sfwd", j), sb.sb_shard_fwd, self.sdesc[j], 0, self.P[j], self.X[j + 1], None,
+              stream)
+        c(("loss", k), sb.sb_log_softmax_nll, self.B, self.classes, self.X[L], self.labels[k],
+          1.0 / self.B, None, self.loss[k], self.dZl, None, stream)
+        for j in reversed(range(L)):
+            for r in range(K):
+                if j == L - 1:
+                    dy = self.dZl.data_ptr() + 4 * r * self.ns[j]     # its columns of dZl
+                else:
+                    dy = self.dP[j][r]
+                mask = self.P[j][r] if self.relu[j] else None
+                c(("fc_bwd", j), sb.sb_fc_shard_bwd, self.bdesc[j], self.X[j], self.W[j][r], dy,
+                  mask, self.dF[j][r], self.dW[j][r], self.db[j][r], False, self.ws, stream)
+            if j > 0:
+                c(("sbwd", j), sb.sb_shard_bwd, self.sdesc[j - 1], 0, self.dF[j], self.dP[j - 1],
+                  None, None, stream)
+            else:
+                c(("mbwd", k), sb.sb_modulo_bwd, self.mdesc, 0, k, self.dF[0], self.dlocal,
+                  None, None, stream)
+        c(("sgd_fc", k), sb.sb_sgd_update, self.sgd_fc, self.lr, stream)
+
+    def finish(self, stream=None):
+        """Conv backward from the gathered local-row gradients, conv update."""
+        self.conv.backward(stream)
+        self.call(("sgd_conv", 0), sb.sb_sgd_update, self.sgd_conv, self.lr, stream)
+
+    def step(self, stream=None):
+        self.conv.forward(stream)
+        for k in range(self.K):
+            self.iteration(k, stream)
+        self.finish(stream)
 
     def step_calls(self):
         """The ordered (key, libsb function, args) calls of one step."""

@@ -332,42 +332,73 @@ def test_paper_variant_hybrid_step_end_to_end():
     _check_hybrid(hs, r, layers)
 
 
-def test_paper_variant_training_step_end_to_end():
-    """The paper's VGG variant as a whole training step of one worker of an
-    MP group of 2: the log-softmax + NLL of the full 10-class logits (this
-    shard's 5 columns and a stand-in for the other shard's) gives the
-    gradient of the last shard, and one SGD step updates the conv layers at
-    rate lr and the FC shards at lr / K."""
-    n, hw, R, S, lr = 3, 32, 2, 2, 0.05
-    print_case("paper_variant_training_step", n=n, replicas=R, shards=S)
-    fc_shapes = configs.PAPER_VARIANT_FC
-    layers, x, wts, bs, fw, fb, rows, cols, _ = _hybrid_inputs(
-        n, hw, R, S, configs.PAPER_VARIANT_CONV, fc_shapes, 9)
-    m, classes, ns = n * R, fc_shapes[-1][1], fc_shapes[-1][1] // S
-    labels = synth.labels(m, classes, 9, synth.TID.LABELS)
-    logits_remote = synth.normal((m, classes - ns), 9, synth.TID.LOGITS_REMOTE)
-    hs = HybridStep(configs.PAPER_VARIANT_CONV, n, 3, hw, R, fc_shapes, S, train=True, lr=lr)
-    hs.load_inputs(x, wts, bs, fw, fb, rows, cols, None)
-    hs.load_targets(labels, logits_remote)
-    hs.step()
+def _group_inputs(n, K, fc_shapes, seed, schedule=configs.PAPER_VARIANT_CONV):
+    layers = configs.conv_layers(schedule, 3, 32)
+    x, wts, bs = _vgg_inputs(n, 32, seed, layers)
+    F = fc_shapes[0][0]
+    fw = [synth.xavier_uniform(fi, fo, seed, synth.TID.FC_W + j)
+          for j, (fi, fo) in enumerate(fc_shapes)]
+    fb = [synth.normal((fo,), seed, synth.TID.FC_B + j, std=0.05)
+          for j, (_, fo) in enumerate(fc_shapes)]
+    remote = synth.relu_normal((K - 1, n, F), seed, synth.TID.X0_REMOTE)
+    labels = synth.labels(K * n, fc_shapes[-1][1], seed, synth.TID.LABELS).reshape(K, n)
+    return layers, x, wts, bs, fw, fb, remote, labels
+
+
+@pytest.mark.parametrize("K,n,fc_shapes", [
+    (2, 4, configs.PAPER_VARIANT_FC),
+    (4, 8, [(4096, 256), (256, 128), (128, 8)])], ids=["paper_variant_K2", "K4"])
+def test_group_training_step_end_to_end(K, n, fc_shapes):
+    """A training step of an MP group of K (the paper's VGG variant's conv
+    stack on worker 0): K modulo iterations, each gathering B rows, running
+    every worker's FC shards with shard layers between them, the loss of the
+    full logits, the backward and an FC update with the gradient divided by
+    K; then the conv backward and update.  Every iteration's gathered batch,
+    logits, losses and shard gradients, and the step's updated parameters,
+    against the oracle's group step (sec. 3.1, Modulo Layer)."""
+    from paper_2112_15317_amd import partition as P
+    from paper_2112_15317_amd.stack import GroupTrainStep
+    lr = 0.05
+    print_case("group_training_step", K=K, n=n, fc=fc_shapes)
+    plan = P.fc_plan(P.partition(P.vgg_net(configs.PAPER_VARIANT_CONV, 3, 32, fc_shapes), K))
+    layers, x, wts, bs, fw, fb, remote, labels = _group_inputs(n, K, fc_shapes, 9 + K)
+    gs = GroupTrainStep(configs.PAPER_VARIANT_CONV, n, 3, 32, plan, lr=lr)
+    gs.load_inputs(x, wts, bs, fw, fb, remote, labels)
+    gs.conv.forward()
+    snaps = []
+    for k in range(K):
+        gs.iteration(k)
+        torch.cuda.synchronize()
+        snaps.append({"gathered": to_host(gs.X[0]), "logits": to_host(gs.X[gs.L]),
+                      "loss": to_host(gs.loss[k]),
+                      "dW": [to_host(w) for w in gs.dW], "db": [to_host(b) for b in gs.db]})
+    gs.finish()
     torch.cuda.synchronize()
     pools = [L.pool_after for L in layers]
-    r = OS.hybrid_step(x, wts, bs, pools, fw, fb, rows, cols, None,
-                       train={"labels": labels, "logits_remote": logits_remote, "lr": lr,
-                              "shards": S})
+    r = OS.group_train_step(x, wts, bs, pools, fw, fb, remote, labels, lr)
     tol = TOL["f32"]
-    assert rel_l2(to_host(hs.loss), r["loss"]) <= tol
-    assert rel_l2(to_host(hs.dZl)[:, :ns], r["dz"][:, :ns]) <= tol
-    for j in range(hs.L):
-        assert rel_l2(to_host(hs.fc[j].dW), r["dw"][j]) <= tol, "dW_fc%d" % j
-        # The update itself (new minus old parameters): lr / K times the gradient.
-        assert rel_l2(to_host(hs.fc[j].W) - fw[j], r["fc_w_new"][j] - fw[j]) <= tol, "W_fc%d" % j
-        assert rel_l2(to_host(hs.fc[j].b) - fb[j], r["fc_b_new"][j] - fb[j]) <= tol, "b_fc%d" % j
+    for L in layers:
+        if L.pool_after:
+            np.testing.assert_array_equal(gs.conv.idx[L.index].cpu().numpy(),
+                                          r["fwd"]["idx"][L.index])
+    for k, (sn, it) in enumerate(zip(snaps, r["iters"])):
+        assert rel_l2(sn["gathered"], it["gathered"]) <= tol, "gathered, iteration %d" % k
+        assert rel_l2(sn["logits"], it["logits"]) <= tol, "logits, iteration %d" % k
+        assert rel_l2(sn["loss"], it["loss"]) <= tol, "loss, iteration %d" % k
+        for j in range(gs.L):
+            for w in range(K):
+                assert rel_l2(sn["dW"][j][w], it["dw"][j][w]) <= tol, "dW fc%d w%d it%d" % (j, w, k)
+                assert rel_l2(sn["db"][j][w], it["db"][j][w]) <= tol, "db fc%d w%d it%d" % (j, w, k)
+    for j in range(gs.L):
+        # The accumulated update of K steps (new minus initial parameters).
+        assert rel_l2(gs.full_weights(j) - fw[j], r["fc_w_new"][j] - fw[j]) <= tol, "W_fc%d" % j
+        assert rel_l2(gs.full_bias(j) - fb[j], r["fc_b_new"][j] - fb[j]) <= tol, "b_fc%d" % j
+    assert rel_l2(to_host(gs.dlocal), r["dlocal"]) <= tol
     for L in layers:
         i = L.index
-        assert rel_l2(to_host(hs.conv.dW[i]), r["bwd"]["dW"][i]) <= tol, "dW%d" % i
-        assert rel_l2(to_host(hs.conv.W[i]) - wts[i], r["conv_w_new"][i] - wts[i]) <= tol, "W%d" % i
-        assert rel_l2(to_host(hs.conv.b[i]) - bs[i], r["conv_b_new"][i] - bs[i]) <= tol, "b%d" % i
+        assert rel_l2(to_host(gs.conv.dW[i]), r["bwd"]["dW"][i]) <= tol, "dW%d" % i
+        assert rel_l2(to_host(gs.conv.W[i]) - wts[i], r["conv_w_new"][i] - wts[i]) <= tol, "W%d" % i
+        assert rel_l2(to_host(gs.conv.b[i]) - bs[i], r["conv_b_new"][i] - bs[i]) <= tol, "b%d" % i
 
 
 def test_graph_replay_matches_eager():

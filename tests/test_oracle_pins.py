@@ -354,52 +354,6 @@ def test_hybrid_step_matches_torch_autograd():
         np.testing.assert_allclose(r["bwd"]["dW"][l], wt[l].grad.numpy(), rtol=1e-10, atol=1e-11)
 
 
-def test_hybrid_training_step_matches_torch_autograd_and_sgd():
-    """The training form of the step: the last shard's output and remote
-    logit columns form the full logits, the loss is torch's mean
-    cross-entropy (log-softmax + NLL), and the updated parameters are the
-    torch gradients stepped by lr (conv) and lr / K (FC shards)."""
-    n, rep, K, lr = 2, 3, 2, 0.3
-    sched = [(3, 4, True), (4, 8, True)]
-    x = rng.standard_normal((n, 3, 4, 4))
-    ws = [rng.standard_normal((k, c, 3, 3)) for c, k, _ in sched]
-    bs = [rng.standard_normal(k) * 0.1 for _, k, _ in sched]
-    pools = [p for *_, p in sched]
-    ns, remote, classes = [5, 3], [4], 7
-    ins = [8, ns[0] + remote[0]]
-    fw = [rng.standard_normal((ins[j], ns[j])) for j in range(2)]
-    fb = [rng.standard_normal(ns[j]) for j in range(2)]
-    m = n * rep
-    rows = np.maximum(rng.standard_normal((m - n, 8)), 0)
-    cols = [np.maximum(rng.standard_normal((m, remote[0])), 0)]
-    logits_remote = rng.standard_normal((m, classes - ns[1]))
-    labels = np.array([0, 6, 2, 3, 4, 1])
-    r = OS.hybrid_step(x, ws, bs, pools, fw, fb, rows, cols, None,
-                       train={"labels": labels, "logits_remote": logits_remote, "lr": lr,
-                              "shards": K})
-    xt = _t(x, True); wt = [_t(w, True) for w in ws]; bt = [_t(b, True) for b in bs]
-    a = xt
-    for l in range(2):
-        a = torch.relu(F.max_pool2d(F.conv2d(a, wt[l], bt[l], padding=1), 2, 2))
-    h = torch.cat([a.reshape(n, 8), _t(rows)], 0)
-    fwt = [_t(w, True) for w in fw]; fbt = [_t(b, True) for b in fb]
-    h = torch.cat([torch.relu(h @ fwt[0] + fbt[0]), _t(cols[0])], 1)
-    z = torch.cat([h @ fwt[1] + fbt[1], _t(logits_remote)], 1)
-    loss = F.cross_entropy(z, torch.tensor(labels), reduction="mean")
-    loss.backward()
-    assert abs(r["loss"].mean() - loss.item()) < 1e-12
-    for l in range(2):
-        np.testing.assert_allclose(r["conv_w_new"][l], ws[l] - lr * wt[l].grad.numpy(),
-                                   rtol=1e-10, atol=1e-11)
-        np.testing.assert_allclose(r["conv_b_new"][l], bs[l] - lr * bt[l].grad.numpy(),
-                                   rtol=1e-10, atol=1e-11)
-    for j in range(2):
-        np.testing.assert_allclose(r["fc_w_new"][j], fw[j] - lr / K * fwt[j].grad.numpy(),
-                                   rtol=1e-10, atol=1e-11)
-        np.testing.assert_allclose(r["fc_b_new"][j], fb[j] - lr / K * fbt[j].grad.numpy(),
-                                   rtol=1e-10, atol=1e-11)
-
-
 def test_bf16_stack_rounds_at_storage_points():
     sched = [(3, 4, False), (4, 4, True)]
     x = O.round_bf16(rng.standard_normal((1, 3, 4, 4)))

@@ -11,22 +11,7 @@ from paper_2112_15317_amd import partition as P
 
 def vgg_variant():
     """The paper's VGG variant on 3x32x32 images as a sequential CNN."""
-    layers, c, hw = [], 3, 32
-    for v in configs.PAPER_VARIANT_CONV:
-        if v == configs.POOL:
-            layers.append(P.Layer(P.POOLING, c * hw * hw, c * (hw // 2) ** 2))
-            hw //= 2
-        else:
-            layers += [P.Layer(P.CONV, c * hw * hw, v * hw * hw), P.Layer(P.RELU)]
-            c = v
-    layers.append(P.Layer(P.RESHAPE, c * hw * hw, c * hw * hw))
-    fc = configs.PAPER_VARIANT_FC
-    for j, (i, o) in enumerate(fc):
-        layers.append(P.linear(i, o))
-        if j < len(fc) - 1:
-            layers.append(P.Layer(P.RELU))
-    layers.append(P.Layer(P.LOG_SOFTMAX))
-    return P.seq(*layers)
+    return P.vgg_net(configs.PAPER_VARIANT_CONV, 3, 32, configs.PAPER_VARIANT_FC)
 
 
 def kinds(layers):
@@ -104,3 +89,23 @@ def test_unsplittable_layer_after_a_split_layer_is_rejected():
         P.partition(net, 2)
     with pytest.raises(ValueError):
         P.partition(P.seq(P.linear(64, 30)), 4)      # 30 outputs do not split in 4
+
+
+def test_fc_plan_of_the_vgg_variant():
+    """The call sequence of the training step's model-parallel part."""
+    plan = P.fc_plan(P.partition(vgg_variant(), 2))
+    assert plan == [("modulo", 4096),
+                    ("linear", 4096, 512, 1024, True), ("shard", 512, 1024),
+                    ("linear", 1024, 512, 1024, True), ("shard", 512, 1024),
+                    ("linear", 1024, 5, 10, False), ("shard", 5, 10),
+                    ("loss", 10)]
+    with pytest.raises(ValueError):
+        P.fc_plan(P.partition(vgg_variant(), 1))       # no model parallelism
+
+
+def test_nested_containers_flatten_in_order():
+    inner = P.seq(P.linear(64, 32), P.Layer(P.RELU))
+    net = P.seq(inner, P.seq(P.linear(32, 16)), P.Layer(P.LOG_SOFTMAX))
+    assert [l.kind for l in P.flatten(net)] == [P.LINEAR, P.RELU, P.LINEAR, P.LOG_SOFTMAX]
+    assert kinds(P.partition(net, 4)) == [P.MODULO, P.LINEAR, P.RELU, P.SHARD, P.LINEAR,
+                                          P.SHARD, P.LOG_SOFTMAX]
