@@ -259,6 +259,11 @@ def num_threads() -> int:
 
 
 # ------------------------------------------------------------- rounding --
+def round_f32(a):
+    """Nearest float32 value (ties to even) of each element, as float64."""
+    return np.asarray(_f64(a), np.float64).astype(np.float32).astype(np.float64)
+
+
 def round_bf16(a):
     """Nearest bfloat16 value (ties to even) of each element, as float64."""
     a = _f64(a).copy()

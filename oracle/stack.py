@@ -10,18 +10,24 @@ The stack's layer list is an input: ``weights[l]`` (KCRS), ``biases[l]`` and
 ``pool_after[l]`` (a ReLU + 2x2 max pool follows conv l; otherwise a ReLU
 follows it).  The stack must end with a pool.
 
-With ``bf16=True`` every tensor the bf16 GPU path stores in bfloat16 is
-rounded to bfloat16 at the same point: conv outputs (before the pool, or
-after the fused ReLU), the pooled outputs (already bf16 values), and the
-activation gradients produced by the data-gradient convolution.  Weight and
-bias gradients stay in full precision.
+``store`` names the element type the GPU path keeps its activations and
+activation gradients in: with ``"bf16"`` (or ``bf16=True``) / ``"f32"``
+every such tensor is rounded to bfloat16 / float32 (nearest, ties to even)
+at the point where the GPU stores it: conv outputs (before the pool, or
+after the fused ReLU), the pooled outputs (already representable), the
+activation gradients the data-gradient convolution produces and, in the
+hybrid step, the FC shard outputs and partial input gradients.  Weight and
+bias gradients stay in full precision.  The rounded chain is what the
+per-call parity tests feed the GPU: every call's inputs are the oracle's own
+tensors, held exactly in the GPU's storage type.  ``store=None`` keeps
+everything in float64.
 """
 from __future__ import annotations
 
 import numpy as np
 
 from . import (_f64, conv3x3_bwd_data, conv3x3_bwd_weight, conv3x3_fwd,
-               fc_bwd, fc_fwd, relu_maxpool_bwd, relu_maxpool_fwd, round_bf16)
+               fc_bwd, fc_fwd, relu_maxpool_bwd, relu_maxpool_fwd, round_bf16, round_f32)
 from .modulo import modulo_bwd, modulo_fwd, shard_bwd, shard_fwd
 from .train import log_softmax_nll, sgd_update
 
@@ -30,12 +36,22 @@ def _identity(a):
     return a
 
 
-def vgg_forward(x, weights, biases, pool_after, bf16=False):
+def _rounder(store, bf16=False):
+    if bf16 or store == "bf16":
+        return round_bf16
+    if store == "f32":
+        return round_f32
+    if store is None:
+        return _identity
+    raise ValueError("store must be None, 'f32' or 'bf16'")
+
+
+def vgg_forward(x, weights, biases, pool_after, bf16=False, store=None):
     """Forward of the conv stack.  Returns a dict with
     ``A``: list of layer inputs A[0] = x ... A[L] = stack output,
     ``Z``: {l: pre-pool conv output} for pooled layers,
     ``idx``: {l: pool window codes} for pooled layers."""
-    rnd = round_bf16 if bf16 else _identity
+    rnd = _rounder(store, bf16)
     if not pool_after[-1]:
         raise ValueError("the stack must end with a pooled layer")
     A = [_f64(x)]
@@ -51,12 +67,12 @@ def vgg_forward(x, weights, biases, pool_after, bf16=False):
     return {"A": A, "Z": Z, "idx": idx}
 
 
-def vgg_backward(fwd, weights, pool_after, dy_top, bf16=False, want_dx=True):
+def vgg_backward(fwd, weights, pool_after, dy_top, bf16=False, want_dx=True, store=None):
     """Backward of the conv stack from the gradient of its output.
     Returns ``dZ`` (gradient at each conv output, after the ReLU/pool),
     ``dA`` (gradient arriving at each pooled output), ``dW``, ``db`` and
     ``dX`` (gradient of the stack input; None unless want_dx)."""
-    rnd = round_bf16 if bf16 else _identity
+    rnd = _rounder(store, bf16)
     A, idx = fwd["A"], fwd["idx"]
     L = len(weights)
     dZ, dA, dW, db = {}, {}, {}, {}
@@ -76,13 +92,14 @@ def vgg_backward(fwd, weights, pool_after, dy_top, bf16=False, want_dx=True):
     return {"dZ": dZ, "dA": dA, "dW": dW, "db": db, "dX": dX}
 
 
-def vgg_step(x, weights, biases, pool_after, dy_top, bf16=False, want_dx=True):
-    f = vgg_forward(x, weights, biases, pool_after, bf16=bf16)
-    b = vgg_backward(f, weights, pool_after, dy_top, bf16=bf16, want_dx=want_dx)
+def vgg_step(x, weights, biases, pool_after, dy_top, bf16=False, want_dx=True, store=None):
+    f = vgg_forward(x, weights, biases, pool_after, bf16=bf16, store=store)
+    b = vgg_backward(f, weights, pool_after, dy_top, bf16=bf16, want_dx=want_dx, store=store)
     return f, b
 
 
-def hybrid_step(x, weights, biases, pool_after, fc_w, fc_b, rows_remote, cols_remote, dy):
+def hybrid_step(x, weights, biases, pool_after, fc_w, fc_b, rows_remote, cols_remote, dy,
+                store=None):
     """One worker's forward and backward of the hybrid scheme on one device,
     with L FC shards and no update (so the gathered rows of all K modulo
     iterations can go through the FC shards in one batch: with no update in
@@ -102,14 +119,15 @@ def hybrid_step(x, weights, biases, pool_after, fc_w, fc_b, rows_remote, cols_re
     and are not part of one worker's compute.)
     """
     L = len(fc_w)
-    f = vgg_forward(x, weights, biases, pool_after)
+    rnd = _rounder(store)
+    f = vgg_forward(x, weights, biases, pool_after, store=store)
     top = f["A"][-1]
     n = top.shape[0]
     feat = int(np.prod(top.shape[1:]))
     xs = [np.concatenate([top.reshape(n, feat), np.asarray(rows_remote, np.float64)], axis=0)]
     ys = []
     for j in range(L):
-        y = fc_fwd(xs[j], fc_w[j], fc_b[j], relu=j < L - 1)
+        y = rnd(fc_fwd(xs[j], fc_w[j], fc_b[j], relu=j < L - 1))
         ys.append(y)
         if j < L - 1:
             xs.append(np.concatenate([y, np.asarray(cols_remote[j], np.float64)], axis=1))
@@ -119,10 +137,11 @@ def hybrid_step(x, weights, biases, pool_after, fc_w, fc_b, rows_remote, cols_re
         dys[j] = g
         dxp[j], dw[j], db[j] = fc_bwd(xs[j], fc_w[j], g,
                                       mask_src=ys[j] if j < L - 1 else None)
+        dxp[j] = rnd(dxp[j])
         if j > 0:
             g = np.ascontiguousarray(dxp[j][:, :ys[j - 1].shape[1]])
     dtop = np.ascontiguousarray(dxp[0][:n]).reshape(top.shape)
-    b = vgg_backward(f, weights, pool_after, dtop)
+    b = vgg_backward(f, weights, pool_after, dtop, store=store)
     return {"fwd": f, "bwd": b, "xs": xs, "ys": ys, "dys": dys, "dxp": dxp, "dw": dw, "db": db}
 
 

@@ -1,0 +1,107 @@
+"""Per-call parity on the oracle's chain: helpers shared by the full-size
+GPU tests.
+
+Every call of a step reads tensors the calls before it produced.  The
+oracle's storage-rounded chain (``oracle.stack`` with ``store=``) holds each
+of those tensors exactly in the GPU's storage type, so a call can be run on
+the GPU with *the oracle's* inputs (uploaded into the step's own buffers,
+with the step's own descriptors and workspaces: the launch configuration
+the benchmark times) and its outputs compared, in full, with the oracle's
+outputs of the same call.  No GPU result ever feeds the oracle, and every
+decision (a ReLU mask, a pool window's first maximum) is taken on the same
+values on both sides, so pool codes and routed gradients must match bit for
+bit and every other output meets the dtype's tolerance.
+"""
+import numpy as np
+import torch
+
+from tests.helpers import TOL, rel_l2, to_host
+
+EXACT = "exact"
+
+
+def put(buf, arr):
+    """Upload a host array into a device buffer (any view), exactly."""
+    t = torch.from_numpy(np.ascontiguousarray(arr, dtype=np.float32)).reshape(buf.shape)
+    if buf.dtype == torch.uint8:
+        t = torch.from_numpy(np.ascontiguousarray(arr, dtype=np.uint8)).reshape(buf.shape)
+    buf.copy_(t.to(buf.dtype))
+
+
+def conv_io(st, f, b, key):
+    """(uploads, checks) of one ConvStack call on the oracle chain (f, b).
+    uploads: [(buffer, host array)]; checks: [(name, buffer, ref, tol|EXACT)]."""
+    kind, i = key
+    L = st.layers
+    pool = L[i].pool_after if kind != "pack" else False
+    tol = TOL[st.dtype]
+    if kind == "pack":
+        return [], []
+    if kind == "fwd":
+        out, ref = (st.Z[i], f["Z"][i]) if pool else (st.A[i + 1], f["A"][i + 1])
+        return [(st.A[i], f["A"][i])], [("fwd%d" % i, out, ref, tol)]
+    if kind == "pool_fwd":
+        return [(st.Z[i], f["Z"][i])], [("pool_fwd%d.y" % i, st.A[i + 1], f["A"][i + 1], EXACT),
+                                         ("pool_fwd%d.idx" % i, st.idx[i], f["idx"][i], EXACT)]
+    if kind == "pool_bwd":
+        return ([(st.gA[i + 1], b["dA"][i]), (st.idx[i], f["idx"][i])],
+                [("pool_bwd%d" % i, st.dZ[i], b["dZ"][i], EXACT)])
+    g = st.dZ[i] if pool else st.gA[i + 1]
+    if kind == "wgrad":
+        # fp32 weight and bias gradients (sums of exact products in bf16 too).
+        return ([(st.A[i], f["A"][i]), (g, b["dZ"][i])],
+                [("wgrad%d.dw" % i, st.dW[i], b["dW"][i], TOL["f32"]),
+                 ("wgrad%d.db" % i, st.db[i], b["db"][i], TOL["f32"])])
+    if kind == "dgrad":
+        ups = [(g, b["dZ"][i])]
+        if i == 0:
+            ref = b["dX"]
+        elif L[i - 1].pool_after:
+            ref = b["dA"][i - 1]
+        else:
+            ups.append((st.A[i], f["A"][i]))      # the ReLU mask of layer i-1
+            ref = b["dZ"][i - 1]
+        return ups, [("dgrad%d" % i, st.gA[i], ref, tol)]
+    raise KeyError(key)
+
+
+def run_and_check(call, uploads, checks):
+    """Upload, run the one call, compare every output in full."""
+    _, fn, args = call
+    for buf, arr in uploads:
+        put(buf, arr)
+    torch.cuda.synchronize()
+    fn(*args)
+    torch.cuda.synchronize()
+    worst = {}
+    for name, buf, ref, tol in checks:
+        got = to_host(buf)
+        ref = np.asarray(ref).reshape(got.shape)
+        if tol == EXACT:
+            bad = int(np.count_nonzero(got != ref))
+            assert bad == 0, "%s: %d elements differ" % (name, bad)
+            worst[name] = 0.0
+        else:
+            e = rel_l2(got, ref)
+            worst[name] = e
+            assert e <= tol, "%s: relative L2 %.3g > %.3g" % (name, e, tol)
+    return worst
+
+
+def near_tie_flips(z, ref_idx, got_idx, eps):
+    """Windows whose codes differ; each must be a near-tie of the oracle's
+    values (the two candidates, or the maximum and zero for the ReLU flag,
+    within eps).  Returns the number of such windows."""
+    bad = np.nonzero(np.asarray(ref_idx).ravel() != np.asarray(got_idx).ravel())[0]
+    if bad.size == 0:
+        return 0
+    n, c, h, w = z.shape
+    zw = z.reshape(n, c, h // 2, 2, w // 2, 2).transpose(0, 1, 2, 4, 3, 5).reshape(-1, 4)
+    r, g = np.asarray(ref_idx).ravel(), np.asarray(got_idx).ravel()
+    for f in bad:
+        a, bb = r[f], g[f]
+        va, vb = zw[f, a & 3], zw[f, bb & 3]
+        gap = abs(va - vb) if (a & 3) != (bb & 3) else 0.0
+        flag_gap = abs(va) if (a & 0x80) != (bb & 0x80) else 0.0
+        assert max(gap, flag_gap) <= eps, "code mismatch at window %d is not a near-tie" % f
+    return int(bad.size)

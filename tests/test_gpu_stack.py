@@ -1,12 +1,7 @@
-"""GPU parity at the workloads' real shapes, and end-to-end through the stacks.
-
-* Every distinct layer shape of the VGG-16 CIFAR stack (batch 128) runs each
-  conv pass in the same launch configuration the benchmark times; the oracle
-  evaluates a sample of outputs one by one.
-* The whole VGG-16 stack and the hybrid worker step run end-to-end from the
-  seeded inputs at a batch the oracle finishes in seconds; every forward
-  tensor, pool code and gradient is compared layer by layer.
-"""
+"""GPU parity end to end through the stacks at small batches (nonzero
+biases, the paper's VGG variant, the group training step), graph replays,
+the overlapped backward and packed filters.  The workloads' own shapes are
+checked call by call in test_gpu_full_size*.py."""
 import numpy as np
 import pytest
 import torch
@@ -15,107 +10,10 @@ import oracle as O
 from oracle import stack as OS
 from paper_2112_15317_amd import configs, sb, synth
 from paper_2112_15317_amd.stack import ConvStack, HybridStep
-from tests.helpers import TOL, print_case, rel_l2, sample_idx, to_dev, to_host
+from tests.helpers import TOL, print_case, rel_l2, to_host
 
 pytestmark = pytest.mark.gpu
 
-VGG_CIFAR = configs.conv_layers(configs.VGG16, 3, 32)
-SAMPLES = 3000
-
-
-def _ws(nbytes):
-    # The workspace needs no initialisation: hand it over full of NaN bytes.
-    return torch.full((max(int(nbytes), 256),), 0xFF, dtype=torch.uint8, device="cuda")
-
-
-@pytest.mark.parametrize("L", VGG_CIFAR, ids=lambda L: "conv%d_%dx%d_%d" % (L.index + 1, L.c, L.k, L.h))
-def test_vgg_cifar_layer_full_size_sampled(L):
-    n = 128
-    print_case("layer_full", layer=L.index, c=L.c, k=L.k, h=L.h, n=n)
-    seed = 100 + L.index
-    x = np.maximum(synth.normal((n, L.c, L.h, L.w), seed, synth.TID.IMAGES), 0)
-    if L.index == 0:
-        x = synth.normal((n, L.c, L.h, L.w), seed, synth.TID.IMAGES)
-    wt = synth.he_normal_conv3x3(L.k, L.c, seed, synth.TID.CONV_W)
-    dy = synth.normal((n, L.k, L.h, L.w), seed, synth.TID.DY_TOP)
-    relu = not L.pool_after
-    mask = x if L.index > 0 else None
-    xd, wd, dyd = to_dev(x), to_dev(wt), to_dev(dy)
-    df = sb.conv_desc(n, L.c, L.h, L.w, L.k, sb.SB_F32, relu=relu)
-    db_ = sb.conv_desc(n, L.c, L.h, L.w, L.k, sb.SB_F32)
-    ws = _ws(max(sb.sb_conv3x3_workspace_bytes(df, 0), sb.sb_conv3x3_workspace_bytes(db_, 1),
-                 sb.sb_conv3x3_workspace_bytes(db_, 2)))
-    y = torch.empty((n, L.k, L.h, L.w), device="cuda")
-    dx = torch.empty((n, L.c, L.h, L.w), device="cuda")
-    dw = torch.empty((L.k, L.c, 3, 3), device="cuda")
-    dbias = torch.empty((L.k,), device="cuda")
-    sb.sb_conv3x3_fwd(df, xd, wd, None, y, ws)
-    sb.sb_conv3x3_bwd_data(db_, dyd, wd, xd if mask is not None else None, dx, ws)
-    sb.sb_conv3x3_bwd_weight(db_, xd, dyd, dw, dbias, ws)
-    torch.cuda.synchronize()
-    f = sample_idx(y.numel(), SAMPLES, seed)
-    assert rel_l2(to_host(y).ravel()[f], O.conv3x3_fwd_at(x, wt, f, relu=relu)) <= TOL["f32"]
-    f = sample_idx(dx.numel(), SAMPLES, seed + 1)
-    ref = O.conv3x3_bwd_data_at(dy, wt, f, mask_src=mask)
-    assert rel_l2(to_host(dx).ravel()[f], ref) <= TOL["f32"]
-    f = sample_idx(dw.numel(), min(SAMPLES, 600), seed + 2)
-    assert rel_l2(to_host(dw).ravel()[f], O.conv3x3_bwd_weight_at(x, dy, f)) <= TOL["f32"]
-    assert rel_l2(to_host(dbias), dy.astype(np.float64).sum(axis=(0, 2, 3))) <= TOL["f32"]
-
-
-def _distinct(layers):
-    seen, out = set(), []
-    for L in layers:
-        key = (L.c, L.k, L.h, L.pool_after, L.index == 0)
-        if key not in seen:
-            seen.add(key)
-            out.append(L)
-    return out
-
-
-VGG_IMAGENET = _distinct(configs.conv_layers(configs.VGG16, 3, 224))
-
-
-@pytest.mark.parametrize("L", VGG_IMAGENET,
-                         ids=lambda L: "conv%d_%dx%d_%d" % (L.index + 1, L.c, L.k, L.h))
-def test_vgg_imagenet_bf16_layer_full_size_sampled(L):
-    """bf16 activations / filters, fp32 accumulation, batch 32 at 224x224:
-    each distinct layer shape of the ImageNet-shaped stack, sampled."""
-    n = 32
-    print_case("layer_full_bf16", layer=L.index, c=L.c, k=L.k, h=L.h, n=n)
-    seed = 300 + L.index
-    x = synth.normal((n, L.c, L.h, L.w), seed, synth.TID.IMAGES)
-    if L.index > 0:
-        x = np.maximum(x, 0)
-    wt = synth.he_normal_conv3x3(L.k, L.c, seed, synth.TID.CONV_W)
-    dy = synth.normal((n, L.k, L.h, L.w), seed, synth.TID.DY_TOP)
-    relu = not L.pool_after
-    xd, wd, dyd = to_dev(x, "bf16"), to_dev(wt, "bf16"), to_dev(dy, "bf16")
-    del x, dy
-    # The oracle sees the bf16 values the kernels read.
-    x, wt, dy = to_host(xd), to_host(wd), to_host(dyd)
-    mask = x if L.index > 0 else None
-    df = sb.conv_desc(n, L.c, L.h, L.w, L.k, sb.SB_BF16, relu=relu)
-    db_ = sb.conv_desc(n, L.c, L.h, L.w, L.k, sb.SB_BF16)
-    ws = _ws(max(sb.sb_conv3x3_workspace_bytes(df, 0), sb.sb_conv3x3_workspace_bytes(db_, 1),
-                 sb.sb_conv3x3_workspace_bytes(db_, 2)))
-    y = torch.empty((n, L.k, L.h, L.w), dtype=torch.bfloat16, device="cuda")
-    dx = torch.empty((n, L.c, L.h, L.w), dtype=torch.bfloat16, device="cuda")
-    dw = torch.empty((L.k, L.c, 3, 3), device="cuda")
-    dbias = torch.empty((L.k,), device="cuda")
-    sb.sb_conv3x3_fwd(df, xd, wd, None, y, ws)
-    sb.sb_conv3x3_bwd_data(db_, dyd, wd, xd if mask is not None else None, dx, ws)
-    sb.sb_conv3x3_bwd_weight(db_, xd, dyd, dw, dbias, ws)
-    torch.cuda.synchronize()
-    f = sample_idx(y.numel(), SAMPLES, seed)
-    assert rel_l2(to_host(y).ravel()[f], O.conv3x3_fwd_at(x, wt, f, relu=relu)) <= TOL["bf16"]
-    f = sample_idx(dx.numel(), SAMPLES, seed + 1)
-    ref = O.conv3x3_bwd_data_at(dy, wt, f, mask_src=mask)
-    assert rel_l2(to_host(dx).ravel()[f], ref) <= TOL["bf16"]
-    # Weight gradients are fp32 sums of exact bf16 products: fp32 bound.
-    f = sample_idx(dw.numel(), 300, seed + 2)
-    assert rel_l2(to_host(dw).ravel()[f], O.conv3x3_bwd_weight_at(x, dy, f)) <= TOL["f32"]
-    assert rel_l2(to_host(dbias), dy.astype(np.float64).sum(axis=(0, 2, 3))) <= TOL["f32"]
 
 
 def _vgg_inputs(n, hw, seed, layers):
@@ -125,24 +23,11 @@ def _vgg_inputs(n, hw, seed, layers):
     return x, ws, bs
 
 
-def _near_ties(z, ref_idx, got_idx, eps):
-    """Windows whose codes differ must be near-ties in the oracle's values:
-    the two candidates (or the max and zero, for the ReLU flag) within eps."""
-    bad = np.nonzero(ref_idx.ravel() != got_idx.ravel())[0]
-    if bad.size == 0:
-        return 0
-    n, c, h, w = z.shape
-    zw = z.reshape(n, c, h // 2, 2, w // 2, 2).transpose(0, 1, 2, 4, 3, 5).reshape(-1, 4)
-    for f in bad:
-        a, b = ref_idx.ravel()[f], got_idx.ravel()[f]
-        va, vb = zw[f, a & 3], zw[f, b & 3]
-        gap = abs(va - vb) if (a & 3) != (b & 3) else 0.0
-        flag_gap = abs(va) if (a & 0x80) != (b & 0x80) else 0.0
-        assert max(gap, flag_gap) <= eps, "code mismatch at window %d is not a near-tie" % f
-    return bad.size
-
-
 def test_vgg16_cifar_stack_end_to_end():
+    """The stack with nonzero biases at a small batch, end to end from the
+    seeded inputs (each side taking its own decisions; see
+    test_gpu_full_size.independent_check)."""
+    from tests.test_gpu_full_size import independent_check
     n, hw = 2, 32
     print_case("vgg16_stack", n=n, hw=hw)
     layers = configs.conv_layers(configs.VGG16, 3, hw)
@@ -153,77 +38,8 @@ def test_vgg16_cifar_stack_end_to_end():
     st.step()
     torch.cuda.synchronize()
     pools = [L.pool_after for L in layers]
-    f, b = OS.vgg_step(x, wts, bs, pools, dy_top)
-    flips = 0
-    for L in layers:
-        i = L.index
-        if L.pool_after:
-            z = f["Z"][i]
-            assert rel_l2(to_host(st.Z[i]), z) <= TOL["f32"], "Z%d" % i
-            eps = 1e-5 * np.sqrt(np.mean(z * z))
-            flips += _near_ties(z, f["idx"][i], st.idx[i].cpu().numpy(), eps)
-        assert rel_l2(to_host(st.A[i + 1]), f["A"][i + 1]) <= TOL["f32"], "A%d" % (i + 1)
-    if flips == 0:
-        # Identical ReLU / pool decisions: every gradient meets the bound.
-        for L in layers:
-            i = L.index
-            assert rel_l2(to_host(st.grad_at_conv_output(i)), b["dZ"][i]) <= TOL["f32"], "dZ%d" % i
-            assert rel_l2(to_host(st.dW[i]), b["dW"][i]) <= TOL["f32"], "dW%d" % i
-            assert rel_l2(to_host(st.db[i]), b["db"][i]) <= TOL["f32"], "db%d" % i
-        assert rel_l2(to_host(st.gA[0]), b["dX"]) <= TOL["f32"]
-    else:
-        pytest.fail("%d certified near-tie pool decisions differ; choose another seed" % flips)
-
-
-def test_vgg16_stack_bf16_end_to_end():
-    """The bf16 stack against the oracle that rounds to bf16 wherever the GPU
-    path stores a tensor (activations, pool outputs, activation gradients).
-
-    Forward: every tensor within the bf16 bound; pool codes may differ only at
-    certified near-ties.  Such ties are common in bf16: the two sides round
-    sums that differ in their last fp32 bits, so a few windows in a thousand
-    hold two maxima that are equal on one side only.  Each such window sends
-    its gradient to another pixel, which moves the gradients of every layer
-    below by ~0.1-0.2 in relative L2 (measured), so the backward is held to the
-    bf16 bound only above the deepest pool with a differing code, and below it
-    to a gross-error bound that a wrong sign, index or transposition (relative
-    error >= 1) fails.  Per-pass bf16 parity with identical inputs is tested
-    layer by layer at full size."""
-    n, hw = 2, 32
-    print_case("vgg16_stack_bf16", n=n, hw=hw)
-    layers = configs.conv_layers(configs.VGG16, 3, hw)
-    x, wts, bs = _vgg_inputs(n, hw, 15, layers)
-    dy_top = synth.normal((n, 512, 1, 1), 15, synth.TID.DY_TOP)
-    # The stack's inputs as the GPU holds them (bf16 values).
-    x = O.round_bf16(x)
-    wts = [O.round_bf16(w) for w in wts]
-    dy_top = O.round_bf16(dy_top)
-    st = ConvStack(configs.VGG16, n, 3, hw, "bf16")
-    st.load_inputs(x, wts, bs, dy_top)
-    st.step()
-    torch.cuda.synchronize()
-    pools = [L.pool_after for L in layers]
-    f, b = OS.vgg_step(x, wts, bs, pools, dy_top, bf16=True)
-    tol = TOL["bf16"]
-    deepest_flip = -1
-    for L in layers:
-        i = L.index
-        if L.pool_after:
-            z = f["Z"][i]
-            assert rel_l2(to_host(st.Z[i]), z) <= tol, "Z%d" % i
-            # Differing codes must be near-ties: within two bf16 steps.
-            eps = 2.0 ** -6 * np.max(np.abs(z))
-            if _near_ties(z, f["idx"][i], st.idx[i].cpu().numpy(), eps):
-                deepest_flip = i
-        assert rel_l2(to_host(st.A[i + 1]), f["A"][i + 1]) <= tol, "A%d" % (i + 1)
-    for L in layers:
-        i = L.index
-        bound = tol if i > deepest_flip else 0.5
-        assert rel_l2(to_host(st.grad_at_conv_output(i)), b["dZ"][i]) <= bound, "dZ%d" % i
-        assert rel_l2(to_host(st.dW[i]), b["dW"][i]) <= bound, "dW%d" % i
-        assert rel_l2(to_host(st.db[i]), b["db"][i]) <= bound, "db%d" % i
-    bound = tol if deepest_flip < 0 else 0.5
-    assert rel_l2(to_host(st.gA[0]), b["dX"]) <= bound
+    f, b = OS.vgg_step(x, wts, bs, pools, dy_top, store="f32")
+    print(independent_check(st, f, b, "f32", 1e-5))
 
 
 def test_vgg16_imagenet_bf16_stack_full_size_properties():

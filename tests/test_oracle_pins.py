@@ -364,3 +364,35 @@ def test_bf16_stack_rounds_at_storage_points():
     f, b = OS.vgg_step(x, ws, bs, pools, dy, bf16=True)
     for a in f["A"][1:] + list(f["Z"].values()) + [b["dX"]] + list(b["dZ"].values()):
         np.testing.assert_array_equal(a, O.round_bf16(a))
+
+
+def test_round_f32_matches_torch_and_halfway_cases():
+    a = rng.standard_normal(1000) * 10.0 ** rng.integers(-30, 30, 1000)
+    np.testing.assert_array_equal(O.round_f32(a), torch.tensor(a).float().double().numpy())
+    u = 2.0 ** -24                                   # half an ulp of 1 in float32
+    half = np.array([1 + u, 1 + 3 * u, -(1 + u), 1 + u * 1.5])
+    np.testing.assert_array_equal(O.round_f32(half), [1.0, 1 + 4 * u, -1.0, 1 + 2 * u])
+
+
+@pytest.mark.parametrize("store", ["f32", "bf16"])
+def test_stack_chain_rounds_at_storage_points(store):
+    """The storage-rounded chain: every stored activation and activation
+    gradient is representable in the storage type, and each stored tensor
+    is the rounding of the exact layer function applied to the stored
+    tensors before it (one layer checked by hand here)."""
+    rnd = O.round_f32 if store == "f32" else O.round_bf16
+    sched = [(3, 4, False), (4, 4, True)]
+    x = rnd(rng.standard_normal((2, 3, 4, 4)))
+    ws = [rnd(rng.standard_normal((k, c, 3, 3))) for c, k, _ in sched]
+    bs = [np.zeros(k) for _, k, _ in sched]
+    pools = [p for *_, p in sched]
+    dy = rnd(rng.standard_normal((2, 4, 2, 2)))
+    f, b = OS.vgg_step(x, ws, bs, pools, dy, store=store)
+    for a in f["A"][1:] + list(f["Z"].values()) + [b["dX"]] + list(b["dZ"].values()):
+        np.testing.assert_array_equal(a, rnd(a))
+    np.testing.assert_array_equal(f["A"][1], rnd(np.maximum(
+        F.conv2d(_t(x), _t(ws[0]), padding=1).numpy(), 0)))
+    if store == "f32":
+        f64, b64 = OS.vgg_step(x, ws, bs, pools, dy)
+        for l in range(2):
+            np.testing.assert_allclose(b["dW"][l], b64["dW"][l], rtol=1e-5, atol=1e-6)
