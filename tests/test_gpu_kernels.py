@@ -379,7 +379,11 @@ def test_workspace_too_small_is_reported():
 
 
 # -------------------------------------------------------------- FC shard --
-FC_SHAPES = [(512, 4096, 1024), (37, 70, 50), (130, 200, 257), (1, 1, 1), (64, 33, 129)]
+# The FC workloads' shapes (hybrid step: 512 gathered rows; group training
+# step: 128 rows, FC 4096 -> 512 and 1024 -> 5 shards), ragged shapes, and a
+# tall reduction whose weight gradient is split (bias gradient summed apart).
+FC_SHAPES = [(512, 4096, 1024), (512, 512, 1024), (128, 4096, 512), (128, 1024, 5),
+             (37, 70, 50), (130, 200, 257), (1, 1, 1), (64, 33, 129), (4096, 64, 64)]
 
 
 def _fc_inputs(m, kin, ns, seed):
@@ -437,10 +441,11 @@ def test_fc_bwd(shape, masked, dtype):
     assert rel_l2(to_host(db), rdb) <= TOL["f32"]
 
 
-def test_fc_bwd_accumulates_over_modulo_iterations():
+@pytest.mark.parametrize("m,kin,ns,K", [(512, 300, 96, 4), (16384, 64, 64, 4)])
+def test_fc_bwd_accumulates_over_modulo_iterations(m, kin, ns, K):
     """K calls with accumulate=1 on the K row blocks equal one call on all
-    rows (the FC shard's gradient summed over the modulo iterations)."""
-    m, kin, ns, K = 512, 300, 96, 4
+    rows (the FC shard's gradient summed over the modulo iterations); the
+    second shape splits the weight-gradient product."""
     x, w, _, dy, _ = _fc_inputs(m, kin, ns, 23)
     blk = m // K
     d = sb.fc_desc(blk, kin, ns)
