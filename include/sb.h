@@ -31,7 +31,8 @@
  *    returns SB_ERR_HIP.  Faults during execution surface, as in HIP, at
  *    the caller's next synchronisation.
  *  * Outputs must not overlap inputs (checked by address range).
- *  * Layouts: activations NCHW row-major; conv weights KCRS
+ *  * Layouts: activations NCHW row-major, or channel-blocked NCHW8C
+ *    (sb_layout) for the conv and pooling calls; conv weights KCRS
  *    ([out][in][3][3]); FC input X [M][Kin] and shard weights
  *    W_shard [Kin][Ns] row-major.  Element strides are in elements.
  *  * dtype SB_F32: every tensor fp32.  SB_BF16: activations, activation
@@ -60,6 +61,13 @@ typedef enum {
 
 typedef enum { SB_F32 = 0, SB_BF16 = 1 } sb_dtype;
 
+/* Activation layouts.  SB_NCHW: [n][c][h][w].  SB_NCHW8C (channel-blocked):
+ * [n][c/8][h][w][c%8], i.e. element (n, c, h, w) at
+ * ((n * C/8 + c/8) * H + h) * W + w) * 8 + c % 8, for channel counts that
+ * are multiples of 8; the 8 channels of a pixel are one 16-byte bf16 piece.
+ * Filters are KCRS in both. */
+typedef enum { SB_NCHW = 0, SB_NCHW8C = 1 } sb_layout;
+
 /* flags */
 #define SB_FUSE_RELU 1u       /* apply ReLU to the output (conv fwd, FC fwd) */
 #define SB_PACKED_FILTERS 2u  /* conv fwd / data gradient: `w` holds filters
@@ -76,9 +84,13 @@ int sb_version(void);
  * stage multiplies successive input patches with square filters; the
  * operation is the cross-correlation used by deep-learning frameworks).
  *
- *   x  [n][c][h][w]    input activations
+ *   x  [n][c][h][w]    input activations (or channel-blocked, see layout)
  *   w  [k][c][3][3]    filters
- *   y  [n][k][h][w]    output
+ *   y  [n][k][h][w]    output (same layout as x)
+ * The layout applies to every activation tensor of a call (x, y, dy, dx,
+ * the ReLU mask).  SB_NCHW8C is provided for SB_BF16 with c and k multiples
+ * of 8 and w >= 8 (the bf16 MFMA kernels); other combinations return
+ * SB_ERR_UNSUPPORTED.
  * ---------------------------------------------------------------------- */
 typedef struct {
     int n, c, h, w;       /* batch, input channels, height, width (all > 0) */
@@ -86,6 +98,7 @@ typedef struct {
     int dtype;            /* sb_dtype                                       */
     unsigned flags;       /* SB_FUSE_RELU (forward only), SB_PACKED_FILTERS
                              (forward and data gradient)                    */
+    int layout;           /* sb_layout of the activations                   */
 } sb_conv3x3_desc;
 
 enum { SB_PASS_FWD = 0, SB_PASS_BWD_DATA = 1, SB_PASS_BWD_WEIGHT = 2 };
@@ -207,11 +220,14 @@ size_t sb_conv3x3_plan_string(const sb_conv3x3_desc *desc, int pass, char *buf,
  *                          2-6 zero.
  * Backward: dx (un-pooled shape) is zero except dx[window position] = dy
  * for windows whose bit 7 is clear.  dx is fully overwritten.
+ * layout (sb_layout) applies to x, y, dy, dx and idx alike (idx one byte per
+ * element of y); SB_NCHW8C needs c a multiple of 8 (SB_ERR_INVALID_ARG
+ * otherwise).
  * ---------------------------------------------------------------------- */
-sb_status sb_relu_maxpool_fwd(int n, int c, int h, int w, int dtype,
+sb_status sb_relu_maxpool_fwd(int n, int c, int h, int w, int dtype, int layout,
                               const void *x, void *y, uint8_t *idx,
                               void *stream);
-sb_status sb_relu_maxpool_bwd(int n, int c, int h, int w, int dtype,
+sb_status sb_relu_maxpool_bwd(int n, int c, int h, int w, int dtype, int layout,
                               const void *dy, const uint8_t *idx, void *dx,
                               void *stream);
 

@@ -23,6 +23,17 @@ int conv_igemm_describe(bool dgrad, int dtype, int N, int Cin, int H, int W, int
 int conv_wgrad_describe(int dtype, int N, int C, int H, int W, int K, char* buf, size_t len);
 sb_status conv_wgrad(int dtype, int N, int C, int H, int W, int K, const void* x, const void* dy,
                      float* dw, float* db, void* ws, size_t ws_bytes, hipStream_t st);
+// Channel-blocked bf16 (SB_NCHW8C).
+bool conv_bf16_takes(int N, int Cin, int H, int W, int Cout);
+int conv_bf16c8_describe(bool dgrad, int N, int Cin, int H, int W, int Cout, char* buf,
+                         size_t len);
+sb_status conv_bf16c8(bool dgrad, int N, int Cin, int H, int W, int Cout, const void* in,
+                      const void* wt, const float* bias, const void* mask, void* out, void* ws,
+                      size_t ws_bytes, int relu, bool prepacked, hipStream_t st);
+bool conv_wgrad_c8_takes(int N, int C, int H, int W, int K);
+int conv_wgrad_c8_describe(int N, int C, int H, int W, int K, char* buf, size_t len);
+sb_status conv_wgrad_c8(int N, int C, int H, int W, int K, const void* x, const void* dy,
+                        float* dw, float* db, void* ws, size_t ws_bytes, hipStream_t st);
 }  // namespace sbh
 
 extern "C" const char* sb_status_string(sb_status s) {
@@ -45,6 +56,18 @@ static sb_status conv_check(const sb_conv3x3_desc* d, int pass) {
   if (d->flags & ~(SB_FUSE_RELU | SB_PACKED_FILTERS)) return SB_ERR_INVALID_ARG;
   if (pass != SB_PASS_FWD && (d->flags & SB_FUSE_RELU)) return SB_ERR_INVALID_ARG;
   if (pass == SB_PASS_BWD_WEIGHT && d->flags) return SB_ERR_INVALID_ARG;
+  if (d->layout != SB_NCHW && d->layout != SB_NCHW8C) return SB_ERR_INVALID_ARG;
+  if (d->layout == SB_NCHW8C) {
+    // Channel-blocked tensors: whole 8-channel blocks, on the bf16 MFMA
+    // kernels (images at least 8 wide).
+    if (d->c % 8 || d->k % 8) return SB_ERR_INVALID_ARG;
+    if (d->dtype != SB_BF16) return SB_ERR_UNSUPPORTED;
+    const bool ok = pass == SB_PASS_BWD_WEIGHT
+                        ? sbh::conv_wgrad_c8_takes(d->n, d->c, d->h, d->w, d->k)
+                    : pass == SB_PASS_FWD ? sbh::conv_bf16_takes(d->n, d->c, d->h, d->w, d->k)
+                                          : sbh::conv_bf16_takes(d->n, d->k, d->h, d->w, d->c);
+    if (!ok) return SB_ERR_UNSUPPORTED;
+  }
   // Kernels index weights and activations with 32-bit ints.
   if ((int64_t)d->k * d->c * 9 >= (1ll << 31)) return SB_ERR_UNSUPPORTED;
   if ((int64_t)d->n * d->c * d->h * d->w >= (1ll << 31)) return SB_ERR_UNSUPPORTED;
@@ -166,6 +189,10 @@ extern "C" sb_status sb_conv3x3_fwd(const sb_conv3x3_desc* d, const void* x, con
                sbh::overlaps(ws, need, w, wb) ||
                sbh::overlaps(ws, need, bias, bias ? d->k * sizeof(float) : 0)))
     return SB_ERR_INVALID_ARG;
+  if (d->layout == SB_NCHW8C)
+    return sbh::conv_bf16c8(false, d->n, d->c, d->h, d->w, d->k, x, w, bias, nullptr, y, ws,
+                            ws_bytes, (d->flags & SB_FUSE_RELU) ? 1 : 0, pk,
+                            sbh::stream_of(stream));
   return sbh::conv_igemm(false, d->dtype, d->n, d->c, d->h, d->w, d->k, x, w, bias, nullptr, y,
                          ws, ws_bytes, (d->flags & SB_FUSE_RELU) ? 1 : 0, pk,
                          sbh::stream_of(stream));
@@ -190,6 +217,9 @@ extern "C" sb_status sb_conv3x3_bwd_data(const sb_conv3x3_desc* d, const void* d
                sbh::overlaps(ws, need, w, wb) ||
                sbh::overlaps(ws, need, mask, mask ? dxb : 0)))
     return SB_ERR_INVALID_ARG;
+  if (d->layout == SB_NCHW8C)
+    return sbh::conv_bf16c8(true, d->n, d->k, d->h, d->w, d->c, dy, w, nullptr, mask, dx, ws,
+                            ws_bytes, 0, pk, sbh::stream_of(stream));
   return sbh::conv_igemm(true, d->dtype, d->n, d->k, d->h, d->w, d->c, dy, w, nullptr, mask, dx,
                          ws, ws_bytes, 0, pk, sbh::stream_of(stream));
 }
@@ -211,6 +241,9 @@ extern "C" sb_status sb_conv3x3_bwd_weight(const sb_conv3x3_desc* d, const void*
   if (need && (sbh::overlaps(ws, need, dw, dwb) || sbh::overlaps(ws, need, db, dbb) ||
                sbh::overlaps(ws, need, x, xb) || sbh::overlaps(ws, need, dy, dyb)))
     return SB_ERR_INVALID_ARG;
+  if (d->layout == SB_NCHW8C)
+    return sbh::conv_wgrad_c8(d->n, d->c, d->h, d->w, d->k, x, dy, dw, db, ws, ws_bytes,
+                              sbh::stream_of(stream));
   return sbh::conv_wgrad(d->dtype, d->n, d->c, d->h, d->w, d->k, x, dy, dw, db, ws, ws_bytes,
                          sbh::stream_of(stream));
 }
@@ -266,6 +299,9 @@ extern "C" sb_status sb_conv3x3_bwd_weight_noalloc(const sb_conv3x3_desc* d, con
   if (need && (sbh::overlaps(ws, need, dw, dwb) || sbh::overlaps(ws, need, db, dbb) ||
                sbh::overlaps(ws, need, x, xb) || sbh::overlaps(ws, need, dy, dyb)))
     return SB_ERR_INVALID_ARG;
+  if (d->layout == SB_NCHW8C)
+    return sbh::conv_wgrad_c8(d->n, d->c, d->h, d->w, d->k, x, dy, dw, db, ws, kScratchBytes,
+                              sbh::stream_of(stream));
   return sbh::conv_wgrad(d->dtype, d->n, d->c, d->h, d->w, d->k, x, dy, dw, db, ws,
                          kScratchBytes, sbh::stream_of(stream));
 }
@@ -275,6 +311,15 @@ extern "C" size_t sb_conv3x3_plan_string(const sb_conv3x3_desc* d, int pass, cha
   if (pass < SB_PASS_FWD || pass > SB_PASS_BWD_WEIGHT) return 0;
   if (conv_check(d, pass) != SB_OK) return 0;
   int r;
+  if (d->layout == SB_NCHW8C) {
+    if (pass == SB_PASS_FWD)
+      r = sbh::conv_bf16c8_describe(false, d->n, d->c, d->h, d->w, d->k, buf, len);
+    else if (pass == SB_PASS_BWD_DATA)
+      r = sbh::conv_bf16c8_describe(true, d->n, d->k, d->h, d->w, d->c, buf, len);
+    else
+      r = sbh::conv_wgrad_c8_describe(d->n, d->c, d->h, d->w, d->k, buf, len);
+    return r < 0 ? 0 : (size_t)r + 1;
+  }
   switch (pass) {
     case SB_PASS_FWD:
       r = sbh::conv_igemm_describe(false, d->dtype, d->n, d->c, d->h, d->w, d->k, buf, len);

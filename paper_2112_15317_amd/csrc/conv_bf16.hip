@@ -26,6 +26,7 @@
 
 #include <algorithm>
 #include <cstdio>
+#include <mutex>
 
 namespace sb {
 
@@ -356,6 +357,255 @@ __global__ __launch_bounds__(256, 2) void conv3x3_igemm_bf16(ConvArgs a) {
   }
 }
 
+// ------------------------------------------------------ channel-blocked --
+// The same contraction on channel-blocked tensors (SB_NCHW8C: element
+// (n, c, h, w) at ((n * C/8 + c/8) * H + h) * W + w) * 8 + c % 8, C a
+// multiple of 8).  Eight consecutive channels of a pixel are one 16-byte
+// piece, which is exactly what an MFMA lane supplies, so the input halo is
+// staged as whole pieces: one 16-byte load and one 16-byte LDS store per
+// (channel block, halo pixel), no transposition.  The compute is the NCHW
+// kernel's.  The output tile goes out through LDS as [pixel][channel] rows
+// and leaves as 16-byte pieces (one pixel's 8 channels), the ReLU mask read
+// in the same pieces; split partials are written in the same channel-blocked
+// order (four consecutive channels of a lane are one 16-byte store).
+// Single-buffer LDS of the channel-blocked kernel: the chunk buffer, or the
+// output tile staged as [pixel][BN + 8 channels], whichever is larger.
+template <class T>
+__host__ __device__ constexpr size_t c8_one_buf_lds_bytes() {
+  return (T::LDS_BUF > T::BM * (T::BN + 8) ? T::LDS_BUF : T::BM * (T::BN + 8)) * sizeof(u16);
+}
+
+template <class T, bool DGRAD, bool ONE = false>
+__global__ __launch_bounds__(256, 2) void conv3x3_c8_bf16(ConvArgs a) {
+  extern __shared__ u16 ldsb[];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int lc = lane & 31, lh = lane >> 5;
+
+  int bt = blockIdx.x;
+  const int tx = bt % a.tiles_w; bt /= a.tiles_w;
+  const int ty = bt % a.tiles_h;
+  const int tn = bt / a.tiles_h;
+  const int n0 = tn * T::IMGS, h0 = ty * T::TH, w0 = tx * T::TW;
+  const int co0 = blockIdx.y * T::BN;
+  const int kc0 = blockIdx.z * a.chunks_per_split;
+  const int kc1 = min(a.nchunks, kc0 + a.chunks_per_split);
+  const int HWs = a.H * a.W;
+  const int CB = a.Cin / 8;                          // input channel blocks
+
+  // Halo staging: piece u = (channel block cb of the chunk, halo pixel hp),
+  // halo pixels fastest.  Element offset of the piece for chunk 0 (from
+  // image n0), -1 outside the image; a chunk adds 2 blocks of H*W pixels.
+  constexpr int NP = 2 * T::PLANE;
+  constexpr int XI = (NP + 255) / 256;
+  int x_off[XI], x_cb[XI];
+#pragma unroll
+  for (int i = 0; i < XI; ++i) {
+    const int u = tid + 256 * i;
+    const int cb = u / T::PLANE, hp = u % T::PLANE;
+    const int row = hp / T::HW, hx = hp % T::HW;
+    const int img = row / T::HH, hy = row % T::HH;
+    const int h = h0 + hy - 1, w = w0 + hx - 1;
+    const bool ok = u < NP && n0 + img < a.N && (unsigned)h < (unsigned)a.H &&
+                    (unsigned)w < (unsigned)a.W;
+    x_off[i] = ok ? ((img * CB + cb) * HWs + h * a.W + w) * 8 : -1;
+    x_cb[i] = u < NP ? cb : 1 << 20;
+  }
+  int b_off[T::MB];
+#pragma unroll
+  for (int mb = 0; mb < T::MB; ++mb) {
+    const int p = wave * T::WP + mb * 32 + lc;
+    b_off[mb] = (lh * T::PLANE + T::hp(T::img_of(p), T::yy_of(p), T::xx_of(p))) * 8;
+  }
+
+  f16 acc[T::NB][T::MB];
+#pragma unroll
+  for (int i = 0; i < T::NB; ++i)
+#pragma unroll
+    for (int j = 0; j < T::MB; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+  const rsrc_t xr = input_rsrc<u16>(a, n0, T::IMGS);
+  const rsrc_t wr = packed_rsrc<u16, T::WTS>(a, blockIdx.y);
+  s8 rx[XI];
+  s8 rw[T::WTS_I];
+  auto gload = [&](int kc) {
+#pragma unroll
+    for (int i = 0; i < XI; ++i) {
+      const bool ok = x_off[i] >= 0 && 2 * kc + x_cb[i] < CB;
+      const uint32_t off = ok ? (uint32_t)(x_off[i] + 2 * kc * HWs * 8) * 2u : kOOB;
+      rx[i] = __builtin_bit_cast(s8, __builtin_amdgcn_raw_buffer_load_b128(xr, (int)off, 0, 0));
+    }
+#pragma unroll
+    for (int i = 0; i < T::WTS_I; ++i) {
+      const int g = tid + 256 * i;
+      const uint32_t off = g < T::WTS_V ? (uint32_t)(kc * T::WTS + g * 8) * 2u : kOOB;
+      rw[i] = __builtin_bit_cast(s8, __builtin_amdgcn_raw_buffer_load_b128(wr, (int)off, 0, 0));
+    }
+  };
+  auto lstore = [&](int buf) {
+    u16* X = ldsb + buf * T::LDS_BUF;
+    u16* Wl = X + T::LDS_X;
+#pragma unroll
+    for (int i = 0; i < XI; ++i) {
+      const int u = tid + 256 * i;
+      if (u < NP) *reinterpret_cast<s8*>(X + u * 8) = rx[i];      // = [cb][halo pixel][8]
+    }
+#pragma unroll
+    for (int i = 0; i < T::WTS_I; ++i) {
+      const int g = tid + 256 * i;
+      if (g < T::WTS_V) *reinterpret_cast<s8*>(Wl + g * 8) = rw[i];
+    }
+  };
+  auto compute = [&](int buf) {
+    const u16* X = ldsb + buf * T::LDS_BUF;
+    const u16* Wl = X + T::LDS_X;
+#pragma unroll
+    for (int t = 0; t < 9; ++t) {
+      const int toff = T::hp(0, t / 3, t % 3) * 8;
+      s8 fa[T::NB], fb[T::MB];
+#pragma unroll
+      for (int nb = 0; nb < T::NB; ++nb)
+        fa[nb] = *reinterpret_cast<const s8*>(Wl + ((t * 2 + lh) * T::BN + nb * 32 + lc) * 8);
+#pragma unroll
+      for (int mb = 0; mb < T::MB; ++mb)
+        fb[mb] = *reinterpret_cast<const s8*>(X + b_off[mb] + toff);
+#pragma unroll
+      for (int nb = 0; nb < T::NB; ++nb)
+#pragma unroll
+        for (int mb = 0; mb < T::MB; ++mb)
+          acc[nb][mb] = mfma32x32x16bf16(fa[nb], fb[mb], acc[nb][mb]);
+    }
+  };
+
+  const int nk = kc1 - kc0;
+  if constexpr (ONE) {
+    if (nk > 0) {
+      gload(kc0);
+      lstore(0);
+    }
+    __syncthreads();
+    for (int t = 0; t < nk; ++t) {
+      if (t + 1 < nk) gload(kc0 + t + 1);
+      compute(0);
+      __syncthreads();
+      if (t + 1 < nk) {
+        lstore(0);
+        __syncthreads();
+      }
+    }
+  } else {
+    if (nk > 0) {
+      gload(kc0);
+      lstore(0);
+      if (nk > 1) gload(kc0 + 1);
+    }
+    __syncthreads();
+    for (int t = 0; t < nk; ++t) {
+      const int buf = t & 1;
+      if (t + 1 < nk) lstore(buf ^ 1);
+      if (t + 2 < nk) gload(kc0 + t + 2);
+      compute(buf);
+      __syncthreads();
+    }
+  }
+
+  // acc[nb][mb] element v: output channel co0 + nb*32 + 8*(v/4) + 4*lh +
+  // v%4 of pixel wave*WP + mb*32 + lc; the four elements v = 4q .. 4q+3 are
+  // four consecutive channels of one 8-channel block.
+  const int KB = a.Cout / 8;
+  if (a.splits > 1) {
+    float* mine = a.part + (size_t)blockIdx.z * a.N * a.Cout * HWs;
+#pragma unroll
+    for (int mb = 0; mb < T::MB; ++mb) {
+      const int p = wave * T::WP + mb * 32 + lc;
+      const int img = T::img_of(p), h = h0 + T::yy_of(p), w = w0 + T::xx_of(p);
+      if (n0 + img >= a.N || h >= a.H || w >= a.W) continue;
+#pragma unroll
+      for (int nb = 0; nb < T::NB; ++nb)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int co = co0 + nb * 32 + 8 * q;          // block start
+          if (co >= a.Cout) continue;
+          const size_t o = (((size_t)(n0 + img) * KB + co / 8) * HWs + h * a.W + w) * 8 + 4 * lh;
+          *reinterpret_cast<f4*>(mine + o) =
+              f4{acc[nb][mb][4 * q], acc[nb][mb][4 * q + 1], acc[nb][mb][4 * q + 2],
+                 acc[nb][mb][4 * q + 3]};
+        }
+    }
+    return;
+  }
+  // Unsplit: bias and ReLU, rounded to bf16, staged as [pixel][channel]
+  // (row pitch BN + 8) and written as 16-byte pieces; piece q = (channel
+  // block q / BM, pixel q % BM), so consecutive threads write consecutive
+  // pixels of one block.
+  constexpr int EP = T::BN + 8;
+  static_assert(T::BM * EP * sizeof(u16) <= (ONE ? c8_one_buf_lds_bytes<T>() : T::LDS_BYTES),
+                "output tile fits the staging LDS");
+  u16* E = ldsb;
+#pragma unroll
+  for (int nb = 0; nb < T::NB; ++nb)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int cl = nb * 32 + 8 * q + 4 * lh;           // channel within the tile
+      float bv[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        bv[e] = a.bias && co0 + cl + e < a.Cout ? a.bias[co0 + cl + e] : 0.f;
+#pragma unroll
+      for (int mb = 0; mb < T::MB; ++mb) {
+        float r[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          r[e] = acc[nb][mb][4 * q + e] + bv[e];
+          if (a.relu && !(r[e] > 0.f)) r[e] = 0.f;
+        }
+        typedef uint32_t u2 __attribute__((ext_vector_type(2)));
+        *reinterpret_cast<u2*>(E + (wave * T::WP + mb * 32 + lc) * EP + cl) =
+            u2{f32x2_to_bf16x2(r[0], r[1]), f32x2_to_bf16x2(r[2], r[3])};
+      }
+    }
+  __syncthreads();
+  constexpr int NPC = T::BM * (T::BN / 8);               // pieces per block
+  constexpr int EPI = NPC / 256;
+  static_assert(NPC % 256 == 0, "whole rounds of pieces");
+  int goff[EPI];                                          // element offset, -1 outside
+#pragma unroll
+  for (int i = 0; i < EPI; ++i) {
+    const int q = tid + 256 * i;
+    const int p = q % T::BM, kb = q / T::BM;
+    const int img = T::img_of(p), h = h0 + T::yy_of(p), w = w0 + T::xx_of(p);
+    const int co = co0 + kb * 8;
+    goff[i] = co < a.Cout && n0 + img < a.N && h < a.H && w < a.W
+                  ? (((n0 + img) * KB + co / 8) * HWs + h * a.W + w) * 8 : -1;
+  }
+  s8 mk[EPI];
+  if (a.mask) {
+    const rsrc_t mr = make_rsrc(a.mask, (uint32_t)((size_t)a.N * a.Cout * HWs * 2));
+#pragma unroll
+    for (int i = 0; i < EPI; ++i) {
+      const uint32_t off = goff[i] >= 0 ? (uint32_t)goff[i] * 2u : kOOB;
+      mk[i] = __builtin_bit_cast(s8, __builtin_amdgcn_raw_buffer_load_b128(mr, (int)off, 0, 0));
+    }
+  }
+  u16* out = (u16*)a.out;
+#pragma unroll
+  for (int i = 0; i < EPI; ++i) {
+    if (goff[i] < 0) continue;
+    const int q = tid + 256 * i;
+    s8 o = *reinterpret_cast<const s8*>(E + (q % T::BM) * EP + (q / T::BM) * 8);
+    if (a.mask) {
+      // A bf16 mask value m keeps the output iff m > 0: bits 0x0001..0x7f80.
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const uint32_t m16 = (uint16_t)mk[i][e];
+        if (!(((m16 - 1u) & 0xffffu) < 0x7f80u)) o[e] = 0;
+      }
+    }
+    *reinterpret_cast<s8*>(out + goff[i]) = o;
+  }
+}
+
 // ---------------------------------------------------------------- host --
 using BTileW32 = BTile<8, 32, 1>;
 using BTileW16 = BTile<16, 16, 1>;
@@ -516,6 +766,46 @@ static void bf16_dispatch(int v, const BPlan& p, const ConvArgs& a, bool pack, h
   }
 }
 
+template <class T, bool DGRAD>
+static void c8_launch(const BPlan& p, const ConvArgs& a, bool pack, hipStream_t st) {
+  constexpr bool can_one = T::BM == 256;
+  const bool one = can_one && p.cps <= 8;
+  static std::once_flag once;
+  std::call_once(once, [] {
+    (void)hipFuncSetAttribute((const void*)conv3x3_c8_bf16<T, DGRAD>,
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)T::LDS_BYTES);
+    if constexpr (can_one)
+      (void)hipFuncSetAttribute((const void*)conv3x3_c8_bf16<T, DGRAD, true>,
+                                hipFuncAttributeMaxDynamicSharedMemorySize,
+                                (int)c8_one_buf_lds_bytes<T>());
+  });
+  if (pack) bf16_pack<DGRAD>(p, a.wt, (void*)a.wpk, a.Cin, a.Cout, st);
+  dim3 grid(p.grid_x, p.co_tiles, p.splits);
+  ConvArgs k = a;
+  if (p.splits > 1) { k.bias = nullptr; k.mask = nullptr; k.relu = 0; }
+  if (can_one && one)
+    conv3x3_c8_bf16<T, DGRAD, true><<<grid, 256, c8_one_buf_lds_bytes<T>(), st>>>(k);
+  else
+    conv3x3_c8_bf16<T, DGRAD><<<grid, 256, T::LDS_BYTES, st>>>(k);
+  if (p.splits > 1) {
+    size_t total = (size_t)a.N * a.Cout * a.H * a.W;
+    launch_splitk_reduce<u16, true>(a.part, p.splits, total, a.Cout, a.H * a.W, a.bias,
+                                    a.relu, (const u16*)a.mask, (u16*)a.out, st);
+  }
+}
+
+template <bool DGRAD>
+static void c8_dispatch(const BPlan& p, const ConvArgs& a, bool pack, hipStream_t st) {
+  switch (p.tile) {
+    case 0: c8_launch<BTileW32, DGRAD>(p, a, pack, st); break;
+    case 1: c8_launch<BTileW16, DGRAD>(p, a, pack, st); break;
+    case 2: c8_launch<BTileW8, DGRAD>(p, a, pack, st); break;
+    case 3: c8_launch<BTileW32L, DGRAD>(p, a, pack, st); break;
+    case 4: c8_launch<BTileW64L, DGRAD>(p, a, pack, st); break;
+    default: c8_launch<BTileW32N, DGRAD>(p, a, pack, st); break;
+  }
+}
+
 }  // namespace sb
 
 namespace sbh {
@@ -588,6 +878,42 @@ sb_status conv_bf16(bool dgrad, int N, int Cin, int H, int W, int Cout, const vo
   a.nchunks = p.nchunks; a.chunks_per_split = p.cps; a.splits = p.splits; a.relu = relu;
   if (dgrad) sb::bf16_dispatch<true>(v, p, a, !prepacked, st);
   else sb::bf16_dispatch<false>(v, p, a, !prepacked, st);
+  return launch_status();
+}
+
+// Channel-blocked bf16 tensors (SB_NCHW8C): the same plans (and filter
+// packing) as the NCHW bf16 path with 16-byte staging.
+int conv_bf16c8_describe(bool dgrad, int N, int Cin, int H, int W, int Cout, char* buf,
+                         size_t len) {
+  sb::BPlan p = sb::bf16_plan(N, Cin, H, W, Cout, true);
+  static const char* kNames[] = {"8, 32, 1", "16, 16, 1", "8, 8, 4", "16, 32, 1", "8, 64, 1",
+                                 "8, 32, 1, 1"};
+  return snprintf(buf, len, "sb::conv3x3_c8_bf16<sb::BTile<%s>, %s> grid=%dx%dx%d",
+                  kNames[p.tile], dgrad ? "true" : "false", p.grid_x, p.co_tiles, p.splits);
+}
+
+sb_status conv_bf16c8(bool dgrad, int N, int Cin, int H, int W, int Cout, const void* in,
+                      const void* wt, const float* bias, const void* mask, void* out, void* ws,
+                      size_t ws_bytes, int relu, bool prepacked, hipStream_t st) {
+  sb::BPlan p = sb::bf16_plan(N, Cin, H, W, Cout, true);
+  if (!p.ok) return SB_ERR_UNSUPPORTED;
+  // Buffer ranges: the whole output (mask) tensor, one block's images of the
+  // input, one tile's packed filters.
+  if ((int64_t)N * std::max(Cin, Cout) * H * W * 2 >= (1ll << 31) ||
+      (int64_t)p.pack_bytes >= (1ll << 31))
+    return SB_ERR_UNSUPPORTED;
+  const size_t part_off = prepacked ? 0 : p.part_off;
+  const size_t need = prepacked ? p.ws_bytes - p.part_off : p.ws_bytes;
+  if (need && (ws == nullptr || ws_bytes < need)) return SB_ERR_WORKSPACE;
+  sb::ConvArgs a{};
+  a.in = in; a.wt = wt; a.bias = bias; a.mask = mask; a.out = out;
+  a.wpk = prepacked ? wt : ws;
+  a.part = p.splits > 1 ? (float*)((char*)ws + part_off) : nullptr;
+  a.N = N; a.Cin = Cin; a.H = H; a.W = W; a.Cout = Cout;
+  a.tiles_w = p.tiles_w; a.tiles_h = p.tiles_h;
+  a.nchunks = p.nchunks; a.chunks_per_split = p.cps; a.splits = p.splits; a.relu = relu;
+  if (dgrad) sb::c8_dispatch<true>(p, a, !prepacked, st);
+  else sb::c8_dispatch<false>(p, a, !prepacked, st);
   return launch_status();
 }
 

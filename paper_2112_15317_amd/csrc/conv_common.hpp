@@ -265,8 +265,15 @@ __device__ __forceinline__ rsrc_t packed_rsrc(const ConvArgs& a, int ct) {
                    (uint32_t)((size_t)a.nchunks * WTS * sizeof(E)));
 }
 
+// Channel of flat output element i: NCHW, or channel-blocked (C8: blocks
+// of 8 channels innermost per pixel).
+template <bool C8>
+__device__ __forceinline__ int flat_channel(size_t i, int Cout, int HWs) {
+  if (C8) return (int)(((i >> 3) / HWs) % (size_t)(Cout >> 3)) * 8 + (int)(i & 7);
+  return (int)((i / HWs) % Cout);
+}
 // Sum of the split partials in a fixed order, then the epilogue.
-template <class E>
+template <class E, bool C8 = false>
 __global__ __launch_bounds__(256) void conv_splitk_reduce(
     const float* __restrict__ part, int splits, size_t total, int Cout, int HWs,
     const float* __restrict__ bias, int relu, const E* __restrict__ mask,
@@ -276,7 +283,7 @@ __global__ __launch_bounds__(256) void conv_splitk_reduce(
   const size_t i = (size_t)blockIdx.x * 64 + lane;
   float v = SplitSum{part, splits, total, total}(i, wave, lds, lane);
   if (wave != 0 || i >= total) return;
-  if (bias) v += bias[(i / HWs) % Cout];
+  if (bias) v += bias[flat_channel<C8>(i, Cout, HWs)];
   if (relu && !(v > 0.f)) v = 0.f;
   if (mask && !(Elem<E>::load(mask, i) > 0.f)) v = 0.f;
   Elem<E>::store(out, i, v);
@@ -285,7 +292,7 @@ __global__ __launch_bounds__(256) void conv_splitk_reduce(
 // The same for 4 consecutive outputs per thread (total a multiple of 4 and
 // the partials 16-byte aligned): 16-byte partial loads, all splits of a
 // thread's outputs summed in one thread in split order.
-template <class E>
+template <class E, bool C8 = false>
 __global__ __launch_bounds__(256) void conv_splitk_reduce4(
     const float* __restrict__ part, int splits, size_t total, int Cout, int HWs,
     const float* __restrict__ bias, int relu, const E* __restrict__ mask,
@@ -297,7 +304,7 @@ __global__ __launch_bounds__(256) void conv_splitk_reduce4(
   for (int j = 0; j < 4; ++j) {
     const size_t i = i4 + j;
     float r = v[j];
-    if (bias) r += bias[(i / HWs) % Cout];
+    if (bias) r += bias[flat_channel<C8>(i, Cout, HWs)];
     if (relu && !(r > 0.f)) r = 0.f;
     if (mask && !(Elem<E>::load(mask, i) > 0.f)) r = 0.f;
     Elem<E>::store(out, i, r);
@@ -306,15 +313,15 @@ __global__ __launch_bounds__(256) void conv_splitk_reduce4(
 
 // Launches the split reduction of a convolution pass: the 4-wide form when
 // the sizes allow, else one output per lane.
-template <class E>
+template <class E, bool C8 = false>
 inline void launch_splitk_reduce(const float* part, int splits, size_t total, int Cout, int HWs,
                                  const float* bias, int relu, const E* mask, E* out,
                                  hipStream_t st) {
   if (total % 4 == 0 && ((uintptr_t)part & 15) == 0)
-    conv_splitk_reduce4<E><<<(unsigned)((total / 4 + 255) / 256), 256, 0, st>>>(
+    conv_splitk_reduce4<E, C8><<<(unsigned)((total / 4 + 255) / 256), 256, 0, st>>>(
         part, splits, total, Cout, HWs, bias, relu, mask, out);
   else
-    conv_splitk_reduce<E><<<(unsigned)((total + 63) / 64), 256, 0, st>>>(
+    conv_splitk_reduce<E, C8><<<(unsigned)((total + 63) / 64), 256, 0, st>>>(
         part, splits, total, Cout, HWs, bias, relu, mask, out);
 }
 

@@ -44,6 +44,7 @@
 
 #include <algorithm>
 #include <cstdio>
+#include <mutex>
 
 namespace sb {
 
@@ -581,6 +582,115 @@ struct WgBTile {
 
 typedef short s8 __attribute__((ext_vector_type(8)));
 
+// End of a bf16 weight-gradient block (both tile forms): the bias row sums,
+// the two pixel-step halves summed (waves wp = 1 hand their accumulators to
+// the waves wp = 0 of the same (wk, wc) through LDS), and the block's
+// 64 k x (BC c x 9 taps) tile written to dw or to its split's partials.
+template <class T>
+__device__ __forceinline__ void wgrad_bf16_finish(const WgArgs& a, const WgBlock& blk, int k0,
+                                                  int c0, bool do_db, int wk, int wp, int wc,
+                                                  f4 (&acc)[T::MA][9], float (&sbias)[T::MA],
+                                                  u16* ldsw) {
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int kq = lane >> 4, lr = lane & 15;
+  f4 accb[T::MA];
+#pragma unroll
+  for (int m = 0; m < T::MA; ++m) accb[m] = wave_row_sums(sbias[m]);
+
+  // Sum the two step halves: waves wp = 1 hand their accumulators to the
+  // waves wp = 0 of the same (wk, wc) through LDS (lane fastest, so the
+  // stores and loads are conflict-free), in rounds of RA k blocks.
+  {
+    constexpr int RA =                                 // k blocks per round
+        T::MA >= 2 && T::WC * T::WK * 2 * 40 * 64 * 4 <= (int)T::LDS_BYTES ? 2 : 1;
+    constexpr int NF = RA * 10 * 4;                    // floats per lane per round
+    static_assert(T::WC * T::WK * NF * 64 * 4 <= T::LDS_BYTES, "reduction fits the LDS");
+    float* R = reinterpret_cast<float*>(ldsw) + (wk * T::WC + wc) * NF * 64;
+#pragma unroll
+    for (int r0 = 0; r0 < T::MA; r0 += RA) {
+      if (wp == 1) {
+#pragma unroll
+        for (int m = 0; m < RA; ++m) {
+#pragma unroll
+          for (int t = 0; t < 9; ++t)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) R[((m * 10 + t) * 4 + i) * 64 + lane] = acc[r0 + m][t][i];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) R[((m * 10 + 9) * 4 + i) * 64 + lane] = accb[r0 + m][i];
+        }
+      }
+      __syncthreads();
+      if (wp == 0) {
+#pragma unroll
+        for (int m = 0; m < RA; ++m) {
+#pragma unroll
+          for (int t = 0; t < 9; ++t)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) acc[r0 + m][t][i] += R[((m * 10 + t) * 4 + i) * 64 + lane];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) accb[r0 + m][i] += R[((m * 10 + 9) * 4 + i) * 64 + lane];
+        }
+      }
+      __syncthreads();
+    }
+  }
+  // acc[m][t] of the waves wp = 0 holds rows k = k0 + (wk*MA + m)*16 +
+  // 4*kq + i and channel c0 + wc*16 + lr.  The block's 64 k x (BC c x 9
+  // taps) tile goes out through LDS in rounds of 32 rows of BC * 9
+  // consecutive floats (the dw order), written in 16-byte pieces; every
+  // wave takes part in the barriers and the stores.
+  {
+    constexpr int RW = T::BC * 9, RP = RW + 4, ROWS = 32, QPR = RW / 4;
+    static_assert(ROWS * RP * sizeof(float) <= T::LDS_BYTES && RW % 4 == 0, "rows fit the LDS");
+    float* L = reinterpret_cast<float*>(ldsw);
+    const int cw = min(T::BC, a.C - c0) * 9;         // live columns of the tile
+    const size_t wsz = (size_t)a.K * a.C * 9;
+    float* dst = a.splits == 1 ? a.dw : a.part + (size_t)blk.z * (wsz + a.K);
+    const bool vec = (a.C * 9) % 4 == 0 && cw % 4 == 0 &&
+                     (((uintptr_t)dst + (size_t)c0 * 9 * sizeof(float)) & 15) == 0;
+#pragma unroll
+    for (int r0 = 0; r0 < T::BK; r0 += ROWS) {
+      __syncthreads();                                // the LDS is free
+      if (wp == 0) {
+#pragma unroll
+        for (int m = 0; m < T::MA; ++m) {
+          const int row = (wk * T::MA + m) * 16 - r0;
+          if (row < 0 || row >= ROWS) continue;
+#pragma unroll
+          for (int t = 0; t < 9; ++t)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              L[(row + 4 * kq + i) * RP + (wc * 16 + lr) * 9 + t] = acc[m][t][i];
+        }
+      }
+      __syncthreads();
+      for (int q = tid; q < ROWS * QPR; q += 256) {
+        const int row = q / QPR, col = (q % QPR) * 4, k = k0 + r0 + row;
+        if (k >= a.K || col >= cw) continue;
+        float* o = dst + (size_t)k * a.C * 9 + (size_t)c0 * 9 + col;
+        const float* l = L + row * RP + col;
+        if (vec) {
+          *reinterpret_cast<f4*>(o) = *reinterpret_cast<const f4*>(l);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (col + e < cw) o[e] = l[e];
+        }
+      }
+    }
+    if (wp == 0 && do_db && lr == 0) {
+      float* pb = a.splits == 1 ? a.db : dst + wsz;
+#pragma unroll
+      for (int m = 0; m < T::MA; ++m)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int k = k0 + (wk * T::MA + m) * 16 + 4 * kq + i;
+          if (k < a.K) pb[k] = accb[m][i];
+        }
+    }
+  }
+}
+
 template <class T, int V>
 __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_bf16(WgArgs a) {
   extern __shared__ u16 ldsw[];
@@ -596,7 +706,7 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_bf16(WgArgs a) {
   const bool do_db = (a.db != nullptr) && ct == 0 && wc == 0;
   const int HWs = a.H * a.W;
 
-  f4 acc[T::MA][9], accb[T::MA];
+  f4 acc[T::MA][9];
   float sbias[T::MA];    // this lane's share of the bias gradient of row block m
 #pragma unroll
   for (int m = 0; m < T::MA; ++m) {
@@ -787,101 +897,212 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_bf16(WgArgs a) {
     compute(buf);
     __syncthreads();
   }
-#pragma unroll
-  for (int m = 0; m < T::MA; ++m) accb[m] = wave_row_sums(sbias[m]);
+  wgrad_bf16_finish<T>(a, blk, k0, c0, do_db, wk, wp, wc, acc, sbias, ldsw);
+}
 
-  // Sum the two step halves: waves wp = 1 hand their accumulators to the
-  // waves wp = 0 of the same (wk, wc) through LDS (lane fastest, so the
-  // stores and loads are conflict-free), in rounds of RA k blocks.
-  {
-    constexpr int RA =                                 // k blocks per round
-        T::MA >= 2 && T::WC * T::WK * 2 * 40 * 64 * 4 <= (int)T::LDS_BYTES ? 2 : 1;
-    constexpr int NF = RA * 10 * 4;                    // floats per lane per round
-    static_assert(T::WC * T::WK * NF * 64 * 4 <= T::LDS_BYTES, "reduction fits the LDS");
-    float* R = reinterpret_cast<float*>(ldsw) + (wk * T::WC + wc) * NF * 64;
+// ------------------------------------------------- channel-blocked bf16 --
+// Weight gradient of channel-blocked tensors (SB_NCHW8C: 8 consecutive
+// channels of a pixel are one 16-byte piece).  The GEMM and the waves' work
+// are the NCHW bf16 kernel's (rows 64 k, columns BC channels x 9 taps,
+// reduction over 64-pixel tiles, v_mfma_f32_16x16x32_bf16, the two 32-pixel
+// steps of a stage on different waves), but the tiles sit in LDS as they sit
+// in memory: dy as [pixel][k] and the x halo as [halo pixel][c], staged as
+// whole 16-byte pieces (one load and one LDS store each, no transposition,
+// no shifted copies: a tap's shift is a whole row of the halo).  A lane of
+// this MFMA needs 8 consecutive pixels of one k (or one c); it reads them
+// with two LDS transpose loads (ds_read_b64_tr_b16: within each group of 16
+// lanes, lane 4a + e receives element e of the 8-byte pieces the lanes
+// a, a + 4, a + 8, a + 12 point at), each lane of the group pointing at 4
+// consecutive channels of one of 4 consecutive pixels.
+template <int TH_, int TW_, int BC_>
+struct WgC8Tile {
+  static constexpr int TH = TH_, TW = TW_, BC = BC_;
+  static constexpr int BP = TH * TW;
+  static_assert(BP == 64 && TW % 8 == 0, "64-pixel tiles of 8-pixel row groups");
+  static constexpr int BK = 64;
+  static_assert(BC == 16 || BC == 32, "16 or 32 input channels per block");
+  static constexpr int WC = BC / 16, WP = 2, WK = 4 / (WC * WP), MA = 4 / WK;
+  static_assert(WC * WP * WK == 4, "four waves");
+  static constexpr int HH = TH + 2, HWD = TW + 2, HPIX = HH * HWD;
+  // Row pitches (bf16): a transpose load's 16 lanes read 4 rows x 32 bytes;
+  // 144-byte dy rows and (BC + 16) * 2-byte x rows put the 4 rows' bytes on
+  // distinct banks.  Both are whole 16-byte pieces.
+  static constexpr int DYP = BK + 8, XP = BC + 16;
+  static constexpr int LDS_DY = BP * DYP, LDS_X = HPIX * XP;
+  static constexpr int LDS_BUF = LDS_DY + LDS_X;
+  static constexpr int DY_PIECES = BP * BK / 8, X_PIECES = HPIX * BC / 8;
+  static constexpr int DY_I = DY_PIECES / 256, X_I = (X_PIECES + 255) / 256;
+  static_assert(DY_PIECES % 256 == 0, "whole rounds of dy pieces");
+  // The block's end reuses the LDS for the step-half reduction (up to
+  // 2 * 40 floats per lane of each (wk, wc) wave) and the dw row staging
+  // (32 rows of BC * 9 + 4 floats).
+  static constexpr size_t STAGE = 2 * LDS_BUF * sizeof(u16);
+  static constexpr size_t RED = (size_t)WC * WK * 2 * 40 * 64 * 4;
+  static constexpr size_t ROWS = (size_t)32 * (BC * 9 + 4) * 4;
+  static constexpr size_t LDS_BYTES = STAGE > RED ? (STAGE > ROWS ? STAGE : ROWS)
+                                                  : (RED > ROWS ? RED : ROWS);
+  static_assert(LDS_BYTES <= 80 * 1024, "two blocks must fit in the 160 KB of LDS");
+};
+
+typedef short v4s __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4s lds_v4s;
+
+// 8 consecutive-row values of one column from two transpose loads: rows
+// r0 .. r0 + 3 and r0 + 4 .. r0 + 7 (row pitch `pitch` bf16), the 16-lane
+// group's column block at col0 (lane 4a + e of the group gets column
+// col0 + 4a + e).  `lrow(j)` maps j = 0..7 to the LDS row.
+template <class Row>
+__device__ __forceinline__ s8 tr_read8(const u16* base, int pitch, int col0, Row lrow) {
+  const int s = threadIdx.x & 15, a = s & 3, j = s >> 2;
+  const v4s lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (lds_v4s*)(base + lrow(j) * pitch + col0 + 4 * a));
+  const v4s hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (lds_v4s*)(base + lrow(j + 4) * pitch + col0 + 4 * a));
+  return s8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+}
+
+template <class T>
+__global__ __launch_bounds__(256, 2) void conv3x3_wgrad_c8(WgArgs a) {
+  extern __shared__ u16 ldsw[];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int kq = lane >> 4;
+  const WgBlock blk = wg_block();
+  const int ct = blk.x % a.c_tiles, kt = blk.x / a.c_tiles;
+  const int c0 = ct * T::BC, k0 = kt * T::BK;
+  const int pt0 = blk.z * a.tiles_per_split;
+  const int pt1 = min(a.ptiles, pt0 + a.tiles_per_split);
+  const int wc = wave % T::WC, wp = (wave / T::WC) % T::WP, wk = wave / (T::WC * T::WP);
+  const bool do_db = (a.db != nullptr) && ct == 0 && wc == 0;
+  const int HWs = a.H * a.W, KB = a.K / 8, CB = a.C / 8;
+
+  f4 acc[T::MA][9];
+  float sbias[T::MA];
 #pragma unroll
-    for (int r0 = 0; r0 < T::MA; r0 += RA) {
-      if (wp == 1) {
+  for (int m = 0; m < T::MA; ++m) {
+    sbias[m] = 0.f;
 #pragma unroll
-        for (int m = 0; m < RA; ++m) {
-#pragma unroll
-          for (int t = 0; t < 9; ++t)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) R[((m * 10 + t) * 4 + i) * 64 + lane] = acc[r0 + m][t][i];
-#pragma unroll
-          for (int i = 0; i < 4; ++i) R[((m * 10 + 9) * 4 + i) * 64 + lane] = accb[r0 + m][i];
-        }
-      }
-      __syncthreads();
-      if (wp == 0) {
-#pragma unroll
-        for (int m = 0; m < RA; ++m) {
-#pragma unroll
-          for (int t = 0; t < 9; ++t)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) acc[r0 + m][t][i] += R[((m * 10 + t) * 4 + i) * 64 + lane];
-#pragma unroll
-          for (int i = 0; i < 4; ++i) accb[r0 + m][i] += R[((m * 10 + 9) * 4 + i) * 64 + lane];
-        }
-      }
-      __syncthreads();
-    }
+    for (int t = 0; t < 9; ++t) acc[m][t] = f4{0.f, 0.f, 0.f, 0.f};
   }
-  // acc[m][t] of the waves wp = 0 holds rows k = k0 + (wk*MA + m)*16 +
-  // 4*kq + i and channel c0 + wc*16 + lr.  The block's 64 k x (BC c x 9
-  // taps) tile goes out through LDS in rounds of 32 rows of BC * 9
-  // consecutive floats (the dw order), written in 16-byte pieces; every
-  // wave takes part in the barriers and the stores.
-  {
-    constexpr int RW = T::BC * 9, RP = RW + 4, ROWS = 32, QPR = RW / 4;
-    static_assert(ROWS * RP * sizeof(float) <= T::LDS_BYTES && RW % 4 == 0, "rows fit the LDS");
-    float* L = reinterpret_cast<float*>(ldsw);
-    const int cw = min(T::BC, a.C - c0) * 9;         // live columns of the tile
-    const size_t wsz = (size_t)a.K * a.C * 9;
-    float* dst = a.splits == 1 ? a.dw : a.part + (size_t)blk.z * (wsz + a.K);
-    const bool vec = (a.C * 9) % 4 == 0 && cw % 4 == 0 &&
-                     (((uintptr_t)dst + (size_t)c0 * 9 * sizeof(float)) & 15) == 0;
+
+  // Staging: dy piece q = (k block q / 64, tile pixel q % 64); x piece
+  // q = (c block q / HPIX, halo pixel q % HPIX).  Offsets (elements) within
+  // an image for a tile at (h0, w0) = (0, 0) (negative for the halo's first
+  // row or column), and whether the piece's k or c block exists.
+  int dy_rel[T::DY_I], dy_yy[T::DY_I], dy_xx[T::DY_I];
+  bool dy_live[T::DY_I];
 #pragma unroll
-    for (int r0 = 0; r0 < T::BK; r0 += ROWS) {
-      __syncthreads();                                // the LDS is free
-      if (wp == 0) {
+  for (int i = 0; i < T::DY_I; ++i) {
+    const int q = tid + 256 * i, p = q % 64, kb = k0 / 8 + q / 64;
+    dy_yy[i] = p / T::TW;
+    dy_xx[i] = p % T::TW;
+    dy_live[i] = kb < KB;
+    dy_rel[i] = (kb * HWs + dy_yy[i] * a.W + dy_xx[i]) * 8;
+  }
+  int x_rel[T::X_I], x_hy[T::X_I], x_hx[T::X_I];
+  bool x_live[T::X_I];
 #pragma unroll
-        for (int m = 0; m < T::MA; ++m) {
-          const int row = (wk * T::MA + m) * 16 - r0;
-          if (row < 0 || row >= ROWS) continue;
-#pragma unroll
-          for (int t = 0; t < 9; ++t)
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-              L[(row + 4 * kq + i) * RP + (wc * 16 + lr) * 9 + t] = acc[m][t][i];
-        }
-      }
-      __syncthreads();
-      for (int q = tid; q < ROWS * QPR; q += 256) {
-        const int row = q / QPR, col = (q % QPR) * 4, k = k0 + r0 + row;
-        if (k >= a.K || col >= cw) continue;
-        float* o = dst + (size_t)k * a.C * 9 + (size_t)c0 * 9 + col;
-        const float* l = L + row * RP + col;
-        if (vec) {
-          *reinterpret_cast<f4*>(o) = *reinterpret_cast<const f4*>(l);
-        } else {
-#pragma unroll
-          for (int e = 0; e < 4; ++e)
-            if (col + e < cw) o[e] = l[e];
-        }
-      }
+  for (int i = 0; i < T::X_I; ++i) {
+    const int q = tid + 256 * i, hp = q % T::HPIX, cb = c0 / 8 + q / T::HPIX;
+    x_hy[i] = hp / T::HWD - 1;
+    x_hx[i] = hp % T::HWD - 1;
+    x_live[i] = q < T::X_PIECES && cb < CB;
+    x_rel[i] = (cb * HWs + x_hy[i] * a.W + x_hx[i]) * 8;
+  }
+
+  int ntx = pt0 % a.tiles_w, nty = (pt0 / a.tiles_w) % a.tiles_h,
+      nn = pt0 / (a.tiles_w * a.tiles_h);
+  s8 rdy[T::DY_I], rx[T::X_I];
+
+  auto gload = [&]() {
+    const int h0 = nty * T::TH, w0 = ntx * T::TW, n0 = nn;
+    if (++ntx == a.tiles_w) {
+      ntx = 0;
+      if (++nty == a.tiles_h) { nty = 0; ++nn; }
     }
-    if (wp == 0 && do_db && lr == 0) {
-      float* pb = a.splits == 1 ? a.db : dst + wsz;
+    const rsrc_t dr = image_rsrc<u16>(a.dy, n0, 1, a.N, a.K * HWs);
+    const rsrc_t xr = image_rsrc<u16>(a.x, n0, 1, a.N, a.C * HWs);
+    const int tile = (h0 * a.W + w0) * 8;
+#pragma unroll
+    for (int i = 0; i < T::DY_I; ++i) {
+      const bool ok = dy_live[i] && h0 + dy_yy[i] < a.H && w0 + dy_xx[i] < a.W;
+      const uint32_t off = ok ? (uint32_t)(dy_rel[i] + tile) * 2u : kOOB;
+      rdy[i] = __builtin_bit_cast(s8, __builtin_amdgcn_raw_buffer_load_b128(dr, (int)off, 0, 0));
+    }
+#pragma unroll
+    for (int i = 0; i < T::X_I; ++i) {
+      const bool ok = x_live[i] && (unsigned)(h0 + x_hy[i]) < (unsigned)a.H &&
+                      (unsigned)(w0 + x_hx[i]) < (unsigned)a.W;
+      const uint32_t off = ok ? (uint32_t)(x_rel[i] + tile) * 2u : kOOB;
+      rx[i] = __builtin_bit_cast(s8, __builtin_amdgcn_raw_buffer_load_b128(xr, (int)off, 0, 0));
+    }
+  };
+  auto lstore = [&](int buf) {
+    u16* Dl = ldsw + buf * T::LDS_BUF;
+    u16* Xl = Dl + T::LDS_DY;
+#pragma unroll
+    for (int i = 0; i < T::DY_I; ++i) {
+      const int q = tid + 256 * i;
+      *reinterpret_cast<s8*>(Dl + (q % 64) * T::DYP + (q / 64) * 8) = rdy[i];
+    }
+#pragma unroll
+    for (int i = 0; i < T::X_I; ++i) {
+      const int q = tid + 256 * i;
+      if (q < T::X_PIECES)
+        *reinterpret_cast<s8*>(Xl + (q % T::HPIX) * T::XP + (q / T::HPIX) * 8) = rx[i];
+    }
+  };
+  auto compute = [&](int buf) {
+    const u16* Dl = ldsw + buf * T::LDS_BUF;
+    const u16* Xl = Dl + T::LDS_DY;
+    // This wave's step wp; lane group kq takes pixels p .. p + 7 (one row).
+    const int p = wp * 32 + 8 * kq;
+    const int yy = p / T::TW, xx = p % T::TW;
+    s8 av[T::MA];
+#pragma unroll
+    for (int m = 0; m < T::MA; ++m)
+      av[m] = tr_read8(Dl, T::DYP, (wk * T::MA + m) * 16, [&](int j) { return p + j; });
+#pragma unroll
+    for (int t = 0; t < 9; ++t) {
+      const int r = t / 3, sft = t % 3;
+      const s8 bv = tr_read8(Xl, T::XP, wc * 16,
+                             [&](int j) { return (yy + r) * T::HWD + xx + sft + j; });
 #pragma unroll
       for (int m = 0; m < T::MA; ++m)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int k = k0 + (wk * T::MA + m) * 16 + 4 * kq + i;
-          if (k < a.K) pb[k] = accb[m][i];
-        }
+        acc[m][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+            __builtin_bit_cast(bf16x8, av[m]), __builtin_bit_cast(bf16x8, bv), acc[m][t], 0, 0,
+            0);
     }
+    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+    const bf16x2 one2 = {(__bf16)1.0f, (__bf16)1.0f};
+#pragma unroll
+    for (int m = 0; m < T::MA; ++m) {
+      const bf16x8 v = __builtin_bit_cast(bf16x8, av[m]);
+      sbias[m] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(v, v, 0, 1), one2,
+                                                 sbias[m], false);
+      sbias[m] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(v, v, 2, 3), one2,
+                                                 sbias[m], false);
+      sbias[m] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(v, v, 4, 5), one2,
+                                                 sbias[m], false);
+      sbias[m] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(v, v, 6, 7), one2,
+                                                 sbias[m], false);
+    }
+  };
+
+  const int nt = pt1 - pt0;
+  if (nt > 0) {
+    gload();
+    lstore(0);
+    if (nt > 1) gload();
   }
+  __syncthreads();
+  for (int t = 0; t < nt; ++t) {
+    const int buf = t & 1;
+    if (t + 1 < nt) lstore(buf ^ 1);
+    if (t + 2 < nt) gload();
+    compute(buf);
+    __syncthreads();
+  }
+  wgrad_bf16_finish<T>(a, blk, k0, c0, do_db, wk, wp, wc, acc, sbias, ldsw);
 }
 
 // ------------------------------------------------------ small whole images --
@@ -1414,6 +1635,61 @@ sb_status conv_wgrad(int dtype, int N, int C, int H, int W, int K, const void* x
     wg_dispatch<sb::u16>(p, a, st);
   } else {
     wg_dispatch<float>(p, a, st);
+  }
+  return launch_status();
+}
+
+
+// Channel-blocked bf16 tensors (SB_NCHW8C): the plan of the NCHW bf16 path
+// (tiles of 64 pixels, 16 or 32 channels per block), the transpose-load
+// kernel.
+template <class T>
+static void wg_launch_c8(const sb::WgPlan& p, const sb::WgArgs& a, hipStream_t st) {
+  static std::once_flag once;
+  std::call_once(once, [] {
+    (void)hipFuncSetAttribute((const void*)sb::conv3x3_wgrad_c8<T>,
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)T::LDS_BYTES);
+  });
+  dim3 grid(p.k_tiles * p.c_tiles, 1, p.splits);
+  sb::conv3x3_wgrad_c8<T><<<grid, 256, T::LDS_BYTES, st>>>(a);
+  if (p.splits > 1) sb::launch_splits_reduce(a.part, p.splits, a.K, a.C, a.dw, a.db, st);
+}
+
+bool conv_wgrad_c8_takes(int N, int C, int H, int W, int K) {
+  return W >= 8 && C % 8 == 0 && K % 8 == 0 && sb::wg_plan(N, C, H, W, K, false, true).bc != 0;
+}
+
+int conv_wgrad_c8_describe(int N, int C, int H, int W, int K, char* buf, size_t len) {
+  sb::WgPlan p = sb::wg_plan(N, C, H, W, K, false, true);
+  static const char* kT[] = {"2, 32", "4, 16", "8, 8"};
+  return snprintf(buf, len, "sb::conv3x3_wgrad_c8<sb::WgC8Tile<%s, %d>> grid=%dx1x%d",
+                  kT[p.tile], p.bc, p.k_tiles * p.c_tiles, p.splits);
+}
+
+sb_status conv_wgrad_c8(int N, int C, int H, int W, int K, const void* x, const void* dy,
+                        float* dw, float* db, void* ws, size_t ws_bytes, hipStream_t st) {
+  sb::WgPlan p = sb::wg_plan(N, C, H, W, K, false, true);
+  if (!conv_wgrad_c8_takes(N, C, H, W, K)) return SB_ERR_UNSUPPORTED;
+  if ((int64_t)std::max(C, K) * H * W * 2 >= (1ll << 31)) return SB_ERR_UNSUPPORTED;
+  if (p.ws_bytes > 0 && (ws == nullptr || ws_bytes < p.ws_bytes)) return SB_ERR_WORKSPACE;
+  sb::WgArgs a{};
+  a.x = x; a.dy = dy; a.dw = dw; a.db = db;
+  a.part = p.splits > 1 ? (float*)ws : nullptr;
+  a.N = N; a.C = C; a.H = H; a.W = W; a.K = K;
+  a.tiles_w = p.tiles_w; a.tiles_h = p.tiles_h; a.ptiles = p.ptiles;
+  a.tiles_per_split = p.tps; a.c_tiles = p.c_tiles; a.splits = p.splits;
+  if (p.bc == 32) {
+    switch (p.tile) {
+      case 0: wg_launch_c8<sb::WgC8Tile<2, 32, 32>>(p, a, st); break;
+      case 1: wg_launch_c8<sb::WgC8Tile<4, 16, 32>>(p, a, st); break;
+      default: wg_launch_c8<sb::WgC8Tile<8, 8, 32>>(p, a, st); break;
+    }
+  } else {
+    switch (p.tile) {
+      case 0: wg_launch_c8<sb::WgC8Tile<2, 32, 16>>(p, a, st); break;
+      case 1: wg_launch_c8<sb::WgC8Tile<4, 16, 16>>(p, a, st); break;
+      default: wg_launch_c8<sb::WgC8Tile<8, 8, 16>>(p, a, st); break;
+    }
   }
   return launch_status();
 }

@@ -157,6 +157,86 @@ __global__ __launch_bounds__(256) void relu_maxpool_bwd_vec(
   *reinterpret_cast<row_t*>(p0 + W) = r1;
 }
 
+// Channel-blocked tensors (SB_NCHW8C): a thread owns one window of 8
+// channels (one 16-byte bf16 piece per pixel): its two input rows are 16
+// contiguous elements each, its output and codes 8 contiguous elements and
+// bytes, and neighbouring threads take neighbouring windows.
+template <typename T>
+__global__ __launch_bounds__(256) void relu_maxpool_fwd_c8(
+    const T* __restrict__ x, T* __restrict__ y, uint8_t* __restrict__ idx, uint32_t Wo,
+    uint32_t total) {
+  const uint32_t g = blockIdx.x * 256u + threadIdx.x;   // ((n*CB + cb)*Ho + oh)*Wo + ow
+  if (g >= total) return;
+  const uint32_t row = g / Wo, ow = g - row * Wo;
+  const size_t W = 2 * (size_t)Wo;
+  const T* p0 = x + ((size_t)row * 2 * W + 2 * ow) * 8;
+  const T* p1 = p0 + W * 8;
+  typedef typename V8<T>::t v8;
+  const v8 a0 = *reinterpret_cast<const v8*>(p0), a1 = *reinterpret_cast<const v8*>(p0 + 8);
+  const v8 b0 = *reinterpret_cast<const v8*>(p1), b1 = *reinterpret_cast<const v8*>(p1 + 8);
+  v8 o;
+  uint32_t codes[2] = {0u, 0u};
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    float m = V8<T>::get(a0, e);
+    uint32_t c = 0;
+    const float v1 = V8<T>::get(a1, e), v2 = V8<T>::get(b0, e), v3 = V8<T>::get(b1, e);
+    if (v1 > m) { m = v1; c = 1; }
+    if (v2 > m) { m = v2; c = 2; }
+    if (v3 > m) { m = v3; c = 3; }
+    const bool pos = m > 0.0f;
+    V8<T>::put(o, e, pos ? m : 0.0f);
+    codes[e / 4] |= (c | (pos ? 0u : 0x80u)) << (8 * (e % 4));
+  }
+  *reinterpret_cast<v8*>(y + (size_t)g * 8) = o;
+  *reinterpret_cast<uint2*>(idx + (size_t)g * 8) = make_uint2(codes[0], codes[1]);
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void relu_maxpool_bwd_c8(
+    const T* __restrict__ dy, const uint8_t* __restrict__ idx, T* __restrict__ dx, uint32_t Wo,
+    uint32_t total) {
+  const uint32_t g = blockIdx.x * 256u + threadIdx.x;
+  if (g >= total) return;
+  const uint32_t row = g / Wo, ow = g - row * Wo;
+  const size_t W = 2 * (size_t)Wo;
+  typedef typename V8<T>::t v8;
+  const v8 gv = *reinterpret_cast<const v8*>(dy + (size_t)g * 8);
+  const uint2 cw = *reinterpret_cast<const uint2*>(idx + (size_t)g * 8);
+  v8 a0, a1, b0, b1;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const uint32_t code = ((e < 4 ? cw.x : cw.y) >> (8 * (e % 4))) & 0xffu;
+    const bool live = !(code & 0x80u);
+    const uint32_t c = code & 3u;
+    const float v = V8<T>::get(gv, e);
+    V8<T>::put(a0, e, (live && c == 0) ? v : 0.0f);
+    V8<T>::put(a1, e, (live && c == 1) ? v : 0.0f);
+    V8<T>::put(b0, e, (live && c == 2) ? v : 0.0f);
+    V8<T>::put(b1, e, (live && c == 3) ? v : 0.0f);
+  }
+  T* p0 = dx + ((size_t)row * 2 * W + 2 * ow) * 8;
+  T* p1 = p0 + W * 8;
+  *reinterpret_cast<v8*>(p0) = a0;
+  *reinterpret_cast<v8*>(p0 + 8) = a1;
+  *reinterpret_cast<v8*>(p1) = b0;
+  *reinterpret_cast<v8*>(p1 + 8) = b1;
+}
+
+template <typename T>
+static sb_status pool_launch_c8(bool fwd, int n, int c, int h, int w, const void* in,
+                                const uint8_t* idx_in, void* out, uint8_t* idx_out,
+                                hipStream_t st) {
+  const uint32_t Wo = (uint32_t)(w / 2);
+  const uint32_t total = (uint32_t)n * (c / 8) * (h / 2) * Wo;
+  dim3 grid((total + 255) / 256), block(256);
+  if (fwd)
+    relu_maxpool_fwd_c8<T><<<grid, block, 0, st>>>((const T*)in, (T*)out, idx_out, Wo, total);
+  else
+    relu_maxpool_bwd_c8<T><<<grid, block, 0, st>>>((const T*)in, idx_in, (T*)out, Wo, total);
+  return sbh::launch_status();
+}
+
 template <typename T>
 static sb_status pool_launch(bool fwd, int n, int c, int h, int w, const void* in,
                              const uint8_t* idx_in, void* out, uint8_t* idx_out,
@@ -192,19 +272,21 @@ static sb_status pool_launch(bool fwd, int n, int c, int h, int w, const void* i
 
 using namespace sb;
 
-static sb_status pool_check(int n, int c, int h, int w, int dtype) {
+static sb_status pool_check(int n, int c, int h, int w, int dtype, int layout) {
   if (n <= 0 || c <= 0 || h <= 0 || w <= 0) return SB_ERR_INVALID_ARG;
   if ((h & 1) || (w & 1)) return SB_ERR_INVALID_ARG;
   if (dtype != SB_F32 && dtype != SB_BF16) return SB_ERR_INVALID_ARG;
+  if (layout != SB_NCHW && layout != SB_NCHW8C) return SB_ERR_INVALID_ARG;
+  if (layout == SB_NCHW8C && c % 8) return SB_ERR_INVALID_ARG;
   // 32-bit window indexing inside the kernels.
   if ((uint64_t)n * c * h * w >= (1ull << 32)) return SB_ERR_UNSUPPORTED;
   return SB_OK;
 }
 
-extern "C" sb_status sb_relu_maxpool_fwd(int n, int c, int h, int w, int dtype,
+extern "C" sb_status sb_relu_maxpool_fwd(int n, int c, int h, int w, int dtype, int layout,
                                          const void* x, void* y, uint8_t* idx,
                                          void* stream) {
-  sb_status s = pool_check(n, c, h, w, dtype);
+  sb_status s = pool_check(n, c, h, w, dtype, layout);
   if (s != SB_OK) return s;
   if (!x || !y || !idx) return SB_ERR_INVALID_ARG;
   size_t es = sbh::dsize(dtype);
@@ -213,14 +295,20 @@ extern "C" sb_status sb_relu_maxpool_fwd(int n, int c, int h, int w, int dtype,
       sbh::overlaps(y, out_n * es, idx, out_n))
     return SB_ERR_INVALID_ARG;
   hipStream_t st = sbh::stream_of(stream);
+  if (layout == SB_NCHW8C) {
+    // 16-byte pieces (8 bf16 or 2 x 4 fp32), 8-byte code groups.
+    if (((uintptr_t)x | (uintptr_t)y) & 15 || (uintptr_t)idx & 7) return SB_ERR_INVALID_ARG;
+    return dtype == SB_F32 ? pool_launch_c8<float>(true, n, c, h, w, x, nullptr, y, idx, st)
+                           : pool_launch_c8<u16>(true, n, c, h, w, x, nullptr, y, idx, st);
+  }
   return dtype == SB_F32 ? pool_launch<float>(true, n, c, h, w, x, nullptr, y, idx, st)
                          : pool_launch<u16>(true, n, c, h, w, x, nullptr, y, idx, st);
 }
 
-extern "C" sb_status sb_relu_maxpool_bwd(int n, int c, int h, int w, int dtype,
+extern "C" sb_status sb_relu_maxpool_bwd(int n, int c, int h, int w, int dtype, int layout,
                                          const void* dy, const uint8_t* idx, void* dx,
                                          void* stream) {
-  sb_status s = pool_check(n, c, h, w, dtype);
+  sb_status s = pool_check(n, c, h, w, dtype, layout);
   if (s != SB_OK) return s;
   if (!dy || !idx || !dx) return SB_ERR_INVALID_ARG;
   size_t es = sbh::dsize(dtype);
@@ -228,6 +316,11 @@ extern "C" sb_status sb_relu_maxpool_bwd(int n, int c, int h, int w, int dtype,
   if (sbh::overlaps(dx, out_b, dy, in_n * es) || sbh::overlaps(dx, out_b, idx, in_n))
     return SB_ERR_INVALID_ARG;
   hipStream_t st = sbh::stream_of(stream);
+  if (layout == SB_NCHW8C) {
+    if (((uintptr_t)dy | (uintptr_t)dx) & 15 || (uintptr_t)idx & 7) return SB_ERR_INVALID_ARG;
+    return dtype == SB_F32 ? pool_launch_c8<float>(false, n, c, h, w, dy, idx, dx, nullptr, st)
+                           : pool_launch_c8<u16>(false, n, c, h, w, dy, idx, dx, nullptr, st);
+  }
   return dtype == SB_F32 ? pool_launch<float>(false, n, c, h, w, dy, idx, dx, nullptr, st)
                          : pool_launch<u16>(false, n, c, h, w, dy, idx, dx, nullptr, st);
 }

@@ -21,6 +21,7 @@ LIB_PATH = os.path.join(HERE, "libsb.so")
 
 SB_OK, SB_ERR_INVALID_ARG, SB_ERR_UNSUPPORTED, SB_ERR_WORKSPACE, SB_ERR_HIP = range(5)
 SB_F32, SB_BF16 = 0, 1
+SB_NCHW, SB_NCHW8C = 0, 1
 SB_FUSE_RELU = 1
 SB_PACKED_FILTERS = 2
 SB_PASS_FWD, SB_PASS_BWD_DATA, SB_PASS_BWD_WEIGHT = 0, 1, 2
@@ -35,7 +36,7 @@ _sz = ctypes.c_size_t
 
 class sb_conv3x3_desc(ctypes.Structure):
     _fields_ = [("n", _i), ("c", _i), ("h", _i), ("w", _i), ("k", _i),
-                ("dtype", _i), ("flags", ctypes.c_uint)]
+                ("dtype", _i), ("flags", ctypes.c_uint), ("layout", _i)]
 
 
 class sb_fc_desc(ctypes.Structure):
@@ -67,8 +68,8 @@ SIGNATURES = {
     "sb_conv3x3_bwd_weight": (_i, [ctypes.POINTER(sb_conv3x3_desc), _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "sb_conv3x3_bwd_weight_noalloc": (_i, [ctypes.POINTER(sb_conv3x3_desc), _vp, _vp, _vp, _vp,
                                            _vp]),
-    "sb_relu_maxpool_fwd": (_i, [_i, _i, _i, _i, _i, _vp, _vp, _vp, _vp]),
-    "sb_relu_maxpool_bwd": (_i, [_i, _i, _i, _i, _i, _vp, _vp, _vp, _vp]),
+    "sb_relu_maxpool_fwd": (_i, [_i, _i, _i, _i, _i, _i, _vp, _vp, _vp, _vp]),
+    "sb_relu_maxpool_bwd": (_i, [_i, _i, _i, _i, _i, _i, _vp, _vp, _vp, _vp]),
     "sb_fc_workspace_bytes": (_sz, [ctypes.POINTER(sb_fc_desc), _i]),
     "sb_fc_shard_fwd": (_i, [ctypes.POINTER(sb_fc_desc), _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "sb_fc_shard_bwd": (_i, [ctypes.POINTER(sb_fc_desc), _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i,
@@ -157,9 +158,10 @@ def _ws(ws):
     return ws.data_ptr(), ws.numel() * ws.element_size()
 
 
-def conv_desc(n, c, h, w, k, dtype=SB_F32, relu=False, packed=False):
+def conv_desc(n, c, h, w, k, dtype=SB_F32, relu=False, packed=False, layout=SB_NCHW):
     return sb_conv3x3_desc(n, c, h, w, k, dtype,
-                           (SB_FUSE_RELU if relu else 0) | (SB_PACKED_FILTERS if packed else 0))
+                           (SB_FUSE_RELU if relu else 0) | (SB_PACKED_FILTERS if packed else 0),
+                           layout)
 
 
 def fc_desc(m, k_in, n_shard, dtype=SB_F32, ldx=None, ldy=None, relu=False):
@@ -239,14 +241,14 @@ def sb_conv3x3_bwd_weight_noalloc(desc, x, dy, dw, db, stream=None):
         ctypes.byref(desc), _ptr(x), _ptr(dy), _ptr(dw), _ptr(db), _stream(stream)))
 
 
-def sb_relu_maxpool_fwd(n, c, h, w, dtype, x, y, idx, stream=None):
+def sb_relu_maxpool_fwd(n, c, h, w, dtype, layout, x, y, idx, stream=None):
     _check("sb_relu_maxpool_fwd", load().sb_relu_maxpool_fwd(
-        n, c, h, w, dtype, _ptr(x), _ptr(y), _ptr(idx), _stream(stream)))
+        n, c, h, w, dtype, layout, _ptr(x), _ptr(y), _ptr(idx), _stream(stream)))
 
 
-def sb_relu_maxpool_bwd(n, c, h, w, dtype, dy, idx, dx, stream=None):
+def sb_relu_maxpool_bwd(n, c, h, w, dtype, layout, dy, idx, dx, stream=None):
     _check("sb_relu_maxpool_bwd", load().sb_relu_maxpool_bwd(
-        n, c, h, w, dtype, _ptr(dy), _ptr(idx), _ptr(dx), _stream(stream)))
+        n, c, h, w, dtype, layout, _ptr(dy), _ptr(idx), _ptr(dx), _stream(stream)))
 
 
 def sb_fc_workspace_bytes(desc, pass_):

@@ -71,27 +71,40 @@ class ConvStack:
     """
 
     def __init__(self, schedule, n, in_ch, hw, dtype="f32", device="cuda",
-                 out_buffer=None, out_grad_buffer=None, packed=True, overlap=True):
+                 out_buffer=None, out_grad_buffer=None, packed=True, overlap=True,
+                 layout="nchw"):
+        """layout: "nchw", or "c8" for channel-blocked activations
+        (SB_NCHW8C, bf16 only): every activation buffer is then
+        [n][c/8][h][w][8], and the first layer's input channels are padded
+        with zeros to a whole block of 8 (zero filters for the padding, so
+        every result is the unpadded network's)."""
         self.layers = conv_layers(schedule, in_ch, hw)
         if not self.layers[-1].pool_after:
             raise ValueError("the stack must end with a pooled layer")
+        if layout not in ("nchw", "c8") or (layout == "c8" and dtype != "bf16"):
+            raise ValueError("layout 'c8' is for bf16 stacks")
         self.n, self.dtype = n, dtype
         self.code = _code(dtype)
+        self.c8 = layout == "c8"
+        self.layout = sb.SB_NCHW8C if self.c8 else sb.SB_NCHW
         tdt = _dev_dtype(dtype)
         dev = torch.device(device)
         self.device = dev
         L = self.layers
-        self.A = [torch.empty((n, in_ch, hw, hw), dtype=tdt, device=dev)]
+        # Input channels of each layer as stored (the first padded for c8).
+        self.cin = [(-(-l.c // 8) * 8 if self.c8 else l.c) for l in L]
+        shp = self.shape_of
+        self.A = [torch.empty(shp(n, self.cin[0], hw, hw), dtype=tdt, device=dev)]
         self.Z, self.idx, self.dZ = {}, {}, {}
         for l in L:
             if l.pool_after:
-                self.Z[l.index] = torch.empty((n, l.k, l.h, l.w), dtype=tdt, device=dev)
-                self.idx[l.index] = torch.empty((n, l.k, l.h // 2, l.w // 2), dtype=torch.uint8,
-                                                device=dev)
-                self.dZ[l.index] = torch.empty((n, l.k, l.h, l.w), dtype=tdt, device=dev)
-                shape = (n, l.k, l.h // 2, l.w // 2)
+                self.Z[l.index] = torch.empty(shp(n, l.k, l.h, l.w), dtype=tdt, device=dev)
+                self.idx[l.index] = torch.empty(shp(n, l.k, l.h // 2, l.w // 2),
+                                                dtype=torch.uint8, device=dev)
+                self.dZ[l.index] = torch.empty(shp(n, l.k, l.h, l.w), dtype=tdt, device=dev)
+                shape = shp(n, l.k, l.h // 2, l.w // 2)
             else:
-                shape = (n, l.k, l.h, l.w)
+                shape = shp(n, l.k, l.h, l.w)
             last = l.index == len(L) - 1
             if last and out_buffer is not None:
                 self.A.append(out_buffer.view(shape))
@@ -100,13 +113,17 @@ class ConvStack:
         self.gA = [torch.empty_like(a) for a in self.A[:-1]]
         self.gA.append(out_grad_buffer.view(self.A[-1].shape) if out_grad_buffer is not None
                        else torch.empty_like(self.A[-1]))
-        self.W = [torch.empty((l.k, l.c, 3, 3), dtype=tdt, device=dev) for l in L]
+        C = self.cin
+        lay = self.layout
+        self.W = [torch.zeros((l.k, C[l.index], 3, 3), dtype=tdt, device=dev) for l in L]
         self.b = [torch.zeros((l.k,), dtype=torch.float32, device=dev) for l in L]
-        self.dW = [torch.empty((l.k, l.c, 3, 3), dtype=torch.float32, device=dev) for l in L]
+        self.dW = [torch.empty((l.k, C[l.index], 3, 3), dtype=torch.float32, device=dev)
+                   for l in L]
         self.db = [torch.empty((l.k,), dtype=torch.float32, device=dev) for l in L]
-        self.desc = [sb.conv_desc(n, l.c, l.h, l.w, l.k, self.code, relu=not l.pool_after)
-                     for l in L]
-        self.desc_b = [sb.conv_desc(n, l.c, l.h, l.w, l.k, self.code) for l in L]
+        self.desc = [sb.conv_desc(n, C[l.index], l.h, l.w, l.k, self.code, relu=not l.pool_after,
+                                  layout=lay) for l in L]
+        self.desc_b = [sb.conv_desc(n, C[l.index], l.h, l.w, l.k, self.code, layout=lay)
+                       for l in L]
         # packed: every layer's filters are packed for the forward and the
         # data-gradient pass in one launch at the start of the step
         # (sb_conv3x3_pack_filters_many), and the passes take them with
@@ -116,10 +133,11 @@ class ConvStack:
         self.pdesc = self.desc
         self.pdesc_b = self.desc_b
         if packed:
-            self.pdesc = [sb.conv_desc(n, l.c, l.h, l.w, l.k, self.code, relu=not l.pool_after,
-                                       packed=True) for l in L]
-            self.pdesc_b = [sb.conv_desc(n, l.c, l.h, l.w, l.k, self.code, packed=True)
-                            for l in L]
+            self.pdesc = [sb.conv_desc(n, C[l.index], l.h, l.w, l.k, self.code,
+                                       relu=not l.pool_after, packed=True, layout=lay)
+                          for l in L]
+            self.pdesc_b = [sb.conv_desc(n, C[l.index], l.h, l.w, l.k, self.code, packed=True,
+                                         layout=lay) for l in L]
 
             def buf(i, pass_):
                 nb = sb.sb_conv3x3_packed_bytes(self.desc_b[i], pass_)
@@ -148,19 +166,45 @@ class ConvStack:
             self.side = torch.cuda.Stream(device=dev)     # default priority
         self.call = _plain      # hook: every libsb call of the step goes through it
 
+    # -- layouts -----------------------------------------------------------------
+    def shape_of(self, n, c, h, w):
+        """Buffer shape of an activation of c channels in this stack's layout."""
+        return (n, c // 8, h, w, 8) if self.c8 else (n, c, h, w)
+
+    def to_layout(self, a, c=None):
+        """A host NCHW array or tensor as a CPU tensor in this stack's layout
+        (channels zero-padded to c)."""
+        t = a if isinstance(a, torch.Tensor) else torch.from_numpy(np.ascontiguousarray(a))
+        if not self.c8:
+            return t
+        n, ch, h, w = t.shape
+        c = c or ch
+        if c != ch:
+            t = torch.cat([t, torch.zeros((n, c - ch, h, w), dtype=t.dtype)], dim=1)
+        return t.reshape(n, c // 8, 8, h, w).permute(0, 1, 3, 4, 2).contiguous()
+
+    def nchw(self, t):
+        """A device buffer of this stack as an NCHW tensor (a copy for c8)."""
+        if not self.c8:
+            return t
+        n, cb, h, w, e = t.shape
+        return t.permute(0, 1, 4, 2, 3).reshape(n, cb * e, h, w)
+
     # -- data placement (host -> device copies of seeded inputs) --------------
     def load_inputs(self, x, weights, biases=None, dy_top=None):
-        def put(dst, src):
-            t = src if isinstance(src, torch.Tensor) else torch.from_numpy(np.ascontiguousarray(src))
+        def put(dst, t):
             dst.copy_(t.to(dst.dtype) if t.dtype != dst.dtype else t)
-        put(self.A[0], x)
+        put(self.A[0], self.to_layout(x, self.cin[0]))
         for l, w in enumerate(weights):
-            put(self.W[l], w)
+            t = w if isinstance(w, torch.Tensor) else torch.from_numpy(np.ascontiguousarray(w))
+            self.W[l].zero_()
+            self.W[l][:, :t.shape[1]].copy_(t.to(self.W[l].dtype))
         if biases is not None:
             for l, b in enumerate(biases):
-                put(self.b[l], b)
+                t = b if isinstance(b, torch.Tensor) else torch.from_numpy(np.ascontiguousarray(b))
+                put(self.b[l], t)
         if dy_top is not None:
-            put(self.gA[-1], dy_top)
+            put(self.gA[-1], self.to_layout(dy_top))
 
     # -- the step ---------------------------------------------------------------
     def forward(self, stream=None):
@@ -174,7 +218,7 @@ class ConvStack:
                 c(("fwd", i), sb.sb_conv3x3_fwd, self.pdesc[i], self.A[i], w, self.b[i],
                   self.Z[i], self.ws, stream)
                 c(("pool_fwd", i), sb.sb_relu_maxpool_fwd, self.n, l.k, l.h, l.w, self.code,
-                  self.Z[i], self.A[i + 1], self.idx[i], stream)
+                  self.layout, self.Z[i], self.A[i + 1], self.idx[i], stream)
             else:
                 c(("fwd", i), sb.sb_conv3x3_fwd, self.pdesc[i], self.A[i], w, self.b[i],
                   self.A[i + 1], self.ws, stream)
@@ -193,7 +237,7 @@ class ConvStack:
             i = l.index
             if l.pool_after:
                 c(("pool_bwd", i), sb.sb_relu_maxpool_bwd, self.n, l.k, l.h, l.w, self.code,
-                  self.gA[i + 1], self.idx[i], self.dZ[i], stream)
+                  self.layout, self.gA[i + 1], self.idx[i], self.dZ[i], stream)
                 g = self.dZ[i]
             else:
                 g = self.gA[i + 1]

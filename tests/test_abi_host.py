@@ -76,13 +76,17 @@ def test_conv_workspace_is_checked_before_launch():
 
 def test_pool_argument_validation():
     for shape in [(0, 1, 2, 2), (1, 1, 3, 2), (1, 1, 2, 5), (1, -2, 2, 2)]:
-        assert _raw("sb_relu_maxpool_fwd", *shape, 0, P, P + 4096, P + 8192, None) == sb.SB_ERR_INVALID_ARG
-        assert _raw("sb_relu_maxpool_bwd", *shape, 0, P, P + 4096, P + 8192, None) == sb.SB_ERR_INVALID_ARG
-    assert _raw("sb_relu_maxpool_fwd", 1, 1, 2, 2, 5, P, P + 4096, P + 8192, None) == sb.SB_ERR_INVALID_ARG
-    assert _raw("sb_relu_maxpool_fwd", 1, 1, 2, 2, 0, None, P + 4096, P + 8192, None) == sb.SB_ERR_INVALID_ARG
+        assert _raw("sb_relu_maxpool_fwd", *shape, 0, 0, P, P + 4096, P + 8192, None) == sb.SB_ERR_INVALID_ARG
+        assert _raw("sb_relu_maxpool_bwd", *shape, 0, 0, P, P + 4096, P + 8192, None) == sb.SB_ERR_INVALID_ARG
+    assert _raw("sb_relu_maxpool_fwd", 1, 1, 2, 2, 5, 0, P, P + 4096, P + 8192, None) == sb.SB_ERR_INVALID_ARG
+    assert _raw("sb_relu_maxpool_fwd", 1, 1, 2, 2, 0, 0, None, P + 4096, P + 8192, None) == sb.SB_ERR_INVALID_ARG
     # Output aliasing the input.
-    assert _raw("sb_relu_maxpool_fwd", 1, 4, 4, 4, 0, P, P + 8, P + 8192, None) == sb.SB_ERR_INVALID_ARG
-    assert _raw("sb_relu_maxpool_bwd", 1, 4, 4, 4, 0, P, P + 8192, P + 16, None) == sb.SB_ERR_INVALID_ARG
+    assert _raw("sb_relu_maxpool_fwd", 1, 4, 4, 4, 0, 0, P, P + 8, P + 8192, None) == sb.SB_ERR_INVALID_ARG
+    assert _raw("sb_relu_maxpool_bwd", 1, 4, 4, 4, 0, 0, P, P + 8192, P + 16, None) == sb.SB_ERR_INVALID_ARG
+    # Bad layout; channel-blocked needs whole 8-channel blocks.
+    assert _raw("sb_relu_maxpool_fwd", 1, 8, 4, 4, 1, 2, P, P + 8192, P + 16384, None) == sb.SB_ERR_INVALID_ARG
+    assert _raw("sb_relu_maxpool_fwd", 1, 12, 4, 4, 1, 1, P, P + 8192, P + 16384, None) == sb.SB_ERR_INVALID_ARG
+    assert _raw("sb_relu_maxpool_bwd", 1, 12, 4, 4, 1, 1, P, P + 8192, P + 16384, None) == sb.SB_ERR_INVALID_ARG
 
 
 def test_fc_argument_validation():
@@ -261,9 +265,10 @@ def test_pack_many_rejects_packing_over_another_tasks_filters():
 
 
 def test_fc_workspace_must_not_overlap_operands():
-    d = sb.fc_desc(512, 4096, 1024)            # 32 output tiles: the reduction is split
+    d = sb.fc_desc(512, 4096, 1024)            # few output tiles: the forward is split
+    d2 = sb.fc_desc(4096, 64, 64)              # a 64 x 64 weight gradient over 4096 rows: split
     need_f = sb.sb_fc_workspace_bytes(d, sb.SB_FC_FWD)
-    need_b = sb.sb_fc_workspace_bytes(d, sb.SB_FC_BWD)
+    need_b = sb.sb_fc_workspace_bytes(d2, sb.SB_FC_BWD)
     assert need_f > 0 and need_b > 0
     x, w, y = P, P + (16 << 20), P + (96 << 20)
     ws = P + (128 << 20)
@@ -273,7 +278,7 @@ def test_fc_workspace_must_not_overlap_operands():
     assert fwd(y - 1024) == sb.SB_ERR_INVALID_ARG        # over y
     dy, dx, dw = P + (200 << 20), P + (240 << 20), P + (300 << 20)
     ws = P + (400 << 20)
-    bwd = lambda ws_: _raw("sb_fc_shard_bwd", ctypes.byref(d), x, w, dy, None, dx, dw, None, 0,
+    bwd = lambda ws_: _raw("sb_fc_shard_bwd", ctypes.byref(d2), x, w, dy, None, dx, dw, None, 0,
                            ws_, need_b, None)
     for bad in (x, w, dy, dx, dw):
         assert bwd(bad + 256) == sb.SB_ERR_INVALID_ARG
@@ -305,3 +310,23 @@ def test_noalloc_weight_gradient_validation():
         for L in configs.conv_layers(configs.VGG16, 3, hw):
             q = sb.conv_desc(n, L.c, L.h, L.w, L.k, dt)
             assert sb.sb_conv3x3_workspace_bytes(q, 2) <= sb.SB_NOALLOC_SCRATCH_BYTES
+
+
+def test_channel_blocked_layout_validation():
+    """SB_NCHW8C: bf16 only (fp32 is unsupported), whole 8-channel blocks,
+    images at least 8 wide; an unknown layout is rejected."""
+    ok = sb.conv_desc(2, 16, 16, 16, 32, sb.SB_BF16, layout=sb.SB_NCHW8C)
+    for p in range(3):
+        assert sb.sb_conv3x3_workspace_bytes(ok, p) != 2 ** 64 - 1
+        assert "c8" in sb.sb_conv3x3_plan_string(ok, p)
+    bad_layout = sb.conv_desc(2, 16, 16, 16, 32, sb.SB_BF16, layout=3)
+    ragged = sb.conv_desc(2, 12, 16, 16, 32, sb.SB_BF16, layout=sb.SB_NCHW8C)
+    f32 = sb.conv_desc(2, 16, 16, 16, 32, sb.SB_F32, layout=sb.SB_NCHW8C)
+    narrow = sb.conv_desc(2, 16, 4, 4, 32, sb.SB_BF16, layout=sb.SB_NCHW8C)
+    x, w, y = P, P + (1 << 20), P + (2 << 20)
+    for d, status in ((bad_layout, sb.SB_ERR_INVALID_ARG), (ragged, sb.SB_ERR_INVALID_ARG),
+                      (f32, sb.SB_ERR_UNSUPPORTED), (narrow, sb.SB_ERR_UNSUPPORTED)):
+        assert _raw("sb_conv3x3_fwd", ctypes.byref(d), x, w, None, y, None, 0, None) == status
+        assert _raw("sb_conv3x3_bwd_weight", ctypes.byref(d), x, y, P + (3 << 20), None, None, 0,
+                    None) == status
+        assert sb.sb_conv3x3_workspace_bytes(d, 0) == 2 ** 64 - 1

@@ -38,8 +38,8 @@ def test_relu_maxpool_fwd_bwd(shape, dtype):
     idx = torch.empty((n, c, h // 2, w // 2), dtype=torch.uint8, device="cuda")
     dx = torch.full(shape, 7.0, dtype=tdt, device="cuda")          # must be overwritten
     code = sb.SB_F32 if dtype == "f32" else sb.SB_BF16
-    sb.sb_relu_maxpool_fwd(n, c, h, w, code, xd, y, idx)
-    sb.sb_relu_maxpool_bwd(n, c, h, w, code, dyd, idx, dx)
+    sb.sb_relu_maxpool_fwd(n, c, h, w, code, sb.SB_NCHW, xd, y, idx)
+    sb.sb_relu_maxpool_bwd(n, c, h, w, code, sb.SB_NCHW, dyd, idx, dx)
     torch.cuda.synchronize()
     y_ref, idx_ref = O.relu_maxpool_fwd(xd.cpu())
     np.testing.assert_array_equal(idx.cpu().numpy(), idx_ref)
@@ -55,7 +55,7 @@ def test_relu_maxpool_constructed_ties():
     xd = to_dev(x)
     y = torch.empty((1, 1, 1, 5), device="cuda")
     idx = torch.empty((1, 1, 1, 5), dtype=torch.uint8, device="cuda")
-    sb.sb_relu_maxpool_fwd(1, 1, 2, 10, sb.SB_F32, xd, y, idx)
+    sb.sb_relu_maxpool_fwd(1, 1, 2, 10, sb.SB_F32, sb.SB_NCHW, xd, y, idx)
     torch.cuda.synchronize()
     np.testing.assert_array_equal(idx.cpu().numpy().ravel(), [0, 1, 0x81, 0x80, 2])
     np.testing.assert_array_equal(y.cpu().numpy().ravel(), np.float32([1.0, 0.7, 0.0, 0.0, 5.0]))
