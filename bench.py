@@ -196,16 +196,17 @@ class Workload:
 
 
 class VggWorkload(Workload):
-    def __init__(self, name, batch, hw, dtype, metric, text):
+    def __init__(self, name, batch, hw, dtype, metric, text, layout="nchw"):
         self.name, self.n, self.hw, self.dtype = name, batch, hw, dtype
         self.metric, self.text, self.images = metric, text, batch
         self.top = hw // 32
+        self.layout = layout
 
     def build(self):
         from paper_2112_15317_amd import configs
         from paper_2112_15317_amd.stack import ConvStack
         self.layers, x, ws, _, dy = vgg_inputs(self.n, self.hw, self.top)
-        self.st = ConvStack(configs.VGG16, self.n, 3, self.hw, self.dtype)
+        self.st = ConvStack(configs.VGG16, self.n, 3, self.hw, self.dtype, layout=self.layout)
         self.st.load_inputs(x, ws, None, dy)
         return self.st.step_calls()
 
@@ -525,13 +526,13 @@ def workloads():
         "vgg16-cifar-f32": VggWorkload(
             "vgg16-cifar-f32", 128, 32, "f32", CIFAR_METRIC,
             "VGG-16 CIFAR conv stack fwd+bwd (13 conv, 5 relu+maxpool), batch 128, 3x32x32, "
-            "fp32, NCHW"),
+            "fp32"),
         "vgg16-imagenet-bf16": VggWorkload(
             "vgg16-imagenet-bf16", 32, 224, "bf16",
             "images/sec/GPU VGG-16 ImageNet-shaped conv fwd+bwd (bf16); achieved TFLOP/s vs "
             "MFMA peak",
             "VGG-16 ImageNet-shaped conv stack fwd+bwd (13 conv, 5 relu+maxpool), batch 32, "
-            "3x224x224, bf16 activations and filters, fp32 accumulation, NCHW"),
+            "3x224x224, bf16 activations and filters, fp32 accumulation", layout="c8"),
         "fc-shard-f32": FcWorkload(),
         "hybrid-f32": HybridWorkload(
             "hybrid-f32", configs.VGG16, HYBRID_FC, 4,
@@ -577,6 +578,8 @@ def kernel_name(key, call_args, dtype):
         return "sb::sgd_update_kernel"
     if kind == "avg":
         return "sb::model_average_kernel<4>"
+    if call_args[5] == sb.SB_NCHW8C:
+        return "sb::relu_maxpool_%s_c8" % kind.split("_")[1]
     return "sb::relu_maxpool_%s_kernel<%s, 2>" % (
         kind.split("_")[1], "float" if dtype == "f32" else "unsigned short")
 
@@ -607,6 +610,8 @@ def main():
     ap.add_argument("--cpu-sample", type=int, default=None,
                     help="images (rows for the FC shard) the oracle times")
     ap.add_argument("--profile-pass", action="store_true")
+    ap.add_argument("--layout", choices=["nchw", "c8"], default=None,
+                    help="activation layout of a VGG stack (default: the workload's)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: this library has no multi-GPU path "
@@ -617,6 +622,10 @@ def main():
     from paper_2112_15317_amd.stack import capture_graph
 
     wl = W[args.workload]
+    if args.layout is not None:
+        if not isinstance(wl, VggWorkload):
+            ap.error("--layout applies to the VGG stack workloads")
+        wl.layout = args.layout
     dtype = wl.dtype
     torch.cuda.set_device(0)
     K = args.steps
@@ -730,8 +739,9 @@ def main():
         "ms_per_step": round(ms, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": dtype, "data": "synthetic",
-        "config": {"workload": wl.text, "global_batch": wl.images or FC_SHAPE[0],
-                   "parallelism": "none (1 GPU)"},
+        "config": dict({"workload": wl.text, "global_batch": wl.images or FC_SHAPE[0],
+                        "parallelism": "none (1 GPU)"},
+                       **({"layout": wl.layout} if isinstance(wl, VggWorkload) else {})),
         "launch": "HIP graph of %d steps" % K,
         "tflops_nominal": None if moved else round(tf_nom, 2),
         "tflops_valid_tap": None if moved else round(tf_valid, 2),

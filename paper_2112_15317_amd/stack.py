@@ -83,6 +83,8 @@ class ConvStack:
             raise ValueError("the stack must end with a pooled layer")
         if layout not in ("nchw", "c8") or (layout == "c8" and dtype != "bf16"):
             raise ValueError("layout 'c8' is for bf16 stacks")
+        if layout == "c8" and min(l.w for l in self.layers) < 8:
+            raise ValueError("layout 'c8' needs images at least 8 wide at every layer")
         self.n, self.dtype = n, dtype
         self.code = _code(dtype)
         self.c8 = layout == "c8"

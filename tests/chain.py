@@ -28,9 +28,40 @@ def put(buf, arr):
     buf.copy_(t.to(buf.dtype))
 
 
+def in_layout(st, buf, arr):
+    """An NCHW oracle array in the layout and shape of one of st's buffers:
+    channel-blocked for an activation of a c8 stack, and zero-padded along
+    the channels where the stack pads them (the first layer's input, its
+    data gradient and its filters' gradient)."""
+    arr = np.asarray(arr)
+    if tuple(arr.shape) == tuple(buf.shape):
+        return arr
+    if buf.dim() == 5:
+        return st.to_layout(torch.from_numpy(np.ascontiguousarray(arr)),
+                            buf.shape[1] * buf.shape[4]).numpy()
+    pad = [(0, 0)] * arr.ndim
+    pad[1] = (0, buf.shape[1] - arr.shape[1])
+    return np.pad(arr, pad)
+
+
+def host_nchw(st, buf, ref_shape):
+    """A buffer of st on the host as NCHW, cut to the oracle's channels."""
+    got = to_host(st.nchw(buf) if buf.dim() == 5 else buf)
+    if got.ndim > 1 and got.shape[1] != ref_shape[1]:
+        got = got[:, :ref_shape[1]]
+    return got
+
+
 def conv_io(st, f, b, key):
-    """(uploads, checks) of one ConvStack call on the oracle chain (f, b).
+    """(uploads, checks) of one ConvStack call on the oracle chain (f, b),
+    every array already in the buffer's layout.
     uploads: [(buffer, host array)]; checks: [(name, buffer, ref, tol|EXACT)]."""
+    ups, checks = _conv_io(st, f, b, key)
+    return ([(buf, in_layout(st, buf, a)) for buf, a in ups],
+            [(name, buf, in_layout(st, buf, r), t) for name, buf, r, t in checks])
+
+
+def _conv_io(st, f, b, key):
     kind, i = key
     L = st.layers
     pool = L[i].pool_after if kind != "pack" else False

@@ -1,7 +1,10 @@
 """GPU parity of the ImageNet-shaped VGG-16 step in bf16 (batch 32 at
-224x224, bf16 activations and filters, fp32 accumulation), every call in
+224x224, bf16 activations and filters, fp32 accumulation, channel-blocked
+activations with the input's 3 channels zero-padded to 8), every call in
 full, with the benchmark's seeded inputs (see tests/test_gpu_full_size.py
-for the method).
+for the method).  Oracle arrays are laid out (and padded) like the stack's
+buffers before they are uploaded or compared, so the padding is checked
+too: the padded channels' data and filter gradients must be zero.
 
 Per call, on the oracle's chain rounded to bf16 at the GPU's storage points:
 pool codes and routed gradients bit for bit, bf16 outputs within relative L2
@@ -26,8 +29,8 @@ import oracle as O
 from oracle import stack as OS
 from paper_2112_15317_amd import configs
 from paper_2112_15317_amd.stack import ConvStack
-from tests.chain import conv_io, near_tie_flips, run_and_check
-from tests.helpers import TOL, print_case, rel_l2, to_host
+from tests.chain import conv_io, host_nchw, near_tie_flips, run_and_check
+from tests.helpers import TOL, print_case, rel_l2
 from tests.test_gpu_full_size import _id, bench_vgg_inputs, stack_keys
 
 pytestmark = pytest.mark.gpu
@@ -43,7 +46,7 @@ def cfg5():
     xb, wsb, dyb = O.round_bf16(x), [O.round_bf16(w) for w in ws], O.round_bf16(dy)
     pools = [L.pool_after for L in LAYERS]
     f, b = OS.vgg_step(xb, wsb, bs, pools, dyb, store="bf16")
-    st = ConvStack(configs.VGG16, N, 3, HW, "bf16")
+    st = ConvStack(configs.VGG16, N, 3, HW, "bf16", layout="c8")
     st.load_inputs(x, ws, bs, dy)            # rounded to bf16 on the way in
     calls = {c[0]: c for c in st.step_calls()}
     run_and_check(calls[("pack", 0)], [], [])
@@ -70,10 +73,11 @@ def test_vgg16_imagenet_bf16_step_end_to_end(cfg5):
         i = L.index
         if L.pool_after:
             z = f["Z"][i]
-            assert rel_l2(to_host(st.Z[i]), z) <= tol, "Z%d" % i
-            flips[i] = near_tie_flips(z, f["idx"][i], st.idx[i].cpu().numpy(),
+            assert rel_l2(host_nchw(st, st.Z[i], z.shape), z) <= tol, "Z%d" % i
+            flips[i] = near_tie_flips(z, f["idx"][i], host_nchw(st, st.idx[i], z.shape),
                                       2.0 ** -6 * np.max(np.abs(z)))
-        assert rel_l2(to_host(st.A[i + 1]), f["A"][i + 1]) <= tol, "A%d" % (i + 1)
+        a = f["A"][i + 1]
+        assert rel_l2(host_nchw(st, st.A[i + 1], a.shape), a) <= tol, "A%d" % (i + 1)
     deepest = max([i for i, c in flips.items() if c] or [-1])
     report = {"near_tie_windows": flips}
     for L in st.layers:
@@ -81,11 +85,11 @@ def test_vgg16_imagenet_bf16_step_end_to_end(cfg5):
         for name, buf, ref, t in [("dZ%d" % i, st.grad_at_conv_output(i), b["dZ"][i], tol),
                                   ("dW%d" % i, st.dW[i], b["dW"][i], tol),
                                   ("db%d" % i, st.db[i], b["db"][i], tol)]:
-            got = to_host(buf)
+            got = host_nchw(st, buf, ref.shape)
             e = rel_l2(got, ref)
             report[name] = round(e, 5)
             assert np.all(np.isfinite(got)), name
             if i > deepest:
                 assert e <= t, "%s: %.3g" % (name, e)
-    report["dX"] = round(rel_l2(to_host(st.gA[0]), b["dX"]), 5)
+    report["dX"] = round(rel_l2(host_nchw(st, st.gA[0], b["dX"].shape), b["dX"]), 5)
     print(report)

@@ -43,25 +43,27 @@ def test_vgg16_cifar_stack_end_to_end():
 
 
 def test_vgg16_imagenet_bf16_stack_full_size_properties():
-    """The whole ImageNet-shaped bf16 stack (batch 32, 224x224) through one
-    step: every pool output and code is consistent with the stored
-    pre-activation (y = max(0, window max), first maximum, ReLU flag), the
-    un-pooled gradient routes exactly, and every gradient is finite."""
+    """The whole ImageNet-shaped bf16 stack (batch 32, 224x224, the
+    benchmark's channel-blocked layout) through one step: every pool output
+    and code is consistent with the stored pre-activation (y = max(0, window
+    max), first maximum, ReLU flag), the un-pooled gradient routes exactly,
+    and every gradient is finite."""
     n, hw = 32, 224
     print_case("vgg16_imagenet_bf16_stack", n=n, hw=hw)
     layers = configs.conv_layers(configs.VGG16, 3, hw)
     x, wts, bs = _vgg_inputs(n, hw, 21, layers)
     dy_top = synth.normal((n, 512, 7, 7), 21, synth.TID.DY_TOP)
-    st = ConvStack(configs.VGG16, n, 3, hw, "bf16")
+    st = ConvStack(configs.VGG16, n, 3, hw, "bf16", layout="c8")
     st.load_inputs(x, wts, bs, dy_top)
     st.step()
     torch.cuda.synchronize()
+    nchw = st.nchw
     for L in layers:
         i = L.index
         assert torch.isfinite(st.dW[i]).all() and torch.isfinite(st.db[i]).all(), "dW%d" % i
         if not L.pool_after:
             continue
-        z = st.Z[i].float()
+        z = nchw(st.Z[i]).float()
         nn_, c, h, w = z.shape
         win = z.reshape(nn_, c, h // 2, 2, w // 2, 2).permute(0, 1, 2, 4, 3, 5).reshape(
             nn_, c, h // 2, w // 2, 4)
@@ -69,14 +71,15 @@ def test_vgg16_imagenet_bf16_stack_full_size_properties():
         is_max = win == mx.unsqueeze(-1)
         first = torch.argmax(is_max.to(torch.float32), dim=-1)
         code = first.to(torch.uint8) | ((mx <= 0).to(torch.uint8) << 7)
-        assert torch.equal(st.idx[i], code), "pool code %d" % i
-        assert torch.equal(st.A[i + 1].float(), torch.clamp(mx, min=0)), "pool value %d" % i
+        assert torch.equal(nchw(st.idx[i]), code), "pool code %d" % i
+        assert torch.equal(nchw(st.A[i + 1]).float(), torch.clamp(mx, min=0)), \
+            "pool value %d" % i
         del win, is_max, z
-        g = st.gA[i + 1].float().unsqueeze(-1)
+        g = nchw(st.gA[i + 1]).float().unsqueeze(-1)
         sel = (torch.arange(4, device=g.device) == first.unsqueeze(-1)) & (mx > 0).unsqueeze(-1)
         dz = torch.where(sel, g, torch.zeros_like(g)).reshape(nn_, c, h // 2, w // 2, 2, 2)
         dz = dz.permute(0, 1, 2, 4, 3, 5).reshape(nn_, c, h, w)
-        assert torch.equal(st.dZ[i].float(), dz), "pool gradient routing %d" % i
+        assert torch.equal(nchw(st.dZ[i]).float(), dz), "pool gradient routing %d" % i
         del g, sel, dz
 
 
@@ -244,19 +247,28 @@ def test_graph_replay_matches_eager():
             assert torch.equal(a, b), "replay %d differs from the eager step" % rep
 
 
-@pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_overlapped_backward_matches_single_stream(dtype):
+LAYOUTS = [("f32", "nchw"), ("bf16", "nchw"), ("bf16", "c8")]
+
+
+def _small(layout):
+    """(batch, image size) of the small-stack tests: the channel-blocked
+    kernels need images at least 8 wide, so 128x128 (deepest layer 8x8)."""
+    return (2, 128) if layout == "c8" else (4, 32)
+
+
+@pytest.mark.parametrize("dtype,layout", LAYOUTS)
+def test_overlapped_backward_matches_single_stream(dtype, layout):
     """The weight gradients run on a second stream beside the data-gradient
     chain; eagerly on a non-default torch stream and replayed from a graph,
     the step must equal, bit for bit, the same step on one stream."""
     from paper_2112_15317_amd.stack import capture_graph
-    n, hw = 4, 32
-    print_case("overlapped_backward", n=n, hw=hw, dtype=dtype)
+    n, hw = _small(layout)
+    print_case("overlapped_backward", n=n, hw=hw, dtype=dtype, layout=layout)
     layers = configs.conv_layers(configs.VGG16, 3, hw)
     x, wts, bs = _vgg_inputs(n, hw, 10, layers)
-    dy_top = synth.normal((n, 512, 1, 1), 10, synth.TID.DY_TOP)
-    one = ConvStack(configs.VGG16, n, 3, hw, dtype, overlap=False)
-    two = ConvStack(configs.VGG16, n, 3, hw, dtype, overlap=True)
+    dy_top = synth.normal((n, 512, hw // 32, hw // 32), 10, synth.TID.DY_TOP)
+    one = ConvStack(configs.VGG16, n, 3, hw, dtype, overlap=False, layout=layout)
+    two = ConvStack(configs.VGG16, n, 3, hw, dtype, overlap=True, layout=layout)
     for st in (one, two):
         st.load_inputs(x, wts, bs, dy_top)
     one.step()
@@ -283,19 +295,19 @@ def test_overlapped_backward_matches_single_stream(dtype):
             assert torch.equal(a, b), "replay %d of the overlapped step differs" % rep
 
 
-@pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_packed_filter_step_matches_unpacked(dtype):
+@pytest.mark.parametrize("dtype,layout", LAYOUTS)
+def test_packed_filter_step_matches_unpacked(dtype, layout):
     """The stack packs every layer's filters once per step on a side stream
     (SB_PACKED_FILTERS); the step must equal, bit for bit, a stack whose
     calls pack their filters themselves."""
-    n, hw = 4, 32
-    print_case("packed_step", n=n, hw=hw, dtype=dtype)
+    n, hw = _small(layout)
+    print_case("packed_step", n=n, hw=hw, dtype=dtype, layout=layout)
     layers = configs.conv_layers(configs.VGG16, 3, hw)
     x, wts, bs = _vgg_inputs(n, hw, 10, layers)
-    dy_top = synth.normal((n, 512, 1, 1), 10, synth.TID.DY_TOP)
+    dy_top = synth.normal((n, 512, hw // 32, hw // 32), 10, synth.TID.DY_TOP)
     outs = []
     for packed in (True, False):
-        st = ConvStack(configs.VGG16, n, 3, hw, dtype, packed=packed)
+        st = ConvStack(configs.VGG16, n, 3, hw, dtype, packed=packed, layout=layout)
         st.load_inputs(x, wts, bs, dy_top)
         st.step()
         torch.cuda.synchronize()
