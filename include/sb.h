@@ -365,6 +365,20 @@ sb_status sb_shard_bwd(const sb_shard_desc *desc, int iproc,
 sb_status sb_model_average(int workers, int mp, size_t n, float *params,
                            size_t stride, void *stream);
 
+/* Model averaging of replicas in separate buffers (the same reduce as
+ * sb_model_average, sec. 2 and sec. 4, for replicas that do not share one
+ * slotted allocation: one call per parameter tensor, with the tensor of
+ * every replica, e.g. a conv layer's filters in every MP group, or FC shard
+ * r of every group).  params is a HOST array of `replicas` device pointers,
+ * each to n fp32 elements; every one is replaced, in place, by the mean
+ * over the replicas (the sum in increasing replica index, divided once by
+ * the count).  1 <= replicas <= SB_MAX_REPLICAS; the pointers must be
+ * non-NULL and their ranges must not overlap (SB_ERR_INVALID_ARG).  n = 0
+ * or a single replica does nothing. */
+#define SB_MAX_REPLICAS 64
+sb_status sb_model_average_replicas(int replicas, size_t n, float *const *params,
+                                    void *stream);
+
 /* ------------------------------------------------------------------------
  * Loss and parameter update (NEXT after the worker's forward and backward).
  *

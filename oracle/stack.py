@@ -28,6 +28,7 @@ import numpy as np
 
 from . import (_f64, conv3x3_bwd_data, conv3x3_bwd_weight, conv3x3_fwd,
                fc_bwd, fc_fwd, relu_maxpool_bwd, relu_maxpool_fwd, round_bf16, round_f32)
+from .average import model_average
 from .modulo import modulo_bwd, modulo_fwd, shard_bwd, shard_fwd
 from .train import log_softmax_nll, sgd_update
 
@@ -238,3 +239,41 @@ def group_train_step(x, weights, biases, pool_after, fc_w, fc_b, local_remote, l
             "fc_w_new": W, "fc_b_new": bvec,
             "conv_w_new": [sgd_update(w, b["dW"][i], lr, 1.0) for i, w in enumerate(weights)],
             "conv_b_new": [sgd_update(bb, b["db"][i], lr, 1.0) for i, bb in enumerate(biases)]}
+
+
+def averaged_group_training(groups, weights, biases, pool_after, fc_w, fc_b, steps, period,
+                            lr):
+    """Training of G MP groups that start from the same model and average it
+    every ``period`` steps (sec. 4: the workers exchange the parameters up to
+    the modulo layer every few batches, and the FC shards are averaged
+    across the MP groups; sec. 2: the reduce is the mean of the replicas).
+
+    ``groups[g]`` = (x, local_remote, labels): group g's inputs, the same at
+    every step (one fixed synthetic batch per group).  Each step runs
+    ``group_train_step`` in every group on that group's parameters; after
+    steps period, 2 period, ... every parameter tensor (each conv layer's
+    filters and bias, each FC layer as the full matrix: its shard r in every
+    group is averaged with shard r of the others) is replaced in every group
+    by the mean over the groups, in increasing group index.  Returns the
+    per-group parameters after ``steps`` steps: a list of dicts with
+    ``conv_w``, ``conv_b``, ``fc_w``, ``fc_b``.
+    """
+    G = len(groups)
+    state = [{"conv_w": [np.array(w, np.float64) for w in weights],
+              "conv_b": [np.array(b, np.float64) for b in biases],
+              "fc_w": [np.array(w, np.float64) for w in fc_w],
+              "fc_b": [np.array(b, np.float64) for b in fc_b]} for _ in range(G)]
+    for s in range(steps):
+        for g, (x, remote, labels) in enumerate(groups):
+            p = state[g]
+            r = group_train_step(x, p["conv_w"], p["conv_b"], pool_after, p["fc_w"], p["fc_b"],
+                                 remote, labels, lr)
+            state[g] = {"conv_w": r["conv_w_new"], "conv_b": r["conv_b_new"],
+                        "fc_w": r["fc_w_new"], "fc_b": r["fc_b_new"]}
+        if (s + 1) % period == 0:
+            for key in ("conv_w", "conv_b", "fc_w", "fc_b"):
+                for i in range(len(state[0][key])):
+                    mean = model_average(np.stack([state[g][key][i] for g in range(G)]), 1)
+                    for g in range(G):
+                        state[g][key][i] = mean[g]
+    return state

@@ -119,6 +119,31 @@ __global__ __launch_bounds__(256) void model_average_kernel(float* __restrict__ 
   for (int g = 0; g < groups; ++g) st<V>(base + g * step, acc);
 }
 
+// Model averaging of replicas held in separate buffers: the n elements of
+// every replica are replaced by their mean (sum in increasing replica id,
+// one division).  The replica pointers travel in the kernel arguments.
+struct ReplicaSet {
+  float* p[SB_MAX_REPLICAS];
+};
+
+template <int V>
+__global__ __launch_bounds__(256) void replica_average_kernel(ReplicaSet rs, int replicas,
+                                                              size_t total) {
+  const size_t q = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (q >= total) return;
+  const size_t e = q * V;
+  typename VecOf<V>::T acc = ld<V>(rs.p[0] + e);
+  for (int g = 1; g < replicas; ++g) acc += ld<V>(rs.p[g] + e);
+  const float cnt = (float)replicas;
+  if constexpr (V == 1) {
+    acc = acc / cnt;
+  } else {
+#pragma unroll
+    for (int j = 0; j < V; ++j) acc[j] = acc[j] / cnt;
+  }
+  for (int g = 0; g < replicas; ++g) st<V>(rs.p[g] + e, acc);
+}
+
 }  // namespace sb
 
 using namespace sb;
@@ -259,5 +284,31 @@ extern "C" sb_status sb_model_average(int workers, int mp, size_t n, float* para
     model_average_kernel<1><<<blocks_for(total), 256, 0, st>>>(params, stride, mp, groups, n,
                                                                total);
   }
+  return sbh::launch_status();
+}
+
+extern "C" sb_status sb_model_average_replicas(int replicas, size_t n, float* const* params,
+                                               void* stream) {
+  if (replicas < 1 || replicas > SB_MAX_REPLICAS || !params) return SB_ERR_INVALID_ARG;
+  for (int g = 0; g < replicas; ++g)
+    if (!params[g]) return SB_ERR_INVALID_ARG;
+  if (n == 0) return SB_OK;
+  if (n >= (1ull << 40)) return SB_ERR_UNSUPPORTED;
+  const size_t bytes = n * sizeof(float);
+  for (int g = 0; g < replicas; ++g)
+    for (int h = g + 1; h < replicas; ++h)
+      if (sbh::overlaps(params[g], bytes, params[h], bytes)) return SB_ERR_INVALID_ARG;
+  if (replicas == 1) return SB_OK;                // one replica: already its own mean
+  ReplicaSet rs{};
+  bool v4 = n % 4 == 0;
+  for (int g = 0; g < replicas; ++g) {
+    rs.p[g] = params[g];
+    v4 = v4 && aligned16(params[g]);
+  }
+  hipStream_t st = sbh::stream_of(stream);
+  if (v4)
+    replica_average_kernel<4><<<blocks_for(n / 4), 256, 0, st>>>(rs, replicas, n / 4);
+  else
+    replica_average_kernel<1><<<blocks_for(n), 256, 0, st>>>(rs, replicas, n);
   return sbh::launch_status();
 }

@@ -79,6 +79,7 @@ SIGNATURES = {
     "sb_shard_fwd": (_i, [ctypes.POINTER(sb_shard_desc), _i, _vp, _sz, _vp, _vp]),
     "sb_shard_bwd": (_i, [ctypes.POINTER(sb_shard_desc), _i, _vp, _sz, _vp, _sz, _vp]),
     "sb_model_average": (_i, [_i, _i, _sz, _vp, _sz, _vp]),
+    "sb_model_average_replicas": (_i, [_i, _sz, ctypes.POINTER(_vp), _vp]),
     "sb_log_softmax_nll": (_i, [_i, _i, _i, _vp, _vp, ctypes.c_float, _vp, _vp, _vp, _vp]),
     "sb_sgd_update": (_i, [_i, ctypes.POINTER(_vp), ctypes.POINTER(_vp), ctypes.POINTER(_sz),
                            ctypes.POINTER(ctypes.c_float), ctypes.c_float, _vp]),
@@ -324,6 +325,23 @@ def sb_model_average(workers, mp, params, n=None, stride=None, stream=None):
     st = _slot_stride(params, workers, stride)
     _check("sb_model_average", load().sb_model_average(
         int(workers), int(mp), int(st if n is None else n), _ptr(params), st, _stream(stream)))
+
+
+SB_MAX_REPLICAS = 64
+
+
+def sb_model_average_replicas(replicas, n=None, stream=None):
+    """replicas: one fp32 tensor (or device pointer) per replica; each is
+    replaced by the mean of all.  n defaults to the first tensor's numel."""
+    k = len(replicas)
+    if n is None:
+        n = replicas[0].numel()
+    for t in replicas:
+        if not isinstance(t, int) and (str(t.dtype) != "torch.float32" or t.numel() < n):
+            raise ValueError("replicas must be fp32 tensors of at least n elements")
+    ptrs = (_vp * max(k, 1))(*[_ptr(t) for t in replicas])
+    _check("sb_model_average_replicas", load().sb_model_average_replicas(
+        int(k), int(n), ptrs, _stream(stream)))
 
 
 # --------------------------------------------------- loss and SGD update --

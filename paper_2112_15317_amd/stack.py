@@ -605,3 +605,56 @@ class GroupTrainStep:
         finally:
             self.call, self.conv.call = saved
         return rec
+
+
+class AveragedGroups:
+    """G MP groups (each a GroupTrainStep on its own data) whose models are
+    averaged every ``period`` steps: the data parallelism across MP groups
+    (sec. 4: every worker exchanges its parameters up to the modulo layer
+    every few batches, and each FC shard is averaged with the same shard of
+    the other groups; sec. 2: the reduce is the mean of the replicas).
+
+    One device holds every group: group g's tensors are its own
+    GroupTrainStep's buffers, and the average of each parameter tensor (every
+    conv layer's filters and bias, every FC layer's [K][in][ns] shards and
+    [K][ns] biases, shard r of group g beside shard r of every other group)
+    is one ``sb_model_average_replicas`` call over the G buffers.  ``step``
+    runs every group's training step, then, after steps period, 2 period,
+    ..., the averages.
+    """
+
+    def __init__(self, schedule, n, in_ch, hw, plan, groups, period, lr=0.01, device="cuda"):
+        if groups < 1 or groups > sb.SB_MAX_REPLICAS:
+            raise ValueError("1 .. %d groups" % sb.SB_MAX_REPLICAS)
+        if period < 1:
+            raise ValueError("the averaging period is a positive number of steps")
+        self.groups = [GroupTrainStep(schedule, n, in_ch, hw, plan, lr, device)
+                       for _ in range(groups)]
+        self.period = period
+        self.steps_done = 0
+
+        def params(gs):
+            c = gs.conv
+            return list(c.W) + list(c.b) + list(gs.W) + list(gs.b)
+        per_group = [params(gs) for gs in self.groups]
+        self.sets = [list(ts) for ts in zip(*per_group)]     # one entry per parameter tensor
+        self.call = _plain      # hook: every libsb call goes through it
+
+    def load_inputs(self, group_inputs, conv_w, conv_b, fc_w, fc_b):
+        """group_inputs[g] = (x, local_remote, labels) of group g; every group
+        starts from the same model."""
+        if len(group_inputs) != len(self.groups):
+            raise ValueError("one input set per group")
+        for gs, (x, remote, labels) in zip(self.groups, group_inputs):
+            gs.load_inputs(x, conv_w, conv_b, fc_w, fc_b, remote, labels)
+
+    def average(self, stream=None):
+        for i, ts in enumerate(self.sets):
+            self.call(("avg", i), sb.sb_model_average_replicas, ts, None, stream)
+
+    def step(self, stream=None):
+        for gs in self.groups:
+            gs.step(stream)
+        self.steps_done += 1
+        if self.steps_done % self.period == 0:
+            self.average(stream)

@@ -250,6 +250,21 @@ def test_model_average_argument_validation():
     assert avg(4, 4, 16, P, 16, None) == sb.SB_OK                   # one worker per set
 
 
+def test_model_average_replicas_argument_validation():
+    ptrs = lambda *a: (ctypes.c_void_p * max(len(a), 1))(*a)
+    avg = lambda k, n, p: _raw("sb_model_average_replicas", k, n, p, None)
+    a, b = P, P + (1 << 20)
+    assert avg(0, 16, ptrs(a)) == sb.SB_ERR_INVALID_ARG
+    assert avg(sb.SB_MAX_REPLICAS + 1, 16, ptrs(*[P + (i << 20) for i in range(65)])) == \
+        sb.SB_ERR_INVALID_ARG
+    assert avg(2, 16, None) == sb.SB_ERR_INVALID_ARG
+    assert avg(2, 16, ptrs(a, None)) == sb.SB_ERR_INVALID_ARG
+    assert avg(2, 16, ptrs(a, a + 32)) == sb.SB_ERR_INVALID_ARG      # ranges overlap
+    assert avg(3, 16, ptrs(a, b, b)) == sb.SB_ERR_INVALID_ARG
+    assert avg(2, 0, ptrs(a, b)) == sb.SB_OK                          # nothing to average
+    assert avg(1, 16, ptrs(a)) == sb.SB_OK                            # one replica
+
+
 def test_pack_many_rejects_packing_over_another_tasks_filters():
     d = sb.conv_desc(2, 3, 8, 8, 4)
     need = sb.sb_conv3x3_packed_bytes(d, sb.SB_PASS_FWD)

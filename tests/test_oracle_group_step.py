@@ -5,7 +5,10 @@ each modulo iteration built here from the paper's index map (gathered
 example b comes from worker b // (B/K), local row k*(B/K) + b % (B/K)), the
 mean cross-entropy of the B gathered rows, an SGD step of the FC layers at
 lr / K after every iteration, and the conv layers' gradient accumulated over
-the K iterations and applied once at the end.  No GPU."""
+the K iterations and applied once at the end.  The averaged training of
+several MP groups (sec. 4: the models averaged every few steps) is pinned
+against torch groups stepping on their own data and torch means of their
+parameters.  No GPU."""
 import numpy as np
 import pytest
 import torch
@@ -135,3 +138,72 @@ def test_group_step_iteration_records():
         if k == 0:
             for j in range(3):
                 np.testing.assert_array_equal(it["w_before"][j], fw[j])
+
+
+def _torch_averaged_training(groups, ws, bs, fw, fb, steps, period, lr):
+    """G groups stepping independently, their models replaced by the torch
+    mean over the groups every `period` steps."""
+    state = [{"conv_w": list(ws), "conv_b": list(bs), "fc_w": list(fw), "fc_b": list(fb)}
+             for _ in groups]
+    for s in range(steps):
+        for g, (x, remote, labels) in enumerate(groups):
+            p = state[g]
+            t = _torch_group_step(x, p["conv_w"], p["conv_b"], p["fc_w"], p["fc_b"], remote,
+                                  labels, lr)
+            state[g] = {"conv_w": t["conv_w"], "conv_b": t["conv_b"], "fc_w": t["W"],
+                        "fc_b": t["b"]}
+        if (s + 1) % period == 0:
+            for key in state[0]:
+                for i in range(len(state[0][key])):
+                    m = torch.stack([torch.from_numpy(np.asarray(st[key][i])) for st in state])
+                    m = m.mean(dim=0).numpy()
+                    for st in state:
+                        st[key][i] = m
+    return state
+
+
+def _groups(K, B, G, seed):
+    base = _setup(K, B, seed)
+    out = []
+    for g in range(G):
+        x, *_, remote, labels = _setup(K, B, seed + 1 + g)
+        out.append((x, remote, labels))
+    return base, out
+
+
+@pytest.mark.parametrize("G,steps,period", [(2, 3, 2), (3, 2, 1)])
+def test_averaged_training_matches_torch(G, steps, period):
+    """Groups with different data, averaged every `period` steps (sec. 4):
+    the oracle against torch autograd groups and torch means."""
+    K, B, lr = 2, 4, 0.3
+    (_, ws, bs, pools, fw, fb, _, _), groups = _groups(K, B, G, 300 + G)
+    r = OS.averaged_group_training(groups, ws, bs, pools, fw, fb, steps, period, lr)
+    t = _torch_averaged_training(groups, ws, bs, fw, fb, steps, period, lr)
+    for g in range(G):
+        for key in ("conv_w", "conv_b", "fc_w", "fc_b"):
+            for a, b in zip(r[g][key], t[g][key]):
+                np.testing.assert_allclose(a, b, rtol=1e-10, atol=1e-12)
+
+
+def test_averaging_schedule_invariants():
+    """Averaged steps leave every group with the same model; steps between
+    averages let groups with different data drift apart; groups that see
+    the same data never differ, so their training is one group's."""
+    K, B, lr = 2, 4, 0.3
+    (x, ws, bs, pools, fw, fb, remote, labels), groups = _groups(K, B, 2, 77)
+    after1 = OS.averaged_group_training(groups, ws, bs, pools, fw, fb, 1, 2, lr)
+    after2 = OS.averaged_group_training(groups, ws, bs, pools, fw, fb, 2, 2, lr)
+    for key in ("conv_w", "fc_w"):
+        assert any(np.abs(a - b).max() > 1e-6 for a, b in zip(after1[0][key], after1[1][key]))
+        for a, b in zip(after2[0][key], after2[1][key]):
+            np.testing.assert_array_equal(a, b)
+    same = [(x, remote, labels)] * 3
+    avg = OS.averaged_group_training(same, ws, bs, pools, fw, fb, 2, 1, lr)
+    one = OS.group_train_step(x, ws, bs, pools, fw, fb, remote, labels, lr)
+    two = OS.group_train_step(x, one["conv_w_new"], one["conv_b_new"], pools, one["fc_w_new"],
+                              one["fc_b_new"], remote, labels, lr)
+    for g in range(3):
+        for a, b in zip(avg[g]["fc_w"], two["fc_w_new"]):
+            np.testing.assert_allclose(a, b, rtol=1e-13, atol=1e-15)
+        for a, b in zip(avg[g]["conv_w"], two["conv_w_new"]):
+            np.testing.assert_allclose(a, b, rtol=1e-13, atol=1e-15)
