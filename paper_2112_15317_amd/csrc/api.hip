@@ -31,6 +31,7 @@ sb_status conv_bf16c8(bool dgrad, int N, int Cin, int H, int W, int Cout, const 
                       const void* wt, const float* bias, const void* mask, void* out, void* ws,
                       size_t ws_bytes, int relu, bool prepacked, hipStream_t st);
 bool conv_wgrad_c8_takes(int N, int C, int H, int W, int K);
+size_t conv_wgrad_c8_ws(int N, int C, int H, int W, int K);
 int conv_wgrad_c8_describe(int N, int C, int H, int W, int K, char* buf, size_t len);
 sb_status conv_wgrad_c8(int N, int C, int H, int W, int K, const void* x, const void* dy,
                         float* dw, float* db, void* ws, size_t ws_bytes, hipStream_t st);
@@ -75,6 +76,12 @@ static sb_status conv_check(const sb_conv3x3_desc* d, int pass) {
   return SB_OK;
 }
 
+// Split-partial bytes of a weight-gradient call (the kernel depends on the layout).
+static size_t wgrad_ws(const sb_conv3x3_desc* d) {
+  return d->layout == SB_NCHW8C ? sbh::conv_wgrad_c8_ws(d->n, d->c, d->h, d->w, d->k)
+                                : sbh::conv_wgrad_ws(d->dtype, d->n, d->c, d->h, d->w, d->k);
+}
+
 extern "C" size_t sb_conv3x3_workspace_bytes(const sb_conv3x3_desc* d, int pass) {
   if (pass < SB_PASS_FWD || pass > SB_PASS_BWD_WEIGHT) return (size_t)-1;
   if (conv_check(d, pass) != SB_OK) return (size_t)-1;
@@ -82,7 +89,7 @@ extern "C" size_t sb_conv3x3_workspace_bytes(const sb_conv3x3_desc* d, int pass)
   switch (pass) {
     case SB_PASS_FWD: return sbh::conv_igemm_ws(d->dtype, d->n, d->c, d->h, d->w, d->k, pk);
     case SB_PASS_BWD_DATA: return sbh::conv_igemm_ws(d->dtype, d->n, d->k, d->h, d->w, d->c, pk);
-    default: return sbh::conv_wgrad_ws(d->dtype, d->n, d->c, d->h, d->w, d->k);
+    default: return wgrad_ws(d);
   }
 }
 
@@ -236,7 +243,7 @@ extern "C" sb_status sb_conv3x3_bwd_weight(const sb_conv3x3_desc* d, const void*
       sbh::overlaps(db, dbb, x, xb) || sbh::overlaps(db, dbb, dy, dyb) ||
       sbh::overlaps(dw, dwb, db, dbb))
     return SB_ERR_INVALID_ARG;
-  size_t need = sbh::conv_wgrad_ws(d->dtype, d->n, d->c, d->h, d->w, d->k);
+  size_t need = wgrad_ws(d);
   if (need && (!ws || ws_bytes < need)) return SB_ERR_WORKSPACE;
   if (need && (sbh::overlaps(ws, need, dw, dwb) || sbh::overlaps(ws, need, db, dbb) ||
                sbh::overlaps(ws, need, x, xb) || sbh::overlaps(ws, need, dy, dyb)))
@@ -291,7 +298,7 @@ extern "C" sb_status sb_conv3x3_bwd_weight_noalloc(const sb_conv3x3_desc* d, con
       sbh::overlaps(db, dbb, x, xb) || sbh::overlaps(db, dbb, dy, dyb) ||
       sbh::overlaps(dw, dwb, db, dbb))
     return SB_ERR_INVALID_ARG;
-  const size_t need = sbh::conv_wgrad_ws(d->dtype, d->n, d->c, d->h, d->w, d->k);
+  const size_t need = wgrad_ws(d);
   if (need > kScratchBytes) return SB_ERR_WORKSPACE;
   void* ws = nullptr;
   s = scratch_address(&ws);

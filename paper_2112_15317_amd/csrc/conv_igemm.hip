@@ -76,11 +76,10 @@ struct ConvTile {
   static constexpr int HALO = CK * PLANE;
   static constexpr int WTS = 9 * CK * BN;
   static constexpr int HALO_PT = (HALO + 255) / 256;
-  static constexpr int WTS_PT = (WTS + 255) / 256;
   static constexpr int LDS_X = CK * PLANE_P;
   static constexpr int LDS_W = 9 * CK * BN_P;
-  // Staging lanes past the end of the halo or filter slice store into a
-  // private slot after the two (256 floats), so every staging store is
+  // Halo staging lanes past the end of the halo store into a private slot
+  // after the two regions (256 floats), so every halo staging store is
   // unconditional (no exec-mask juggling in the loop).
   static constexpr int LDS_SPARE = 256;
   static constexpr int LDS_BUF = LDS_X + LDS_W + LDS_SPARE;
@@ -166,12 +165,15 @@ __global__ __launch_bounds__(T::THREADS, 2 / T::KSPLIT) void conv3x3_igemm_f32(C
     x_c[i] = c;
     x_loff[i] = live ? c * T::PLANE_P + rem : T::LDS_X + T::LDS_W + tid;
   }
-  // Packed filter slice element e -> LDS row e / BN, column e % BN.
-  int w_loff[T::WTS_PT];
+  // Packed filter slice, 4 elements (one row, 4 consecutive columns) per
+  // load: piece g = elements 4g .. 4g+3 -> LDS row 4g / BN, column 4g % BN.
+  static_assert(T::BN % 4 == 0 && T::WTS % 4 == 0, "whole 4-column pieces");
+  constexpr int WTS4 = T::WTS / 4, W4_PT = (WTS4 + 255) / 256;
+  int w_loff[W4_PT];
 #pragma unroll
-  for (int i = 0; i < T::WTS_PT; ++i) {
-    int e = tid + i * 256;
-    w_loff[i] = e < T::WTS ? (e / T::BN) * T::BN_P + e % T::BN : T::LDS_W + tid;
+  for (int i = 0; i < W4_PT; ++i) {
+    const int e = 4 * (tid + i * 256);
+    w_loff[i] = (e / T::BN) * T::BN_P + e % T::BN;
   }
   int pix_off[T::MB];
 #pragma unroll
@@ -189,7 +191,8 @@ __global__ __launch_bounds__(T::THREADS, 2 / T::KSPLIT) void conv3x3_igemm_f32(C
 
   const rsrc_t xr = input_rsrc<E>(a, n0, T::IMGS);
   const rsrc_t wr = packed_rsrc<E, T::WTS>(a, blockIdx.y);
-  float rx[T::HALO_PT], rw[T::WTS_PT];
+  float rx[T::HALO_PT];
+  f4 rw[W4_PT];
   auto gload = [&](int kc) {
     const int cbase = kc * T::CK;
 #pragma unroll
@@ -199,10 +202,10 @@ __global__ __launch_bounds__(T::THREADS, 2 / T::KSPLIT) void conv3x3_igemm_f32(C
       rx[i] = BufLoad<E>::one(xr, ok ? (uint32_t)(x_off[i] + ci * HWs) * (uint32_t)sizeof(E) : kOOB);
     }
 #pragma unroll
-    for (int i = 0; i < T::WTS_PT; ++i) {
-      const int e = tid + i * 256;
-      rw[i] = BufLoad<E>::one(wr, e < T::WTS ? (uint32_t)(kc * T::WTS + e) * (uint32_t)sizeof(E)
-                                             : kOOB);
+    for (int i = 0; i < W4_PT; ++i) {
+      const int g = tid + i * 256;
+      rw[i] = BufLoad<E>::four(wr, g < WTS4 ? (uint32_t)(kc * T::WTS + 4 * g) * (uint32_t)sizeof(E)
+                                            : kOOB);
     }
   };
   auto lstore = [&](int buf) {
@@ -211,7 +214,9 @@ __global__ __launch_bounds__(T::THREADS, 2 / T::KSPLIT) void conv3x3_igemm_f32(C
 #pragma unroll
     for (int i = 0; i < T::HALO_PT; ++i) X[x_loff[i]] = rx[i];
 #pragma unroll
-    for (int i = 0; i < T::WTS_PT; ++i) Wl[w_loff[i]] = rw[i];
+    for (int i = 0; i < W4_PT; ++i)
+      if (WTS4 % 256 == 0 || tid + i * 256 < WTS4)
+        *reinterpret_cast<f4*>(Wl + w_loff[i]) = rw[i];
   };
   // WMC: the wave's pixel-row position wm as a compile-time constant (only
   // used with WHOLE_H, to skip padding blocks).
@@ -436,9 +441,8 @@ struct SmallTile {
   static constexpr int X_F4 = CK * IMGS * P / 4;  // float4 per chunk
   static constexpr int X_PT = X_F4 / 256;
   static constexpr int WTS = 9 * CK * BN;
-  static constexpr int WTS_PT = WTS / 256;
-  // Every staging lane is live: the stores need no condition.
-  static_assert(X_F4 % 256 == 0 && WTS % 256 == 0, "staging covers whole 256-thread rounds");
+  // Every image-plane staging lane is live: those stores need no condition.
+  static_assert(X_F4 % 256 == 0 && WTS % 4 == 0, "staging covers whole 256-thread rounds");
   static constexpr int MB = BM / 16;              // column blocks: (position, image group)
   static constexpr int OUT_IMG_STRIDE = BN * P + 4;
   static constexpr int LDS_OUT = IMGS * OUT_IMG_STRIDE;
@@ -484,11 +488,13 @@ __global__ __launch_bounds__(T::THREADS, 2 / T::KSPLIT) void conv3x3_small_f32(C
     x_c[i] = c;
     x_loff[i] = c * T::PLANE_P + quarter * 4 * T::PS + img;
   }
-  // Packed filter slice element e -> LDS row e / BN, column e % BN.
-  int w_loff[T::WTS_PT];
+  // Packed filter slice, 4 elements (one row, 4 consecutive columns) per
+  // load: piece g = elements 4g .. 4g+3 -> LDS row 4g / BN, column 4g % BN.
+  constexpr int WTS4 = T::WTS / 4, W4_PT = (WTS4 + 255) / 256;
+  int w_loff[W4_PT];
 #pragma unroll
-  for (int i = 0; i < T::WTS_PT; ++i) {
-    int e = tid + i * 256;
+  for (int i = 0; i < W4_PT; ++i) {
+    const int e = 4 * (tid + i * 256);
     w_loff[i] = (e / T::BN) * T::BN_P + e % T::BN;
   }
 
@@ -499,7 +505,7 @@ __global__ __launch_bounds__(T::THREADS, 2 / T::KSPLIT) void conv3x3_small_f32(C
   const rsrc_t xr = input_rsrc<E>(a, n0, T::IMGS);
   const rsrc_t wr = packed_rsrc<E, T::WTS>(a, blockIdx.y);
   f4 rx[T::X_PT];
-  float rw[T::WTS_PT];
+  f4 rw[W4_PT];
   auto gload = [&](int kc) {
     const int cbase = kc * T::CK;
 #pragma unroll
@@ -509,8 +515,11 @@ __global__ __launch_bounds__(T::THREADS, 2 / T::KSPLIT) void conv3x3_small_f32(C
       rx[i] = BufLoad<E>::four(xr, ok ? (uint32_t)(x_off[i] + ci * T::P) * (uint32_t)sizeof(E) : kOOB);
     }
 #pragma unroll
-    for (int i = 0; i < T::WTS_PT; ++i)
-      rw[i] = BufLoad<E>::one(wr, (uint32_t)(kc * T::WTS + tid + i * 256) * (uint32_t)sizeof(E));
+    for (int i = 0; i < W4_PT; ++i) {
+      const int g = tid + i * 256;
+      rw[i] = BufLoad<E>::four(wr, g < WTS4 ? (uint32_t)(kc * T::WTS + 4 * g) * (uint32_t)sizeof(E)
+                                            : kOOB);
+    }
   };
   auto lstore = [&](int buf) {
     float* X = lds + buf * T::LDS_BUF;
@@ -520,7 +529,9 @@ __global__ __launch_bounds__(T::THREADS, 2 / T::KSPLIT) void conv3x3_small_f32(C
 #pragma unroll
       for (int j = 0; j < 4; ++j) X[x_loff[i] + j * T::PS] = rx[i][j];
 #pragma unroll
-    for (int i = 0; i < T::WTS_PT; ++i) Wl[w_loff[i]] = rw[i];
+    for (int i = 0; i < W4_PT; ++i)
+      if (WTS4 % 256 == 0 || tid + i * 256 < WTS4)
+        *reinterpret_cast<f4*>(Wl + w_loff[i]) = rw[i];
   };
   auto compute = [&](int buf) {
     const float* X = lds + buf * T::LDS_BUF;

@@ -1659,6 +1659,10 @@ bool conv_wgrad_c8_takes(int N, int C, int H, int W, int K) {
   return W >= 8 && C % 8 == 0 && K % 8 == 0 && sb::wg_plan(N, C, H, W, K, false, true).bc != 0;
 }
 
+size_t conv_wgrad_c8_ws(int N, int C, int H, int W, int K) {
+  return sb::wg_plan(N, C, H, W, K, false, true).ws_bytes;
+}
+
 int conv_wgrad_c8_describe(int N, int C, int H, int W, int K, char* buf, size_t len) {
   sb::WgPlan p = sb::wg_plan(N, C, H, W, K, false, true);
   static const char* kT[] = {"2, 32", "4, 16", "8, 8"};
