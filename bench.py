@@ -560,9 +560,9 @@ def kernel_name(key, call_args, dtype):
     FC calls launch several GEMMs and are grouped by call."""
     from paper_2112_15317_amd import sb
     kind, j = key
-    if kind in ("fwd", "dgrad", "wgrad"):
+    if kind in ("fwd", "dgrad", "wgrad", "fwd_pool"):
         p = {"fwd": sb.SB_PASS_FWD, "dgrad": sb.SB_PASS_BWD_DATA,
-             "wgrad": sb.SB_PASS_BWD_WEIGHT}[kind]
+             "wgrad": sb.SB_PASS_BWD_WEIGHT, "fwd_pool": sb.SB_PASS_FWD_POOL}[kind]
         return sb.sb_conv3x3_plan_string(call_args[0], p)
     if kind.startswith("fc_"):
         d = call_args[0]
@@ -587,7 +587,7 @@ def kernel_name(key, call_args, dtype):
 def call_work(wl, key, args):
     """Algorithmic work of one call: (amount, 'flop' | 'bytes')."""
     kind, i = key
-    if kind in ("fwd", "dgrad", "wgrad"):
+    if kind in ("fwd", "dgrad", "wgrad", "fwd_pool"):
         return layer_flops(wl.layers[i], args[0].n)[0], "flop"
     if kind.startswith("fc_"):
         return fc_flops(args[0], kind, kind == "fc_fwd" or args[5] is not None), "flop"

@@ -101,7 +101,9 @@ typedef struct {
     int layout;           /* sb_layout of the activations                   */
 } sb_conv3x3_desc;
 
-enum { SB_PASS_FWD = 0, SB_PASS_BWD_DATA = 1, SB_PASS_BWD_WEIGHT = 2 };
+/* SB_PASS_FWD_POOL: the forward with ReLU + 2x2 max pooling fused
+ * (sb_conv3x3_fwd_pool); it takes the forward's workspace and packing. */
+enum { SB_PASS_FWD = 0, SB_PASS_BWD_DATA = 1, SB_PASS_BWD_WEIGHT = 2, SB_PASS_FWD_POOL = 3 };
 
 /* Workspace bytes that `pass` needs for `desc` (0 is a valid answer, and a
  * NULL workspace is then accepted).  With SB_PACKED_FILTERS set the answer
@@ -152,6 +154,23 @@ sb_status sb_conv3x3_pack_filters_many(int count, const sb_conv3x3_desc *descs,
 sb_status sb_conv3x3_fwd(const sb_conv3x3_desc *desc, const void *x,
                          const void *w, const float *bias, void *y,
                          void *workspace, size_t workspace_bytes, void *stream);
+
+/* Forward followed by ReLU + 2x2 / stride 2 max pooling in one call
+ * (sec. 2.2: a convolution, its ReLU and the pooling layer after it; the
+ * pooled layer's pre-activation is read by nothing else in a step, so it is
+ * never written): the forward's output z as sb_conv3x3_fwd would store it
+ * without SB_FUSE_RELU (bias added, rounded to the storage type), then
+ * y and idx exactly as sb_relu_maxpool_fwd computes them from z.  y is
+ * [n][k][h/2][w/2] and idx one byte per element of y, both in desc->layout.
+ * Supported for SB_NCHW8C bf16 with even h and w when the forward's channel
+ * loop is not split (sb_conv3x3_workspace_bytes(desc, SB_PASS_FWD_POOL) is
+ * then not (size_t)-1): SB_ERR_UNSUPPORTED otherwise, SB_ERR_INVALID_ARG
+ * for odd h or w, SB_FUSE_RELU, NULL pointers or overlapping outputs.
+ * With SB_PACKED_FILTERS, w is the forward packing (SB_PASS_FWD). */
+sb_status sb_conv3x3_fwd_pool(const sb_conv3x3_desc *desc, const void *x,
+                              const void *w, const float *bias, void *y,
+                              uint8_t *idx, void *workspace,
+                              size_t workspace_bytes, void *stream);
 
 /* Data gradient (sec. 2.2 backward propagation):
  *   dx[n,c,i,j] = sum_{k,r,s} dy[n,k,i-r+1,j-s+1] * w[k,c,r,s]

@@ -26,10 +26,12 @@ sb_status conv_wgrad(int dtype, int N, int C, int H, int W, int K, const void* x
 // Channel-blocked bf16 (SB_NCHW8C).
 bool conv_bf16_takes(int N, int Cin, int H, int W, int Cout);
 int conv_bf16c8_describe(bool dgrad, int N, int Cin, int H, int W, int Cout, char* buf,
-                         size_t len);
+                         size_t len, bool pool = false);
+bool conv_bf16c8_pools(int N, int Cin, int H, int W, int Cout);
 sb_status conv_bf16c8(bool dgrad, int N, int Cin, int H, int W, int Cout, const void* in,
                       const void* wt, const float* bias, const void* mask, void* out, void* ws,
-                      size_t ws_bytes, int relu, bool prepacked, hipStream_t st);
+                      size_t ws_bytes, int relu, bool prepacked, hipStream_t st,
+                      uint8_t* pool_idx = nullptr);
 bool conv_wgrad_c8_takes(int N, int C, int H, int W, int K);
 size_t conv_wgrad_c8_ws(int N, int C, int H, int W, int K);
 int conv_wgrad_c8_describe(int N, int C, int H, int W, int K, char* buf, size_t len);
@@ -65,9 +67,17 @@ static sb_status conv_check(const sb_conv3x3_desc* d, int pass) {
     if (d->dtype != SB_BF16) return SB_ERR_UNSUPPORTED;
     const bool ok = pass == SB_PASS_BWD_WEIGHT
                         ? sbh::conv_wgrad_c8_takes(d->n, d->c, d->h, d->w, d->k)
-                    : pass == SB_PASS_FWD ? sbh::conv_bf16_takes(d->n, d->c, d->h, d->w, d->k)
-                                          : sbh::conv_bf16_takes(d->n, d->k, d->h, d->w, d->c);
+                    : pass == SB_PASS_BWD_DATA
+                        ? sbh::conv_bf16_takes(d->n, d->k, d->h, d->w, d->c)
+                        : sbh::conv_bf16_takes(d->n, d->c, d->h, d->w, d->k);
     if (!ok) return SB_ERR_UNSUPPORTED;
+  }
+  if (pass == SB_PASS_FWD_POOL) {
+    // Forward with fused ReLU + 2x2 pooling: channel-blocked bf16, even
+    // image sizes, an unsplit channel loop.
+    if (d->h % 2 || d->w % 2) return SB_ERR_INVALID_ARG;
+    if (d->layout != SB_NCHW8C) return SB_ERR_UNSUPPORTED;
+    if (!sbh::conv_bf16c8_pools(d->n, d->c, d->h, d->w, d->k)) return SB_ERR_UNSUPPORTED;
   }
   // Kernels index weights and activations with 32-bit ints.
   if ((int64_t)d->k * d->c * 9 >= (1ll << 31)) return SB_ERR_UNSUPPORTED;
@@ -83,11 +93,12 @@ static size_t wgrad_ws(const sb_conv3x3_desc* d) {
 }
 
 extern "C" size_t sb_conv3x3_workspace_bytes(const sb_conv3x3_desc* d, int pass) {
-  if (pass < SB_PASS_FWD || pass > SB_PASS_BWD_WEIGHT) return (size_t)-1;
+  if (pass < SB_PASS_FWD || pass > SB_PASS_FWD_POOL) return (size_t)-1;
   if (conv_check(d, pass) != SB_OK) return (size_t)-1;
   const bool pk = (d->flags & SB_PACKED_FILTERS) != 0;
   switch (pass) {
-    case SB_PASS_FWD: return sbh::conv_igemm_ws(d->dtype, d->n, d->c, d->h, d->w, d->k, pk);
+    case SB_PASS_FWD:
+    case SB_PASS_FWD_POOL: return sbh::conv_igemm_ws(d->dtype, d->n, d->c, d->h, d->w, d->k, pk);
     case SB_PASS_BWD_DATA: return sbh::conv_igemm_ws(d->dtype, d->n, d->k, d->h, d->w, d->c, pk);
     default: return wgrad_ws(d);
   }
@@ -95,7 +106,7 @@ extern "C" size_t sb_conv3x3_workspace_bytes(const sb_conv3x3_desc* d, int pass)
 
 // Packed-filter bytes of a forward or data-gradient pass (0: invalid).
 static size_t packed_bytes(const sb_conv3x3_desc* d, int pass) {
-  if (pass == SB_PASS_FWD) return sbh::conv_igemm_pack_bytes(d->dtype, d->n, d->c, d->h, d->w, d->k);
+  if (pass == SB_PASS_FWD || pass == SB_PASS_FWD_POOL) return sbh::conv_igemm_pack_bytes(d->dtype, d->n, d->c, d->h, d->w, d->k);
   return sbh::conv_igemm_pack_bytes(d->dtype, d->n, d->k, d->h, d->w, d->c);
 }
 
@@ -203,6 +214,31 @@ extern "C" sb_status sb_conv3x3_fwd(const sb_conv3x3_desc* d, const void* x, con
   return sbh::conv_igemm(false, d->dtype, d->n, d->c, d->h, d->w, d->k, x, w, bias, nullptr, y,
                          ws, ws_bytes, (d->flags & SB_FUSE_RELU) ? 1 : 0, pk,
                          sbh::stream_of(stream));
+}
+
+extern "C" sb_status sb_conv3x3_fwd_pool(const sb_conv3x3_desc* d, const void* x, const void* w,
+                                         const float* bias, void* y, uint8_t* idx, void* ws,
+                                         size_t ws_bytes, void* stream) {
+  sb_status s = conv_check(d, SB_PASS_FWD_POOL);
+  if (s != SB_OK) return s;
+  if (!x || !w || !y || !idx) return SB_ERR_INVALID_ARG;
+  const bool pk = (d->flags & SB_PACKED_FILTERS) != 0;
+  const size_t pooled = (size_t)d->n * d->k * (d->h / 2) * (d->w / 2);
+  const size_t yb = pooled * sbh::dsize(d->dtype), ib = pooled, xb = act_bytes(d, d->c);
+  const size_t wb = pk ? packed_bytes(d, SB_PASS_FWD) : (size_t)d->k * d->c * 9 * sbh::dsize(d->dtype);
+  const size_t bb = bias ? d->k * sizeof(float) : 0;
+  if (sbh::overlaps(y, yb, x, xb) || sbh::overlaps(y, yb, w, wb) || sbh::overlaps(y, yb, bias, bb) ||
+      sbh::overlaps(idx, ib, x, xb) || sbh::overlaps(idx, ib, w, wb) ||
+      sbh::overlaps(idx, ib, bias, bb) || sbh::overlaps(idx, ib, y, yb))
+    return SB_ERR_INVALID_ARG;
+  size_t need = sbh::conv_igemm_ws(d->dtype, d->n, d->c, d->h, d->w, d->k, pk);
+  if (need && (!ws || ws_bytes < need)) return SB_ERR_WORKSPACE;
+  if (need && (sbh::overlaps(ws, need, x, xb) || sbh::overlaps(ws, need, y, yb) ||
+               sbh::overlaps(ws, need, idx, ib) || sbh::overlaps(ws, need, w, wb) ||
+               sbh::overlaps(ws, need, bias, bb)))
+    return SB_ERR_INVALID_ARG;
+  return sbh::conv_bf16c8(false, d->n, d->c, d->h, d->w, d->k, x, w, bias, nullptr, y, ws,
+                          ws_bytes, 0, pk, sbh::stream_of(stream), idx);
 }
 
 extern "C" sb_status sb_conv3x3_bwd_data(const sb_conv3x3_desc* d, const void* dy, const void* w,
@@ -315,12 +351,13 @@ extern "C" sb_status sb_conv3x3_bwd_weight_noalloc(const sb_conv3x3_desc* d, con
 
 extern "C" size_t sb_conv3x3_plan_string(const sb_conv3x3_desc* d, int pass, char* buf,
                                          size_t len) {
-  if (pass < SB_PASS_FWD || pass > SB_PASS_BWD_WEIGHT) return 0;
+  if (pass < SB_PASS_FWD || pass > SB_PASS_FWD_POOL) return 0;
   if (conv_check(d, pass) != SB_OK) return 0;
   int r;
   if (d->layout == SB_NCHW8C) {
-    if (pass == SB_PASS_FWD)
-      r = sbh::conv_bf16c8_describe(false, d->n, d->c, d->h, d->w, d->k, buf, len);
+    if (pass == SB_PASS_FWD || pass == SB_PASS_FWD_POOL)
+      r = sbh::conv_bf16c8_describe(false, d->n, d->c, d->h, d->w, d->k, buf, len,
+                                    pass == SB_PASS_FWD_POOL);
     else if (pass == SB_PASS_BWD_DATA)
       r = sbh::conv_bf16c8_describe(true, d->n, d->k, d->h, d->w, d->c, buf, len);
     else

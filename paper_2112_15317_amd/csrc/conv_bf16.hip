@@ -375,8 +375,14 @@ __host__ __device__ constexpr size_t c8_one_buf_lds_bytes() {
   return (T::LDS_BUF > T::BM * (T::BN + 8) ? T::LDS_BUF : T::BM * (T::BN + 8)) * sizeof(u16);
 }
 
-template <class T, bool DGRAD, bool ONE = false>
+// POOL (forward only): the unsplit output tile is not written; ReLU and 2x2
+// max pooling run on it in LDS (bias added, rounded to bf16: the tensor the
+// unfused forward would write), and the pooled tile and its window codes
+// are written instead (a.out, a.pool_idx), as sb_relu_maxpool_fwd computes
+// them from that tensor.
+template <class T, bool DGRAD, bool ONE = false, bool POOL = false>
 __global__ __launch_bounds__(256, 2) void conv3x3_c8_bf16(ConvArgs a) {
+  static_assert(!(POOL && DGRAD), "pooling follows the forward pass");
   extern __shared__ u16 ldsb[];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lc = lane & 31, lh = lane >> 5;
@@ -566,6 +572,52 @@ __global__ __launch_bounds__(256, 2) void conv3x3_c8_bf16(ConvArgs a) {
       }
     }
   __syncthreads();
+  if constexpr (POOL) {
+    // Piece q = (channel block q / PP, pooled pixel q % PP): the window's
+    // four 8-channel pieces come from LDS; per channel the first maximum in
+    // row-major window order wins (strict >), the output is the maximum if
+    // it is positive, else +0, and bit 7 of the code flags the latter.
+    static_assert(T::TH % 2 == 0 && T::TW % 2 == 0, "whole 2x2 windows per tile");
+    constexpr int PTH = T::TH / 2, PTW = T::TW / 2, PP = T::IMGS * PTH * PTW;
+    constexpr int NPP = PP * (T::BN / 8);
+    static_assert(NPP % 256 == 0, "whole rounds of pooled pieces");
+    const int Hh = a.H / 2, Wh = a.W / 2;
+    u16* yout = (u16*)a.out;
+#pragma unroll
+    for (int i = 0; i < NPP / 256; ++i) {
+      const int q = tid + 256 * i;
+      const int kb = q / PP, pp = q % PP;
+      const int img = pp / (PTH * PTW), r = pp % (PTH * PTW);
+      const int py = r / PTW, px = r % PTW;
+      const int n = n0 + img, oh = h0 / 2 + py, ow = w0 / 2 + px, co = co0 + kb * 8;
+      if (n >= a.N || oh >= Hh || ow >= Wh || co >= a.Cout) continue;
+      const int p00 = (img * T::TH + 2 * py) * T::TW + 2 * px;
+      const s8 v[4] = {*reinterpret_cast<const s8*>(E + p00 * EP + kb * 8),
+                       *reinterpret_cast<const s8*>(E + (p00 + 1) * EP + kb * 8),
+                       *reinterpret_cast<const s8*>(E + (p00 + T::TW) * EP + kb * 8),
+                       *reinterpret_cast<const s8*>(E + (p00 + T::TW + 1) * EP + kb * 8)};
+      s8 o;
+      uint32_t codes[2] = {0u, 0u};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        short best = v[0][e];
+        float m = bf16_to_f32((u16)best);
+        uint32_t c = 0;
+#pragma unroll
+        for (int j = 1; j < 4; ++j) {
+          const float f = bf16_to_f32((u16)v[j][e]);
+          if (f > m) { m = f; best = v[j][e]; c = (uint32_t)j; }
+        }
+        const bool pos = m > 0.f;
+        o[e] = pos ? best : (short)0;
+        codes[e / 4] |= (c | (pos ? 0u : 0x80u)) << (8 * (e % 4));
+      }
+      const size_t off = ((((size_t)n * KB + co / 8) * Hh + oh) * Wh + ow) * 8;
+      *reinterpret_cast<s8*>(yout + off) = o;
+      *reinterpret_cast<uint2*>(a.pool_idx + off) = make_uint2(codes[0], codes[1]);
+    }
+    return;
+  }
   constexpr int NPC = T::BM * (T::BN / 8);               // pieces per block
   constexpr int EPI = NPC / 256;
   static_assert(NPC % 256 == 0, "whole rounds of pieces");
@@ -778,11 +830,28 @@ static void c8_launch(const BPlan& p, const ConvArgs& a, bool pack, hipStream_t 
       (void)hipFuncSetAttribute((const void*)conv3x3_c8_bf16<T, DGRAD, true>,
                                 hipFuncAttributeMaxDynamicSharedMemorySize,
                                 (int)c8_one_buf_lds_bytes<T>());
+    if constexpr (!DGRAD) {
+      (void)hipFuncSetAttribute((const void*)conv3x3_c8_bf16<T, false, false, true>,
+                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)T::LDS_BYTES);
+      if constexpr (can_one)
+        (void)hipFuncSetAttribute((const void*)conv3x3_c8_bf16<T, false, true, true>,
+                                  hipFuncAttributeMaxDynamicSharedMemorySize,
+                                  (int)c8_one_buf_lds_bytes<T>());
+    }
   });
   if (pack) bf16_pack<DGRAD>(p, a.wt, (void*)a.wpk, a.Cin, a.Cout, st);
   dim3 grid(p.grid_x, p.co_tiles, p.splits);
   ConvArgs k = a;
   if (p.splits > 1) { k.bias = nullptr; k.mask = nullptr; k.relu = 0; }
+  if constexpr (!DGRAD) {
+    if (a.pool_idx) {                      // the caller checked: one split
+      if (can_one && one)
+        conv3x3_c8_bf16<T, false, true, true><<<grid, 256, c8_one_buf_lds_bytes<T>(), st>>>(k);
+      else
+        conv3x3_c8_bf16<T, false, false, true><<<grid, 256, T::LDS_BYTES, st>>>(k);
+      return;
+    }
+  }
   if (can_one && one)
     conv3x3_c8_bf16<T, DGRAD, true><<<grid, 256, c8_one_buf_lds_bytes<T>(), st>>>(k);
   else
@@ -884,19 +953,32 @@ sb_status conv_bf16(bool dgrad, int N, int Cin, int H, int W, int Cout, const vo
 // Channel-blocked bf16 tensors (SB_NCHW8C): the same plans (and filter
 // packing) as the NCHW bf16 path with 16-byte staging.
 int conv_bf16c8_describe(bool dgrad, int N, int Cin, int H, int W, int Cout, char* buf,
-                         size_t len) {
+                         size_t len, bool pool) {
   sb::BPlan p = sb::bf16_plan(N, Cin, H, W, Cout, true);
   static const char* kNames[] = {"8, 32, 1", "16, 16, 1", "8, 8, 4", "16, 32, 1", "8, 64, 1",
                                  "8, 32, 1, 1"};
-  return snprintf(buf, len, "sb::conv3x3_c8_bf16<sb::BTile<%s>, %s> grid=%dx%dx%d",
-                  kNames[p.tile], dgrad ? "true" : "false", p.grid_x, p.co_tiles, p.splits);
+  return snprintf(buf, len, "sb::conv3x3_c8_bf16<sb::BTile<%s>, %s%s> grid=%dx%dx%d",
+                  kNames[p.tile], dgrad ? "true" : "false", pool ? ", pool" : "", p.grid_x,
+                  p.co_tiles, p.splits);
 }
 
+// Whether the forward can pool its output in the kernel (fused ReLU + 2x2
+// max pooling): even image sizes and an unsplit channel loop.
+bool conv_bf16c8_pools(int N, int Cin, int H, int W, int Cout) {
+  sb::BPlan p = sb::bf16_plan(N, Cin, H, W, Cout, true);
+  return p.ok && p.splits == 1 && H % 2 == 0 && W % 2 == 0;
+}
+
+// pool_idx: forward only; when given, `out` receives the pooled tensor
+// [N][Cout/8][H/2][W/2][8] and pool_idx its codes (relu must be 0).
 sb_status conv_bf16c8(bool dgrad, int N, int Cin, int H, int W, int Cout, const void* in,
                       const void* wt, const float* bias, const void* mask, void* out, void* ws,
-                      size_t ws_bytes, int relu, bool prepacked, hipStream_t st) {
+                      size_t ws_bytes, int relu, bool prepacked, hipStream_t st,
+                      uint8_t* pool_idx) {
   sb::BPlan p = sb::bf16_plan(N, Cin, H, W, Cout, true);
   if (!p.ok) return SB_ERR_UNSUPPORTED;
+  if (pool_idx && (dgrad || relu || !conv_bf16c8_pools(N, Cin, H, W, Cout)))
+    return SB_ERR_UNSUPPORTED;
   // Buffer ranges: the whole output (mask) tensor, one block's images of the
   // input, one tile's packed filters.
   if ((int64_t)N * std::max(Cin, Cout) * H * W * 2 >= (1ll << 31) ||
@@ -912,6 +994,7 @@ sb_status conv_bf16c8(bool dgrad, int N, int Cin, int H, int W, int Cout, const 
   a.N = N; a.Cin = Cin; a.H = H; a.W = W; a.Cout = Cout;
   a.tiles_w = p.tiles_w; a.tiles_h = p.tiles_h;
   a.nchunks = p.nchunks; a.chunks_per_split = p.cps; a.splits = p.splits; a.relu = relu;
+  a.pool_idx = pool_idx;
   if (dgrad) sb::c8_dispatch<true>(p, a, !prepacked, st);
   else sb::c8_dispatch<false>(p, a, !prepacked, st);
   return launch_status();

@@ -19,6 +19,7 @@ struct ConvArgs {
   const void* mask;      // [N][Cout][H][W] or null (data gradient)
   void* out;             // [N][Cout][H][W]
   float* part;           // split partials [splits][N][Cout][H][W]
+  uint8_t* pool_idx;     // fused ReLU + 2x2 pooling (channel-blocked forward): codes
   int N, Cin, H, W, Cout;
   int tiles_w, tiles_h, nchunks, chunks_per_split, splits, relu;
 };

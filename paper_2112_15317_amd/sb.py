@@ -24,7 +24,8 @@ SB_F32, SB_BF16 = 0, 1
 SB_NCHW, SB_NCHW8C = 0, 1
 SB_FUSE_RELU = 1
 SB_PACKED_FILTERS = 2
-SB_PASS_FWD, SB_PASS_BWD_DATA, SB_PASS_BWD_WEIGHT = 0, 1, 2
+SB_PASS_FWD, SB_PASS_BWD_DATA, SB_PASS_BWD_WEIGHT, SB_PASS_FWD_POOL = 0, 1, 2, 3
+SIZE_MAX = 2 ** 64 - 1          # (size_t)-1: the workspace queries' "not supported"
 SB_FC_FWD, SB_FC_BWD = 0, 1
 SB_SGD_MAX_TENSORS = 64
 SB_NOALLOC_SCRATCH_BYTES = 40 << 20
@@ -64,6 +65,8 @@ SIGNATURES = {
                                           ctypes.POINTER(_vp), ctypes.POINTER(_sz), _vp]),
     "sb_conv3x3_plan_string": (_sz, [ctypes.POINTER(sb_conv3x3_desc), _i, ctypes.c_char_p, _sz]),
     "sb_conv3x3_fwd": (_i, [ctypes.POINTER(sb_conv3x3_desc), _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "sb_conv3x3_fwd_pool": (_i, [ctypes.POINTER(sb_conv3x3_desc), _vp, _vp, _vp, _vp, _vp, _vp,
+                                 _sz, _vp]),
     "sb_conv3x3_bwd_data": (_i, [ctypes.POINTER(sb_conv3x3_desc), _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "sb_conv3x3_bwd_weight": (_i, [ctypes.POINTER(sb_conv3x3_desc), _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "sb_conv3x3_bwd_weight_noalloc": (_i, [ctypes.POINTER(sb_conv3x3_desc), _vp, _vp, _vp, _vp,
@@ -222,6 +225,13 @@ def sb_conv3x3_fwd(desc, x, w, bias, y, ws=None, stream=None):
     p, nb = _ws(ws)
     _check("sb_conv3x3_fwd", load().sb_conv3x3_fwd(
         ctypes.byref(desc), _ptr(x), _ptr(w), _ptr(bias), _ptr(y), p, nb, _stream(stream)))
+
+
+def sb_conv3x3_fwd_pool(desc, x, w, bias, y, idx, ws=None, stream=None):
+    p, nb = _ws(ws)
+    _check("sb_conv3x3_fwd_pool", load().sb_conv3x3_fwd_pool(
+        ctypes.byref(desc), _ptr(x), _ptr(w), _ptr(bias), _ptr(y), _ptr(idx), p, nb,
+        _stream(stream)))
 
 
 def sb_conv3x3_bwd_data(desc, dy, w, relu_mask_src, dx, ws=None, stream=None):

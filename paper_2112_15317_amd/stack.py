@@ -76,12 +76,17 @@ class ConvStack:
 
     def __init__(self, schedule, n, in_ch, hw, dtype="f32", device="cuda",
                  out_buffer=None, out_grad_buffer=None, packed=True, overlap=False,
-                 layout="nchw"):
+                 layout="nchw", fuse_pool=True):
         """layout: "nchw", or "c8" for channel-blocked activations
         (SB_NCHW8C, bf16 only): every activation buffer is then
         [n][c/8][h][w][8], and the first layer's input channels are padded
         with zeros to a whole block of 8 (zero filters for the padding, so
-        every result is the unpadded network's)."""
+        every result is the unpadded network's).
+
+        fuse_pool: a pooled layer whose forward can pool in the kernel
+        (sb_conv3x3_fwd_pool: channel-blocked, unsplit) runs its forward,
+        ReLU and pooling as one call and has no Z buffer (``self.fused``
+        lists those layers)."""
         self.layers = conv_layers(schedule, in_ch, hw)
         if not self.layers[-1].pool_after:
             raise ValueError("the stack must end with a pooled layer")
@@ -121,6 +126,11 @@ class ConvStack:
                        else torch.empty_like(self.A[-1]))
         C = self.cin
         lay = self.layout
+        # Pooled layers that pool inside the forward (their Z is never stored).
+        self.fused = (self.fused_layers(schedule, n, in_ch, hw, dtype, layout, packed)
+                      if fuse_pool else set())
+        for i in self.fused:
+            del self.Z[i]
         self.W = [torch.zeros((l.k, C[l.index], 3, 3), dtype=tdt, device=dev) for l in L]
         self.b = [torch.zeros((l.k,), dtype=torch.float32, device=dev) for l in L]
         self.dW = [torch.empty((l.k, C[l.index], 3, 3), dtype=torch.float32, device=dev)
@@ -172,6 +182,22 @@ class ConvStack:
             self.side = torch.cuda.Stream(device=dev)     # default priority
         self.call = _plain      # hook: every libsb call of the step goes through it
 
+    @staticmethod
+    def fused_layers(schedule, n, in_ch, hw, dtype="f32", layout="nchw", packed=True):
+        """Indices of the pooled layers whose forward pools in the kernel
+        (sb_conv3x3_fwd_pool takes their descriptor): host-side queries only."""
+        if layout != "c8":
+            return set()
+        out = set()
+        for l in conv_layers(schedule, in_ch, hw):
+            c = -(-l.c // 8) * 8
+            d = sb.conv_desc(n, c, l.h, l.w, l.k, _code(dtype), packed=packed,
+                             layout=sb.SB_NCHW8C)
+            if l.pool_after and \
+                    sb.sb_conv3x3_workspace_bytes(d, sb.SB_PASS_FWD_POOL) != sb.SIZE_MAX:
+                out.add(l.index)
+        return out
+
     # -- layouts -----------------------------------------------------------------
     def shape_of(self, n, c, h, w):
         """Buffer shape of an activation of c channels in this stack's layout."""
@@ -220,7 +246,10 @@ class ConvStack:
         for l in self.layers:
             i = l.index
             w = self.Wf[i] if self.packed else self.W[i]
-            if l.pool_after:
+            if i in self.fused:
+                c(("fwd_pool", i), sb.sb_conv3x3_fwd_pool, self.pdesc_b[i], self.A[i], w,
+                  self.b[i], self.A[i + 1], self.idx[i], self.ws, stream)
+            elif l.pool_after:
                 c(("fwd", i), sb.sb_conv3x3_fwd, self.pdesc[i], self.A[i], w, self.b[i],
                   self.Z[i], self.ws, stream)
                 c(("pool_fwd", i), sb.sb_relu_maxpool_fwd, self.n, l.k, l.h, l.w, self.code,

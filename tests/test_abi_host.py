@@ -59,7 +59,8 @@ def test_conv_argument_validation():
     # ReLU flag is forward-only.
     dr = sb.conv_desc(2, 3, 8, 8, 4, relu=True)
     assert _raw("sb_conv3x3_bwd_data", ctypes.byref(dr), P, P + (1 << 20), None, P + (2 << 20), None, 0, None) == sb.SB_ERR_INVALID_ARG
-    assert sb.sb_conv3x3_workspace_bytes(d, 3) == 2 ** 64 - 1
+    assert sb.sb_conv3x3_workspace_bytes(d, 4) == 2 ** 64 - 1
+    assert sb.sb_conv3x3_workspace_bytes(d, -1) == 2 ** 64 - 1
 
 
 def test_conv_workspace_is_checked_before_launch():
@@ -263,6 +264,38 @@ def test_model_average_replicas_argument_validation():
     assert avg(3, 16, ptrs(a, b, b)) == sb.SB_ERR_INVALID_ARG
     assert avg(2, 0, ptrs(a, b)) == sb.SB_OK                          # nothing to average
     assert avg(1, 16, ptrs(a)) == sb.SB_OK                            # one replica
+
+
+def test_fused_forward_pool_validation():
+    """sb_conv3x3_fwd_pool: channel-blocked bf16 with even sizes and an
+    unsplit plan; the pass-3 workspace query says which descriptors it
+    takes, with the forward's workspace; nothing is launched on an error."""
+    c8 = lambda n, c, h, w, k, **kw: sb.conv_desc(n, c, h, w, k, sb.SB_BF16,
+                                                  layout=sb.SB_NCHW8C, **kw)
+    ok = c8(32, 64, 224, 224, 64)          # 6272 tiles: one split
+    need = sb.sb_conv3x3_workspace_bytes(ok, sb.SB_PASS_FWD_POOL)
+    assert need == sb.sb_conv3x3_workspace_bytes(ok, sb.SB_PASS_FWD)
+    assert "pool" in sb.sb_conv3x3_plan_string(ok, sb.SB_PASS_FWD_POOL)
+    fwd_pool = lambda d, x, w, y, idx, ws=None, nb=0: _raw(
+        "sb_conv3x3_fwd_pool", ctypes.byref(d), x, w, None, y, idx, ws, nb, None)
+    x, w, y, idx = P, P + (256 << 20), P + (512 << 20), P + (768 << 20)
+    ws = P + (1024 << 20) if need else None
+    for bad, status in ((sb.conv_desc(32, 64, 224, 224, 64, sb.SB_BF16), sb.SB_ERR_UNSUPPORTED),
+                        (sb.conv_desc(32, 64, 224, 224, 64, sb.SB_F32, layout=sb.SB_NCHW8C),
+                         sb.SB_ERR_UNSUPPORTED),
+                        (c8(32, 64, 224, 223, 64), sb.SB_ERR_INVALID_ARG),
+                        (c8(32, 64, 224, 224, 64, relu=True), sb.SB_ERR_INVALID_ARG),
+                        (c8(2, 64, 32, 32, 64), sb.SB_ERR_UNSUPPORTED)):     # split plan
+        assert sb.sb_conv3x3_workspace_bytes(bad, sb.SB_PASS_FWD_POOL) == sb.SIZE_MAX
+        assert fwd_pool(bad, x, w, y, idx, ws, need) == status
+    assert fwd_pool(ok, x, w, y, None, ws, need) == sb.SB_ERR_INVALID_ARG
+    assert fwd_pool(ok, x, w, y, y + 64, ws, need) == sb.SB_ERR_INVALID_ARG   # idx over y
+    assert fwd_pool(ok, x, w, x + 64, idx, ws, need) == sb.SB_ERR_INVALID_ARG  # y over x
+    # A plan that splits the channel loop cannot pool in the kernel.
+    split = c8(1, 512, 14, 14, 512)
+    splits = int(sb.sb_conv3x3_plan_string(split, sb.SB_PASS_FWD).rsplit("x", 1)[1])
+    assert (sb.sb_conv3x3_workspace_bytes(split, sb.SB_PASS_FWD_POOL) == sb.SIZE_MAX) == \
+        (splits > 1)
 
 
 def test_pack_many_rejects_packing_over_another_tasks_filters():

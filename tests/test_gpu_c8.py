@@ -176,3 +176,48 @@ def test_c8_relu_maxpool(shape, dtype):
     np.testing.assert_array_equal(nchw(idx), ridx)
     np.testing.assert_array_equal(nchw(y), ry)
     np.testing.assert_array_equal(nchw(dx), O.relu_maxpool_bwd(dyv, ridx))
+
+
+# Forward with fused ReLU + 2x2 pooling (sb_conv3x3_fwd_pool): shapes whose
+# plan is one split (8x32 tiles with 64 and 32 output channels, a ragged
+# last tile row, 16x16 tiles).
+FUSED_SHAPES = [(32, 32, 64, 64, 64), (32, 16, 64, 64, 32), (40, 32, 50, 64, 64),
+                (32, 64, 28, 28, 512)]
+
+
+@pytest.mark.parametrize("shape", FUSED_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_c8_conv_fwd_pool(shape):
+    """The fused call equals, bit for bit, the forward then the pool kernel
+    (the same sums, rounded at the same point, pooled by the same rule), and
+    against the oracle (pooling of the bf16-rounded fp64 forward) the pooled
+    values meet 2e-2 and every differing code is a certified near-tie of the
+    oracle's window values (the two sides round sums that differ in their
+    last fp32 bits)."""
+    from tests.chain import near_tie_flips
+    n, c, h, w, k = shape
+    print_case("c8_conv_fwd_pool", shape=shape)
+    x, wt, b, _, _ = _inputs(n, c, h, w, k, 61)
+    d = _desc(shape)
+    need = sb.sb_conv3x3_workspace_bytes(d, sb.SB_PASS_FWD_POOL)
+    assert need != sb.SIZE_MAX, "planned as one split"
+    ws = _ws(need)
+    wd = torch.from_numpy(wt.astype(np.float32)).to(torch.bfloat16).cuda()
+    bd = torch.from_numpy(b).cuda()
+    xd = c8(x)
+    pooled = (n, k // 8, h // 2, w // 2, 8)
+    y = torch.full(pooled, float("nan"), dtype=torch.bfloat16, device="cuda")
+    idx = torch.full(pooled, 0x55, dtype=torch.uint8, device="cuda")
+    sb.sb_conv3x3_fwd_pool(d, xd, wd, bd, y, idx, ws)
+    z = torch.full((n, k // 8, h, w, 8), float("nan"), dtype=torch.bfloat16, device="cuda")
+    y2 = torch.full(pooled, float("nan"), dtype=torch.bfloat16, device="cuda")
+    idx2 = torch.full(pooled, 0x55, dtype=torch.uint8, device="cuda")
+    sb.sb_conv3x3_fwd(d, xd, wd, bd, z, ws)
+    sb.sb_relu_maxpool_fwd(n, k, h, w, sb.SB_BF16, sb.SB_NCHW8C, z, y2, idx2)
+    torch.cuda.synchronize()
+    assert torch.equal(idx, idx2), "codes differ from the unfused forward and pool"
+    assert torch.equal(y.view(torch.int16), y2.view(torch.int16)), "pooled values differ"
+    zr = bf(O.conv3x3_fwd(x, wt, b))
+    ry, ridx = O.relu_maxpool_fwd(zr)
+    assert rel_l2(nchw(y), ry) <= TOL["bf16"]
+    flips = near_tie_flips(zr, ridx, nchw(idx), 2.0 ** -6 * np.max(np.abs(zr)))
+    print("near-tie windows:", flips)

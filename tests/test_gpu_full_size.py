@@ -37,10 +37,14 @@ HYBRID_FC = [(512, 4096), (4096, 4096)]
 GROSS = 1e-2
 
 
-def stack_keys(layers):
-    """The calls of ConvStack.step, in order."""
+def stack_keys(layers, fused=()):
+    """The calls of ConvStack.step, in order (fused: the layers whose
+    forward pools in the kernel)."""
     keys = [("pack", 0)]
     for L in layers:
+        if L.index in fused:
+            keys.append(("fwd_pool", L.index))
+            continue
         keys.append(("fwd", L.index))
         if L.pool_after:
             keys.append(("pool_fwd", L.index))

@@ -44,16 +44,17 @@ def test_vgg16_cifar_stack_end_to_end():
 
 def test_vgg16_imagenet_bf16_stack_full_size_properties():
     """The whole ImageNet-shaped bf16 stack (batch 32, 224x224, the
-    benchmark's channel-blocked layout) through one step: every pool output
-    and code is consistent with the stored pre-activation (y = max(0, window
-    max), first maximum, ReLU flag), the un-pooled gradient routes exactly,
-    and every gradient is finite."""
+    benchmark's channel-blocked layout, each pooled layer's forward and
+    pooling as separate calls so that its pre-activation is stored) through
+    one step: every pool output and code is consistent with the stored
+    pre-activation (y = max(0, window max), first maximum, ReLU flag), the
+    un-pooled gradient routes exactly, and every gradient is finite."""
     n, hw = 32, 224
     print_case("vgg16_imagenet_bf16_stack", n=n, hw=hw)
     layers = configs.conv_layers(configs.VGG16, 3, hw)
     x, wts, bs = _vgg_inputs(n, hw, 21, layers)
     dy_top = synth.normal((n, 512, 7, 7), 21, synth.TID.DY_TOP)
-    st = ConvStack(configs.VGG16, n, 3, hw, "bf16", layout="c8")
+    st = ConvStack(configs.VGG16, n, 3, hw, "bf16", layout="c8", fuse_pool=False)
     st.load_inputs(x, wts, bs, dy_top)
     st.step()
     torch.cuda.synchronize()
