@@ -1,6 +1,6 @@
 """Benchmark: one SplitBrain worker's compute share on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline] [--only]
                     [--workload vgg16-cifar-f32 | vgg16-imagenet-bf16 |
                                 fc-shard-f32 | hybrid-f32 | paper-variant-f32 |
                                 exchange-f32]
@@ -43,6 +43,11 @@ roofline of the dominant kernel and the fp64 CPU oracle's rate on a sample
 of the same workload.  Per-call durations come from a second timed region:
 each call of the step captured K times back to back in a graph of its own,
 replayed between two HIP events on the stream the kernels run on.
+
+The default run (the headline workload, no --only) then times every other
+workload the same way in the same process and adds their rate, step time
+and dominant-kernel roofline to the line under `other_workloads`; the
+headline's fields and timed regions are unaffected.
 
 --profile-pass runs W + K plain (eager, ungraphed) steps and then three
 copies of a 256 MiB buffer, and prints a one-line summary: the program that
@@ -599,58 +604,20 @@ def call_work(wl, key, args):
     return pool_bytes(wl.layers[i], args[0], esize), "bytes"
 
 
-def main():
-    W = workloads()
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", choices=sorted(W), default="vgg16-cifar-f32")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample", type=int, default=None,
-                    help="images (rows for the FC shard) the oracle times")
-    ap.add_argument("--profile-pass", action="store_true")
-    ap.add_argument("--layout", choices=["nchw", "c8"], default=None,
-                    help="activation layout of a VGG stack (default: the workload's)")
-    args = ap.parse_args()
-    if args.gpus != 1:
-        print("bench.py measures one GPU: this library has no multi-GPU path "
-              "(collectives are outside its scope); run with --gpus 1", file=sys.stderr)
-        sys.exit(2)
-
+def measure(wl, K, warmup):
+    """Time workload `wl` (already chosen and configured) on the current
+    GPU: warm-up steps, timed region 1 (a graph of K steps), timed region 2
+    (each call K times in a graph of its own).  Returns the JSON fields."""
     import torch
     from paper_2112_15317_amd.stack import capture_graph
-
-    wl = W[args.workload]
-    if args.layout is not None:
-        if not isinstance(wl, VggWorkload):
-            ap.error("--layout applies to the VGG stack workloads")
-        wl.layout = args.layout
     dtype = wl.dtype
-    torch.cuda.set_device(0)
-    K = args.steps
     calls = wl.build()
 
     def run_step():
         for _, fn, a in calls:
             fn(*a)
 
-    if args.profile_pass:
-        for _ in range(args.warmup + K):
-            run_step()
-        torch.cuda.synchronize()
-        a = torch.empty(COPY_MIB << 18, dtype=torch.float32, device="cuda")
-        b = torch.empty_like(a)
-        a.fill_(1.0)
-        for _ in range(3):
-            b.copy_(a)
-        torch.cuda.synchronize()
-        print(json.dumps({"profile_pass": args.workload, "steps": args.warmup + K,
-                          "copy_bytes": COPY_MIB << 20, "csrc_sha256": csrc_digest()}),
-              flush=True)
-        return
-
-    for _ in range(args.warmup):
+    for _ in range(warmup):
         run_step()
     torch.cuda.synchronize()
 
@@ -735,7 +702,7 @@ def main():
         "metric": wl.metric,
         "value": value,
         "unit": unit,
-        "n_gpus": 1, "steps": K, "warmup": args.warmup,
+        "n_gpus": 1, "steps": K, "warmup": warmup,
         "ms_per_step": round(ms, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": dtype, "data": "synthetic",
@@ -752,8 +719,81 @@ def main():
         "per_kernel_us_per_step": {k: round(v["ms"] * 1e3, 1) for k, v in
                                    sorted(groups.items(), key=lambda kv: -kv[1]["ms"])},
     }
+    return out
+
+
+def main():
+    W = workloads()
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", choices=sorted(W), default="vgg16-cifar-f32")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample", type=int, default=None,
+                    help="images (rows for the FC shard) the oracle times")
+    ap.add_argument("--profile-pass", action="store_true")
+    ap.add_argument("--layout", choices=["nchw", "c8"], default=None,
+                    help="activation layout of a VGG stack (default: the workload's)")
+    ap.add_argument("--only", action="store_true",
+                    help="time the chosen workload alone (by default the headline run "
+                         "also times every other workload, reported under "
+                         "other_workloads)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: this library has no multi-GPU path "
+              "(collectives are outside its scope); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    wl = W[args.workload]
+    if args.layout is not None:
+        if not isinstance(wl, VggWorkload):
+            ap.error("--layout applies to the VGG stack workloads")
+        wl.layout = args.layout
+    torch.cuda.set_device(0)
+    K = args.steps
+
+    if args.profile_pass:
+        calls = wl.build()
+        for _ in range(args.warmup + K):
+            for _, fn, a in calls:
+                fn(*a)
+        torch.cuda.synchronize()
+        a = torch.empty(COPY_MIB << 18, dtype=torch.float32, device="cuda")
+        b = torch.empty_like(a)
+        a.fill_(1.0)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        print(json.dumps({"profile_pass": args.workload, "steps": args.warmup + K,
+                          "copy_bytes": COPY_MIB << 20, "csrc_sha256": csrc_digest()}),
+              flush=True)
+        return
+
+    out = measure(wl, K, args.warmup)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = wl.cpu_baseline(args.cpu_sample)
+    if not args.only and args.workload == "vgg16-cifar-f32" and args.layout is None:
+        # The other workloads at their own configurations, same process and
+        # GPU, after the headline's timed regions (their rate, step time and
+        # dominant kernel's roofline; no CPU baselines).
+        others = {}
+        for name, other in W.items():
+            if name == args.workload:
+                continue
+            try:
+                o = measure(other, K, args.warmup)
+                others[name] = {k: o[k] for k in ("metric", "value", "unit", "ms_per_step",
+                                                  "dtype", "config")}
+                others[name]["roofline"] = {k: o["roofline"][k] for k in
+                                            ("kernel", "bound", "achieved", "unit", "frac")}
+            except Exception as e:          # reported, never hides the headline
+                others[name] = {"error": "%s: %s" % (type(e).__name__, e)}
+            torch.cuda.synchronize()
+            torch.cuda.empty_cache()
+        out["other_workloads"] = others
     print(json.dumps(out), flush=True)
 
 
