@@ -1472,11 +1472,12 @@ static WgPlan wg_plan(int N, int C, int H, int W, int K, bool allow_small, bool 
   }
   long blocks = (long)p.k_tiles * p.c_tiles;
   // About two blocks per CU (one for the 2x2 GEMM, whose splits would each
-  // write a whole dW), at most 256 splits of the pixel range.
+  // write a whole dW), at most 512 splits of the pixel range (a layer of
+  // one block, the first layer, then still fills every CU twice).
   const long target = p.tile == 9 ? 256 : 512;
   int splits = 1;
   if (blocks < target)
-    splits = (int)std::min<long>(std::min<long>(p.ptiles, 256), cdiv((int)target, (int)blocks));
+    splits = (int)std::min<long>(std::min<long>(p.ptiles, 512), cdiv((int)target, (int)blocks));
   p.tps = cdiv(p.ptiles, splits);
   p.splits = cdiv(p.ptiles, p.tps);
   p.ws_bytes = p.splits > 1 ? (size_t)p.splits * ((size_t)K * C * 9 + K) * sizeof(float) : 0;
