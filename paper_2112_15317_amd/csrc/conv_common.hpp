@@ -71,17 +71,20 @@ __device__ __forceinline__ void pack_slice(const E* __restrict__ w, E* __restric
   constexpr int PT = (SL + 255) / 256;
   const int nchunks = cdiv(Cin, CK);
   const int ct = slice / nchunks, kc = slice - ct * nchunks;   // co tile, chunk
-  // fp32 filters whose channel counts are multiples of 4 (and 16-byte
-  // aligned): every run of consecutive source elements (CK * 9 per output
-  // channel, or BN * 9 per input channel for the data gradient) starts
-  // 16-byte aligned and is a multiple of 4 long, so the slice is read in
-  // groups of 4 consecutive slice elements with one 16-byte load each (a
-  // quarter of the load instructions).  A group lies in one run; it is read
-  // whole when all 4 elements are in range, element by element otherwise.
-  if constexpr (std::is_same<E, float>::value) {
-    static_assert(SL % 4 == 0 && (CK * 9) % 4 == 0 && (BN * 9) % 4 == 0, "whole groups per run");
-    if (Cin % 4 == 0 && Cout % 4 == 0 && ((uintptr_t)w & 15) == 0) {
-      constexpr int PT4 = (SL / 4 + 255) / 256;
+  // Filters whose channel counts are multiples of VEC = 16 / sizeof(E)
+  // (4 fp32 or 8 bf16 elements) and 16-byte aligned: every run of
+  // consecutive source elements (CK * 9 per output channel, or BN * 9 per
+  // input channel for the data gradient) then starts 16-byte aligned and is
+  // a multiple of VEC long, so the slice is read in groups of VEC
+  // consecutive slice elements with one 16-byte load each.  A group lies in
+  // one run; it is read whole when all its elements are in range, element by
+  // element otherwise.  The permuted slice goes out in 16-byte pieces too
+  // when LDS rows hold whole groups.
+  constexpr int VEC = 16 / (int)sizeof(E);
+  struct alignas(16) Piece { E e[VEC]; };
+  if constexpr (SL % VEC == 0 && (CK * 9) % VEC == 0 && (BN * 9) % VEC == 0) {
+    if (Cin % VEC == 0 && Cout % VEC == 0 && ((uintptr_t)w & 15) == 0) {
+      constexpr int PTV = (SL / VEC + 255) / 256;
       // Slice element g -> (channel within the run's tile, its source offset).
       auto locate = [&](int g, int& tap, int& cc, int& nn, size_t& src) {
         if (!DGRAD) {                                 // g = (nn, cc, tap), tap fastest
@@ -100,49 +103,51 @@ __device__ __forceinline__ void pack_slice(const E* __restrict__ w, E* __restric
         }
       };
       auto live = [&](int cc, int nn) { return ct * BN + nn < Cout && kc * CK + cc < Cin; };
-      f4 v4[PT4];
+      Piece v[PTV];
 #pragma unroll
-      for (int i = 0; i < PT4; ++i) {
-        const int g = (threadIdx.x + i * 256) * 4;
+      for (int i = 0; i < PTV; ++i) {
+        const int g = (threadIdx.x + i * 256) * VEC;
         if (g >= SL) continue;
-        int tap, cc, nn, tap3, cc3, nn3;
-        size_t src, src3;
+        int tap, cc, nn, tapl, ccl, nnl;
+        size_t src, srcl;
         locate(g, tap, cc, nn, src);
-        locate(g + 3, tap3, cc3, nn3, src3);
-        if (live(cc, nn) && live(cc3, nn3)) {         // the group's first and last in range
-          v4[i] = *reinterpret_cast<const f4*>(w + src);
+        locate(g + VEC - 1, tapl, ccl, nnl, srcl);
+        if (live(cc, nn) && live(ccl, nnl)) {         // the group's first and last in range
+          v[i] = *reinterpret_cast<const Piece*>(w + src);
         } else {
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
+          for (int e = 0; e < VEC; ++e) {
             int te, ce, ne;
             size_t se;
             locate(g + e, te, ce, ne, se);
-            v4[i][e] = live(ce, ne) ? w[se] : 0.f;
+            v[i].e[e] = live(ce, ne) ? w[se] : E{};
           }
         }
       }
 #pragma unroll
-      for (int i = 0; i < PT4; ++i) {
-        const int g0 = (threadIdx.x + i * 256) * 4;
+      for (int i = 0; i < PTV; ++i) {
+        const int g0 = (threadIdx.x + i * 256) * VEC;
         if (g0 >= SL) continue;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
+        for (int e = 0; e < VEC; ++e) {
           int tap, cc, nn;
           size_t src;
           locate(g0 + e, tap, cc, nn, src);
           slice_lds[CI8 ? ((tap * (CK / 8) + cc / 8) * BN + nn) * RS + cc % 8
-                        : (tap * CK + cc) * RS + nn] = v4[i][e];
+                        : (tap * CK + cc) * RS + nn] = v[i].e[e];
         }
       }
       __syncthreads();
       E* dst = out + (size_t)slice * SL;
-      if (((uintptr_t)out & 15) == 0) {
-        // Rows of ROW (a multiple of 4) elements: a group of 4 never crosses
-        // a row, and each slice starts 16-byte aligned (SL % 4 == 0).
-        static_assert(ROW % 4 == 0, "whole groups per LDS row");
-        for (int e = threadIdx.x * 4; e < SL; e += 1024) {
-          const float* l = slice_lds + (e / ROW) * RS + e % ROW;
-          *reinterpret_cast<f4*>(dst + e) = f4{l[0], l[1], l[2], l[3]};
+      if (ROW % VEC == 0 && ((uintptr_t)out & 15) == 0) {
+        // A group of VEC never crosses an LDS row, and each slice starts
+        // 16-byte aligned (SL % VEC == 0).
+        for (int e = threadIdx.x * VEC; e < SL; e += 256 * VEC) {
+          const E* l = slice_lds + (e / ROW) * RS + e % ROW;
+          Piece q;
+#pragma unroll
+          for (int k = 0; k < VEC; ++k) q.e[k] = l[k];
+          *reinterpret_cast<Piece*>(dst + e) = q;
         }
       } else {
         for (int e = threadIdx.x; e < SL; e += 256) dst[e] = slice_lds[(e / ROW) * RS + e % ROW];
@@ -218,9 +223,14 @@ __host__ __device__ constexpr int pack_kind(bool dgrad, int layout, int ck, int 
          ((bn == 16 ? 0 : bn == 32 ? 1 : 2) << 4);
 }
 
+// fp32 filters only take the PackCO kinds (the bf16 kernels' PackCI8 slices
+// are bf16), so the fp32 kernel sizes its LDS for those alone: the larger
+// PackCI8 buffer would cut the resident blocks per CU by more than half.
 template <class E>
 __global__ __launch_bounds__(256) void filter_pack_many(PackBatch b) {
-  constexpr int LDS = slice_lds_elems<16, 64, E, PackCI8>() > slice_lds_elems<8, 64, E, PackCO>()
+  constexpr bool F32 = std::is_same<E, float>::value;
+  constexpr int LDS = !F32 && slice_lds_elems<16, 64, E, PackCI8>() >
+                                  slice_lds_elems<8, 64, E, PackCO>()
                           ? slice_lds_elems<16, 64, E, PackCI8>()
                           : slice_lds_elems<8, 64, E, PackCO>();
   __shared__ E slice_lds[LDS];
@@ -242,11 +252,17 @@ __global__ __launch_bounds__(256) void filter_pack_many(PackBatch b) {
     SB_PACK_CASE(true, PackCO, 4, 64)
     SB_PACK_CASE(false, PackCO, 8, 16)
     SB_PACK_CASE(true, PackCO, 8, 16)
-    SB_PACK_CASE(false, PackCI8, 16, 64)
-    SB_PACK_CASE(true, PackCI8, 16, 64)
-    SB_PACK_CASE(false, PackCI8, 16, 32)
-    SB_PACK_CASE(true, PackCI8, 16, 32)
-    default: break;
+    default:
+      if constexpr (!F32) {
+        switch (k.kind) {
+          SB_PACK_CASE(false, PackCI8, 16, 64)
+          SB_PACK_CASE(true, PackCI8, 16, 64)
+          SB_PACK_CASE(false, PackCI8, 16, 32)
+          SB_PACK_CASE(true, PackCI8, 16, 32)
+          default: break;
+        }
+      }
+      break;
   }
 #undef SB_PACK_CASE
 }

@@ -961,6 +961,14 @@ __device__ __forceinline__ s8 tr_read8(const u16* base, int pitch, int col0, Row
   return s8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
 }
 
+// The first half of tr_read8: rows r0 .. r0 + 3 only.
+template <class Row>
+__device__ __forceinline__ v4s tr_read4(const u16* base, int pitch, int col0, Row lrow) {
+  const int s = threadIdx.x & 15, a = s & 3, j = s >> 2;
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (lds_v4s*)(base + lrow(j) * pitch + col0 + 4 * a));
+}
+
 template <class T>
 __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_c8(WgArgs a) {
   extern __shared__ u16 ldsw[];
@@ -1061,16 +1069,28 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_c8(WgArgs a) {
 #pragma unroll
     for (int m = 0; m < T::MA; ++m)
       av[m] = tr_read8(Dl, T::DYP, (wk * T::MA + m) * 16, [&](int j) { return p + j; });
+    // The three taps of a filter row read the same halo row at column
+    // offsets 0, 1, 2: the lane's 8 pixels at offset 0 are read once, with
+    // the next 4 (of which the first 2 are used; a lane whose columns would
+    // pass the row's end reads its last column instead), and the windows at
+    // offsets 1 and 2 are shifted out of those 12 values in registers.
 #pragma unroll
-    for (int t = 0; t < 9; ++t) {
-      const int r = t / 3, sft = t % 3;
-      const s8 bv = tr_read8(Xl, T::XP, wc * 16,
-                             [&](int j) { return (yy + r) * T::HWD + xx + sft + j; });
+    for (int r = 0; r < 3; ++r) {
+      const s8 b0 = tr_read8(Xl, T::XP, wc * 16, [&](int j) { return (yy + r) * T::HWD + xx + j; });
+      const v4s nx = tr_read4(Xl, T::XP, wc * 16, [&](int j) {
+        return (yy + r) * T::HWD + min(xx + 8 + j, T::HWD - 1);
+      });
+      const s8 b1 = s8{b0[1], b0[2], b0[3], b0[4], b0[5], b0[6], b0[7], nx[0]};
+      const s8 b2 = s8{b0[2], b0[3], b0[4], b0[5], b0[6], b0[7], nx[0], nx[1]};
 #pragma unroll
-      for (int m = 0; m < T::MA; ++m)
-        acc[m][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-            __builtin_bit_cast(bf16x8, av[m]), __builtin_bit_cast(bf16x8, bv), acc[m][t], 0, 0,
-            0);
+      for (int sft = 0; sft < 3; ++sft) {
+        const s8 bv = sft == 0 ? b0 : sft == 1 ? b1 : b2;
+#pragma unroll
+        for (int m = 0; m < T::MA; ++m)
+          acc[m][r * 3 + sft] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+              __builtin_bit_cast(bf16x8, av[m]), __builtin_bit_cast(bf16x8, bv),
+              acc[m][r * 3 + sft], 0, 0, 0);
+      }
     }
     typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
     const bf16x2 one2 = {(__bf16)1.0f, (__bf16)1.0f};
