@@ -33,7 +33,22 @@
 // loads of whole image planes.  The output tile is staged through LDS so it
 // is written with coalesced float4 stores.
 //
-// Both kernels split the channel chunks over gridDim.z when the output grid
+// conv3x3_few_f32 (passes with at most 4 output channels: the first layer's
+// data gradient, whose outputs are the image's 3 channels).  An MFMA tile
+// pads the output channels to at least 16 rows, so 3 channels would use
+// 3/16 of its work; here each lane computes every output channel of 2
+// vertically adjacent pixels on the vector ALU.  Per 8-channel chunk the
+// block stages the input halo in LDS and the first 4 output channels of the
+// packed filter slice (the 16-channel-output tile's slice, so packed buffers
+// serve either kernel); a lane reads its 4 x 3 input neighbourhood of a
+// channel once and each (tap, channel)'s filter values as one 16-byte LDS
+// read at the same address in every lane.  (Scalar loads of the filter
+// values straight into scalar registers measured slower: their latency sat
+// in the FMA chain.)  Two groups of lanes split the channel chunks and add
+// their sums at the end, in a fixed order.  The whole reduction runs in the
+// block (no split).
+//
+// Both MFMA kernels split the channel chunks over gridDim.z when the output grid
 // alone cannot fill the 256 CUs; each split writes its raw partial tile to
 // the workspace and conv_splitk_reduce adds the splits in a fixed order and
 // applies the epilogue.  (Reducing inside the kernel with a last-block
@@ -643,6 +658,160 @@ __global__ __launch_bounds__(T::THREADS, 2 / T::KSPLIT) void conv3x3_small_f32(C
   for_each_out4([&](f4 v, int, size_t off) { *reinterpret_cast<f4*>(mine + off) = v; });
 }
 
+// ------------------------------------------------- few output channels --
+struct FewTile {
+  static constexpr int TH = 8, TW = 32, CK = 8, BN = 16;   // BN: the packed slice's width
+  // Two groups of 128 lanes (2 pixels, rows, per lane) take alternate
+  // channel chunks through LDS buffers of their own and add their sums in
+  // LDS at the end: two waves per SIMD for the grid's one wave per SIMD of
+  // pixels.
+  static constexpr int GT = 128, THREADS = 2 * GT;
+  static constexpr int HH = TH + 2, HW = TW + 2, PLANE = HH * HW;
+  static constexpr int XS = CK * PLANE;                      // halo floats per chunk
+  static constexpr int X_PT = (XS + GT - 1) / GT;
+  static constexpr int WQ = 9 * CK;                          // (tap, channel) rows of 4
+  static constexpr int W_PT = (WQ * 4 + GT - 1) / GT;
+};
+
+template <int CO, class E>
+__global__ __launch_bounds__(FewTile::THREADS) void conv3x3_few_f32(ConvArgs a) {
+  using T = FewTile;
+  static_assert(CO >= 1 && CO <= 4, "one 16-byte filter read per (tap, channel)");
+  static_assert(T::GT * 2 * CO <= 2 * T::XS, "the partial sums fit one group's halo buffers");
+  __shared__ float X[2][2][T::XS];                 // [group][buffer]
+  __shared__ f4 Wl[2][2][T::WQ];
+  const int grp = threadIdx.x / T::GT, tid = threadIdx.x % T::GT;
+  const int tx = tid % T::TW, ty = (tid / T::TW) * 2;   // the lane's pixels: rows ty, ty + 1
+  int bt = blockIdx.x;
+  const int txi = bt % a.tiles_w; bt /= a.tiles_w;
+  const int tyi = bt % a.tiles_h;
+  const int n = bt / a.tiles_h;
+  const int h0 = tyi * T::TH, w0 = txi * T::TW;
+  const int HWs = a.H * a.W;
+  const int nchunks = cdiv(a.Cin, T::CK);
+  // Raw buffer loads: out-of-range offsets read 0.  Padding offsets start at
+  // kOOB and the channels past Cin in the last chunk lie past the image's
+  // range, so adding a chunk's offset keeps both out of range.
+  const rsrc_t xr = input_rsrc<E>(a, n, 1);
+  const rsrc_t wr = packed_rsrc<E, 9 * T::CK * T::BN>(a, 0);
+
+  // Staging plan: halo element e = (channel, halo row, halo column); its
+  // byte offset within the chunk.
+  uint32_t x_off[T::X_PT];
+#pragma unroll
+  for (int i = 0; i < T::X_PT; ++i) {
+    const int e = tid + i * T::GT;
+    const int c = e / T::PLANE, r = e % T::PLANE;
+    const int h = h0 + r / T::HW - 1, w = w0 + r % T::HW - 1;
+    const bool ok = e < T::XS && (unsigned)h < (unsigned)a.H && (unsigned)w < (unsigned)a.W;
+    x_off[i] = ok ? (uint32_t)((c * HWs + h * a.W + w) * (int)sizeof(E)) : kOOB;
+  }
+  // Filter value f = (tap, channel) row f / 4, output channel f % 4 of the
+  // chunk's packed slice [tap][channel][BN output channels].
+  uint32_t w_off[T::W_PT];
+#pragma unroll
+  for (int i = 0; i < T::W_PT; ++i) {
+    const int f = tid + i * T::GT;
+    w_off[i] = f < T::WQ * 4 ? (uint32_t)(((f / 4) * T::BN + f % 4) * (int)sizeof(E)) : kOOB;
+  }
+  float rx[T::X_PT], rw[T::W_PT];
+  auto gload = [&](int kc) {
+    const uint32_t xc = (uint32_t)(kc * T::CK * HWs * (int)sizeof(E));
+    const uint32_t wc = (uint32_t)(kc * T::WQ * T::BN * (int)sizeof(E));
+#pragma unroll
+    for (int i = 0; i < T::X_PT; ++i) rx[i] = BufLoad<E>::one(xr, x_off[i] + xc);
+#pragma unroll
+    for (int i = 0; i < T::W_PT; ++i) rw[i] = BufLoad<E>::one(wr, w_off[i] + wc);
+  };
+  auto lstore = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < T::X_PT; ++i) {
+      const int e = tid + i * T::GT;
+      if (e < T::XS) X[grp][buf][e] = rx[i];
+    }
+#pragma unroll
+    for (int i = 0; i < T::W_PT; ++i) {
+      const int f = tid + i * T::GT;
+      if (f < T::WQ * 4) reinterpret_cast<float*>(Wl[grp][buf])[f] = rw[i];
+    }
+  };
+
+  float acc[2][CO];
+#pragma unroll
+  for (int q = 0; q < 2; ++q)
+#pragma unroll
+    for (int co = 0; co < CO; ++co) acc[q][co] = 0.f;
+  auto compute = [&](int buf) {
+    const float* Xb = X[grp][buf];
+    const f4* Wb = Wl[grp][buf];
+    // Two channels at a time: unrolling all eight would let the compiler
+    // hoist every channel's reads and spill.
+#pragma unroll 2
+    for (int c = 0; c < T::CK; ++c) {
+      // Halo rows ty .. ty + 3, columns tx .. tx + 2: both pixels' taps.
+      float v[4][3];
+#pragma unroll
+      for (int dr = 0; dr < 4; ++dr)
+#pragma unroll
+        for (int ds = 0; ds < 3; ++ds) v[dr][ds] = Xb[c * T::PLANE + (ty + dr) * T::HW + tx + ds];
+#pragma unroll
+      for (int tap = 0; tap < 9; ++tap) {
+        const f4 wv = Wb[tap * T::CK + c];       // the same address in every lane
+#pragma unroll
+        for (int q = 0; q < 2; ++q)
+#pragma unroll
+          for (int co = 0; co < CO; ++co)
+            acc[q][co] = fmaf(v[q + tap / 3][tap % 3], wv[co], acc[q][co]);
+      }
+    }
+  };
+
+  // Group g takes chunks g, g + 2, ...; both run the same number of
+  // iterations (the barriers are block-wide).
+  const int nit = (nchunks + 1) / 2;
+  auto live = [&](int t) { return 2 * t + grp < nchunks; };
+  if (live(0)) {
+    gload(grp);
+    lstore(0);
+  }
+  __syncthreads();
+  for (int t = 0; t < nit; ++t) {
+    const int buf = t & 1;
+    if (live(t + 1)) gload(2 * (t + 1) + grp);
+    if (live(t)) compute(buf);
+    if (live(t + 1)) lstore(buf ^ 1);
+    __syncthreads();
+  }
+  // Group 1 hands its sums to group 0 through its own halo buffers (lane
+  // fastest: conflict-free), group 0 adds them and stores.
+  float* xfer = &X[1][0][0];
+  if (grp == 1) {
+#pragma unroll
+    for (int q = 0; q < 2; ++q)
+#pragma unroll
+      for (int co = 0; co < CO; ++co) xfer[(q * CO + co) * T::GT + tid] = acc[q][co];
+  }
+  __syncthreads();
+  if (grp == 1) return;
+#pragma unroll
+  for (int q = 0; q < 2; ++q)
+#pragma unroll
+    for (int co = 0; co < CO; ++co) acc[q][co] += xfer[(q * CO + co) * T::GT + tid];
+
+  const int j = w0 + tx;
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const int i = h0 + ty + q;
+    if (i >= a.H || j >= a.W) continue;
+#pragma unroll
+    for (int co = 0; co < CO; ++co) {
+      if (co >= a.Cout) continue;
+      const size_t off = ((size_t)n * a.Cout + co) * HWs + (size_t)i * a.W + j;
+      Elem<E>::store((E*)a.out, off, conv_epilogue<E>(a, acc[q][co], co, off));
+    }
+  }
+}
+
 // ---------------------------------------------------------------- host --
 struct IgemmPlan {
   int tile;          // index into the tile table
@@ -789,8 +958,34 @@ static void igemm_launch(const IgemmPlan& p, const ConvArgs& a, bool pack, hipSt
   }
 }
 
+// Passes with at most 4 output channels on the 16-channel-output tile's plan
+// (and its packed filters) take the vector-ALU kernel, in the whole
+// reduction: 8 x 32-pixel tiles, no split.
+inline bool few_takes(const IgemmPlan& p, int Cout) { return p.tile == 6 && Cout <= 4; }
+
+template <bool DGRAD, class E>
+static void few_launch(const IgemmPlan& p, const ConvArgs& a, bool pack, hipStream_t st) {
+  if (pack)
+    filter_pack<DGRAD, FewTile::CK, FewTile::BN, E><<<p.co_tiles * p.nchunks, 256, 0, st>>>(
+        (const E*)a.wt, (E*)a.wpk, a.Cin, a.Cout);
+  ConvArgs k = a;
+  k.tiles_w = cdiv(a.W, FewTile::TW);
+  k.tiles_h = cdiv(a.H, FewTile::TH);
+  const unsigned grid = (unsigned)(k.tiles_w * k.tiles_h * a.N);
+  switch (a.Cout) {
+    case 1: conv3x3_few_f32<1, E><<<grid, FewTile::THREADS, 0, st>>>(k); break;
+    case 2: conv3x3_few_f32<2, E><<<grid, FewTile::THREADS, 0, st>>>(k); break;
+    case 3: conv3x3_few_f32<3, E><<<grid, FewTile::THREADS, 0, st>>>(k); break;
+    default: conv3x3_few_f32<4, E><<<grid, FewTile::THREADS, 0, st>>>(k); break;
+  }
+}
+
 template <bool DGRAD, class E>
 static void igemm_dispatch(const IgemmPlan& p, const ConvArgs& a, bool pack, hipStream_t st) {
+  if (few_takes(p, a.Cout)) {
+    few_launch<DGRAD, E>(p, a, pack, st);
+    return;
+  }
   switch (p.tile) {
     case 0: igemm_launch<TileW32, DGRAD, false, E>(p, a, pack, st); break;
     case 1: igemm_launch<TileW16, DGRAD, false, E>(p, a, pack, st); break;
@@ -914,9 +1109,12 @@ int conv_igemm_describe(bool dgrad, int dtype, int N, int Cin, int H, int W, int
   if (dtype == SB_BF16 && conv_bf16_takes(N, Cin, H, W, Cout))
     return conv_bf16_describe(dgrad, N, Cin, H, W, Cout, buf, len);
   sb::IgemmPlan p = sb::igemm_plan(N, Cin, H, W, Cout, (int)dsize(dtype));
+  const char* et = dtype == SB_BF16 ? "unsigned short" : "float";
+  if (sb::few_takes(p, Cout))
+    return snprintf(buf, len, "sb::conv3x3_few_f32<%d, %s> grid=%dx1x1", Cout, et,
+                    sb::cdiv(W, sb::FewTile::TW) * sb::cdiv(H, sb::FewTile::TH) * N);
   char name[160];
-  snprintf(name, sizeof(name), sb::kTileNames[p.tile], dgrad ? "true" : "false",
-           dtype == SB_BF16 ? "unsigned short" : "float");
+  snprintf(name, sizeof(name), sb::kTileNames[p.tile], dgrad ? "true" : "false", et);
   return snprintf(buf, len, "%s grid=%dx%dx%d", name, p.grid_x, p.co_tiles, p.splits);
 }
 
