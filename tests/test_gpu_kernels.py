@@ -81,6 +81,10 @@ CONV_SHAPES = [
                              # ragged column tile); 3-channel data gradient in two groups
                              # over an odd number of chunks
     (3, 2, 5, 38, 12),       # the same with an odd width (element-wise stores)
+    (2, 12, 5, 38, 3),       # at most 4 output channels (vector-ALU kernel): forward
+    (3, 20, 9, 33, 1),       # with bias and ReLU, ragged row and column tiles, a
+    (2, 16, 8, 40, 4),       # partial last channel chunk; 1, 2, 3 and 4 channels
+    (1, 9, 3, 64, 2),
     (1, 1, 1, 1, 1),         # degenerate: every tap but the centre is padding
     (1, 9, 3, 1, 5),
 ]
@@ -284,7 +288,8 @@ def test_conv_bwd_weight_bf16_staging(shape, offset):
 
 
 PACKED_SHAPES = [(8, 3, 32, 32, 64), (2, 5, 7, 9, 70), (9, 40, 4, 4, 72), (33, 20, 2, 2, 130),
-                 (2, 64, 6, 40, 80), (2, 36, 20, 20, 64), (2, 48, 14, 14, 64), (2, 12, 5, 37, 17)]
+                 (2, 64, 6, 40, 80), (2, 36, 20, 20, 64), (2, 48, 14, 14, 64), (2, 12, 5, 37, 17),
+                 (2, 12, 5, 38, 3)]
 
 
 @pytest.mark.parametrize("dtype", DTYPES)
