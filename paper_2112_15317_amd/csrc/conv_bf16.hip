@@ -205,21 +205,28 @@ __global__ __launch_bounds__(256, 2) void conv3x3_igemm_bf16(ConvArgs a) {
   auto compute = [&](int buf) {
     const u16* X = ldsb + buf * T::LDS_BUF;
     const u16* Wl = X + T::LDS_X;
-#pragma unroll
-    for (int t = 0; t < 9; ++t) {
+    // The operands of tap t + 1 are read before tap t's MFMAs are issued,
+    // so each read has a whole tap's MFMAs to arrive under.
+    s8 fa[2][T::NB], fb[2][T::MB];
+    auto rd = [&](int t, int s) {
       const int toff = T::hp(0, t / 3, t % 3) * 8;
-      s8 fa[T::NB], fb[T::MB];
 #pragma unroll
       for (int nb = 0; nb < T::NB; ++nb)
-        fa[nb] = *reinterpret_cast<const s8*>(Wl + ((t * 2 + lh) * T::BN + nb * 32 + lc) * 8);
+        fa[s][nb] = *reinterpret_cast<const s8*>(Wl + ((t * 2 + lh) * T::BN + nb * 32 + lc) * 8);
 #pragma unroll
       for (int mb = 0; mb < T::MB; ++mb)
-        fb[mb] = *reinterpret_cast<const s8*>(X + b_off[mb] + toff);
+        fb[s][mb] = *reinterpret_cast<const s8*>(X + b_off[mb] + toff);
+    };
+    rd(0, 0);
+#pragma unroll
+    for (int t = 0; t < 9; ++t) {
+      if (t + 1 < 9) rd(t + 1, (t + 1) & 1);
+      __builtin_amdgcn_sched_barrier(0);   // keep those reads ahead of the MFMAs
 #pragma unroll
       for (int nb = 0; nb < T::NB; ++nb)
 #pragma unroll
         for (int mb = 0; mb < T::MB; ++mb)
-          acc[nb][mb] = mfma32x32x16bf16(fa[nb], fb[mb], acc[nb][mb]);
+          acc[nb][mb] = mfma32x32x16bf16(fa[t & 1][nb], fb[t & 1][mb], acc[nb][mb]);
     }
   };
 
@@ -466,21 +473,28 @@ __global__ __launch_bounds__(256, 2) void conv3x3_c8_bf16(ConvArgs a) {
   auto compute = [&](int buf) {
     const u16* X = ldsb + buf * T::LDS_BUF;
     const u16* Wl = X + T::LDS_X;
-#pragma unroll
-    for (int t = 0; t < 9; ++t) {
+    // The operands of tap t + 1 are read before tap t's MFMAs are issued,
+    // so each read has a whole tap's MFMAs to arrive under.
+    s8 fa[2][T::NB], fb[2][T::MB];
+    auto rd = [&](int t, int s) {
       const int toff = T::hp(0, t / 3, t % 3) * 8;
-      s8 fa[T::NB], fb[T::MB];
 #pragma unroll
       for (int nb = 0; nb < T::NB; ++nb)
-        fa[nb] = *reinterpret_cast<const s8*>(Wl + ((t * 2 + lh) * T::BN + nb * 32 + lc) * 8);
+        fa[s][nb] = *reinterpret_cast<const s8*>(Wl + ((t * 2 + lh) * T::BN + nb * 32 + lc) * 8);
 #pragma unroll
       for (int mb = 0; mb < T::MB; ++mb)
-        fb[mb] = *reinterpret_cast<const s8*>(X + b_off[mb] + toff);
+        fb[s][mb] = *reinterpret_cast<const s8*>(X + b_off[mb] + toff);
+    };
+    rd(0, 0);
+#pragma unroll
+    for (int t = 0; t < 9; ++t) {
+      if (t + 1 < 9) rd(t + 1, (t + 1) & 1);
+      __builtin_amdgcn_sched_barrier(0);   // keep those reads ahead of the MFMAs
 #pragma unroll
       for (int nb = 0; nb < T::NB; ++nb)
 #pragma unroll
         for (int mb = 0; mb < T::MB; ++mb)
-          acc[nb][mb] = mfma32x32x16bf16(fa[nb], fb[mb], acc[nb][mb]);
+          acc[nb][mb] = mfma32x32x16bf16(fa[t & 1][nb], fb[t & 1][mb], acc[nb][mb]);
     }
   };
 

@@ -1074,12 +1074,21 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_c8(WgArgs a) {
     // the next 4 (of which the first 2 are used; a lane whose columns would
     // pass the row's end reads its last column instead), and the windows at
     // offsets 1 and 2 are shifted out of those 12 values in registers.
-#pragma unroll
-    for (int r = 0; r < 3; ++r) {
-      const s8 b0 = tr_read8(Xl, T::XP, wc * 16, [&](int j) { return (yy + r) * T::HWD + xx + j; });
-      const v4s nx = tr_read4(Xl, T::XP, wc * 16, [&](int j) {
+    s8 rb[3];
+    v4s rn[3];
+    auto rrow = [&](int r) {
+      rb[r] = tr_read8(Xl, T::XP, wc * 16, [&](int j) { return (yy + r) * T::HWD + xx + j; });
+      rn[r] = tr_read4(Xl, T::XP, wc * 16, [&](int j) {
         return (yy + r) * T::HWD + min(xx + 8 + j, T::HWD - 1);
       });
+    };
+    rrow(0);
+#pragma unroll
+    for (int r = 0; r < 3; ++r) {
+      if (r + 1 < 3) rrow(r + 1);
+      __builtin_amdgcn_sched_barrier(0);
+      const s8 b0 = rb[r];
+      const v4s nx = rn[r];
       const s8 b1 = s8{b0[1], b0[2], b0[3], b0[4], b0[5], b0[6], b0[7], nx[0]};
       const s8 b2 = s8{b0[2], b0[3], b0[4], b0[5], b0[6], b0[7], nx[0], nx[1]};
 #pragma unroll
