@@ -273,6 +273,9 @@ __global__ __launch_bounds__(256, 2) void gemm_f32(GemmArgs g) {
         frag32<BM, A_KC, T::RB>(A, wm * (BM / 2), c + 1, h, l32, na);
         frag32<BN, B_KC, T::CB>(B, wn * (BN / 2), c + 1, h, l32, nb);
       }
+      // Keep those reads ahead of this chunk's MFMAs (the scheduler would
+      // otherwise sink them next to their first use).
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int j = 0; j < 4; ++j)
 #pragma unroll
