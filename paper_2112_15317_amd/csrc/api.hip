@@ -16,10 +16,11 @@ void conv_igemm_pack(bool dgrad, int dtype, int N, int Cin, int H, int W, int Co
 sb_status conv_igemm(bool dgrad, int dtype, int N, int Cin, int H, int W, int Cout,
                      const void* in, const void* wt, const float* bias, const void* mask,
                      void* out, void* ws, size_t ws_bytes, int relu, bool prepacked,
-                     hipStream_t st);
+                     hipStream_t st, uint8_t* pool_idx = nullptr);
+bool conv_igemm_pools(int dtype, int N, int Cin, int H, int W, int Cout);
 size_t conv_wgrad_ws(int dtype, int N, int C, int H, int W, int K);
 int conv_igemm_describe(bool dgrad, int dtype, int N, int Cin, int H, int W, int Cout, char* buf,
-                        size_t len);
+                        size_t len, bool pool = false);
 int conv_wgrad_describe(int dtype, int N, int C, int H, int W, int K, char* buf, size_t len);
 sb_status conv_wgrad(int dtype, int N, int C, int H, int W, int K, const void* x, const void* dy,
                      float* dw, float* db, void* ws, size_t ws_bytes, hipStream_t st);
@@ -73,11 +74,13 @@ static sb_status conv_check(const sb_conv3x3_desc* d, int pass) {
     if (!ok) return SB_ERR_UNSUPPORTED;
   }
   if (pass == SB_PASS_FWD_POOL) {
-    // Forward with fused ReLU + 2x2 pooling: channel-blocked bf16, even
-    // image sizes, an unsplit channel loop.
+    // Forward with fused ReLU + 2x2 pooling: channel-blocked bf16 or NCHW
+    // fp32, even image sizes, an unsplit channel loop.
     if (d->h % 2 || d->w % 2) return SB_ERR_INVALID_ARG;
-    if (d->layout != SB_NCHW8C) return SB_ERR_UNSUPPORTED;
-    if (!sbh::conv_bf16c8_pools(d->n, d->c, d->h, d->w, d->k)) return SB_ERR_UNSUPPORTED;
+    const bool ok = d->layout == SB_NCHW8C
+                        ? sbh::conv_bf16c8_pools(d->n, d->c, d->h, d->w, d->k)
+                        : sbh::conv_igemm_pools(d->dtype, d->n, d->c, d->h, d->w, d->k);
+    if (!ok) return SB_ERR_UNSUPPORTED;
   }
   // Kernels index weights and activations with 32-bit ints.
   if ((int64_t)d->k * d->c * 9 >= (1ll << 31)) return SB_ERR_UNSUPPORTED;
@@ -237,8 +240,11 @@ extern "C" sb_status sb_conv3x3_fwd_pool(const sb_conv3x3_desc* d, const void* x
                sbh::overlaps(ws, need, idx, ib) || sbh::overlaps(ws, need, w, wb) ||
                sbh::overlaps(ws, need, bias, bb)))
     return SB_ERR_INVALID_ARG;
-  return sbh::conv_bf16c8(false, d->n, d->c, d->h, d->w, d->k, x, w, bias, nullptr, y, ws,
-                          ws_bytes, 0, pk, sbh::stream_of(stream), idx);
+  if (d->layout == SB_NCHW8C)
+    return sbh::conv_bf16c8(false, d->n, d->c, d->h, d->w, d->k, x, w, bias, nullptr, y, ws,
+                            ws_bytes, 0, pk, sbh::stream_of(stream), idx);
+  return sbh::conv_igemm(false, d->dtype, d->n, d->c, d->h, d->w, d->k, x, w, bias, nullptr, y,
+                         ws, ws_bytes, 0, pk, sbh::stream_of(stream), idx);
 }
 
 extern "C" sb_status sb_conv3x3_bwd_data(const sb_conv3x3_desc* d, const void* dy, const void* w,
@@ -370,6 +376,9 @@ extern "C" size_t sb_conv3x3_plan_string(const sb_conv3x3_desc* d, int pass, cha
       break;
     case SB_PASS_BWD_DATA:
       r = sbh::conv_igemm_describe(true, d->dtype, d->n, d->k, d->h, d->w, d->c, buf, len);
+      break;
+    case SB_PASS_FWD_POOL:
+      r = sbh::conv_igemm_describe(false, d->dtype, d->n, d->c, d->h, d->w, d->k, buf, len, true);
       break;
     default: r = sbh::conv_wgrad_describe(d->dtype, d->n, d->c, d->h, d->w, d->k, buf, len); break;
   }

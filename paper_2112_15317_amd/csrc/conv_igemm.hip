@@ -58,6 +58,7 @@
 
 #include <algorithm>
 #include <cstdio>
+#include <cstring>
 #include <type_traits>
 
 namespace sb {
@@ -141,10 +142,18 @@ __device__ constexpr bool igemm_pad_block(int wm, int mb, int tap) {
 
 // WHOLE_H: every tile spans the whole image height (H = TH); the MFMAs of
 // column blocks whose taps read only padding rows are skipped.
-template <class T, bool DGRAD, class E, bool WHOLE_H = false>
+// POOL (forward of fp32 tensors, unsplit, staged tiles): the output tile is
+// not written; ReLU and 2x2 max pooling run on it in LDS (bias added: the
+// tensor the unfused forward would write), and the pooled tile and its
+// window codes go out instead (a.out, a.pool_idx), as sb_relu_maxpool_fwd
+// computes them from that tensor.
+template <class T, bool DGRAD, class E, bool WHOLE_H = false, bool POOL = false>
 __global__ __launch_bounds__(T::THREADS, 2 / T::KSPLIT) void conv3x3_igemm_f32(ConvArgs a) {
   static_assert(!WHOLE_H || (T::TW * T::IMGS) % 16 == 0,
                 "column blocks must not straddle tile rows");
+  static_assert(!POOL || (!DGRAD && T::STAGED && std::is_same<E, float>::value &&
+                          T::TH % 2 == 0 && T::TW % 2 == 0),
+                "pooling: fp32 forward, staged tiles of whole 2x2 windows");
   extern __shared__ float lds_all[];
 
   // grp: which chunk stream this thread's 256-thread group takes.
@@ -379,6 +388,37 @@ __global__ __launch_bounds__(T::THREADS, 2 / T::KSPLIT) void conv3x3_igemm_f32(C
         }
       }
       __syncthreads();
+      if constexpr (POOL) {
+        // Pooled pixel q = (channel, image, pooled row, pooled column),
+        // pooled columns fastest: per channel the first maximum in row-major
+        // window order wins (strict >), the output is the maximum if it is
+        // positive, else +0, and bit 7 of the code flags the latter.
+        constexpr int PTH = T::TH / 2, PTW = T::TW / 2, PP = T::IMGS * PTH * PTW;
+        static_assert(T::BN * PP % T::THREADS == 0, "whole rounds of pooled pixels");
+        const int Hh = a.H / 2, Wh = a.W / 2;
+#pragma unroll 4
+        for (int j = 0; j < T::BN * PP / T::THREADS; ++j) {
+          const int q = (int)threadIdx.x + T::THREADS * j;
+          const int col = q / PP, pp = q % PP;
+          const int img = pp / (PTH * PTW), r = pp % (PTH * PTW);
+          const int py = r / PTW, px = r % PTW;
+          const int n = n0 + img, oh = h0 / 2 + py, ow = w0 / 2 + px, co = co0 + col;
+          if (n >= a.N || oh >= Hh || ow >= Wh || co >= a.Cout) continue;
+          const float* l = lds_all + col * EP + (img * T::TH + 2 * py) * T::TW + 2 * px;
+          const float bv = a.bias ? a.bias[co] : 0.f;
+          const float v[4] = {l[0] + bv, l[1] + bv, l[T::TW] + bv, l[T::TW + 1] + bv};
+          float m = v[0];
+          uint32_t c = 0;
+#pragma unroll
+          for (int k = 1; k < 4; ++k)
+            if (v[k] > m) { m = v[k]; c = (uint32_t)k; }
+          const bool pos = m > 0.f;
+          const size_t off = (((size_t)n * a.Cout + co) * Hh + oh) * Wh + ow;
+          ((float*)a.out)[off] = pos ? m : 0.f;
+          a.pool_idx[off] = (uint8_t)(c | (pos ? 0u : 0x80u));
+        }
+        return;
+      }
       constexpr int QPR = T::BM / 4;                 // 4-pixel pieces per channel row
       static_assert(T::BN * QPR % T::THREADS == 0, "whole rounds of pieces");
       const bool vec = std::is_same<E, float>::value && a.W % 4 == 0 &&
@@ -916,10 +956,19 @@ constexpr bool has_whole_h() {
   else return T::TH == 8 && T::TW == 8;
 }
 
+// Tiles whose forward can pool in its epilogue (fp32, staged output tile of
+// whole 2x2 windows).
+template <class T, bool SMALL, class E>
+constexpr bool can_pool() {
+  if constexpr (SMALL) return false;
+  else return T::STAGED && std::is_same<E, float>::value && T::TH % 2 == 0 && T::TW % 2 == 0;
+}
+
 template <class T, bool DGRAD, bool SMALL, class E>
 static void igemm_launch(const IgemmPlan& p, const ConvArgs& a, bool pack, hipStream_t st) {
   static bool attr_set = false;
   constexpr bool can_whole = has_whole_h<T, SMALL>();
+  constexpr bool pool_ok = !DGRAD && can_pool<T, SMALL, E>();
   const bool whole = can_whole && a.H == 8;
   if (!attr_set) {
     if constexpr (SMALL) {
@@ -932,6 +981,15 @@ static void igemm_launch(const IgemmPlan& p, const ConvArgs& a, bool pack, hipSt
         (void)hipFuncSetAttribute((const void*)conv3x3_igemm_f32<T, DGRAD, E, true>,
                                   hipFuncAttributeMaxDynamicSharedMemorySize,
                                   (int)T::LDS_BYTES);
+      if constexpr (pool_ok) {
+        (void)hipFuncSetAttribute((const void*)conv3x3_igemm_f32<T, false, E, false, true>,
+                                  hipFuncAttributeMaxDynamicSharedMemorySize,
+                                  (int)T::LDS_BYTES);
+        if constexpr (can_whole)
+          (void)hipFuncSetAttribute((const void*)conv3x3_igemm_f32<T, false, E, true, true>,
+                                    hipFuncAttributeMaxDynamicSharedMemorySize,
+                                    (int)T::LDS_BYTES);
+      }
     }
     attr_set = true;
   }
@@ -941,6 +999,18 @@ static void igemm_launch(const IgemmPlan& p, const ConvArgs& a, bool pack, hipSt
   dim3 grid(p.grid_x, p.co_tiles, p.splits);
   ConvArgs k = a;
   if (p.splits > 1) { k.bias = nullptr; k.mask = nullptr; k.relu = 0; }
+  if (a.pool_idx) {                        // the caller checked the plan can pool
+    if constexpr (pool_ok) {
+      if constexpr (can_whole) {
+        if (whole) {
+          conv3x3_igemm_f32<T, false, E, true, true><<<grid, T::THREADS, T::LDS_BYTES, st>>>(k);
+          return;
+        }
+      }
+      conv3x3_igemm_f32<T, false, E, false, true><<<grid, T::THREADS, T::LDS_BYTES, st>>>(k);
+    }
+    return;
+  }
   if constexpr (SMALL) {
     conv3x3_small_f32<T, DGRAD, E><<<grid, T::THREADS, T::LDS_BYTES, st>>>(k);
   } else {
@@ -962,6 +1032,23 @@ static void igemm_launch(const IgemmPlan& p, const ConvArgs& a, bool pack, hipSt
 // (and its packed filters) take the vector-ALU kernel, in the whole
 // reduction: 8 x 32-pixel tiles, no split.
 inline bool few_takes(const IgemmPlan& p, int Cout) { return p.tile == 6 && Cout <= 4; }
+
+// Whether an fp32 forward on plan p can pool in its epilogue: one split and
+// a staged tile of whole 2x2 windows (not the few-channel kernel).
+inline bool igemm_pools(const IgemmPlan& p, int Cout) {
+  if (p.splits != 1 || few_takes(p, Cout)) return false;
+  switch (p.tile) {
+    case 0: return can_pool<TileW32, false, float>();
+    case 1: return can_pool<TileW16, false, float>();
+    case 2: return can_pool<TileW8, false, float>();
+    case 5: return can_pool<TileW32c4, false, float>();
+    case 9: return can_pool<TileW32L, false, float>();
+    case 10: return can_pool<TileW16L, false, float>();
+    case 11: return can_pool<TileW8L, false, float>();
+    case 12: return can_pool<TileW8K2, false, float>();
+    default: return false;
+  }
+}
 
 template <bool DGRAD, class E>
 static void few_launch(const IgemmPlan& p, const ConvArgs& a, bool pack, hipStream_t st) {
@@ -1104,8 +1191,17 @@ void conv_igemm_pack(bool dgrad, int dtype, int N, int Cin, int H, int W, int Co
   }
 }
 
+// Whether sb_conv3x3_fwd_pool takes an NCHW forward of this shape: fp32,
+// even image sizes, and a plan that pools for aligned and unaligned tensors.
+bool conv_igemm_pools(int dtype, int N, int Cin, int H, int W, int Cout) {
+  if (dtype != SB_F32 || H % 2 || W % 2) return false;
+  for (bool aligned : {true, false})
+    if (!sb::igemm_pools(sb::igemm_plan(N, Cin, H, W, Cout, 4, aligned), Cout)) return false;
+  return true;
+}
+
 int conv_igemm_describe(bool dgrad, int dtype, int N, int Cin, int H, int W, int Cout,
-                        char* buf, size_t len) {
+                        char* buf, size_t len, bool pool) {
   if (dtype == SB_BF16 && conv_bf16_takes(N, Cin, H, W, Cout))
     return conv_bf16_describe(dgrad, N, Cin, H, W, Cout, buf, len);
   sb::IgemmPlan p = sb::igemm_plan(N, Cin, H, W, Cout, (int)dsize(dtype));
@@ -1115,13 +1211,20 @@ int conv_igemm_describe(bool dgrad, int dtype, int N, int Cin, int H, int W, int
                     sb::cdiv(W, sb::FewTile::TW) * sb::cdiv(H, sb::FewTile::TH) * N);
   char name[160];
   snprintf(name, sizeof(name), sb::kTileNames[p.tile], dgrad ? "true" : "false", et);
+  if (pool) {
+    // The pooled instantiation: conv3x3_igemm_f32<T, false, float, WHOLE_H, true>.
+    const size_t l = strlen(name);
+    if (l > 0 && name[l - 1] == '>')
+      snprintf(name + l - 1, sizeof(name) - (l - 1), ", %s, true>",
+               H == 8 && (p.tile == 2 || p.tile == 11 || p.tile == 12) ? "true" : "false");
+  }
   return snprintf(buf, len, "%s grid=%dx%dx%d", name, p.grid_x, p.co_tiles, p.splits);
 }
 
 sb_status conv_igemm(bool dgrad, int dtype, int N, int Cin, int H, int W, int Cout,
                      const void* in, const void* wt, const float* bias, const void* mask,
                      void* out, void* ws, size_t ws_bytes, int relu, bool prepacked,
-                     hipStream_t st) {
+                     hipStream_t st, uint8_t* pool_idx) {
   if (dtype == SB_BF16 && conv_bf16_takes(N, Cin, H, W, Cout))
     return conv_bf16(dgrad, N, Cin, H, W, Cout, in, wt, bias, mask, out, ws, ws_bytes, relu,
                      prepacked, st);
@@ -1146,6 +1249,12 @@ sb_status conv_igemm(bool dgrad, int dtype, int N, int Cin, int H, int W, int Co
   a.N = N; a.Cin = Cin; a.H = H; a.W = W; a.Cout = Cout;
   a.tiles_w = p.tiles_w; a.tiles_h = p.tiles_h;
   a.nchunks = p.nchunks; a.chunks_per_split = p.cps; a.splits = p.splits; a.relu = relu;
+  if (pool_idx) {
+    // Pooled forward: the caller checked conv_igemm_pools (fp32, unsplit,
+    // a staged tile); ReLU comes with the pooling.
+    if (dgrad || relu || !sb::igemm_pools(p, Cout)) return SB_ERR_UNSUPPORTED;
+    a.pool_idx = pool_idx;
+  }
   if (dtype == SB_BF16) {
     if (dgrad) sb::igemm_dispatch<true, sb::u16>(p, a, !prepacked, st);
     else sb::igemm_dispatch<false, sb::u16>(p, a, !prepacked, st);

@@ -84,9 +84,9 @@ class ConvStack:
         every result is the unpadded network's).
 
         fuse_pool: a pooled layer whose forward can pool in the kernel
-        (sb_conv3x3_fwd_pool: channel-blocked, unsplit) runs its forward,
-        ReLU and pooling as one call and has no Z buffer (``self.fused``
-        lists those layers)."""
+        (sb_conv3x3_fwd_pool takes its descriptor: channel-blocked bf16 or
+        NCHW fp32, an unsplit plan) runs its forward, ReLU and pooling as one
+        call and has no Z buffer (``self.fused`` lists those layers)."""
         self.layers = conv_layers(schedule, in_ch, hw)
         if not self.layers[-1].pool_after:
             raise ValueError("the stack must end with a pooled layer")
@@ -186,13 +186,12 @@ class ConvStack:
     def fused_layers(schedule, n, in_ch, hw, dtype="f32", layout="nchw", packed=True):
         """Indices of the pooled layers whose forward pools in the kernel
         (sb_conv3x3_fwd_pool takes their descriptor): host-side queries only."""
-        if layout != "c8":
-            return set()
+        c8 = layout == "c8"
         out = set()
         for l in conv_layers(schedule, in_ch, hw):
-            c = -(-l.c // 8) * 8
+            c = -(-l.c // 8) * 8 if c8 else l.c
             d = sb.conv_desc(n, c, l.h, l.w, l.k, _code(dtype), packed=packed,
-                             layout=sb.SB_NCHW8C)
+                             layout=sb.SB_NCHW8C if c8 else sb.SB_NCHW)
             if l.pool_after and \
                     sb.sb_conv3x3_workspace_bytes(d, sb.SB_PASS_FWD_POOL) != sb.SIZE_MAX:
                 out.add(l.index)

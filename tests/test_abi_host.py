@@ -267,9 +267,10 @@ def test_model_average_replicas_argument_validation():
 
 
 def test_fused_forward_pool_validation():
-    """sb_conv3x3_fwd_pool: channel-blocked bf16 with even sizes and an
-    unsplit plan; the pass-3 workspace query says which descriptors it
-    takes, with the forward's workspace; nothing is launched on an error."""
+    """sb_conv3x3_fwd_pool: channel-blocked bf16 or NCHW fp32 with even
+    sizes and an unsplit plan; the pass-3 workspace query says which
+    descriptors it takes, with the forward's workspace; nothing is launched
+    on an error."""
     c8 = lambda n, c, h, w, k, **kw: sb.conv_desc(n, c, h, w, k, sb.SB_BF16,
                                                   layout=sb.SB_NCHW8C, **kw)
     ok = c8(32, 64, 224, 224, 64)          # 6272 tiles: one split
@@ -291,6 +292,18 @@ def test_fused_forward_pool_validation():
     assert fwd_pool(ok, x, w, y, None, ws, need) == sb.SB_ERR_INVALID_ARG
     assert fwd_pool(ok, x, w, y, y + 64, ws, need) == sb.SB_ERR_INVALID_ARG   # idx over y
     assert fwd_pool(ok, x, w, x + 64, idx, ws, need) == sb.SB_ERR_INVALID_ARG  # y over x
+    # NCHW fp32 pools in the kernel on unsplit plans too (not bf16 NCHW, not
+    # the split plans of small batches or of the 4x4 and 2x2 images).
+    f32 = sb.conv_desc(128, 64, 32, 32, 64, sb.SB_F32)
+    assert sb.sb_conv3x3_workspace_bytes(f32, sb.SB_PASS_FWD_POOL) == \
+        sb.sb_conv3x3_workspace_bytes(f32, sb.SB_PASS_FWD)
+    assert sb.sb_conv3x3_plan_string(f32, sb.SB_PASS_FWD_POOL).split(" grid")[0].endswith(
+        ", true>")
+    for bad in (sb.conv_desc(2, 64, 32, 32, 64, sb.SB_F32),
+                sb.conv_desc(128, 512, 4, 4, 512, sb.SB_F32),
+                sb.conv_desc(128, 512, 2, 2, 512, sb.SB_F32)):
+        assert sb.sb_conv3x3_workspace_bytes(bad, sb.SB_PASS_FWD_POOL) == sb.SIZE_MAX
+        assert fwd_pool(bad, x, w, y, idx, ws, need) == sb.SB_ERR_UNSUPPORTED
     # A plan that splits the channel loop cannot pool in the kernel.
     split = c8(1, 512, 14, 14, 512)
     splits = int(sb.sb_conv3x3_plan_string(split, sb.SB_PASS_FWD).rsplit("x", 1)[1])

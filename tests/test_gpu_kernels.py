@@ -360,6 +360,49 @@ def test_conv_pack_filters_many_matches_single(dtype):
         assert torch.equal(many, one), (d.n, d.c, d.h, d.w, d.k, p_)
 
 
+# Forward with fused ReLU + 2x2 pooling on NCHW fp32 (sb_conv3x3_fwd_pool):
+# shapes whose plan is one split: 4x32 tiles, 8x16 tiles with two channel
+# tiles, the two-group 8x8 tiles on whole 8x8 images, and the same tiles
+# over 14x14 images (ragged tiles, a ragged pooled edge).
+FUSED_F32_SHAPES = [(64, 64, 32, 32, 64), (128, 64, 16, 16, 128), (128, 128, 8, 8, 256),
+                    (128, 64, 14, 14, 64)]
+
+
+@pytest.mark.parametrize("shape", FUSED_F32_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_conv_fwd_pool_f32(shape):
+    """The fused call equals, bit for bit, the forward then the pool kernel
+    (the same sums, pooled by the same rule), and against the oracle the
+    pooled values meet 1e-4 and every differing code is a certified near-tie
+    of the oracle's window values (the two sides' sums differ in their last
+    bits)."""
+    from tests.chain import NEAR_TIE_REL, near_tie_flips
+    n, c, h, w, k = shape
+    print_case("conv_fwd_pool_f32", shape=shape)
+    x, wt, b, _, _ = _conv_inputs(n, c, h, w, k, 62)
+    d = sb.conv_desc(n, c, h, w, k, sb.SB_F32)
+    need = sb.sb_conv3x3_workspace_bytes(d, sb.SB_PASS_FWD_POOL)
+    assert need != sb.SIZE_MAX, "planned as one split"
+    ws = _ws(need)
+    xd, wd, bd = to_dev(x), to_dev(wt), to_dev(b)
+    pooled = (n, k, h // 2, w // 2)
+    y = torch.full(pooled, float("nan"), device="cuda")
+    idx = torch.full(pooled, 0x55, dtype=torch.uint8, device="cuda")
+    sb.sb_conv3x3_fwd_pool(d, xd, wd, bd, y, idx, ws)
+    z = torch.full((n, k, h, w), float("nan"), device="cuda")
+    y2 = torch.full(pooled, float("nan"), device="cuda")
+    idx2 = torch.full(pooled, 0x55, dtype=torch.uint8, device="cuda")
+    sb.sb_conv3x3_fwd(d, xd, wd, bd, z, _ws(sb.sb_conv3x3_workspace_bytes(d, sb.SB_PASS_FWD)))
+    sb.sb_relu_maxpool_fwd(n, k, h, w, sb.SB_F32, sb.SB_NCHW, z, y2, idx2)
+    torch.cuda.synchronize()
+    assert torch.equal(idx, idx2), "codes differ from the unfused forward and pool"
+    assert torch.equal(y.view(torch.int32), y2.view(torch.int32)), "pooled values differ"
+    zr = O.conv3x3_fwd(x, wt, b)
+    ry, ridx = O.relu_maxpool_fwd(zr)
+    assert rel_l2(to_host(y), ry) <= TOL["f32"]
+    flips = near_tie_flips(zr, ridx, idx.cpu().numpy(), NEAR_TIE_REL["f32"] * np.max(np.abs(zr)))
+    print("near-tie windows:", flips)
+
+
 def test_conv_bwd_weight_without_bias_grad():
     n, c, h, w, k = 2, 8, 6, 6, 20
     x, _, _, dy, _ = _conv_inputs(n, c, h, w, k, 14)
