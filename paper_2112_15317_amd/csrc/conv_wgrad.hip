@@ -981,6 +981,7 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_c8(WgArgs a) {
   const int pt1 = min(a.ptiles, pt0 + a.tiles_per_split);
   const int wc = wave % T::WC, wp = (wave / T::WC) % T::WP, wk = wave / (T::WC * T::WP);
   const bool do_db = (a.db != nullptr) && ct == 0 && wc == 0;
+  const bool do_db_w = __builtin_amdgcn_readfirstlane(do_db ? 1 : 0) != 0;
   const int HWs = a.H * a.W, KB = a.K / 8, CB = a.C / 8;
 
   f4 acc[T::MA][9];
@@ -1103,6 +1104,8 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_c8(WgArgs a) {
     }
     typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
     const bf16x2 one2 = {(__bf16)1.0f, (__bf16)1.0f};
+    // Only the waves that write db sum it (the same for a whole wave).
+    if (do_db_w)
 #pragma unroll
     for (int m = 0; m < T::MA; ++m) {
       const bf16x8 v = __builtin_bit_cast(bf16x8, av[m]);
