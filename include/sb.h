@@ -162,10 +162,11 @@ sb_status sb_conv3x3_fwd(const sb_conv3x3_desc *desc, const void *x,
  * without SB_FUSE_RELU (bias added, rounded to the storage type), then
  * y and idx exactly as sb_relu_maxpool_fwd computes them from z.  y is
  * [n][k][h/2][w/2] and idx one byte per element of y, both in desc->layout.
- * Supported for SB_NCHW8C bf16 and SB_NCHW fp32 with even h and w when the
- * forward's channel loop is not split and its tile holds whole 2x2 windows
- * (sb_conv3x3_workspace_bytes(desc, SB_PASS_FWD_POOL) is then not
- * (size_t)-1): SB_ERR_UNSUPPORTED otherwise, SB_ERR_INVALID_ARG
+ * Supported with even h and w for SB_NCHW8C bf16 when the forward's channel
+ * loop is not split, and for SB_NCHW fp32 (an unsplit plan pools in the
+ * kernel, a split one in its split reduction; not the few-output-channel
+ * kernel): sb_conv3x3_workspace_bytes(desc, SB_PASS_FWD_POOL) is then not
+ * (size_t)-1.  SB_ERR_UNSUPPORTED otherwise, SB_ERR_INVALID_ARG
  * for odd h or w, SB_FUSE_RELU, NULL pointers or overlapping outputs.
  * With SB_PACKED_FILTERS, w is the forward packing (SB_PASS_FWD). */
 sb_status sb_conv3x3_fwd_pool(const sb_conv3x3_desc *desc, const void *x,

@@ -328,6 +328,51 @@ __global__ __launch_bounds__(256) void conv_splitk_reduce4(
   }
 }
 
+// Split reduction of a forward pooled in the same call (NCHW, even H and
+// W): per pooled output, the window's four sums over the splits in
+// increasing order (conv_splitk_reduce4's order) plus the bias, then ReLU
+// and 2x2 max pooling as relu_maxpool_fwd takes them: the first maximum in
+// row-major window order (strict >), the maximum if positive, else +0, and
+// bit 7 of the code for the latter.
+template <class E, bool VEC>
+__global__ __launch_bounds__(256) void conv_splitk_reduce_pool(
+    const float* __restrict__ part, int splits, size_t total, int Cout, int H, int W,
+    const float* __restrict__ bias, E* __restrict__ out, uint8_t* __restrict__ idx) {
+  const int Hh = H / 2, Wh = W / 2;
+  const size_t q = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (q >= total / 4) return;
+  const int ow = (int)(q % Wh);
+  const size_t r = q / Wh;
+  const int oh = (int)(r % Hh);
+  const size_t nc = r / Hh;                               // n * Cout + co
+  // The window's two rows are pairs of adjacent floats (W and the window's
+  // first column even), read as 8-byte pieces when the partials are 8-byte
+  // aligned (VEC).
+  const size_t p0 = (nc * H + 2 * oh) * W + 2 * ow;
+  const float bv = bias ? bias[nc % Cout] : 0.f;
+  typedef float f2 __attribute__((ext_vector_type(2)));
+  f2 top = {0.f, 0.f}, bot = {0.f, 0.f};
+  for (int sp = 0; sp < splits; ++sp) {
+    const float* ps = part + (size_t)sp * total;
+    if (VEC) {
+      top += *reinterpret_cast<const f2*>(ps + p0);
+      bot += *reinterpret_cast<const f2*>(ps + p0 + W);
+    } else {
+      top += f2{ps[p0], ps[p0 + 1]};
+      bot += f2{ps[p0 + W], ps[p0 + W + 1]};
+    }
+  }
+  const float v[4] = {top[0] + bv, top[1] + bv, bot[0] + bv, bot[1] + bv};
+  float m = v[0];
+  uint32_t c = 0;
+#pragma unroll
+  for (int k = 1; k < 4; ++k)
+    if (v[k] > m) { m = v[k]; c = (uint32_t)k; }
+  const bool pos = m > 0.f;
+  Elem<E>::store(out, q, pos ? m : 0.f);
+  idx[q] = (uint8_t)(c | (pos ? 0u : 0x80u));
+}
+
 // Launches the split reduction of a convolution pass: the 4-wide form when
 // the sizes allow, else one output per lane.
 template <class E, bool C8 = false>

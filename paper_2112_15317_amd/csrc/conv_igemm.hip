@@ -999,7 +999,7 @@ static void igemm_launch(const IgemmPlan& p, const ConvArgs& a, bool pack, hipSt
   dim3 grid(p.grid_x, p.co_tiles, p.splits);
   ConvArgs k = a;
   if (p.splits > 1) { k.bias = nullptr; k.mask = nullptr; k.relu = 0; }
-  if (a.pool_idx) {                        // the caller checked the plan can pool
+  if (a.pool_idx && p.splits == 1) {       // the caller checked the plan can pool
     if constexpr (pool_ok) {
       if constexpr (can_whole) {
         if (whole) {
@@ -1023,8 +1023,16 @@ static void igemm_launch(const IgemmPlan& p, const ConvArgs& a, bool pack, hipSt
   }
   if (p.splits > 1) {
     size_t total = (size_t)a.N * a.Cout * a.H * a.W;
-    launch_splitk_reduce<E>(a.part, p.splits, total, a.Cout, a.H * a.W, a.bias, a.relu,
-                            (const E*)a.mask, (E*)a.out, st);
+    const unsigned pg = (unsigned)((total / 4 + 255) / 256);
+    if (a.pool_idx && ((uintptr_t)a.part & 7) == 0)   // pooled forward: the reduction pools
+      conv_splitk_reduce_pool<E, true><<<pg, 256, 0, st>>>(
+          a.part, p.splits, total, a.Cout, a.H, a.W, a.bias, (E*)a.out, a.pool_idx);
+    else if (a.pool_idx)
+      conv_splitk_reduce_pool<E, false><<<pg, 256, 0, st>>>(
+          a.part, p.splits, total, a.Cout, a.H, a.W, a.bias, (E*)a.out, a.pool_idx);
+    else
+      launch_splitk_reduce<E>(a.part, p.splits, total, a.Cout, a.H * a.W, a.bias, a.relu,
+                              (const E*)a.mask, (E*)a.out, st);
   }
 }
 
@@ -1033,10 +1041,12 @@ static void igemm_launch(const IgemmPlan& p, const ConvArgs& a, bool pack, hipSt
 // reduction: 8 x 32-pixel tiles, no split.
 inline bool few_takes(const IgemmPlan& p, int Cout) { return p.tile == 6 && Cout <= 4; }
 
-// Whether an fp32 forward on plan p can pool in its epilogue: one split and
-// a staged tile of whole 2x2 windows (not the few-channel kernel).
+// Whether an fp32 forward on plan p can pool in the call: a split plan
+// pools in its split reduction; an unsplit one in its epilogue if its tile
+// is staged and holds whole 2x2 windows (not the few-channel kernel).
 inline bool igemm_pools(const IgemmPlan& p, int Cout) {
-  if (p.splits != 1 || few_takes(p, Cout)) return false;
+  if (few_takes(p, Cout)) return false;
+  if (p.splits > 1) return true;
   switch (p.tile) {
     case 0: return can_pool<TileW32, false, float>();
     case 1: return can_pool<TileW16, false, float>();
@@ -1211,7 +1221,7 @@ int conv_igemm_describe(bool dgrad, int dtype, int N, int Cin, int H, int W, int
                     sb::cdiv(W, sb::FewTile::TW) * sb::cdiv(H, sb::FewTile::TH) * N);
   char name[160];
   snprintf(name, sizeof(name), sb::kTileNames[p.tile], dgrad ? "true" : "false", et);
-  if (pool) {
+  if (pool && p.splits == 1) {
     // The pooled instantiation: conv3x3_igemm_f32<T, false, float, WHOLE_H, true>.
     const size_t l = strlen(name);
     if (l > 0 && name[l - 1] == '>')

@@ -292,18 +292,22 @@ def test_fused_forward_pool_validation():
     assert fwd_pool(ok, x, w, y, None, ws, need) == sb.SB_ERR_INVALID_ARG
     assert fwd_pool(ok, x, w, y, y + 64, ws, need) == sb.SB_ERR_INVALID_ARG   # idx over y
     assert fwd_pool(ok, x, w, x + 64, idx, ws, need) == sb.SB_ERR_INVALID_ARG  # y over x
-    # NCHW fp32 pools in the kernel on unsplit plans too (not bf16 NCHW, not
-    # the split plans of small batches or of the 4x4 and 2x2 images).
+    # NCHW fp32 pools in the call too: an unsplit plan in the kernel's
+    # epilogue, a split one (small batches, the 4x4 and 2x2 images) in its
+    # split reduction; not bf16 NCHW, not the few-output-channel kernel.
     f32 = sb.conv_desc(128, 64, 32, 32, 64, sb.SB_F32)
     assert sb.sb_conv3x3_workspace_bytes(f32, sb.SB_PASS_FWD_POOL) == \
         sb.sb_conv3x3_workspace_bytes(f32, sb.SB_PASS_FWD)
     assert sb.sb_conv3x3_plan_string(f32, sb.SB_PASS_FWD_POOL).split(" grid")[0].endswith(
         ", true>")
-    for bad in (sb.conv_desc(2, 64, 32, 32, 64, sb.SB_F32),
-                sb.conv_desc(128, 512, 4, 4, 512, sb.SB_F32),
-                sb.conv_desc(128, 512, 2, 2, 512, sb.SB_F32)):
-        assert sb.sb_conv3x3_workspace_bytes(bad, sb.SB_PASS_FWD_POOL) == sb.SIZE_MAX
-        assert fwd_pool(bad, x, w, y, idx, ws, need) == sb.SB_ERR_UNSUPPORTED
+    for good in (sb.conv_desc(2, 64, 32, 32, 64, sb.SB_F32),
+                 sb.conv_desc(128, 512, 4, 4, 512, sb.SB_F32),
+                 sb.conv_desc(128, 512, 2, 2, 512, sb.SB_F32)):
+        assert sb.sb_conv3x3_workspace_bytes(good, sb.SB_PASS_FWD_POOL) == \
+            sb.sb_conv3x3_workspace_bytes(good, sb.SB_PASS_FWD)
+    few = sb.conv_desc(2, 12, 6, 38, 3, sb.SB_F32)          # 3 outputs: vector-ALU kernel
+    assert sb.sb_conv3x3_workspace_bytes(few, sb.SB_PASS_FWD_POOL) == sb.SIZE_MAX
+    assert fwd_pool(few, x, w, y, idx, ws, need) == sb.SB_ERR_UNSUPPORTED
     # A plan that splits the channel loop cannot pool in the kernel.
     split = c8(1, 512, 14, 14, 512)
     splits = int(sb.sb_conv3x3_plan_string(split, sb.SB_PASS_FWD).rsplit("x", 1)[1])

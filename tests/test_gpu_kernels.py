@@ -361,11 +361,14 @@ def test_conv_pack_filters_many_matches_single(dtype):
 
 
 # Forward with fused ReLU + 2x2 pooling on NCHW fp32 (sb_conv3x3_fwd_pool):
-# shapes whose plan is one split: 4x32 tiles, 8x16 tiles with two channel
-# tiles, the two-group 8x8 tiles on whole 8x8 images, and the same tiles
-# over 14x14 images (ragged tiles, a ragged pooled edge).
+# unsplit plans pooling in the epilogue (4x32 tiles, 8x16 tiles with two
+# channel tiles, the two-group 8x8 tiles on whole 8x8 images, the same tiles
+# over 14x14 images: ragged tiles and pooled edge) and split plans pooling in
+# the split reduction (a small batch, the whole-image 4x4 and 2x2 tiles, a
+# ragged output-channel tile).
 FUSED_F32_SHAPES = [(64, 64, 32, 32, 64), (128, 64, 16, 16, 128), (128, 128, 8, 8, 256),
-                    (128, 64, 14, 14, 64)]
+                    (128, 64, 14, 14, 64), (2, 64, 32, 32, 64), (128, 512, 4, 4, 512),
+                    (128, 512, 2, 2, 512), (33, 64, 2, 2, 130), (33, 40, 4, 4, 70)]
 
 
 @pytest.mark.parametrize("shape", FUSED_F32_SHAPES, ids=lambda s: "x".join(map(str, s)))
@@ -381,7 +384,7 @@ def test_conv_fwd_pool_f32(shape):
     x, wt, b, _, _ = _conv_inputs(n, c, h, w, k, 62)
     d = sb.conv_desc(n, c, h, w, k, sb.SB_F32)
     need = sb.sb_conv3x3_workspace_bytes(d, sb.SB_PASS_FWD_POOL)
-    assert need != sb.SIZE_MAX, "planned as one split"
+    assert need != sb.SIZE_MAX, "pooled in the call"
     ws = _ws(need)
     xd, wd, bd = to_dev(x), to_dev(wt), to_dev(b)
     pooled = (n, k, h // 2, w // 2)
