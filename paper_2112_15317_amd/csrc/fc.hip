@@ -19,6 +19,7 @@
 #include "sb_internal.hpp"
 
 #include <algorithm>
+#include <type_traits>
 #include <mutex>
 
 namespace sb {
@@ -197,7 +198,7 @@ __device__ __forceinline__ void gemm_block(const GemmArgs& g, int& mtile, int& n
   ntile = t - mtile * g.nt;
 }
 
-template <int BM, int BN, bool A_KC, bool B_KC, bool VEC, class E, class CE>
+template <int BM, int BN, bool A_KC, bool B_KC, bool VEC, class E, class CE, bool AMK, bool BMK>
 __global__ __launch_bounds__(256, 2) void gemm_f32(GemmArgs g) {
   using T = GemmTile<BM, BN>;
   extern __shared__ float lds[];
@@ -216,7 +217,7 @@ __global__ __launch_bounds__(256, 2) void gemm_f32(GemmArgs g) {
   const rsrc_t rb = make_rsrc(g.b, (uint32_t)(b_elems * sizeof(E)));
   const rsrc_t ram = make_rsrc(g.amask ? g.amask : g.a, (uint32_t)(a_elems * sizeof(E)));
   const rsrc_t rbm = make_rsrc(g.bmask ? g.bmask : g.b, (uint32_t)(b_elems * sizeof(E)));
-  const bool amasked = g.amask != nullptr, bmasked = g.bmask != nullptr;
+  constexpr bool amasked = AMK, bmasked = BMK;
   const bool do_colsum = g.colsum != nullptr && mtile == 0;
 
   f16v acc[T::RB][T::CB];
@@ -230,43 +231,46 @@ __global__ __launch_bounds__(256, 2) void gemm_f32(GemmArgs g) {
 #pragma unroll
   for (int j = 0; j < T::CB; ++j) csum[j] = 0.f;
 
-  Stage<BM, A_KC, VEC, E> sa;
-  Stage<BN, B_KC, VEC, E> sb_;
-  sa.init(g.lda, g.M, m0, tid);
-  sb_.init(g.ldb, g.N, n0, tid);
+  Stage<BM, A_KC, VEC, E> sa[2];
+  Stage<BN, B_KC, VEC, E> sb_[2];
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    sa[q].init(g.lda, g.M, m0, tid);
+    sb_[q].init(g.ldb, g.N, n0, tid);
+  }
   auto Abuf = [&](int b) { return lds + b * T::BUF; };
   auto Bbuf = [&](int b) { return lds + b * T::BUF + T::OPA; };
 
   const int nk = ke > kb ? cdiv(ke - kb, GBK) : 0;
-  if (nk > 0) {
-    sa.load(ra, ram, amasked, g.M, m0, kb, ke, tid);
-    sb_.load(rb, rbm, bmasked, g.N, n0, kb, ke, tid);
-    sa.store(Abuf(0), amasked, tid);
-    sb_.store(Bbuf(0), bmasked, tid);
-    if (nk > 1) {
-      sa.load(ra, ram, amasked, g.M, m0, kb + GBK, ke, tid);
-      sb_.load(rb, rbm, bmasked, g.N, n0, kb + GBK, ke, tid);
-    }
-  }
+  sa[0].load(ra, ram, amasked, g.M, m0, kb, ke, tid);
+  sb_[0].load(rb, rbm, bmasked, g.N, n0, kb, ke, tid);
+  sa[1].load(ra, ram, amasked, g.M, m0, kb + GBK, ke, tid);
+  sb_[1].load(rb, rbm, bmasked, g.N, n0, kb + GBK, ke, tid);
+  sa[0].store(Abuf(0), amasked, tid);
+  sb_[0].store(Bbuf(0), bmasked, tid);
+  sa[0].load(ra, ram, amasked, g.M, m0, kb + 2 * GBK, ke, tid);
+  sb_[0].load(rb, rbm, bmasked, g.N, n0, kb + 2 * GBK, ke, tid);
   __syncthreads();
-  // Per tile: the first chunk's operands are read from LDS while the next
-  // tile is stored and the one after is requested; then each chunk's MFMAs
-  // run while the following chunk's operands are read.
-  for (int t = 0; t < nk; ++t) {
-    const int buf = t & 1;
+  // Tile j's operands travel in register set j % 2.  Per tile t: the first
+  // chunk's operands are read from LDS, tile t + 1 is stored to the other
+  // LDS buffer and tile t + 3 is requested into the register set that store
+  // frees (two tiles ahead of its own store); then each chunk's MFMAs run
+  // while the following chunk's operands are read.
+  auto step = [&](auto P, int t) {
+    constexpr int Q = decltype(P)::value;          // t % 2
+    const int buf = Q;
     const float* A = Abuf(buf);
     const float* B = Bbuf(buf);
     f4 fa[T::RB], fb[T::CB], na[T::RB], nb[T::CB];
     frag32<BM, A_KC, T::RB>(A, wm * (BM / 2), 0, h, l32, fa);
     frag32<BN, B_KC, T::CB>(B, wn * (BN / 2), 0, h, l32, fb);
-    if (t + 1 < nk) {
-      sa.store(Abuf(buf ^ 1), amasked, tid);
-      sb_.store(Bbuf(buf ^ 1), bmasked, tid);
-    }
-    if (t + 2 < nk) {
-      sa.load(ra, ram, amasked, g.M, m0, kb + (t + 2) * GBK, ke, tid);
-      sb_.load(rb, rbm, bmasked, g.N, n0, kb + (t + 2) * GBK, ke, tid);
-    }
+    // Unconditional: a tile past the end loads as zeros (every offset out
+    // of range) and its LDS copy is never read, so the loop body has one
+    // path and the compiler counts outstanding loads exactly.
+    sa[Q ^ 1].store(Abuf(buf ^ 1), amasked, tid);
+    sb_[Q ^ 1].store(Bbuf(buf ^ 1), bmasked, tid);
+    sa[Q ^ 1].load(ra, ram, amasked, g.M, m0, kb + (t + 3) * GBK, ke, tid);
+    sb_[Q ^ 1].load(rb, rbm, bmasked, g.N, n0, kb + (t + 3) * GBK, ke, tid);
 #pragma unroll
     for (int c = 0; c < GBK / 8; ++c) {
       if (c + 1 < GBK / 8) {
@@ -294,7 +298,13 @@ __global__ __launch_bounds__(256, 2) void gemm_f32(GemmArgs g) {
       }
     }
     __syncthreads();
+  };
+  int t = 0;
+  for (; t + 1 < nk; t += 2) {
+    step(std::integral_constant<int, 0>{}, t);
+    step(std::integral_constant<int, 1>{}, t + 1);
   }
+  if (t < nk) step(std::integral_constant<int, 0>{}, t);
 
   if (do_colsum) {
 #pragma unroll
@@ -444,22 +454,37 @@ static bool vec_ok(const void* p, int ld, int contiguous_extent) {
   return ((uintptr_t)p & (4 * sizeof(E) - 1)) == 0 && ld % 4 == 0 && contiguous_extent % 4 == 0;
 }
 
-template <int BM, int BN, bool AK, bool BK, bool VEC, class E, class CE>
+template <int BM, int BN, bool AK, bool BK, bool VEC, class E, class CE, bool AMK, bool BMK>
 static void gemm_launch_t(const GemmPlan& p, const GemmArgs& g, hipStream_t st) {
   using T = GemmTile<BM, BN>;
   static std::once_flag once;
   std::call_once(once, [] {
-    (void)hipFuncSetAttribute((const void*)gemm_f32<BM, BN, AK, BK, VEC, E, CE>,
+    (void)hipFuncSetAttribute((const void*)gemm_f32<BM, BN, AK, BK, VEC, E, CE, AMK, BMK>,
                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)T::LDS_BYTES);
   });
-  gemm_f32<BM, BN, AK, BK, VEC, E, CE><<<p.mt * p.nt * p.splits, 256, T::LDS_BYTES, st>>>(g);
+  gemm_f32<BM, BN, AK, BK, VEC, E, CE, AMK, BMK><<<p.mt * p.nt * p.splits, 256, T::LDS_BYTES, st>>>(g);
 }
 
+template <bool AK, bool BK, bool VEC, class E, class CE, bool AMK, bool BMK>
+static void gemm_launch_m(const GemmPlan& p, const GemmArgs& g, hipStream_t st) {
+  if (p.bm == 128 && p.bn == 128) gemm_launch_t<128, 128, AK, BK, VEC, E, CE, AMK, BMK>(p, g, st);
+  else if (p.bm == 128) gemm_launch_t<128, 64, AK, BK, VEC, E, CE, AMK, BMK>(p, g, st);
+  else gemm_launch_t<64, 64, AK, BK, VEC, E, CE, AMK, BMK>(p, g, st);
+}
+
+// The masks are template arguments, so that no load or store of the
+// staging carries a branch.  The library's products mask only dY: the A
+// operand of the data-gradient product (both operands K-contiguous) or
+// the B operand of the weight-gradient product (neither).
 template <bool AK, bool BK, bool VEC, class E, class CE>
 static void gemm_launch(const GemmPlan& p, const GemmArgs& g, hipStream_t st) {
-  if (p.bm == 128 && p.bn == 128) gemm_launch_t<128, 128, AK, BK, VEC, E, CE>(p, g, st);
-  else if (p.bm == 128) gemm_launch_t<128, 64, AK, BK, VEC, E, CE>(p, g, st);
-  else gemm_launch_t<64, 64, AK, BK, VEC, E, CE>(p, g, st);
+  if constexpr (AK && BK) {
+    if (g.amask) { gemm_launch_m<AK, BK, VEC, E, CE, true, false>(p, g, st); return; }
+  }
+  if constexpr (!AK && !BK) {
+    if (g.bmask) { gemm_launch_m<AK, BK, VEC, E, CE, false, true>(p, g, st); return; }
+  }
+  gemm_launch_m<AK, BK, VEC, E, CE, false, false>(p, g, st);
 }
 
 // C (ldc) = epi(A * B): the GEMM applies the epilogue itself when the
@@ -470,6 +495,8 @@ static void gemm_launch(const GemmPlan& p, const GemmArgs& g, hipStream_t st) {
 template <bool AK, bool BK, class E, class CE>
 static sb_status gemm_run(GemmArgs g, float* ws, size_t ws_bytes, hipStream_t st,
                           const E* csrc = nullptr, const E* cmask = nullptr, int cld = 0) {
+  // Masks exist only where gemm_launch instantiates them.
+  if ((g.amask && !(AK && BK)) || (g.bmask && (AK || BK))) return SB_ERR_UNSUPPORTED;
   GemmPlan p = gemm_plan(g.M, g.N, g.K, (int)sizeof(E));
   if (p.ws_bytes > 0 && (!ws || ws_bytes < p.ws_bytes)) return SB_ERR_WORKSPACE;
   // Buffer ranges cover whole operands.
