@@ -433,8 +433,11 @@ def test_workspace_too_small_is_reported():
 # The FC workloads' shapes (hybrid step: 512 gathered rows; group training
 # step: 128 rows, FC 4096 -> 512 and 1024 -> 5 shards), ragged shapes, and a
 # tall reduction whose weight gradient is split (bias gradient summed apart).
+# (64, 4128, 256): the forward's reduction splits into ranges of an odd
+# number of k tiles (the GEMM's two-set operand pipeline ends on either set).
 FC_SHAPES = [(512, 4096, 1024), (512, 512, 1024), (128, 4096, 512), (128, 1024, 5),
-             (37, 70, 50), (130, 200, 257), (1, 1, 1), (64, 33, 129), (4096, 64, 64)]
+             (37, 70, 50), (130, 200, 257), (1, 1, 1), (64, 33, 129), (4096, 64, 64),
+             (64, 4128, 256)]
 
 
 def _fc_inputs(m, kin, ns, seed):
