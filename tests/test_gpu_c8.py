@@ -23,7 +23,7 @@ pytestmark = pytest.mark.gpu
 # (n, c, h, w, k)
 SHAPES = [(2, 8, 32, 32, 64), (2, 16, 16, 16, 32), (3, 64, 33, 40, 24), (2, 64, 14, 14, 64),
           (4, 24, 9, 12, 16), (2, 128, 28, 28, 128), (1, 512, 14, 14, 512),
-          (2, 64, 56, 56, 64), (1, 256, 32, 64, 256)]
+          (2, 64, 56, 56, 64), (1, 256, 32, 64, 256), (3, 8, 30, 36, 72)]
 
 
 def c8(a):
