@@ -197,6 +197,32 @@ sb_status sb_conv3x3_bwd_weight(const sb_conv3x3_desc *desc, const void *x,
                                 void *workspace, size_t workspace_bytes,
                                 void *stream);
 
+/* Weight gradients of `count` layers (1..SB_MANY_MAX) in one call, each as
+ * sb_conv3x3_bwd_weight computes it (bit-identical results).  The weight
+ * gradient of a step reads nothing a later layer's backward writes, so a
+ * caller may defer several layers' weight gradients and issue them
+ * together; consecutive layers whose plans run the same kernel then share
+ * one launch (one round of blocks ramping up and draining instead of one
+ * per layer).
+ *  * descs[i], x[i], dy[i], dw[i] as for sb_conv3x3_bwd_weight; db may be
+ *    NULL (no bias gradients) or an array whose entries may be NULL.  The
+ *    arrays are host memory, read during the call only.
+ *  * workspace: sb_conv3x3_bwd_weight_many_workspace_bytes(count, descs)
+ *    bytes, layer i's split partials in its own region; needs no
+ *    initialisation.
+ *  * SB_ERR_INVALID_ARG for a count out of range, null arrays or pointers,
+ *    an invalid descriptor, an output overlapping any layer's input or any
+ *    other output, or a workspace overlapping any operand;
+ *    SB_ERR_WORKSPACE for a short workspace.  Nothing is enqueued then. */
+#define SB_MANY_MAX 64
+size_t sb_conv3x3_bwd_weight_many_workspace_bytes(int count,
+                                                  const sb_conv3x3_desc *descs);
+sb_status sb_conv3x3_bwd_weight_many(int count, const sb_conv3x3_desc *descs,
+                                     const void *const *x,
+                                     const void *const *dy, float *const *dw,
+                                     float *const *db, void *workspace,
+                                     size_t workspace_bytes, void *stream);
+
 /* Weight gradient for callers that cannot allocate device memory: code under
  * HIP graph capture, tight serving loops, harnesses that forbid allocation.
  * Computes exactly what sb_conv3x3_bwd_weight computes, with the same kernels

@@ -24,6 +24,11 @@ int conv_igemm_describe(bool dgrad, int dtype, int N, int Cin, int H, int W, int
 int conv_wgrad_describe(int dtype, int N, int C, int H, int W, int K, char* buf, size_t len);
 sb_status conv_wgrad(int dtype, int N, int C, int H, int W, int K, const void* x, const void* dy,
                      float* dw, float* db, void* ws, size_t ws_bytes, hipStream_t st);
+int conv_wgrad_batch_key(int dtype, int N, int C, int H, int W, int K, const void* x,
+                         const void* dy);
+sb_status conv_wgrad_group(int n, const int (*shape)[5], const void* const* x,
+                           const void* const* dy, float* const* dw, float* const* db,
+                           void* const* ws, const size_t* ws_bytes, hipStream_t st);
 // Channel-blocked bf16 (SB_NCHW8C).
 bool conv_bf16_takes(int N, int Cin, int H, int W, int Cout);
 int conv_bf16c8_describe(bool dgrad, int N, int Cin, int H, int W, int Cout, char* buf,
@@ -295,6 +300,117 @@ extern "C" sb_status sb_conv3x3_bwd_weight(const sb_conv3x3_desc* d, const void*
                               sbh::stream_of(stream));
   return sbh::conv_wgrad(d->dtype, d->n, d->c, d->h, d->w, d->k, x, dy, dw, db, ws, ws_bytes,
                          sbh::stream_of(stream));
+}
+
+// ---------------------------------------------------------------------------
+// Weight gradients of several layers.  Layer i's split partials live in its
+// own region of the workspace (regions in layer order, each rounded up to
+// 256 bytes), so the layers need not run one after another: consecutive
+// layers whose plans run the same kernel instantiation share one launch.
+namespace {
+constexpr int kWgGroup = 4;          // layers per shared launch
+
+size_t wgrad_region(const sb_conv3x3_desc* d) { return (wgrad_ws(d) + 255) / 256 * 256; }
+}  // namespace
+
+extern "C" size_t sb_conv3x3_bwd_weight_many_workspace_bytes(int count,
+                                                             const sb_conv3x3_desc* descs) {
+  if (count < 1 || count > SB_MANY_MAX || !descs) return (size_t)-1;
+  size_t total = 0;
+  for (int i = 0; i < count; ++i) {
+    if (conv_check(&descs[i], SB_PASS_BWD_WEIGHT) != SB_OK) return (size_t)-1;
+    total += wgrad_region(&descs[i]);
+  }
+  return total;
+}
+
+extern "C" sb_status sb_conv3x3_bwd_weight_many(int count, const sb_conv3x3_desc* d,
+                                                const void* const* x, const void* const* dy,
+                                                float* const* dw, float* const* db, void* ws,
+                                                size_t ws_bytes, void* stream) {
+  if (count < 1 || count > SB_MANY_MAX || !d || !x || !dy || !dw) return SB_ERR_INVALID_ARG;
+  size_t xb[SB_MANY_MAX], dyb[SB_MANY_MAX], dwb[SB_MANY_MAX], dbb[SB_MANY_MAX];
+  size_t off[SB_MANY_MAX + 1];
+  off[0] = 0;
+  for (int i = 0; i < count; ++i) {
+    sb_status s = conv_check(&d[i], SB_PASS_BWD_WEIGHT);
+    if (s != SB_OK) return s;
+    if (!x[i] || !dy[i] || !dw[i]) return SB_ERR_INVALID_ARG;
+    xb[i] = act_bytes(&d[i], d[i].c);
+    dyb[i] = act_bytes(&d[i], d[i].k);
+    dwb[i] = (size_t)d[i].k * d[i].c * 9 * sizeof(float);
+    dbb[i] = db && db[i] ? d[i].k * sizeof(float) : 0;
+    off[i + 1] = off[i] + wgrad_region(&d[i]);
+  }
+  const float* dbp[SB_MANY_MAX];
+  for (int i = 0; i < count; ++i) dbp[i] = db ? db[i] : nullptr;
+  // No output may overlap any layer's inputs or any other output.
+  for (int i = 0; i < count; ++i) {
+    if (sbh::overlaps(dw[i], dwb[i], dbp[i], dbb[i])) return SB_ERR_INVALID_ARG;
+    for (int j = 0; j < count; ++j) {
+      if (sbh::overlaps(dw[i], dwb[i], x[j], xb[j]) || sbh::overlaps(dw[i], dwb[i], dy[j], dyb[j]) ||
+          sbh::overlaps(dbp[i], dbb[i], x[j], xb[j]) || sbh::overlaps(dbp[i], dbb[i], dy[j], dyb[j]))
+        return SB_ERR_INVALID_ARG;
+      if (j != i && (sbh::overlaps(dw[i], dwb[i], dw[j], dwb[j]) ||
+                     sbh::overlaps(dw[i], dwb[i], dbp[j], dbb[j]) ||
+                     sbh::overlaps(dbp[i], dbb[i], dbp[j], dbb[j])))
+        return SB_ERR_INVALID_ARG;
+    }
+  }
+  const size_t need = off[count];
+  if (need && (!ws || ws_bytes < need)) return SB_ERR_WORKSPACE;
+  if (need)
+    for (int j = 0; j < count; ++j)
+      if (sbh::overlaps(ws, need, x[j], xb[j]) || sbh::overlaps(ws, need, dy[j], dyb[j]) ||
+          sbh::overlaps(ws, need, dw[j], dwb[j]) || sbh::overlaps(ws, need, dbp[j], dbb[j]))
+        return SB_ERR_INVALID_ARG;
+  hipStream_t st = sbh::stream_of(stream);
+  char* wsc = (char*)ws;
+  auto key_of = [&](int i) {
+    return d[i].layout == SB_NCHW8C
+               ? -1
+               : sbh::conv_wgrad_batch_key(d[i].dtype, d[i].n, d[i].c, d[i].h, d[i].w, d[i].k,
+                                           x[i], dy[i]);
+  };
+  int i = 0;
+  while (i < count) {
+    const int key = key_of(i);
+    sb_status s;
+    if (key < 0) {
+      void* wsi = need ? wsc + off[i] : nullptr;
+      const size_t wsb = off[i + 1] - off[i];
+      s = d[i].layout == SB_NCHW8C
+              ? sbh::conv_wgrad_c8(d[i].n, d[i].c, d[i].h, d[i].w, d[i].k, x[i], dy[i], dw[i],
+                                   dbp[i] ? (float*)dbp[i] : nullptr, wsi, wsb, st)
+              : sbh::conv_wgrad(d[i].dtype, d[i].n, d[i].c, d[i].h, d[i].w, d[i].k, x[i], dy[i],
+                                dw[i], dbp[i] ? (float*)dbp[i] : nullptr, wsi, wsb, st);
+      if (s != SB_OK) return s;
+      ++i;
+      continue;
+    }
+    int j = i + 1;
+    while (j < count && j - i < kWgGroup && key_of(j) == key) ++j;
+    int shape[kWgGroup][5];
+    const void* xs[kWgGroup];
+    const void* dys[kWgGroup];
+    float* dws[kWgGroup];
+    float* dbs[kWgGroup];
+    void* wss[kWgGroup];
+    size_t wsbs[kWgGroup];
+    for (int t = i; t < j; ++t) {
+      const int u = t - i;
+      shape[u][0] = d[t].n; shape[u][1] = d[t].c; shape[u][2] = d[t].h;
+      shape[u][3] = d[t].w; shape[u][4] = d[t].k;
+      xs[u] = x[t]; dys[u] = dy[t]; dws[u] = dw[t];
+      dbs[u] = dbp[t] ? (float*)dbp[t] : nullptr;
+      wss[u] = need ? wsc + off[t] : nullptr;
+      wsbs[u] = off[t + 1] - off[t];
+    }
+    s = sbh::conv_wgrad_group(j - i, shape, xs, dys, dws, dbs, wss, wsbs, st);
+    if (s != SB_OK) return s;
+    i = j;
+  }
+  return sbh::launch_status();
 }
 
 // ---------------------------------------------------------------------------

@@ -321,14 +321,15 @@ __device__ constexpr bool wg_pad_step(int st, int t) {
 // worked out once per thread, and per tile an element costs an add and a row
 // test.  WHOLE (with ROWS): every tile is a whole image (H = TH as well), and
 // the steps whose taps read only padding are skipped (wg_pad_step).
-template <class T, class E, bool ROWS = false, bool WHOLE = false>
-__global__ __launch_bounds__(256, 2) void conv3x3_wgrad_f32(WgArgs a) {
+// The block's work for block (x, z) of the layer `a`; the kernels below
+// pick the layer and the block.
+template <class T, class E, bool ROWS, bool WHOLE>
+__device__ __forceinline__ void wgrad_f32_block(const WgArgs& a, const WgBlock blk) {
   static_assert(!WHOLE || (ROWS && T::IMGS == 1 && !T::NARROW), "whole-image tiles are full-width");
   extern __shared__ float lds[];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int jq = lane >> 4, lr = lane & 15;
-  const WgBlock blk = wg_block();
   const int ct = blk.x % a.c_tiles, kt = blk.x / a.c_tiles;
   const int c0 = ct * T::BC, k0 = kt * T::BK;
   const int pt0 = blk.z * a.tiles_per_split;
@@ -525,6 +526,36 @@ __global__ __launch_bounds__(256, 2) void conv3x3_wgrad_f32(WgArgs a) {
         int c = c0 + lr;
         return c < a.C ? c * 9 + t : -1;
       });
+}
+
+template <class T, class E, bool ROWS = false, bool WHOLE = false>
+__global__ __launch_bounds__(256, 2) void conv3x3_wgrad_f32(WgArgs a) {
+  wgrad_f32_block<T, E, ROWS, WHOLE>(a, wg_block());
+}
+
+// Weight gradients of up to kWgMany layers that take the same kernel, in
+// one launch: layer i owns the blocks first[i] .. first[i+1]-1 of a 1-D
+// grid, numbered within the layer as wg_block numbers a layer's own grid
+// (dealt to the XCDs in whole splits when its block count and its first
+// block are multiples of 8).  One launch instead of one per layer lets the
+// next layer's blocks start while the previous layer's last blocks drain.
+constexpr int kWgMany = 4;
+struct WgMany {
+  WgArgs a[kWgMany];
+  int first[kWgMany + 1];   // first block of each layer, then the total
+  int gx[kWgMany];          // the layer's column blocks (its grid's x extent)
+  int n;
+};
+
+template <class T, class E, bool ROWS, bool WHOLE>
+__global__ __launch_bounds__(256, 2) void conv3x3_wgrad_f32_many(WgMany m) {
+  const int b = blockIdx.x;
+  int i = 0;
+  while (i + 1 < m.n && b >= m.first[i + 1]) ++i;
+  const int nb = m.first[i + 1] - m.first[i], gx = m.gx[i];
+  int h = b - m.first[i];
+  if (nb % 8 == 0 && m.first[i] % 8 == 0) h = (h % 8) * (nb / 8) + h / 8;
+  wgrad_f32_block<T, E, ROWS, WHOLE>(m.a[i], WgBlock{h % gx, h / gx});
 }
 
 // --------------------------------------------------------- bf16 MFMA --
@@ -1547,6 +1578,31 @@ static void wg_launch(const WgPlan& p, const WgArgs& a, hipStream_t st) {
   if (p.splits > 1) launch_splits_reduce(a.part, p.splits, a.K, a.C, a.dw, a.db, st);
 }
 
+// n (<= kWgMany) layers' weight gradients on one launch of
+// conv3x3_wgrad_f32_many, then each layer's split reduction in layer order.
+template <class T, class E, bool ROWS, bool WHOLE>
+static void wg_launch_many(const WgPlan* p, const WgArgs* a, int n, hipStream_t st) {
+  static std::once_flag once;
+  std::call_once(once, [] {
+    (void)hipFuncSetAttribute((const void*)conv3x3_wgrad_f32_many<T, E, ROWS, WHOLE>,
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)T::LDS_BYTES);
+  });
+  WgMany m{};
+  m.n = n;
+  int total = 0;
+  for (int i = 0; i < n; ++i) {
+    m.a[i] = a[i];
+    m.first[i] = total;
+    m.gx[i] = p[i].k_tiles * p[i].c_tiles;
+    total += m.gx[i] * p[i].splits;
+  }
+  for (int i = n; i <= kWgMany; ++i) m.first[i] = total;
+  conv3x3_wgrad_f32_many<T, E, ROWS, WHOLE><<<total, 256, T::LDS_BYTES, st>>>(m);
+  for (int i = 0; i < n; ++i)
+    if (p[i].splits > 1)
+      launch_splits_reduce(a[i].part, p[i].splits, a[i].K, a[i].C, a[i].dw, a[i].db, st);
+}
+
 }  // namespace sb
 
 namespace sbh {
@@ -1672,6 +1728,62 @@ sb_status conv_wgrad(int dtype, int N, int C, int H, int W, int K, const void* x
   return launch_status();
 }
 
+// Batch key of an NCHW weight gradient: layers whose plan runs the same
+// conv3x3_wgrad_f32 instantiation (fp32, wide tiles) share a key; -1 for a
+// layer that takes another kernel (it runs on its own).
+int conv_wgrad_batch_key(int dtype, int N, int C, int H, int W, int K, const void* x,
+                         const void* dy) {
+  if (dtype != SB_F32) return -1;
+  const bool aligned = (((uintptr_t)x | (uintptr_t)dy) & 15) == 0;
+  const sb::WgPlan p = sb::wg_plan(N, C, H, W, K, aligned, false);
+  if (p.bc != 0 || p.tile > 2) return -1;
+  if ((int64_t)std::min(p.imgs, N) * std::max(C, K) * H * W * 4 >= (1ll << 31)) return -1;
+  const bool rows = (p.tile == 0 && W == 32) || (p.tile == 1 && W == 16) ||
+                    (p.tile == 2 && W == 8);
+  const bool whole = p.tile == 2 && W == 8 && H == 8;
+  return p.tile * 4 + (rows ? 2 : 0) + (whole ? 1 : 0);
+}
+
+// n (1..4) layers with one batch key on one launch: the same partials,
+// reductions and results as n conv_wgrad calls.  shape[i] = {N, C, H, W, K};
+// ws[i] / ws_bytes[i]: layer i's own workspace region.
+sb_status conv_wgrad_group(int n, const int (*shape)[5], const void* const* x,
+                           const void* const* dy, float* const* dw, float* const* db,
+                           void* const* ws, const size_t* ws_bytes, hipStream_t st) {
+  if (n < 1 || n > sb::kWgMany) return SB_ERR_INVALID_ARG;
+  sb::WgPlan p[sb::kWgMany];
+  sb::WgArgs a[sb::kWgMany];
+  int key = -2;
+  for (int i = 0; i < n; ++i) {
+    const int N = shape[i][0], C = shape[i][1], H = shape[i][2], W = shape[i][3],
+              K = shape[i][4];
+    const int k = conv_wgrad_batch_key(SB_F32, N, C, H, W, K, x[i], dy[i]);
+    if (k < 0 || (key != -2 && k != key)) return SB_ERR_INVALID_ARG;
+    key = k;
+    const bool aligned = (((uintptr_t)x[i] | (uintptr_t)dy[i]) & 15) == 0;
+    p[i] = sb::wg_plan(N, C, H, W, K, aligned, false);
+    if (p[i].ws_bytes > 0 && (ws[i] == nullptr || ws_bytes[i] < p[i].ws_bytes))
+      return SB_ERR_WORKSPACE;
+    sb::WgArgs& g = a[i];
+    g = sb::WgArgs{};
+    g.x = x[i]; g.dy = dy[i]; g.dw = dw[i]; g.db = db ? db[i] : nullptr;
+    g.part = p[i].splits > 1 ? (float*)ws[i] : nullptr;
+    g.N = N; g.C = C; g.H = H; g.W = W; g.K = K;
+    g.tiles_w = p[i].tiles_w; g.tiles_h = p[i].tiles_h; g.ptiles = p[i].ptiles;
+    g.tiles_per_split = p[i].tps; g.c_tiles = p[i].c_tiles; g.splits = p[i].splits;
+  }
+  switch (key) {
+    case 0: sb::wg_launch_many<sb::WgW32, float, false, false>(p, a, n, st); break;
+    case 2: sb::wg_launch_many<sb::WgW32, float, true, false>(p, a, n, st); break;
+    case 4: sb::wg_launch_many<sb::WgW16, float, false, false>(p, a, n, st); break;
+    case 6: sb::wg_launch_many<sb::WgW16, float, true, false>(p, a, n, st); break;
+    case 8: sb::wg_launch_many<sb::WgW8, float, false, false>(p, a, n, st); break;
+    case 10: sb::wg_launch_many<sb::WgW8, float, true, false>(p, a, n, st); break;
+    case 11: sb::wg_launch_many<sb::WgW8, float, true, true>(p, a, n, st); break;
+    default: return SB_ERR_INVALID_ARG;
+  }
+  return launch_status();
+}
 
 // Channel-blocked bf16 tensors (SB_NCHW8C): the plan of the NCHW bf16 path
 // (tiles of 64 pixels, 16 or 32 channels per block), the transpose-load

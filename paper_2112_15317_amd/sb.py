@@ -71,6 +71,10 @@ SIGNATURES = {
     "sb_conv3x3_bwd_weight": (_i, [ctypes.POINTER(sb_conv3x3_desc), _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "sb_conv3x3_bwd_weight_noalloc": (_i, [ctypes.POINTER(sb_conv3x3_desc), _vp, _vp, _vp, _vp,
                                            _vp]),
+    "sb_conv3x3_bwd_weight_many_workspace_bytes": (_sz, [_i, ctypes.POINTER(sb_conv3x3_desc)]),
+    "sb_conv3x3_bwd_weight_many": (_i, [_i, ctypes.POINTER(sb_conv3x3_desc), ctypes.POINTER(_vp),
+                                        ctypes.POINTER(_vp), ctypes.POINTER(_vp),
+                                        ctypes.POINTER(_vp), _vp, _sz, _vp]),
     "sb_relu_maxpool_fwd": (_i, [_i, _i, _i, _i, _i, _i, _vp, _vp, _vp, _vp]),
     "sb_relu_maxpool_bwd": (_i, [_i, _i, _i, _i, _i, _i, _vp, _vp, _vp, _vp]),
     "sb_fc_workspace_bytes": (_sz, [ctypes.POINTER(sb_fc_desc), _i]),
@@ -245,6 +249,30 @@ def sb_conv3x3_bwd_weight(desc, x, dy, dw, db, ws=None, stream=None):
     p, nb = _ws(ws)
     _check("sb_conv3x3_bwd_weight", load().sb_conv3x3_bwd_weight(
         ctypes.byref(desc), _ptr(x), _ptr(dy), _ptr(dw), _ptr(db), p, nb, _stream(stream)))
+
+
+class WgradList:
+    """Host arrays of a sb_conv3x3_bwd_weight_many call (kept alive with the
+    object, so a recorded call can be issued again)."""
+
+    def __init__(self, descs, x, dy, dw, db):
+        n = len(descs)
+        self.count = n
+        self.descs = (sb_conv3x3_desc * n)(*descs)
+        self.x = (_vp * n)(*[_ptr(t) for t in x])
+        self.dy = (_vp * n)(*[_ptr(t) for t in dy])
+        self.dw = (_vp * n)(*[_ptr(t) for t in dw])
+        self.db = (_vp * n)(*[_ptr(t) for t in db])
+
+    def workspace_bytes(self):
+        return load().sb_conv3x3_bwd_weight_many_workspace_bytes(self.count, self.descs)
+
+
+def sb_conv3x3_bwd_weight_many(wlist, ws=None, stream=None):
+    p, nb = _ws(ws)
+    _check("sb_conv3x3_bwd_weight_many", load().sb_conv3x3_bwd_weight_many(
+        wlist.count, wlist.descs, wlist.x, wlist.dy, wlist.dw, wlist.db, p, nb,
+        _stream(stream)))
 
 
 def sb_conv3x3_bwd_weight_noalloc(desc, x, dy, dw, db, stream=None):

@@ -395,3 +395,36 @@ def test_channel_blocked_layout_validation():
         assert _raw("sb_conv3x3_bwd_weight", ctypes.byref(d), x, y, P + (3 << 20), None, None, 0,
                     None) == status
         assert sb.sb_conv3x3_workspace_bytes(d, 0) == 2 ** 64 - 1
+
+
+def test_bwd_weight_many_validation():
+    d8 = sb.conv_desc(8, 256, 8, 8, 256)
+    d16 = sb.conv_desc(8, 128, 16, 16, 128)
+    n = 2
+
+    def call(descs, xs, dys, dws, dbs, ws, wsb):
+        k = len(descs)
+        arr = lambda v: (ctypes.c_void_p * k)(*v) if v is not None else None
+        return _raw("sb_conv3x3_bwd_weight_many", k, (sb.sb_conv3x3_desc * k)(*descs),
+                    arr(xs), arr(dys), arr(dws), arr(dbs), ws, wsb, None)
+    x0, y0, x1, y1 = P, P + (64 << 20), P + (128 << 20), P + (192 << 20)
+    w0, w1, b0, b1 = P + (256 << 20), P + (264 << 20), P + (272 << 20), P + (273 << 20)
+    ws = P + (320 << 20)
+    need = sb.load().sb_conv3x3_bwd_weight_many_workspace_bytes(
+        n, (sb.sb_conv3x3_desc * n)(d8, d16))
+    one = [sb.sb_conv3x3_workspace_bytes(d, sb.SB_PASS_BWD_WEIGHT) for d in (d8, d16)]
+    assert need == sum((b + 255) // 256 * 256 for b in one)
+    assert sb.load().sb_conv3x3_bwd_weight_many_workspace_bytes(0, None) == ctypes.c_size_t(-1).value
+    ok = lambda **kw: call(**dict(dict(descs=[d8, d16], xs=[x0, x1], dys=[y0, y1], dws=[w0, w1],
+                                       dbs=[b0, b1], ws=ws, wsb=need), **kw))
+    E, W = sb.SB_ERR_INVALID_ARG, sb.SB_ERR_WORKSPACE
+    assert _raw("sb_conv3x3_bwd_weight_many", 0, None, None, None, None, None, None, 0,
+                None) == E
+    assert ok(xs=None) == E                                   # null arrays
+    assert ok(dws=[w0, None]) == E                            # a null output
+    assert ok(dws=[w0, x1 + 64]) == E                         # dW over another layer's input
+    assert ok(dws=[w0, w0 + 4]) == E                          # two layers' dW overlap
+    assert ok(dbs=[b0, w0]) == E                              # a db over another layer's dW
+    assert ok(ws=y1) == E                                     # workspace over an input
+    assert ok(wsb=need - 1) == W                              # short workspace
+    assert ok(descs=[d8, sb.conv_desc(8, 128, 16, 16, 0)]) == E   # a bad descriptor
