@@ -569,6 +569,11 @@ def kernel_name(key, call_args, dtype):
         p = {"fwd": sb.SB_PASS_FWD, "dgrad": sb.SB_PASS_BWD_DATA,
              "wgrad": sb.SB_PASS_BWD_WEIGHT, "fwd_pool": sb.SB_PASS_FWD_POOL}[kind]
         return sb.sb_conv3x3_plan_string(call_args[0], p)
+    if kind == "wgrad_many":       # one launch of the batched kernel for the group
+        wl = call_args[0]
+        name = sb.sb_conv3x3_plan_string(wl.descs[0], sb.SB_PASS_BWD_WEIGHT).split(" grid=")[0]
+        return name.replace("conv3x3_wgrad_f32<", "conv3x3_wgrad_f32_many<") + \
+            " grid=%dx1x2" % wl.count
     if kind.startswith("fc_"):
         d = call_args[0]
         return "sb_fc_shard_%s m=%d k_in=%d n_shard=%d" % (kind[3:], d.m, d.k_in, d.n_shard)
@@ -594,6 +599,10 @@ def call_work(wl, key, args):
     kind, i = key
     if kind in ("fwd", "dgrad", "wgrad", "fwd_pool"):
         return layer_flops(wl.layers[i], args[0].n)[0], "flop"
+    if kind == "wgrad_many":       # the group's layers, from their descriptors
+        from paper_2112_15317_amd.configs import _valid_taps
+        return sum(2 * d.n * d.k * d.c * _valid_taps(d.h) * _valid_taps(d.w)
+                   for d in args[0].descs), "flop"
     if kind.startswith("fc_"):
         return fc_flops(args[0], kind, kind == "fc_fwd" or args[5] is not None), "flop"
     if kind in ("mfwd", "mbwd", "sfwd", "sbwd", "loss", "sgd_fc", "sgd_conv", "avg"):

@@ -18,6 +18,8 @@ by a libsb kernel.  torch only allocates device memory and orders streams.
 """
 from __future__ import annotations
 
+import re
+
 import numpy as np
 import torch
 
@@ -76,7 +78,7 @@ class ConvStack:
 
     def __init__(self, schedule, n, in_ch, hw, dtype="f32", device="cuda",
                  out_buffer=None, out_grad_buffer=None, packed=True, overlap=False,
-                 layout="nchw", fuse_pool=True):
+                 layout="nchw", fuse_pool=True, batch_wgrad=True):
         """layout: "nchw", or "c8" for channel-blocked activations
         (SB_NCHW8C, bf16 only): every activation buffer is then
         [n][c/8][h][w][8], and the first layer's input channels are padded
@@ -86,7 +88,13 @@ class ConvStack:
         fuse_pool: a pooled layer whose forward can pool in the kernel
         (sb_conv3x3_fwd_pool takes its descriptor: channel-blocked bf16 or
         NCHW fp32, an unsplit plan) runs its forward, ReLU and pooling as one
-        call and has no Z buffer (``self.fused`` lists those layers)."""
+        call and has no Z buffer (``self.fused`` lists those layers).
+
+        batch_wgrad: consecutive layers whose weight gradients run on the same
+        fp32 kernel (``group_wgrads``) have them issued together, by one
+        sb_conv3x3_bwd_weight_many call at the group's last layer (nothing in
+        the step reads dW before the update), as one launch instead of one
+        per layer (``self.wg_groups``)."""
         self.layers = conv_layers(schedule, in_ch, hw)
         if not self.layers[-1].pool_after:
             raise ValueError("the stack must end with a pooled layer")
@@ -170,13 +178,28 @@ class ConvStack:
                        sb.sb_conv3x3_workspace_bytes(self.pdesc[l.index], sb.SB_PASS_FWD),
                        sb.sb_conv3x3_workspace_bytes(self.pdesc_b[l.index], sb.SB_PASS_BWD_DATA),
                        sb.sb_conv3x3_workspace_bytes(self.desc_b[l.index], sb.SB_PASS_BWD_WEIGHT))
+        # Weight gradients batched into one call per group (layers in
+        # backward order); each group's call needs the sum of its layers'
+        # workspace regions.
+        self.wg_groups = self.group_wgrads([self.desc_b[l.index] for l in L]) if batch_wgrad \
+            else []
+        self.wg_group_of = {}
+        self.wg_lists = {}
+        for grp in self.wg_groups:
+            for i in grp:
+                self.wg_group_of[i] = grp
+            self.wg_lists[grp[0]] = sb.WgradList(
+                [self.desc_b[i] for i in grp], [self.A[i] for i in grp],
+                [self.grad_at_conv_output(i) for i in grp], [self.dW[i] for i in grp],
+                [self.db[i] for i in grp])
+            need = max(need, self.wg_lists[grp[0]].workspace_bytes())
         # Split-reduction scratch; needs no initialisation.
         self.ws = torch.empty((max(need, 256) + 255) // 256 * 256, dtype=torch.uint8, device=dev)
         self.overlap = overlap and dev.type == "cuda"
         self.ws_w = self.ws
         if self.overlap:
-            need_w = max(sb.sb_conv3x3_workspace_bytes(self.desc_b[l.index], sb.SB_PASS_BWD_WEIGHT)
-                         for l in L)
+            need_w = max([sb.sb_conv3x3_workspace_bytes(self.desc_b[l.index], sb.SB_PASS_BWD_WEIGHT)
+                          for l in L] + [w.workspace_bytes() for w in self.wg_lists.values()])
             self.ws_w = torch.empty((max(need_w, 256) + 255) // 256 * 256, dtype=torch.uint8,
                                     device=dev)
             self.side = torch.cuda.Stream(device=dev)     # default priority
@@ -196,6 +219,29 @@ class ConvStack:
                     sb.sb_conv3x3_workspace_bytes(d, sb.SB_PASS_FWD_POOL) != sb.SIZE_MAX:
                 out.add(l.index)
         return out
+
+    @staticmethod
+    def group_wgrads(descs, most=4):
+        """Groups (of two or more, at most `most`) of consecutive layers, in
+        backward order, whose weight gradients run on the same fp32 wide-tile
+        kernel, which sb_conv3x3_bwd_weight_many then issues as one launch:
+        host-side queries only."""
+        def name(d):
+            s = sb.sb_conv3x3_plan_string(d, sb.SB_PASS_BWD_WEIGHT).split(" grid=")[0]
+            return s if re.fullmatch(r"sb::conv3x3_wgrad_f32<sb::WgTile<\d+, \d+, \d+, 0>, float>",
+                                     s) else None
+        groups, run = [], []
+        for i in reversed(range(len(descs))):
+            nm = name(descs[i])
+            if run and (nm is None or nm != name(descs[run[0]]) or len(run) == most):
+                if len(run) > 1:
+                    groups.append(run)
+                run = []
+            if nm is not None:
+                run.append(i)
+        if len(run) > 1:
+            groups.append(run)
+        return groups
 
     # -- layouts -----------------------------------------------------------------
     def shape_of(self, n, c, h, w):
@@ -276,13 +322,21 @@ class ConvStack:
             else:
                 g = self.gA[i + 1]
             ws_stream = stream
-            if fork:
-                ready = torch.cuda.Event()
-                ready.record(main)
-                self.side.wait_event(ready)
-                ws_stream = self.side
-            c(("wgrad", i), sb.sb_conv3x3_bwd_weight, self.desc_b[i], self.A[i], g, self.dW[i],
-              self.db[i], self.ws_w, ws_stream)
+            grp = self.wg_group_of.get(i)
+            if grp is None or i == grp[-1]:
+                if fork:
+                    ready = torch.cuda.Event()
+                    ready.record(main)
+                    self.side.wait_event(ready)
+                    ws_stream = self.side
+                if grp is None:
+                    c(("wgrad", i), sb.sb_conv3x3_bwd_weight, self.desc_b[i], self.A[i], g,
+                      self.dW[i], self.db[i], self.ws_w, ws_stream)
+                else:
+                    # The group's last layer: every member's output gradient
+                    # is ready now.
+                    c(("wgrad_many", grp[0]), sb.sb_conv3x3_bwd_weight_many,
+                      self.wg_lists[grp[0]], self.ws_w, ws_stream)
             w = self.Wb[i] if self.packed else self.W[i]
             if i > 0:
                 mask = None if L[i - 1].pool_after else self.A[i]

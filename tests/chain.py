@@ -94,6 +94,15 @@ def _conv_io(st, f, b, key):
         return ([(st.gA[i + 1], b["dA"][i]), (st.idx[i], f["idx"][i])],
                 [("pool_bwd%d" % i, st.dZ[i], b["dZ"][i], EXACT)])
     g = st.dZ[i] if pool else st.gA[i + 1]
+    if kind == "wgrad_many":
+        # Every layer of the group, each on its own oracle inputs.
+        ups, checks = [], []
+        for j in st.wg_group_of[i]:
+            gj = st.grad_at_conv_output(j)
+            ups += [(st.A[j], f["A"][j]), (gj, b["dZ"][j])]
+            checks += [("wgrad%d.dw" % j, st.dW[j], b["dW"][j], TOL["f32"]),
+                       ("wgrad%d.db" % j, st.db[j], b["db"][j], TOL["f32"])]
+        return ups, checks
     if kind == "wgrad":
         # fp32 weight and bias gradients (sums of exact products in bf16 too).
         return ([(st.A[i], f["A"][i]), (g, b["dZ"][i])],

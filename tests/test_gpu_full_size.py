@@ -24,7 +24,7 @@ import pytest
 import torch
 
 from oracle import stack as OS
-from paper_2112_15317_amd import configs, synth
+from paper_2112_15317_amd import configs, sb, synth
 from paper_2112_15317_amd.stack import ConvStack, HybridStep
 from tests.chain import conv_io, near_tie_flips, put, run_and_check
 from tests.helpers import TOL, print_case, rel_l2, to_host
@@ -45,13 +45,26 @@ def _fused():
 
 
 FUSED = _fused()
+
+
+def _groups():
+    """The weight-gradient groups of the fp32 stack (host-side queries)."""
+    try:
+        return ConvStack.group_wgrads([sb.conv_desc(N, L.c, L.h, L.w, L.k) for L in LAYERS])
+    except Exception:
+        return []
+
+
+GROUPS = _groups()
 HYBRID_FC = [(512, 4096), (4096, 4096)]
 GROSS = 1e-2
 
 
-def stack_keys(layers, fused=()):
+def stack_keys(layers, fused=(), groups=()):
     """The calls of ConvStack.step, in order (fused: the layers whose
-    forward pools in the kernel)."""
+    forward pools in the kernel; groups: ConvStack.wg_groups, the layers
+    whose weight gradients go out as one call at the group's last layer)."""
+    group_of = {i: g for g in groups for i in g}
     keys = [("pack", 0)]
     for L in layers:
         if L.index in fused:
@@ -63,7 +76,12 @@ def stack_keys(layers, fused=()):
     for L in reversed(layers):
         if L.pool_after:
             keys.append(("pool_bwd", L.index))
-        keys += [("wgrad", L.index), ("dgrad", L.index)]
+        g = group_of.get(L.index)
+        if g is None:
+            keys.append(("wgrad", L.index))
+        elif L.index == g[-1]:
+            keys.append(("wgrad_many", g[0]))
+        keys.append(("dgrad", L.index))
     return keys
 
 
@@ -119,14 +137,14 @@ def cfg2():
     pools = [L.pool_after for L in LAYERS]
     f, b = OS.vgg_step(x, ws, bs, pools, dy, store="f32")
     st = ConvStack(configs.VGG16, N, 3, 32, "f32")
-    assert st.fused == FUSED
+    assert st.fused == FUSED and st.wg_groups == GROUPS
     st.load_inputs(x, ws, bs, dy)
     calls = {c[0]: c for c in st.step_calls()}
     run_and_check(calls[("pack", 0)], [], [])
     yield {"st": st, "f": f, "b": b, "calls": calls, "inputs": (x, ws, bs, dy)}
 
 
-@pytest.mark.parametrize("key", stack_keys(LAYERS, FUSED)[1:], ids=_id)
+@pytest.mark.parametrize("key", stack_keys(LAYERS, FUSED, GROUPS)[1:], ids=_id)
 def test_vgg16_cifar_call_on_oracle_chain(cfg2, key):
     print_case("cfg2_call", call=_id(key), n=N)
     ups, checks = conv_io(cfg2["st"], cfg2["f"], cfg2["b"], key)
@@ -159,7 +177,7 @@ def bench_hybrid_inputs(n, R):
 
 
 def hybrid_keys():
-    conv = stack_keys(LAYERS, FUSED)
+    conv = stack_keys(LAYERS, FUSED, GROUPS)
     split = conv.index(("pool_bwd", LAYERS[-1].index))
     return conv[:split] + [("fc_fwd", 0), ("fc_fwd", 1), ("fc_bwd", 1), ("fc_bwd", 0)] + \
         conv[split:]
